@@ -1,0 +1,55 @@
+// Kernel launchers behind the C ABI.  Arguments are already validated by the
+// caller (lsh_api.cpp); every launcher only enqueues work on `stream` and
+// returns the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <cmath>
+
+namespace lsh {
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+constexpr int kHeadDimHost = 64;  // d_k the kernels are specialised for
+constexpr int kChunkHost = 64;    // chunk length m the kernels are specialised for
+
+// ---- hashing ----
+size_t hash_workspace_bytes(int n_rounds, int n_buckets);
+hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int n_buckets,
+                       const float* R, int32_t* buckets, void* workspace, hipStream_t stream);
+
+// ---- counting sort and row gather ----
+int sort_tile_positions(int L);
+size_t sort_workspace_bytes(int64_t BH, int L, int n_rounds, int n_buckets);
+hipError_t launch_sort(int64_t BH, int L, int n_rounds, int n_buckets, const int32_t* buckets,
+                       int32_t* perm, int32_t* undo, int32_t* bucket_start, void* workspace,
+                       hipStream_t stream);
+hipError_t launch_gather(int64_t BH, int L, int n_rounds, bool f32, const void* src,
+                         const int32_t* perm, void* dst, hipStream_t stream);
+
+// ---- chunked attention, forward ----
+hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, bool causal,
+                           float scale, float self_mask, bool f32, const void* q, const void* v,
+                           const int32_t* buckets, const int32_t* perm,
+                           const int32_t* bucket_start, float* o_rounds, float* lse_rounds,
+                           hipStream_t stream);
+
+// ---- round combination ----
+hipError_t launch_combine(int64_t BH, int L, int n_rounds, bool f32_out, const float* o_rounds,
+                          const float* lse_rounds, const int32_t* undo, void* out,
+                          float* lse_total, hipStream_t stream);
+
+// ---- backward ----
+size_t bwd_workspace_bytes(int64_t BH, int L, int n_rounds);
+hipError_t launch_attn_bwd(int64_t BH, int L, int n_rounds, int n_buckets, bool causal,
+                           float scale, float self_mask, const void* q, const void* v,
+                           const void* out, const void* dout, const float* lse_total,
+                           const int32_t* buckets, const int32_t* perm, const int32_t* undo,
+                           const int32_t* bucket_start, float* dq, float* dv, void* workspace,
+                           hipStream_t stream);
+
+}  // namespace lsh

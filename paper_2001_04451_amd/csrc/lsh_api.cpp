@@ -1,0 +1,193 @@
+// The C ABI of liblsh (declared in include/lsh.h): argument validation,
+// workspace carving and kernel launches.  Validation runs before any HIP
+// call, so every LSH_ERR_INVALID / LSH_ERR_UNSUPPORTED path works without a
+// GPU.
+#include "lsh.h"
+
+#include <cmath>
+
+#include "launch.h"
+
+namespace {
+
+constexpr int64_t kMaxElems = (int64_t)1 << 31;
+
+bool finitef(float x) { return std::isfinite(x); }
+
+// Shape checks shared by every entry point.
+int check_config(const lsh_config* cfg) {
+    if (!cfg) return LSH_ERR_INVALID;
+    if (cfg->B < 1 || cfg->H < 1 || cfg->L < 1 || cfg->d < 1) return LSH_ERR_INVALID;
+    if (cfg->n_buckets < 2 || (cfg->n_buckets % 2) != 0) return LSH_ERR_INVALID;
+    if (cfg->n_rounds < 1 || cfg->chunk < 1) return LSH_ERR_INVALID;
+    if (cfg->L % cfg->chunk != 0) return LSH_ERR_INVALID;
+    if (!finitef(cfg->scale) || !finitef(cfg->self_mask)) return LSH_ERR_INVALID;
+    return LSH_OK;
+}
+
+int check_dtype(int dtype) {
+    return (dtype == LSH_F32 || dtype == LSH_BF16) ? LSH_OK : LSH_ERR_INVALID;
+}
+
+// What the kernels are specialised for.
+int check_supported(const lsh_config* cfg) {
+    if (cfg->d != lsh::kHeadDimHost || cfg->chunk != lsh::kChunkHost) return LSH_ERR_UNSUPPORTED;
+    if (cfg->n_buckets > 1024 || cfg->n_rounds > 16) return LSH_ERR_UNSUPPORTED;
+    const int64_t rr = (int64_t)cfg->B * cfg->H * cfg->L * cfg->n_rounds;
+    if (rr >= kMaxElems || rr * cfg->d >= ((int64_t)1 << 40)) return LSH_ERR_UNSUPPORTED;
+    if ((int64_t)cfg->B * cfg->H * cfg->n_rounds >= 65536) return LSH_ERR_UNSUPPORTED;
+    return LSH_OK;
+}
+
+int64_t bh_of(const lsh_config* cfg) { return (int64_t)cfg->B * cfg->H; }
+
+int status_of(hipError_t e) { return e == hipSuccess ? LSH_OK : LSH_ERR_HIP; }
+
+size_t fwd_rounds_bytes(const lsh_config* cfg) {
+    const size_t rr = (size_t)bh_of(cfg) * cfg->n_rounds * cfg->L;
+    return lsh::align256(rr * cfg->d * sizeof(float)) + lsh::align256(rr * sizeof(float));
+}
+
+#define LSH_TRY(expr)              \
+    do {                           \
+        const int _st = (expr);    \
+        if (_st != LSH_OK) return _st; \
+    } while (0)
+
+}  // namespace
+
+extern "C" {
+
+const char* lsh_status_string(int status) {
+    switch (status) {
+        case LSH_OK: return "ok";
+        case LSH_ERR_INVALID: return "invalid argument";
+        case LSH_ERR_UNSUPPORTED: return "unsupported configuration";
+        case LSH_ERR_HIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+size_t lsh_workspace_bytes(const lsh_config* cfg, lsh_dtype dtype, int op) {
+    if (check_config(cfg) != LSH_OK || check_dtype(dtype) != LSH_OK) return 0;
+    const int64_t BH = bh_of(cfg);
+    const size_t hash = lsh::hash_workspace_bytes(cfg->n_rounds, cfg->n_buckets);
+    const size_t sort = lsh::sort_workspace_bytes(BH, cfg->L, cfg->n_rounds, cfg->n_buckets);
+    switch (op) {
+        case LSH_OP_HASH: return hash;
+        case LSH_OP_SORT: return sort;
+        case LSH_OP_ATTN_FWD: return 0;
+        case LSH_OP_COMBINE: return 0;
+        case LSH_OP_ATTN_BWD: return lsh::bwd_workspace_bytes(BH, cfg->L, cfg->n_rounds);
+        case LSH_OP_FORWARD: return fwd_rounds_bytes(cfg) + (hash > sort ? hash : sort);
+        default: return 0;
+    }
+}
+
+int lsh_hash(const lsh_config* cfg, lsh_dtype dtype, const void* q, const float* R,
+             int32_t* buckets, void* workspace, size_t workspace_bytes, void* stream) {
+    LSH_TRY(check_config(cfg));
+    LSH_TRY(check_dtype(dtype));
+    if (!q || !R || !buckets || !workspace) return LSH_ERR_INVALID;
+    if (workspace_bytes < lsh::hash_workspace_bytes(cfg->n_rounds, cfg->n_buckets))
+        return LSH_ERR_INVALID;
+    LSH_TRY(check_supported(cfg));
+    const int64_t rows = bh_of(cfg) * cfg->L;
+    return status_of(lsh::launch_hash(q, dtype == LSH_F32, rows, cfg->n_rounds, cfg->n_buckets, R,
+                                      buckets, workspace, static_cast<hipStream_t>(stream)));
+}
+
+int lsh_sort_permute(const lsh_config* cfg, const int32_t* buckets, int32_t* perm, int32_t* undo,
+                     int32_t* bucket_start, void* workspace, size_t workspace_bytes,
+                     void* stream) {
+    LSH_TRY(check_config(cfg));
+    if (!buckets || !perm || !undo || !bucket_start || !workspace) return LSH_ERR_INVALID;
+    if (workspace_bytes <
+        lsh::sort_workspace_bytes(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets))
+        return LSH_ERR_INVALID;
+    LSH_TRY(check_supported(cfg));
+    return status_of(lsh::launch_sort(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets, buckets,
+                                      perm, undo, bucket_start, workspace,
+                                      static_cast<hipStream_t>(stream)));
+}
+
+int lsh_gather_rows(const lsh_config* cfg, lsh_dtype dtype, const void* src, const int32_t* perm,
+                    void* dst, void* stream) {
+    LSH_TRY(check_config(cfg));
+    LSH_TRY(check_dtype(dtype));
+    if (!src || !perm || !dst) return LSH_ERR_INVALID;
+    LSH_TRY(check_supported(cfg));
+    return status_of(lsh::launch_gather(bh_of(cfg), cfg->L, cfg->n_rounds, dtype == LSH_F32, src,
+                                        perm, dst, static_cast<hipStream_t>(stream)));
+}
+
+int lsh_chunk_attn_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, const void* v,
+                       const int32_t* buckets, const int32_t* perm, const int32_t* bucket_start,
+                       float* o_rounds, float* lse_rounds, void* stream) {
+    LSH_TRY(check_config(cfg));
+    LSH_TRY(check_dtype(dtype));
+    if (!q || !v || !buckets || !perm || !bucket_start || !o_rounds || !lse_rounds)
+        return LSH_ERR_INVALID;
+    LSH_TRY(check_supported(cfg));
+    return status_of(lsh::launch_attn_fwd(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets,
+                                          cfg->causal != 0, cfg->scale, cfg->self_mask,
+                                          dtype == LSH_F32, q, v, buckets, perm, bucket_start,
+                                          o_rounds, lse_rounds, static_cast<hipStream_t>(stream)));
+}
+
+int lsh_combine_rounds(const lsh_config* cfg, lsh_dtype dtype, const float* o_rounds,
+                       const float* lse_rounds, const int32_t* undo, void* out, float* lse_total,
+                       void* stream) {
+    LSH_TRY(check_config(cfg));
+    LSH_TRY(check_dtype(dtype));
+    if (!o_rounds || !lse_rounds || !undo || !out) return LSH_ERR_INVALID;
+    LSH_TRY(check_supported(cfg));
+    return status_of(lsh::launch_combine(bh_of(cfg), cfg->L, cfg->n_rounds, dtype == LSH_F32,
+                                         o_rounds, lse_rounds, undo, out, lse_total,
+                                         static_cast<hipStream_t>(stream)));
+}
+
+int lsh_attention_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, const void* v,
+                      const float* R, void* out, float* lse_total, int32_t* buckets,
+                      int32_t* perm, int32_t* undo, int32_t* bucket_start, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+    LSH_TRY(check_config(cfg));
+    LSH_TRY(check_dtype(dtype));
+    if (!q || !v || !R || !out || !buckets || !perm || !undo || !bucket_start || !workspace)
+        return LSH_ERR_INVALID;
+    if (workspace_bytes < lsh_workspace_bytes(cfg, dtype, LSH_OP_FORWARD)) return LSH_ERR_INVALID;
+    LSH_TRY(check_supported(cfg));
+    const size_t rr = (size_t)bh_of(cfg) * cfg->n_rounds * cfg->L;
+    char* ws = static_cast<char*>(workspace);
+    float* o_rounds = reinterpret_cast<float*>(ws);
+    float* lse_rounds = reinterpret_cast<float*>(ws + lsh::align256(rr * cfg->d * sizeof(float)));
+    void* scratch = ws + fwd_rounds_bytes(cfg);
+    const size_t scratch_bytes = workspace_bytes - fwd_rounds_bytes(cfg);
+    LSH_TRY(lsh_hash(cfg, dtype, q, R, buckets, scratch, scratch_bytes, stream));
+    LSH_TRY(lsh_sort_permute(cfg, buckets, perm, undo, bucket_start, scratch, scratch_bytes, stream));
+    LSH_TRY(lsh_chunk_attn_fwd(cfg, dtype, q, v, buckets, perm, bucket_start, o_rounds, lse_rounds,
+                               stream));
+    return lsh_combine_rounds(cfg, dtype, o_rounds, lse_rounds, undo, out, lse_total, stream);
+}
+
+int lsh_chunk_attn_bwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, const void* v,
+                       const void* out, const void* dout, const float* lse_total,
+                       const int32_t* buckets, const int32_t* perm, const int32_t* undo,
+                       const int32_t* bucket_start, float* dq, float* dv, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+    LSH_TRY(check_config(cfg));
+    LSH_TRY(check_dtype(dtype));
+    if (!q || !v || !out || !dout || !lse_total || !buckets || !perm || !undo || !bucket_start ||
+        !dq || !dv || !workspace)
+        return LSH_ERR_INVALID;
+    if (workspace_bytes < lsh::bwd_workspace_bytes(bh_of(cfg), cfg->L, cfg->n_rounds))
+        return LSH_ERR_INVALID;
+    LSH_TRY(check_supported(cfg));
+    if (dtype != LSH_BF16) return LSH_ERR_UNSUPPORTED;
+    return status_of(lsh::launch_attn_bwd(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets,
+                                          cfg->causal != 0, cfg->scale, cfg->self_mask, q, v, out,
+                                          dout, lse_total, buckets, perm, undo, bucket_start, dq,
+                                          dv, workspace, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,196 @@
+// Stable counting sort of each (batch, head, round) segment by bucket, then
+// position (Reformer, Sec. 2 "LSH attention": the permutation i -> s_i;
+// App. A: one permutation s^(r) per round), and the row gather into sorted
+// order.
+//
+// A segment of L positions is cut into tiles of kTile positions.
+//   1. hist:    per (tile, round) bucket counts, LDS atomics.
+//   2. scan:    exclusive scan of the counts in (bucket, tile) order gives
+//               every (bucket, tile) pair its first output slot, and the
+//               bucket start offsets.
+//   3. scatter: each wave ranks its quarter of a tile in position order; the
+//               rank of a position among equal buckets of its 64-lane group
+//               comes from ballots over the bucket bits (peer mask + popcount),
+//               so equal keys keep their position order (stable).
+#include "common.h"
+#include "launch.h"
+
+namespace lsh {
+namespace {
+
+constexpr int kTile = 4096;
+constexpr int kSortWaves = 4;
+constexpr int kPerWave = kTile / kSortWaves;
+constexpr int kHistLdsInts = 8192;
+
+__device__ __forceinline__ int clamp_bucket(int b, int n_b) { return min(max(b, 0), n_b - 1); }
+
+__global__ __launch_bounds__(256) void sort_hist_kernel(const int32_t* __restrict__ buckets, int L,
+                                                        int n_r, int n_b, int rounds_per_group,
+                                                        int n_tiles, int32_t* __restrict__ counts) {
+    extern __shared__ int hist[];
+    const int tile = blockIdx.x;
+    const int64_t bh = blockIdx.y;
+    const int r0 = blockIdx.z * rounds_per_group;
+    const int nr = min(rounds_per_group, n_r - r0);
+    for (int i = threadIdx.x; i < nr * n_b; i += blockDim.x) hist[i] = 0;
+    __syncthreads();
+    const int p0 = tile * kTile, p1 = min(L, p0 + kTile);
+    for (int p = p0 + threadIdx.x; p < p1; p += blockDim.x) {
+        const int32_t* row = buckets + (bh * L + p) * n_r + r0;
+        for (int r = 0; r < nr; ++r) atomicAdd(&hist[r * n_b + clamp_bucket(row[r], n_b)], 1);
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < nr * n_b; i += blockDim.x) {
+        const int r = r0 + i / n_b, b = i % n_b;
+        counts[((bh * n_r + r) * n_b + b) * n_tiles + tile] = hist[i];
+    }
+}
+
+__global__ __launch_bounds__(256) void sort_scan_kernel(int32_t* __restrict__ counts, int L,
+                                                        int n_b, int n_tiles,
+                                                        int32_t* __restrict__ bucket_start) {
+    __shared__ int part[256];
+    const int64_t seg = blockIdx.x;
+    const int64_t E = (int64_t)n_b * n_tiles;
+    int32_t* c = counts + seg * E;
+    int32_t* bs = bucket_start + seg * (n_b + 1);
+    const int64_t per = (E + 255) / 256;
+    const int64_t lo = min(E, threadIdx.x * per), hi = min(E, lo + per);
+    int s = 0;
+    for (int64_t e = lo; e < hi; ++e) s += c[e];
+    part[threadIdx.x] = s;
+    __syncthreads();
+    // Hillis-Steele inclusive scan over 256 partial sums.
+    for (int o = 1; o < 256; o <<= 1) {
+        const int x = (int)threadIdx.x >= o ? part[threadIdx.x - o] : 0;
+        __syncthreads();
+        part[threadIdx.x] += x;
+        __syncthreads();
+    }
+    int run = part[threadIdx.x] - s;
+    for (int64_t e = lo; e < hi; ++e) {
+        const int v = c[e];
+        c[e] = run;
+        if (e % n_tiles == 0) bs[e / n_tiles] = run;
+        run += v;
+    }
+    if (threadIdx.x == 0) bs[n_b] = L;
+}
+
+__global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __restrict__ buckets,
+                                                           const int32_t* __restrict__ offsets,
+                                                           int L, int n_r, int n_b, int n_bits,
+                                                           int n_tiles, int32_t* __restrict__ perm,
+                                                           int32_t* __restrict__ undo) {
+    extern __shared__ int base[];  // [kSortWaves][n_b]
+    const int tile = blockIdx.x;
+    const int64_t seg = blockIdx.y;
+    const int64_t bh = seg / n_r;
+    const int r = (int)(seg % n_r);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int* wbase = base + wave * n_b;
+
+    for (int i = threadIdx.x; i < kSortWaves * n_b; i += blockDim.x) base[i] = 0;
+    __syncthreads();
+    const int p0 = tile * kTile + wave * kPerWave;
+    const int p1 = min(L, p0 + kPerWave);
+    for (int p = p0 + lane; p < p1; p += 64)
+        atomicAdd(&wbase[clamp_bucket(buckets[(bh * L + p) * n_r + r], n_b)], 1);
+    __syncthreads();
+    // Per-wave starting slot of every bucket: the tile's offset plus the counts
+    // of the earlier waves of this tile.
+    for (int b = threadIdx.x; b < n_b; b += blockDim.x) {
+        int off = offsets[(seg * n_b + b) * n_tiles + tile];
+        for (int w = 0; w < kSortWaves; ++w) {
+            const int cnt = base[w * n_b + b];
+            base[w * n_b + b] = off;
+            off += cnt;
+        }
+    }
+    __syncthreads();
+
+    int32_t* pseg = perm + seg * L;
+    int32_t* useg = undo + seg * L;
+    const uint64_t lt_mask = (1ull << lane) - 1ull;
+    for (int p = p0; p < p1; p += 64) {
+        const int pos = p + lane;
+        const bool active = pos < p1;
+        const int b = active ? clamp_bucket(buckets[(bh * L + pos) * n_r + r], n_b) : 0;
+        uint64_t peers = __ballot(active);
+        for (int bit = 0; bit < n_bits; ++bit) {
+            const bool set = (b >> bit) & 1;
+            const uint64_t m = __ballot(set && active);
+            peers &= set ? m : ~m;
+        }
+        const int before = __popcll(peers & lt_mask);
+        const int start = wbase[b];
+        if (active) {
+            const int slot = start + before;
+            pseg[slot] = pos;
+            useg[pos] = slot;
+            if ((peers >> lane) == 1ull) wbase[b] = start + __popcll(peers);
+        }
+    }
+}
+
+// dst[seg][s] = src[bh][perm[seg][s]] for rows of `row_bytes`, 16 B per thread.
+__global__ __launch_bounds__(256) void gather_kernel(const char* __restrict__ src,
+                                                     const int32_t* __restrict__ perm, int L,
+                                                     int n_r, int parts, int64_t total,
+                                                     char* __restrict__ dst) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += stride) {
+        const int part = (int)(idx % parts);
+        const int64_t out_row = idx / parts;  // (seg, s)
+        const int64_t seg = out_row / L;
+        const int64_t bh = seg / n_r;
+        const int64_t in_row = bh * L + min(max(perm[out_row], 0), L - 1);
+        *reinterpret_cast<u32x4*>(dst + (out_row * parts + part) * 16) =
+            *reinterpret_cast<const u32x4*>(src + (in_row * parts + part) * 16);
+    }
+}
+
+}  // namespace
+
+int sort_tile_positions(int L) { return kTile; }
+
+size_t sort_workspace_bytes(int64_t BH, int L, int n_rounds, int n_buckets) {
+    const int64_t n_tiles = (L + kTile - 1) / kTile;
+    return align256((size_t)(BH * n_rounds * n_buckets * n_tiles) * sizeof(int32_t));
+}
+
+hipError_t launch_sort(int64_t BH, int L, int n_rounds, int n_buckets, const int32_t* buckets,
+                       int32_t* perm, int32_t* undo, int32_t* bucket_start, void* workspace,
+                       hipStream_t stream) {
+    if (BH == 0 || L == 0) return hipSuccess;
+    const int n_tiles = (L + kTile - 1) / kTile;
+    int32_t* counts = static_cast<int32_t*>(workspace);
+    const int rpg = std::max(1, std::min(n_rounds, kHistLdsInts / n_buckets));
+    const int groups = (n_rounds + rpg - 1) / rpg;
+    int n_bits = 0;
+    while ((1 << n_bits) < n_buckets) ++n_bits;
+
+    sort_hist_kernel<<<dim3(n_tiles, (unsigned)BH, groups), 256, rpg * n_buckets * sizeof(int), stream>>>(
+        buckets, L, n_rounds, n_buckets, rpg, n_tiles, counts);
+    sort_scan_kernel<<<(unsigned)(BH * n_rounds), 256, 0, stream>>>(counts, L, n_buckets, n_tiles,
+                                                                    bucket_start);
+    sort_scatter_kernel<<<dim3(n_tiles, (unsigned)(BH * n_rounds)), 256,
+                          kSortWaves * n_buckets * sizeof(int), stream>>>(
+        buckets, counts, L, n_rounds, n_buckets, n_bits, n_tiles, perm, undo);
+    return hipGetLastError();
+}
+
+hipError_t launch_gather(int64_t BH, int L, int n_rounds, bool f32, const void* src,
+                         const int32_t* perm, void* dst, hipStream_t stream) {
+    const int parts = (f32 ? 4 : 2) * kHeadDim / 16;
+    const int64_t total = BH * n_rounds * (int64_t)L * parts;
+    if (total == 0) return hipSuccess;
+    const int64_t blocks = std::min<int64_t>((total + 255) / 256, 65536);
+    gather_kernel<<<(unsigned)blocks, 256, 0, stream>>>(static_cast<const char*>(src), perm, L,
+                                                         n_rounds, parts, total,
+                                                         static_cast<char*>(dst));
+    return hipGetLastError();
+}
+
+}  // namespace lsh

@@ -1,0 +1,295 @@
+"""Thin Python binding of liblsh (the C ABI in include/lsh.h).
+
+Two layers:
+  * ``lib()`` exposes the raw C entry points; they take an ``LshConfig``,
+    raw device pointers (ints), sizes and a stream handle, and return the
+    status code unchanged.
+  * The module functions of the same names (``lsh_hash``,
+    ``lsh_sort_permute``, ``lsh_chunk_attn_fwd``, ...) marshal torch tensors: they check shapes and dtypes, allocate outputs and
+    workspace with torch, call the C entry point on torch's current stream
+    and raise ``LshError`` on a non-zero status.  All arithmetic happens in
+    the HIP kernels behind the C ABI.
+
+Nothing here falls back to another implementation: if liblsh.so is missing
+or fails to load, importing a compute function raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "liblsh.so")
+
+LSH_OK, LSH_ERR_INVALID, LSH_ERR_UNSUPPORTED, LSH_ERR_HIP = 0, -1, -2, -3
+LSH_F32, LSH_BF16 = 0, 1
+(LSH_OP_HASH, LSH_OP_SORT, LSH_OP_ATTN_FWD, LSH_OP_COMBINE, LSH_OP_ATTN_BWD,
+ LSH_OP_FORWARD) = range(6)
+
+# Every symbol include/lsh.h declares.
+EXPORTED = ("lsh_status_string", "lsh_workspace_bytes", "lsh_hash", "lsh_sort_permute",
+            "lsh_gather_rows", "lsh_chunk_attn_fwd", "lsh_combine_rounds", "lsh_attention_fwd",
+            "lsh_chunk_attn_bwd")
+
+
+class LshConfig(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("L", ctypes.c_int32),
+                ("d", ctypes.c_int32), ("n_buckets", ctypes.c_int32),
+                ("n_rounds", ctypes.c_int32), ("chunk", ctypes.c_int32),
+                ("causal", ctypes.c_int32), ("scale", ctypes.c_float),
+                ("self_mask", ctypes.c_float)]
+
+
+class LshError(RuntimeError):
+    def __init__(self, call: str, status: int):
+        msg = _lib.lsh_status_string(status).decode() if _lib is not None else str(status)
+        super().__init__(f"{call} failed: {msg} ({status})")
+        self.status = status
+
+
+_lib = None
+_P = ctypes.c_void_p
+_CFG = ctypes.POINTER(LshConfig)
+_SZ = ctypes.c_size_t
+_I = ctypes.c_int
+
+
+def lib() -> ctypes.CDLL:
+    """Load liblsh.so (built by paper_2001_04451_amd.build); raise if absent."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2001_04451_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        L.lsh_status_string.argtypes = [_I]
+        L.lsh_status_string.restype = ctypes.c_char_p
+        L.lsh_workspace_bytes.argtypes = [_CFG, _I, _I]
+        L.lsh_workspace_bytes.restype = _SZ
+        sigs = {
+            "lsh_hash": [_CFG, _I, _P, _P, _P, _P, _SZ, _P],
+            "lsh_sort_permute": [_CFG, _P, _P, _P, _P, _P, _SZ, _P],
+            "lsh_gather_rows": [_CFG, _I, _P, _P, _P, _P],
+            "lsh_chunk_attn_fwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P],
+            "lsh_combine_rounds": [_CFG, _I, _P, _P, _P, _P, _P, _P],
+            "lsh_attention_fwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
+            "lsh_chunk_attn_bwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ,
+                                   _P],
+        }
+        for name, args in sigs.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = _I
+        _lib = L
+    return _lib
+
+
+# --------------------------------------------------------------------------
+# configuration
+# --------------------------------------------------------------------------
+@dataclass(frozen=True)
+class Config:
+    B: int
+    H: int
+    L: int
+    n_buckets: int
+    n_rounds: int
+    chunk: int = 64
+    causal: bool = False
+    d: int = 64
+    scale: float | None = None
+    self_mask: float = 1e5
+
+    def c(self) -> LshConfig:
+        scale = 1.0 / math.sqrt(self.d) if self.scale is None else self.scale
+        return LshConfig(self.B, self.H, self.L, self.d, self.n_buckets, self.n_rounds, self.chunk,
+                         int(bool(self.causal)), scale, self.self_mask)
+
+    @staticmethod
+    def of(w) -> "Config":
+        """From a workloads.Workload."""
+        return Config(B=w.B, H=w.H, L=w.L, n_buckets=w.n_buckets, n_rounds=w.n_rounds,
+                      chunk=w.chunk, causal=w.causal, d=w.d)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return LSH_F32
+    if t.dtype == torch.bfloat16:
+        return LSH_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(device: torch.device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _check(call: str, status: int) -> None:
+    if status != LSH_OK:
+        raise LshError(call, status)
+
+
+def _need(t: torch.Tensor, shape, dtype=None, name="tensor") -> None:
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def workspace_bytes(cfg: Config, dtype: torch.dtype, op: int) -> int:
+    code = LSH_BF16 if dtype == torch.bfloat16 else LSH_F32
+    return int(lib().lsh_workspace_bytes(ctypes.byref(cfg.c()), code, op))
+
+
+def _workspace(cfg: Config, dtype: torch.dtype, op: int, device) -> torch.Tensor:
+    n = workspace_bytes(cfg, dtype, op)
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+
+
+# --------------------------------------------------------------------------
+# torch-level calls, one per C entry point
+# --------------------------------------------------------------------------
+def lsh_hash(cfg: Config, q: torch.Tensor, R: torch.Tensor, buckets: torch.Tensor | None = None,
+         workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """Bucket ids [B,H,L,n_rounds] int32 (lsh_hash)."""
+    _need(q, (cfg.B, cfg.H, cfg.L, cfg.d), name="q")
+    _need(R, (cfg.n_rounds, cfg.d, cfg.n_buckets // 2), torch.float32, "R")
+    if buckets is None:
+        buckets = torch.empty((cfg.B, cfg.H, cfg.L, cfg.n_rounds), dtype=torch.int32, device=q.device)
+    if workspace is None:
+        workspace = _workspace(cfg, q.dtype, LSH_OP_HASH, q.device)
+    _check("lsh_hash", lib().lsh_hash(ctypes.byref(cfg.c()), _dtype_code(q), _ptr(q), _ptr(R),
+                                      _ptr(buckets), _ptr(workspace), workspace.numel(),
+                                      _stream(q.device)))
+    return buckets
+
+
+def lsh_sort_permute(cfg: Config, buckets: torch.Tensor, workspace: torch.Tensor | None = None):
+    """perm, undo [B,H,n_r,L] and bucket_start [B,H,n_r,n_b+1] (lsh_sort_permute)."""
+    _need(buckets, (cfg.B, cfg.H, cfg.L, cfg.n_rounds), torch.int32, "buckets")
+    dev = buckets.device
+    perm = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.L), dtype=torch.int32, device=dev)
+    undo = torch.empty_like(perm)
+    bstart = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.n_buckets + 1), dtype=torch.int32,
+                         device=dev)
+    if workspace is None:
+        workspace = _workspace(cfg, torch.float32, LSH_OP_SORT, dev)
+    _check("lsh_sort_permute",
+           lib().lsh_sort_permute(ctypes.byref(cfg.c()), _ptr(buckets), _ptr(perm), _ptr(undo),
+                                  _ptr(bstart), _ptr(workspace), workspace.numel(), _stream(dev)))
+    return perm, undo, bstart
+
+
+def lsh_gather_rows(cfg: Config, src: torch.Tensor, perm: torch.Tensor) -> torch.Tensor:
+    """Rows of src in sorted order [B,H,n_r,L,d] (lsh_gather_rows)."""
+    _need(src, (cfg.B, cfg.H, cfg.L, cfg.d), name="src")
+    _need(perm, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.int32, "perm")
+    dst = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.L, cfg.d), dtype=src.dtype, device=src.device)
+    _check("lsh_gather_rows", lib().lsh_gather_rows(ctypes.byref(cfg.c()), _dtype_code(src),
+                                                    _ptr(src), _ptr(perm), _ptr(dst),
+                                                    _stream(src.device)))
+    return dst
+
+
+def lsh_chunk_attn_fwd(cfg: Config, q, v, buckets, perm, bstart, o_rounds=None, lse_rounds=None):
+    """Per-round outputs o_rounds [B,H,n_r,L,d] and lse_rounds [B,H,n_r,L], sorted order."""
+    _need(q, (cfg.B, cfg.H, cfg.L, cfg.d), name="q")
+    _need(v, (cfg.B, cfg.H, cfg.L, cfg.d), q.dtype, "v")
+    _need(perm, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.int32, "perm")
+    _need(bstart, (cfg.B, cfg.H, cfg.n_rounds, cfg.n_buckets + 1), torch.int32, "bucket_start")
+    _need(buckets, (cfg.B, cfg.H, cfg.L, cfg.n_rounds), torch.int32, "buckets")
+    dev = q.device
+    if o_rounds is None:
+        o_rounds = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.L, cfg.d), dtype=torch.float32,
+                               device=dev)
+    if lse_rounds is None:
+        lse_rounds = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.L), dtype=torch.float32,
+                                 device=dev)
+    _check("lsh_chunk_attn_fwd",
+           lib().lsh_chunk_attn_fwd(ctypes.byref(cfg.c()), _dtype_code(q), _ptr(q), _ptr(v),
+                                    _ptr(buckets), _ptr(perm), _ptr(bstart), _ptr(o_rounds),
+                                    _ptr(lse_rounds), _stream(dev)))
+    return o_rounds, lse_rounds
+
+
+def lsh_combine_rounds(cfg: Config, o_rounds, lse_rounds, undo, out_dtype: torch.dtype,
+                   out=None, lse_total=None):
+    """Output [B,H,L,d] in out_dtype and lse_total [B,H,L] fp32 (lsh_combine_rounds)."""
+    _need(o_rounds, (cfg.B, cfg.H, cfg.n_rounds, cfg.L, cfg.d), torch.float32, "o_rounds")
+    _need(lse_rounds, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.float32, "lse_rounds")
+    _need(undo, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.int32, "undo")
+    dev = o_rounds.device
+    if out is None:
+        out = torch.empty((cfg.B, cfg.H, cfg.L, cfg.d), dtype=out_dtype, device=dev)
+    if lse_total is None:
+        lse_total = torch.empty((cfg.B, cfg.H, cfg.L), dtype=torch.float32, device=dev)
+    _check("lsh_combine_rounds",
+           lib().lsh_combine_rounds(ctypes.byref(cfg.c()), _dtype_code(out), _ptr(o_rounds),
+                                    _ptr(lse_rounds), _ptr(undo), _ptr(out), _ptr(lse_total),
+                                    _stream(dev)))
+    return out, lse_total
+
+
+class ForwardState:
+    """Buffers of one forward pass; reusable across calls of the same shape."""
+
+    def __init__(self, cfg: Config, dtype: torch.dtype, device):
+        self.cfg = cfg
+        B, H, L, nr, nb = cfg.B, cfg.H, cfg.L, cfg.n_rounds, cfg.n_buckets
+        self.out = torch.empty((B, H, L, cfg.d), dtype=dtype, device=device)
+        self.lse = torch.empty((B, H, L), dtype=torch.float32, device=device)
+        self.buckets = torch.empty((B, H, L, nr), dtype=torch.int32, device=device)
+        self.perm = torch.empty((B, H, nr, L), dtype=torch.int32, device=device)
+        self.undo = torch.empty_like(self.perm)
+        self.bstart = torch.empty((B, H, nr, nb + 1), dtype=torch.int32, device=device)
+        self.workspace = _workspace(cfg, dtype, LSH_OP_FORWARD, device)
+
+
+def lsh_attention_fwd(cfg: Config, q, v, R, state: ForwardState | None = None) -> ForwardState:
+    """The whole forward (lsh_attention_fwd): hash, sort, chunked attention, combine."""
+    _need(q, (cfg.B, cfg.H, cfg.L, cfg.d), name="q")
+    _need(v, (cfg.B, cfg.H, cfg.L, cfg.d), q.dtype, "v")
+    _need(R, (cfg.n_rounds, cfg.d, cfg.n_buckets // 2), torch.float32, "R")
+    if state is None:
+        state = ForwardState(cfg, q.dtype, q.device)
+    s = state
+    _check("lsh_attention_fwd",
+           lib().lsh_attention_fwd(ctypes.byref(cfg.c()), _dtype_code(q), _ptr(q), _ptr(v), _ptr(R),
+                                   _ptr(s.out), _ptr(s.lse), _ptr(s.buckets), _ptr(s.perm),
+                                   _ptr(s.undo), _ptr(s.bstart), _ptr(s.workspace),
+                                   s.workspace.numel(), _stream(q.device)))
+    return state
+
+
+def lsh_chunk_attn_bwd(cfg: Config, q, v, out, dout, lse_total, buckets, perm, undo, bstart,
+                   dq=None, dv=None, workspace=None):
+    """dq, dv [B,H,L,d] fp32 (lsh_chunk_attn_bwd)."""
+    shp = (cfg.B, cfg.H, cfg.L, cfg.d)
+    _need(q, shp, name="q")
+    for name, t in (("v", v), ("out", out), ("dout", dout)):
+        _need(t, shp, q.dtype, name)
+    _need(lse_total, (cfg.B, cfg.H, cfg.L), torch.float32, "lse_total")
+    dev = q.device
+    if dq is None:
+        dq = torch.empty(shp, dtype=torch.float32, device=dev)
+    if dv is None:
+        dv = torch.empty(shp, dtype=torch.float32, device=dev)
+    if workspace is None:
+        workspace = _workspace(cfg, q.dtype, LSH_OP_ATTN_BWD, dev)
+    _check("lsh_chunk_attn_bwd",
+           lib().lsh_chunk_attn_bwd(ctypes.byref(cfg.c()), _dtype_code(q), _ptr(q), _ptr(v),
+                                    _ptr(out), _ptr(dout), _ptr(lse_total), _ptr(buckets),
+                                    _ptr(perm), _ptr(undo), _ptr(bstart), _ptr(dq), _ptr(dv),
+                                    _ptr(workspace), workspace.numel(), _stream(dev)))
+    return dq, dv

@@ -1,0 +1,113 @@
+"""The C ABI without a GPU: the library loads, exports every symbol the header
+declares, sizes workspaces, and rejects bad arguments before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2001_04451_amd import lsh
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lsh.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(lsh.LIB_PATH):
+        pytest.skip("liblsh.so not built (run __graft_entry__.build())")
+    return lsh.lib()
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lsh_[a-z_]+)\s*\(", text)))
+
+
+def test_header_symbols_exported(L):
+    names = declared_symbols()
+    assert set(names) == set(lsh.EXPORTED)
+    for name in names:
+        assert hasattr(L, name), f"{name} missing from liblsh.so"
+
+
+def test_status_strings(L):
+    assert L.lsh_status_string(0) == b"ok"
+    assert L.lsh_status_string(-1) == b"invalid argument"
+    assert L.lsh_status_string(-2) == b"unsupported configuration"
+    assert L.lsh_status_string(-3) == b"HIP runtime error"
+
+
+def _cfg(**kw):
+    base = dict(B=1, H=2, L=1024, d=64, n_buckets=64, n_rounds=2, chunk=64, causal=0,
+                scale=0.125, self_mask=1e5)
+    base.update(kw)
+    return lsh.LshConfig(**base)
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation
+
+
+@pytest.mark.parametrize("bad", [dict(B=0), dict(L=0), dict(d=0), dict(n_buckets=7),
+                                 dict(n_buckets=0), dict(n_rounds=0), dict(chunk=0),
+                                 dict(L=1000), dict(scale=float("nan"))])
+def test_invalid_config(L, bad):
+    c = _cfg(**bad)
+    rc = L.lsh_hash(ctypes.byref(c), lsh.LSH_BF16, FAKE, FAKE, FAKE, FAKE, 1 << 30, None)
+    assert rc == lsh.LSH_ERR_INVALID
+    rc = L.lsh_chunk_attn_fwd(ctypes.byref(c), lsh.LSH_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                              FAKE, None)
+    assert rc == lsh.LSH_ERR_INVALID
+    assert L.lsh_workspace_bytes(ctypes.byref(c), lsh.LSH_BF16, lsh.LSH_OP_FORWARD) == 0
+
+
+def test_null_pointers_and_small_workspace(L):
+    c = _cfg()
+    assert L.lsh_hash(None, 1, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == lsh.LSH_ERR_INVALID
+    assert L.lsh_hash(ctypes.byref(c), 1, None, FAKE, FAKE, FAKE, 1 << 30, None) == lsh.LSH_ERR_INVALID
+    need = L.lsh_workspace_bytes(ctypes.byref(c), 1, lsh.LSH_OP_HASH)
+    assert need > 0
+    assert L.lsh_hash(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, need - 1, None) == lsh.LSH_ERR_INVALID
+    assert L.lsh_hash(ctypes.byref(c), 7, FAKE, FAKE, FAKE, FAKE, need, None) == lsh.LSH_ERR_INVALID
+    assert L.lsh_sort_permute(ctypes.byref(c), FAKE, None, FAKE, FAKE, FAKE, 1 << 30, None) == lsh.LSH_ERR_INVALID
+    assert L.lsh_combine_rounds(ctypes.byref(c), 1, FAKE, FAKE, None, FAKE, None, None) == lsh.LSH_ERR_INVALID
+    fwd = L.lsh_workspace_bytes(ctypes.byref(c), 1, lsh.LSH_OP_FORWARD)
+    assert L.lsh_attention_fwd(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE,
+                               FAKE, FAKE, fwd - 1, None) == lsh.LSH_ERR_INVALID
+
+
+@pytest.mark.parametrize("unsup", [dict(d=32), dict(chunk=128, L=1024), dict(n_buckets=2048),
+                                   dict(n_rounds=17)])
+def test_unsupported_shapes(L, unsup):
+    c = _cfg(**unsup)
+    need = L.lsh_workspace_bytes(ctypes.byref(c), 1, lsh.LSH_OP_FORWARD)
+    rc = L.lsh_attention_fwd(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE,
+                             FAKE, FAKE, need, None)
+    assert rc == lsh.LSH_ERR_UNSUPPORTED
+
+
+def test_backward_is_bf16_only(L):
+    c = _cfg()
+    need = L.lsh_workspace_bytes(ctypes.byref(c), lsh.LSH_F32, lsh.LSH_OP_ATTN_BWD)
+    rc = L.lsh_chunk_attn_bwd(ctypes.byref(c), lsh.LSH_F32, *([FAKE] * 12), need, None)
+    assert rc == lsh.LSH_ERR_UNSUPPORTED
+
+
+def test_workspace_sizes(L):
+    c = _cfg(B=1, H=16, L=65536, n_buckets=1024, n_rounds=8)
+    rr = 16 * 65536 * 8
+    fwd = L.lsh_workspace_bytes(ctypes.byref(c), 1, lsh.LSH_OP_FORWARD)
+    assert fwd >= rr * 64 * 4 + rr * 4
+    assert L.lsh_workspace_bytes(ctypes.byref(c), 1, lsh.LSH_OP_ATTN_FWD) == 0
+
+
+def test_product_never_touches_the_oracle():
+    """The GPU package imports, links and includes nothing from oracle/."""
+    pkg = os.path.join(ROOT, "paper_2001_04451_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".cpp", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"^\s*(import|from)\s+oracle", text, re.M), f
+                assert "lsh_oracle" not in text and "lsh_ref_" not in text, f

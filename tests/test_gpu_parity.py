@@ -1,0 +1,166 @@
+"""GPU path (through the C ABI) against the fp64 oracle, stage by stage.
+
+Every input is drawn by the seeded generators of paper_2001_04451_amd.workloads
+or by the test itself; nothing the GPU writes is fed to the oracle.  Bucket
+ids, permutations and bucket offsets must be bit-exact; floating-point
+outputs must be within 1e-5 (fp32) or 2e-2 (bf16, fp32 accumulation) max-abs.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2001_04451_amd import lsh
+from paper_2001_04451_amd import workloads as W
+
+from gpu_common import log, lse_close, out_tolerance, small, to_device, torch_dtype
+
+pytestmark = pytest.mark.gpu
+
+# Reduced copies of the five workloads: same n_b, n_r, dtype, causal flag and
+# input distribution; sizes span several chunks, rows blocks and sort tiles.
+SMALL = {
+    "tiny_f32_L1024": small("tiny_f32_L1024"),
+    "mixture_bf16_L4096": small("mixture_bf16_L4096", B=2, H=2),
+    "causal_bf16_L16384": small("causal_bf16_L16384", B=1, H=2, L=4096),
+    "long_bf16_L65536": small("long_bf16_L65536", H=1, L=8192),
+    "fwdbwd_bf16_L32768": small("fwdbwd_bf16_L32768", B=1, H=2, L=4096),
+}
+
+
+def _inputs(w):
+    x = W.make_inputs(w)
+    q64, v64 = W.as_f64(x["q"], w.dtype), W.as_f64(x["v"], w.dtype)
+    return x, q64, v64
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lsh.lib()
+    return torch.device("cuda:0")
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_hash_bit_exact(gpu, name):
+    w = SMALL[name]
+    x, q64, _ = _inputs(w)
+    want, near = oracle.lsh_hash(q64, x["R"].astype(np.float64))
+    cfg = lsh.Config.of(w)
+    log("hash", name, w)
+    got = lsh.lsh_hash(cfg, to_device(x["q"], w.dtype), to_device(x["R"], "f32")).cpu().numpy()
+    mism = got != want
+    print(f"{name}: near-tie row-rounds {int(near.sum())}, mismatches {int(mism.sum())}"
+          f" (all inside near ties: {bool((~mism | near).all())})")
+    assert not (mism & ~near).any(), "bucket id differs outside the near-tie set"
+    assert mism.sum() == 0
+
+
+@pytest.mark.parametrize("n_buckets,L,n_rounds,B,H", [
+    (2, 64, 1, 1, 1), (16, 1024, 1, 1, 1), (64, 4096, 2, 2, 3), (1024, 8192, 3, 1, 2),
+    (1024, 4160, 2, 1, 1), (512, 12352, 4, 1, 1), (256, 64, 16, 2, 1)])
+def test_sort_bit_exact(gpu, n_buckets, L, n_rounds, B, H):
+    """Counting sort vs the oracle on test-drawn ids, including ragged tiles
+    (L not a multiple of 4096), empty buckets and one-bucket segments."""
+    rng = np.random.Generator(np.random.PCG64(L + n_buckets))
+    b = rng.integers(0, n_buckets, size=(B, H, L, n_rounds)).astype(np.int32)
+    b[0, 0, :, 0] = n_buckets - 1  # one segment entirely in the last bucket
+    if n_buckets >= 64:
+        b[..., -1] = rng.integers(0, 3, size=(B, H, L))  # a segment with few buckets
+    perm_want, undo_want = oracle.lsh_sort_permute(b)
+    cfg = lsh.Config(B=B, H=H, L=L, n_buckets=n_buckets, n_rounds=n_rounds)
+    log("sort", B, H, L, n_rounds, n_buckets)
+    perm, undo, bstart = lsh.lsh_sort_permute(cfg, torch.from_numpy(b).cuda())
+    assert np.array_equal(perm.cpu().numpy(), perm_want)
+    assert np.array_equal(undo.cpu().numpy(), undo_want)
+    # first sorted slot of every bucket, last entry L
+    bs = bstart.cpu().numpy()
+    for bb in range(B):
+        for hh in range(H):
+            for r in range(n_rounds):
+                keys = b[bb, hh, :, r][perm_want[bb, hh, r]]
+                want_bs = np.searchsorted(keys, np.arange(n_buckets + 1), side="left")
+                assert np.array_equal(bs[bb, hh, r], want_bs)
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_chunk_attention_and_combine(gpu, name):
+    """Attention and combine on oracle-drawn bucket ids (the oracle's own
+    hash of the generator's q), sorted on the GPU."""
+    w = SMALL[name]
+    x, q64, v64 = _inputs(w)
+    ref = oracle.lsh_attention_fwd(q64, v64, x["R"].astype(np.float64), w.chunk, w.causal)
+    cfg = lsh.Config.of(w)
+    q, v = to_device(x["q"], w.dtype), to_device(x["v"], w.dtype)
+    buckets = torch.from_numpy(ref["buckets"]).cuda()
+    log("attn", name, w)
+    perm, undo, bstart = lsh.lsh_sort_permute(cfg, buckets)
+    o_r, lse_r = lsh.lsh_chunk_attn_fwd(cfg, q, v, buckets, perm, bstart)
+    out, lse = lsh.lsh_combine_rounds(cfg, o_r, lse_r, undo, torch_dtype(w.dtype))
+    torch.cuda.synchronize()
+    tol = out_tolerance(w.dtype)
+    err_or = np.abs(o_r.cpu().numpy() - ref["o_rounds"]).max()
+    assert err_or <= tol, f"per-round output max-abs error {err_or}"
+    assert lse_close(lse_r.cpu().numpy(), ref["lse_rounds"], w.dtype).all()
+    got = out.float().cpu().numpy()
+    err = np.abs(got - ref["out"]).max()
+    print(f"{name}: out max-abs err {err:.3e} (tol {tol})")
+    assert err <= tol
+    assert lse_close(lse.cpu().numpy(), ref["lse"], w.dtype).all()
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_end_to_end_forward(gpu, name):
+    """lsh_attention_fwd (all four stages chained in the library) vs the oracle."""
+    w = SMALL[name]
+    x, q64, v64 = _inputs(w)
+    ref = oracle.lsh_attention_fwd(q64, v64, x["R"].astype(np.float64), w.chunk, w.causal)
+    cfg = lsh.Config.of(w)
+    log("forward", name, w)
+    st = lsh.lsh_attention_fwd(cfg, to_device(x["q"], w.dtype), to_device(x["v"], w.dtype),
+                               to_device(x["R"], "f32"))
+    torch.cuda.synchronize()
+    assert np.array_equal(st.buckets.cpu().numpy(), ref["buckets"])
+    assert np.array_equal(st.perm.cpu().numpy(), ref["perm"])
+    assert np.array_equal(st.undo.cpu().numpy(), ref["undo"])
+    err = np.abs(st.out.float().cpu().numpy() - ref["out"]).max()
+    print(f"{name}: end-to-end max-abs err {err:.3e}")
+    assert err <= out_tolerance(w.dtype)
+    assert lse_close(st.lse.cpu().numpy(), ref["lse"], w.dtype).all()
+
+
+def test_forward_deterministic(gpu):
+    w = SMALL["long_bf16_L65536"]
+    x = W.make_inputs(w)
+    cfg = lsh.Config.of(w)
+    q, v, R = to_device(x["q"], w.dtype), to_device(x["v"], w.dtype), to_device(x["R"], "f32")
+    log("determinism", w)
+    a = lsh.lsh_attention_fwd(cfg, q, v, R)
+    out_a = a.out.clone()
+    b = lsh.lsh_attention_fwd(cfg, q, v, R)
+    assert torch.equal(out_a.view(torch.int16), b.out.view(torch.int16))
+
+
+def test_gather_rows(gpu):
+    w = SMALL["mixture_bf16_L4096"]
+    x = W.make_inputs(w)
+    cfg = lsh.Config.of(w)
+    q = to_device(x["q"], w.dtype)
+    buckets = torch.from_numpy(oracle.lsh_hash(W.as_f64(x["q"], w.dtype), x["R"])[0]).cuda()
+    log("gather", w)
+    perm, _, _ = lsh.lsh_sort_permute(cfg, buckets)
+    got = lsh.lsh_gather_rows(cfg, q, perm)
+    p = perm.long()
+    want = torch.stack([torch.stack([q[b, h][p[b, h, r]] for r in range(w.n_rounds)])
+                        for b in range(w.B) for h in range(w.H)]).view(got.shape)
+    assert torch.equal(got.view(torch.int16), want.view(torch.int16))
+
+
+def test_invalid_arguments_on_gpu(gpu):
+    cfg = lsh.Config(B=1, H=1, L=100, n_buckets=16, n_rounds=1)  # L % 64 != 0
+    q = torch.zeros((1, 1, 100, 64), device=gpu)
+    R = torch.zeros((1, 64, 8), device=gpu)
+    with pytest.raises(lsh.LshError) as e:
+        lsh.lsh_hash(cfg, q, R)
+    assert e.value.status == lsh.LSH_ERR_INVALID
