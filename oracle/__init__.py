@@ -51,11 +51,17 @@ def _load():
         lib.lsh_ref_chunk_attn_bwd.argtypes = [_i64, _i64, _i64, _i64, _i64, ctypes.c_int,
                                                _f64, _f64, _ptr, _ptr, _ptr, _ptr, _ptr, _ptr,
                                                _ptr, _ptr, _ptr]
-        for name in ("lsh_ref_hash", "lsh_ref_sort_permute", "lsh_ref_chunk_attn_fwd",
+        lib.lsh_ref_num_threads.argtypes = []
+        for name in ("lsh_ref_num_threads", "lsh_ref_hash", "lsh_ref_sort_permute", "lsh_ref_chunk_attn_fwd",
                      "lsh_ref_combine_rounds", "lsh_ref_chunk_attn_bwd"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
     return _lib
+
+
+def num_threads() -> int:
+    """Threads the oracle's OpenMP loops use."""
+    return int(_load().lsh_ref_num_threads())
 
 
 def _f(a) -> np.ndarray:

@@ -38,10 +38,23 @@
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 #define REF_OK 0
 #define REF_ERR_INVALID -1
 #define REF_ERR_NOMEM -4
+
+/* Number of threads the parallel loops below use (reporting only). */
+int lsh_ref_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
 
 static double dot(const double *a, const double *b, int64_t d)
 {

@@ -2,14 +2,18 @@
 //   z_i = log sum_r exp z_r(i),   o_i = sum_r exp(z_r(i) - z_i) o_r(i).
 // The scatter back to position order is done as a gather through `undo`, so
 // every write is a contiguous output row.  Sixteen lanes share a row (one
-// float4 of the 64 values each); the per-round log-partitions are read once
-// per lane group and stay in L1 for the three passes.
+// float4 of the 64 values each).
 #include "common.h"
 #include "launch.h"
 
 namespace lsh {
 namespace {
 
+constexpr int kMaxRounds = 16;
+
+// All loads of a row are issued before they are used (slots, then the
+// log-partitions, then the rows), so each lane keeps up to 16 independent
+// requests in flight instead of walking a dependent chain per round.
 template <bool F32_OUT>
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ o_rounds,
                                                       const float* __restrict__ lse_rounds,
@@ -24,27 +28,37 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     const int64_t i = row % L;
     const int64_t seg0 = bh * n_r;
 
+    int64_t base[kMaxRounds];
+    float z_r[kMaxRounds];
+#pragma unroll
+    for (int r = 0; r < kMaxRounds; ++r)
+        if (r < n_r) base[r] = (seg0 + r) * L + min(max(undo[(seg0 + r) * L + i], 0), L - 1);
     float zmax = -__builtin_inff();
-    for (int r = 0; r < n_r; ++r) {
-        const int64_t s = min(max(undo[(seg0 + r) * L + i], 0), L - 1);
-        zmax = fmaxf(zmax, lse_rounds[(seg0 + r) * L + s]);
-    }
+#pragma unroll
+    for (int r = 0; r < kMaxRounds; ++r)
+        if (r < n_r) {
+            z_r[r] = lse_rounds[base[r]];
+            zmax = fmaxf(zmax, z_r[r]);
+        }
     float sum = 0.f;
-    for (int r = 0; r < n_r; ++r) {
-        const int64_t s = min(max(undo[(seg0 + r) * L + i], 0), L - 1);
-        sum += expf(lse_rounds[(seg0 + r) * L + s] - zmax);
-    }
+#pragma unroll
+    for (int r = 0; r < kMaxRounds; ++r)
+        if (r < n_r) sum += expf(z_r[r] - zmax);
     const float z = zmax + logf(sum);
+    f32x4 o[kMaxRounds];
+#pragma unroll
+    for (int r = 0; r < kMaxRounds; ++r)
+        if (r < n_r) o[r] = *reinterpret_cast<const f32x4*>(o_rounds + base[r] * kHeadDim + part * 4);
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int r = 0; r < n_r; ++r) {
-        const int64_t s = min(max(undo[(seg0 + r) * L + i], 0), L - 1);
-        const float w = expf(lse_rounds[(seg0 + r) * L + s] - z);
-        const f32x4 o = *reinterpret_cast<const f32x4*>(o_rounds + ((seg0 + r) * L + s) * kHeadDim + part * 4);
-        acc[0] = fmaf(w, o[0], acc[0]);
-        acc[1] = fmaf(w, o[1], acc[1]);
-        acc[2] = fmaf(w, o[2], acc[2]);
-        acc[3] = fmaf(w, o[3], acc[3]);
-    }
+#pragma unroll
+    for (int r = 0; r < kMaxRounds; ++r)
+        if (r < n_r) {
+            const float w = expf(z_r[r] - z);
+            acc[0] = fmaf(w, o[r][0], acc[0]);
+            acc[1] = fmaf(w, o[r][1], acc[1]);
+            acc[2] = fmaf(w, o[r][2], acc[2]);
+            acc[3] = fmaf(w, o[r][3], acc[3]);
+        }
     if constexpr (F32_OUT) {
         *reinterpret_cast<f32x4*>(static_cast<float*>(out) + row * kHeadDim + part * 4) = acc;
     } else {

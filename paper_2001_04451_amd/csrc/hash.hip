@@ -13,9 +13,10 @@
 //    argmax index rides in the low mantissa bits of the key, so one
 //    bit-insert, one max and one median-of-three per projection suffice.
 //  * If the gap between the best and second-best key cannot rule out an
-//    exchange under the error bound, the row-round is recomputed exactly in
-//    fp64 (same product and summation order as a plain loop), so the ids
-//    always equal the exact argmax.
+//    exchange under the error bound, the row-round is appended to a list and
+//    recomputed afterwards in fp64 by a second kernel (same products and
+//    summation order as a plain loop), so the ids always equal the exact
+//    argmax.
 #include "common.h"
 #include "launch.h"
 
@@ -25,41 +26,51 @@ namespace {
 constexpr int kHashWaves = 4;
 constexpr int kHashRowsPerBlock = 64 * kHashWaves;  // each wave: two 32-row blocks
 constexpr int kColStride = 72;                      // bf16 per staged R column (64 + pad)
+constexpr int kTilesPerStage = 2;                   // 64 R columns per LDS stage
 constexpr int kMaxColsPerLane = 16;                 // exact path: n_b/2 <= 1024
 
-// R [n_r][64][half] fp32 -> bf16 planes hi/mid and an fp32 copy, all
-// [n_r][half_pad][64] (one R column contiguous), zero-padded to half_pad
-// columns, plus the largest column 2-norm of each round.
-__global__ __launch_bounds__(256) void prep_r_kernel(const float* __restrict__ R, int half,
-                                                     int half_pad, uint16_t* __restrict__ r_hi,
-                                                     uint16_t* __restrict__ r_mid,
-                                                     float* __restrict__ r_t,
-                                                     float* __restrict__ col_norm_max) {
-    const int r = blockIdx.x;
+// One R column per block of 64 lanes (lane = t): bf16 planes hi/mid and an
+// fp32 copy, all [n_r][half_pad][64] (column contiguous, zero padded), and
+// the column's 2-norm.
+__global__ __launch_bounds__(64) void prep_r_cols_kernel(const float* __restrict__ R, int half,
+                                                         int half_pad, uint16_t* __restrict__ r_hi,
+                                                         uint16_t* __restrict__ r_mid,
+                                                         float* __restrict__ r_t,
+                                                         float* __restrict__ col_norm) {
+    const int c = blockIdx.x, r = blockIdx.y, t = threadIdx.x;
+    const float x = c < half ? R[((size_t)r * kHeadDim + t) * half + c] : 0.f;
+    const uint32_t hi = f32_to_bf16_bits(x);
+    const float res = x - bf16_bits_to_f32(hi);  // exact (Sterbenz)
+    const uint32_t mid = f32_to_bf16_bits(res);
+    const size_t o = ((size_t)r * half_pad + c) * kHeadDim + t;
+    r_hi[o] = (uint16_t)hi;
+    r_mid[o] = (uint16_t)mid;
+    r_t[o] = x;
+    float ss = x * x;
+    for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
+    if (t == 0) col_norm[(size_t)r * half_pad + c] = sqrtf(ss);
+}
+
+// Largest column norm of each round; also clears the refinement counter.
+__global__ __launch_bounds__(256) void prep_r_max_kernel(const float* __restrict__ col_norm,
+                                                         int half_pad,
+                                                         float* __restrict__ col_norm_max,
+                                                         int* __restrict__ refine_count) {
     __shared__ float red[256];
+    const int r = blockIdx.x;
     float mx = 0.f;
-    for (int c = threadIdx.x; c < half_pad; c += blockDim.x) {
-        float ss = 0.f;
-        for (int t = 0; t < kHeadDim; ++t) {
-            const float x = c < half ? R[((size_t)r * kHeadDim + t) * half + c] : 0.f;
-            const uint32_t hi = f32_to_bf16_bits(x);
-            const float res = x - bf16_bits_to_f32(hi);  // exact (Sterbenz)
-            const uint32_t mid = f32_to_bf16_bits(res);
-            const size_t o = ((size_t)r * half_pad + c) * kHeadDim + t;
-            r_hi[o] = (uint16_t)hi;
-            r_mid[o] = (uint16_t)mid;
-            r_t[o] = x;
-            ss = fmaf(x, x, ss);
-        }
-        mx = fmaxf(mx, sqrtf(ss));
-    }
+    for (int c = threadIdx.x; c < half_pad; c += blockDim.x)
+        mx = fmaxf(mx, col_norm[(size_t)r * half_pad + c]);
     red[threadIdx.x] = mx;
     __syncthreads();
     for (int s = 128; s > 0; s >>= 1) {
         if ((int)threadIdx.x < s) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + s]);
         __syncthreads();
     }
-    if (threadIdx.x == 0) col_norm_max[r] = red[0];
+    if (threadIdx.x == 0) {
+        col_norm_max[r] = red[0];
+        if (r == 0) *refine_count = 0;
+    }
 }
 
 template <bool F32>
@@ -73,9 +84,10 @@ __device__ __forceinline__ float q_value(const void* q, int64_t row, int k) {
 
 // Exact argmax of [xR; -xR] for one row-round, computed by the whole wave in
 // fp64: column c's projection is the left-to-right sum over t of the exact
-// products q_t * R_tc.  Ties go to the first index.  Returns the bucket.
+// products q_t * R_tc, read from R in its input layout [d][n_b/2] so that the
+// lanes of a wave load consecutive columns.  Ties go to the first index.
 template <bool F32>
-__device__ int exact_bucket(const void* q, int64_t row, const float* __restrict__ r_t_round,
+__device__ int exact_bucket(const void* q, int64_t row, const float* __restrict__ R_round,
                             int half) {
     const int lane = lane_id();
     const float qv = q_value<F32>(q, row, lane);
@@ -87,7 +99,7 @@ __device__ int exact_bucket(const void* q, int64_t row, const float* __restrict_
 #pragma unroll
         for (int k = 0; k < kMaxColsPerLane; ++k) {
             const int c = lane + 64 * k;
-            if (c < half) p[k] = __dadd_rn(p[k], __dmul_rn(qt, (double)r_t_round[(size_t)c * kHeadDim + t]));
+            if (c < half) p[k] = __dadd_rn(p[k], __dmul_rn(qt, (double)R_round[(size_t)t * half + c]));
         }
     }
     double bv = -__builtin_inf();
@@ -109,13 +121,78 @@ __device__ int exact_bucket(const void* q, int64_t row, const float* __restrict_
     return bi;
 }
 
+// Settles the listed row-rounds exactly; one wave per entry, grid-stride.
+template <bool F32>
+__global__ __launch_bounds__(256) void hash_refine_kernel(const void* __restrict__ q,
+                                                          const float* __restrict__ R, int half,
+                                                          int n_r, const int* __restrict__ list,
+                                                          const int* __restrict__ count,
+                                                          int32_t* __restrict__ buckets) {
+    const int n = *count;
+    const int waves = gridDim.x * (blockDim.x / 64);
+    for (int e = blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6); e < n; e += waves) {
+        const int code = list[e];
+        const int64_t row = code / n_r;
+        const int r = code % n_r;
+        const int bkt = exact_bucket<F32>(q, row, R + (size_t)r * kHeadDim * half, half);
+        if (lane_id() == 0) buckets[code] = bkt;
+    }
+}
+
+struct Tile {
+    f32x16 acc[2];
+};
+
+template <bool F32>
+__device__ __forceinline__ void tile_mfma(Tile& T, const uint16_t (*st)[kColStride],
+                                          const uint16_t (*st_mid)[kColStride], int col, int h,
+                                          const bf16x8 (&qa)[2][4], const bf16x8 (&qm)[2][4]) {
+    bf16x8 ahi[4], amid[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        ahi[s] = as_bf16x8(*reinterpret_cast<const u32x4*>(&st[col][32 * h + 8 * s]));
+        amid[s] = as_bf16x8(*reinterpret_cast<const u32x4*>(&st_mid[col][32 * h + 8 * s]));
+    }
+    T.acc[0] = f32x16{};
+    T.acc[1] = f32x16{};
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        T.acc[0] = mfma32x32x16(ahi[s], qa[0][s], T.acc[0]);
+        T.acc[1] = mfma32x32x16(ahi[s], qa[1][s], T.acc[1]);
+        T.acc[0] = mfma32x32x16(amid[s], qa[0][s], T.acc[0]);
+        T.acc[1] = mfma32x32x16(amid[s], qa[1][s], T.acc[1]);
+        if constexpr (F32) {
+            T.acc[0] = mfma32x32x16(ahi[s], qm[0][s], T.acc[0]);
+            T.acc[1] = mfma32x32x16(ahi[s], qm[1][s], T.acc[1]);
+        }
+    }
+}
+
+__device__ __forceinline__ void tile_epilogue(const Tile& T, uint32_t ubase, uint32_t idx_mask,
+                                              float (&best)[2], float (&second)[2]) {
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+        float b = best[rb], sc = second[rb];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const float key = fabsf(__uint_as_float((__float_as_uint(T.acc[rb][j]) & ~idx_mask) | (ubase | (uint32_t)j)));
+            sc = __builtin_amdgcn_fmed3f(key, b, sc);
+            b = fmaxf(key, b);
+        }
+        best[rb] = b;
+        second[rb] = sc;
+    }
+}
+
 template <bool F32>
 __global__ __launch_bounds__(256, 2) void hash_kernel(
     const void* __restrict__ q, int64_t rows, int n_r, int half, int half_pad,
     const uint16_t* __restrict__ r_hi, const uint16_t* __restrict__ r_mid,
-    const float* __restrict__ r_t, const float* __restrict__ col_norm_max, float thr_coef,
-    int idx_bits, int32_t* __restrict__ buckets) {
-    __shared__ __attribute__((aligned(16))) uint16_t stage[2][2][64][kColStride];
+    const float* __restrict__ r_t, const float* __restrict__ col_norm_max, float err_sum,
+    float err_pack, int idx_bits, int32_t* __restrict__ buckets, int* __restrict__ refine_list,
+    int* __restrict__ refine_count) {
+    // [buf][plane][column][k]
+    __shared__ __attribute__((aligned(16))) uint16_t stage[2][2][kTilesPerStage * 32][kColStride];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6, h = lane >> 5, n = lane & 31;
@@ -164,6 +241,7 @@ __global__ __launch_bounds__(256, 2) void hash_kernel(
                     ss = fmaf(b, b, ss);
                 }
                 qa[rb][s] = as_bf16x8(raw);
+                qm[rb][s] = as_bf16x8(u32x4{0, 0, 0, 0});
             }
         }
         ss += __shfl_xor(ss, 32);
@@ -172,21 +250,23 @@ __global__ __launch_bounds__(256, 2) void hash_kernel(
 
     const uint32_t idx_mask = (1u << idx_bits) - 1u;
     const int n_tiles = half_pad / 32;
-    const int n_stages = (n_tiles + 1) / 2;
+    const int cols_per_stage = kTilesPerStage * 32;
+    const int n_stages = (half_pad + cols_per_stage - 1) / cols_per_stage;
+    constexpr int kLoads = 2 * kTilesPerStage * 32 * 8 / 256;  // 16-byte pieces per thread
 
     for (int r = 0; r < n_r; ++r) {
         const uint16_t* hi_r = r_hi + (size_t)r * half_pad * kHeadDim;
         const uint16_t* mid_r = r_mid + (size_t)r * half_pad * kHeadDim;
         float best[2] = {0.f, 0.f}, second[2] = {0.f, 0.f};
 
-        // Stage loader: 2 planes x 64 columns x 128 B = 1024 x 16 B per stage.
-        u32x4 pre[4];
+        u32x4 pre[kLoads];
         auto gload = [&](int st) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < kLoads; ++i) {
                 const int idx = tid + 256 * i;
-                const int plane = idx >> 9, col = (idx >> 3) & 63, part = idx & 7;
-                const int gcol = st * 64 + col;
+                const int plane = idx / (cols_per_stage * 8);
+                const int col = (idx >> 3) % cols_per_stage, part = idx & 7;
+                const int gcol = st * cols_per_stage + col;
                 const uint16_t* base = plane ? mid_r : hi_r;
                 pre[i] = gcol < half_pad
                              ? *reinterpret_cast<const u32x4*>(base + (size_t)gcol * kHeadDim + part * 8)
@@ -195,9 +275,10 @@ __global__ __launch_bounds__(256, 2) void hash_kernel(
         };
         auto lstore = [&](int buf) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < kLoads; ++i) {
                 const int idx = tid + 256 * i;
-                const int plane = idx >> 9, col = (idx >> 3) & 63, part = idx & 7;
+                const int plane = idx / (cols_per_stage * 8);
+                const int col = (idx >> 3) % cols_per_stage, part = idx & 7;
                 *reinterpret_cast<u32x4*>(&stage[buf][plane][col][part * 8]) = pre[i];
             }
         };
@@ -208,47 +289,25 @@ __global__ __launch_bounds__(256, 2) void hash_kernel(
         for (int st = 0; st < n_stages; ++st) {
             if (st + 1 < n_stages) gload(st + 1);
             const int buf = st & 1;
-#pragma unroll
-            for (int tt = 0; tt < 2; ++tt) {
-                const int tile = st * 2 + tt;
-                if (tile < n_tiles) {
-                    bf16x8 ahi[4], amid[4];
-#pragma unroll
-                    for (int s = 0; s < 4; ++s) {
-                        ahi[s] = as_bf16x8(*reinterpret_cast<const u32x4*>(&stage[buf][0][tt * 32 + n][32 * h + 8 * s]));
-                        amid[s] = as_bf16x8(*reinterpret_cast<const u32x4*>(&stage[buf][1][tt * 32 + n][32 * h + 8 * s]));
-                    }
-                    const uint32_t ubase = (uint32_t)tile << 4;
-#pragma unroll
-                    for (int rb = 0; rb < 2; ++rb) {
-                        f32x16 acc = {};
-#pragma unroll
-                        for (int s = 0; s < 4; ++s) {
-                            acc = mfma32x32x16(ahi[s], qa[rb][s], acc);
-                            acc = mfma32x32x16(amid[s], qa[rb][s], acc);
-                            if constexpr (F32) acc = mfma32x32x16(ahi[s], qm[rb][s], acc);
-                        }
-                        float b = best[rb], sc = second[rb];
-#pragma unroll
-                        for (int j = 0; j < 16; ++j) {
-                            const float key = fabsf(__uint_as_float((__float_as_uint(acc[j]) & ~idx_mask) | (ubase | (uint32_t)j)));
-                            sc = __builtin_amdgcn_fmed3f(key, b, sc);
-                            b = fmaxf(key, b);
-                        }
-                        best[rb] = b;
-                        second[rb] = sc;
-                    }
-                }
+            const int t0 = st * kTilesPerStage;
+            const int nt = min(kTilesPerStage, n_tiles - t0);
+            // Two waves share a SIMD (from different workgroups, so their
+            // barriers do not align): one wave's epilogue runs on the vector
+            // ALUs while the other's MFMAs occupy the matrix core.
+#pragma unroll 1
+            for (int k = 0; k < nt; ++k) {
+                Tile cur;
+                tile_mfma<F32>(cur, stage[buf][0], stage[buf][1], k * 32 + n, h, qa, qm);
+                tile_epilogue(cur, (uint32_t)(t0 + k) << 4, idx_mask, best, second);
             }
             if (st + 1 < n_stages) lstore((st + 1) & 1);
             __syncthreads();
         }
 
         // Round epilogue: merge the two lane halves (different columns of the
-        // same row), decide, and settle close calls exactly.
+        // same row), decide, and queue close calls for the exact pass.
         const float cn = col_norm_max[r];
         const float* r_t_round = r_t + (size_t)r * half_pad * kHeadDim;
-        bool flag[2];
 #pragma unroll
         for (int rb = 0; rb < 2; ++rb) {
             const int64_t row = row0 + rb * 32 + n;
@@ -259,28 +318,42 @@ __global__ __launch_bounds__(256, 2) void hash_kernel(
             const int hw = mine ? h : (h ^ 1);
             const uint32_t u = __float_as_uint(b1) & idx_mask;
             const int col = (int)(u >> 4) * 32 + 8 * (int)((u & 15u) >> 2) + 4 * hw + (int)(u & 3u);
-            const float thr = thr_coef * qn[rb] * cn;
-            flag[rb] = !(b1 - s1 > thr) || col >= half;
+            // Every screened key is within eps = err_sum*|q|*max|R_c| + err_pack*key
+            // of its exact |projection|; an exchange of winners needs a gap <= 2 eps.
+            const float thr = 2.04f * (err_sum * qn[rb] * cn + err_pack * b1);
+            const bool flag = !(b1 - s1 > thr) || col >= half;
             // Sign of the winning projection.  When the row is not flagged its
             // magnitude exceeds the error bound, so fp32 gets the sign right.
             const int colc = col < half ? col : 0;
-            const float* rt = r_t_round + (size_t)colc * kHeadDim + 32 * h;
+            const f32x4* rt = reinterpret_cast<const f32x4*>(r_t_round + (size_t)colc * kHeadDim + 32 * h);
             float part = 0.f;
-            if (valid[rb]) {
-                for (int k = 0; k < 32; ++k) part = fmaf(q_value<F32>(q, row, 32 * h + k), rt[k], part);
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const f32x4 ra = rt[2 * s], rb4 = rt[2 * s + 1];
+                const float rv[8] = {ra[0], ra[1], ra[2], ra[3], rb4[0], rb4[1], rb4[2], rb4[3]};
+                const u32x4 w = __builtin_bit_cast(u32x4, qa[rb][s]);
+                const u32x4 m = __builtin_bit_cast(u32x4, qm[rb][s]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float lo = __uint_as_float(w[e] << 16) + __uint_as_float(m[e] << 16);
+                    const float hi = __uint_as_float(w[e] & 0xFFFF0000u) + __uint_as_float(m[e] & 0xFFFF0000u);
+                    part = fmaf(lo, rv[2 * e], part);
+                    part = fmaf(hi, rv[2 * e + 1], part);
+                }
             }
             const float p = part + __shfl_xor(part, 32);
-            if (valid[rb] && h == 0 && !flag[rb]) buckets[row * n_r + r] = p > 0.f ? col : half + col;
-        }
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
-            uint64_t fl = __ballot(flag[rb] && valid[rb] && h == 0);
-            while (fl) {
-                const int src = __ffsll((unsigned long long)fl) - 1;
-                fl &= fl - 1;
-                const int64_t frow = row0 + rb * 32 + src;
-                const int bkt = exact_bucket<F32>(q, frow, r_t_round, half);
-                if (lane == 0) buckets[frow * n_r + r] = bkt;
+            const bool queue = flag && valid[rb] && h == 0;
+            if (valid[rb] && h == 0 && !flag) buckets[row * n_r + r] = p > 0.f ? col : half + col;
+            // wave-aggregated append to the refinement list
+            const uint64_t qmask = __ballot(queue);
+            if (qmask) {
+                int slot0 = 0;
+                if (lane == __ffsll((unsigned long long)qmask) - 1) slot0 = atomicAdd(refine_count, __popcll(qmask));
+                slot0 = __shfl(slot0, __ffsll((unsigned long long)qmask) - 1);
+                if (queue) {
+                    const int before = __popcll(qmask & ((1ull << lane) - 1ull));
+                    refine_list[slot0 + before] = (int)(row * n_r + r);
+                }
             }
         }
     }
@@ -292,45 +365,85 @@ int ceil_log2(int x) {
     return b;
 }
 
+struct HashWs {
+    uint16_t* r_hi;
+    uint16_t* r_mid;
+    float* r_t;
+    float* col_norm;
+    float* col_norm_max;
+    int* count;
+    int* list;
+    size_t bytes;
+};
+
+HashWs carve(void* base, int64_t rows, int n_rounds, int half_pad) {
+    const size_t per = (size_t)n_rounds * half_pad * kHeadDim;
+    char* p = static_cast<char*>(base);
+    HashWs w{};
+    size_t off = 0;
+    w.r_hi = reinterpret_cast<uint16_t*>(p + off);
+    off += align256(per * 2);
+    w.r_mid = reinterpret_cast<uint16_t*>(p + off);
+    off += align256(per * 2);
+    w.r_t = reinterpret_cast<float*>(p + off);
+    off += align256(per * 4);
+    w.col_norm = reinterpret_cast<float*>(p + off);
+    off += align256((size_t)n_rounds * half_pad * 4);
+    w.col_norm_max = reinterpret_cast<float*>(p + off);
+    off += align256((size_t)n_rounds * 4);
+    w.count = reinterpret_cast<int*>(p + off);
+    off += 256;
+    w.list = reinterpret_cast<int*>(p + off);
+    off += align256((size_t)rows * n_rounds * 4);
+    w.bytes = off;
+    return w;
+}
+
 }  // namespace
 
-size_t hash_workspace_bytes(int n_rounds, int n_buckets) {
-    const size_t half_pad = (size_t)((n_buckets / 2 + 31) / 32) * 32;
-    const size_t per = (size_t)n_rounds * half_pad * kHeadDim;
-    return align256(per * 2) * 2 + align256(per * 4) + align256((size_t)n_rounds * 4);
+size_t hash_workspace_bytes(int64_t rows, int n_rounds, int n_buckets) {
+    const int half_pad = (n_buckets / 2 + 31) / 32 * 32;
+    return carve(nullptr, rows, n_rounds, half_pad).bytes;
 }
 
 hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int n_buckets,
                        const float* R, int32_t* buckets, void* workspace, hipStream_t stream) {
     const int half = n_buckets / 2;
     const int half_pad = (half + 31) / 32 * 32;
-    const size_t per = (size_t)n_rounds * half_pad * kHeadDim;
-    char* ws = static_cast<char*>(workspace);
-    uint16_t* r_hi = reinterpret_cast<uint16_t*>(ws);
-    uint16_t* r_mid = reinterpret_cast<uint16_t*>(ws + align256(per * 2));
-    float* r_t = reinterpret_cast<float*>(ws + 2 * align256(per * 2));
-    float* cnm = reinterpret_cast<float*>(ws + 2 * align256(per * 2) + align256(per * 4));
+    const HashWs w = carve(workspace, rows, n_rounds, half_pad);
 
-    prep_r_kernel<<<n_rounds, 256, 0, stream>>>(R, half, half_pad, r_hi, r_mid, r_t, cnm);
+    prep_r_cols_kernel<<<dim3(half_pad, n_rounds), 64, 0, stream>>>(R, half, half_pad, w.r_hi,
+                                                                     w.r_mid, w.r_t, w.col_norm);
+    prep_r_max_kernel<<<n_rounds, 256, 0, stream>>>(w.col_norm, half_pad, w.col_norm_max, w.count);
     if (rows == 0) return hipGetLastError();
 
     const int n_tiles = half_pad / 32;
     const int idx_bits = 4 + ceil_log2(n_tiles);
-    // Error bound of a screened projection, as a multiple of |q| * max_c |R_c|:
-    // plane residual(s), fp32 accumulation (2^-22 per addition, a 4x margin
-    // over round-to-nearest), and the index bits packed into the mantissa.
-    const double acc_terms = f32 ? 3 * kHeadDim : 2 * kHeadDim;
+    // Error bound of a screened key against the exact |projection| p_c:
+    //  * the dropped bf16 plane(s), <= 2^-16 sum_t |q_t R_tc| each;
+    //  * fp32 accumulation of the exact bf16 products, <= one ulp of the
+    //    partial sum (<= 2^-23 sum_t |q_t R_tc|) per addition;
+    //  * the index bits written over the low mantissa, < 2^(idx_bits-23) |key|.
+    // sum_t |q_t R_tc| <= |q| |R_c| (Cauchy-Schwarz) <= |q| max_c |R_c|.
+    const double adds = f32 ? 3 * kHeadDim : 2 * kHeadDim;
     const double resid = f32 ? 3.1 * 0x1p-16 : 0x1p-16;
-    const double eps = resid + acc_terms * 0x1p-22 + std::ldexp(1.0, idx_bits - 23);
-    const float thr_coef = (float)(2.0 * eps * 1.02);
+    const float err_sum = (float)((resid + adds * 0x1p-23) * 1.01);
+    const float err_pack = (float)std::ldexp(1.0, idx_bits - 23);
 
     const unsigned grid = (unsigned)((rows + kHashRowsPerBlock - 1) / kHashRowsPerBlock);
-    if (f32)
-        hash_kernel<true><<<grid, 256, 0, stream>>>(q, rows, n_rounds, half, half_pad, r_hi, r_mid,
-                                                     r_t, cnm, thr_coef, idx_bits, buckets);
-    else
-        hash_kernel<false><<<grid, 256, 0, stream>>>(q, rows, n_rounds, half, half_pad, r_hi, r_mid,
-                                                      r_t, cnm, thr_coef, idx_bits, buckets);
+    if (f32) {
+        hash_kernel<true><<<grid, 256, 0, stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi,
+                                                     w.r_mid, w.r_t, w.col_norm_max, err_sum,
+                                                     err_pack, idx_bits, buckets, w.list, w.count);
+        hash_refine_kernel<true><<<512, 256, 0, stream>>>(q, R, half, n_rounds, w.list, w.count,
+                                                          buckets);
+    } else {
+        hash_kernel<false><<<grid, 256, 0, stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi,
+                                                      w.r_mid, w.r_t, w.col_norm_max, err_sum,
+                                                      err_pack, idx_bits, buckets, w.list, w.count);
+        hash_refine_kernel<false><<<512, 256, 0, stream>>>(q, R, half, n_rounds, w.list, w.count,
+                                                           buckets);
+    }
     return hipGetLastError();
 }
 

@@ -18,7 +18,7 @@ constexpr int kHeadDimHost = 64;  // d_k the kernels are specialised for
 constexpr int kChunkHost = 64;    // chunk length m the kernels are specialised for
 
 // ---- hashing ----
-size_t hash_workspace_bytes(int n_rounds, int n_buckets);
+size_t hash_workspace_bytes(int64_t rows, int n_rounds, int n_buckets);
 hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int n_buckets,
                        const float* R, int32_t* buckets, void* workspace, hipStream_t stream);
 

@@ -71,7 +71,7 @@ const char* lsh_status_string(int status) {
 size_t lsh_workspace_bytes(const lsh_config* cfg, lsh_dtype dtype, int op) {
     if (check_config(cfg) != LSH_OK || check_dtype(dtype) != LSH_OK) return 0;
     const int64_t BH = bh_of(cfg);
-    const size_t hash = lsh::hash_workspace_bytes(cfg->n_rounds, cfg->n_buckets);
+    const size_t hash = lsh::hash_workspace_bytes(BH * cfg->L, cfg->n_rounds, cfg->n_buckets);
     const size_t sort = lsh::sort_workspace_bytes(BH, cfg->L, cfg->n_rounds, cfg->n_buckets);
     switch (op) {
         case LSH_OP_HASH: return hash;
@@ -89,7 +89,7 @@ int lsh_hash(const lsh_config* cfg, lsh_dtype dtype, const void* q, const float*
     LSH_TRY(check_config(cfg));
     LSH_TRY(check_dtype(dtype));
     if (!q || !R || !buckets || !workspace) return LSH_ERR_INVALID;
-    if (workspace_bytes < lsh::hash_workspace_bytes(cfg->n_rounds, cfg->n_buckets))
+    if (workspace_bytes < lsh::hash_workspace_bytes(bh_of(cfg) * cfg->L, cfg->n_rounds, cfg->n_buckets))
         return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
     const int64_t rows = bh_of(cfg) * cfg->L;

@@ -175,14 +175,21 @@ def lsh_hash(cfg: Config, q: torch.Tensor, R: torch.Tensor, buckets: torch.Tenso
     return buckets
 
 
-def lsh_sort_permute(cfg: Config, buckets: torch.Tensor, workspace: torch.Tensor | None = None):
+def lsh_sort_permute(cfg: Config, buckets: torch.Tensor, workspace: torch.Tensor | None = None,
+                     perm=None, undo=None, bstart=None):
     """perm, undo [B,H,n_r,L] and bucket_start [B,H,n_r,n_b+1] (lsh_sort_permute)."""
     _need(buckets, (cfg.B, cfg.H, cfg.L, cfg.n_rounds), torch.int32, "buckets")
     dev = buckets.device
-    perm = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.L), dtype=torch.int32, device=dev)
-    undo = torch.empty_like(perm)
-    bstart = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.n_buckets + 1), dtype=torch.int32,
-                         device=dev)
+    if perm is None:
+        perm = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.L), dtype=torch.int32, device=dev)
+    if undo is None:
+        undo = torch.empty_like(perm)
+    if bstart is None:
+        bstart = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.n_buckets + 1), dtype=torch.int32,
+                             device=dev)
+    _need(perm, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.int32, "perm")
+    _need(undo, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.int32, "undo")
+    _need(bstart, (cfg.B, cfg.H, cfg.n_rounds, cfg.n_buckets + 1), torch.int32, "bucket_start")
     if workspace is None:
         workspace = _workspace(cfg, torch.float32, LSH_OP_SORT, dev)
     _check("lsh_sort_permute",
