@@ -12,7 +12,8 @@
  * Pointers.  Every tensor argument is a DEVICE pointer to contiguous,
  *   row-major memory that the caller allocated and owns; the library never
  *   allocates, frees or synchronises.  Inputs are only read.  Outputs must
- *   not alias inputs or each other.
+ *   not alias inputs or each other.  q, v, R, dout, the row outputs and the
+ *   workspace must be 16-byte aligned (LSH_ERR_INVALID otherwise).
  * Layouts.  "BH" is B*H flattened, batch-major.
  *   q, v, dout        [B][H][L][d]        dtype of the call (fp32 or bf16)
  *   R                 [n_rounds][d][n_buckets/2]   fp32

@@ -1,0 +1,67 @@
+// Device helpers shared by the chunked-attention kernels (forward and
+// backward): swizzled LDS row tiles, the key-row permutation that lets an
+// S^T accumulator be reused as a matrix-core operand, and the packed bucket
+// signatures behind N_ij.
+#pragma once
+
+#include "common.h"
+
+namespace lsh {
+
+// Rows of 64 bf16 values (128 B) are staged in LDS as 8 pieces of 16 B with
+// piece p of row r stored at slot p ^ (r & 7) ^ (((r >> 3) & 1) << 2).  Rows
+// read together by the operand loads (rows kappa(0..7), rows r..r+7, and the
+// two lane halves 8 rows apart) then fall into different banks.
+__device__ __forceinline__ int swz(int row, int piece) {
+    return piece ^ (row & 7) ^ (((row >> 3) & 1) << 2);
+}
+
+__device__ __forceinline__ uint32_t row_piece_offset(int row, int piece) {
+    return (uint32_t)row * 128u + (uint32_t)swz(row, piece) * 16u;
+}
+
+__device__ __forceinline__ u32x4 lds_piece(const char* base, int row, int piece) {
+    return *reinterpret_cast<const u32x4*>(base + row_piece_offset(row, piece));
+}
+
+__device__ __forceinline__ void lds_store_piece(char* base, int row, int piece, u32x4 v) {
+    *reinterpret_cast<u32x4*>(base + row_piece_offset(row, piece)) = v;
+}
+
+__device__ __forceinline__ uint32_t lds_elem(const char* base, int row, int d) {
+    return *reinterpret_cast<const uint16_t*>(base + row_piece_offset(row, d >> 3) + (d & 7) * 2);
+}
+
+// The A operand of a 32-row tile (lane l, row l%32) holds tile row kappa(l%32)
+// so that accumulator register j of lane l corresponds to tile row
+// 16*(j/8) + 8*(l/32) + (j%8): registers 8u..8u+7 are then exactly the
+// k-slots of the 16-row block u in the B-operand layout of the next product.
+__device__ __forceinline__ int kappa(int m) {
+    return 16 * (m >> 4) + 8 * ((m >> 2) & 1) + 4 * ((m >> 3) & 1) + (m & 3);
+}
+
+// Operand with rows along the lane (row r0 + lane%32, k = 32h + 8s + e).
+__device__ __forceinline__ bf16x8 row_operand(const char* base, int row, int h, int s) {
+    return as_bf16x8(lds_piece(base, row, 4 * h + s));
+}
+
+// Transposed operand: lane holds column d (fixed) of the 8 rows r0 .. r0+7.
+__device__ __forceinline__ bf16x8 col_operand(const char* base, int r0, int d) {
+    u32x4 v;
+#pragma unroll
+    for (int e2 = 0; e2 < 4; ++e2)
+        v[e2] = lds_elem(base, r0 + 2 * e2, d) | (lds_elem(base, r0 + 2 * e2 + 1, d) << 16);
+    return as_bf16x8(v);
+}
+
+// Bucket signatures: two rounds' ids (10 bits each) per word at bits 0 and 11,
+// guard bits 10 and 21.  For a = sig_i, b = sig_j the number of rounds in which
+// the ids differ is popcount(((a ^ b) + kSigAdd) & kSigGuard) summed over words.
+constexpr uint32_t kSigAdd = 0x3FFu | (0x3FFu << 11);
+constexpr uint32_t kSigGuard = (1u << 10) | (1u << 21);
+
+__device__ __forceinline__ int sig_mismatches(uint32_t a, uint32_t b) {
+    return __popc(((a ^ b) + kSigAdd) & kSigGuard);
+}
+
+}  // namespace lsh

@@ -34,10 +34,6 @@ constexpr int kVStride = 68;
 constexpr uint32_t kSigAdd = 0x3FFu | (0x3FFu << 11);
 constexpr uint32_t kSigGuard = (1u << 10) | (1u << 21);
 
-__device__ __forceinline__ int key_of_reg(int j, int h) {
-    return 16 * (j >> 3) + 8 * h + (j & 7);
-}
-
 // A-operand row m of a key tile holds key kappa(m), which puts key
 // 16*(j/8) + 8*(l/32) + (j%8) in accumulator register j of lane l.
 __device__ __forceinline__ int kappa(int m) {
@@ -153,30 +149,46 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
         }
     }
 
-    // pass 1: masked logits (log2 units) and the row maximum
+    // pass 1: masked logits (log2 units) and the row maximum.  The lane's 16
+    // keys of a tile are two runs of 8 consecutive rows, so their per-key
+    // factors and signatures come in as 16-byte LDS reads.
     float mrow = -__builtin_inff();
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
         if (!act[kt]) continue;
         const int tb = (c - 1) * kChunk + kt * 32;
-        const int rk0 = kb + kt * 32;
+        const int lo_t = lo - tb, hi_t = hi - tb, self_t = s_q - tb;  // bounds in tile coordinates
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            const int kk = key_of_reg(j, h);
-            const int t = tb + kk;
-            bool valid = t >= lo && t <= hi;
-            if constexpr (!CAUSAL) valid = valid && t != s_q;
-            float nlog2 = 0.f;
-            if constexpr (NW > 0) {
-                int nm = 0;
+        for (int run = 0; run < 2; ++run) {
+            const int kbase = kb + kt * 32 + 16 * run + 8 * h;  // LDS row of the run's first key
+            const f32x4 c0 = *reinterpret_cast<const f32x4*>(&cf[kbase]);
+            const f32x4 c1 = *reinterpret_cast<const f32x4*>(&cf[kbase + 4]);
 #pragma unroll
-                for (int w = 0; w < NW; ++w)
-                    nm += __popc(((qsig[w] ^ sig[rk0 + kk][w]) + kSigAdd) & kSigGuard);
-                nlog2 = __log2f((float)(n_r - nm));
+            for (int e = 0; e < 8; ++e) {
+                const int j = 8 * run + e;
+                const int kk = 16 * run + 8 * h + e;  // key index inside the tile
+                bool valid = kk >= lo_t && kk <= hi_t;
+                if constexpr (!CAUSAL) valid = valid && kk != self_t;
+                float nlog2 = 0.f;
+                if constexpr (NW > 0) {
+                    const u32x4 k0 = *reinterpret_cast<const u32x4*>(&sig[kbase + e][0]);
+                    int nm = 0;
+#pragma unroll
+                    for (int w = 0; w < (NW < 4 ? NW : 4); ++w)
+                        nm += __popc(((qsig[w] ^ k0[w]) + kSigAdd) & kSigGuard);
+                    if constexpr (NW > 4) {
+                        const u32x4 k1 = *reinterpret_cast<const u32x4*>(&sig[kbase + e][4]);
+#pragma unroll
+                        for (int w = 4; w < NW; ++w)
+                            nm += __popc(((qsig[w] ^ k1[w - 4]) + kSigAdd) & kSigGuard);
+                    }
+                    nlog2 = __log2f((float)(n_r - nm));
+                }
+                const float cfk = e < 4 ? c0[e] : c1[e - 4];
+                const float x = fmaf(acc[kt][j], cfk, -nlog2);
+                acc[kt][j] = valid ? x : -__builtin_inff();
+                mrow = fmaxf(mrow, acc[kt][j]);
             }
-            const float x = fmaf(acc[kt][j], cf[rk0 + kk], -nlog2);
-            acc[kt][j] = valid ? x : -__builtin_inff();
-            mrow = fmaxf(mrow, acc[kt][j]);
         }
     }
     mrow = fmaxf(mrow, __shfl_xor(mrow, 32));

@@ -10,8 +10,9 @@
 //    exact one by a bounded amount (residual, fp32 accumulation, and the
 //    index bits packed into the low mantissa).
 //  * Each lane keeps the two largest |projection| keys it has seen; the
-//    argmax index rides in the low mantissa bits of the key, so one
-//    bit-insert, one max and one median-of-three per projection suffice.
+//    argmax index inside a 32-column tile rides in the low mantissa bits of
+//    the key, so one and-or, one max and one median-of-three per projection
+//    suffice, and the tile of the best key is noted once per tile.
 //  * If the gap between the best and second-best key cannot rule out an
 //    exchange under the error bound, the row-round is appended to a list and
 //    recomputed afterwards in fp64 by a second kernel (same products and
@@ -24,10 +25,12 @@ namespace lsh {
 namespace {
 
 constexpr int kHashWaves = 4;
-constexpr int kHashRowsPerBlock = 64 * kHashWaves;  // each wave: two 32-row blocks
+constexpr int kRB = 2;  // 32-row blocks per wave: each staged R tile feeds 2 * 8 MFMAs
+constexpr uint32_t kKeyMask = 0x7FFFFFF0u;  // |value| with 4 index bits
+constexpr int kHashRowsPerBlock = 32 * kRB * kHashWaves;
 constexpr int kColStride = 72;                      // bf16 per staged R column (64 + pad)
 constexpr int kTilesPerStage = 2;                   // 64 R columns per LDS stage
-constexpr int kMaxColsPerLane = 16;                 // exact path: n_b/2 <= 1024
+constexpr int kMaxColsPerLane = 8;                  // exact path: n_b/2 <= 512
 
 // One R column per block of 64 lanes (lane = t): bf16 planes hi/mid and an
 // fp32 copy, all [n_r][half_pad][64] (column contiguous, zero padded), and
@@ -51,7 +54,7 @@ __global__ __launch_bounds__(64) void prep_r_cols_kernel(const float* __restrict
     if (t == 0) col_norm[(size_t)r * half_pad + c] = sqrtf(ss);
 }
 
-// Largest column norm of each round; also clears the refinement counter.
+// Largest column norm of each round; also clears the round's refinement counter.
 __global__ __launch_bounds__(256) void prep_r_max_kernel(const float* __restrict__ col_norm,
                                                          int half_pad,
                                                          float* __restrict__ col_norm_max,
@@ -69,7 +72,7 @@ __global__ __launch_bounds__(256) void prep_r_max_kernel(const float* __restrict
     }
     if (threadIdx.x == 0) {
         col_norm_max[r] = red[0];
-        if (r == 0) *refine_count = 0;
+        refine_count[r] = 0;
     }
 }
 
@@ -82,103 +85,130 @@ __device__ __forceinline__ float q_value(const void* q, int64_t row, int k) {
     }
 }
 
-// Exact argmax of [xR; -xR] for one row-round, computed by the whole wave in
-// fp64: column c's projection is the left-to-right sum over t of the exact
-// products q_t * R_tc, read from R in its input layout [d][n_b/2] so that the
-// lanes of a wave load consecutive columns.  Ties go to the first index.
+// Exact argmax of [xR; -xR] for the listed row-rounds of one round.  The
+// round's R (fp32, [d][n_b/2], at most 128 KB) is staged in LDS once per
+// block; each wave settles one row-round at a time.  Column c's projection
+// is the left-to-right sum over t of the exact products q_t * R_tc in fp64
+// (the order of a plain loop), and ties go to the first index of [xR; -xR].
+constexpr int kRefineThreads = 512;
+
 template <bool F32>
-__device__ int exact_bucket(const void* q, int64_t row, const float* __restrict__ R_round,
-                            int half) {
-    const int lane = lane_id();
-    const float qv = q_value<F32>(q, row, lane);
-    double p[kMaxColsPerLane];
+__global__ __launch_bounds__(kRefineThreads) void hash_refine_kernel(const void* __restrict__ q,
+                                                          const float* __restrict__ R, int half,
+                                                          int n_r, int64_t list_stride,
+                                                          const int* __restrict__ lists,
+                                                          const int* __restrict__ counts,
+                                                          int32_t* __restrict__ buckets) {
+    extern __shared__ float Rs[];  // [64][half]
+    const int r = blockIdx.y;
+    const int n = counts[r];
+    constexpr int kWavesPerBlock = kRefineThreads / 64;
+    if (n == 0 || (int)blockIdx.x * kWavesPerBlock >= n) return;  // uniform per block
+    // stage the round's R: 16-byte pieces, eight loads in flight per thread
+    const f32x4* Rr = reinterpret_cast<const f32x4*>(R + (size_t)r * kHeadDim * half);
+    f32x4* Rs4 = reinterpret_cast<f32x4*>(Rs);
+    const int n4 = kHeadDim * half / 4;
+    for (int i0 = threadIdx.x; i0 < n4; i0 += 8 * blockDim.x) {
+        f32x4 tmp[8];
 #pragma unroll
-    for (int k = 0; k < kMaxColsPerLane; ++k) p[k] = 0.0;
-    for (int t = 0; t < kHeadDim; ++t) {
-        const double qt = (double)__shfl(qv, t);
+        for (int u = 0; u < 8; ++u) {
+            const int i = i0 + u * blockDim.x;
+            if (i < n4) tmp[u] = Rr[i];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int i = i0 + u * blockDim.x;
+            if (i < n4) Rs4[i] = tmp[u];
+        }
+    }
+    __syncthreads();
+    const int* list = lists + list_stride * r;
+    const int lane = lane_id();
+    const int waves = gridDim.x * kWavesPerBlock;
+    for (int e = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6); e < n; e += waves) {
+        const int64_t row = list[e];
+        const float qv = q_value<F32>(q, row, lane);
+        double p[kMaxColsPerLane];
+#pragma unroll
+        for (int k = 0; k < kMaxColsPerLane; ++k) p[k] = 0.0;
+        // q_t reaches every lane through a scalar register (readlane), and the
+        // fully unrolled sum lets the LDS reads run ahead of the fp64 adds.
+#pragma unroll
+        for (int t = 0; t < kHeadDim; ++t) {
+            const double qt = (double)__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, qv), t));
+#pragma unroll
+            for (int k = 0; k < kMaxColsPerLane; ++k) {
+                const int c = lane + 64 * k;
+                if (c < half) p[k] = __dadd_rn(p[k], __dmul_rn(qt, (double)Rs[t * half + c]));
+            }
+        }
+        double bv = -__builtin_inf();
+        int bi = 0x7FFFFFFF;
 #pragma unroll
         for (int k = 0; k < kMaxColsPerLane; ++k) {
             const int c = lane + 64 * k;
-            if (c < half) p[k] = __dadd_rn(p[k], __dmul_rn(qt, (double)R_round[(size_t)t * half + c]));
+            if (c < half) {
+                if (p[k] > bv || (p[k] == bv && c < bi)) { bv = p[k]; bi = c; }
+                const double m = -p[k];
+                if (m > bv || (m == bv && half + c < bi)) { bv = m; bi = half + c; }
+            }
         }
-    }
-    double bv = -__builtin_inf();
-    int bi = 0x7FFFFFFF;
-#pragma unroll
-    for (int k = 0; k < kMaxColsPerLane; ++k) {
-        const int c = lane + 64 * k;
-        if (c < half) {
-            if (p[k] > bv || (p[k] == bv && c < bi)) { bv = p[k]; bi = c; }
-            const double m = -p[k];
-            if (m > bv || (m == bv && half + c < bi)) { bv = m; bi = half + c; }
+        for (int o = 32; o >= 1; o >>= 1) {
+            const double ov = __shfl_xor(bv, o);
+            const int oi = __shfl_xor(bi, o);
+            if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
         }
-    }
-    for (int o = 32; o >= 1; o >>= 1) {
-        const double ov = __shfl_xor(bv, o);
-        const int oi = __shfl_xor(bi, o);
-        if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
-    }
-    return bi;
-}
-
-// Settles the listed row-rounds exactly; one wave per entry, grid-stride.
-template <bool F32>
-__global__ __launch_bounds__(256) void hash_refine_kernel(const void* __restrict__ q,
-                                                          const float* __restrict__ R, int half,
-                                                          int n_r, const int* __restrict__ list,
-                                                          const int* __restrict__ count,
-                                                          int32_t* __restrict__ buckets) {
-    const int n = *count;
-    const int waves = gridDim.x * (blockDim.x / 64);
-    for (int e = blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6); e < n; e += waves) {
-        const int code = list[e];
-        const int64_t row = code / n_r;
-        const int r = code % n_r;
-        const int bkt = exact_bucket<F32>(q, row, R + (size_t)r * kHeadDim * half, half);
-        if (lane_id() == 0) buckets[code] = bkt;
+        if (lane == 0) buckets[row * n_r + r] = bi;
     }
 }
 
 struct Tile {
-    f32x16 acc[2];
+    f32x16 acc[kRB];
 };
 
 template <bool F32>
 __device__ __forceinline__ void tile_mfma(Tile& T, const uint16_t (*st)[kColStride],
                                           const uint16_t (*st_mid)[kColStride], int col, int h,
-                                          const bf16x8 (&qa)[2][4], const bf16x8 (&qm)[2][4]) {
+                                          const bf16x8 (&qa)[kRB][4], const bf16x8 (&qm)[kRB][4]) {
     bf16x8 ahi[4], amid[4];
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
         ahi[s] = as_bf16x8(*reinterpret_cast<const u32x4*>(&st[col][32 * h + 8 * s]));
         amid[s] = as_bf16x8(*reinterpret_cast<const u32x4*>(&st_mid[col][32 * h + 8 * s]));
     }
-    T.acc[0] = f32x16{};
-    T.acc[1] = f32x16{};
+#pragma unroll
+    for (int rb = 0; rb < kRB; ++rb) T.acc[rb] = f32x16{};
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-        T.acc[0] = mfma32x32x16(ahi[s], qa[0][s], T.acc[0]);
-        T.acc[1] = mfma32x32x16(ahi[s], qa[1][s], T.acc[1]);
-        T.acc[0] = mfma32x32x16(amid[s], qa[0][s], T.acc[0]);
-        T.acc[1] = mfma32x32x16(amid[s], qa[1][s], T.acc[1]);
+#pragma unroll
+        for (int rb = 0; rb < kRB; ++rb) T.acc[rb] = mfma32x32x16(ahi[s], qa[rb][s], T.acc[rb]);
+#pragma unroll
+        for (int rb = 0; rb < kRB; ++rb) T.acc[rb] = mfma32x32x16(amid[s], qa[rb][s], T.acc[rb]);
         if constexpr (F32) {
-            T.acc[0] = mfma32x32x16(ahi[s], qm[0][s], T.acc[0]);
-            T.acc[1] = mfma32x32x16(ahi[s], qm[1][s], T.acc[1]);
+#pragma unroll
+            for (int rb = 0; rb < kRB; ++rb) T.acc[rb] = mfma32x32x16(ahi[s], qm[rb][s], T.acc[rb]);
         }
     }
 }
 
-__device__ __forceinline__ void tile_epilogue(const Tile& T, uint32_t ubase, uint32_t idx_mask,
-                                              float (&best)[2], float (&second)[2]) {
+// Keys are |projection| bit patterns (non-negative floats order like their
+// bits as unsigned integers) with the low 4 mantissa bits replaced by the
+// register index j inside the tile: one and-or, one unsigned median-of-three
+// and one unsigned max per projection.  The tile holding the best key is
+// recorded when the running best changes during the tile.
+__device__ __forceinline__ void tile_epilogue(const Tile& T, int tile, uint32_t (&best)[kRB],
+                                              uint32_t (&second)[kRB], int (&best_tile)[kRB]) {
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-        float b = best[rb], sc = second[rb];
+    for (int rb = 0; rb < kRB; ++rb) {
+        uint32_t b = best[rb], sc = second[rb];
+        const uint32_t b0 = b;
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-            const float key = fabsf(__uint_as_float((__float_as_uint(T.acc[rb][j]) & ~idx_mask) | (ubase | (uint32_t)j)));
-            sc = __builtin_amdgcn_fmed3f(key, b, sc);
-            b = fmaxf(key, b);
+            const uint32_t key = (__float_as_uint(T.acc[rb][j]) & kKeyMask) | (uint32_t)j;
+            sc = max(min(key, b), min(max(key, b), sc));  // median of three
+            b = max(key, b);
         }
+        best_tile[rb] = b != b0 ? tile : best_tile[rb];
         best[rb] = b;
         second[rb] = sc;
     }
@@ -189,31 +219,30 @@ __global__ __launch_bounds__(256, 2) void hash_kernel(
     const void* __restrict__ q, int64_t rows, int n_r, int half, int half_pad,
     const uint16_t* __restrict__ r_hi, const uint16_t* __restrict__ r_mid,
     const float* __restrict__ r_t, const float* __restrict__ col_norm_max, float err_sum,
-    float err_pack, int idx_bits, int32_t* __restrict__ buckets, int* __restrict__ refine_list,
-    int* __restrict__ refine_count) {
+    float err_pack, int32_t* __restrict__ buckets, int* __restrict__ refine_lists,
+    int* __restrict__ refine_counts) {
     // [buf][plane][column][k]
     __shared__ __attribute__((aligned(16))) uint16_t stage[2][2][kTilesPerStage * 32][kColStride];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6, h = lane >> 5, n = lane & 31;
-    const int64_t row0 = (int64_t)blockIdx.x * kHashRowsPerBlock + wave * 64;
+    const int64_t row0 = (int64_t)blockIdx.x * kHashRowsPerBlock + wave * (32 * kRB);
 
     // Queries as the B operand: lane holds row (n) and k = 32h + 8s + e, s = 0..3.
-    bf16x8 qa[2][4];
-    bf16x8 qm[2][4];  // fp32 input: second bf16 plane of q
-    float qn[2];
-    bool valid[2];
+    bf16x8 qa[kRB][4];
+    bf16x8 qm[kRB][4];  // fp32 input: second bf16 plane of q
+    float qn[kRB];
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
+    for (int rb = 0; rb < kRB; ++rb) {
         const int64_t row = row0 + rb * 32 + n;
-        valid[rb] = row < rows;
+        const bool valid = row < rows;
         float ss = 0.f;
         if constexpr (F32) {
             const float* src = static_cast<const float*>(q) + row * kHeadDim + 32 * h;
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
-                f32x4 x0 = valid[rb] ? *reinterpret_cast<const f32x4*>(src + 8 * s) : f32x4{0, 0, 0, 0};
-                f32x4 x1 = valid[rb] ? *reinterpret_cast<const f32x4*>(src + 8 * s + 4) : f32x4{0, 0, 0, 0};
+                f32x4 x0 = valid ? *reinterpret_cast<const f32x4*>(src + 8 * s) : f32x4{0, 0, 0, 0};
+                f32x4 x1 = valid ? *reinterpret_cast<const f32x4*>(src + 8 * s + 4) : f32x4{0, 0, 0, 0};
                 float xs[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
                 u32x4 hi, mid;
 #pragma unroll
@@ -233,7 +262,7 @@ __global__ __launch_bounds__(256, 2) void hash_kernel(
             const uint16_t* src = static_cast<const uint16_t*>(q) + row * kHeadDim + 32 * h;
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
-                const u32x4 raw = valid[rb] ? *reinterpret_cast<const u32x4*>(src + 8 * s) : u32x4{0, 0, 0, 0};
+                const u32x4 raw = valid ? *reinterpret_cast<const u32x4*>(src + 8 * s) : u32x4{0, 0, 0, 0};
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const float a = __uint_as_float(raw[e] << 16), b = __uint_as_float(raw[e] & 0xFFFF0000u);
@@ -248,7 +277,6 @@ __global__ __launch_bounds__(256, 2) void hash_kernel(
         qn[rb] = sqrtf(ss);
     }
 
-    const uint32_t idx_mask = (1u << idx_bits) - 1u;
     const int n_tiles = half_pad / 32;
     const int cols_per_stage = kTilesPerStage * 32;
     const int n_stages = (half_pad + cols_per_stage - 1) / cols_per_stage;
@@ -257,7 +285,13 @@ __global__ __launch_bounds__(256, 2) void hash_kernel(
     for (int r = 0; r < n_r; ++r) {
         const uint16_t* hi_r = r_hi + (size_t)r * half_pad * kHeadDim;
         const uint16_t* mid_r = r_mid + (size_t)r * half_pad * kHeadDim;
-        float best[2] = {0.f, 0.f}, second[2] = {0.f, 0.f};
+        uint32_t best[kRB], second[kRB];
+        int best_tile[kRB];
+#pragma unroll
+        for (int rb = 0; rb < kRB; ++rb) {
+            best[rb] = second[rb] = 0u;
+            best_tile[rb] = 0;
+        }
 
         u32x4 pre[kLoads];
         auto gload = [&](int st) {
@@ -291,15 +325,15 @@ __global__ __launch_bounds__(256, 2) void hash_kernel(
             const int buf = st & 1;
             const int t0 = st * kTilesPerStage;
             const int nt = min(kTilesPerStage, n_tiles - t0);
-            // Two waves share a SIMD (from different workgroups, so their
-            // barriers do not align): one wave's epilogue runs on the vector
-            // ALUs while the other's MFMAs occupy the matrix core.
-#pragma unroll 1
-            for (int k = 0; k < nt; ++k) {
-                Tile cur;
-                tile_mfma<F32>(cur, stage[buf][0], stage[buf][1], k * 32 + n, h, qa, qm);
-                tile_epilogue(cur, (uint32_t)(t0 + k) << 4, idx_mask, best, second);
-            }
+            // The second tile's MFMAs are issued before the first tile's
+            // epilogue, so the matrix core and the vector ALUs overlap inside
+            // the wave; the two waves sharing a SIMD overlap the rest.
+            static_assert(kTilesPerStage == 2, "pipeline written for two tiles per stage");
+            Tile ta, tb;
+            tile_mfma<F32>(ta, stage[buf][0], stage[buf][1], n, h, qa, qm);
+            if (nt > 1) tile_mfma<F32>(tb, stage[buf][0], stage[buf][1], 32 + n, h, qa, qm);
+            tile_epilogue(ta, t0, best, second, best_tile);
+            if (nt > 1) tile_epilogue(tb, t0 + 1, best, second, best_tile);
             if (st + 1 < n_stages) lstore((st + 1) & 1);
             __syncthreads();
         }
@@ -308,16 +342,21 @@ __global__ __launch_bounds__(256, 2) void hash_kernel(
         // same row), decide, and queue close calls for the exact pass.
         const float cn = col_norm_max[r];
         const float* r_t_round = r_t + (size_t)r * half_pad * kHeadDim;
+        int* list = refine_lists + rows * r;
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
+        for (int rb = 0; rb < kRB; ++rb) {
             const int64_t row = row0 + rb * 32 + n;
-            const float bp = __shfl_xor(best[rb], 32), sp = __shfl_xor(second[rb], 32);
+            const bool valid = row < rows;
+            const uint32_t bp = __shfl_xor(best[rb], 32), sp = __shfl_xor(second[rb], 32);
+            const int tp = __shfl_xor(best_tile[rb], 32);
             const bool mine = best[rb] > bp || (best[rb] == bp && h == 0);
-            const float b1 = mine ? best[rb] : bp;
-            const float s1 = fmaxf(fminf(best[rb], bp), fmaxf(second[rb], sp));
+            const uint32_t bk = mine ? best[rb] : bp;
+            const float b1 = __uint_as_float(bk);
+            const float s1 = __uint_as_float(max(min(best[rb], bp), max(second[rb], sp)));
             const int hw = mine ? h : (h ^ 1);
-            const uint32_t u = __float_as_uint(b1) & idx_mask;
-            const int col = (int)(u >> 4) * 32 + 8 * (int)((u & 15u) >> 2) + 4 * hw + (int)(u & 3u);
+            const int tw = mine ? best_tile[rb] : tp;
+            const uint32_t j = bk & 15u;
+            const int col = tw * 32 + 8 * (int)(j >> 2) + 4 * hw + (int)(j & 3u);
             // Every screened key is within eps = err_sum*|q|*max|R_c| + err_pack*key
             // of its exact |projection|; an exchange of winners needs a gap <= 2 eps.
             const float thr = 2.04f * (err_sum * qn[rb] * cn + err_pack * b1);
@@ -342,27 +381,19 @@ __global__ __launch_bounds__(256, 2) void hash_kernel(
                 }
             }
             const float p = part + __shfl_xor(part, 32);
-            const bool queue = flag && valid[rb] && h == 0;
-            if (valid[rb] && h == 0 && !flag) buckets[row * n_r + r] = p > 0.f ? col : half + col;
-            // wave-aggregated append to the refinement list
+            const bool queue = flag && valid && h == 0;
+            if (valid && h == 0 && !flag) buckets[row * n_r + r] = p > 0.f ? col : half + col;
+            // wave-aggregated append to this round's refinement list
             const uint64_t qmask = __ballot(queue);
             if (qmask) {
+                const int leader = __ffsll((unsigned long long)qmask) - 1;
                 int slot0 = 0;
-                if (lane == __ffsll((unsigned long long)qmask) - 1) slot0 = atomicAdd(refine_count, __popcll(qmask));
-                slot0 = __shfl(slot0, __ffsll((unsigned long long)qmask) - 1);
-                if (queue) {
-                    const int before = __popcll(qmask & ((1ull << lane) - 1ull));
-                    refine_list[slot0 + before] = (int)(row * n_r + r);
-                }
+                if (lane == leader) slot0 = atomicAdd(&refine_counts[r], __popcll(qmask));
+                slot0 = __shfl(slot0, leader);
+                if (queue) list[slot0 + __popcll(qmask & ((1ull << lane) - 1ull))] = (int)row;
             }
         }
     }
-}
-
-int ceil_log2(int x) {
-    int b = 0;
-    while ((1 << b) < x) ++b;
-    return b;
 }
 
 struct HashWs {
@@ -392,7 +423,7 @@ HashWs carve(void* base, int64_t rows, int n_rounds, int half_pad) {
     w.col_norm_max = reinterpret_cast<float*>(p + off);
     off += align256((size_t)n_rounds * 4);
     w.count = reinterpret_cast<int*>(p + off);
-    off += 256;
+    off += align256((size_t)n_rounds * 4);
     w.list = reinterpret_cast<int*>(p + off);
     off += align256((size_t)rows * n_rounds * 4);
     w.bytes = off;
@@ -417,32 +448,39 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
     prep_r_max_kernel<<<n_rounds, 256, 0, stream>>>(w.col_norm, half_pad, w.col_norm_max, w.count);
     if (rows == 0) return hipGetLastError();
 
-    const int n_tiles = half_pad / 32;
-    const int idx_bits = 4 + ceil_log2(n_tiles);
     // Error bound of a screened key against the exact |projection| p_c:
     //  * the dropped bf16 plane(s), <= 2^-16 sum_t |q_t R_tc| each;
     //  * fp32 accumulation of the exact bf16 products, <= one ulp of the
     //    partial sum (<= 2^-23 sum_t |q_t R_tc|) per addition;
-    //  * the index bits written over the low mantissa, < 2^(idx_bits-23) |key|.
+    //  * the 4 index bits written over the low mantissa, < 2^-19 |key|.
     // sum_t |q_t R_tc| <= |q| |R_c| (Cauchy-Schwarz) <= |q| max_c |R_c|.
     const double adds = f32 ? 3 * kHeadDim : 2 * kHeadDim;
     const double resid = f32 ? 3.1 * 0x1p-16 : 0x1p-16;
     const float err_sum = (float)((resid + adds * 0x1p-23) * 1.01);
-    const float err_pack = (float)std::ldexp(1.0, idx_bits - 23);
+    const float err_pack = (float)0x1p-19;
 
     const unsigned grid = (unsigned)((rows + kHashRowsPerBlock - 1) / kHashRowsPerBlock);
+    const size_t refine_lds = (size_t)kHeadDim * half * sizeof(float);
+    // Refinement blocks per round: one 128 KB-LDS block per CU over all rounds
+    // (a typical list holds well under 1% of the rows; longer ones are strided).
+    const unsigned refine_blocks =
+        (unsigned)std::max<int64_t>(1, std::min<int64_t>((256 + n_rounds - 1) / n_rounds, rows / 1024));
     if (f32) {
         hash_kernel<true><<<grid, 256, 0, stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi,
                                                      w.r_mid, w.r_t, w.col_norm_max, err_sum,
-                                                     err_pack, idx_bits, buckets, w.list, w.count);
-        hash_refine_kernel<true><<<512, 256, 0, stream>>>(q, R, half, n_rounds, w.list, w.count,
-                                                          buckets);
+                                                     err_pack, buckets, w.list, w.count);
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&hash_refine_kernel<true>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)refine_lds);
+        hash_refine_kernel<true><<<dim3(refine_blocks, n_rounds), kRefineThreads, refine_lds, stream>>>(
+            q, R, half, n_rounds, rows, w.list, w.count, buckets);
     } else {
         hash_kernel<false><<<grid, 256, 0, stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi,
                                                       w.r_mid, w.r_t, w.col_norm_max, err_sum,
-                                                      err_pack, idx_bits, buckets, w.list, w.count);
-        hash_refine_kernel<false><<<512, 256, 0, stream>>>(q, R, half, n_rounds, w.list, w.count,
-                                                           buckets);
+                                                      err_pack, buckets, w.list, w.count);
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&hash_refine_kernel<false>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)refine_lds);
+        hash_refine_kernel<false><<<dim3(refine_blocks, n_rounds), kRefineThreads, refine_lds, stream>>>(
+            q, R, half, n_rounds, rows, w.list, w.count, buckets);
     }
     return hipGetLastError();
 }

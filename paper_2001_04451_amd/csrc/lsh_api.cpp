@@ -41,6 +41,13 @@ int check_supported(const lsh_config* cfg) {
 
 int64_t bh_of(const lsh_config* cfg) { return (int64_t)cfg->B * cfg->H; }
 
+// The kernels move rows in 16-byte pieces.
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+template <typename... P>
+bool all_aligned(P... p) {
+    return (aligned16(p) && ...);
+}
+
 int status_of(hipError_t e) { return e == hipSuccess ? LSH_OK : LSH_ERR_HIP; }
 
 size_t fwd_rounds_bytes(const lsh_config* cfg) {
@@ -89,6 +96,7 @@ int lsh_hash(const lsh_config* cfg, lsh_dtype dtype, const void* q, const float*
     LSH_TRY(check_config(cfg));
     LSH_TRY(check_dtype(dtype));
     if (!q || !R || !buckets || !workspace) return LSH_ERR_INVALID;
+    if (!all_aligned(q, R, workspace)) return LSH_ERR_INVALID;
     if (workspace_bytes < lsh::hash_workspace_bytes(bh_of(cfg) * cfg->L, cfg->n_rounds, cfg->n_buckets))
         return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
@@ -116,6 +124,7 @@ int lsh_gather_rows(const lsh_config* cfg, lsh_dtype dtype, const void* src, con
     LSH_TRY(check_config(cfg));
     LSH_TRY(check_dtype(dtype));
     if (!src || !perm || !dst) return LSH_ERR_INVALID;
+    if (!all_aligned(src, dst)) return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
     return status_of(lsh::launch_gather(bh_of(cfg), cfg->L, cfg->n_rounds, dtype == LSH_F32, src,
                                         perm, dst, static_cast<hipStream_t>(stream)));
@@ -128,6 +137,7 @@ int lsh_chunk_attn_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, co
     LSH_TRY(check_dtype(dtype));
     if (!q || !v || !buckets || !perm || !bucket_start || !o_rounds || !lse_rounds)
         return LSH_ERR_INVALID;
+    if (!all_aligned(q, v, o_rounds)) return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
     return status_of(lsh::launch_attn_fwd(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets,
                                           cfg->causal != 0, cfg->scale, cfg->self_mask,
@@ -141,6 +151,7 @@ int lsh_combine_rounds(const lsh_config* cfg, lsh_dtype dtype, const float* o_ro
     LSH_TRY(check_config(cfg));
     LSH_TRY(check_dtype(dtype));
     if (!o_rounds || !lse_rounds || !undo || !out) return LSH_ERR_INVALID;
+    if (!all_aligned(o_rounds, out)) return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
     return status_of(lsh::launch_combine(bh_of(cfg), cfg->L, cfg->n_rounds, dtype == LSH_F32,
                                          o_rounds, lse_rounds, undo, out, lse_total,
