@@ -198,7 +198,7 @@ __global__ __launch_bounds__(256, 2) void bwd_kv_kernel(
             sacc = mfma32x32x16(row_operand(Qs, arow, h, s), bk[s], sacc);
             dpacc = mfma32x32x16(row_operand(Ds, arow, h, s), bv[s], dpacc);
         }
-        u32x4 pk[2], dak[2];
+        u32x4 pk[2], pl[2], dak[2];  // P as bf16 hi + lo planes (dV), dA as bf16 (dK)
 #pragma unroll
         for (int run = 0; run < 2; ++run) {
             const int qb = qr0 + 16 * run + 8 * h;  // first query row of the lane's run
@@ -219,17 +219,24 @@ __global__ __launch_bounds__(256, 2) void bwd_kv_kernel(
                     pv[u] = p;
                     dav[u] = p * (dpacc[j] - M.D[qi]);
                 }
-                pk[run][e2] = pack_bf16x2(pv[0], pv[1]);
+                const uint32_t hi = pack_bf16x2(pv[0], pv[1]);
+                pk[run][e2] = hi;
+                pl[run][e2] = pack_bf16x2(pv[0] - __uint_as_float(hi << 16),
+                                          pv[1] - __uint_as_float(hi & 0xFFFF0000u));
                 dak[run][e2] = pack_bf16x2(dav[0], dav[1]);
             }
         }
-        // dV^T += dO^T P,  dK^T += Q^T dA  (k = queries of the tile)
+        // dV^T += dO^T (P_hi + P_lo),  dK^T += Q^T dA  (k = queries of the tile).
+        // dO is exact in bf16 and P_hi + P_lo carries P to ~2^-16, so dV keeps
+        // fp32-level accuracy; dA (then scaled and summed) stays one plane.
 #pragma unroll
         for (int ku = 0; ku < 2; ++ku) {
             const int r0 = qr0 + 16 * ku + 8 * h;
 #pragma unroll
             for (int dt = 0; dt < 2; ++dt) {
-                dv_acc[dt] = mfma32x32x16(col_operand(Ds, r0, 32 * dt + n), as_bf16x8(pk[ku]), dv_acc[dt]);
+                const bf16x8 dOt = col_operand(Ds, r0, 32 * dt + n);
+                dv_acc[dt] = mfma32x32x16(dOt, as_bf16x8(pk[ku]), dv_acc[dt]);
+                dv_acc[dt] = mfma32x32x16(dOt, as_bf16x8(pl[ku]), dv_acc[dt]);
                 dk_acc[dt] = mfma32x32x16(col_operand(Qs, r0, 32 * dt + n), as_bf16x8(dak[ku]), dk_acc[dt]);
             }
         }
