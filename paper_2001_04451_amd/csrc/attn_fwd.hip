@@ -10,34 +10,119 @@
 // its weight exp(-1e5) vanishes in fp32 and fp64 alike, and without one the
 // output is v_i and the log-partition is scale*|q_i| - 1e5.
 //
-// Logits are kept in log2 units: x = (q_i.q_j) * scale*log2(e)/|q_j| - log2 N_ij.
-// N_ij (the number of rounds in which j shares i's bucket) comes from packed
-// bucket signatures, two 10-bit ids per word with guard bits:
-//   nonzero fields of (a ^ b) = popcount(((a ^ b) + 0x1FFBFF) & 0x200400).
+// Logits are kept in log2 units: x = (q_i.q_j) * scale*log2(e)/|q_j| - log2 N_ij,
+// with N_ij from packed bucket signatures (attn_common.h).
 //
-// bf16 path (gfx950 matrix cores): one workgroup stages the rows of chunks
-// c0-1 .. c0+1 (gathered through perm) in LDS; each wave takes 32 queries
-// against the 128-key window as four 32x32 tiles: S^T = K Q^T on
-// mfma_f32_32x32x16_bf16, masks/softmax on the accumulators, then
-// O^T = V^T P^T reusing the accumulators as the B operand (the K rows are
-// loaded in a permuted order so that no shuffle is needed).  Tiles without
-// any valid key for the wave's queries are skipped entirely.
-#include "common.h"
+// bf16 path (gfx950 matrix cores).  A workgroup walks a strip of chunk
+// pairs of one segment.  The rows of the three live chunks (c0-1, c0, c0+1)
+// sit in an LDS ring of three 64-row slots (chunk c in slot (c+3) % 3),
+// gathered through perm into XOR-swizzled 128-byte rows; moving to the next
+// pair only brings in two new chunks, and their loads are issued while the
+// current pair computes (perm first, the rows after the first half of the
+// compute) so that their latency hides behind it.  Each wave takes 32
+// queries against their 128-key window as four 32x32 tiles:
+// S^T = K Q^T on mfma_f32_32x32x16_bf16, masks and softmax on the
+// accumulators, then O^T = V^T P^T with the accumulators reused as the B
+// operand (the K rows are loaded in a permuted order; see kappa).  Tiles with
+// no valid key for the wave's queries are skipped.
+#include "attn_common.h"
 #include "launch.h"
 
 namespace lsh {
 namespace {
 
-constexpr int kRows = 192;  // LDS rows: chunks c0-1, c0, c0+1
-constexpr int kQStride = 72;
-constexpr int kVStride = 68;
-constexpr uint32_t kSigAdd = 0x3FFu | (0x3FFu << 11);
-constexpr uint32_t kSigGuard = (1u << 10) | (1u << 21);
+constexpr int kRing = 192;  // three chunk slots of 64 rows
+constexpr int kMaxBucketsStaged = 1024;
 
-// A-operand row m of a key tile holds key kappa(m), which puts key
-// 16*(j/8) + 8*(l/32) + (j%8) in accumulator register j of lane l.
-__device__ __forceinline__ int kappa(int m) {
-    return 16 * (m >> 4) + 8 * ((m >> 2) & 1) + 4 * ((m >> 3) & 1) + (m & 3);
+__device__ __forceinline__ int ring_row(int chunk, int i) { return ((chunk + 3) % 3) * kChunk + i; }
+
+template <int NW>
+struct FwdSig {
+    static constexpr int stride = NW == 0 ? 1 : (NW <= 1 ? 1 : (NW <= 2 ? 2 : (NW <= 4 ? 4 : 8)));
+};
+
+template <int NW>
+struct FwdShared {
+    char Qs[kRing * 128];
+    char Vs[kRing * 128];
+    float cf[kRing];     // scale*log2(e)/|q_row| (0 for a zero row)
+    int beta[kRing];     // the row's bucket in this round (-1 outside the sequence)
+    uint32_t sig[kRing][FwdSig<NW>::stride];
+    int bstart[kMaxBucketsStaged + 1];  // the segment's bucket starts
+};
+
+// One row of a chunk, as loaded by its eight threads (one 16-byte piece each).
+template <int NW>
+struct RowLoad {
+    u32x4 q, v;
+    int beta;
+    uint32_t sig;
+    bool ok;
+};
+
+template <int NW>
+__device__ __forceinline__ void load_piece(RowLoad<NW>& R, const uint16_t* __restrict__ q,
+                                           const uint16_t* __restrict__ v,
+                                           const int32_t* __restrict__ buckets, int64_t bh, int L,
+                                           int n_r, int n_b, int r, int pos, int part) {
+    R.ok = pos >= 0;
+    const int64_t grow = bh * L + (R.ok ? pos : 0);
+    const u32x4 zero = {0, 0, 0, 0};
+    R.q = R.ok ? *reinterpret_cast<const u32x4*>(q + grow * kHeadDim + part * 8) : zero;
+    R.v = R.ok ? *reinterpret_cast<const u32x4*>(v + grow * kHeadDim + part * 8) : zero;
+    const int32_t* brow = buckets + grow * n_r;
+    R.beta = (R.ok && part == 0) ? min(max(brow[r], 0), n_b - 1) : -1;
+    R.sig = 0;
+    if constexpr (NW > 0) {
+        if (R.ok && part < NW) {
+            R.sig = (uint32_t)brow[2 * part];
+            if (2 * part + 1 < n_r) R.sig |= (uint32_t)brow[2 * part + 1] << 11;
+        }
+    }
+}
+
+// Store one loaded piece; the eight threads of the row reduce |q|^2 together.
+template <int NW>
+__device__ __forceinline__ void store_piece(FwdShared<NW>& S, const RowLoad<NW>& R, int lrow,
+                                            int part, float scale_log2e) {
+    lds_store_piece(S.Qs, lrow, part, R.q);
+    lds_store_piece(S.Vs, lrow, part, R.v);
+    float ss = 0.f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float a = __uint_as_float(R.q[e] << 16), b = __uint_as_float(R.q[e] & 0xFFFF0000u);
+        ss = fmaf(a, a, fmaf(b, b, ss));
+    }
+    ss += __shfl_xor(ss, 1);
+    ss += __shfl_xor(ss, 2);
+    ss += __shfl_xor(ss, 4);
+    if (part == 0) {
+        const float nn = sqrtf(ss);
+        S.cf[lrow] = nn > 0.f ? scale_log2e / nn : 0.f;
+        S.beta[lrow] = R.beta;
+    }
+    if constexpr (NW > 0) {
+        if (part < FwdSig<NW>::stride) S.sig[lrow][part] = part < NW ? R.sig : 0u;
+    }
+}
+
+template <int NW>
+__device__ __forceinline__ void read_sig(const FwdShared<NW>& S, int row, uint32_t (&out)[NW > 0 ? NW : 1]) {
+    if constexpr (NW == 1) {
+        out[0] = S.sig[row][0];
+    } else if constexpr (NW == 2) {
+        const uint2 w = *reinterpret_cast<const uint2*>(&S.sig[row][0]);
+        out[0] = w.x;
+        out[1] = w.y;
+    } else if constexpr (NW > 2) {
+#pragma unroll
+        for (int w4 = 0; w4 < (NW + 3) / 4; ++w4) {
+            const u32x4 w = *reinterpret_cast<const u32x4*>(&S.sig[row][4 * w4]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (4 * w4 + e < NW) out[4 * w4 + e] = w[e];
+        }
+    }
 }
 
 template <int NW, bool CAUSAL>
@@ -45,214 +130,185 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ v,
     const int32_t* __restrict__ buckets, const int32_t* __restrict__ perm,
     const int32_t* __restrict__ bstart, float* __restrict__ o_rounds,
-    float* __restrict__ lse_rounds, int L, int n_r, int n_b, float scale, float self_mask) {
-    constexpr int SIGS = NW == 0 ? 1 : (NW <= 4 ? 4 : 8);
-    __shared__ __attribute__((aligned(16))) uint16_t Qs[kRows][kQStride];
-    __shared__ __attribute__((aligned(16))) uint16_t Vs[kRows][kVStride];
-    __shared__ __attribute__((aligned(16))) float cf[kRows];
-    __shared__ float nrm[kRows];
-    __shared__ int sbeta[kRows];
-    __shared__ __attribute__((aligned(16))) uint32_t sig[kRows][SIGS];
+    float* __restrict__ lse_rounds, int L, int n_r, int n_b, float scale, float self_mask,
+    int pairs_per_strip) {
+    __shared__ __attribute__((aligned(16))) FwdShared<NW> S;
 
     const int tid = threadIdx.x;
     const int64_t seg = blockIdx.y;
     const int64_t bh = seg / n_r;
     const int r = (int)(seg % n_r);
-    const int pair = blockIdx.x;
-    const int slot0 = (2 * pair - 1) * kChunk;
+    const int n_chunks = L / kChunk;
+    const int n_pairs = (n_chunks + 1) / 2;
+    const int p0 = blockIdx.x * pairs_per_strip;
+    const int p1 = min(n_pairs, p0 + pairs_per_strip);
     const float scale_log2e = scale * kLog2e;
+    const int32_t* pseg = perm + seg * L;
+    const int part = tid & 7;
+    for (int b = tid; b <= n_b; b += 256) S.bstart[b] = bstart[seg * (n_b + 1) + b];
 
-    // ---- stage rows [slot0, slot0 + 192) gathered through perm ----
+    // ---- stage the first window: chunks 2p0-1 .. 2p0+1 ----
 #pragma unroll
     for (int i = 0; i < 6; ++i) {
-        const int idx = tid + 256 * i;
-        const int rho = idx >> 3, part = idx & 7;
-        const int slot = slot0 + rho;
-        const bool ok = slot >= 0 && slot < L;
-        const int pos = ok ? min(max(perm[seg * L + slot], 0), L - 1) : 0;
-        const int64_t grow = bh * L + pos;
-        const u32x4 qq = ok ? *reinterpret_cast<const u32x4*>(q + grow * kHeadDim + part * 8) : u32x4{0, 0, 0, 0};
-        const u32x4 vv = ok ? *reinterpret_cast<const u32x4*>(v + grow * kHeadDim + part * 8) : u32x4{0, 0, 0, 0};
-        *reinterpret_cast<u32x4*>(&Qs[rho][part * 8]) = qq;
-        uint32_t* vdst = reinterpret_cast<uint32_t*>(&Vs[rho][part * 8]);
-        *reinterpret_cast<uint2*>(vdst) = make_uint2(vv[0], vv[1]);
-        *reinterpret_cast<uint2*>(vdst + 2) = make_uint2(vv[2], vv[3]);
-        float ss = 0.f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float a = __uint_as_float(qq[e] << 16), b = __uint_as_float(qq[e] & 0xFFFF0000u);
-            ss = fmaf(a, a, fmaf(b, b, ss));
-        }
-        ss += __shfl_xor(ss, 1);
-        ss += __shfl_xor(ss, 2);
-        ss += __shfl_xor(ss, 4);
-        const int32_t* brow = buckets + grow * n_r;
-        if (part == 0) {
-            const float nn = sqrtf(ss);
-            nrm[rho] = nn;
-            cf[rho] = nn > 0.f ? scale_log2e / nn : 0.f;
-            sbeta[rho] = ok ? min(max(brow[r], 0), n_b - 1) : -1;
-        }
-        if constexpr (NW > 0) {
-            if (part < NW) {
-                const int ra = 2 * part, rb = 2 * part + 1;
-                uint32_t w = 0;
-                if (ok) {
-                    w = (uint32_t)brow[ra];
-                    if (rb < n_r) w |= (uint32_t)brow[rb] << 11;
-                }
-                sig[rho][part] = w;
-            }
-        }
+        const int rr = (tid >> 3) + 32 * i;  // 0..191 over the three chunks
+        const int chunk = 2 * p0 - 1 + rr / kChunk;
+        const int slot = chunk * kChunk + rr % kChunk;
+        const int pos = (slot >= 0 && slot < L) ? min(max(pseg[slot], 0), L - 1) : -1;
+        RowLoad<NW> R;
+        load_piece<NW>(R, q, v, buckets, bh, L, n_r, n_b, r, pos, part);
+        store_piece<NW>(S, R, ring_row(chunk, rr % kChunk), part, scale_log2e);
     }
     __syncthreads();
 
-    // ---- per wave: 32 queries against the 128-key window ----
     const int lane = tid & 63, wave = tid >> 6, h = lane >> 5, n = lane & 31;
     const int cw = wave >> 1, qh = wave & 1;
-    const int c = 2 * pair + cw;
-    if (c >= L / kChunk) return;  // no barrier follows
-    const int kb = cw * kChunk;                  // LDS row of the first window key
-    const int rq = kb + kChunk + qh * 32 + n;    // LDS row of this lane's query
-    const int s_q = c * kChunk + qh * 32 + n;    // its sorted slot
-    const int wlo = max(0, (c - 1) * kChunk);
-    const int32_t* bs = bstart + seg * (n_b + 1);
-    const int beta = sbeta[rq];
-    const int lo = max(bs[beta], wlo);
-    const int hi = CAUSAL ? s_q - 1 : min(bs[beta + 1], (c + 1) * kChunk) - 1;
 
-    bf16x8 qb[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) qb[s] = as_bf16x8(*reinterpret_cast<const u32x4*>(&Qs[rq][32 * h + 8 * s]));
-    uint32_t qsig[NW > 0 ? NW : 1];
-#pragma unroll
-    for (int w = 0; w < NW; ++w) qsig[w] = sig[rq][w];
-
-    bool act[4];
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-        const int tb = (c - 1) * kChunk + kt * 32;
-        act[kt] = __ballot(lo <= hi && lo <= tb + 31 && hi >= tb) != 0;
-    }
-
-    f32x16 acc[4];
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-        acc[kt] = f32x16{};
-        if (act[kt]) {
-            const int arow = kb + kt * 32 + kappa(n);
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4*>(&Qs[arow][32 * h + 8 * s]));
-                acc[kt] = mfma32x32x16(a, qb[s], acc[kt]);
-            }
-        }
-    }
-
-    // pass 1: masked logits (log2 units) and the row maximum.  The lane's 16
-    // keys of a tile are two runs of 8 consecutive rows, so their per-key
-    // factors and signatures come in as 16-byte LDS reads.
-    float mrow = -__builtin_inff();
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-        if (!act[kt]) continue;
-        const int tb = (c - 1) * kChunk + kt * 32;
-        const int lo_t = lo - tb, hi_t = hi - tb, self_t = s_q - tb;  // bounds in tile coordinates
-#pragma unroll
-        for (int run = 0; run < 2; ++run) {
-            const int kbase = kb + kt * 32 + 16 * run + 8 * h;  // LDS row of the run's first key
-            const f32x4 c0 = *reinterpret_cast<const f32x4*>(&cf[kbase]);
-            const f32x4 c1 = *reinterpret_cast<const f32x4*>(&cf[kbase + 4]);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int j = 8 * run + e;
-                const int kk = 16 * run + 8 * h + e;  // key index inside the tile
-                bool valid = kk >= lo_t && kk <= hi_t;
-                if constexpr (!CAUSAL) valid = valid && kk != self_t;
-                float nlog2 = 0.f;
-                if constexpr (NW > 0) {
-                    const u32x4 k0 = *reinterpret_cast<const u32x4*>(&sig[kbase + e][0]);
-                    int nm = 0;
-#pragma unroll
-                    for (int w = 0; w < (NW < 4 ? NW : 4); ++w)
-                        nm += __popc(((qsig[w] ^ k0[w]) + kSigAdd) & kSigGuard);
-                    if constexpr (NW > 4) {
-                        const u32x4 k1 = *reinterpret_cast<const u32x4*>(&sig[kbase + e][4]);
-#pragma unroll
-                        for (int w = 4; w < NW; ++w)
-                            nm += __popc(((qsig[w] ^ k1[w - 4]) + kSigAdd) & kSigGuard);
-                    }
-                    nlog2 = __log2f((float)(n_r - nm));
-                }
-                const float cfk = e < 4 ? c0[e] : c1[e - 4];
-                const float x = fmaf(acc[kt][j], cfk, -nlog2);
-                acc[kt][j] = valid ? x : -__builtin_inff();
-                mrow = fmaxf(mrow, acc[kt][j]);
-            }
-        }
-    }
-    mrow = fmaxf(mrow, __shfl_xor(mrow, 32));
-    const bool alone = !(mrow > -__builtin_inff());  // only itself left as a target
-
-    // Rows left with only themselves still take part in the matrix-core
-    // products below (every lane supplies operands); their probabilities are 0.
-    const float msub = alone ? 0.f : mrow;
-
-    // pass 2: probabilities, row sum, bf16 B operands for P V
-    float lsum = 0.f;
-    u32x4 pk[4][2];
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-        if (!act[kt]) continue;
-#pragma unroll
-        for (int ku = 0; ku < 2; ++ku)
-#pragma unroll
-            for (int e2 = 0; e2 < 4; ++e2) {
-                const int j = 8 * ku + 2 * e2;
-                const float p0 = __builtin_amdgcn_exp2f(acc[kt][j] - msub);
-                const float p1 = __builtin_amdgcn_exp2f(acc[kt][j + 1] - msub);
-                lsum += p0 + p1;
-                pk[kt][ku][e2] = pack_bf16x2(p0, p1);
-            }
-    }
-    lsum += __shfl_xor(lsum, 32);
-
-    f32x16 oacc[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-        if (!act[kt]) continue;
-#pragma unroll
-        for (int ku = 0; ku < 2; ++ku) {
-            const bf16x8 pb = as_bf16x8(pk[kt][ku]);
-            const int vr = kb + kt * 32 + 16 * ku + 8 * h;
-#pragma unroll
-            for (int dt = 0; dt < 2; ++dt) {
-                const int dcol = 32 * dt + n;
-                u32x4 va;
-#pragma unroll
-                for (int e2 = 0; e2 < 4; ++e2)
-                    va[e2] = (uint32_t)Vs[vr + 2 * e2][dcol] | ((uint32_t)Vs[vr + 2 * e2 + 1][dcol] << 16);
-                oacc[dt] = mfma32x32x16(as_bf16x8(va), pb, oacc[dt]);
-            }
-        }
-    }
-
-    float* orow = o_rounds + (seg * L + s_q) * kHeadDim;
-    const float inv = alone ? 0.f : 1.f / lsum;
-#pragma unroll
-    for (int dt = 0; dt < 2; ++dt)
+    // positions of the next pair's two new chunks (prefetch, step 1)
+    int pf_pos[4];
+    auto load_pos = [&](int pn, int (&pos)[4]) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int d0 = 32 * dt + 8 * i + 4 * h;
-            f32x4 o;
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                o[e] = alone ? bf16_bits_to_f32(Vs[rq][d0 + e]) : oacc[dt][4 * i + e] * inv;
-            *reinterpret_cast<f32x4*>(orow + d0) = o;
+            const int rr = (tid >> 3) + 32 * i;  // 0..127 over chunks 2pn, 2pn+1
+            const int slot = 2 * pn * kChunk + rr;
+            pos[i] = (pn < p1 && slot < L) ? min(max(pseg[slot], 0), L - 1) : -1;
         }
-    // z = scale*|q_i| - self_mask when the token is its own only target
-    if (h == 0)
-        lse_rounds[seg * L + s_q] = alone ? scale * nrm[rq] - self_mask : (mrow + __log2f(lsum)) * kLn2;
+    };
+    load_pos(p0 + 1, pf_pos);
+
+    for (int p = p0; p < p1; ++p) {
+        const bool more = p + 1 < p1;
+        // prefetch, step 2: the rows of the next pair's new chunks, in flight
+        // during this pair's compute; step 1 for the pair after that
+        RowLoad<NW> pf[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            load_piece<NW>(pf[i], q, v, buckets, bh, L, n_r, n_b, r, pf_pos[i], part);
+        int pf_pos2[4];
+        load_pos(p + 2, pf_pos2);
+
+        // ---- compute: per key tile, S^T, masks, online softmax, P V ----
+        const int cq = 2 * p + cw;  // this wave's query chunk
+        const bool active = cq < n_chunks;
+        if (active) {
+            const int rq = ring_row(cq, qh * 32 + n);
+            const int s_q = cq * kChunk + qh * 32 + n;
+            const int beta = max(S.beta[rq], 0);
+            const int wlo = max(0, (cq - 1) * kChunk);
+            const int lo = max(S.bstart[beta], wlo);
+            const int hi = CAUSAL ? s_q - 1 : min(S.bstart[beta + 1], (cq + 1) * kChunk) - 1;
+            bf16x8 qb[4];
+#pragma unroll
+            for (int s = 0; s < 4; ++s) qb[s] = row_operand(S.Qs, rq, h, s);
+            uint32_t qsig[NW > 0 ? NW : 1];
+            read_sig<NW>(S, rq, qsig);
+            bool act[4];
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt) {
+                const int tb = (cq - 1) * kChunk + kt * 32;
+                act[kt] = __ballot(lo <= hi && lo <= tb + 31 && hi >= tb) != 0;
+            }
+            float m = -__builtin_inff(), lsum = 0.f;
+            f32x16 oacc[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt) {
+                if (!act[kt]) continue;
+                const int kr0 = ring_row(cq - 1 + (kt >> 1), (kt & 1) * 32);
+                f32x16 acc = {};
+#pragma unroll
+                for (int s = 0; s < 4; ++s)
+                    acc = mfma32x32x16(row_operand(S.Qs, kr0 + kappa(n), h, s), qb[s], acc);
+                const int tb = (cq - 1) * kChunk + kt * 32;
+                const int lo_t = lo - tb, hi_t = hi - tb, self_t = s_q - tb;
+                float mt = -__builtin_inff();
+#pragma unroll
+                for (int run = 0; run < 2; ++run) {
+                    const int kbase = kr0 + 16 * run + 8 * h;
+                    const f32x4 c0 = *reinterpret_cast<const f32x4*>(&S.cf[kbase]);
+                    const f32x4 c1 = *reinterpret_cast<const f32x4*>(&S.cf[kbase + 4]);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int j = 8 * run + e;
+                        const int kk = 16 * run + 8 * h + e;
+                        bool valid = kk >= lo_t && kk <= hi_t;
+                        if constexpr (!CAUSAL) valid = valid && kk != self_t;
+                        float nlog2 = 0.f;
+                        if constexpr (NW > 0) {
+                            uint32_t ksig[NW];
+                            read_sig<NW>(S, kbase + e, ksig);
+                            int nm = 0;
+#pragma unroll
+                            for (int w = 0; w < NW; ++w) nm += sig_mismatches(qsig[w], ksig[w]);
+                            nlog2 = __log2f((float)(n_r - nm));
+                        }
+                        const float cfk = e < 4 ? c0[e] : c1[e - 4];
+                        acc[j] = valid ? fmaf(acc[j], cfk, -nlog2) : -__builtin_inff();
+                        mt = fmaxf(mt, acc[j]);
+                    }
+                }
+                // online softmax over the tiles (both lane halves share the row max)
+                mt = fmaxf(mt, __shfl_xor(mt, 32));
+                const float m_new = fmaxf(m, mt);
+                const float msub = m_new > -__builtin_inff() ? m_new : 0.f;
+                const float corr = __builtin_amdgcn_exp2f(m - msub);
+                lsum *= corr;
+#pragma unroll
+                for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+                    for (int k = 0; k < 16; ++k) oacc[dt][k] *= corr;
+                m = m_new;
+                u32x4 pk[2];
+#pragma unroll
+                for (int ku = 0; ku < 2; ++ku)
+#pragma unroll
+                    for (int e2 = 0; e2 < 4; ++e2) {
+                        const int j = 8 * ku + 2 * e2;
+                        const float pa = __builtin_amdgcn_exp2f(acc[j] - msub);
+                        const float pb2 = __builtin_amdgcn_exp2f(acc[j + 1] - msub);
+                        lsum += pa + pb2;
+                        pk[ku][e2] = pack_bf16x2(pa, pb2);
+                    }
+#pragma unroll
+                for (int ku = 0; ku < 2; ++ku)
+#pragma unroll
+                    for (int dt = 0; dt < 2; ++dt)
+                        oacc[dt] = mfma32x32x16(col_operand(S.Vs, kr0 + 16 * ku + 8 * h, 32 * dt + n),
+                                                as_bf16x8(pk[ku]), oacc[dt]);
+            }
+            lsum += __shfl_xor(lsum, 32);
+            const bool alone = !(m > -__builtin_inff());  // only itself left as a target
+            float* orow = o_rounds + (seg * L + s_q) * kHeadDim;
+            const float inv = alone ? 0.f : 1.f / lsum;
+#pragma unroll
+            for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int d0 = 32 * dt + 8 * i + 4 * h;
+                    f32x4 o;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        o[e] = alone ? bf16_bits_to_f32(lds_elem(S.Vs, rq, d0 + e)) : oacc[dt][4 * i + e] * inv;
+                    *reinterpret_cast<f32x4*>(orow + d0) = o;
+                }
+            if (h == 0) {
+                // z = scale*|q_i| - self_mask when the token is its own only target
+                const float cfq = S.cf[rq];
+                const float qnorm = cfq > 0.f ? scale_log2e / cfq : 0.f;
+                lse_rounds[seg * L + s_q] = alone ? scale * qnorm - self_mask : (m + __log2f(lsum)) * kLn2;
+            }
+        }
+
+        __syncthreads();  // every wave is done with the slots of chunks 2p-1 and 2p
+        if (more) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int rr = (tid >> 3) + 32 * i;
+                store_piece<NW>(S, pf[i], ring_row(2 * p + 2 + rr / kChunk, rr % kChunk), part, scale_log2e);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pf_pos[i] = pf_pos2[i];
+        __syncthreads();
+    }
 }
 
 // fp32 path: one wave per chunk, one lane per query, exact fp32 arithmetic
@@ -338,14 +394,14 @@ __global__ __launch_bounds__(64) void attn_fwd_f32_kernel(
 template <int NW>
 hipError_t launch_bf16(dim3 grid, bool causal, const uint16_t* q, const uint16_t* v,
                        const int32_t* buckets, const int32_t* perm, const int32_t* bs, float* o,
-                       float* lse, int L, int n_r, int n_b, float scale, float self_mask,
+                       float* lse, int L, int n_r, int n_b, float scale, float self_mask, int pps,
                        hipStream_t stream) {
     if (causal)
         attn_fwd_bf16_kernel<NW, true><<<grid, 256, 0, stream>>>(q, v, buckets, perm, bs, o, lse, L,
-                                                                 n_r, n_b, scale, self_mask);
+                                                                 n_r, n_b, scale, self_mask, pps);
     else
         attn_fwd_bf16_kernel<NW, false><<<grid, 256, 0, stream>>>(q, v, buckets, perm, bs, o, lse, L,
-                                                                  n_r, n_b, scale, self_mask);
+                                                                  n_r, n_b, scale, self_mask, pps);
     return hipGetLastError();
 }
 
@@ -364,14 +420,19 @@ hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, bool 
             o_rounds, lse_rounds, L, n_rounds, n_buckets, causal ? 1 : 0, scale, self_mask);
         return hipGetLastError();
     }
-    const dim3 grid((unsigned)((L / kChunk + 1) / 2), segs);
+    // Strips of chunk pairs: long enough to reuse the shared chunk between
+    // neighbouring pairs and to hide the next pair's loads, short enough to
+    // leave several workgroups per CU for the whole chip.
+    const int64_t n_pairs = (L / kChunk + 1) / 2;
+    const int pps = (int)std::max<int64_t>(1, std::min<int64_t>(16, n_pairs * segs / 3072));
+    const dim3 grid((unsigned)((n_pairs + pps - 1) / pps), segs);
     const uint16_t* qb = static_cast<const uint16_t*>(q);
     const uint16_t* vb = static_cast<const uint16_t*>(v);
     const int nw = n_rounds == 1 ? 0 : (n_rounds + 1) / 2;
 #define LSH_FWD_CASE(W)                                                                         \
     case W:                                                                                     \
         return launch_bf16<W>(grid, causal, qb, vb, buckets, perm, bucket_start, o_rounds,      \
-                              lse_rounds, L, n_rounds, n_buckets, scale, self_mask, stream);
+                              lse_rounds, L, n_rounds, n_buckets, scale, self_mask, pps, stream);
     switch (nw) {
         LSH_FWD_CASE(0)
         LSH_FWD_CASE(1)
