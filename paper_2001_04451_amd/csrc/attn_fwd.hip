@@ -10,21 +10,30 @@
 // its weight exp(-1e5) vanishes in fp32 and fp64 alike, and without one the
 // output is v_i and the log-partition is scale*|q_i| - 1e5.
 //
-// Logits are kept in log2 units: x = (q_i.q_j) * scale*log2(e)/|q_j| - log2 N_ij,
-// with N_ij from packed bucket signatures (attn_common.h).
+// Logits are kept in log2 units: x = (q_i.q_j) * scale*log2(e)/|q_j| - log2 N_ij.
 //
 // bf16 path (gfx950 matrix cores).  A workgroup walks a strip of chunk
 // pairs of one segment.  The rows of the three live chunks (c0-1, c0, c0+1)
-// sit in an LDS ring of three 64-row slots (chunk c in slot (c+3) % 3),
-// gathered through perm into XOR-swizzled 128-byte rows; moving to the next
-// pair only brings in two new chunks, and their loads are issued while the
-// current pair computes (perm first, the rows after the first half of the
-// compute) so that their latency hides behind it.  Each wave takes 32
+// sit in an LDS ring of three 64-row slots (chunk c in slot (c+3) % 3): the
+// query/key rows as XOR-swizzled 128-byte rows, V transposed (row d holds the
+// 192 ring keys) so that the V^T operand is one 16-byte read.  Moving to the
+// next pair only brings in two new chunks; their loads are issued before the
+// current pair computes and land in LDS after it.  Each wave takes 32
 // queries against their 128-key window as four 32x32 tiles:
 // S^T = K Q^T on mfma_f32_32x32x16_bf16, masks and softmax on the
 // accumulators, then O^T = V^T P^T with the accumulators reused as the B
 // operand (the K rows are loaded in a permuted order; see kappa).  Tiles with
 // no valid key for the wave's queries are skipped.
+//
+// Per score element the VALU work is what bounds this kernel, so it is kept
+// to a few instructions: the interval mask is one bit of a per-lane word, the
+// count of rounds in which i and j differ is one popcount over the guard bits
+// of the packed bucket signatures (all words merged, see sig_word), and the
+// mask and log2 N_ij come together from one 33-entry LDS table indexed by that
+// popcount (index 32 = masked).  The softmax needs no running maximum when
+// the wave's logit bound B_i = scale*log2(e)*|q_i| is moderate: every logit
+// lies in [-B_i - log2 n_r, B_i], so exp2(x - B_i) neither overflows nor
+// underflows; waves with a larger bound fall back to the online maximum.
 #include "attn_common.h"
 #include "launch.h"
 
@@ -33,76 +42,136 @@ namespace {
 
 constexpr int kRing = 192;  // three chunk slots of 64 rows
 constexpr int kMaxBucketsStaged = 1024;
+constexpr float kFastBound = 60.f;  // largest B_i handled without a running maximum
+constexpr int kMaskedIndex = 32;    // table index of a masked-out key
 
 __device__ __forceinline__ int ring_row(int chunk, int i) { return ((chunk + 3) % 3) * kChunk + i; }
 
+// Bucket signature word w of a token: its ids in rounds 2w and 2w+1 (10 bits
+// each) at bit offsets w and w+11.  Adding sig_add(w) to (a ^ b) carries into
+// guard bit w+10 (w+21) exactly when the first (second) ids differ; the guard
+// bits of different words are distinct, so the number of rounds in which two
+// tokens differ is the popcount of the OR over w of
+// ((a_w ^ b_w) + sig_add(w)) & sig_guard(w).
+__device__ __forceinline__ constexpr uint32_t sig_add(int w) {
+    return (0x3FFu << w) | (0x3FFu << (w + 11));
+}
+__device__ __forceinline__ constexpr uint32_t sig_guard(int w) {
+    return (1u << (w + 10)) | (1u << (w + 21));
+}
+
 template <int NW>
 struct FwdSig {
-    static constexpr int stride = NW == 0 ? 1 : (NW <= 1 ? 1 : (NW <= 2 ? 2 : (NW <= 4 ? 4 : 8)));
+    static constexpr int stride = NW <= 1 ? 1 : (NW <= 2 ? 2 : (NW <= 4 ? 4 : 8));
 };
 
 template <int NW>
 struct FwdShared {
-    char Qs[kRing * 128];
-    char Vs[kRing * 128];
-    float cf[kRing];     // scale*log2(e)/|q_row| (0 for a zero row)
-    int beta[kRing];     // the row's bucket in this round (-1 outside the sequence)
+    char Qs[kRing * 128];           // query/key rows (swizzled)
+    char Vt[kHeadDim * kRing * 2];  // V^T: row d, 16-byte blocks of 8 keys (swizzled)
+    float cf[kRing];                // scale*log2(e)/|q_row| (0 for a zero row)
+    int beta[kRing];                // the row's bucket in this round (-1 outside the sequence)
     uint32_t sig[kRing][FwdSig<NW>::stride];
     int bstart[kMaxBucketsStaged + 1];  // the segment's bucket starts
+    float tab[kMaskedIndex + 1];        // -log2 N by mismatch count; -inf = masked
 };
 
-// One row of a chunk, as loaded by its eight threads (one 16-byte piece each).
-template <int NW>
-struct RowLoad {
-    u32x4 q, v;
-    int beta;
-    uint32_t sig;
-    bool ok;
+// Byte offset of keys k..k+3 (k % 4 == 0) in row d of V^T.  Block b of row d
+// sits at b ^ vt_swz(d): the 16 rows read together land in distinct banks.
+__device__ __forceinline__ int vt_swz(int d) { return (d + (d >> 3)) & 7; }
+__device__ __forceinline__ uint32_t vt_offset(int d, int k) {
+    return (uint32_t)d * (kRing * 2) + (uint32_t)(((k >> 3) ^ vt_swz(d)) << 4) + (uint32_t)((k & 4) << 1);
+}
+
+// Four consecutive rows of a batch, as loaded by one thread (16-byte piece
+// `part` of each row, plus signature word `part` and, for one part, the
+// rows' buckets in this round).
+struct RowQuad {
+    u32x4 q[4], v[4];
+    uint32_t sig[4];
+    int beta[4];
 };
 
 template <int NW>
-__device__ __forceinline__ void load_piece(RowLoad<NW>& R, const uint16_t* __restrict__ q,
-                                           const uint16_t* __restrict__ v,
-                                           const int32_t* __restrict__ buckets, int64_t bh, int L,
-                                           int n_r, int n_b, int r, int pos, int part) {
-    R.ok = pos >= 0;
-    const int64_t grow = bh * L + (R.ok ? pos : 0);
+__device__ __forceinline__ void load_quad(RowQuad& R, const uint16_t* __restrict__ q,
+                                          const uint16_t* __restrict__ v,
+                                          const int32_t* __restrict__ buckets, int64_t bh, int L,
+                                          int n_r, int n_b, int r, const int (&pos)[4], int part) {
     const u32x4 zero = {0, 0, 0, 0};
-    R.q = R.ok ? *reinterpret_cast<const u32x4*>(q + grow * kHeadDim + part * 8) : zero;
-    R.v = R.ok ? *reinterpret_cast<const u32x4*>(v + grow * kHeadDim + part * 8) : zero;
-    const int32_t* brow = buckets + grow * n_r;
-    R.beta = (R.ok && part == 0) ? min(max(brow[r], 0), n_b - 1) : -1;
-    R.sig = 0;
-    if constexpr (NW > 0) {
-        if (R.ok && part < NW) {
-            R.sig = (uint32_t)brow[2 * part];
-            if (2 * part + 1 < n_r) R.sig |= (uint32_t)brow[2 * part + 1] << 11;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const bool ok = pos[i] >= 0;
+        const int64_t grow = bh * L + (ok ? pos[i] : 0);
+        R.q[i] = ok ? *reinterpret_cast<const u32x4*>(q + grow * kHeadDim + part * 8) : zero;
+        R.v[i] = ok ? *reinterpret_cast<const u32x4*>(v + grow * kHeadDim + part * 8) : zero;
+        const int32_t* brow = buckets + grow * n_r;
+        R.sig[i] = 0;
+        R.beta[i] = -1;
+        if constexpr (NW > 0) {
+            if (ok && part < NW) {
+                const uint32_t id0 = (uint32_t)brow[2 * part] & 0x3FFu;
+                const uint32_t id1 = 2 * part + 1 < n_r ? (uint32_t)brow[2 * part + 1] & 0x3FFu : 0u;
+                R.sig[i] = (id0 << part) | (id1 << (part + 11));
+                if (part == (r >> 1)) R.beta[i] = min((int)((r & 1) ? id1 : id0), n_b - 1);
+            }
+        } else {
+            if (ok && part == 0) R.beta[i] = min(max(brow[0], 0), n_b - 1);
         }
     }
 }
 
-// Store one loaded piece; the eight threads of the row reduce |q|^2 together.
+// Store a quad at ring rows rr0 .. rr0+3; the eight threads of the quad
+// reduce |q|^2 of the four rows together.
 template <int NW>
-__device__ __forceinline__ void store_piece(FwdShared<NW>& S, const RowLoad<NW>& R, int lrow,
-                                            int part, float scale_log2e) {
-    lds_store_piece(S.Qs, lrow, part, R.q);
-    lds_store_piece(S.Vs, lrow, part, R.v);
-    float ss = 0.f;
+__device__ __forceinline__ void store_quad(FwdShared<NW>& S, const RowQuad& R, int rr0, int part,
+                                           int r, float scale_log2e) {
+    float ss[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        lds_store_piece(S.Qs, rr0 + i, part, R.q[i]);
+        float a = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float lo = __uint_as_float(R.q[i][e] << 16), hi = __uint_as_float(R.q[i][e] & 0xFFFF0000u);
+            a = fmaf(lo, lo, fmaf(hi, hi, a));
+        }
+        ss[i] = a;
+    }
+    // V^T: dword e of a piece holds d = 8*part + 2e (low half) and 2e+1 (high)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-        const float a = __uint_as_float(R.q[e] << 16), b = __uint_as_float(R.q[e] & 0xFFFF0000u);
-        ss = fmaf(a, a, fmaf(b, b, ss));
+        const uint32_t a0 = R.v[0][e], a1 = R.v[1][e], a2 = R.v[2][e], a3 = R.v[3][e];
+        uint2 lo, hi;
+        lo.x = (a0 & 0xFFFFu) | (a1 << 16);
+        lo.y = (a2 & 0xFFFFu) | (a3 << 16);
+        hi.x = (a0 >> 16) | (a1 & 0xFFFF0000u);
+        hi.y = (a2 >> 16) | (a3 & 0xFFFF0000u);
+        const int d = 8 * part + 2 * e;
+        *reinterpret_cast<uint2*>(S.Vt + vt_offset(d, rr0)) = lo;
+        *reinterpret_cast<uint2*>(S.Vt + vt_offset(d + 1, rr0)) = hi;
     }
-    ss += __shfl_xor(ss, 1);
-    ss += __shfl_xor(ss, 2);
-    ss += __shfl_xor(ss, 4);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        ss[i] += __shfl_xor(ss[i], 1);
+        ss[i] += __shfl_xor(ss[i], 2);
+        ss[i] += __shfl_xor(ss[i], 4);
+    }
     if (part == 0) {
-        const float nn = sqrtf(ss);
-        S.cf[lrow] = nn > 0.f ? scale_log2e / nn : 0.f;
-        S.beta[lrow] = R.beta;
+        f32x4 c;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float nn = sqrtf(ss[i]);
+            c[i] = nn > 0.f ? scale_log2e / nn : 0.f;
+        }
+        *reinterpret_cast<f32x4*>(&S.cf[rr0]) = c;
     }
+    if (part == (NW > 0 ? (r >> 1) : 0))
+        *reinterpret_cast<int4*>(&S.beta[rr0]) = make_int4(R.beta[0], R.beta[1], R.beta[2], R.beta[3]);
     if constexpr (NW > 0) {
-        if (part < FwdSig<NW>::stride) S.sig[lrow][part] = part < NW ? R.sig : 0u;
+        if (part < FwdSig<NW>::stride) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) S.sig[rr0 + i][part] = part < NW ? R.sig[i] : 0u;
+        }
     }
 }
 
@@ -125,6 +194,23 @@ __device__ __forceinline__ void read_sig(const FwdShared<NW>& S, int row, uint32
     }
 }
 
+// Slots of the quads that thread `tid` loads for the batch of chunks
+// c_first .. c_first + n_chunks_batch - 1 (four consecutive rows per group of
+// eight threads); -1 outside the sequence or past the strip.
+__device__ __forceinline__ void quad_positions(const int32_t* __restrict__ pseg, int c_first,
+                                               int n_chunks_batch, bool live, int n_chunks, int L,
+                                               int tid, int (&pos)[4]) {
+    const int g = tid >> 3;
+    const int chunk = c_first + (4 * g) / kChunk;
+    const bool ok = live && g < n_chunks_batch * (kChunk / 4) && chunk >= 0 && chunk < n_chunks;
+    int4 p4 = make_int4(-1, -1, -1, -1);
+    if (ok) p4 = *reinterpret_cast<const int4*>(pseg + (int64_t)c_first * kChunk + 4 * g);
+    pos[0] = ok ? min(max(p4.x, 0), L - 1) : -1;
+    pos[1] = ok ? min(max(p4.y, 0), L - 1) : -1;
+    pos[2] = ok ? min(max(p4.z, 0), L - 1) : -1;
+    pos[3] = ok ? min(max(p4.w, 0), L - 1) : -1;
+}
+
 template <int NW, bool CAUSAL>
 __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ v,
@@ -145,51 +231,41 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
     const float scale_log2e = scale * kLog2e;
     const int32_t* pseg = perm + seg * L;
     const int part = tid & 7;
+    const int qrow = 4 * (tid >> 3);  // first row of this thread's quad in a batch
     for (int b = tid; b <= n_b; b += 256) S.bstart[b] = bstart[seg * (n_b + 1) + b];
+    if (tid <= kMaskedIndex)
+        S.tab[tid] = tid < n_r ? -__log2f((float)(n_r - tid)) : -__builtin_inff();
 
-    // ---- stage the first window: chunks 2p0-1 .. 2p0+1 ----
-#pragma unroll
-    for (int i = 0; i < 6; ++i) {
-        const int rr = (tid >> 3) + 32 * i;  // 0..191 over the three chunks
-        const int chunk = 2 * p0 - 1 + rr / kChunk;
-        const int slot = chunk * kChunk + rr % kChunk;
-        const int pos = (slot >= 0 && slot < L) ? min(max(pseg[slot], 0), L - 1) : -1;
-        RowLoad<NW> R;
-        load_piece<NW>(R, q, v, buckets, bh, L, n_r, n_b, r, pos, part);
-        store_piece<NW>(S, R, ring_row(chunk, rr % kChunk), part, scale_log2e);
+    // ---- stage the first window: chunk 2p0-1, then chunks 2p0 and 2p0+1 ----
+    {
+        int pos[4];
+        RowQuad R;
+        quad_positions(pseg, 2 * p0 - 1, 1, true, n_chunks, L, tid, pos);
+        load_quad<NW>(R, q, v, buckets, bh, L, n_r, n_b, r, pos, part);
+        if (qrow < kChunk) store_quad<NW>(S, R, ring_row(2 * p0 - 1, qrow), part, r, scale_log2e);
+        quad_positions(pseg, 2 * p0, 2, true, n_chunks, L, tid, pos);
+        load_quad<NW>(R, q, v, buckets, bh, L, n_r, n_b, r, pos, part);
+        store_quad<NW>(S, R, ring_row(2 * p0 + qrow / kChunk, qrow % kChunk), part, r, scale_log2e);
     }
     __syncthreads();
 
     const int lane = tid & 63, wave = tid >> 6, h = lane >> 5, n = lane & 31;
     const int cw = wave >> 1, qh = wave & 1;
 
-    // positions of the next pair's two new chunks (prefetch, step 1)
     int pf_pos[4];
-    auto load_pos = [&](int pn, int (&pos)[4]) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int rr = (tid >> 3) + 32 * i;  // 0..127 over chunks 2pn, 2pn+1
-            const int slot = 2 * pn * kChunk + rr;
-            pos[i] = (pn < p1 && slot < L) ? min(max(pseg[slot], 0), L - 1) : -1;
-        }
-    };
-    load_pos(p0 + 1, pf_pos);
+    quad_positions(pseg, 2 * (p0 + 1), 2, p0 + 1 < p1, n_chunks, L, tid, pf_pos);
 
     for (int p = p0; p < p1; ++p) {
         const bool more = p + 1 < p1;
-        // prefetch, step 2: the rows of the next pair's new chunks, in flight
-        // during this pair's compute; step 1 for the pair after that
-        RowLoad<NW> pf[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            load_piece<NW>(pf[i], q, v, buckets, bh, L, n_r, n_b, r, pf_pos[i], part);
+        // the next pair's new chunks load during this pair's compute
+        RowQuad pf;
+        load_quad<NW>(pf, q, v, buckets, bh, L, n_r, n_b, r, pf_pos, part);
         int pf_pos2[4];
-        load_pos(p + 2, pf_pos2);
+        quad_positions(pseg, 2 * (p + 2), 2, p + 2 < p1, n_chunks, L, tid, pf_pos2);
 
-        // ---- compute: per key tile, S^T, masks, online softmax, P V ----
+        // ---- compute: per key tile, S^T, masks, softmax, P V ----
         const int cq = 2 * p + cw;  // this wave's query chunk
-        const bool active = cq < n_chunks;
-        if (active) {
+        if (cq < n_chunks) {
             const int rq = ring_row(cq, qh * 32 + n);
             const int s_q = cq * kChunk + qh * 32 + n;
             const int beta = max(S.beta[rq], 0);
@@ -201,6 +277,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
             for (int s = 0; s < 4; ++s) qb[s] = row_operand(S.Qs, rq, h, s);
             uint32_t qsig[NW > 0 ? NW : 1];
             read_sig<NW>(S, rq, qsig);
+            const float cfq = S.cf[rq];
+            const float bound = cfq > 0.f ? scale_log2e * scale_log2e / cfq : 0.f;  // B_i
+            const bool fast = __ballot(!(bound <= kFastBound)) == 0;
             bool act[4];
 #pragma unroll
             for (int kt = 0; kt < 4; ++kt) {
@@ -217,9 +296,15 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
 #pragma unroll
                 for (int s = 0; s < 4; ++s)
                     acc = mfma32x32x16(row_operand(S.Qs, kr0 + kappa(n), h, s), qb[s], acc);
+                // masked keys of this lane's query: bit k of minv <-> tile key 8h + k
                 const int tb = (cq - 1) * kChunk + kt * 32;
-                const int lo_t = lo - tb, hi_t = hi - tb, self_t = s_q - tb;
-                float mt = -__builtin_inff();
+                const int lo_t = max(lo - tb, 0), hi_t = min(hi - tb, 31);
+                uint32_t valid = lo_t <= hi_t ? (0xFFFFFFFFu >> (31 - hi_t)) & (0xFFFFFFFFu << lo_t) : 0u;
+                if constexpr (!CAUSAL) {
+                    const int self_t = s_q - tb;
+                    if (self_t >= 0 && self_t < 32) valid &= ~(1u << self_t);
+                }
+                const uint32_t minv = ~valid >> (8 * h);
 #pragma unroll
                 for (int run = 0; run < 2; ++run) {
                     const int kbase = kr0 + 16 * run + 8 * h;
@@ -228,54 +313,58 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
                         const int j = 8 * run + e;
-                        const int kk = 16 * run + 8 * h + e;
-                        bool valid = kk >= lo_t && kk <= hi_t;
-                        if constexpr (!CAUSAL) valid = valid && kk != self_t;
-                        float nlog2 = 0.f;
+                        uint32_t t = (uint32_t)((int32_t)(minv << (31 - (16 * run + e))) >> 31);
                         if constexpr (NW > 0) {
                             uint32_t ksig[NW];
                             read_sig<NW>(S, kbase + e, ksig);
-                            int nm = 0;
 #pragma unroll
-                            for (int w = 0; w < NW; ++w) nm += sig_mismatches(qsig[w], ksig[w]);
-                            nlog2 = __log2f((float)(n_r - nm));
+                            for (int w = 0; w < NW; ++w) t |= ((qsig[w] ^ ksig[w]) + sig_add(w)) & sig_guard(w);
                         }
                         const float cfk = e < 4 ? c0[e] : c1[e - 4];
-                        acc[j] = valid ? fmaf(acc[j], cfk, -nlog2) : -__builtin_inff();
-                        mt = fmaxf(mt, acc[j]);
+                        acc[j] = fmaf(acc[j], cfk, S.tab[__popc(t)]);
                     }
                 }
-                // online softmax over the tiles (both lane halves share the row max)
-                mt = fmaxf(mt, __shfl_xor(mt, 32));
-                const float m_new = fmaxf(m, mt);
-                const float msub = m_new > -__builtin_inff() ? m_new : 0.f;
-                const float corr = __builtin_amdgcn_exp2f(m - msub);
-                lsum *= corr;
+                float off = bound;
+                if (!fast) {  // online maximum (both lane halves share the row max)
+                    float mt = acc[0];
 #pragma unroll
-                for (int dt = 0; dt < 2; ++dt)
+                    for (int j = 1; j < 16; ++j) mt = fmaxf(mt, acc[j]);
+                    mt = fmaxf(mt, __shfl_xor(mt, 32));
+                    const float m_new = fmaxf(m, mt);
+                    off = m_new > -__builtin_inff() ? m_new : 0.f;
+                    const float corr = __builtin_amdgcn_exp2f(m - off);
+                    lsum *= corr;
 #pragma unroll
-                    for (int k = 0; k < 16; ++k) oacc[dt][k] *= corr;
-                m = m_new;
+                    for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+                        for (int k = 0; k < 16; ++k) oacc[dt][k] *= corr;
+                    m = m_new;
+                }
                 u32x4 pk[2];
 #pragma unroll
                 for (int ku = 0; ku < 2; ++ku)
 #pragma unroll
                     for (int e2 = 0; e2 < 4; ++e2) {
                         const int j = 8 * ku + 2 * e2;
-                        const float pa = __builtin_amdgcn_exp2f(acc[j] - msub);
-                        const float pb2 = __builtin_amdgcn_exp2f(acc[j + 1] - msub);
+                        const float pa = __builtin_amdgcn_exp2f(acc[j] - off);
+                        const float pb2 = __builtin_amdgcn_exp2f(acc[j + 1] - off);
                         lsum += pa + pb2;
                         pk[ku][e2] = pack_bf16x2(pa, pb2);
                     }
 #pragma unroll
-                for (int ku = 0; ku < 2; ++ku)
+                for (int ku = 0; ku < 2; ++ku) {
+                    const int kb = kr0 + 16 * ku + 8 * h;
 #pragma unroll
-                    for (int dt = 0; dt < 2; ++dt)
-                        oacc[dt] = mfma32x32x16(col_operand(S.Vs, kr0 + 16 * ku + 8 * h, 32 * dt + n),
-                                                as_bf16x8(pk[ku]), oacc[dt]);
+                    for (int dt = 0; dt < 2; ++dt) {
+                        const int d = 32 * dt + n;
+                        const u32x4 va = *reinterpret_cast<const u32x4*>(S.Vt + vt_offset(d, kb));
+                        oacc[dt] = mfma32x32x16(as_bf16x8(va), as_bf16x8(pk[ku]), oacc[dt]);
+                    }
+                }
             }
             lsum += __shfl_xor(lsum, 32);
-            const bool alone = !(m > -__builtin_inff());  // only itself left as a target
+            const bool alone = !(lsum > 0.f);  // only itself left as a target
+            const float mref = fast ? bound : m;
             float* orow = o_rounds + (seg * L + s_q) * kHeadDim;
             const float inv = alone ? 0.f : 1.f / lsum;
 #pragma unroll
@@ -285,26 +374,24 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
                     const int d0 = 32 * dt + 8 * i + 4 * h;
                     f32x4 o;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        o[e] = alone ? bf16_bits_to_f32(lds_elem(S.Vs, rq, d0 + e)) : oacc[dt][4 * i + e] * inv;
+                    for (int e = 0; e < 4; ++e) o[e] = oacc[dt][4 * i + e] * inv;
+                    if (alone) {
+                        const int kq = qh * 32 + n + ((cq + 3) % 3) * kChunk;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            o[e] = bf16_bits_to_f32(*reinterpret_cast<const uint16_t*>(
+                                S.Vt + vt_offset(d0 + e, kq & ~3) + (kq & 3) * 2));
+                    }
                     *reinterpret_cast<f32x4*>(orow + d0) = o;
                 }
             if (h == 0) {
                 // z = scale*|q_i| - self_mask when the token is its own only target
-                const float cfq = S.cf[rq];
-                const float qnorm = cfq > 0.f ? scale_log2e / cfq : 0.f;
-                lse_rounds[seg * L + s_q] = alone ? scale * qnorm - self_mask : (m + __log2f(lsum)) * kLn2;
+                lse_rounds[seg * L + s_q] = alone ? bound * kLn2 - self_mask : (mref + __log2f(lsum)) * kLn2;
             }
         }
 
         __syncthreads();  // every wave is done with the slots of chunks 2p-1 and 2p
-        if (more) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int rr = (tid >> 3) + 32 * i;
-                store_piece<NW>(S, pf[i], ring_row(2 * p + 2 + rr / kChunk, rr % kChunk), part, scale_log2e);
-            }
-        }
+        if (more) store_quad<NW>(S, pf, ring_row(2 * p + 2 + qrow / kChunk, qrow % kChunk), part, r, scale_log2e);
 #pragma unroll
         for (int i = 0; i < 4; ++i) pf_pos[i] = pf_pos2[i];
         __syncthreads();

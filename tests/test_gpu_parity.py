@@ -164,3 +164,42 @@ def test_invalid_arguments_on_gpu(gpu):
     with pytest.raises(lsh.LshError) as e:
         lsh.lsh_hash(cfg, q, R)
     assert e.value.status == lsh.LSH_ERR_INVALID
+
+
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("variant", ["large_norm", "duplicates_and_zeros"])
+def test_attention_edge_inputs(gpu, variant, causal):
+    """Attention on edited inputs, with the oracle's bucket ids.
+
+    large_norm: every fifth query scaled by 64, so its logit bound
+    scale*log2(e)*|q| is far above the range the kernel covers without a
+    running maximum; the waves holding such rows take the online-maximum path.
+    duplicates_and_zeros: pairs of identical tokens (N_ij = n_r, the largest
+    repeat count) and all-zero rows (zero norm, every logit zero)."""
+    w = small("mixture_bf16_L4096", B=1, H=2, L=2048, causal=causal)
+    x = W.make_inputs(w)
+    qf = W.bf16_bits_to_f32(x["q"])
+    if variant == "large_norm":
+        qf[:, :, ::5, :] *= 64.0
+    else:
+        qf[:, :, 1::4, :] = qf[:, :, 0::4, :]
+        qf[:, :, 2::16, :] = 0.0
+    x["q"] = W.f32_to_bf16_bits(qf)
+    q64, v64 = W.as_f64(x["q"], w.dtype), W.as_f64(x["v"], w.dtype)
+    ref = oracle.lsh_attention_fwd(q64, v64, x["R"].astype(np.float64), w.chunk, w.causal)
+    cfg = lsh.Config.of(w)
+    q, v = to_device(x["q"], w.dtype), to_device(x["v"], w.dtype)
+    buckets = torch.from_numpy(ref["buckets"]).cuda()
+    log("attn-edge", variant, w)
+    perm, undo, bstart = lsh.lsh_sort_permute(cfg, buckets)
+    o_r, lse_r = lsh.lsh_chunk_attn_fwd(cfg, q, v, buckets, perm, bstart)
+    out, lse = lsh.lsh_combine_rounds(cfg, o_r, lse_r, undo, torch.bfloat16)
+    torch.cuda.synchronize()
+    tol = out_tolerance(w.dtype)
+    err_or = np.abs(o_r.cpu().numpy() - ref["o_rounds"]).max()
+    print(f"{variant} causal={causal}: per-round err {err_or:.3e}")
+    assert err_or <= tol
+    assert lse_close(lse_r.cpu().numpy(), ref["lse_rounds"], w.dtype).all()
+    got = out.float().cpu().numpy()
+    assert (np.abs(got - ref["out"]) <= tol + np.abs(ref["out"]) * 2.0 ** -8).all()
+    assert lse_close(lse.cpu().numpy(), ref["lse"], w.dtype).all()
