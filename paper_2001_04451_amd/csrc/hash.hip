@@ -9,10 +9,15 @@
 //    products are exact in fp32, so the screened projection differs from the
 //    exact one by a bounded amount (residual, fp32 accumulation, and the
 //    index bits packed into the low mantissa).
+//  * R streams through LDS by direct global-to-LDS copies, 256 columns per
+//    stage, while each wave's products for the next tile are interleaved
+//    with the vector epilogue of the current one (one in-order instruction
+//    stream keeps both the matrix core and the vector ALUs busy).
 //  * Each lane keeps the two largest |projection| keys it has seen; the
-//    argmax index inside a 32-column tile rides in the low mantissa bits of
-//    the key, so one and-or, one max and one median-of-three per projection
-//    suffice, and the tile of the best key is noted once per tile.
+//    sign and the index inside a 32-column tile ride in the low bits of the
+//    key, so a rotate, an and-or, a max and a median-of-three per projection
+//    suffice, and the tile of the best key is noted once per tile.  A row's
+//    ids for all rounds are written together at the end.
 //  * If the gap between the best and second-best key cannot rule out an
 //    exchange under the error bound, the row-round is appended to a list and
 //    recomputed afterwards in fp64 by a second kernel (same products and
@@ -24,21 +29,15 @@
 namespace lsh {
 namespace {
 
-constexpr int kHashWaves = 4;
 constexpr int kRB = 2;  // 32-row blocks per wave: each staged R tile feeds 2 * 8 MFMAs
-constexpr uint32_t kKeyMask = 0x7FFFFFF0u;  // |value| with 4 index bits
-constexpr int kHashRowsPerBlock = 32 * kRB * kHashWaves;
-constexpr int kColStride = 72;                      // bf16 per staged R column (64 + pad)
-constexpr int kTilesPerStage = 2;                   // 64 R columns per LDS stage
 constexpr int kMaxColsPerLane = 8;                  // exact path: n_b/2 <= 512
 
-// One R column per block of 64 lanes (lane = t): bf16 planes hi/mid and an
-// fp32 copy, all [n_r][half_pad][64] (column contiguous, zero padded), and
-// the column's 2-norm.
+// One R column per block of 64 lanes (lane = t): bf16 planes hi/mid,
+// [n_r][half_pad][64] (column contiguous, zero padded), and the column's
+// 2-norm.
 __global__ __launch_bounds__(64) void prep_r_cols_kernel(const float* __restrict__ R, int half,
                                                          int half_pad, uint16_t* __restrict__ r_hi,
                                                          uint16_t* __restrict__ r_mid,
-                                                         float* __restrict__ r_t,
                                                          float* __restrict__ col_norm) {
     const int c = blockIdx.x, r = blockIdx.y, t = threadIdx.x;
     const float x = c < half ? R[((size_t)r * kHeadDim + t) * half + c] : 0.f;
@@ -48,7 +47,6 @@ __global__ __launch_bounds__(64) void prep_r_cols_kernel(const float* __restrict
     const size_t o = ((size_t)r * half_pad + c) * kHeadDim + t;
     r_hi[o] = (uint16_t)hi;
     r_mid[o] = (uint16_t)mid;
-    r_t[o] = x;
     float ss = x * x;
     for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
     if (t == 0) col_norm[(size_t)r * half_pad + c] = sqrtf(ss);
@@ -162,230 +160,364 @@ __global__ __launch_bounds__(kRefineThreads) void hash_refine_kernel(const void*
     }
 }
 
+// R streams through LDS in stages of 256 columns (8 tiles of 32) of one
+// round, both bf16 planes, double-buffered: 2 x 2 x 256 x 128 B = 128 KB.  A
+// stage is copied straight from global memory into LDS (global_load_lds, no
+// registers in between) while the previous one is consumed, so there is one
+// barrier per 8 tiles.  A 16-byte piece p of column c sits at slot
+// p ^ stage_swz(c) of the column's 128 bytes: the 16 columns read together
+// by one operand load then hit distinct banks.
+constexpr int kStageCols = 256;
+constexpr int kStageTiles = kStageCols / 32;
+constexpr size_t kStageBytes = 2ull * 2 * kStageCols * 128;
+
+__device__ __forceinline__ int stage_swz(int c) { return (c ^ (c >> 3)) & 7; }
+
+__device__ __forceinline__ uint32_t stage_offset(int buf, int plane, int col) {
+    return (uint32_t)(((buf * 2 + plane) * kStageCols + col) * 128);
+}
+
 struct Tile {
     f32x16 acc[kRB];
 };
 
-template <bool F32>
-__device__ __forceinline__ void tile_mfma(Tile& T, const uint16_t (*st)[kColStride],
-                                          const uint16_t (*st_mid)[kColStride], int col, int h,
-                                          const bf16x8 (&qa)[kRB][4], const bf16x8 (&qm)[kRB][4]) {
-    bf16x8 ahi[4], amid[4];
+// Keys: the projection's bit pattern rotated left by one (sign in bit 0,
+// |projection| in bits 5..31: non-negative floats order like their bits),
+// with bits 1..4 replaced by the register index j inside the tile.  Unsigned
+// order of keys is the order of |projection| truncated to 19 mantissa bits.
+// Per projection: one rotate, one and-or, one unsigned median-of-three (the
+// running second best) and one unsigned max (the running best).
+__device__ __forceinline__ uint32_t proj_key(float x, int j, uint32_t live_mask) {
+    const uint32_t u = __float_as_uint(x);
+    return (__builtin_amdgcn_alignbit(u, u, 31) & live_mask) | ((uint32_t)j << 1);
+}
+constexpr uint32_t kKeyLive = 0xFFFFFFE1u;
+
+__device__ __forceinline__ void key_update(uint32_t key, uint32_t& b, uint32_t& sc) {
+    sc = max(min(key, b), min(max(key, b), sc));  // median of three
+    b = max(key, b);
+}
+
+__device__ __forceinline__ void load_ops(u32x4 (&op)[8], const char* __restrict__ hi_base,
+                                         const char* __restrict__ mid_base, int col, int h) {
+    const int sw = stage_swz(col);
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-        ahi[s] = as_bf16x8(*reinterpret_cast<const u32x4*>(&st[col][32 * h + 8 * s]));
-        amid[s] = as_bf16x8(*reinterpret_cast<const u32x4*>(&st_mid[col][32 * h + 8 * s]));
+        const uint32_t o = (uint32_t)col * 128u + (uint32_t)(((4 * h + s) ^ sw) << 4);
+        op[2 * s] = *reinterpret_cast<const u32x4*>(hi_base + o);
+        op[2 * s + 1] = *reinterpret_cast<const u32x4*>(mid_base + o);
     }
+}
+
+// One step of the tile pipeline, in eight slices.  Slice i issues the two
+// (three for fp32 input) products of operand piece i of the tile held in
+// `op` into `nxt`, refills op[i] with the same piece of the following tile
+// (PREF), and runs one eighth of the epilogue of the previous tile `cur`
+// (EPI).  A wave issues in order, so this interleaving is what lets the
+// vector ALUs work while the matrix core runs; the scheduling barriers keep
+// the compiler from regrouping the slices.
+template <bool F32, bool PREF, bool EPI>
+__device__ __forceinline__ void tile_step(Tile& nxt, u32x4 (&op)[8], const char* __restrict__ hi_base,
+                                          const char* __restrict__ mid_base, int col_pref, int h,
+                                          const bf16x8 (&qa)[kRB][4], const bf16x8 (&qm)[kRB][4],
+                                          const Tile& cur, int tile_cur, bool live,
+                                          uint32_t (&best)[kRB], uint32_t (&second)[kRB],
+                                          int (&best_tile)[kRB]) {
+    static_assert(kRB == 2, "slices written for two row blocks");
+    const int sw = stage_swz(col_pref);
+    uint32_t b[kRB] = {best[0], best[1]}, sc[kRB] = {second[0], second[1]};
+    const uint32_t mask = live ? kKeyLive : 0u;
 #pragma unroll
-    for (int rb = 0; rb < kRB; ++rb) T.acc[rb] = f32x16{};
+    for (int i = 0; i < 8; ++i) {
+        __builtin_amdgcn_sched_barrier(0);
+        const int s = i >> 1;
+        const bf16x8 a = as_bf16x8(op[i]);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-#pragma unroll
-        for (int rb = 0; rb < kRB; ++rb) T.acc[rb] = mfma32x32x16(ahi[s], qa[rb][s], T.acc[rb]);
-#pragma unroll
-        for (int rb = 0; rb < kRB; ++rb) T.acc[rb] = mfma32x32x16(amid[s], qa[rb][s], T.acc[rb]);
+        for (int rb = 0; rb < kRB; ++rb)
+            nxt.acc[rb] = mfma32x32x16(a, qa[rb][s], i == 0 ? f32x16{} : nxt.acc[rb]);
         if constexpr (F32) {
+            if ((i & 1) == 0) {
 #pragma unroll
-            for (int rb = 0; rb < kRB; ++rb) T.acc[rb] = mfma32x32x16(ahi[s], qm[rb][s], T.acc[rb]);
+                for (int rb = 0; rb < kRB; ++rb) nxt.acc[rb] = mfma32x32x16(a, qm[rb][s], nxt.acc[rb]);
+            }
+        }
+        if constexpr (PREF) {
+            const uint32_t o = (uint32_t)col_pref * 128u + (uint32_t)(((4 * h + s) ^ sw) << 4);
+            op[i] = *reinterpret_cast<const u32x4*>(((i & 1) ? mid_base : hi_base) + o);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (EPI) {
+#pragma unroll
+            for (int rb = 0; rb < kRB; ++rb)
+#pragma unroll
+                for (int jj = 0; jj < 2; ++jj) {
+                    const int j = 2 * i + jj;
+                    key_update(proj_key(cur.acc[rb][j], j, mask), b[rb], sc[rb]);
+                }
+        }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (EPI) {
+#pragma unroll
+        for (int rb = 0; rb < kRB; ++rb) {
+            best_tile[rb] = b[rb] != best[rb] ? tile_cur : best_tile[rb];
+            best[rb] = b[rb];
+            second[rb] = sc[rb];
         }
     }
 }
 
-// Keys are |projection| bit patterns (non-negative floats order like their
-// bits as unsigned integers) with the low 4 mantissa bits replaced by the
-// register index j inside the tile: one and-or, one unsigned median-of-three
-// and one unsigned max per projection.  The tile holding the best key is
-// recorded when the running best changes during the tile.
-__device__ __forceinline__ void tile_epilogue(const Tile& T, int tile, uint32_t (&best)[kRB],
+__device__ __forceinline__ void tile_epilogue(const Tile& T, int tile, bool live, uint32_t (&best)[kRB],
                                               uint32_t (&second)[kRB], int (&best_tile)[kRB]) {
+    const uint32_t mask = live ? kKeyLive : 0u;
 #pragma unroll
     for (int rb = 0; rb < kRB; ++rb) {
         uint32_t b = best[rb], sc = second[rb];
-        const uint32_t b0 = b;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            const uint32_t key = (__float_as_uint(T.acc[rb][j]) & kKeyMask) | (uint32_t)j;
-            sc = max(min(key, b), min(max(key, b), sc));  // median of three
-            b = max(key, b);
-        }
-        best_tile[rb] = b != b0 ? tile : best_tile[rb];
+        for (int j = 0; j < 16; ++j) key_update(proj_key(T.acc[rb][j], j, mask), b, sc);
+        best_tile[rb] = b != best[rb] ? tile : best_tile[rb];
         best[rb] = b;
         second[rb] = sc;
     }
 }
 
-template <bool F32>
-__global__ __launch_bounds__(256, 2) void hash_kernel(
+// Copy global stage g (round g / spr, columns (g % spr) * 256 ...) into
+// buffer buf.  Each wave moves whole 1 KB runs of 8 columns of one plane.
+template <int WAVES>
+__device__ __forceinline__ void load_stage(char* smem, int buf, int g, int spr, int half_pad,
+                                           const uint16_t* __restrict__ r_hi,
+                                           const uint16_t* __restrict__ r_mid, int wave, int lane) {
+    constexpr int kRuns = 2 * kStageCols / 8;  // 1 KB runs per stage
+    static_assert(kRuns % WAVES == 0, "runs split evenly over the waves");
+    const int r = g / spr, st = g % spr;
+    const int cl_lane = lane >> 3, slot = lane & 7;
+#pragma unroll
+    for (int i = 0; i < kRuns / WAVES; ++i) {
+        const int run = wave * (kRuns / WAVES) + i;
+        const int plane = run / (kStageCols / 8);
+        const int c0 = (run % (kStageCols / 8)) * 8;
+        const int c = c0 + cl_lane;
+        int gcol = st * kStageCols + c;
+        gcol = gcol < half_pad ? gcol : 0;  // past the round: any valid address, never read
+        const uint16_t* src = (plane ? r_mid : r_hi) +
+                              ((size_t)r * half_pad + gcol) * kHeadDim + (slot ^ stage_swz(c)) * 8;
+        __builtin_amdgcn_global_load_lds(
+            (const __attribute__((address_space(1))) void*)src,
+            (__attribute__((address_space(3))) void*)(smem + stage_offset(buf, plane, c0)), 16, 0, 0);
+    }
+}
+
+// Winner of a row-round as kept in LDS until the row's ids are written:
+// the bucket id, or kUnsettled when the exact pass must decide.
+constexpr uint16_t kUnsettled = 0xFFFFu;
+
+// A wave owns PAIRS pairs of 32-row blocks (64 * PAIRS rows); every staged
+// tile is swept once per pair, so a stage feeds PAIRS times as many products.
+template <bool F32, int WAVES, int PAIRS>
+__global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
     const void* __restrict__ q, int64_t rows, int n_r, int half, int half_pad,
     const uint16_t* __restrict__ r_hi, const uint16_t* __restrict__ r_mid,
-    const float* __restrict__ r_t, const float* __restrict__ col_norm_max, float err_sum,
-    float err_pack, int32_t* __restrict__ buckets, int* __restrict__ refine_lists,
-    int* __restrict__ refine_counts) {
-    // [buf][plane][column][k]
-    __shared__ __attribute__((aligned(16))) uint16_t stage[2][2][kTilesPerStage * 32][kColStride];
+    const float* __restrict__ col_norm_max, float err_sum, float err_pack,
+    int32_t* __restrict__ buckets, int* __restrict__ refine_lists, int* __restrict__ refine_counts) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    constexpr int kWaveRows = 64 * PAIRS;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6, h = lane >> 5, n = lane & 31;
-    const int64_t row0 = (int64_t)blockIdx.x * kHashRowsPerBlock + wave * (32 * kRB);
+    const int64_t row0 = (int64_t)blockIdx.x * (WAVES * kWaveRows) + wave * kWaveRows;
+    const int tpr = half_pad / 32;                         // tiles per round
+    const int spr = (tpr + kStageTiles - 1) / kStageTiles;  // stages per round
+    const int n_stages = n_r * spr;
+    // this wave's winners: [row in wave][round]
+    uint16_t* win = reinterpret_cast<uint16_t*>(smem + kStageBytes) + (size_t)wave * kWaveRows * n_r;
+
+    load_stage<WAVES>(smem, 0, 0, spr, half_pad, r_hi, r_mid, wave, lane);
 
     // Queries as the B operand: lane holds row (n) and k = 32h + 8s + e, s = 0..3.
-    bf16x8 qa[kRB][4];
-    bf16x8 qm[kRB][4];  // fp32 input: second bf16 plane of q
-    float qn[kRB];
+    bf16x8 qa[PAIRS][kRB][4];
+    bf16x8 qm[PAIRS][kRB][4];  // fp32 input: second bf16 plane of q
+    float qn[PAIRS][kRB];
 #pragma unroll
-    for (int rb = 0; rb < kRB; ++rb) {
-        const int64_t row = row0 + rb * 32 + n;
-        const bool valid = row < rows;
-        float ss = 0.f;
-        if constexpr (F32) {
-            const float* src = static_cast<const float*>(q) + row * kHeadDim + 32 * h;
+    for (int pr = 0; pr < PAIRS; ++pr)
 #pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                f32x4 x0 = valid ? *reinterpret_cast<const f32x4*>(src + 8 * s) : f32x4{0, 0, 0, 0};
-                f32x4 x1 = valid ? *reinterpret_cast<const f32x4*>(src + 8 * s + 4) : f32x4{0, 0, 0, 0};
-                float xs[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-                u32x4 hi, mid;
+        for (int rb = 0; rb < kRB; ++rb) {
+            const int64_t row = row0 + pr * 64 + rb * 32 + n;
+            const bool valid = row < rows;
+            float ss = 0.f;
+            if constexpr (F32) {
+                const float* src = static_cast<const float*>(q) + row * kHeadDim + 32 * h;
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const uint32_t h0 = f32_to_bf16_bits(xs[2 * e]), h1 = f32_to_bf16_bits(xs[2 * e + 1]);
-                    const uint32_t m0 = f32_to_bf16_bits(xs[2 * e] - bf16_bits_to_f32(h0));
-                    const uint32_t m1 = f32_to_bf16_bits(xs[2 * e + 1] - bf16_bits_to_f32(h1));
-                    hi[e] = h0 | (h1 << 16);
-                    mid[e] = m0 | (m1 << 16);
-                    ss = fmaf(xs[2 * e], xs[2 * e], ss);
-                    ss = fmaf(xs[2 * e + 1], xs[2 * e + 1], ss);
+                for (int s = 0; s < 4; ++s) {
+                    f32x4 x0 = valid ? *reinterpret_cast<const f32x4*>(src + 8 * s) : f32x4{0, 0, 0, 0};
+                    f32x4 x1 = valid ? *reinterpret_cast<const f32x4*>(src + 8 * s + 4) : f32x4{0, 0, 0, 0};
+                    float xs[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+                    u32x4 hi, mid;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const uint32_t h0 = f32_to_bf16_bits(xs[2 * e]), h1 = f32_to_bf16_bits(xs[2 * e + 1]);
+                        const uint32_t m0 = f32_to_bf16_bits(xs[2 * e] - bf16_bits_to_f32(h0));
+                        const uint32_t m1 = f32_to_bf16_bits(xs[2 * e + 1] - bf16_bits_to_f32(h1));
+                        hi[e] = h0 | (h1 << 16);
+                        mid[e] = m0 | (m1 << 16);
+                        ss = fmaf(xs[2 * e], xs[2 * e], ss);
+                        ss = fmaf(xs[2 * e + 1], xs[2 * e + 1], ss);
+                    }
+                    qa[pr][rb][s] = as_bf16x8(hi);
+                    qm[pr][rb][s] = as_bf16x8(mid);
                 }
-                qa[rb][s] = as_bf16x8(hi);
-                qm[rb][s] = as_bf16x8(mid);
-            }
-        } else {
-            const uint16_t* src = static_cast<const uint16_t*>(q) + row * kHeadDim + 32 * h;
+            } else {
+                const uint16_t* src = static_cast<const uint16_t*>(q) + row * kHeadDim + 32 * h;
 #pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const u32x4 raw = valid ? *reinterpret_cast<const u32x4*>(src + 8 * s) : u32x4{0, 0, 0, 0};
+                for (int s = 0; s < 4; ++s) {
+                    const u32x4 raw = valid ? *reinterpret_cast<const u32x4*>(src + 8 * s) : u32x4{0, 0, 0, 0};
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float a = __uint_as_float(raw[e] << 16), b = __uint_as_float(raw[e] & 0xFFFF0000u);
-                    ss = fmaf(a, a, ss);
-                    ss = fmaf(b, b, ss);
+                    for (int e = 0; e < 4; ++e) {
+                        const float a = __uint_as_float(raw[e] << 16), b = __uint_as_float(raw[e] & 0xFFFF0000u);
+                        ss = fmaf(a, a, ss);
+                        ss = fmaf(b, b, ss);
+                    }
+                    qa[pr][rb][s] = as_bf16x8(raw);
+                    qm[pr][rb][s] = as_bf16x8(u32x4{0, 0, 0, 0});
                 }
-                qa[rb][s] = as_bf16x8(raw);
-                qm[rb][s] = as_bf16x8(u32x4{0, 0, 0, 0});
             }
+            ss += __shfl_xor(ss, 32);
+            qn[pr][rb] = sqrtf(ss);
         }
-        ss += __shfl_xor(ss, 32);
-        qn[rb] = sqrtf(ss);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+
+    uint32_t best[PAIRS][kRB], second[PAIRS][kRB];
+    int best_tile[PAIRS][kRB];
+    for (int g = 0; g < n_stages; ++g) {
+        const int r = g / spr, st = g % spr, buf = g & 1;
+        if (st == 0) {
+#pragma unroll
+            for (int pr = 0; pr < PAIRS; ++pr)
+#pragma unroll
+                for (int rb = 0; rb < kRB; ++rb) {
+                    best[pr][rb] = second[pr][rb] = 0u;
+                    best_tile[pr][rb] = 0;
+                }
+        }
+        // the next stage lands in the other buffer while this one computes
+        if (g + 1 < n_stages)
+            load_stage<WAVES>(smem, buf ^ 1, g + 1, spr, half_pad, r_hi, r_mid, wave, lane);
+        const char* hi_base = smem + stage_offset(buf, 0, 0);
+        const char* mid_base = smem + stage_offset(buf, 1, 0);
+        const int nt = min(kStageTiles, tpr - st * kStageTiles);
+        const int t0 = st * kStageTiles;
+        // Every stage runs all eight tiles; tiles past the round (a last,
+        // partial stage) compute on stale LDS and their keys are masked to
+        // (near) zero, so they can only win when every key is tiny, and such
+        // a row is flagged and settled exactly.
+        static_assert(kStageTiles == 8, "pipeline written for eight tiles per stage");
+#pragma unroll 1
+        for (int pr = 0; pr < PAIRS; ++pr) {
+            // the pair's operands and running state, selected without indexing
+            bf16x8 qc[kRB][4], qmc[kRB][4];
+            uint32_t bc[kRB], sc[kRB];
+            int tc[kRB];
+#pragma unroll
+            for (int rb = 0; rb < kRB; ++rb) {
+#pragma unroll
+                for (int s4 = 0; s4 < 4; ++s4) {
+                    qc[rb][s4] = qa[0][rb][s4];
+                    qmc[rb][s4] = qm[0][rb][s4];
+#pragma unroll
+                    for (int o = 1; o < PAIRS; ++o)
+                        if (pr == o) {
+                            qc[rb][s4] = qa[o][rb][s4];
+                            qmc[rb][s4] = qm[o][rb][s4];
+                        }
+                }
+                bc[rb] = best[0][rb];
+                sc[rb] = second[0][rb];
+                tc[rb] = best_tile[0][rb];
+#pragma unroll
+                for (int o = 1; o < PAIRS; ++o)
+                    if (pr == o) {
+                        bc[rb] = best[o][rb];
+                        sc[rb] = second[o][rb];
+                        tc[rb] = best_tile[o][rb];
+                    }
+            }
+            Tile ta, tb;
+            u32x4 op[8];
+            load_ops(op, hi_base, mid_base, n, h);
+            tile_step<F32, true, false>(ta, op, hi_base, mid_base, 32 + n, h, qc, qmc, tb, 0, false,
+                                        bc, sc, tc);
+#pragma unroll 1
+            for (int t = 1; t < kStageTiles - 1; t += 2) {
+                tile_step<F32, true, true>(tb, op, hi_base, mid_base, 32 * (t + 1) + n, h, qc, qmc,
+                                           ta, t0 + t - 1, t - 1 < nt, bc, sc, tc);
+                tile_step<F32, true, true>(ta, op, hi_base, mid_base, 32 * (t + 2) + n, h, qc, qmc,
+                                           tb, t0 + t, t < nt, bc, sc, tc);
+            }
+            tile_step<F32, false, true>(tb, op, hi_base, mid_base, 0, h, qc, qmc, ta, t0 + 6, 6 < nt,
+                                        bc, sc, tc);
+            tile_epilogue(tb, t0 + 7, 7 < nt, bc, sc, tc);
+#pragma unroll
+            for (int o = 0; o < PAIRS; ++o)
+                if (pr == o) {
+#pragma unroll
+                    for (int rb = 0; rb < kRB; ++rb) {
+                        best[o][rb] = bc[rb];
+                        second[o][rb] = sc[rb];
+                        best_tile[o][rb] = tc[rb];
+                    }
+                }
+        }
+
+        if (st == spr - 1) {
+            // Round epilogue: merge the two lane halves (different columns of
+            // the same row) and decide; lane half h keeps row block h's result.
+            const float cn = col_norm_max[r];
+#pragma unroll
+            for (int pr = 0; pr < PAIRS; ++pr)
+#pragma unroll
+                for (int rb = 0; rb < kRB; ++rb) {
+                    const uint32_t bb = best[pr][rb], ss2 = second[pr][rb];
+                    const uint32_t bp = __shfl_xor(bb, 32), sp = __shfl_xor(ss2, 32);
+                    const int tp = __shfl_xor(best_tile[pr][rb], 32);
+                    const bool mine = bb > bp || (bb == bp && h == 0);
+                    const uint32_t bk = mine ? bb : bp;
+                    const uint32_t sk = max(min(bb, bp), max(ss2, sp));
+                    const float b1 = __uint_as_float((bk >> 1) & 0x7FFFFFF0u);
+                    const float s1 = __uint_as_float((sk >> 1) & 0x7FFFFFF0u);
+                    const int hw = mine ? h : (h ^ 1);
+                    const int tw = mine ? best_tile[pr][rb] : tp;
+                    const uint32_t j = (bk >> 1) & 15u;
+                    const int col = tw * 32 + 8 * (int)(j >> 2) + 4 * hw + (int)(j & 3u);
+                    // Every screened key is within eps = err_sum*|q|*max|R_c| + err_pack*key
+                    // of its exact |projection|; an exchange of winners needs a gap <= 2 eps.
+                    // When the gap is larger the winner's magnitude exceeds eps, so the
+                    // screened sign (bit 0 of the key) is the exact one.
+                    const float thr = 2.04f * (err_sum * qn[pr][rb] * cn + err_pack * b1);
+                    const bool flag = !(b1 - s1 > thr) || col >= half;
+                    const int id = (bk & 1u) ? half + col : col;
+                    if (rb == h) win[(pr * 64 + rb * 32 + n) * n_r + r] = flag ? kUnsettled : (uint16_t)id;
+                }
+        }
+        // the next stage has landed and every wave is done with this buffer
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
     }
 
-    const int n_tiles = half_pad / 32;
-    const int cols_per_stage = kTilesPerStage * 32;
-    const int n_stages = (half_pad + cols_per_stage - 1) / cols_per_stage;
-    constexpr int kLoads = 2 * kTilesPerStage * 32 * 8 / 256;  // 16-byte pieces per thread
-
-    for (int r = 0; r < n_r; ++r) {
-        const uint16_t* hi_r = r_hi + (size_t)r * half_pad * kHeadDim;
-        const uint16_t* mid_r = r_mid + (size_t)r * half_pad * kHeadDim;
-        uint32_t best[kRB], second[kRB];
-        int best_tile[kRB];
+    // Write each row's ids (contiguous) and queue the unsettled row-rounds.
 #pragma unroll
-        for (int rb = 0; rb < kRB; ++rb) {
-            best[rb] = second[rb] = 0u;
-            best_tile[rb] = 0;
-        }
-
-        u32x4 pre[kLoads];
-        auto gload = [&](int st) {
-#pragma unroll
-            for (int i = 0; i < kLoads; ++i) {
-                const int idx = tid + 256 * i;
-                const int plane = idx / (cols_per_stage * 8);
-                const int col = (idx >> 3) % cols_per_stage, part = idx & 7;
-                const int gcol = st * cols_per_stage + col;
-                const uint16_t* base = plane ? mid_r : hi_r;
-                pre[i] = gcol < half_pad
-                             ? *reinterpret_cast<const u32x4*>(base + (size_t)gcol * kHeadDim + part * 8)
-                             : u32x4{0, 0, 0, 0};
-            }
-        };
-        auto lstore = [&](int buf) {
-#pragma unroll
-            for (int i = 0; i < kLoads; ++i) {
-                const int idx = tid + 256 * i;
-                const int plane = idx / (cols_per_stage * 8);
-                const int col = (idx >> 3) % cols_per_stage, part = idx & 7;
-                *reinterpret_cast<u32x4*>(&stage[buf][plane][col][part * 8]) = pre[i];
-            }
-        };
-
-        gload(0);
-        lstore(0);
-        __syncthreads();
-        for (int st = 0; st < n_stages; ++st) {
-            if (st + 1 < n_stages) gload(st + 1);
-            const int buf = st & 1;
-            const int t0 = st * kTilesPerStage;
-            const int nt = min(kTilesPerStage, n_tiles - t0);
-            // The second tile's MFMAs are issued before the first tile's
-            // epilogue, so the matrix core and the vector ALUs overlap inside
-            // the wave; the two waves sharing a SIMD overlap the rest.
-            static_assert(kTilesPerStage == 2, "pipeline written for two tiles per stage");
-            Tile ta, tb;
-            tile_mfma<F32>(ta, stage[buf][0], stage[buf][1], n, h, qa, qm);
-            if (nt > 1) tile_mfma<F32>(tb, stage[buf][0], stage[buf][1], 32 + n, h, qa, qm);
-            tile_epilogue(ta, t0, best, second, best_tile);
-            if (nt > 1) tile_epilogue(tb, t0 + 1, best, second, best_tile);
-            if (st + 1 < n_stages) lstore((st + 1) & 1);
-            __syncthreads();
-        }
-
-        // Round epilogue: merge the two lane halves (different columns of the
-        // same row), decide, and queue close calls for the exact pass.
-        const float cn = col_norm_max[r];
-        const float* r_t_round = r_t + (size_t)r * half_pad * kHeadDim;
-        int* list = refine_lists + rows * r;
-#pragma unroll
-        for (int rb = 0; rb < kRB; ++rb) {
-            const int64_t row = row0 + rb * 32 + n;
-            const bool valid = row < rows;
-            const uint32_t bp = __shfl_xor(best[rb], 32), sp = __shfl_xor(second[rb], 32);
-            const int tp = __shfl_xor(best_tile[rb], 32);
-            const bool mine = best[rb] > bp || (best[rb] == bp && h == 0);
-            const uint32_t bk = mine ? best[rb] : bp;
-            const float b1 = __uint_as_float(bk);
-            const float s1 = __uint_as_float(max(min(best[rb], bp), max(second[rb], sp)));
-            const int hw = mine ? h : (h ^ 1);
-            const int tw = mine ? best_tile[rb] : tp;
-            const uint32_t j = bk & 15u;
-            const int col = tw * 32 + 8 * (int)(j >> 2) + 4 * hw + (int)(j & 3u);
-            // Every screened key is within eps = err_sum*|q|*max|R_c| + err_pack*key
-            // of its exact |projection|; an exchange of winners needs a gap <= 2 eps.
-            const float thr = 2.04f * (err_sum * qn[rb] * cn + err_pack * b1);
-            const bool flag = !(b1 - s1 > thr) || col >= half;
-            // Sign of the winning projection.  When the row is not flagged its
-            // magnitude exceeds the error bound, so fp32 gets the sign right.
-            const int colc = col < half ? col : 0;
-            const f32x4* rt = reinterpret_cast<const f32x4*>(r_t_round + (size_t)colc * kHeadDim + 32 * h);
-            float part = 0.f;
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const f32x4 ra = rt[2 * s], rb4 = rt[2 * s + 1];
-                const float rv[8] = {ra[0], ra[1], ra[2], ra[3], rb4[0], rb4[1], rb4[2], rb4[3]};
-                const u32x4 w = __builtin_bit_cast(u32x4, qa[rb][s]);
-                const u32x4 m = __builtin_bit_cast(u32x4, qm[rb][s]);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float lo = __uint_as_float(w[e] << 16) + __uint_as_float(m[e] << 16);
-                    const float hi = __uint_as_float(w[e] & 0xFFFF0000u) + __uint_as_float(m[e] & 0xFFFF0000u);
-                    part = fmaf(lo, rv[2 * e], part);
-                    part = fmaf(hi, rv[2 * e + 1], part);
-                }
-            }
-            const float p = part + __shfl_xor(part, 32);
-            const bool queue = flag && valid && h == 0;
-            if (valid && h == 0 && !flag) buckets[row * n_r + r] = p > 0.f ? col : half + col;
+    for (int pr = 0; pr < PAIRS; ++pr) {
+        const int64_t row = row0 + pr * 64 + h * 32 + n;
+        const bool valid = row < rows;
+        const uint16_t* w = win + (pr * 64 + h * 32 + n) * n_r;
+        int32_t* out = buckets + row * n_r;
+        for (int r = 0; r < n_r; ++r) {
+            const uint16_t id = w[r];
+            const bool queue = valid && id == kUnsettled;
+            if (valid) out[r] = id == kUnsettled ? 0 : (int32_t)id;
             // wave-aggregated append to this round's refinement list
             const uint64_t qmask = __ballot(queue);
             if (qmask) {
+                int* list = refine_lists + rows * r;
                 const int leader = __ffsll((unsigned long long)qmask) - 1;
                 int slot0 = 0;
                 if (lane == leader) slot0 = atomicAdd(&refine_counts[r], __popcll(qmask));
@@ -399,7 +531,6 @@ __global__ __launch_bounds__(256, 2) void hash_kernel(
 struct HashWs {
     uint16_t* r_hi;
     uint16_t* r_mid;
-    float* r_t;
     float* col_norm;
     float* col_norm_max;
     int* count;
@@ -416,8 +547,6 @@ HashWs carve(void* base, int64_t rows, int n_rounds, int half_pad) {
     off += align256(per * 2);
     w.r_mid = reinterpret_cast<uint16_t*>(p + off);
     off += align256(per * 2);
-    w.r_t = reinterpret_cast<float*>(p + off);
-    off += align256(per * 4);
     w.col_norm = reinterpret_cast<float*>(p + off);
     off += align256((size_t)n_rounds * half_pad * 4);
     w.col_norm_max = reinterpret_cast<float*>(p + off);
@@ -444,7 +573,7 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
     const HashWs w = carve(workspace, rows, n_rounds, half_pad);
 
     prep_r_cols_kernel<<<dim3(half_pad, n_rounds), 64, 0, stream>>>(R, half, half_pad, w.r_hi,
-                                                                     w.r_mid, w.r_t, w.col_norm);
+                                                                     w.r_mid, w.col_norm);
     prep_r_max_kernel<<<n_rounds, 256, 0, stream>>>(w.col_norm, half_pad, w.col_norm_max, w.count);
     if (rows == 0) return hipGetLastError();
 
@@ -459,23 +588,31 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
     const float err_sum = (float)((resid + adds * 0x1p-23) * 1.01);
     const float err_pack = (float)0x1p-19;
 
-    const unsigned grid = (unsigned)((rows + kHashRowsPerBlock - 1) / kHashRowsPerBlock);
+    constexpr int kWaves = 8, kPairsBf16 = 1, kPairsF32 = 1;
+    const int64_t rows_per_block = kWaves * 64 * (f32 ? kPairsF32 : kPairsBf16);
+    const unsigned grid = (unsigned)((rows + rows_per_block - 1) / rows_per_block);
     const size_t refine_lds = (size_t)kHeadDim * half * sizeof(float);
     // Refinement blocks per round: one 128 KB-LDS block per CU over all rounds
     // (a typical list holds well under 1% of the rows; longer ones are strided).
     const unsigned refine_blocks =
         (unsigned)std::max<int64_t>(1, std::min<int64_t>((256 + n_rounds - 1) / n_rounds, rows / 1024));
     if (f32) {
-        hash_kernel<true><<<grid, 256, 0, stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi,
-                                                     w.r_mid, w.r_t, w.col_norm_max, err_sum,
+        const size_t lds = kStageBytes + (size_t)rows_per_block * n_rounds * 2;
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&hash_kernel<true, kWaves, kPairsF32>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hash_kernel<true, kWaves, kPairsF32><<<grid, kWaves * 64, lds, stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi,
+                                                     w.r_mid, w.col_norm_max, err_sum,
                                                      err_pack, buckets, w.list, w.count);
         hipFuncSetAttribute(reinterpret_cast<const void*>(&hash_refine_kernel<true>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)refine_lds);
         hash_refine_kernel<true><<<dim3(refine_blocks, n_rounds), kRefineThreads, refine_lds, stream>>>(
             q, R, half, n_rounds, rows, w.list, w.count, buckets);
     } else {
-        hash_kernel<false><<<grid, 256, 0, stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi,
-                                                      w.r_mid, w.r_t, w.col_norm_max, err_sum,
+        const size_t lds = kStageBytes + (size_t)rows_per_block * n_rounds * 2;
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&hash_kernel<false, kWaves, kPairsBf16>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hash_kernel<false, kWaves, kPairsBf16><<<grid, kWaves * 64, lds, stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi,
+                                                      w.r_mid, w.col_norm_max, err_sum,
                                                       err_pack, buckets, w.list, w.count);
         hipFuncSetAttribute(reinterpret_cast<const void*>(&hash_refine_kernel<false>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)refine_lds);
