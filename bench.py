@@ -45,13 +45,13 @@ def algorithmic_work(w: W.Workload) -> dict:
         "hash_flop": rr * d * w.n_buckets,
         # QK^T and PV over a 2m-key window: 2 * (2m * d) * 2 flops per row-round
         "attn_flop": rr * 8 * m * d,
-        # q and v rows read once per round (gathered), o_rounds row (fp32) and
+        # q and v rows read once per round (gathered), o_rounds row (dtype) and
         # lse written, ids/positions read
-        "attn_bytes": rr * (2 * d * e + 4 * d + 4 + 3 * 4),
+        "attn_bytes": rr * (2 * d * e + e * d + 4 + 3 * 4),
         # ids read twice, perm and undo written
         "sort_bytes": rr * 16,
-        # per row: n_r o_rounds rows (fp32) + lse + undo read, one output row written
-        "combine_bytes": rows * (n_r * (4 * d + 8) + d * e + 4),
+        # per row: n_r o_rounds rows (dtype) + lse + undo read, one output row written
+        "combine_bytes": rows * (n_r * (e * d + 8) + d * e + 4),
     }
 
 
@@ -73,7 +73,7 @@ def run_gpu(w: W.Workload, steps: int, warmup: int) -> dict:
     perm = torch.empty((B, H, nr, L), dtype=torch.int32, device=dev)
     undo = torch.empty_like(perm)
     bstart = torch.empty((B, H, nr, nb + 1), dtype=torch.int32, device=dev)
-    o_r = torch.empty((B, H, nr, L, d), dtype=torch.float32, device=dev)
+    o_r = torch.empty((B, H, nr, L, d), dtype=tdt, device=dev)
     lse_r = torch.empty((B, H, nr, L), dtype=torch.float32, device=dev)
     out = torch.empty((B, H, L, d), dtype=tdt, device=dev)
     lse = torch.empty((B, H, L), dtype=torch.float32, device=dev)

@@ -22,7 +22,7 @@
  *                                                   undo: position -> sorted slot
  *   bucket_start      [B][H][n_rounds][n_buckets+1] int32: first sorted slot of
  *                     each bucket, last entry = L
- *   o_rounds          [B][H][n_rounds][L][d] fp32, sorted-slot order
+ *   o_rounds          [B][H][n_rounds][L][d] dtype of the call, sorted-slot order
  *   lse_rounds        [B][H][n_rounds][L]    fp32, sorted-slot order
  *   out               [B][H][L][d]        dtype of the call
  *   lse_total         [B][H][L]           fp32
@@ -135,20 +135,23 @@ int lsh_gather_rows(const lsh_config *cfg, lsh_dtype dtype, const void *src,
  * rounds in which j shares i's bucket).
  *   q, v          [B][H][L][d] (dtype), in original position order
  *   buckets, perm, bucket_start: as written by lsh_hash / lsh_sort_permute
- *   o_rounds      [B][H][n_rounds][L][d] fp32 (written, sorted order)
+ *   o_rounds      [B][H][n_rounds][L][d] (dtype, written, sorted order): each
+ *                 round's output is normalised and accumulated in fp32, then
+ *                 stored in the call's dtype
  *   lse_rounds    [B][H][n_rounds][L] fp32 (written, sorted order) */
 int lsh_chunk_attn_fwd(const lsh_config *cfg, lsh_dtype dtype, const void *q, const void *v,
                        const int32_t *buckets, const int32_t *perm,
-                       const int32_t *bucket_start, float *o_rounds, float *lse_rounds,
+                       const int32_t *bucket_start, void *o_rounds, float *lse_rounds,
                        void *stream);
 
 /* Undo the sort and combine the rounds (App. A):
  *   z_i = log sum_r exp z_r(i),  out_i = sum_r exp(z_r(i) - z_i) o_r(i).
- *   o_rounds, lse_rounds: as written by lsh_chunk_attn_fwd
+ *   o_rounds, lse_rounds: as written by lsh_chunk_attn_fwd (o_rounds in dtype);
+ *                 the weighted sum is formed in fp32
  *   undo          [B][H][n_rounds][L] int32
  *   out           [B][H][L][d] (dtype, written)
  *   lse_total     [B][H][L] fp32 (written; may be NULL) */
-int lsh_combine_rounds(const lsh_config *cfg, lsh_dtype dtype, const float *o_rounds,
+int lsh_combine_rounds(const lsh_config *cfg, lsh_dtype dtype, const void *o_rounds,
                        const float *lse_rounds, const int32_t *undo, void *out,
                        float *lse_total, void *stream);
 

@@ -215,7 +215,7 @@ template <int NW, bool CAUSAL>
 __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ v,
     const int32_t* __restrict__ buckets, const int32_t* __restrict__ perm,
-    const int32_t* __restrict__ bstart, float* __restrict__ o_rounds,
+    const int32_t* __restrict__ bstart, uint16_t* __restrict__ o_rounds,
     float* __restrict__ lse_rounds, int L, int n_r, int n_b, float scale, float self_mask,
     int pairs_per_strip) {
     __shared__ __attribute__((aligned(16))) FwdShared<NW> S;
@@ -365,24 +365,26 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
             lsum += __shfl_xor(lsum, 32);
             const bool alone = !(lsum > 0.f);  // only itself left as a target
             const float mref = fast ? bound : m;
-            float* orow = o_rounds + (seg * L + s_q) * kHeadDim;
+            uint16_t* orow = o_rounds + (seg * L + s_q) * kHeadDim;
             const float inv = alone ? 0.f : 1.f / lsum;
 #pragma unroll
             for (int dt = 0; dt < 2; ++dt)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int d0 = 32 * dt + 8 * i + 4 * h;
-                    f32x4 o;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) o[e] = oacc[dt][4 * i + e] * inv;
-                    if (alone) {
-                        const int kq = qh * 32 + n + ((cq + 3) % 3) * kChunk;
+                    uint2 o;
+                    if (alone) {  // v_i itself, copied bit for bit
+                        uint32_t e4[4];
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            o[e] = bf16_bits_to_f32(*reinterpret_cast<const uint16_t*>(
-                                S.Vt + vt_offset(d0 + e, kq & ~3) + (kq & 3) * 2));
+                            e4[e] = *reinterpret_cast<const uint16_t*>(S.Vt + vt_offset(d0 + e, rq & ~3) + (rq & 3) * 2);
+                        o.x = e4[0] | (e4[1] << 16);
+                        o.y = e4[2] | (e4[3] << 16);
+                    } else {
+                        o.x = pack_bf16x2(oacc[dt][4 * i] * inv, oacc[dt][4 * i + 1] * inv);
+                        o.y = pack_bf16x2(oacc[dt][4 * i + 2] * inv, oacc[dt][4 * i + 3] * inv);
                     }
-                    *reinterpret_cast<f32x4*>(orow + d0) = o;
+                    *reinterpret_cast<uint2*>(orow + d0) = o;
                 }
             if (h == 0) {
                 // z = scale*|q_i| - self_mask when the token is its own only target
@@ -480,7 +482,7 @@ __global__ __launch_bounds__(64) void attn_fwd_f32_kernel(
 
 template <int NW>
 hipError_t launch_bf16(dim3 grid, bool causal, const uint16_t* q, const uint16_t* v,
-                       const int32_t* buckets, const int32_t* perm, const int32_t* bs, float* o,
+                       const int32_t* buckets, const int32_t* perm, const int32_t* bs, uint16_t* o,
                        float* lse, int L, int n_r, int n_b, float scale, float self_mask, int pps,
                        hipStream_t stream) {
     if (causal)
@@ -497,14 +499,15 @@ hipError_t launch_bf16(dim3 grid, bool causal, const uint16_t* q, const uint16_t
 hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, bool causal,
                            float scale, float self_mask, bool f32, const void* q, const void* v,
                            const int32_t* buckets, const int32_t* perm,
-                           const int32_t* bucket_start, float* o_rounds, float* lse_rounds,
+                           const int32_t* bucket_start, void* o_rounds, float* lse_rounds,
                            hipStream_t stream) {
     if (BH == 0 || L == 0) return hipSuccess;
     const unsigned segs = (unsigned)(BH * n_rounds);
     if (f32) {
         attn_fwd_f32_kernel<<<dim3(L / kChunk, segs), 64, 0, stream>>>(
             static_cast<const float*>(q), static_cast<const float*>(v), buckets, perm, bucket_start,
-            o_rounds, lse_rounds, L, n_rounds, n_buckets, causal ? 1 : 0, scale, self_mask);
+            static_cast<float*>(o_rounds), lse_rounds, L, n_rounds, n_buckets, causal ? 1 : 0, scale,
+            self_mask);
         return hipGetLastError();
     }
     // Strips of chunk pairs: long enough to reuse the shared chunk between
@@ -515,10 +518,11 @@ hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, bool 
     const dim3 grid((unsigned)((n_pairs + pps - 1) / pps), segs);
     const uint16_t* qb = static_cast<const uint16_t*>(q);
     const uint16_t* vb = static_cast<const uint16_t*>(v);
+    uint16_t* ob = static_cast<uint16_t*>(o_rounds);
     const int nw = n_rounds == 1 ? 0 : (n_rounds + 1) / 2;
 #define LSH_FWD_CASE(W)                                                                         \
     case W:                                                                                     \
-        return launch_bf16<W>(grid, causal, qb, vb, buckets, perm, bucket_start, o_rounds,      \
+        return launch_bf16<W>(grid, causal, qb, vb, buckets, perm, bucket_start, ob,            \
                               lse_rounds, L, n_rounds, n_buckets, scale, self_mask, pps, stream);
     switch (nw) {
         LSH_FWD_CASE(0)

@@ -1,8 +1,7 @@
 // Undo the per-round sort and combine the rounds (Reformer App. A):
 //   z_i = log sum_r exp z_r(i),   o_i = sum_r exp(z_r(i) - z_i) o_r(i).
 // The scatter back to position order is done as a gather through `undo`, so
-// every write is a contiguous output row.  Sixteen lanes share a row (one
-// float4 of the 64 values each).
+// every write is a contiguous output row.
 #include "common.h"
 #include "launch.h"
 
@@ -11,18 +10,20 @@ namespace {
 
 constexpr int kMaxRounds = 16;
 
-// All loads of a row are issued before they are used (slots, then the
-// log-partitions, then the rows), so each lane keeps up to 16 independent
-// requests in flight instead of walking a dependent chain per round.
-template <bool F32_OUT>
-__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ o_rounds,
+// Eight lanes share a row (8 of its 64 values each, 16 bytes of bf16 or two
+// float4 of fp32).  All loads of a row are issued before they are used
+// (slots, then the log-partitions, then the rows), so each lane keeps up to
+// 16 independent requests in flight instead of walking a dependent chain per
+// round.  The weighted sum is formed in fp32.
+template <bool F32>
+__global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o_rounds,
                                                       const float* __restrict__ lse_rounds,
                                                       const int32_t* __restrict__ undo,
                                                       void* __restrict__ out,
                                                       float* __restrict__ lse_total, int64_t rows,
                                                       int L, int n_r) {
-    const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
-    const int part = threadIdx.x & 15;
+    const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 3;
+    const int part = threadIdx.x & 7;
     if (row >= rows) return;
     const int64_t bh = row / L;
     const int64_t i = row % L;
@@ -45,38 +46,59 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     for (int r = 0; r < kMaxRounds; ++r)
         if (r < n_r) sum += expf(z_r[r] - zmax);
     const float z = zmax + logf(sum);
-    f32x4 o[kMaxRounds];
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if constexpr (F32) {
+        const float* src = static_cast<const float*>(o_rounds);
+        f32x4 o[kMaxRounds][2];
 #pragma unroll
-    for (int r = 0; r < kMaxRounds; ++r)
-        if (r < n_r) o[r] = *reinterpret_cast<const f32x4*>(o_rounds + base[r] * kHeadDim + part * 4);
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int r = 0; r < kMaxRounds; ++r)
+            if (r < n_r) {
+                o[r][0] = *reinterpret_cast<const f32x4*>(src + base[r] * kHeadDim + part * 8);
+                o[r][1] = *reinterpret_cast<const f32x4*>(src + base[r] * kHeadDim + part * 8 + 4);
+            }
 #pragma unroll
-    for (int r = 0; r < kMaxRounds; ++r)
-        if (r < n_r) {
-            const float w = expf(z_r[r] - z);
-            acc[0] = fmaf(w, o[r][0], acc[0]);
-            acc[1] = fmaf(w, o[r][1], acc[1]);
-            acc[2] = fmaf(w, o[r][2], acc[2]);
-            acc[3] = fmaf(w, o[r][3], acc[3]);
-        }
-    if constexpr (F32_OUT) {
-        *reinterpret_cast<f32x4*>(static_cast<float*>(out) + row * kHeadDim + part * 4) = acc;
+        for (int r = 0; r < kMaxRounds; ++r)
+            if (r < n_r) {
+                const float w = expf(z_r[r] - z);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc[e] = fmaf(w, o[r][e >> 2][e & 3], acc[e]);
+            }
+        float* dst = static_cast<float*>(out) + row * kHeadDim + part * 8;
+        *reinterpret_cast<f32x4*>(dst) = f32x4{acc[0], acc[1], acc[2], acc[3]};
+        *reinterpret_cast<f32x4*>(dst + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
     } else {
-        uint2 packed = make_uint2(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]));
-        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(out) + row * kHeadDim + part * 4) = packed;
+        const uint16_t* src = static_cast<const uint16_t*>(o_rounds);
+        u32x4 o[kMaxRounds];
+#pragma unroll
+        for (int r = 0; r < kMaxRounds; ++r)
+            if (r < n_r) o[r] = *reinterpret_cast<const u32x4*>(src + base[r] * kHeadDim + part * 8);
+#pragma unroll
+        for (int r = 0; r < kMaxRounds; ++r)
+            if (r < n_r) {
+                const float w = expf(z_r[r] - z);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    acc[2 * e] = fmaf(w, bf16_bits_to_f32(o[r][e] & 0xFFFFu), acc[2 * e]);
+                    acc[2 * e + 1] = fmaf(w, __uint_as_float(o[r][e] & 0xFFFF0000u), acc[2 * e + 1]);
+                }
+            }
+        u32x4 packed;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) packed[e] = pack_bf16x2(acc[2 * e], acc[2 * e + 1]);
+        *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(out) + row * kHeadDim + part * 8) = packed;
     }
     if (lse_total && part == 0) lse_total[row] = z;
 }
 
 }  // namespace
 
-hipError_t launch_combine(int64_t BH, int L, int n_rounds, bool f32_out, const float* o_rounds,
+hipError_t launch_combine(int64_t BH, int L, int n_rounds, bool f32, const void* o_rounds,
                           const float* lse_rounds, const int32_t* undo, void* out,
                           float* lse_total, hipStream_t stream) {
     const int64_t rows = BH * L;
     if (rows == 0) return hipSuccess;
-    const unsigned grid = (unsigned)((rows * 16 + 255) / 256);
-    if (f32_out)
+    const unsigned grid = (unsigned)((rows * 8 + 255) / 256);
+    if (f32)
         combine_kernel<true><<<grid, 256, 0, stream>>>(o_rounds, lse_rounds, undo, out, lse_total,
                                                        rows, L, n_rounds);
     else

@@ -35,11 +35,11 @@ hipError_t launch_gather(int64_t BH, int L, int n_rounds, bool f32, const void* 
 hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, bool causal,
                            float scale, float self_mask, bool f32, const void* q, const void* v,
                            const int32_t* buckets, const int32_t* perm,
-                           const int32_t* bucket_start, float* o_rounds, float* lse_rounds,
+                           const int32_t* bucket_start, void* o_rounds, float* lse_rounds,
                            hipStream_t stream);
 
 // ---- round combination ----
-hipError_t launch_combine(int64_t BH, int L, int n_rounds, bool f32_out, const float* o_rounds,
+hipError_t launch_combine(int64_t BH, int L, int n_rounds, bool f32, const void* o_rounds,
                           const float* lse_rounds, const int32_t* undo, void* out,
                           float* lse_total, hipStream_t stream);
 

@@ -50,9 +50,12 @@ bool all_aligned(P... p) {
 
 int status_of(hipError_t e) { return e == hipSuccess ? LSH_OK : LSH_ERR_HIP; }
 
-size_t fwd_rounds_bytes(const lsh_config* cfg) {
+size_t elem_bytes(lsh_dtype dtype) { return dtype == LSH_F32 ? 4 : 2; }
+
+// o_rounds (dtype) then lse_rounds (fp32), each 256-byte aligned
+size_t fwd_rounds_bytes(const lsh_config* cfg, lsh_dtype dtype) {
     const size_t rr = (size_t)bh_of(cfg) * cfg->n_rounds * cfg->L;
-    return lsh::align256(rr * cfg->d * sizeof(float)) + lsh::align256(rr * sizeof(float));
+    return lsh::align256(rr * cfg->d * elem_bytes(dtype)) + lsh::align256(rr * sizeof(float));
 }
 
 #define LSH_TRY(expr)              \
@@ -86,7 +89,7 @@ size_t lsh_workspace_bytes(const lsh_config* cfg, lsh_dtype dtype, int op) {
         case LSH_OP_ATTN_FWD: return 0;
         case LSH_OP_COMBINE: return 0;
         case LSH_OP_ATTN_BWD: return lsh::bwd_workspace_bytes(BH, cfg->L, cfg->n_rounds);
-        case LSH_OP_FORWARD: return fwd_rounds_bytes(cfg) + (hash > sort ? hash : sort);
+        case LSH_OP_FORWARD: return fwd_rounds_bytes(cfg, dtype) + (hash > sort ? hash : sort);
         default: return 0;
     }
 }
@@ -132,7 +135,7 @@ int lsh_gather_rows(const lsh_config* cfg, lsh_dtype dtype, const void* src, con
 
 int lsh_chunk_attn_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, const void* v,
                        const int32_t* buckets, const int32_t* perm, const int32_t* bucket_start,
-                       float* o_rounds, float* lse_rounds, void* stream) {
+                       void* o_rounds, float* lse_rounds, void* stream) {
     LSH_TRY(check_config(cfg));
     LSH_TRY(check_dtype(dtype));
     if (!q || !v || !buckets || !perm || !bucket_start || !o_rounds || !lse_rounds)
@@ -145,7 +148,7 @@ int lsh_chunk_attn_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, co
                                           o_rounds, lse_rounds, static_cast<hipStream_t>(stream)));
 }
 
-int lsh_combine_rounds(const lsh_config* cfg, lsh_dtype dtype, const float* o_rounds,
+int lsh_combine_rounds(const lsh_config* cfg, lsh_dtype dtype, const void* o_rounds,
                        const float* lse_rounds, const int32_t* undo, void* out, float* lse_total,
                        void* stream) {
     LSH_TRY(check_config(cfg));
@@ -170,10 +173,10 @@ int lsh_attention_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, con
     LSH_TRY(check_supported(cfg));
     const size_t rr = (size_t)bh_of(cfg) * cfg->n_rounds * cfg->L;
     char* ws = static_cast<char*>(workspace);
-    float* o_rounds = reinterpret_cast<float*>(ws);
-    float* lse_rounds = reinterpret_cast<float*>(ws + lsh::align256(rr * cfg->d * sizeof(float)));
-    void* scratch = ws + fwd_rounds_bytes(cfg);
-    const size_t scratch_bytes = workspace_bytes - fwd_rounds_bytes(cfg);
+    void* o_rounds = ws;
+    float* lse_rounds = reinterpret_cast<float*>(ws + lsh::align256(rr * cfg->d * elem_bytes(dtype)));
+    void* scratch = ws + fwd_rounds_bytes(cfg, dtype);
+    const size_t scratch_bytes = workspace_bytes - fwd_rounds_bytes(cfg, dtype);
     LSH_TRY(lsh_hash(cfg, dtype, q, R, buckets, scratch, scratch_bytes, stream));
     LSH_TRY(lsh_sort_permute(cfg, buckets, perm, undo, bucket_start, scratch, scratch_bytes, stream));
     LSH_TRY(lsh_chunk_attn_fwd(cfg, dtype, q, v, buckets, perm, bucket_start, o_rounds, lse_rounds,

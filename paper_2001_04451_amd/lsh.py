@@ -210,7 +210,8 @@ def lsh_gather_rows(cfg: Config, src: torch.Tensor, perm: torch.Tensor) -> torch
 
 
 def lsh_chunk_attn_fwd(cfg: Config, q, v, buckets, perm, bstart, o_rounds=None, lse_rounds=None):
-    """Per-round outputs o_rounds [B,H,n_r,L,d] and lse_rounds [B,H,n_r,L], sorted order."""
+    """Per-round outputs o_rounds [B,H,n_r,L,d] (q's dtype) and lse_rounds [B,H,n_r,L]
+    (fp32), sorted order."""
     _need(q, (cfg.B, cfg.H, cfg.L, cfg.d), name="q")
     _need(v, (cfg.B, cfg.H, cfg.L, cfg.d), q.dtype, "v")
     _need(perm, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.int32, "perm")
@@ -218,8 +219,9 @@ def lsh_chunk_attn_fwd(cfg: Config, q, v, buckets, perm, bstart, o_rounds=None, 
     _need(buckets, (cfg.B, cfg.H, cfg.L, cfg.n_rounds), torch.int32, "buckets")
     dev = q.device
     if o_rounds is None:
-        o_rounds = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.L, cfg.d), dtype=torch.float32,
+        o_rounds = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.L, cfg.d), dtype=q.dtype,
                                device=dev)
+    _need(o_rounds, (cfg.B, cfg.H, cfg.n_rounds, cfg.L, cfg.d), q.dtype, "o_rounds")
     if lse_rounds is None:
         lse_rounds = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.L), dtype=torch.float32,
                                  device=dev)
@@ -232,8 +234,9 @@ def lsh_chunk_attn_fwd(cfg: Config, q, v, buckets, perm, bstart, o_rounds=None, 
 
 def lsh_combine_rounds(cfg: Config, o_rounds, lse_rounds, undo, out_dtype: torch.dtype,
                    out=None, lse_total=None):
-    """Output [B,H,L,d] in out_dtype and lse_total [B,H,L] fp32 (lsh_combine_rounds)."""
-    _need(o_rounds, (cfg.B, cfg.H, cfg.n_rounds, cfg.L, cfg.d), torch.float32, "o_rounds")
+    """Output [B,H,L,d] and lse_total [B,H,L] fp32 (lsh_combine_rounds).  o_rounds and the
+    output share the call's dtype (out_dtype)."""
+    _need(o_rounds, (cfg.B, cfg.H, cfg.n_rounds, cfg.L, cfg.d), out_dtype, "o_rounds")
     _need(lse_rounds, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.float32, "lse_rounds")
     _need(undo, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.int32, "undo")
     dev = o_rounds.device

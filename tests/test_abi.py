@@ -97,8 +97,11 @@ def test_backward_is_bf16_only(L):
 def test_workspace_sizes(L):
     c = _cfg(B=1, H=16, L=65536, n_buckets=1024, n_rounds=8)
     rr = 16 * 65536 * 8
+    # per-round outputs in the call's dtype (bf16 here) plus fp32 log-partitions
     fwd = L.lsh_workspace_bytes(ctypes.byref(c), 1, lsh.LSH_OP_FORWARD)
-    assert fwd >= rr * 64 * 4 + rr * 4
+    assert fwd >= rr * 64 * 2 + rr * 4
+    fwd32 = L.lsh_workspace_bytes(ctypes.byref(c), 0, lsh.LSH_OP_FORWARD)
+    assert fwd32 >= rr * 64 * 4 + rr * 4
     assert L.lsh_workspace_bytes(ctypes.byref(c), 1, lsh.LSH_OP_ATTN_FWD) == 0
 
 

@@ -100,7 +100,7 @@ def test_chunk_attention_and_combine(gpu, name):
     out, lse = lsh.lsh_combine_rounds(cfg, o_r, lse_r, undo, torch_dtype(w.dtype))
     torch.cuda.synchronize()
     tol = out_tolerance(w.dtype)
-    err_or = np.abs(o_r.cpu().numpy() - ref["o_rounds"]).max()
+    err_or = np.abs(o_r.float().cpu().numpy() - ref["o_rounds"]).max()
     assert err_or <= tol, f"per-round output max-abs error {err_or}"
     assert lse_close(lse_r.cpu().numpy(), ref["lse_rounds"], w.dtype).all()
     got = out.float().cpu().numpy()
@@ -196,7 +196,7 @@ def test_attention_edge_inputs(gpu, variant, causal):
     out, lse = lsh.lsh_combine_rounds(cfg, o_r, lse_r, undo, torch.bfloat16)
     torch.cuda.synchronize()
     tol = out_tolerance(w.dtype)
-    err_or = np.abs(o_r.cpu().numpy() - ref["o_rounds"]).max()
+    err_or = np.abs(o_r.float().cpu().numpy() - ref["o_rounds"]).max()
     print(f"{variant} causal={causal}: per-round err {err_or:.3e}")
     assert err_or <= tol
     assert lse_close(lse_r.cpu().numpy(), ref["lse_rounds"], w.dtype).all()
