@@ -81,6 +81,8 @@ def run_gpu(w: W.Workload, steps: int, warmup: int) -> dict:
                           dtype=torch.uint8, device=dev)
     ws_sort = torch.empty(max(256, lsh.workspace_bytes(cfg, tdt, lsh.LSH_OP_SORT)),
                           dtype=torch.uint8, device=dev)
+    ws_attn = torch.empty(max(256, lsh.workspace_bytes(cfg, tdt, lsh.LSH_OP_ATTN_FWD)),
+                          dtype=torch.uint8, device=dev)
 
     stages = ["hash", "sort", "attn", "combine"]
 
@@ -93,7 +95,7 @@ def run_gpu(w: W.Workload, steps: int, warmup: int) -> dict:
         lsh.lsh_sort_permute(cfg, buckets, ws_sort, perm, undo, bstart)
         if ev is not None:
             ev[2].record()
-        lsh.lsh_chunk_attn_fwd(cfg, q, v, buckets, perm, bstart, o_r, lse_r)
+        lsh.lsh_chunk_attn_fwd(cfg, q, v, buckets, perm, bstart, o_r, lse_r, ws_attn)
         if ev is not None:
             ev[3].record()
         lsh.lsh_combine_rounds(cfg, o_r, lse_r, undo, tdt, out, lse)

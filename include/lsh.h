@@ -138,11 +138,14 @@ int lsh_gather_rows(const lsh_config *cfg, lsh_dtype dtype, const void *src,
  *   o_rounds      [B][H][n_rounds][L][d] (dtype, written, sorted order): each
  *                 round's output is normalised and accumulated in fp32, then
  *                 stored in the call's dtype
- *   lse_rounds    [B][H][n_rounds][L] fp32 (written, sorted order) */
+ *   lse_rounds    [B][H][n_rounds][L] fp32 (written, sorted order)
+ *   workspace     >= lsh_workspace_bytes(cfg, dtype, LSH_OP_ATTN_FWD) bytes
+ *                 (per-token key scales and packed bucket ids for bf16 calls;
+ *                 0 bytes, and workspace may be NULL, for fp32 calls) */
 int lsh_chunk_attn_fwd(const lsh_config *cfg, lsh_dtype dtype, const void *q, const void *v,
                        const int32_t *buckets, const int32_t *perm,
                        const int32_t *bucket_start, void *o_rounds, float *lse_rounds,
-                       void *stream);
+                       void *workspace, size_t workspace_bytes, void *stream);
 
 /* Undo the sort and combine the rounds (App. A):
  *   z_i = log sum_r exp z_r(i),  out_i = sum_r exp(z_r(i) - z_i) o_r(i).

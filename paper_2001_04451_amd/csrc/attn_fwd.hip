@@ -62,7 +62,7 @@ __device__ __forceinline__ constexpr uint32_t sig_guard(int w) {
 
 template <int NW>
 struct FwdSig {
-    static constexpr int stride = NW <= 1 ? 1 : (NW <= 2 ? 2 : (NW <= 4 ? 4 : 8));
+    static constexpr int stride = NW <= 1 ? 1 : (NW <= 2 ? 2 : (NW <= 4 ? 4 : 8));  // words per token
 };
 
 template <int NW>
@@ -70,8 +70,7 @@ struct FwdShared {
     char Qs[kRing * 128];           // query/key rows (swizzled)
     char Vt[kHeadDim * kRing * 2];  // V^T: row d, 16-byte blocks of 8 keys (swizzled)
     float cf[kRing];                // scale*log2(e)/|q_row| (0 for a zero row)
-    int beta[kRing];                // the row's bucket in this round (-1 outside the sequence)
-    uint32_t sig[kRing][FwdSig<NW>::stride];
+    uint32_t sig[kRing][FwdSig<NW>::stride];  // bucket signature words (0 outside the sequence)
     int bstart[kMaxBucketsStaged + 1];  // the segment's bucket starts
     float tab[kMaskedIndex + 1];        // -log2 N by mismatch count; -inf = masked
 };
@@ -83,20 +82,22 @@ __device__ __forceinline__ uint32_t vt_offset(int d, int k) {
     return (uint32_t)d * (kRing * 2) + (uint32_t)(((k >> 3) ^ vt_swz(d)) << 4) + (uint32_t)((k & 4) << 1);
 }
 
-// Four consecutive rows of a batch, as loaded by one thread (16-byte piece
-// `part` of each row, plus signature word `part` and, for one part, the
-// rows' buckets in this round).
+// Four consecutive rows of a batch, as loaded by one thread: 16-byte piece
+// `part` of each q and v row; thread part 0 (and 1 for eight words) also
+// brings the rows' signature words and part 2 their key scales.
 struct RowQuad {
     u32x4 q[4], v[4];
-    uint32_t sig[4];
-    int beta[4];
+    u32x4 sig[4];
+    float cf[4];
 };
 
 template <int NW>
 __device__ __forceinline__ void load_quad(RowQuad& R, const uint16_t* __restrict__ q,
                                           const uint16_t* __restrict__ v,
-                                          const int32_t* __restrict__ buckets, int64_t bh, int L,
-                                          int n_r, int n_b, int r, const int (&pos)[4], int part) {
+                                          const float* __restrict__ cf_tok,
+                                          const uint32_t* __restrict__ sig_tok, int64_t bh, int L,
+                                          const int (&pos)[4], int part) {
+    constexpr int SW = FwdSig<NW>::stride;
     const u32x4 zero = {0, 0, 0, 0};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -104,39 +105,34 @@ __device__ __forceinline__ void load_quad(RowQuad& R, const uint16_t* __restrict
         const int64_t grow = bh * L + (ok ? pos[i] : 0);
         R.q[i] = ok ? *reinterpret_cast<const u32x4*>(q + grow * kHeadDim + part * 8) : zero;
         R.v[i] = ok ? *reinterpret_cast<const u32x4*>(v + grow * kHeadDim + part * 8) : zero;
-        const int32_t* brow = buckets + grow * n_r;
-        R.sig[i] = 0;
-        R.beta[i] = -1;
-        if constexpr (NW > 0) {
-            if (ok && part < NW) {
-                const uint32_t id0 = (uint32_t)brow[2 * part] & 0x3FFu;
-                const uint32_t id1 = 2 * part + 1 < n_r ? (uint32_t)brow[2 * part + 1] & 0x3FFu : 0u;
-                R.sig[i] = (id0 << part) | (id1 << (part + 11));
-                if (part == (r >> 1)) R.beta[i] = min((int)((r & 1) ? id1 : id0), n_b - 1);
+        R.sig[i] = zero;
+        R.cf[i] = 0.f;
+        const uint32_t* srow = sig_tok + grow * SW;
+        if (ok && part == 0) {
+            if constexpr (SW >= 4) {
+                R.sig[i] = *reinterpret_cast<const u32x4*>(srow);
+            } else if constexpr (SW == 2) {
+                const uint2 w = *reinterpret_cast<const uint2*>(srow);
+                R.sig[i][0] = w.x;
+                R.sig[i][1] = w.y;
+            } else {
+                R.sig[i][0] = srow[0];
             }
-        } else {
-            if (ok && part == 0) R.beta[i] = min(max(brow[0], 0), n_b - 1);
         }
+        if constexpr (SW == 8) {
+            if (ok && part == 1) R.sig[i] = *reinterpret_cast<const u32x4*>(srow + 4);
+        }
+        if (ok && part == 2) R.cf[i] = cf_tok[grow];
     }
 }
 
-// Store a quad at ring rows rr0 .. rr0+3; the eight threads of the quad
-// reduce |q|^2 of the four rows together.
+// Store a quad at ring rows rr0 .. rr0+3 (Q rows, V transposed, signature
+// words and key scales).
 template <int NW>
-__device__ __forceinline__ void store_quad(FwdShared<NW>& S, const RowQuad& R, int rr0, int part,
-                                           int r, float scale_log2e) {
-    float ss[4];
+__device__ __forceinline__ void store_quad(FwdShared<NW>& S, const RowQuad& R, int rr0, int part) {
+    constexpr int SW = FwdSig<NW>::stride;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        lds_store_piece(S.Qs, rr0 + i, part, R.q[i]);
-        float a = 0.f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float lo = __uint_as_float(R.q[i][e] << 16), hi = __uint_as_float(R.q[i][e] & 0xFFFF0000u);
-            a = fmaf(lo, lo, fmaf(hi, hi, a));
-        }
-        ss[i] = a;
-    }
+    for (int i = 0; i < 4; ++i) lds_store_piece(S.Qs, rr0 + i, part, R.q[i]);
     // V^T: dword e of a piece holds d = 8*part + 2e (low half) and 2e+1 (high)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -150,34 +146,25 @@ __device__ __forceinline__ void store_quad(FwdShared<NW>& S, const RowQuad& R, i
         *reinterpret_cast<uint2*>(S.Vt + vt_offset(d, rr0)) = lo;
         *reinterpret_cast<uint2*>(S.Vt + vt_offset(d + 1, rr0)) = hi;
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        ss[i] += __shfl_xor(ss[i], 1);
-        ss[i] += __shfl_xor(ss[i], 2);
-        ss[i] += __shfl_xor(ss[i], 4);
-    }
-    if (part == 0) {
-        f32x4 c;
+    if (part == 2) *reinterpret_cast<f32x4*>(&S.cf[rr0]) = f32x4{R.cf[0], R.cf[1], R.cf[2], R.cf[3]};
+    if (part == 0 || (SW == 8 && part == 1)) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const float nn = sqrtf(ss[i]);
-            c[i] = nn > 0.f ? scale_log2e / nn : 0.f;
-        }
-        *reinterpret_cast<f32x4*>(&S.cf[rr0]) = c;
-    }
-    if (part == (NW > 0 ? (r >> 1) : 0))
-        *reinterpret_cast<int4*>(&S.beta[rr0]) = make_int4(R.beta[0], R.beta[1], R.beta[2], R.beta[3]);
-    if constexpr (NW > 0) {
-        if (part < FwdSig<NW>::stride) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) S.sig[rr0 + i][part] = part < NW ? R.sig[i] : 0u;
+            uint32_t* dst = &S.sig[rr0 + i][4 * part];
+            if constexpr (SW >= 4) {
+                *reinterpret_cast<u32x4*>(dst) = R.sig[i];
+            } else if constexpr (SW == 2) {
+                *reinterpret_cast<uint2*>(dst) = make_uint2(R.sig[i][0], R.sig[i][1]);
+            } else {
+                dst[0] = R.sig[i][0];
+            }
         }
     }
 }
 
 template <int NW>
 __device__ __forceinline__ void read_sig(const FwdShared<NW>& S, int row, uint32_t (&out)[NW > 0 ? NW : 1]) {
-    if constexpr (NW == 1) {
+    if constexpr (NW <= 1) {
         out[0] = S.sig[row][0];
     } else if constexpr (NW == 2) {
         const uint2 w = *reinterpret_cast<const uint2*>(&S.sig[row][0]);
@@ -214,7 +201,8 @@ __device__ __forceinline__ void quad_positions(const int32_t* __restrict__ pseg,
 template <int NW, bool CAUSAL>
 __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ v,
-    const int32_t* __restrict__ buckets, const int32_t* __restrict__ perm,
+    const float* __restrict__ cf_tok, const uint32_t* __restrict__ sig_tok,
+    const int32_t* __restrict__ perm,
     const int32_t* __restrict__ bstart, uint16_t* __restrict__ o_rounds,
     float* __restrict__ lse_rounds, int L, int n_r, int n_b, float scale, float self_mask,
     int pairs_per_strip) {
@@ -241,11 +229,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
         int pos[4];
         RowQuad R;
         quad_positions(pseg, 2 * p0 - 1, 1, true, n_chunks, L, tid, pos);
-        load_quad<NW>(R, q, v, buckets, bh, L, n_r, n_b, r, pos, part);
-        if (qrow < kChunk) store_quad<NW>(S, R, ring_row(2 * p0 - 1, qrow), part, r, scale_log2e);
+        load_quad<NW>(R, q, v, cf_tok, sig_tok, bh, L, pos, part);
+        if (qrow < kChunk) store_quad<NW>(S, R, ring_row(2 * p0 - 1, qrow), part);
         quad_positions(pseg, 2 * p0, 2, true, n_chunks, L, tid, pos);
-        load_quad<NW>(R, q, v, buckets, bh, L, n_r, n_b, r, pos, part);
-        store_quad<NW>(S, R, ring_row(2 * p0 + qrow / kChunk, qrow % kChunk), part, r, scale_log2e);
+        load_quad<NW>(R, q, v, cf_tok, sig_tok, bh, L, pos, part);
+        store_quad<NW>(S, R, ring_row(2 * p0 + qrow / kChunk, qrow % kChunk), part);
     }
     __syncthreads();
 
@@ -259,7 +247,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
         const bool more = p + 1 < p1;
         // the next pair's new chunks load during this pair's compute
         RowQuad pf;
-        load_quad<NW>(pf, q, v, buckets, bh, L, n_r, n_b, r, pf_pos, part);
+        load_quad<NW>(pf, q, v, cf_tok, sig_tok, bh, L, pf_pos, part);
         int pf_pos2[4];
         quad_positions(pseg, 2 * (p + 2), 2, p + 2 < p1, n_chunks, L, tid, pf_pos2);
 
@@ -268,15 +256,16 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
         if (cq < n_chunks) {
             const int rq = ring_row(cq, qh * 32 + n);
             const int s_q = cq * kChunk + qh * 32 + n;
-            const int beta = max(S.beta[rq], 0);
+            uint32_t qsig[NW > 0 ? NW : 1];
+            read_sig<NW>(S, rq, qsig);
+            // the query's bucket in this round: field r of its signature
+            const int beta = min((int)((qsig[r >> 1] >> ((r >> 1) + 11 * (r & 1))) & 0x3FFu), n_b - 1);
             const int wlo = max(0, (cq - 1) * kChunk);
             const int lo = max(S.bstart[beta], wlo);
             const int hi = CAUSAL ? s_q - 1 : min(S.bstart[beta + 1], (cq + 1) * kChunk) - 1;
             bf16x8 qb[4];
 #pragma unroll
             for (int s = 0; s < 4; ++s) qb[s] = row_operand(S.Qs, rq, h, s);
-            uint32_t qsig[NW > 0 ? NW : 1];
-            read_sig<NW>(S, rq, qsig);
             const float cfq = S.cf[rq];
             const float bound = cfq > 0.f ? scale_log2e * scale_log2e / cfq : 0.f;  // B_i
             const bool fast = __ballot(!(bound <= kFastBound)) == 0;
@@ -393,7 +382,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
         }
 
         __syncthreads();  // every wave is done with the slots of chunks 2p-1 and 2p
-        if (more) store_quad<NW>(S, pf, ring_row(2 * p + 2 + qrow / kChunk, qrow % kChunk), part, r, scale_log2e);
+        if (more) store_quad<NW>(S, pf, ring_row(2 * p + 2 + qrow / kChunk, qrow % kChunk), part);
 #pragma unroll
         for (int i = 0; i < 4; ++i) pf_pos[i] = pf_pos2[i];
         __syncthreads();
@@ -480,27 +469,79 @@ __global__ __launch_bounds__(64) void attn_fwd_f32_kernel(
     }
 }
 
+// Per-token data that the chunk kernel gathers with every staged row, made
+// once instead of once per round: the key scale scale*log2(e)/|q| (0 for a
+// zero row) and the bucket signature words (see sig_add).  Eight lanes per
+// token, one 16-byte piece of the q row each.
+template <int SW>
+__global__ __launch_bounds__(256) void attn_prep_kernel(const uint16_t* __restrict__ q,
+                                                        const int32_t* __restrict__ buckets,
+                                                        int64_t rows, int n_r, float scale_log2e,
+                                                        float* __restrict__ cf_tok,
+                                                        uint32_t* __restrict__ sig_tok) {
+    const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 3;
+    const int part = threadIdx.x & 7;
+    if (row >= rows) return;  // whole groups of eight lanes leave together
+    const u32x4 x = *reinterpret_cast<const u32x4*>(q + row * kHeadDim + part * 8);
+    float ss = 0.f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float lo = __uint_as_float(x[e] << 16), hi = __uint_as_float(x[e] & 0xFFFF0000u);
+        ss = fmaf(lo, lo, fmaf(hi, hi, ss));
+    }
+    ss += __shfl_xor(ss, 1);
+    ss += __shfl_xor(ss, 2);
+    ss += __shfl_xor(ss, 4);
+    if (part == 0) {
+        const float nn = sqrtf(ss);
+        cf_tok[row] = nn > 0.f ? scale_log2e / nn : 0.f;
+    }
+    if (part < SW) {
+        const int32_t* brow = buckets + row * n_r;
+        const uint32_t id0 = 2 * part < n_r ? (uint32_t)brow[2 * part] & 0x3FFu : 0u;
+        const uint32_t id1 = 2 * part + 1 < n_r ? (uint32_t)brow[2 * part + 1] & 0x3FFu : 0u;
+        sig_tok[row * SW + part] = (id0 << part) | (id1 << (part + 11));
+    }
+}
+
 template <int NW>
 hipError_t launch_bf16(dim3 grid, bool causal, const uint16_t* q, const uint16_t* v,
                        const int32_t* buckets, const int32_t* perm, const int32_t* bs, uint16_t* o,
-                       float* lse, int L, int n_r, int n_b, float scale, float self_mask, int pps,
-                       hipStream_t stream) {
+                       float* lse, int64_t BH, int L, int n_r, int n_b, float scale, float self_mask,
+                       int pps, void* workspace, hipStream_t stream) {
+    constexpr int SW = FwdSig<NW>::stride;
+    const int64_t rows = BH * L;
+    float* cf_tok = static_cast<float*>(workspace);
+    uint32_t* sig_tok = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + align256((size_t)rows * 4));
+    attn_prep_kernel<SW><<<(unsigned)((rows * 8 + 255) / 256), 256, 0, stream>>>(
+        q, buckets, rows, n_r, scale * kLog2e, cf_tok, sig_tok);
     if (causal)
-        attn_fwd_bf16_kernel<NW, true><<<grid, 256, 0, stream>>>(q, v, buckets, perm, bs, o, lse, L,
-                                                                 n_r, n_b, scale, self_mask, pps);
+        attn_fwd_bf16_kernel<NW, true><<<grid, 256, 0, stream>>>(q, v, cf_tok, sig_tok, perm, bs, o,
+                                                                 lse, L, n_r, n_b, scale, self_mask, pps);
     else
-        attn_fwd_bf16_kernel<NW, false><<<grid, 256, 0, stream>>>(q, v, buckets, perm, bs, o, lse, L,
-                                                                  n_r, n_b, scale, self_mask, pps);
+        attn_fwd_bf16_kernel<NW, false><<<grid, 256, 0, stream>>>(q, v, cf_tok, sig_tok, perm, bs, o,
+                                                                  lse, L, n_r, n_b, scale, self_mask, pps);
     return hipGetLastError();
 }
 
+int sig_words(int n_rounds) {
+    const int nw = n_rounds == 1 ? 0 : (n_rounds + 1) / 2;
+    return nw <= 1 ? 1 : (nw <= 2 ? 2 : (nw <= 4 ? 4 : 8));
+}
+
 }  // namespace
+
+size_t attn_fwd_workspace_bytes(int64_t BH, int L, int n_rounds, bool f32) {
+    if (f32) return 0;
+    const size_t rows = (size_t)BH * L;
+    return align256(rows * 4) + align256(rows * 4 * sig_words(n_rounds));
+}
 
 hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, bool causal,
                            float scale, float self_mask, bool f32, const void* q, const void* v,
                            const int32_t* buckets, const int32_t* perm,
                            const int32_t* bucket_start, void* o_rounds, float* lse_rounds,
-                           hipStream_t stream) {
+                           void* workspace, hipStream_t stream) {
     if (BH == 0 || L == 0) return hipSuccess;
     const unsigned segs = (unsigned)(BH * n_rounds);
     if (f32) {
@@ -522,8 +563,8 @@ hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, bool 
     const int nw = n_rounds == 1 ? 0 : (n_rounds + 1) / 2;
 #define LSH_FWD_CASE(W)                                                                         \
     case W:                                                                                     \
-        return launch_bf16<W>(grid, causal, qb, vb, buckets, perm, bucket_start, ob,            \
-                              lse_rounds, L, n_rounds, n_buckets, scale, self_mask, pps, stream);
+        return launch_bf16<W>(grid, causal, qb, vb, buckets, perm, bucket_start, ob, lse_rounds, \
+                              BH, L, n_rounds, n_buckets, scale, self_mask, pps, workspace, stream);
     switch (nw) {
         LSH_FWD_CASE(0)
         LSH_FWD_CASE(1)

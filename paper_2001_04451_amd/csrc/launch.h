@@ -32,11 +32,12 @@ hipError_t launch_gather(int64_t BH, int L, int n_rounds, bool f32, const void* 
                          const int32_t* perm, void* dst, hipStream_t stream);
 
 // ---- chunked attention, forward ----
+size_t attn_fwd_workspace_bytes(int64_t BH, int L, int n_rounds, bool f32);
 hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, bool causal,
                            float scale, float self_mask, bool f32, const void* q, const void* v,
                            const int32_t* buckets, const int32_t* perm,
                            const int32_t* bucket_start, void* o_rounds, float* lse_rounds,
-                           hipStream_t stream);
+                           void* workspace, hipStream_t stream);
 
 // ---- round combination ----
 hipError_t launch_combine(int64_t BH, int L, int n_rounds, bool f32, const void* o_rounds,

@@ -86,10 +86,14 @@ size_t lsh_workspace_bytes(const lsh_config* cfg, lsh_dtype dtype, int op) {
     switch (op) {
         case LSH_OP_HASH: return hash;
         case LSH_OP_SORT: return sort;
-        case LSH_OP_ATTN_FWD: return 0;
+        case LSH_OP_ATTN_FWD: return lsh::attn_fwd_workspace_bytes(BH, cfg->L, cfg->n_rounds, dtype == LSH_F32);
         case LSH_OP_COMBINE: return 0;
         case LSH_OP_ATTN_BWD: return lsh::bwd_workspace_bytes(BH, cfg->L, cfg->n_rounds);
-        case LSH_OP_FORWARD: return fwd_rounds_bytes(cfg, dtype) + (hash > sort ? hash : sort);
+        case LSH_OP_FORWARD: {
+            const size_t attn = lsh::attn_fwd_workspace_bytes(BH, cfg->L, cfg->n_rounds, dtype == LSH_F32);
+            const size_t scratch = hash > sort ? hash : sort;
+            return fwd_rounds_bytes(cfg, dtype) + (scratch > attn ? scratch : attn);
+        }
         default: return 0;
     }
 }
@@ -135,17 +139,22 @@ int lsh_gather_rows(const lsh_config* cfg, lsh_dtype dtype, const void* src, con
 
 int lsh_chunk_attn_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, const void* v,
                        const int32_t* buckets, const int32_t* perm, const int32_t* bucket_start,
-                       void* o_rounds, float* lse_rounds, void* stream) {
+                       void* o_rounds, float* lse_rounds, void* workspace,
+                       size_t workspace_bytes, void* stream) {
     LSH_TRY(check_config(cfg));
     LSH_TRY(check_dtype(dtype));
     if (!q || !v || !buckets || !perm || !bucket_start || !o_rounds || !lse_rounds)
         return LSH_ERR_INVALID;
     if (!all_aligned(q, v, o_rounds)) return LSH_ERR_INVALID;
+    const size_t need = lsh_workspace_bytes(cfg, dtype, LSH_OP_ATTN_FWD);
+    if (need > 0 && (!workspace || workspace_bytes < need || !all_aligned(workspace)))
+        return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
     return status_of(lsh::launch_attn_fwd(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets,
                                           cfg->causal != 0, cfg->scale, cfg->self_mask,
                                           dtype == LSH_F32, q, v, buckets, perm, bucket_start,
-                                          o_rounds, lse_rounds, static_cast<hipStream_t>(stream)));
+                                          o_rounds, lse_rounds, workspace,
+                                          static_cast<hipStream_t>(stream)));
 }
 
 int lsh_combine_rounds(const lsh_config* cfg, lsh_dtype dtype, const void* o_rounds,
@@ -180,7 +189,7 @@ int lsh_attention_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, con
     LSH_TRY(lsh_hash(cfg, dtype, q, R, buckets, scratch, scratch_bytes, stream));
     LSH_TRY(lsh_sort_permute(cfg, buckets, perm, undo, bucket_start, scratch, scratch_bytes, stream));
     LSH_TRY(lsh_chunk_attn_fwd(cfg, dtype, q, v, buckets, perm, bucket_start, o_rounds, lse_rounds,
-                               stream));
+                               scratch, scratch_bytes, stream));
     return lsh_combine_rounds(cfg, dtype, o_rounds, lse_rounds, undo, out, lse_total, stream);
 }
 

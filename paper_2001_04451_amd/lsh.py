@@ -73,7 +73,7 @@ def lib() -> ctypes.CDLL:
             "lsh_hash": [_CFG, _I, _P, _P, _P, _P, _SZ, _P],
             "lsh_sort_permute": [_CFG, _P, _P, _P, _P, _P, _SZ, _P],
             "lsh_gather_rows": [_CFG, _I, _P, _P, _P, _P],
-            "lsh_chunk_attn_fwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P],
+            "lsh_chunk_attn_fwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
             "lsh_combine_rounds": [_CFG, _I, _P, _P, _P, _P, _P, _P],
             "lsh_attention_fwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
             "lsh_chunk_attn_bwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ,
@@ -209,7 +209,8 @@ def lsh_gather_rows(cfg: Config, src: torch.Tensor, perm: torch.Tensor) -> torch
     return dst
 
 
-def lsh_chunk_attn_fwd(cfg: Config, q, v, buckets, perm, bstart, o_rounds=None, lse_rounds=None):
+def lsh_chunk_attn_fwd(cfg: Config, q, v, buckets, perm, bstart, o_rounds=None, lse_rounds=None,
+                       workspace=None):
     """Per-round outputs o_rounds [B,H,n_r,L,d] (q's dtype) and lse_rounds [B,H,n_r,L]
     (fp32), sorted order."""
     _need(q, (cfg.B, cfg.H, cfg.L, cfg.d), name="q")
@@ -225,10 +226,13 @@ def lsh_chunk_attn_fwd(cfg: Config, q, v, buckets, perm, bstart, o_rounds=None, 
     if lse_rounds is None:
         lse_rounds = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.L), dtype=torch.float32,
                                  device=dev)
+    if workspace is None:
+        workspace = _workspace(cfg, q.dtype, LSH_OP_ATTN_FWD, dev)
     _check("lsh_chunk_attn_fwd",
            lib().lsh_chunk_attn_fwd(ctypes.byref(cfg.c()), _dtype_code(q), _ptr(q), _ptr(v),
                                     _ptr(buckets), _ptr(perm), _ptr(bstart), _ptr(o_rounds),
-                                    _ptr(lse_rounds), _stream(dev)))
+                                    _ptr(lse_rounds), _ptr(workspace), workspace.numel(),
+                                    _stream(dev)))
     return o_rounds, lse_rounds
 
 

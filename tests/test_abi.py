@@ -57,7 +57,7 @@ def test_invalid_config(L, bad):
     rc = L.lsh_hash(ctypes.byref(c), lsh.LSH_BF16, FAKE, FAKE, FAKE, FAKE, 1 << 30, None)
     assert rc == lsh.LSH_ERR_INVALID
     rc = L.lsh_chunk_attn_fwd(ctypes.byref(c), lsh.LSH_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                              FAKE, None)
+                              FAKE, FAKE, 1 << 30, None)
     assert rc == lsh.LSH_ERR_INVALID
     assert L.lsh_workspace_bytes(ctypes.byref(c), lsh.LSH_BF16, lsh.LSH_OP_FORWARD) == 0
 
@@ -75,6 +75,13 @@ def test_null_pointers_and_small_workspace(L):
     fwd = L.lsh_workspace_bytes(ctypes.byref(c), 1, lsh.LSH_OP_FORWARD)
     assert L.lsh_attention_fwd(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE,
                                FAKE, FAKE, fwd - 1, None) == lsh.LSH_ERR_INVALID
+    # bf16 attention needs its per-token workspace; fp32 needs none
+    attn = L.lsh_workspace_bytes(ctypes.byref(c), 1, lsh.LSH_OP_ATTN_FWD)
+    assert attn > 0 and L.lsh_workspace_bytes(ctypes.byref(c), 0, lsh.LSH_OP_ATTN_FWD) == 0
+    assert L.lsh_chunk_attn_fwd(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                FAKE, attn - 1, None) == lsh.LSH_ERR_INVALID
+    assert L.lsh_chunk_attn_fwd(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                None, attn, None) == lsh.LSH_ERR_INVALID
 
 
 @pytest.mark.parametrize("unsup", [dict(d=32), dict(chunk=128, L=1024), dict(n_buckets=2048),
@@ -102,7 +109,7 @@ def test_workspace_sizes(L):
     assert fwd >= rr * 64 * 2 + rr * 4
     fwd32 = L.lsh_workspace_bytes(ctypes.byref(c), 0, lsh.LSH_OP_FORWARD)
     assert fwd32 >= rr * 64 * 4 + rr * 4
-    assert L.lsh_workspace_bytes(ctypes.byref(c), 1, lsh.LSH_OP_ATTN_FWD) == 0
+    assert L.lsh_workspace_bytes(ctypes.byref(c), 0, lsh.LSH_OP_ATTN_FWD) == 0
 
 
 def test_product_never_touches_the_oracle():
