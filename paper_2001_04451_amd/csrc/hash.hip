@@ -84,27 +84,44 @@ __device__ __forceinline__ float q_value(const void* q, int64_t row, int k) {
 }
 
 // Exact argmax of [xR; -xR] for the listed row-rounds of one round.  The
-// round's R (fp32, [d][n_b/2], at most 128 KB) is staged in LDS once per
-// block; each wave settles one row-round at a time.  Column c's projection
-// is the left-to-right sum over t of the exact products q_t * R_tc in fp64
-// (the order of a plain loop), and ties go to the first index of [xR; -xR].
+// round's R (fp32, at most 130 KB) is staged in LDS once per block, column
+// by column; each wave settles one row-round at a time, in two passes:
+//  1. every column's projection in fp32 (a fused multiply-add chain over t),
+//     whose distance to the fp64 value of step 2 is at most
+//     eps = (64 * 2^-24 * 1.01 + 2^-46) * |q| * max_c |R_c|; a column can
+//     hold the fp64 argmax only if its fp32 magnitude is within 2 eps of the
+//     largest one;
+//  2. for those candidates (one lane each), the projection as the oracle
+//     forms it: the left-to-right sum over t of the exact products q_t * R_tc
+//     in fp64.  Ties go to the first index of [xR; -xR].
+// A row with more than 64 candidates (for instance q = 0) takes the plain
+// fp64 pass over every column instead.
 constexpr int kRefineThreads = 512;
+constexpr int kRefineWaves = kRefineThreads / 64;
+constexpr int kRsStride = kHeadDim + 1;  // floats per staged R column
+
+__device__ __forceinline__ void better(double v, int i, double& bv, int& bi) {
+    if (v > bv || (v == bv && i < bi)) {
+        bv = v;
+        bi = i;
+    }
+}
 
 template <bool F32>
-__global__ __launch_bounds__(kRefineThreads) void hash_refine_kernel(const void* __restrict__ q,
+__global__ __launch_bounds__(kRefineThreads, 1) void hash_refine_kernel(const void* __restrict__ q,
                                                           const float* __restrict__ R, int half,
                                                           int n_r, int64_t list_stride,
                                                           const int* __restrict__ lists,
                                                           const int* __restrict__ counts,
+                                                          const float* __restrict__ col_norm_max,
                                                           int32_t* __restrict__ buckets) {
-    extern __shared__ float Rs[];  // [64][half]
+    extern __shared__ float Rs[];  // [half][kRsStride] (column-major), then [waves][64] columns
     const int r = blockIdx.y;
     const int n = counts[r];
-    constexpr int kWavesPerBlock = kRefineThreads / 64;
-    if (n == 0 || (int)blockIdx.x * kWavesPerBlock >= n) return;  // uniform per block
-    // stage the round's R: 16-byte pieces, eight loads in flight per thread
+    if (n == 0 || (int)blockIdx.x * kRefineWaves >= n) return;  // uniform per block
+    // stage the round's R transposed (column c's 64 values contiguous, padded
+    // rows so that 64 lanes reading 64 columns hit distinct banks)
     const f32x4* Rr = reinterpret_cast<const f32x4*>(R + (size_t)r * kHeadDim * half);
-    f32x4* Rs4 = reinterpret_cast<f32x4*>(Rs);
     const int n4 = kHeadDim * half / 4;
     for (int i0 = threadIdx.x; i0 < n4; i0 += 8 * blockDim.x) {
         f32x4 tmp[8];
@@ -116,45 +133,105 @@ __global__ __launch_bounds__(kRefineThreads) void hash_refine_kernel(const void*
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const int i = i0 + u * blockDim.x;
-            if (i < n4) Rs4[i] = tmp[u];
+            if (i < n4) {
+                const int t = (4 * i) / half, c0 = (4 * i) % half;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) Rs[(c0 + e) * kRsStride + t] = tmp[u][e];
+            }
         }
     }
     __syncthreads();
     const int* list = lists + list_stride * r;
     const int lane = lane_id();
-    const int waves = gridDim.x * kWavesPerBlock;
-    for (int e = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6); e < n; e += waves) {
+    int* cand = reinterpret_cast<int*>(Rs + half * kRsStride) + (threadIdx.x >> 6) * 64;
+    const float cn = col_norm_max[r];
+    const int waves = gridDim.x * kRefineWaves;
+    for (int e = blockIdx.x * kRefineWaves + (threadIdx.x >> 6); e < n; e += waves) {
         const int64_t row = list[e];
         const float qv = q_value<F32>(q, row, lane);
-        double p[kMaxColsPerLane];
+        // pass 1: fp32 projections of this lane's columns lane + 64k
+        float p32[kMaxColsPerLane];
 #pragma unroll
-        for (int k = 0; k < kMaxColsPerLane; ++k) p[k] = 0.0;
-        // q_t reaches every lane through a scalar register (readlane), and the
-        // fully unrolled sum lets the LDS reads run ahead of the fp64 adds.
+        for (int k = 0; k < kMaxColsPerLane; ++k) p32[k] = 0.f;
+        // columns past n_b/2 read a valid one instead; their sums are ignored
+        const float* col[kMaxColsPerLane];
 #pragma unroll
+        for (int k = 0; k < kMaxColsPerLane; ++k) col[k] = Rs + min(lane + 64 * k, half - 1) * kRsStride;
+#pragma unroll 8
         for (int t = 0; t < kHeadDim; ++t) {
-            const double qt = (double)__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, qv), t));
+            const float qt = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, qv), t));
 #pragma unroll
-            for (int k = 0; k < kMaxColsPerLane; ++k) {
-                const int c = lane + 64 * k;
-                if (c < half) p[k] = __dadd_rn(p[k], __dmul_rn(qt, (double)Rs[t * half + c]));
-            }
+            for (int k = 0; k < kMaxColsPerLane; ++k) p32[k] = fmaf(qt, col[k][t], p32[k]);
+        }
+        float ss = qv * qv, mx = 0.f;
+#pragma unroll
+        for (int k = 0; k < kMaxColsPerLane; ++k)
+            if (lane + 64 * k < half) mx = fmaxf(mx, fabsf(p32[k]));
+        for (int o = 32; o >= 1; o >>= 1) {
+            ss += __shfl_xor(ss, o);
+            mx = fmaxf(mx, __shfl_xor(mx, o));
+        }
+        const float eps = (float)((64.0 * 0x1p-24 * 1.01 + 0x1p-46) * 1.01) * sqrtf(ss) * cn;
+        const float cut = mx - 2.f * eps;
+        int total = 0;
+        uint64_t masks[kMaxColsPerLane];
+#pragma unroll
+        for (int k = 0; k < kMaxColsPerLane; ++k) {
+            masks[k] = __ballot(lane + 64 * k < half && fabsf(p32[k]) >= cut);
+            total += __popcll(masks[k]);
         }
         double bv = -__builtin_inf();
         int bi = 0x7FFFFFFF;
+        if (total <= 64) {
+            // pass 2: one candidate column per lane, fp64 in the oracle's order
+            int base = 0;
 #pragma unroll
-        for (int k = 0; k < kMaxColsPerLane; ++k) {
-            const int c = lane + 64 * k;
-            if (c < half) {
-                if (p[k] > bv || (p[k] == bv && c < bi)) { bv = p[k]; bi = c; }
-                const double m = -p[k];
-                if (m > bv || (m == bv && half + c < bi)) { bv = m; bi = half + c; }
+            for (int k = 0; k < kMaxColsPerLane; ++k) {
+                if ((masks[k] >> lane) & 1ull)
+                    cand[base + __popcll(masks[k] & ((1ull << lane) - 1ull))] = lane + 64 * k;
+                base += __popcll(masks[k]);
+            }
+            __builtin_amdgcn_s_waitcnt(0);
+            __builtin_amdgcn_wave_barrier();
+            const int c = lane < total ? cand[lane] : 0;
+            // q_t * R_tc is exact in fp64 (at most 48 significant bits), so
+            // whether the compiler fuses the multiply into the add or not, the
+            // sum rounds exactly as the plain loop does.
+            double p = 0.0;
+#pragma unroll 8
+            for (int t = 0; t < kHeadDim; ++t) {
+                const double qt = (double)__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, qv), t));
+                p = __dadd_rn(p, __dmul_rn(qt, (double)Rs[c * kRsStride + t]));
+            }
+            if (lane < total) {
+                better(p, c, bv, bi);
+                better(-p, half + c, bv, bi);
+            }
+            __builtin_amdgcn_wave_barrier();
+        } else {
+            double p[kMaxColsPerLane];
+#pragma unroll
+            for (int k = 0; k < kMaxColsPerLane; ++k) p[k] = 0.0;
+#pragma unroll 8
+            for (int t = 0; t < kHeadDim; ++t) {
+                const double qt = (double)__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, qv), t));
+#pragma unroll
+                for (int k = 0; k < kMaxColsPerLane; ++k)
+                    p[k] = __dadd_rn(p[k], __dmul_rn(qt, (double)col[k][t]));
+            }
+#pragma unroll
+            for (int k = 0; k < kMaxColsPerLane; ++k) {
+                const int c = lane + 64 * k;
+                if (c < half) {
+                    better(p[k], c, bv, bi);
+                    better(-p[k], half + c, bv, bi);
+                }
             }
         }
         for (int o = 32; o >= 1; o >>= 1) {
             const double ov = __shfl_xor(bv, o);
             const int oi = __shfl_xor(bi, o);
-            if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+            better(ov, oi, bv, bi);
         }
         if (lane == 0) buckets[row * n_r + r] = bi;
     }
@@ -591,7 +668,7 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
     constexpr int kWaves = 8, kPairsBf16 = 1, kPairsF32 = 1;
     const int64_t rows_per_block = kWaves * 64 * (f32 ? kPairsF32 : kPairsBf16);
     const unsigned grid = (unsigned)((rows + rows_per_block - 1) / rows_per_block);
-    const size_t refine_lds = (size_t)kHeadDim * half * sizeof(float);
+    const size_t refine_lds = (size_t)half * kRsStride * sizeof(float) + kRefineWaves * 64 * sizeof(int);
     // Refinement blocks per round: one 128 KB-LDS block per CU over all rounds
     // (a typical list holds well under 1% of the rows; longer ones are strided).
     const unsigned refine_blocks =
@@ -606,7 +683,7 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
         hipFuncSetAttribute(reinterpret_cast<const void*>(&hash_refine_kernel<true>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)refine_lds);
         hash_refine_kernel<true><<<dim3(refine_blocks, n_rounds), kRefineThreads, refine_lds, stream>>>(
-            q, R, half, n_rounds, rows, w.list, w.count, buckets);
+            q, R, half, n_rounds, rows, w.list, w.count, w.col_norm_max, buckets);
     } else {
         const size_t lds = kStageBytes + (size_t)rows_per_block * n_rounds * 2;
         hipFuncSetAttribute(reinterpret_cast<const void*>(&hash_kernel<false, kWaves, kPairsBf16>),
@@ -617,7 +694,7 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
         hipFuncSetAttribute(reinterpret_cast<const void*>(&hash_refine_kernel<false>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)refine_lds);
         hash_refine_kernel<false><<<dim3(refine_blocks, n_rounds), kRefineThreads, refine_lds, stream>>>(
-            q, R, half, n_rounds, rows, w.list, w.count, buckets);
+            q, R, half, n_rounds, rows, w.list, w.count, w.col_norm_max, buckets);
     }
     return hipGetLastError();
 }

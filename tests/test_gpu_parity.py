@@ -203,3 +203,28 @@ def test_attention_edge_inputs(gpu, variant, causal):
     got = out.float().cpu().numpy()
     assert (np.abs(got - ref["out"]) <= tol + np.abs(ref["out"]) * 2.0 ** -8).all()
     assert lse_close(lse.cpu().numpy(), ref["lse"], w.dtype).all()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_hash_exact_ties(gpu, dtype):
+    """Exact ties in [xR; -xR]: a duplicated column, a negated column and
+    all-zero queries.  The first index of [xR; -xR] must win, as in the
+    oracle; every such row-round goes through the exact second pass."""
+    w = small("mixture_bf16_L4096", B=1, H=2, L=2048, n_buckets=64, dtype=dtype)
+    x = W.make_inputs(w)
+    R = x["R"].copy()
+    half = w.n_buckets // 2
+    R[:, :, 9] = R[:, :, 5]      # x.R_9 == x.R_5: entry 5 beats entry 9
+    R[:, :, 7] = -R[:, :, 3]     # x.R_7 == -x.R_3: entry 7 beats entry half+3
+    q = x["q"].copy()
+    q[:, :, ::37, :] = 0         # all projections zero: entry 0 wins
+    q64 = W.as_f64(q, dtype)
+    want, near = oracle.lsh_hash(q64, R.astype(np.float64))
+    cfg = lsh.Config.of(w)
+    log("hash-ties", dtype, w)
+    got = lsh.lsh_hash(cfg, to_device(q, dtype), to_device(R, "f32")).cpu().numpy()
+    print(f"{dtype}: near-tie row-rounds {int(near.sum())}, zero-row ids {np.unique(want[:, :, ::37])}, "
+          f"ids 9 {(want == 9).sum()}, ids {half + 3}: {(want == half + 3).sum()}")
+    assert (want[:, :, ::37] == 0).all()
+    assert not (want == 9).any() and not (want == half + 3).any()
+    assert np.array_equal(got, want)
