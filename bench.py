@@ -1,6 +1,7 @@
 """Throughput of Reformer LSH attention on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                    [--cpu-budget S] [--copy-probe BYTES]
 
 One step is one full forward pass over one batch of the workload: hash, sort,
 chunked attention (with the gather fused into its staging) and the round
@@ -13,10 +14,20 @@ the CPU oracle's rate on a bounded sample of the same workload.
 The default workload is B=1, H=16, L=65536, d=64 (d_model 1024), bf16,
 n_buckets=1024, 8 hashing rounds, chunks of 64, causal, with queries from a
 mixture of 256 Gaussians.
+
+Roofline.  The dominant stage (largest time) is placed against the MI355X
+peak that bounds it: algorithmic work of the stage / the stage's average
+duration (HIP events around the stage's one library call on the stream it
+runs on).  `traffic` is the HBM traffic of that stage's kernels per call,
+from rocprofv3 FETCH_SIZE and WRITE_SIZE counters recorded under profiles/
+(scaled by what the same counters read for a plain device copy of known
+size, which --copy-probe launches after the timed steps); it is null when
+the kernel sources differ from the ones the counters were taken on.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -30,6 +41,45 @@ from paper_2001_04451_amd import workloads as W
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, TFLOP/s
+ROOT = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(ROOT, "paper_2001_04451_amd", "csrc")
+
+# Stages as the library runs them: the kernels of each call, the source files
+# they are built from, and the peak that bounds the stage's main kernel.
+STAGES = {
+    "hash": {"kernels": ["prep_r_cols_kernel", "prep_r_max_kernel", "hash_kernel",
+                         "hash_refine_kernel"],
+             "sources": ["hash.hip", "common.h"], "bound": "mfma", "work": "hash_flop"},
+    "sort": {"kernels": ["sort_hist_kernel", "sort_scan_kernel", "sort_scatter_kernel"],
+             "sources": ["sort.hip", "common.h"], "bound": "hbm", "work": "sort_bytes"},
+    "attn": {"kernels": ["attn_prep_kernel", "attn_fwd_bf16_kernel"],
+             "sources": ["attn_fwd.hip", "attn_common.h", "common.h"], "bound": "hbm",
+             "work": "attn_bytes"},
+    "combine": {"kernels": ["combine_kernel"], "sources": ["combine.hip", "common.h"],
+                "bound": "hbm", "work": "combine_bytes"},
+}
+
+
+def sources_digest(files) -> str:
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(workload: str, stage: str):
+    """HBM bytes per call of the stage from the committed counter summary, or
+    None when there is none or the stage's kernel sources have changed."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    st = rec.get("stages", {}).get(stage)
+    if not st or st.get("sources") != sources_digest(STAGES[stage]["sources"]):
+        return None
+    return st["bytes_per_call"]
 
 
 def algorithmic_work(w: W.Workload) -> dict:
@@ -45,9 +95,10 @@ def algorithmic_work(w: W.Workload) -> dict:
         "hash_flop": rr * d * w.n_buckets,
         # QK^T and PV over a 2m-key window: 2 * (2m * d) * 2 flops per row-round
         "attn_flop": rr * 8 * m * d,
-        # q and v rows read once per round (gathered), o_rounds row (dtype) and
-        # lse written, ids/positions read
-        "attn_bytes": rr * (2 * d * e + e * d + 4 + 3 * 4),
+        # per row-round: q and v rows gathered, o_rounds row (dtype) and lse
+        # written, the slot's position read, the token's bucket ids (two per
+        # 32-bit word) gathered
+        "attn_bytes": rr * (2 * d * e + e * d + 4 + 4 + 4 * ((n_r + 1) // 2)),
         # ids read twice, perm and undo written
         "sort_bytes": rr * 16,
         # per row: n_r o_rounds rows (dtype) + lse + undo read, one output row written
@@ -152,6 +203,9 @@ def main() -> int:
     ap.add_argument("--workload", default=W.HEADLINE, choices=sorted(W.WORKLOADS))
     ap.add_argument("--cpu-budget", type=float, default=8.0,
                     help="seconds of oracle time for the CPU baseline (0 to skip)")
+    ap.add_argument("--copy-probe", type=int, default=0,
+                    help="after timing, copy this many bytes device to device (a plain copy "
+                         "kernel of known size, to scale HBM traffic counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -164,28 +218,31 @@ def main() -> int:
     w = W.WORKLOADS[args.workload]
     lsh.lib()
     g = run_gpu(w, args.steps, args.warmup)
+    if args.copy_probe > 0:
+        n = args.copy_probe // 16 * 16
+        src = torch.ones(n // 4, dtype=torch.int32, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     work = algorithmic_work(w)
     st = g["stage_ms"]
-    # dominant kernel: the stage with the largest share of the step
+    # dominant stage: the one with the largest share of the step
     dom = max(st, key=st.get)
-    if dom == "attn":
-        achieved = work["attn_flop"] / (st["attn"] * 1e-3) / 1e12
+    spec = STAGES[dom]
+    if spec["bound"] == "mfma":
+        achieved = work[spec["work"]] / (st[dom] * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": BF16_MFMA_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "kernel": "attn_fwd_bf16_kernel"}
-    elif dom == "hash":
-        achieved = work["hash_flop"] / (st["hash"] * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": BF16_MFMA_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "kernel": "hash_kernel"}
-    elif dom == "combine":
-        achieved = work["combine_bytes"] / (st["combine"] * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "kernel": "combine_kernel"}
+                "unit": "TFLOP/s"}
     else:
-        achieved = work["sort_bytes"] / (st["sort"] * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "kernel": "sort (3 kernels)"}
+        achieved = work[spec["work"]] / (st[dom] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
+    roof["traffic"] = recorded_traffic(w.name, dom)
+    roof["stage"] = dom
+    roof["kernels"] = spec["kernels"]
+    roof["algorithmic"] = work[spec["work"]]
     tokens = w.B * w.L
     value = tokens / (g["ms_per_step"] * 1e-3)
     line = {
