@@ -92,11 +92,20 @@ __global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __rest
     int* wbase = base + wave * n_b;
 
     for (int i = threadIdx.x; i < kSortWaves * n_b; i += blockDim.x) base[i] = 0;
-    __syncthreads();
     const int p0 = tile * kTile + wave * kPerWave;
     const int p1 = min(L, p0 + kPerWave);
-    for (int p = p0 + lane; p < p1; p += 64)
-        atomicAdd(&wbase[clamp_bucket(buckets[(bh * L + p) * n_r + r], n_b)], 1);
+    // this lane's ids, all loads in flight at once (kPerWave / 64 per lane)
+    constexpr int kIter = kPerWave / 64;
+    int ids[kIter];
+#pragma unroll
+    for (int it = 0; it < kIter; ++it) {
+        const int pos = p0 + 64 * it + lane;
+        ids[it] = pos < p1 ? clamp_bucket(buckets[(bh * L + pos) * n_r + r], n_b) : 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int it = 0; it < kIter; ++it)
+        if (p0 + 64 * it + lane < p1) atomicAdd(&wbase[ids[it]], 1);
     __syncthreads();
     // Per-wave starting slot of every bucket: the tile's offset plus the counts
     // of the earlier waves of this tile.
@@ -113,10 +122,11 @@ __global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __rest
     int32_t* pseg = perm + seg * L;
     int32_t* useg = undo + seg * L;
     const uint64_t lt_mask = (1ull << lane) - 1ull;
-    for (int p = p0; p < p1; p += 64) {
-        const int pos = p + lane;
+#pragma unroll
+    for (int it = 0; it < kIter; ++it) {
+        const int pos = p0 + 64 * it + lane;
         const bool active = pos < p1;
-        const int b = active ? clamp_bucket(buckets[(bh * L + pos) * n_r + r], n_b) : 0;
+        const int b = ids[it];
         uint64_t peers = __ballot(active);
         for (int bit = 0; bit < n_bits; ++bit) {
             const bool set = (b >> bit) & 1;
