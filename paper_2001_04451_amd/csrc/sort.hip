@@ -47,6 +47,11 @@ __global__ __launch_bounds__(256) void sort_hist_kernel(const int32_t* __restric
     }
 }
 
+// Each thread owns a contiguous run of the segment's (bucket, tile) counts
+// and holds it in registers (16-byte loads, all in flight together), so the
+// scan costs one round trip to memory instead of one per count.
+constexpr int kScanPerThread = 64;  // counts per thread held in registers
+
 __global__ __launch_bounds__(256) void sort_scan_kernel(int32_t* __restrict__ counts, int L,
                                                         int n_b, int n_tiles,
                                                         int32_t* __restrict__ bucket_start) {
@@ -58,22 +63,63 @@ __global__ __launch_bounds__(256) void sort_scan_kernel(int32_t* __restrict__ co
     const int64_t per = (E + 255) / 256;
     const int64_t lo = min(E, threadIdx.x * per), hi = min(E, lo + per);
     int s = 0;
-    for (int64_t e = lo; e < hi; ++e) s += c[e];
-    part[threadIdx.x] = s;
-    __syncthreads();
-    // Hillis-Steele inclusive scan over 256 partial sums.
-    for (int o = 1; o < 256; o <<= 1) {
-        const int x = (int)threadIdx.x >= o ? part[threadIdx.x - o] : 0;
+    if (per <= kScanPerThread && (E & 3) == 0 && (per & 3) == 0) {
+        int v[kScanPerThread];
+#pragma unroll
+        for (int k = 0; k < kScanPerThread; k += 4) {
+            const int64_t e = lo + k;
+            int4 x = make_int4(0, 0, 0, 0);
+            if (k < per && e < hi) x = *reinterpret_cast<const int4*>(c + e);
+            v[k] = x.x;
+            v[k + 1] = x.y;
+            v[k + 2] = x.z;
+            v[k + 3] = x.w;
+        }
+#pragma unroll
+        for (int k = 0; k < kScanPerThread; ++k) s += v[k];
+        part[threadIdx.x] = s;
         __syncthreads();
-        part[threadIdx.x] += x;
+        for (int o = 1; o < 256; o <<= 1) {
+            const int x = (int)threadIdx.x >= o ? part[threadIdx.x - o] : 0;
+            __syncthreads();
+            part[threadIdx.x] += x;
+            __syncthreads();
+        }
+        int run = part[threadIdx.x] - s;
+#pragma unroll
+        for (int k = 0; k < kScanPerThread; k += 4) {
+            const int64_t e = lo + k;
+            if (k < per && e < hi) {
+                int4 x;
+                x.x = run;
+                x.y = run + v[k];
+                x.z = x.y + v[k + 1];
+                x.w = x.z + v[k + 2];
+                *reinterpret_cast<int4*>(c + e) = x;
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if ((e + u) % n_tiles == 0) bs[(e + u) / n_tiles] = u == 0 ? x.x : (u == 1 ? x.y : (u == 2 ? x.z : x.w));
+                run = x.w + v[k + 3];
+            }
+        }
+    } else {
+        for (int64_t e = lo; e < hi; ++e) s += c[e];
+        part[threadIdx.x] = s;
         __syncthreads();
-    }
-    int run = part[threadIdx.x] - s;
-    for (int64_t e = lo; e < hi; ++e) {
-        const int v = c[e];
-        c[e] = run;
-        if (e % n_tiles == 0) bs[e / n_tiles] = run;
-        run += v;
+        // Hillis-Steele inclusive scan over 256 partial sums.
+        for (int o = 1; o < 256; o <<= 1) {
+            const int x = (int)threadIdx.x >= o ? part[threadIdx.x - o] : 0;
+            __syncthreads();
+            part[threadIdx.x] += x;
+            __syncthreads();
+        }
+        int run = part[threadIdx.x] - s;
+        for (int64_t e = lo; e < hi; ++e) {
+            const int v = c[e];
+            c[e] = run;
+            if (e % n_tiles == 0) bs[e / n_tiles] = run;
+            run += v;
+        }
     }
     if (threadIdx.x == 0) bs[n_b] = L;
 }
