@@ -353,26 +353,41 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
             }
             lsum += __shfl_xor(lsum, 32);
             const bool alone = !(lsum > 0.f);  // only itself left as a target
+            if (__ballot(alone) != 0) {
+                // The output of a lone query is v_i: one more P V step on the
+                // diagonal tile with P = 1 at (i, i) for those queries and 0
+                // elsewhere adds exactly v_i to their (zero) accumulators.
+                // Query n's own key is key n of that tile, held by the lane
+                // half (n / 8) % 2 at element n % 8 of key group n / 16.
+                const bool mine = alone && h == ((n >> 3) & 1);
+                const uint32_t one = (n & 1) ? 0x3F800000u : 0x3F80u;  // bf16 1.0 in its half
+                const int kr_diag = ring_row(cq, qh * 32);
+#pragma unroll
+                for (int ku = 0; ku < 2; ++ku) {
+                    u32x4 pk;
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) pk[w] = (mine && (n >> 4) == ku && ((n & 7) >> 1) == w) ? one : 0u;
+                    const int kb = kr_diag + 16 * ku + 8 * h;
+#pragma unroll
+                    for (int dt = 0; dt < 2; ++dt) {
+                        const u32x4 va = *reinterpret_cast<const u32x4*>(S.Vt + vt_offset(32 * dt + n, kb));
+                        oacc[dt] = mfma32x32x16(as_bf16x8(va), as_bf16x8(pk), oacc[dt]);
+                    }
+                }
+            }
             const float mref = fast ? bound : m;
             uint16_t* orow = o_rounds + (seg * L + s_q) * kHeadDim;
-            const float inv = alone ? 0.f : 1.f / lsum;
+            // 1/l to within 1 ulp; the result is rounded to bf16.  A lone
+            // query divides its exact v_i by 1.
+            const float inv = alone ? 1.f : __builtin_amdgcn_rcpf(lsum);
 #pragma unroll
             for (int dt = 0; dt < 2; ++dt)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int d0 = 32 * dt + 8 * i + 4 * h;
                     uint2 o;
-                    if (alone) {  // v_i itself, copied bit for bit
-                        uint32_t e4[4];
-#pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            e4[e] = *reinterpret_cast<const uint16_t*>(S.Vt + vt_offset(d0 + e, rq & ~3) + (rq & 3) * 2);
-                        o.x = e4[0] | (e4[1] << 16);
-                        o.y = e4[2] | (e4[3] << 16);
-                    } else {
-                        o.x = pack_bf16x2(oacc[dt][4 * i] * inv, oacc[dt][4 * i + 1] * inv);
-                        o.y = pack_bf16x2(oacc[dt][4 * i + 2] * inv, oacc[dt][4 * i + 3] * inv);
-                    }
+                    o.x = pack_bf16x2(oacc[dt][4 * i] * inv, oacc[dt][4 * i + 1] * inv);
+                    o.y = pack_bf16x2(oacc[dt][4 * i + 2] * inv, oacc[dt][4 * i + 3] * inv);
                     *reinterpret_cast<uint2*>(orow + d0) = o;
                 }
             if (h == 0) {
