@@ -32,8 +32,9 @@
 // mask and log2 N_ij come together from one 33-entry LDS table indexed by that
 // popcount (index 32 = masked).  The softmax needs no running maximum when
 // the wave's logit bound B_i = scale*log2(e)*|q_i| is moderate: every logit
-// lies in [-B_i - log2 n_r, B_i], so exp2(x - B_i) neither overflows nor
-// underflows; waves with a larger bound fall back to the online maximum.
+// lies in [-B_i - log2 n_r, B_i], so for B_i <= 60 exp2(x) itself neither
+// overflows nor underflows; waves with a larger bound fall back to the online
+// maximum.  The row sum l_i adds the bf16-rounded weights that enter P V.
 #include "attn_common.h"
 #include "launch.h"
 
@@ -44,6 +45,14 @@ constexpr int kRing = 192;  // three chunk slots of 64 rows
 constexpr int kMaxBucketsStaged = 1024;
 constexpr float kFastBound = 60.f;  // largest B_i handled without a running maximum
 constexpr int kMaskedIndex = 32;    // table index of a masked-out key
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+constexpr bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
+
+template <bool B>
+struct BoolTag {
+    static constexpr bool value = B;
+};
 
 __device__ __forceinline__ int ring_row(int chunk, int i) { return ((chunk + 3) % 3) * kChunk + i; }
 
@@ -60,9 +69,23 @@ __device__ __forceinline__ constexpr uint32_t sig_guard(int w) {
     return (1u << (w + 10)) | (1u << (w + 21));
 }
 
+// (a & b) | c as one v_and_or_b32: left to itself the compiler regroups the
+// OR chain over the signature words into separate ANDs and three-way ORs.
+__device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t b, uint32_t c) {
+    uint32_t d;
+    asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(d) : "v"(a), "s"(b), "v"(c));
+    return d;
+}
+
 template <int NW>
 struct FwdSig {
     static constexpr int stride = NW <= 1 ? 1 : (NW <= 2 ? 2 : (NW <= 4 ? 4 : 8));  // words per token
+    // Per-token record gathered with every staged row: the signature words,
+    // zeros, and the key scale in the last word; 16, 32 or 64 bytes, so one
+    // record is one aligned run of 16-byte pieces.
+    static constexpr int rec_words = stride + 1 <= 4 ? 4 : (stride + 1 <= 8 ? 8 : 16);
+    static constexpr int pieces = rec_words / 4;
+    static constexpr int aux_per_thread = (4 * pieces + 7) / 8;  // pieces a thread loads per quad
 };
 
 template <int NW>
@@ -83,21 +106,20 @@ __device__ __forceinline__ uint32_t vt_offset(int d, int k) {
 }
 
 // Four consecutive rows of a batch, as loaded by one thread: 16-byte piece
-// `part` of each q and v row; thread part 0 (and 1 for eight words) also
-// brings the rows' signature words and part 2 their key scales.
+// `part` of each q and v row, and the record pieces k = part (+8) of the
+// quad (row k / pieces, piece k % pieces).
+template <int NW>
 struct RowQuad {
     u32x4 q[4], v[4];
-    u32x4 sig[4];
-    float cf[4];
+    u32x4 aux[FwdSig<NW>::aux_per_thread];
 };
 
 template <int NW>
-__device__ __forceinline__ void load_quad(RowQuad& R, const uint16_t* __restrict__ q,
+__device__ __forceinline__ void load_quad(RowQuad<NW>& R, const uint16_t* __restrict__ q,
                                           const uint16_t* __restrict__ v,
-                                          const float* __restrict__ cf_tok,
-                                          const uint32_t* __restrict__ sig_tok, int64_t bh, int L,
+                                          const u32x4* __restrict__ rec, int64_t bh, int L,
                                           const int (&pos)[4], int part) {
-    constexpr int SW = FwdSig<NW>::stride;
+    constexpr int PP = FwdSig<NW>::pieces;
     const u32x4 zero = {0, 0, 0, 0};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -105,32 +127,23 @@ __device__ __forceinline__ void load_quad(RowQuad& R, const uint16_t* __restrict
         const int64_t grow = bh * L + (ok ? pos[i] : 0);
         R.q[i] = ok ? *reinterpret_cast<const u32x4*>(q + grow * kHeadDim + part * 8) : zero;
         R.v[i] = ok ? *reinterpret_cast<const u32x4*>(v + grow * kHeadDim + part * 8) : zero;
-        R.sig[i] = zero;
-        R.cf[i] = 0.f;
-        const uint32_t* srow = sig_tok + grow * SW;
-        if (ok && part == 0) {
-            if constexpr (SW >= 4) {
-                R.sig[i] = *reinterpret_cast<const u32x4*>(srow);
-            } else if constexpr (SW == 2) {
-                const uint2 w = *reinterpret_cast<const uint2*>(srow);
-                R.sig[i][0] = w.x;
-                R.sig[i][1] = w.y;
-            } else {
-                R.sig[i][0] = srow[0];
-            }
-        }
-        if constexpr (SW == 8) {
-            if (ok && part == 1) R.sig[i] = *reinterpret_cast<const u32x4*>(srow + 4);
-        }
-        if (ok && part == 2) R.cf[i] = cf_tok[grow];
+    }
+#pragma unroll
+    for (int a = 0; a < FwdSig<NW>::aux_per_thread; ++a) {
+        const int k = part + 8 * a;
+        const int i = k / PP;  // row of the quad (k < 4 * PP)
+        const bool ok = k < 4 * PP && pos[i < 4 ? i : 0] >= 0;
+        const int64_t grow = bh * L + (ok ? pos[i] : 0);
+        R.aux[a] = ok ? rec[grow * PP + k % PP] : zero;
     }
 }
 
 // Store a quad at ring rows rr0 .. rr0+3 (Q rows, V transposed, signature
 // words and key scales).
 template <int NW>
-__device__ __forceinline__ void store_quad(FwdShared<NW>& S, const RowQuad& R, int rr0, int part) {
+__device__ __forceinline__ void store_quad(FwdShared<NW>& S, const RowQuad<NW>& R, int rr0, int part) {
     constexpr int SW = FwdSig<NW>::stride;
+    constexpr int PP = FwdSig<NW>::pieces;
 #pragma unroll
     for (int i = 0; i < 4; ++i) lds_store_piece(S.Qs, rr0 + i, part, R.q[i]);
     // V^T: dword e of a piece holds d = 8*part + 2e (low half) and 2e+1 (high)
@@ -146,18 +159,22 @@ __device__ __forceinline__ void store_quad(FwdShared<NW>& S, const RowQuad& R, i
         *reinterpret_cast<uint2*>(S.Vt + vt_offset(d, rr0)) = lo;
         *reinterpret_cast<uint2*>(S.Vt + vt_offset(d + 1, rr0)) = hi;
     }
-    if (part == 2) *reinterpret_cast<f32x4*>(&S.cf[rr0]) = f32x4{R.cf[0], R.cf[1], R.cf[2], R.cf[3]};
-    if (part == 0 || (SW == 8 && part == 1)) {
+    // record piece pc of row i: signature words 4pc..4pc+3 (those below SW),
+    // the key scale in word 3 of the last piece
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            uint32_t* dst = &S.sig[rr0 + i][4 * part];
+    for (int a = 0; a < FwdSig<NW>::aux_per_thread; ++a) {
+        const int k = part + 8 * a;
+        if (k < 4 * PP) {
+            const int i = k / PP, pc = k % PP;
+            uint32_t* dst = &S.sig[rr0 + i][0];
             if constexpr (SW >= 4) {
-                *reinterpret_cast<u32x4*>(dst) = R.sig[i];
+                if (4 * pc < SW) *reinterpret_cast<u32x4*>(dst + 4 * pc) = R.aux[a];
             } else if constexpr (SW == 2) {
-                *reinterpret_cast<uint2*>(dst) = make_uint2(R.sig[i][0], R.sig[i][1]);
+                *reinterpret_cast<uint2*>(dst) = make_uint2(R.aux[a][0], R.aux[a][1]);
             } else {
-                dst[0] = R.sig[i][0];
+                dst[0] = R.aux[a][0];
             }
+            if (pc == PP - 1) S.cf[rr0 + i] = __uint_as_float(R.aux[a][3]);
         }
     }
 }
@@ -201,8 +218,7 @@ __device__ __forceinline__ void quad_positions(const int32_t* __restrict__ pseg,
 template <int NW, bool CAUSAL>
 __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ v,
-    const float* __restrict__ cf_tok, const uint32_t* __restrict__ sig_tok,
-    const int32_t* __restrict__ perm,
+    const u32x4* __restrict__ rec, const int32_t* __restrict__ perm,
     const int32_t* __restrict__ bstart, uint16_t* __restrict__ o_rounds,
     float* __restrict__ lse_rounds, int L, int n_r, int n_b, float scale, float self_mask,
     int pairs_per_strip) {
@@ -227,12 +243,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
     // ---- stage the first window: chunk 2p0-1, then chunks 2p0 and 2p0+1 ----
     {
         int pos[4];
-        RowQuad R;
+        RowQuad<NW> R;
         quad_positions(pseg, 2 * p0 - 1, 1, true, n_chunks, L, tid, pos);
-        load_quad<NW>(R, q, v, cf_tok, sig_tok, bh, L, pos, part);
+        load_quad<NW>(R, q, v, rec, bh, L, pos, part);
         if (qrow < kChunk) store_quad<NW>(S, R, ring_row(2 * p0 - 1, qrow), part);
         quad_positions(pseg, 2 * p0, 2, true, n_chunks, L, tid, pos);
-        load_quad<NW>(R, q, v, cf_tok, sig_tok, bh, L, pos, part);
+        load_quad<NW>(R, q, v, rec, bh, L, pos, part);
         store_quad<NW>(S, R, ring_row(2 * p0 + qrow / kChunk, qrow % kChunk), part);
     }
     __syncthreads();
@@ -246,8 +262,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
     for (int p = p0; p < p1; ++p) {
         const bool more = p + 1 < p1;
         // the next pair's new chunks load during this pair's compute
-        RowQuad pf;
-        load_quad<NW>(pf, q, v, cf_tok, sig_tok, bh, L, pf_pos, part);
+        RowQuad<NW> pf;
+        load_quad<NW>(pf, q, v, rec, bh, L, pf_pos, part);
         int pf_pos2[4];
         quad_positions(pseg, 2 * (p + 2), 2, p + 2 < p1, n_chunks, L, tid, pf_pos2);
 
@@ -275,6 +291,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
                 const int tb = (cq - 1) * kChunk + kt * 32;
                 act[kt] = __ballot(lo <= hi && lo <= tb + 31 && hi >= tb) != 0;
             }
+            // FAST: every logit of the wave lies in [-B_i - log2 n_r, B_i] with
+            // B_i <= 60, so exp2 of the logit itself is a normal fp32 (and
+            // bf16) number: no running maximum and no offset are needed.
+            auto attend = [&](auto fast_tag) {
+            constexpr bool FAST = decltype(fast_tag)::value;
             float m = -__builtin_inff(), lsum = 0.f;
             f32x16 oacc[2] = {f32x16{}, f32x16{}};
 #pragma unroll
@@ -307,14 +328,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
                             uint32_t ksig[NW];
                             read_sig<NW>(S, kbase + e, ksig);
 #pragma unroll
-                            for (int w = 0; w < NW; ++w) t |= ((qsig[w] ^ ksig[w]) + sig_add(w)) & sig_guard(w);
+                            for (int w = 0; w < NW; ++w) t = and_or(((qsig[w] ^ ksig[w]) + sig_add(w)), sig_guard(w), t);
                         }
                         const float cfk = e < 4 ? c0[e] : c1[e - 4];
                         acc[j] = fmaf(acc[j], cfk, S.tab[__popc(t)]);
                     }
                 }
-                float off = bound;
-                if (!fast) {  // online maximum (both lane halves share the row max)
+                float off = 0.f;
+                if constexpr (!FAST) {  // online maximum (both lane halves share the row max)
                     float mt = acc[0];
 #pragma unroll
                     for (int j = 1; j < 16; ++j) mt = fmaxf(mt, acc[j]);
@@ -335,10 +356,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
 #pragma unroll
                     for (int e2 = 0; e2 < 4; ++e2) {
                         const int j = 8 * ku + 2 * e2;
-                        const float pa = __builtin_amdgcn_exp2f(acc[j] - off);
-                        const float pb2 = __builtin_amdgcn_exp2f(acc[j + 1] - off);
-                        lsum += pa + pb2;
-                        pk[ku][e2] = pack_bf16x2(pa, pb2);
+                        const float pa = __builtin_amdgcn_exp2f(FAST ? acc[j] : acc[j] - off);
+                        const float pb2 = __builtin_amdgcn_exp2f(FAST ? acc[j + 1] : acc[j + 1] - off);
+                        const uint32_t w2 = pack_bf16x2(pa, pb2);
+                        pk[ku][e2] = w2;
+                        // the row sum takes the bf16 weights that enter P V
+                        lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w2), kOnes, lsum, false);
                     }
 #pragma unroll
                 for (int ku = 0; ku < 2; ++ku) {
@@ -375,7 +398,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
                     }
                 }
             }
-            const float mref = fast ? bound : m;
+            const float mref = FAST ? 0.f : m;
             uint16_t* orow = o_rounds + (seg * L + s_q) * kHeadDim;
             // 1/l to within 1 ulp; the result is rounded to bf16.  A lone
             // query divides its exact v_i by 1.
@@ -394,6 +417,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
                 // z = scale*|q_i| - self_mask when the token is its own only target
                 lse_rounds[seg * L + s_q] = alone ? bound * kLn2 - self_mask : (mref + __log2f(lsum)) * kLn2;
             }
+            };
+            if (fast)
+                attend(BoolTag<true>{});
+            else
+                attend(BoolTag<false>{});
         }
 
         __syncthreads();  // every wave is done with the slots of chunks 2p-1 and 2p
@@ -484,16 +512,17 @@ __global__ __launch_bounds__(64) void attn_fwd_f32_kernel(
     }
 }
 
-// Per-token data that the chunk kernel gathers with every staged row, made
-// once instead of once per round: the key scale scale*log2(e)/|q| (0 for a
-// zero row) and the bucket signature words (see sig_add).  Eight lanes per
-// token, one 16-byte piece of the q row each.
-template <int SW>
+// Per-token record that the chunk kernel gathers with every staged row, made
+// once instead of once per round: the bucket signature words (see sig_add)
+// and the key scale scale*log2(e)/|q| (0 for a zero row) in the last word.
+// Eight lanes per token, one 16-byte piece of the q row each; lane p writes
+// record words p (and p + 8).
+template <int NW>
 __global__ __launch_bounds__(256) void attn_prep_kernel(const uint16_t* __restrict__ q,
                                                         const int32_t* __restrict__ buckets,
                                                         int64_t rows, int n_r, float scale_log2e,
-                                                        float* __restrict__ cf_tok,
-                                                        uint32_t* __restrict__ sig_tok) {
+                                                        uint32_t* __restrict__ rec) {
+    constexpr int SW = FwdSig<NW>::stride, RW = FwdSig<NW>::rec_words;
     const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 3;
     const int part = threadIdx.x & 7;
     if (row >= rows) return;  // whole groups of eight lanes leave together
@@ -507,15 +536,19 @@ __global__ __launch_bounds__(256) void attn_prep_kernel(const uint16_t* __restri
     ss += __shfl_xor(ss, 1);
     ss += __shfl_xor(ss, 2);
     ss += __shfl_xor(ss, 4);
-    if (part == 0) {
-        const float nn = sqrtf(ss);
-        cf_tok[row] = nn > 0.f ? scale_log2e / nn : 0.f;
-    }
-    if (part < SW) {
-        const int32_t* brow = buckets + row * n_r;
-        const uint32_t id0 = 2 * part < n_r ? (uint32_t)brow[2 * part] & 0x3FFu : 0u;
-        const uint32_t id1 = 2 * part + 1 < n_r ? (uint32_t)brow[2 * part + 1] & 0x3FFu : 0u;
-        sig_tok[row * SW + part] = (id0 << part) | (id1 << (part + 11));
+    const int32_t* brow = buckets + row * n_r;
+#pragma unroll
+    for (int w = part; w < RW; w += 8) {
+        uint32_t word = 0;
+        if (w < SW) {
+            const uint32_t id0 = 2 * w < n_r ? (uint32_t)brow[2 * w] & 0x3FFu : 0u;
+            const uint32_t id1 = 2 * w + 1 < n_r ? (uint32_t)brow[2 * w + 1] & 0x3FFu : 0u;
+            word = (id0 << w) | (id1 << (w + 11));
+        } else if (w == RW - 1) {
+            const float nn = sqrtf(ss);
+            word = __float_as_uint(nn > 0.f ? scale_log2e / nn : 0.f);
+        }
+        rec[row * RW + w] = word;
     }
 }
 
@@ -524,18 +557,16 @@ hipError_t launch_bf16(dim3 grid, bool causal, const uint16_t* q, const uint16_t
                        const int32_t* buckets, const int32_t* perm, const int32_t* bs, uint16_t* o,
                        float* lse, int64_t BH, int L, int n_r, int n_b, float scale, float self_mask,
                        int pps, void* workspace, hipStream_t stream) {
-    constexpr int SW = FwdSig<NW>::stride;
     const int64_t rows = BH * L;
-    float* cf_tok = static_cast<float*>(workspace);
-    uint32_t* sig_tok = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + align256((size_t)rows * 4));
-    attn_prep_kernel<SW><<<(unsigned)((rows * 8 + 255) / 256), 256, 0, stream>>>(
-        q, buckets, rows, n_r, scale * kLog2e, cf_tok, sig_tok);
+    u32x4* rec = static_cast<u32x4*>(workspace);
+    attn_prep_kernel<NW><<<(unsigned)((rows * 8 + 255) / 256), 256, 0, stream>>>(
+        q, buckets, rows, n_r, scale * kLog2e, reinterpret_cast<uint32_t*>(rec));
     if (causal)
-        attn_fwd_bf16_kernel<NW, true><<<grid, 256, 0, stream>>>(q, v, cf_tok, sig_tok, perm, bs, o,
-                                                                 lse, L, n_r, n_b, scale, self_mask, pps);
+        attn_fwd_bf16_kernel<NW, true><<<grid, 256, 0, stream>>>(q, v, rec, perm, bs, o, lse, L, n_r,
+                                                                 n_b, scale, self_mask, pps);
     else
-        attn_fwd_bf16_kernel<NW, false><<<grid, 256, 0, stream>>>(q, v, cf_tok, sig_tok, perm, bs, o,
-                                                                  lse, L, n_r, n_b, scale, self_mask, pps);
+        attn_fwd_bf16_kernel<NW, false><<<grid, 256, 0, stream>>>(q, v, rec, perm, bs, o, lse, L, n_r,
+                                                                  n_b, scale, self_mask, pps);
     return hipGetLastError();
 }
 
@@ -549,7 +580,9 @@ int sig_words(int n_rounds) {
 size_t attn_fwd_workspace_bytes(int64_t BH, int L, int n_rounds, bool f32) {
     if (f32) return 0;
     const size_t rows = (size_t)BH * L;
-    return align256(rows * 4) + align256(rows * 4 * sig_words(n_rounds));
+    const int sw = sig_words(n_rounds);
+    const size_t rec_words = sw + 1 <= 4 ? 4 : (sw + 1 <= 8 ? 8 : 16);
+    return align256(rows * 4 * rec_words);
 }
 
 hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, bool causal,
