@@ -12,23 +12,29 @@
 //
 // Logits are kept in log2 units: x = (q_i.q_j) * scale*log2(e)/|q_j| - log2 N_ij.
 //
-// bf16 path (gfx950 matrix cores).  A workgroup walks a strip of chunk
-// pairs of one segment.  The rows of the three live chunks (c0-1, c0, c0+1)
-// sit in an LDS ring of three 64-row slots (chunk c in slot (c+3) % 3): the
-// query/key rows as XOR-swizzled 128-byte rows, V transposed (row d holds the
-// 192 ring keys) so that the V^T operand is one 16-byte read.  Moving to the
-// next pair only brings in two new chunks; their loads are issued before the
-// current pair computes and land in LDS after it.  Each wave takes 32
-// queries against their 128-key window as four 32x32 tiles:
-// S^T = K Q^T on mfma_f32_32x32x16_bf16, masks and softmax on the
-// accumulators, then O^T = V^T P^T with the accumulators reused as the B
-// operand (the K rows are loaded in a permuted order; see kappa).  Tiles with
-// no valid key for the wave's queries are skipped.
+// bf16 path (gfx950 matrix cores).  A workgroup of four waves walks a strip
+// of chunks of one segment, one chunk per step.  The rows of chunks c-1, c
+// and the incoming c+1 sit in an LDS ring of three 64-row slots: q and v rows
+// as XOR-swizzled 128-byte rows, the signature words and the key scales.  The
+// slot that chunk c+1 lands in held chunk c-2, which step c never reads, so
+// the next chunk is gathered (through perm) straight from global memory into
+// LDS while step c computes (global_load_lds: no registers, no vector
+// instructions), and one barrier per step suffices.
+//
+// Each wave takes 16 queries of the chunk against their 128-key window as
+// eight 16x16 tiles: S^T = K Q^T on mfma_f32_16x16x32_bf16 (lane l holds keys
+// 4(l/16)..+3 of query l%16), masks and softmax on those four accumulators,
+// then O^T = V^T P^T on mfma_f32_16x16x16_bf16 with the accumulators packed
+// as the B operand as they are, and the V^T operand read from the v rows by
+// the LDS transpose read.  Tiles with no valid key for the wave's queries are
+// skipped.  A query's interval comes from the window's bucket boundaries: a
+// 128-bit mask (two ballots) of the slots whose round-r bucket differs from
+// the previous slot's; lo is the last boundary at or before the query.
 //
 // Per score element the VALU work is what bounds this kernel, so it is kept
 // to a few instructions: the interval mask is one bit of a per-lane word, the
 // count of rounds in which i and j differ is one popcount over the guard bits
-// of the packed bucket signatures (all words merged, see sig_word), and the
+// of the packed bucket signatures (all words merged, see sig_add), and the
 // mask and log2 N_ij come together from one 33-entry LDS table indexed by that
 // popcount (index 32 = masked).  The softmax needs no running maximum when
 // the wave's logit bound B_i = scale*log2(e)*|q_i| is moderate: every logit
@@ -41,12 +47,13 @@
 namespace lsh {
 namespace {
 
-constexpr int kRing = 192;  // three chunk slots of 64 rows
-constexpr int kMaxBucketsStaged = 1024;
+constexpr int kRing = 192;          // three chunk slots of 64 rows
 constexpr float kFastBound = 60.f;  // largest B_i handled without a running maximum
 constexpr int kMaskedIndex = 32;    // table index of a masked-out key
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 constexpr bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
 
 template <bool B>
@@ -81,102 +88,51 @@ template <int NW>
 struct FwdSig {
     static constexpr int stride = NW <= 1 ? 1 : (NW <= 2 ? 2 : (NW <= 4 ? 4 : 8));  // words per token
     // Per-token record gathered with every staged row: the signature words,
-    // zeros, and the key scale in the last word; 16, 32 or 64 bytes, so one
-    // record is one aligned run of 16-byte pieces.
+    // zeros, and the key scale in the last word; 16, 32 or 64 bytes.
     static constexpr int rec_words = stride + 1 <= 4 ? 4 : (stride + 1 <= 8 ? 8 : 16);
-    static constexpr int pieces = rec_words / 4;
-    static constexpr int aux_per_thread = (4 * pieces + 7) / 8;  // pieces a thread loads per quad
 };
 
 template <int NW>
 struct FwdShared {
-    char Qs[kRing * 128];           // query/key rows (swizzled)
-    char Vt[kHeadDim * kRing * 2];  // V^T: row d, 16-byte blocks of 8 keys (swizzled)
-    float cf[kRing];                // scale*log2(e)/|q_row| (0 for a zero row)
-    uint32_t sig[kRing][FwdSig<NW>::stride];  // bucket signature words (0 outside the sequence)
-    int bstart[kMaxBucketsStaged + 1];  // the segment's bucket starts
-    float tab[kMaskedIndex + 1];        // -log2 N by mismatch count; -inf = masked
+    char Qs[kRing * 128];  // q rows, 16-byte pieces at swizzled slots (see swz)
+    char Vs[kRing * 128];  // v rows, same layout
+    uint32_t sig[kRing][FwdSig<NW>::stride];  // bucket signature words
+    float cf[kRing];                          // scale*log2(e)/|q_row| (0 for a zero row)
+    float tab[kMaskedIndex + 1];              // -log2 N by mismatch count; -inf = masked
 };
 
-// Byte offset of keys k..k+3 (k % 4 == 0) in row d of V^T.  Block b of row d
-// sits at b ^ vt_swz(d): the 16 rows read together land in distinct banks.
-__device__ __forceinline__ int vt_swz(int d) { return (d + (d >> 3)) & 7; }
-__device__ __forceinline__ uint32_t vt_offset(int d, int k) {
-    return (uint32_t)d * (kRing * 2) + (uint32_t)(((k >> 3) ^ vt_swz(d)) << 4) + (uint32_t)((k & 4) << 1);
+__device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma16x16x16(bf16x4 a, bf16x4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
 }
 
-// Four consecutive rows of a batch, as loaded by one thread: 16-byte piece
-// `part` of each q and v row, and the record pieces k = part (+8) of the
-// quad (row k / pieces, piece k % pieces).
-template <int NW>
-struct RowQuad {
-    u32x4 q[4], v[4];
-    u32x4 aux[FwdSig<NW>::aux_per_thread];
-};
-
-template <int NW>
-__device__ __forceinline__ void load_quad(RowQuad<NW>& R, const uint16_t* __restrict__ q,
-                                          const uint16_t* __restrict__ v,
-                                          const u32x4* __restrict__ rec, int64_t bh, int L,
-                                          const int (&pos)[4], int part) {
-    constexpr int PP = FwdSig<NW>::pieces;
-    const u32x4 zero = {0, 0, 0, 0};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const bool ok = pos[i] >= 0;
-        const int64_t grow = bh * L + (ok ? pos[i] : 0);
-        R.q[i] = ok ? *reinterpret_cast<const u32x4*>(q + grow * kHeadDim + part * 8) : zero;
-        R.v[i] = ok ? *reinterpret_cast<const u32x4*>(v + grow * kHeadDim + part * 8) : zero;
-    }
-#pragma unroll
-    for (int a = 0; a < FwdSig<NW>::aux_per_thread; ++a) {
-        const int k = part + 8 * a;
-        const int i = k / PP;  // row of the quad (k < 4 * PP)
-        const bool ok = k < 4 * PP && pos[i < 4 ? i : 0] >= 0;
-        const int64_t grow = bh * L + (ok ? pos[i] : 0);
-        R.aux[a] = ok ? rec[grow * PP + k % PP] : zero;
-    }
+// Copy 16 (4) bytes per lane from global memory to LDS at lds_base + 16
+// (4) * lane; lds_base is uniform over the wave.
+__device__ __forceinline__ void copy16_to_lds(const void* src, void* lds_base) {
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                     (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+__device__ __forceinline__ void copy4_to_lds(const void* src, void* lds_base) {
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                     (__attribute__((address_space(3))) void*)lds_base, 4, 0, 0);
 }
 
-// Store a quad at ring rows rr0 .. rr0+3 (Q rows, V transposed, signature
-// words and key scales).
-template <int NW>
-__device__ __forceinline__ void store_quad(FwdShared<NW>& S, const RowQuad<NW>& R, int rr0, int part) {
-    constexpr int SW = FwdSig<NW>::stride;
-    constexpr int PP = FwdSig<NW>::pieces;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) lds_store_piece(S.Qs, rr0 + i, part, R.q[i]);
-    // V^T: dword e of a piece holds d = 8*part + 2e (low half) and 2e+1 (high)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const uint32_t a0 = R.v[0][e], a1 = R.v[1][e], a2 = R.v[2][e], a3 = R.v[3][e];
-        uint2 lo, hi;
-        lo.x = (a0 & 0xFFFFu) | (a1 << 16);
-        lo.y = (a2 & 0xFFFFu) | (a3 << 16);
-        hi.x = (a0 >> 16) | (a1 & 0xFFFF0000u);
-        hi.y = (a2 >> 16) | (a3 & 0xFFFF0000u);
-        const int d = 8 * part + 2 * e;
-        *reinterpret_cast<uint2*>(S.Vt + vt_offset(d, rr0)) = lo;
-        *reinterpret_cast<uint2*>(S.Vt + vt_offset(d + 1, rr0)) = hi;
-    }
-    // record piece pc of row i: signature words 4pc..4pc+3 (those below SW),
-    // the key scale in word 3 of the last piece
-#pragma unroll
-    for (int a = 0; a < FwdSig<NW>::aux_per_thread; ++a) {
-        const int k = part + 8 * a;
-        if (k < 4 * PP) {
-            const int i = k / PP, pc = k % PP;
-            uint32_t* dst = &S.sig[rr0 + i][0];
-            if constexpr (SW >= 4) {
-                if (4 * pc < SW) *reinterpret_cast<u32x4*>(dst + 4 * pc) = R.aux[a];
-            } else if constexpr (SW == 2) {
-                *reinterpret_cast<uint2*>(dst) = make_uint2(R.aux[a][0], R.aux[a][1]);
-            } else {
-                dst[0] = R.aux[a][0];
-            }
-            if (pc == PP - 1) S.cf[rr0 + i] = __uint_as_float(R.aux[a][3]);
-        }
-    }
+// V^T operand of a 16x16x16 product for keys r0 .. r0+15 and dims d0 .. d0+15:
+// lane l needs V[r0 + 4(l/16) + k][d0 + l%16] for k = 0..3.  The transposing
+// read gives lane i of each 16-lane group element i%4 of the 8-byte runs read
+// by lanes 4k + i/4, so lane i reads row r0 + 4(l/16) + i/4, dims
+// d0 + 4(i%4) .. +3.
+__device__ __forceinline__ bf16x4 vt_operand(const char* Vs, int r0, int d0, int lane) {
+    const int i = lane & 15;
+    const int row = r0 + 4 * (lane >> 4) + (i >> 2);
+    const int d = d0 + 4 * (i & 3);
+    const uint32_t off = row_piece_offset(row, d >> 3) + (uint32_t)((d & 4) << 1);
+    typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+    const i16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4*)((__attribute__((address_space(3))) char*)Vs + off));
+    return __builtin_bit_cast(bf16x4, x);
 }
 
 template <int NW>
@@ -187,7 +143,7 @@ __device__ __forceinline__ void read_sig(const FwdShared<NW>& S, int row, uint32
         const uint2 w = *reinterpret_cast<const uint2*>(&S.sig[row][0]);
         out[0] = w.x;
         out[1] = w.y;
-    } else if constexpr (NW > 2) {
+    } else {
 #pragma unroll
         for (int w4 = 0; w4 < (NW + 3) / 4; ++w4) {
             const u32x4 w = *reinterpret_cast<const u32x4*>(&S.sig[row][4 * w4]);
@@ -198,237 +154,218 @@ __device__ __forceinline__ void read_sig(const FwdShared<NW>& S, int row, uint32
     }
 }
 
-// Slots of the quads that thread `tid` loads for the batch of chunks
-// c_first .. c_first + n_chunks_batch - 1 (four consecutive rows per group of
-// eight threads); -1 outside the sequence or past the strip.
-__device__ __forceinline__ void quad_positions(const int32_t* __restrict__ pseg, int c_first,
-                                               int n_chunks_batch, bool live, int n_chunks, int L,
-                                               int tid, int (&pos)[4]) {
-    const int g = tid >> 3;
-    const int chunk = c_first + (4 * g) / kChunk;
-    const bool ok = live && g < n_chunks_batch * (kChunk / 4) && chunk >= 0 && chunk < n_chunks;
-    int4 p4 = make_int4(-1, -1, -1, -1);
-    if (ok) p4 = *reinterpret_cast<const int4*>(pseg + (int64_t)c_first * kChunk + 4 * g);
-    pos[0] = ok ? min(max(p4.x, 0), L - 1) : -1;
-    pos[1] = ok ? min(max(p4.y, 0), L - 1) : -1;
-    pos[2] = ok ? min(max(p4.z, 0), L - 1) : -1;
-    pos[3] = ok ? min(max(p4.w, 0), L - 1) : -1;
-}
-
 template <int NW, bool CAUSAL>
-__global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ v,
-    const u32x4* __restrict__ rec, const int32_t* __restrict__ perm,
-    const int32_t* __restrict__ bstart, uint16_t* __restrict__ o_rounds,
-    float* __restrict__ lse_rounds, int L, int n_r, int n_b, float scale, float self_mask,
-    int pairs_per_strip) {
+__global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ v, const uint32_t* __restrict__ rec,
+    const int32_t* __restrict__ perm, uint16_t* __restrict__ o_rounds,
+    float* __restrict__ lse_rounds, int L, int n_r, float scale, float self_mask,
+    int chunks_per_strip) {
     __shared__ __attribute__((aligned(16))) FwdShared<NW> S;
+    constexpr int SW = FwdSig<NW>::stride, RW = FwdSig<NW>::rec_words;
 
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int n = lane & 15, g = lane >> 4;  // query (and key row) of the lane, key group
     const int64_t seg = blockIdx.y;
     const int64_t bh = seg / n_r;
     const int r = (int)(seg % n_r);
     const int n_chunks = L / kChunk;
-    const int n_pairs = (n_chunks + 1) / 2;
-    const int p0 = blockIdx.x * pairs_per_strip;
-    const int p1 = min(n_pairs, p0 + pairs_per_strip);
+    const int c0 = blockIdx.x * chunks_per_strip;
+    const int c1 = min(n_chunks, c0 + chunks_per_strip);
     const float scale_log2e = scale * kLog2e;
     const int32_t* pseg = perm + seg * L;
-    const int part = tid & 7;
-    const int qrow = 4 * (tid >> 3);  // first row of this thread's quad in a batch
-    for (int b = tid; b <= n_b; b += 256) S.bstart[b] = bstart[seg * (n_b + 1) + b];
-    if (tid <= kMaskedIndex)
-        S.tab[tid] = tid < n_r ? -__log2f((float)(n_r - tid)) : -__builtin_inff();
+    const int64_t rowbase = bh * L;
+    const int rw = r >> 1, rsh = (r >> 1) + 11 * (r & 1);  // field r of a signature
+    if (tid <= kMaskedIndex) S.tab[tid] = tid < n_r ? -__log2f((float)(n_r - tid)) : -__builtin_inff();
 
-    // ---- stage the first window: chunk 2p0-1, then chunks 2p0 and 2p0+1 ----
-    {
-        int pos[4];
-        RowQuad<NW> R;
-        quad_positions(pseg, 2 * p0 - 1, 1, true, n_chunks, L, tid, pos);
-        load_quad<NW>(R, q, v, rec, bh, L, pos, part);
-        if (qrow < kChunk) store_quad<NW>(S, R, ring_row(2 * p0 - 1, qrow), part);
-        quad_positions(pseg, 2 * p0, 2, true, n_chunks, L, tid, pos);
-        load_quad<NW>(R, q, v, rec, bh, L, pos, part);
-        store_quad<NW>(S, R, ring_row(2 * p0 + qrow / kChunk, qrow % kChunk), part);
-    }
+    // Position of row `lane` of chunk cc; outside the sequence any valid row
+    // (those slots are never a valid key, see lo below).
+    auto chunk_pos = [&](int cc) -> int {
+        if (cc < 0 || cc >= n_chunks) return 0;
+        return min(max(pseg[(int64_t)cc * kChunk + lane], 0), L - 1);
+    };
+    // Gather chunk cc into its ring slot: wave w copies q and v rows
+    // 16w .. 16w+15 (each lane the piece that belongs at its LDS slot), and
+    // the signature words and key scales are split over the waves.
+    auto stage = [&](int cc, int pos_lane) {
+        const int slot0 = ring_row(cc, 0);
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const int row = 16 * wave + 8 * k + (lane >> 3);
+            const int p = __shfl(pos_lane, row);
+            const int64_t off = (rowbase + p) * kHeadDim + swz(row, lane & 7) * 8;
+            copy16_to_lds(q + off, S.Qs + (slot0 + 16 * wave + 8 * k) * 128);
+            copy16_to_lds(v + off, S.Vs + (slot0 + 16 * wave + 8 * k) * 128);
+        }
+        if constexpr (SW >= 4) {
+            constexpr int U = SW / 4;  // 16-byte units per row
+#pragma unroll
+            for (int k = 0; k < U; ++k)
+                if (wave == k) {
+                    const int u = 64 * k + lane, row = u / U;
+                    const int p = __shfl(pos_lane, row);
+                    copy16_to_lds(rec + (rowbase + p) * RW + 4 * (u % U), &S.sig[slot0][0] + 256 * k);
+                }
+        } else {
+#pragma unroll
+            for (int k = 0; k < SW; ++k)
+                if (wave == k) {
+                    const int u = 64 * k + lane, row = u / SW;
+                    const int p = __shfl(pos_lane, row);
+                    copy4_to_lds(rec + (rowbase + p) * RW + (u % SW), &S.sig[slot0][0] + 64 * k);
+                }
+        }
+        if (wave == 3) copy4_to_lds(rec + (rowbase + pos_lane) * RW + (RW - 1), &S.cf[slot0]);
+    };
+
+    stage(c0 - 1, chunk_pos(c0 - 1));
+    stage(c0, chunk_pos(c0));
+    int pf_pos = chunk_pos(c0 + 1);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
-    const int lane = tid & 63, wave = tid >> 6, h = lane >> 5, n = lane & 31;
-    const int cw = wave >> 1, qh = wave & 1;
+    for (int c = c0; c < c1; ++c) {
+        if (c + 1 < c1) stage(c + 1, pf_pos);
+        const int pf_next = chunk_pos(c + 2);
 
-    int pf_pos[4];
-    quad_positions(pseg, 2 * (p0 + 1), 2, p0 + 1 < p1, n_chunks, L, tid, pf_pos);
+        // ---- this wave's 16 queries of chunk c ----
+        const int u = 16 * wave + n;  // query row inside the chunk
+        const int s_q = c * kChunk + u;
+        const int rq = ring_row(c, u);
+        uint32_t qsig[NW > 0 ? NW : 1];
+        read_sig<NW>(S, rq, qsig);
+        const bf16x8 qb0 = as_bf16x8(lds_piece(S.Qs, rq, g));
+        const bf16x8 qb1 = as_bf16x8(lds_piece(S.Qs, rq, 4 + g));
+        const float cfq = S.cf[rq];
+        const float bound = cfq > 0.f ? scale_log2e * scale_log2e / cfq : 0.f;  // B_i
+        const bool fast = __ballot(!(bound <= kFastBound)) == 0;
 
-    for (int p = p0; p < p1; ++p) {
-        const bool more = p + 1 < p1;
-        // the next pair's new chunks load during this pair's compute
-        RowQuad<NW> pf;
-        load_quad<NW>(pf, q, v, rec, bh, L, pf_pos, part);
-        int pf_pos2[4];
-        quad_positions(pseg, 2 * (p + 2), 2, p + 2 < p1, n_chunks, L, tid, pf_pos2);
-
-        // ---- compute: per key tile, S^T, masks, softmax, P V ----
-        const int cq = 2 * p + cw;  // this wave's query chunk
-        if (cq < n_chunks) {
-            const int rq = ring_row(cq, qh * 32 + n);
-            const int s_q = cq * kChunk + qh * 32 + n;
-            uint32_t qsig[NW > 0 ? NW : 1];
-            read_sig<NW>(S, rq, qsig);
-            // the query's bucket in this round: field r of its signature
-            const int beta = min((int)((qsig[r >> 1] >> ((r >> 1) + 11 * (r & 1))) & 0x3FFu), n_b - 1);
-            const int wlo = max(0, (cq - 1) * kChunk);
-            const int lo = max(S.bstart[beta], wlo);
-            const int hi = CAUSAL ? s_q - 1 : min(S.bstart[beta + 1], (cq + 1) * kChunk) - 1;
-            bf16x8 qb[4];
+        // bucket boundaries of the window (chunks c-1, c): bit k of bA (bB)
+        // is set when slot k of chunk c-1 (c) starts a new round-r bucket
+        const uint32_t kA = (S.sig[ring_row(c - 1, lane)][rw] >> rsh) & 0x3FFu;
+        const uint32_t kB = (S.sig[ring_row(c, lane)][rw] >> rsh) & 0x3FFu;
+        const uint32_t prevA = __shfl_up(kA, 1);
+        const uint32_t lastA = __shfl(kA, 63);
+        const uint32_t prevB0 = __shfl_up(kB, 1);
+        const uint32_t prevB = lane == 0 ? lastA : prevB0;
+        const uint64_t bA = __ballot(lane == 0 || kA != prevA);
+        const uint64_t bB = __ballot(kB != prevB);
+        const uint64_t upto = bB & (~0ull >> (63 - u));
+        const int lo_w = upto ? 127 - __clzll(upto) : 63 - __clzll(bA);
+        const int lo = max((c - 1) * kChunk + lo_w, 0);
+        int hi;
+        if constexpr (CAUSAL) {
+            hi = s_q - 1;
+        } else {
+            const uint64_t after = u < 63 ? bB & (~0ull << (u + 1)) : 0ull;
+            hi = (c - 1) * kChunk + (after ? 62 + __ffsll((long long)after) : 127);
+        }
+        bool act[8];
 #pragma unroll
-            for (int s = 0; s < 4; ++s) qb[s] = row_operand(S.Qs, rq, h, s);
-            const float cfq = S.cf[rq];
-            const float bound = cfq > 0.f ? scale_log2e * scale_log2e / cfq : 0.f;  // B_i
-            const bool fast = __ballot(!(bound <= kFastBound)) == 0;
-            bool act[4];
-#pragma unroll
-            for (int kt = 0; kt < 4; ++kt) {
-                const int tb = (cq - 1) * kChunk + kt * 32;
-                act[kt] = __ballot(lo <= hi && lo <= tb + 31 && hi >= tb) != 0;
-            }
-            // FAST: every logit of the wave lies in [-B_i - log2 n_r, B_i] with
-            // B_i <= 60, so exp2 of the logit itself is a normal fp32 (and
-            // bf16) number: no running maximum and no offset are needed.
-            auto attend = [&](auto fast_tag) {
+        for (int kt = 0; kt < 8; ++kt) {
+            const int tb = (c - 1) * kChunk + 16 * kt;
+            act[kt] = __ballot(lo <= hi && lo <= tb + 15 && hi >= tb) != 0;
+        }
+
+        auto attend = [&](auto fast_tag) {
             constexpr bool FAST = decltype(fast_tag)::value;
             float m = -__builtin_inff(), lsum = 0.f;
-            f32x16 oacc[2] = {f32x16{}, f32x16{}};
+            f32x4 oacc[4] = {f32x4{}, f32x4{}, f32x4{}, f32x4{}};
 #pragma unroll
-            for (int kt = 0; kt < 4; ++kt) {
+            for (int kt = 0; kt < 8; ++kt) {
                 if (!act[kt]) continue;
-                const int kr0 = ring_row(cq - 1 + (kt >> 1), (kt & 1) * 32);
-                f32x16 acc = {};
-#pragma unroll
-                for (int s = 0; s < 4; ++s)
-                    acc = mfma32x32x16(row_operand(S.Qs, kr0 + kappa(n), h, s), qb[s], acc);
-                // masked keys of this lane's query: bit k of minv <-> tile key 8h + k
-                const int tb = (cq - 1) * kChunk + kt * 32;
-                const int lo_t = max(lo - tb, 0), hi_t = min(hi - tb, 31);
-                uint32_t valid = lo_t <= hi_t ? (0xFFFFFFFFu >> (31 - hi_t)) & (0xFFFFFFFFu << lo_t) : 0u;
+                const int kr0 = ring_row(c - 1 + (kt >> 2), 16 * (kt & 3));
+                f32x4 acc = mfma16x16x32(as_bf16x8(lds_piece(S.Qs, kr0 + n, g)), qb0, f32x4{});
+                acc = mfma16x16x32(as_bf16x8(lds_piece(S.Qs, kr0 + n, 4 + g)), qb1, acc);
+                // masked keys of this lane's query: bit k of minv <-> tile key 4g + k
+                const int tb = (c - 1) * kChunk + 16 * kt;
+                const int lo_t = max(lo - tb, 0), hi_t = min(hi - tb, 15);
+                uint32_t valid = lo_t <= hi_t ? (0xFFFFu >> (15 - hi_t)) & (0xFFFFu << lo_t) : 0u;
                 if constexpr (!CAUSAL) {
                     const int self_t = s_q - tb;
-                    if (self_t >= 0 && self_t < 32) valid &= ~(1u << self_t);
+                    if (self_t >= 0 && self_t < 16) valid &= ~(1u << self_t);
                 }
-                const uint32_t minv = ~valid >> (8 * h);
+                const uint32_t minv = ~valid >> (4 * g);
+                const int kbase = kr0 + 4 * g;
+                const f32x4 cfk = *reinterpret_cast<const f32x4*>(&S.cf[kbase]);
 #pragma unroll
-                for (int run = 0; run < 2; ++run) {
-                    const int kbase = kr0 + 16 * run + 8 * h;
-                    const f32x4 c0 = *reinterpret_cast<const f32x4*>(&S.cf[kbase]);
-                    const f32x4 c1 = *reinterpret_cast<const f32x4*>(&S.cf[kbase + 4]);
+                for (int j = 0; j < 4; ++j) {
+                    uint32_t t = (uint32_t)((int32_t)(minv << (31 - j)) >> 31);
+                    if constexpr (NW > 0) {
+                        uint32_t ksig[NW];
+                        read_sig<NW>(S, kbase + j, ksig);
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const int j = 8 * run + e;
-                        uint32_t t = (uint32_t)((int32_t)(minv << (31 - (16 * run + e))) >> 31);
-                        if constexpr (NW > 0) {
-                            uint32_t ksig[NW];
-                            read_sig<NW>(S, kbase + e, ksig);
-#pragma unroll
-                            for (int w = 0; w < NW; ++w) t = and_or(((qsig[w] ^ ksig[w]) + sig_add(w)), sig_guard(w), t);
-                        }
-                        const float cfk = e < 4 ? c0[e] : c1[e - 4];
-                        acc[j] = fmaf(acc[j], cfk, S.tab[__popc(t)]);
+                        for (int w = 0; w < NW; ++w) t = and_or((qsig[w] ^ ksig[w]) + sig_add(w), sig_guard(w), t);
                     }
+                    acc[j] = fmaf(acc[j], cfk[j], S.tab[__popc(t)]);
                 }
                 float off = 0.f;
-                if constexpr (!FAST) {  // online maximum (both lane halves share the row max)
-                    float mt = acc[0];
-#pragma unroll
-                    for (int j = 1; j < 16; ++j) mt = fmaxf(mt, acc[j]);
+                if constexpr (!FAST) {  // online maximum over the four lane groups of a query
+                    float mt = fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3]));
+                    mt = fmaxf(mt, __shfl_xor(mt, 16));
                     mt = fmaxf(mt, __shfl_xor(mt, 32));
                     const float m_new = fmaxf(m, mt);
                     off = m_new > -__builtin_inff() ? m_new : 0.f;
                     const float corr = __builtin_amdgcn_exp2f(m - off);
                     lsum *= corr;
 #pragma unroll
-                    for (int dt = 0; dt < 2; ++dt)
-#pragma unroll
-                        for (int k = 0; k < 16; ++k) oacc[dt][k] *= corr;
+                    for (int b = 0; b < 4; ++b) oacc[b] *= corr;
                     m = m_new;
                 }
-                u32x4 pk[2];
+                uint32_t pw[2];
 #pragma unroll
-                for (int ku = 0; ku < 2; ++ku)
-#pragma unroll
-                    for (int e2 = 0; e2 < 4; ++e2) {
-                        const int j = 8 * ku + 2 * e2;
-                        const float pa = __builtin_amdgcn_exp2f(FAST ? acc[j] : acc[j] - off);
-                        const float pb2 = __builtin_amdgcn_exp2f(FAST ? acc[j + 1] : acc[j + 1] - off);
-                        const uint32_t w2 = pack_bf16x2(pa, pb2);
-                        pk[ku][e2] = w2;
-                        // the row sum takes the bf16 weights that enter P V
-                        lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w2), kOnes, lsum, false);
-                    }
-#pragma unroll
-                for (int ku = 0; ku < 2; ++ku) {
-                    const int kb = kr0 + 16 * ku + 8 * h;
-#pragma unroll
-                    for (int dt = 0; dt < 2; ++dt) {
-                        const int d = 32 * dt + n;
-                        const u32x4 va = *reinterpret_cast<const u32x4*>(S.Vt + vt_offset(d, kb));
-                        oacc[dt] = mfma32x32x16(as_bf16x8(va), as_bf16x8(pk[ku]), oacc[dt]);
-                    }
+                for (int h2 = 0; h2 < 2; ++h2) {
+                    const float pa = __builtin_amdgcn_exp2f(FAST ? acc[2 * h2] : acc[2 * h2] - off);
+                    const float pb = __builtin_amdgcn_exp2f(FAST ? acc[2 * h2 + 1] : acc[2 * h2 + 1] - off);
+                    pw[h2] = pack_bf16x2(pa, pb);
+                    // the row sum takes the bf16 weights that enter P V
+                    lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw[h2]), kOnes, lsum, false);
                 }
+                const bf16x4 pk = __builtin_bit_cast(bf16x4, make_uint2(pw[0], pw[1]));
+#pragma unroll
+                for (int b = 0; b < 4; ++b) oacc[b] = mfma16x16x16(vt_operand(S.Vs, kr0, 16 * b, lane), pk, oacc[b]);
             }
+            lsum += __shfl_xor(lsum, 16);
             lsum += __shfl_xor(lsum, 32);
             const bool alone = !(lsum > 0.f);  // only itself left as a target
             if (__ballot(alone) != 0) {
                 // The output of a lone query is v_i: one more P V step on the
                 // diagonal tile with P = 1 at (i, i) for those queries and 0
                 // elsewhere adds exactly v_i to their (zero) accumulators.
-                // Query n's own key is key n of that tile, held by the lane
-                // half (n / 8) % 2 at element n % 8 of key group n / 16.
-                const bool mine = alone && h == ((n >> 3) & 1);
+                // Query n's own key is key n of that tile, held by lane group
+                // n / 4 as its element n % 4.
+                const bool mine = alone && g == (n >> 2);
                 const uint32_t one = (n & 1) ? 0x3F800000u : 0x3F80u;  // bf16 1.0 in its half
-                const int kr_diag = ring_row(cq, qh * 32);
+                const uint2 w2 = make_uint2(mine && (n & 2) == 0 ? one : 0u, mine && (n & 2) != 0 ? one : 0u);
+                const bf16x4 pk = __builtin_bit_cast(bf16x4, w2);
+                const int kr_diag = ring_row(c, 16 * wave);
 #pragma unroll
-                for (int ku = 0; ku < 2; ++ku) {
-                    u32x4 pk;
-#pragma unroll
-                    for (int w = 0; w < 4; ++w) pk[w] = (mine && (n >> 4) == ku && ((n & 7) >> 1) == w) ? one : 0u;
-                    const int kb = kr_diag + 16 * ku + 8 * h;
-#pragma unroll
-                    for (int dt = 0; dt < 2; ++dt) {
-                        const u32x4 va = *reinterpret_cast<const u32x4*>(S.Vt + vt_offset(32 * dt + n, kb));
-                        oacc[dt] = mfma32x32x16(as_bf16x8(va), as_bf16x8(pk), oacc[dt]);
-                    }
-                }
+                for (int b = 0; b < 4; ++b) oacc[b] = mfma16x16x16(vt_operand(S.Vs, kr_diag, 16 * b, lane), pk, oacc[b]);
             }
             const float mref = FAST ? 0.f : m;
-            uint16_t* orow = o_rounds + (seg * L + s_q) * kHeadDim;
             // 1/l to within 1 ulp; the result is rounded to bf16.  A lone
             // query divides its exact v_i by 1.
             const float inv = alone ? 1.f : __builtin_amdgcn_rcpf(lsum);
+            uint16_t* orow = o_rounds + (seg * L + s_q) * kHeadDim + 4 * g;
 #pragma unroll
-            for (int dt = 0; dt < 2; ++dt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int d0 = 32 * dt + 8 * i + 4 * h;
-                    uint2 o;
-                    o.x = pack_bf16x2(oacc[dt][4 * i] * inv, oacc[dt][4 * i + 1] * inv);
-                    o.y = pack_bf16x2(oacc[dt][4 * i + 2] * inv, oacc[dt][4 * i + 3] * inv);
-                    *reinterpret_cast<uint2*>(orow + d0) = o;
-                }
-            if (h == 0) {
+            for (int b = 0; b < 4; ++b) {
+                uint2 o;
+                o.x = pack_bf16x2(oacc[b][0] * inv, oacc[b][1] * inv);
+                o.y = pack_bf16x2(oacc[b][2] * inv, oacc[b][3] * inv);
+                *reinterpret_cast<uint2*>(orow + 16 * b) = o;
+            }
+            if (g == 0) {
                 // z = scale*|q_i| - self_mask when the token is its own only target
                 lse_rounds[seg * L + s_q] = alone ? bound * kLn2 - self_mask : (mref + __log2f(lsum)) * kLn2;
             }
-            };
-            if (fast)
-                attend(BoolTag<true>{});
-            else
-                attend(BoolTag<false>{});
-        }
+        };
+        if (fast)
+            attend(BoolTag<true>{});
+        else
+            attend(BoolTag<false>{});
 
-        __syncthreads();  // every wave is done with the slots of chunks 2p-1 and 2p
-        if (more) store_quad<NW>(S, pf, ring_row(2 * p + 2 + qrow / kChunk, qrow % kChunk), part);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) pf_pos[i] = pf_pos2[i];
-        __syncthreads();
+        pf_pos = pf_next;
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of chunk c+1 have landed
+        __syncthreads();                // ... and every wave is done with chunk c-1
     }
 }
 
@@ -552,21 +489,27 @@ __global__ __launch_bounds__(256) void attn_prep_kernel(const uint16_t* __restri
     }
 }
 
+
 template <int NW>
-hipError_t launch_bf16(dim3 grid, bool causal, const uint16_t* q, const uint16_t* v,
-                       const int32_t* buckets, const int32_t* perm, const int32_t* bs, uint16_t* o,
-                       float* lse, int64_t BH, int L, int n_r, int n_b, float scale, float self_mask,
-                       int pps, void* workspace, hipStream_t stream) {
+hipError_t launch_bf16(bool causal, const uint16_t* q, const uint16_t* v, const int32_t* buckets,
+                       const int32_t* perm, uint16_t* o, float* lse, int64_t BH, int L, int n_r,
+                       float scale, float self_mask, void* workspace, hipStream_t stream) {
     const int64_t rows = BH * L;
-    u32x4* rec = static_cast<u32x4*>(workspace);
+    uint32_t* rec = static_cast<uint32_t*>(workspace);
     attn_prep_kernel<NW><<<(unsigned)((rows * 8 + 255) / 256), 256, 0, stream>>>(
-        q, buckets, rows, n_r, scale * kLog2e, reinterpret_cast<uint32_t*>(rec));
+        q, buckets, rows, n_r, scale * kLog2e, rec);
+    // Strips of chunks: long enough that staging the strip's first window is
+    // a small overhead, short enough to give the chip several workgroups per
+    // CU (three fit at once).
+    const int64_t n_chunks = L / kChunk, segs = BH * n_r;
+    const int cps = (int)std::max<int64_t>(1, std::min<int64_t>(16, n_chunks * segs / 3072));
+    const dim3 grid((unsigned)((n_chunks + cps - 1) / cps), (unsigned)segs);
     if (causal)
-        attn_fwd_bf16_kernel<NW, true><<<grid, 256, 0, stream>>>(q, v, rec, perm, bs, o, lse, L, n_r,
-                                                                 n_b, scale, self_mask, pps);
+        attn_fwd_bf16_kernel<NW, true><<<grid, 256, 0, stream>>>(q, v, rec, perm, o, lse, L, n_r, scale,
+                                                                 self_mask, cps);
     else
-        attn_fwd_bf16_kernel<NW, false><<<grid, 256, 0, stream>>>(q, v, rec, perm, bs, o, lse, L, n_r,
-                                                                  n_b, scale, self_mask, pps);
+        attn_fwd_bf16_kernel<NW, false><<<grid, 256, 0, stream>>>(q, v, rec, perm, o, lse, L, n_r, scale,
+                                                                  self_mask, cps);
     return hipGetLastError();
 }
 
@@ -599,20 +542,14 @@ hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, bool 
             self_mask);
         return hipGetLastError();
     }
-    // Strips of chunk pairs: long enough to reuse the shared chunk between
-    // neighbouring pairs and to hide the next pair's loads, short enough to
-    // leave several workgroups per CU for the whole chip.
-    const int64_t n_pairs = (L / kChunk + 1) / 2;
-    const int pps = (int)std::max<int64_t>(1, std::min<int64_t>(16, n_pairs * segs / 3072));
-    const dim3 grid((unsigned)((n_pairs + pps - 1) / pps), segs);
     const uint16_t* qb = static_cast<const uint16_t*>(q);
     const uint16_t* vb = static_cast<const uint16_t*>(v);
     uint16_t* ob = static_cast<uint16_t*>(o_rounds);
     const int nw = n_rounds == 1 ? 0 : (n_rounds + 1) / 2;
-#define LSH_FWD_CASE(W)                                                                         \
-    case W:                                                                                     \
-        return launch_bf16<W>(grid, causal, qb, vb, buckets, perm, bucket_start, ob, lse_rounds, \
-                              BH, L, n_rounds, n_buckets, scale, self_mask, pps, workspace, stream);
+#define LSH_FWD_CASE(W)                                                                             \
+    case W:                                                                                         \
+        return launch_bf16<W>(causal, qb, vb, buckets, perm, ob, lse_rounds, BH, L, n_rounds, scale, \
+                              self_mask, workspace, stream);
     switch (nw) {
         LSH_FWD_CASE(0)
         LSH_FWD_CASE(1)
