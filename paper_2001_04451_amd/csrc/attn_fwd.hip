@@ -223,9 +223,25 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
+    // A chunk's output rows are stored at the start of the next step: the
+    // wait before each barrier (for the staging copies, counted together with
+    // stores) then finds them long completed.
+    uint2 out_pend[4] = {};
+    float lse_pend = 0.f;
+    int64_t row_pend = -1;
+    auto flush = [&]() {
+        if (row_pend >= 0) {
+            uint16_t* orow = o_rounds + row_pend * kHeadDim + 4 * g;
+#pragma unroll
+            for (int b = 0; b < 4; ++b) *reinterpret_cast<uint2*>(orow + 16 * b) = out_pend[b];
+            if (g == 0) lse_rounds[row_pend] = lse_pend;
+        }
+    };
+
     for (int c = c0; c < c1; ++c) {
         if (c + 1 < c1) stage(c + 1, pf_pos);
         const int pf_next = chunk_pos(c + 2);
+        flush();
 
         // ---- this wave's 16 queries of chunk c ----
         const int u = 16 * wave + n;  // query row inside the chunk
@@ -345,18 +361,14 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
             // 1/l to within 1 ulp; the result is rounded to bf16.  A lone
             // query divides its exact v_i by 1.
             const float inv = alone ? 1.f : __builtin_amdgcn_rcpf(lsum);
-            uint16_t* orow = o_rounds + (seg * L + s_q) * kHeadDim + 4 * g;
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
-                uint2 o;
-                o.x = pack_bf16x2(oacc[b][0] * inv, oacc[b][1] * inv);
-                o.y = pack_bf16x2(oacc[b][2] * inv, oacc[b][3] * inv);
-                *reinterpret_cast<uint2*>(orow + 16 * b) = o;
+                out_pend[b].x = pack_bf16x2(oacc[b][0] * inv, oacc[b][1] * inv);
+                out_pend[b].y = pack_bf16x2(oacc[b][2] * inv, oacc[b][3] * inv);
             }
-            if (g == 0) {
-                // z = scale*|q_i| - self_mask when the token is its own only target
-                lse_rounds[seg * L + s_q] = alone ? bound * kLn2 - self_mask : (mref + __log2f(lsum)) * kLn2;
-            }
+            // z = scale*|q_i| - self_mask when the token is its own only target
+            lse_pend = alone ? bound * kLn2 - self_mask : (mref + __log2f(lsum)) * kLn2;
+            row_pend = seg * L + s_q;
         };
         if (fast)
             attend(BoolTag<true>{});
@@ -367,6 +379,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
         __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of chunk c+1 have landed
         __syncthreads();                // ... and every wave is done with chunk c-1
     }
+    flush();
 }
 
 // fp32 path: one wave per chunk, one lane per query, exact fp32 arithmetic
