@@ -109,14 +109,21 @@ __device__ __forceinline__ f32x4 mfma16x16x16(bf16x4 a, bf16x4 b, f32x4 c) {
 }
 
 // Copy 16 (4) bytes per lane from global memory to LDS at lds_base + 16
-// (4) * lane; lds_base is uniform over the wave.
-__device__ __forceinline__ void copy16_to_lds(const void* src, void* lds_base) {
-    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                     (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+// (4) * lane; lds_base is uniform over the wave.  Written as inline assembly
+// so that the compiler does not order every later LDS read of the step
+// behind these copies (it cannot tell the slot being filled from the slots
+// being read); the kernel waits for them itself before each barrier.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    // the same address in every lane; readfirstlane puts it in a scalar register
+    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p);
 }
-__device__ __forceinline__ void copy4_to_lds(const void* src, void* lds_base) {
-    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                     (__attribute__((address_space(3))) void*)lds_base, 4, 0, 0);
+__device__ __forceinline__ void copy16_to_lds(const void* src, const void* lds_base) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_addr(lds_base))
+                 : "memory", "m0");
+}
+__device__ __forceinline__ void copy4_to_lds(const void* src, const void* lds_base) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(src), "s"(lds_addr(lds_base))
+                 : "memory", "m0");
 }
 
 // V^T operand of a 16x16x16 product for keys r0 .. r0+15 and dims d0 .. d0+15:
@@ -163,7 +170,8 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
     __shared__ __attribute__((aligned(16))) FwdShared<NW> S;
     constexpr int SW = FwdSig<NW>::stride, RW = FwdSig<NW>::rec_words;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int n = lane & 15, g = lane >> 4;  // query (and key row) of the lane, key group
     const int64_t seg = blockIdx.y;
     const int64_t bh = seg / n_r;
@@ -177,16 +185,17 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
     const int rw = r >> 1, rsh = (r >> 1) + 11 * (r & 1);  // field r of a signature
     if (tid <= kMaskedIndex) S.tab[tid] = tid < n_r ? -__log2f((float)(n_r - tid)) : -__builtin_inff();
 
-    // Position of row `lane` of chunk cc; outside the sequence any valid row
-    // (those slots are never a valid key, see lo below).
+    // Position of row `lane` of chunk cc, as stored (clamped where it is
+    // used); outside the sequence any valid row (those slots are never a
+    // valid key, see lo below).
     auto chunk_pos = [&](int cc) -> int {
-        if (cc < 0 || cc >= n_chunks) return 0;
-        return min(max(pseg[(int64_t)cc * kChunk + lane], 0), L - 1);
+        return cc >= 0 && cc < n_chunks ? pseg[(int64_t)cc * kChunk + lane] : 0;
     };
     // Gather chunk cc into its ring slot: wave w copies q and v rows
     // 16w .. 16w+15 (each lane the piece that belongs at its LDS slot), and
     // the signature words and key scales are split over the waves.
-    auto stage = [&](int cc, int pos_lane) {
+    auto stage = [&](int cc, int pos_raw) {
+        const int pos_lane = min(max(pos_raw, 0), L - 1);
         const int slot0 = ring_row(cc, 0);
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
