@@ -130,15 +130,17 @@ __device__ __forceinline__ void copy4_to_lds(const void* src, const void* lds_ba
 // lane l needs V[r0 + 4(l/16) + k][d0 + l%16] for k = 0..3.  The transposing
 // read gives lane i of each 16-lane group element i%4 of the 8-byte runs read
 // by lanes 4k + i/4, so lane i reads row r0 + 4(l/16) + i/4, dims
-// d0 + 4(i%4) .. +3.
-__device__ __forceinline__ bf16x4 vt_operand(const char* Vs, int r0, int d0, int lane) {
+// d0 + 4(i%4) .. +3: vt_offset is that byte offset (r0 a multiple of 16, so
+// the swizzle depends on the lane only).
+__device__ __forceinline__ uint32_t vt_offset(int r0, int d0, int lane) {
     const int i = lane & 15;
     const int row = r0 + 4 * (lane >> 4) + (i >> 2);
     const int d = d0 + 4 * (i & 3);
-    const uint32_t off = row_piece_offset(row, d >> 3) + (uint32_t)((d & 4) << 1);
+    return row_piece_offset(row, d >> 3) + (uint32_t)((d & 4) << 1);
+}
+__device__ __forceinline__ bf16x4 vt_read(const char* p) {
     typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-    const i16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_i16x4*)((__attribute__((address_space(3))) char*)Vs + off));
+    const i16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(__attribute__((address_space(3))) char*)p);
     return __builtin_bit_cast(bf16x4, x);
 }
 
@@ -284,11 +286,38 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
             const uint64_t after = u < 63 ? bB & (~0ull << (u + 1)) : 0ull;
             hi = (c - 1) * kChunk + (after ? 62 + __ffsll((long long)after) : 127);
         }
+        // valid keys of this lane's query as a 128-bit window mask (word k:
+        // window slots 32k .. 32k+31), then per lane group the complement
+        // shifted so that bit 16(kt%2) + j of nv[kt/2] is set when tile key
+        // 4g + j of tile kt is masked out
+        const int lo_w2 = lo - (c - 1) * kChunk, hi_w2 = hi - (c - 1) * kChunk;
+        uint32_t nv[4];
         bool act[8];
 #pragma unroll
-        for (int kt = 0; kt < 8; ++kt) {
-            const int tb = (c - 1) * kChunk + 16 * kt;
-            act[kt] = __ballot(lo <= hi && lo <= tb + 15 && hi >= tb) != 0;
+        for (int k = 0; k < 4; ++k) {
+            const int a = min(max(lo_w2 - 32 * k, 0), 32), b = min(max(hi_w2 + 1 - 32 * k, 0), 32);
+            uint32_t word = a < b ? (0xFFFFFFFFu >> (32 - (b - a))) << a : 0u;
+            if constexpr (!CAUSAL) {
+                if ((64 + u) / 32 == k) word &= ~(1u << ((64 + u) & 31));  // the query itself
+            }
+            act[2 * k] = __ballot((word & 0xFFFFu) != 0) != 0;
+            act[2 * k + 1] = __ballot((word >> 16) != 0) != 0;
+            nv[k] = ~word >> (4 * g);
+        }
+
+        // Per-lane LDS offsets of the two window chunks' first rows (tile kt
+        // adds 16 (kt % 4) rows, a constant): K operand pieces g and 4+g,
+        // the V^T operands of the four 16-dim blocks, the signature row.
+        uint32_t kofs[2][2], vofs[2][4];
+        int srow[2];
+#pragma unroll
+        for (int ch = 0; ch < 2; ++ch) {
+            const int base = ring_row(c - 1 + ch, 0);
+            kofs[ch][0] = row_piece_offset(base + n, g);
+            kofs[ch][1] = row_piece_offset(base + n, 4 + g);
+#pragma unroll
+            for (int b = 0; b < 4; ++b) vofs[ch][b] = vt_offset(base, 16 * b, lane);
+            srow[ch] = base + 4 * g;
         }
 
         auto attend = [&](auto fast_tag) {
@@ -298,23 +327,17 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
 #pragma unroll
             for (int kt = 0; kt < 8; ++kt) {
                 if (!act[kt]) continue;
-                const int kr0 = ring_row(c - 1 + (kt >> 2), 16 * (kt & 3));
-                f32x4 acc = mfma16x16x32(as_bf16x8(lds_piece(S.Qs, kr0 + n, g)), qb0, f32x4{});
-                acc = mfma16x16x32(as_bf16x8(lds_piece(S.Qs, kr0 + n, 4 + g)), qb1, acc);
-                // masked keys of this lane's query: bit k of minv <-> tile key 4g + k
-                const int tb = (c - 1) * kChunk + 16 * kt;
-                const int lo_t = max(lo - tb, 0), hi_t = min(hi - tb, 15);
-                uint32_t valid = lo_t <= hi_t ? (0xFFFFu >> (15 - hi_t)) & (0xFFFFu << lo_t) : 0u;
-                if constexpr (!CAUSAL) {
-                    const int self_t = s_q - tb;
-                    if (self_t >= 0 && self_t < 16) valid &= ~(1u << self_t);
-                }
-                const uint32_t minv = ~valid >> (4 * g);
-                const int kbase = kr0 + 4 * g;
+                const int ch = kt >> 2, roff = 16 * (kt & 3);  // chunk of the tile, its first row
+                f32x4 acc = mfma16x16x32(as_bf16x8(*reinterpret_cast<const u32x4*>(S.Qs + kofs[ch][0] + roff * 128)),
+                                         qb0, f32x4{});
+                acc = mfma16x16x32(as_bf16x8(*reinterpret_cast<const u32x4*>(S.Qs + kofs[ch][1] + roff * 128)), qb1,
+                                   acc);
+                const int kbase = srow[ch] + roff;
                 const f32x4 cfk = *reinterpret_cast<const f32x4*>(&S.cf[kbase]);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    uint32_t t = (uint32_t)((int32_t)(minv << (31 - j)) >> 31);
+                    const int bit = 16 * (kt & 1) + j;  // of nv[kt / 2]; -1 when masked
+                    uint32_t t = (uint32_t)((int32_t)(nv[kt >> 1] << (31 - bit)) >> 31);
                     if constexpr (NW > 0) {
                         uint32_t ksig[NW];
                         read_sig<NW>(S, kbase + j, ksig);
@@ -347,7 +370,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
                 }
                 const bf16x4 pk = __builtin_bit_cast(bf16x4, make_uint2(pw[0], pw[1]));
 #pragma unroll
-                for (int b = 0; b < 4; ++b) oacc[b] = mfma16x16x16(vt_operand(S.Vs, kr0, 16 * b, lane), pk, oacc[b]);
+                for (int b = 0; b < 4; ++b) oacc[b] = mfma16x16x16(vt_read(S.Vs + vofs[ch][b] + roff * 128), pk, oacc[b]);
             }
             lsum += __shfl_xor(lsum, 16);
             lsum += __shfl_xor(lsum, 32);
@@ -362,9 +385,8 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
                 const uint32_t one = (n & 1) ? 0x3F800000u : 0x3F80u;  // bf16 1.0 in its half
                 const uint2 w2 = make_uint2(mine && (n & 2) == 0 ? one : 0u, mine && (n & 2) != 0 ? one : 0u);
                 const bf16x4 pk = __builtin_bit_cast(bf16x4, w2);
-                const int kr_diag = ring_row(c, 16 * wave);
 #pragma unroll
-                for (int b = 0; b < 4; ++b) oacc[b] = mfma16x16x16(vt_operand(S.Vs, kr_diag, 16 * b, lane), pk, oacc[b]);
+                for (int b = 0; b < 4; ++b) oacc[b] = mfma16x16x16(vt_read(S.Vs + vofs[1][b] + 16 * wave * 128), pk, oacc[b]);
             }
             const float mref = FAST ? 0.f : m;
             // 1/l to within 1 ulp; the result is rounded to bf16.  A lone
