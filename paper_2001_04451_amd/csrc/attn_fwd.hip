@@ -263,7 +263,9 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
         const bf16x8 qb0 = as_bf16x8(lds_piece(S.Qs, rq, g));
         const bf16x8 qb1 = as_bf16x8(lds_piece(S.Qs, rq, 4 + g));
         const float cfq = S.cf[rq];
-        const float bound = cfq > 0.f ? scale_log2e * scale_log2e / cfq : 0.f;  // B_i
+        // B_i (to within an ulp: it picks the fast path, with a wide margin,
+        // and gives a lone query's log-partition)
+        const float bound = cfq > 0.f ? scale_log2e * scale_log2e * __builtin_amdgcn_rcpf(cfq) : 0.f;
         const bool fast = __ballot(!(bound <= kFastBound)) == 0;
 
         // bucket boundaries of the window (chunks c-1, c): bit k of bA (bB)
@@ -286,23 +288,24 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
             const uint64_t after = u < 63 ? bB & (~0ull << (u + 1)) : 0ull;
             hi = (c - 1) * kChunk + (after ? 62 + __ffsll((long long)after) : 127);
         }
-        // valid keys of this lane's query as a 128-bit window mask (word k:
-        // window slots 32k .. 32k+31), then per lane group the complement
-        // shifted so that bit 16(kt%2) + j of nv[kt/2] is set when tile key
-        // 4g + j of tile kt is masked out
+        // valid keys of this lane's query as a 128-bit window mask (vm[h]:
+        // window slots 64h .. 64h+63; lo_w2 <= 127 and hi_w2 >= 63 always),
+        // then per lane group the complement shifted so that bit 16(kt%2) + j
+        // of nv[kt/2] is set when tile key 4g + j of tile kt is masked out
         const int lo_w2 = lo - (c - 1) * kChunk, hi_w2 = hi - (c - 1) * kChunk;
+        uint64_t vm[2];
+        vm[0] = lo_w2 < 64 ? (~0ull << lo_w2) & (hi_w2 < 64 ? ~0ull >> (63 - hi_w2) : ~0ull) : 0ull;
+        vm[1] = hi_w2 >= 64 ? (~0ull >> (127 - hi_w2)) & (lo_w2 >= 64 ? ~0ull << (lo_w2 - 64) : ~0ull) : 0ull;
+        if constexpr (!CAUSAL) vm[1] &= ~(1ull << u);  // the query itself
         uint32_t nv[4];
         bool act[8];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int a = min(max(lo_w2 - 32 * k, 0), 32), b = min(max(hi_w2 + 1 - 32 * k, 0), 32);
-            uint32_t word = a < b ? (0xFFFFFFFFu >> (32 - (b - a))) << a : 0u;
-            if constexpr (!CAUSAL) {
-                if ((64 + u) / 32 == k) word &= ~(1u << ((64 + u) & 31));  // the query itself
-            }
-            act[2 * k] = __ballot((word & 0xFFFFu) != 0) != 0;
-            act[2 * k + 1] = __ballot((word >> 16) != 0) != 0;
-            nv[k] = ~word >> (4 * g);
+        for (int h2 = 0; h2 < 2; ++h2) {
+            const uint64_t sh = ~vm[h2] >> (4 * g);
+            nv[2 * h2] = (uint32_t)sh;
+            nv[2 * h2 + 1] = (uint32_t)(sh >> 32);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) act[4 * h2 + k] = __ballot(((vm[h2] >> (16 * k)) & 0xFFFFu) != 0) != 0;
         }
 
         // Per-lane LDS offsets of the two window chunks' first rows (tile kt
