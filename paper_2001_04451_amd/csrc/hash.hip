@@ -29,6 +29,8 @@
 namespace lsh {
 namespace {
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
 constexpr int kRB = 2;  // 32-row blocks per wave: each staged R tile feeds 2 * 8 MFMAs
 constexpr int kMaxColsPerLane = 8;                  // exact path: n_b/2 <= 512
 
@@ -258,21 +260,45 @@ struct Tile {
     f32x16 acc[kRB];
 };
 
-// Keys: the projection's bit pattern rotated left by one (sign in bit 0,
-// |projection| in bits 5..31: non-negative floats order like their bits),
-// with bits 1..4 replaced by the register index j inside the tile.  Unsigned
-// order of keys is the order of |projection| truncated to 19 mantissa bits.
-// Per projection: one rotate, one and-or, one unsigned median-of-three (the
-// running second best) and one unsigned max (the running best).
-__device__ __forceinline__ uint32_t proj_key(float x, int j, uint32_t live_mask) {
+// Keys order projections by |projection| truncated to 19 mantissa bits
+// (non-negative floats order like their bit patterns), with the register
+// index j inside the tile in bits the truncation frees.
+//  * fp32 input: the bit pattern rotated left by one (sign in bit 0,
+//    |projection| in bits 5..31, j in bits 1..4): one rotate and one and-or
+//    per projection, and the key also carries the winner's sign.
+//  * bf16 input: |projection| in bits 4..30 and j in bits 0..3, one and-or;
+//    the winner's sign is recomputed once per row and round (win_sign).
+// Keys of tiles past the round are masked to j, near zero.
+template <bool F32>
+__device__ __forceinline__ uint32_t proj_key(float x, int j, bool live) {
     const uint32_t u = __float_as_uint(x);
-    return (__builtin_amdgcn_alignbit(u, u, 31) & live_mask) | ((uint32_t)j << 1);
+    if constexpr (F32) {
+        return (__builtin_amdgcn_alignbit(u, u, 31) & (live ? 0xFFFFFFE1u : 0u)) | ((uint32_t)j << 1);
+    } else {
+        return (u & (live ? 0x7FFFFFF0u : 0u)) | (uint32_t)j;
+    }
 }
-constexpr uint32_t kKeyLive = 0xFFFFFFE1u;
+template <bool F32>
+__device__ __forceinline__ uint32_t key_index(uint32_t key) {
+    return F32 ? (key >> 1) & 15u : key & 15u;
+}
+template <bool F32>
+__device__ __forceinline__ float key_magnitude(uint32_t key) {
+    return __uint_as_float(F32 ? (key >> 1) & 0x7FFFFFF0u : key & 0x7FFFFFF0u);
+}
 
-__device__ __forceinline__ void key_update(uint32_t key, uint32_t& b, uint32_t& sc) {
-    sc = max(min(key, b), min(max(key, b), sc));  // median of three
-    b = max(key, b);
+// Running best b and second best sc (b >= sc) after two more keys: the
+// largest of {b, k1, k2} is the new best, the middle one is the largest of
+// the rest of those three, and sc joins the rest.  One max3, one med3 and
+// one max per two projections.
+// (max3 as inline assembly: left to itself the compiler shares max(b, k1)
+// with the median and spends a fourth instruction.)
+__device__ __forceinline__ void key_update2(uint32_t k1, uint32_t k2, uint32_t& b, uint32_t& sc) {
+    const uint32_t mid = max(min(b, k1), min(max(b, k1), k2));  // median of three
+    uint32_t top;
+    asm("v_max3_u32 %0, %1, %2, %3" : "=v"(top) : "v"(b), "v"(k1), "v"(k2));
+    b = top;
+    sc = max(sc, mid);
 }
 
 __device__ __forceinline__ void load_ops(u32x4 (&op)[8], const char* __restrict__ hi_base,
@@ -303,7 +329,6 @@ __device__ __forceinline__ void tile_step(Tile& nxt, u32x4 (&op)[8], const char*
     static_assert(kRB == 2, "slices written for two row blocks");
     const int sw = stage_swz(col_pref);
     uint32_t b[kRB] = {best[0], best[1]}, sc[kRB] = {second[0], second[1]};
-    const uint32_t mask = live ? kKeyLive : 0u;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         __builtin_amdgcn_sched_barrier(0);
@@ -326,11 +351,8 @@ __device__ __forceinline__ void tile_step(Tile& nxt, u32x4 (&op)[8], const char*
         if constexpr (EPI) {
 #pragma unroll
             for (int rb = 0; rb < kRB; ++rb)
-#pragma unroll
-                for (int jj = 0; jj < 2; ++jj) {
-                    const int j = 2 * i + jj;
-                    key_update(proj_key(cur.acc[rb][j], j, mask), b[rb], sc[rb]);
-                }
+                key_update2(proj_key<F32>(cur.acc[rb][2 * i], 2 * i, live),
+                            proj_key<F32>(cur.acc[rb][2 * i + 1], 2 * i + 1, live), b[rb], sc[rb]);
         }
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -344,14 +366,15 @@ __device__ __forceinline__ void tile_step(Tile& nxt, u32x4 (&op)[8], const char*
     }
 }
 
+template <bool F32>
 __device__ __forceinline__ void tile_epilogue(const Tile& T, int tile, bool live, uint32_t (&best)[kRB],
                                               uint32_t (&second)[kRB], int (&best_tile)[kRB]) {
-    const uint32_t mask = live ? kKeyLive : 0u;
 #pragma unroll
     for (int rb = 0; rb < kRB; ++rb) {
         uint32_t b = best[rb], sc = second[rb];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) key_update(proj_key(T.acc[rb][j], j, mask), b, sc);
+        for (int j = 0; j < 16; j += 2)
+            key_update2(proj_key<F32>(T.acc[rb][j], j, live), proj_key<F32>(T.acc[rb][j + 1], j + 1, live), b, sc);
         best_tile[rb] = b != best[rb] ? tile : best_tile[rb];
         best[rb] = b;
         second[rb] = sc;
@@ -532,7 +555,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
             }
             tile_step<F32, false, true>(tb, op, hi_base, mid_base, 0, h, qc, qmc, ta, t0 + 6, 6 < nt,
                                         bc, sc, tc);
-            tile_epilogue(tb, t0 + 7, 7 < nt, bc, sc, tc);
+            tile_epilogue<F32>(tb, t0 + 7, 7 < nt, bc, sc, tc);
 #pragma unroll
             for (int o = 0; o < PAIRS; ++o)
                 if (pr == o) {
@@ -559,19 +582,47 @@ __global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
                     const bool mine = bb > bp || (bb == bp && h == 0);
                     const uint32_t bk = mine ? bb : bp;
                     const uint32_t sk = max(min(bb, bp), max(ss2, sp));
-                    const float b1 = __uint_as_float((bk >> 1) & 0x7FFFFFF0u);
-                    const float s1 = __uint_as_float((sk >> 1) & 0x7FFFFFF0u);
+                    const float b1 = key_magnitude<F32>(bk);
+                    const float s1 = key_magnitude<F32>(sk);
                     const int hw = mine ? h : (h ^ 1);
                     const int tw = mine ? best_tile[pr][rb] : tp;
-                    const uint32_t j = (bk >> 1) & 15u;
+                    const uint32_t j = key_index<F32>(bk);
                     const int col = tw * 32 + 8 * (int)(j >> 2) + 4 * hw + (int)(j & 3u);
                     // Every screened key is within eps = err_sum*|q|*max|R_c| + err_pack*key
                     // of its exact |projection|; an exchange of winners needs a gap <= 2 eps.
                     // When the gap is larger the winner's magnitude exceeds eps, so the
-                    // screened sign (bit 0 of the key) is the exact one.
+                    // sign of any value within eps of its projection is the exact one.
                     const float thr = 2.04f * (err_sum * qn[pr][rb] * cn + err_pack * b1);
                     const bool flag = !(b1 - s1 > thr) || col >= half;
-                    const int id = (bk & 1u) ? half + col : col;
+                    bool negative;
+                    if constexpr (F32) {
+                        negative = (bk & 1u) != 0;
+                    } else {
+                        // q_row . R_col over both planes (the same products as the
+                        // screen, fp32 sums): each lane half adds its 32 k-values.
+                        // A flagged winner may sit past the round; any valid
+                        // column stands in, its sign unused.
+                        const int colc = min(col, half_pad - 1);
+                        const size_t o = ((size_t)r * half_pad + colc) * kHeadDim + 32 * h;
+                        const u32x4* ph = reinterpret_cast<const u32x4*>(r_hi + o);
+                        const u32x4* pm = reinterpret_cast<const u32x4*>(r_mid + o);
+                        float part = 0.f;
+#pragma unroll
+                        for (int s4 = 0; s4 < 4; ++s4) {
+                            const u32x4 qv = __builtin_bit_cast(u32x4, qa[pr][rb][s4]);
+                            const u32x4 hv = ph[s4], mv = pm[s4];
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                const uint32_t qw = qv[e], hw2 = hv[e], mw = mv[e];
+                                part = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, qw),
+                                                                       __builtin_bit_cast(bf16x2, hw2), part, false);
+                                part = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, qw),
+                                                                       __builtin_bit_cast(bf16x2, mw), part, false);
+                            }
+                        }
+                        negative = part + __shfl_xor(part, 32) < 0.f;
+                    }
+                    const int id = negative ? half + col : col;
                     if (rb == h) win[(pr * 64 + rb * 32 + n) * n_r + r] = flag ? kUnsettled : (uint16_t)id;
                 }
         }
