@@ -14,7 +14,9 @@ constexpr int kMaxRounds = 16;
 // float4 of fp32).  All loads of a row are issued before they are used
 // (slots, then the log-partitions, then the rows), so each lane keeps up to
 // 16 independent requests in flight instead of walking a dependent chain per
-// round.  The weighted sum is formed in fp32.
+// round.  The weighted sum is formed in fp32.  The per-round rows are read
+// once each and marked non-temporal, so they stream past the L2 instead of
+// evicting the log-partition lines, which serve 32 gathers each.
 template <bool F32>
 __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o_rounds,
                                                       const float* __restrict__ lse_rounds,
@@ -53,8 +55,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o
 #pragma unroll
         for (int r = 0; r < kMaxRounds; ++r)
             if (r < n_r) {
-                o[r][0] = *reinterpret_cast<const f32x4*>(src + base[r] * kHeadDim + part * 8);
-                o[r][1] = *reinterpret_cast<const f32x4*>(src + base[r] * kHeadDim + part * 8 + 4);
+                o[r][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src + base[r] * kHeadDim + part * 8));
+                o[r][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src + base[r] * kHeadDim + part * 8 + 4));
             }
 #pragma unroll
         for (int r = 0; r < kMaxRounds; ++r)
@@ -71,7 +73,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o
         u32x4 o[kMaxRounds];
 #pragma unroll
         for (int r = 0; r < kMaxRounds; ++r)
-            if (r < n_r) o[r] = *reinterpret_cast<const u32x4*>(src + base[r] * kHeadDim + part * 8);
+            if (r < n_r) o[r] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + base[r] * kHeadDim + part * 8));
 #pragma unroll
         for (int r = 0; r < kMaxRounds; ++r)
             if (r < n_r) {

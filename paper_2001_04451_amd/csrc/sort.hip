@@ -130,8 +130,16 @@ __global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __rest
                                                            int n_tiles, int32_t* __restrict__ perm,
                                                            int32_t* __restrict__ undo) {
     extern __shared__ int base[];  // [kSortWaves][n_b]
-    const int tile = blockIdx.x;
-    const int64_t seg = blockIdx.y;
+    // Workgroup b of the launch runs on XCD b % 8 (round-robin dispatch).
+    // Each XCD is given a contiguous run of (segment, tile) items, so the
+    // tiles of a segment write their scattered 4-byte slots into the same
+    // XCD's L2, which merges them into whole lines before they reach HBM,
+    // and the rounds of one (batch, head) read its bucket ids through one L2.
+    const int64_t nblk = (int64_t)gridDim.x * gridDim.y;
+    const int64_t bid = blockIdx.x + (int64_t)blockIdx.y * gridDim.x;
+    const int64_t item = nblk % 8 == 0 ? (bid % 8) * (nblk / 8) + bid / 8 : bid;
+    const int tile = (int)(item % gridDim.x);
+    const int64_t seg = item / gridDim.x;
     const int64_t bh = seg / n_r;
     const int r = (int)(seg % n_r);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
