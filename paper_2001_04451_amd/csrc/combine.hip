@@ -5,19 +5,25 @@
 #include "common.h"
 #include "launch.h"
 
+#include <type_traits>
+
 namespace lsh {
 namespace {
 
 constexpr int kMaxRounds = 16;
 
-// Eight lanes share a row (8 of its 64 values each, 16 bytes of bf16 or two
-// float4 of fp32).  All loads of a row are issued before they are used
-// (slots, then the log-partitions, then the rows), so each lane keeps up to
-// 16 independent requests in flight instead of walking a dependent chain per
-// round.  The weighted sum is formed in fp32.  The per-round rows are read
-// once each and marked non-temporal, so they stream past the L2 instead of
-// evicting the log-partition lines, which serve 32 gathers each.
-template <bool F32>
+// Eight lanes share a row.  Lane p of the group first handles round p (and
+// p + 8 when n_r > 8): its slot from undo, its log-partition z_r, and after
+// a max / sum across the group (shuffles) its weight exp(z_r - z).  Then
+// every lane takes 8 of the row's 64 values (16 bytes of bf16, two float4
+// of fp32) from all rounds, with the slots and weights of the other rounds
+// read from their lanes.  The code is straight-line for every n_r: rounds
+// past n_r read a valid slot and get weight 0, so each lane's loads are all
+// in flight together.  The per-round rows are read once each and marked
+// non-temporal, so they stream past the L2 instead of evicting the
+// log-partition lines, which serve 32 gathers each.  The weighted sum is
+// formed in fp32.  NRL is n_r rounded up to a power of two.
+template <bool F32, int NRL>
 __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o_rounds,
                                                       const float* __restrict__ lse_rounds,
                                                       const int32_t* __restrict__ undo,
@@ -26,63 +32,84 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o
                                                       int L, int n_r) {
     const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 3;
     const int part = threadIdx.x & 7;
+    // The row count is a multiple of the 32 rows of a block for every L the
+    // library accepts (L is a multiple of the chunk, 64); whole groups leave.
     if (row >= rows) return;
     const int64_t bh = row / L;
     const int64_t i = row % L;
     const int64_t seg0 = bh * n_r;
+    const int lane = threadIdx.x & 63, group0 = lane & ~7;
+    constexpr int RPL = NRL > 8 ? 2 : 1;  // rounds per lane
 
-    int64_t base[kMaxRounds];
-    float z_r[kMaxRounds];
+    // this lane's rounds: part and part + 8
+    int u[RPL];
+    float zr[RPL];
+    bool live[RPL];
 #pragma unroll
-    for (int r = 0; r < kMaxRounds; ++r)
-        if (r < n_r) base[r] = (seg0 + r) * L + min(max(undo[(seg0 + r) * L + i], 0), L - 1);
+    for (int k = 0; k < RPL; ++k) {
+        const int r = part + 8 * k;
+        live[k] = r < n_r;
+        const int rc = min(r, n_r - 1);
+        u[k] = min(max(undo[(seg0 + rc) * L + i], 0), L - 1);
+        zr[k] = lse_rounds[(seg0 + rc) * L + u[k]];
+    }
     float zmax = -__builtin_inff();
 #pragma unroll
-    for (int r = 0; r < kMaxRounds; ++r)
-        if (r < n_r) {
-            z_r[r] = lse_rounds[base[r]];
-            zmax = fmaxf(zmax, z_r[r]);
-        }
+    for (int k = 0; k < RPL; ++k)
+        if (live[k]) zmax = fmaxf(zmax, zr[k]);
+#pragma unroll
+    for (int o = 1; o < 8; o <<= 1) zmax = fmaxf(zmax, __shfl_xor(zmax, o));
     float sum = 0.f;
 #pragma unroll
-    for (int r = 0; r < kMaxRounds; ++r)
-        if (r < n_r) sum += expf(z_r[r] - zmax);
+    for (int k = 0; k < RPL; ++k) sum += live[k] ? expf(zr[k] - zmax) : 0.f;
+#pragma unroll
+    for (int o = 1; o < 8; o <<= 1) sum += __shfl_xor(sum, o);
     const float z = zmax + logf(sum);
+    float wk[RPL];
+#pragma unroll
+    for (int k = 0; k < RPL; ++k) wk[k] = live[k] ? expf(zr[k] - z) : 0.f;
+
+    // every round's slot and weight in every lane of the group (rounds
+    // n_r .. NRL-1 read round n_r - 1's row with weight 0)
+    constexpr int NR = NRL;
+    int64_t sl[NR];
+    float w[NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        const int src_lane = group0 + (r & 7);
+        const int k = r >> 3;
+        sl[r] = (seg0 + min(r, n_r - 1)) * L + __shfl(u[k], src_lane);
+        w[r] = __shfl(wk[k], src_lane);
+    }
+
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if constexpr (F32) {
         const float* src = static_cast<const float*>(o_rounds);
-        f32x4 o[kMaxRounds][2];
+        f32x4 o[NR][2];
 #pragma unroll
-        for (int r = 0; r < kMaxRounds; ++r)
-            if (r < n_r) {
-                o[r][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src + base[r] * kHeadDim + part * 8));
-                o[r][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src + base[r] * kHeadDim + part * 8 + 4));
-            }
+        for (int r = 0; r < NR; ++r) {
+            o[r][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src + sl[r] * kHeadDim + part * 8));
+            o[r][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src + sl[r] * kHeadDim + part * 8 + 4));
+        }
 #pragma unroll
-        for (int r = 0; r < kMaxRounds; ++r)
-            if (r < n_r) {
-                const float w = expf(z_r[r] - z);
+        for (int r = 0; r < NR; ++r)
 #pragma unroll
-                for (int e = 0; e < 8; ++e) acc[e] = fmaf(w, o[r][e >> 2][e & 3], acc[e]);
-            }
+            for (int e = 0; e < 8; ++e) acc[e] = fmaf(w[r], o[r][e >> 2][e & 3], acc[e]);
         float* dst = static_cast<float*>(out) + row * kHeadDim + part * 8;
         *reinterpret_cast<f32x4*>(dst) = f32x4{acc[0], acc[1], acc[2], acc[3]};
         *reinterpret_cast<f32x4*>(dst + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
     } else {
         const uint16_t* src = static_cast<const uint16_t*>(o_rounds);
-        u32x4 o[kMaxRounds];
+        u32x4 o[NR];
 #pragma unroll
-        for (int r = 0; r < kMaxRounds; ++r)
-            if (r < n_r) o[r] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + base[r] * kHeadDim + part * 8));
+        for (int r = 0; r < NR; ++r)
+            o[r] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + sl[r] * kHeadDim + part * 8));
 #pragma unroll
-        for (int r = 0; r < kMaxRounds; ++r)
-            if (r < n_r) {
-                const float w = expf(z_r[r] - z);
+        for (int r = 0; r < NR; ++r)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    acc[2 * e] = fmaf(w, bf16_bits_to_f32(o[r][e] & 0xFFFFu), acc[2 * e]);
-                    acc[2 * e + 1] = fmaf(w, __uint_as_float(o[r][e] & 0xFFFF0000u), acc[2 * e + 1]);
-                }
+            for (int e = 0; e < 4; ++e) {
+                acc[2 * e] = fmaf(w[r], bf16_bits_to_f32(o[r][e] & 0xFFFFu), acc[2 * e]);
+                acc[2 * e + 1] = fmaf(w[r], __uint_as_float(o[r][e] & 0xFFFF0000u), acc[2 * e + 1]);
             }
         u32x4 packed;
 #pragma unroll
@@ -100,12 +127,22 @@ hipError_t launch_combine(int64_t BH, int L, int n_rounds, bool f32, const void*
     const int64_t rows = BH * L;
     if (rows == 0) return hipSuccess;
     const unsigned grid = (unsigned)((rows * 8 + 255) / 256);
+    if (n_rounds > kMaxRounds) return hipErrorInvalidValue;
+    auto go = [&](auto f32_tag, auto nrl_tag) {
+        combine_kernel<decltype(f32_tag)::value, decltype(nrl_tag)::value><<<grid, 256, 0, stream>>>(
+            o_rounds, lse_rounds, undo, out, lse_total, rows, L, n_rounds);
+    };
+    auto by_rounds = [&](auto f32_tag) {
+        if (n_rounds <= 1) go(f32_tag, std::integral_constant<int, 1>{});
+        else if (n_rounds <= 2) go(f32_tag, std::integral_constant<int, 2>{});
+        else if (n_rounds <= 4) go(f32_tag, std::integral_constant<int, 4>{});
+        else if (n_rounds <= 8) go(f32_tag, std::integral_constant<int, 8>{});
+        else go(f32_tag, std::integral_constant<int, 16>{});
+    };
     if (f32)
-        combine_kernel<true><<<grid, 256, 0, stream>>>(o_rounds, lse_rounds, undo, out, lse_total,
-                                                       rows, L, n_rounds);
+        by_rounds(std::true_type{});
     else
-        combine_kernel<false><<<grid, 256, 0, stream>>>(o_rounds, lse_rounds, undo, out, lse_total,
-                                                        rows, L, n_rounds);
+        by_rounds(std::false_type{});
     return hipGetLastError();
 }
 

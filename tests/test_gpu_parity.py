@@ -228,3 +228,32 @@ def test_hash_exact_ties(gpu, dtype):
     assert (want[:, :, ::37] == 0).all()
     assert not (want == 9).any() and not (want == half + 3).any()
     assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("n_rounds", [3, 6, 9, 16])
+def test_combine_round_counts(gpu, dtype, n_rounds):
+    """The combine for round counts the five workloads do not use: counts that
+    are not a power of two (rounds past n_r padded inside the kernel) and
+    counts above 8 (two rounds per lane).  Per-round rows, log-partitions and
+    the inverse permutations are drawn here."""
+    B, H, L, d = 1, 2, 1024, 64
+    rng = np.random.default_rng(1000 + n_rounds)
+    o = rng.standard_normal((B, H, n_rounds, L, d)).astype(np.float32)
+    if dtype == "bf16":  # round to bf16 first so both sides see the same values
+        o = (torch.from_numpy(o).to(torch.bfloat16).float()).numpy()
+    lse_r = (5.0 * rng.standard_normal((B, H, n_rounds, L))).astype(np.float32)
+    undo = np.stack([np.stack([np.argsort(rng.permutation(L)) for _ in range(n_rounds)])
+                     for _ in range(B * H)]).reshape(B, H, n_rounds, L).astype(np.int32)
+    ref_out, ref_lse = oracle.lsh_combine_rounds(o.astype(np.float64), lse_r.astype(np.float64),
+                                                 undo)
+    cfg = lsh.Config(B=B, H=H, L=L, n_buckets=64, n_rounds=n_rounds)
+    tdt = torch_dtype(dtype)
+    log("combine", dtype, n_rounds)
+    out, lse = lsh.lsh_combine_rounds(cfg, torch.from_numpy(o).to(tdt).cuda(),
+                                      torch.from_numpy(lse_r).cuda(),
+                                      torch.from_numpy(undo).cuda(), tdt)
+    torch.cuda.synchronize()
+    err = np.abs(out.float().cpu().numpy() - ref_out).max()
+    assert err <= out_tolerance(dtype), f"combine max-abs error {err}"
+    assert lse_close(lse.cpu().numpy(), ref_lse, dtype).all()
