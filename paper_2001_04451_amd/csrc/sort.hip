@@ -25,7 +25,11 @@ constexpr int kHistLdsInts = 8192;
 
 __device__ __forceinline__ int clamp_bucket(int b, int n_b) { return min(max(b, 0), n_b - 1); }
 
-__global__ __launch_bounds__(256) void sort_hist_kernel(const int32_t* __restrict__ buckets, int L,
+// A tile is one workgroup (one per CU at the usual sizes), so it runs 16
+// waves to keep enough loads in flight.
+constexpr int kHistThreads = 1024;
+
+__global__ __launch_bounds__(kHistThreads) void sort_hist_kernel(const int32_t* __restrict__ buckets, int L,
                                                         int n_r, int n_b, int rounds_per_group,
                                                         int n_tiles, int32_t* __restrict__ counts) {
     extern __shared__ int hist[];
@@ -86,6 +90,9 @@ __global__ __launch_bounds__(256) void sort_scan_kernel(int32_t* __restrict__ co
             __syncthreads();
         }
         int run = part[threadIdx.x] - s;
+        // (bucket, tile) of element lo, stepped along the run: a bucket's
+        // start is the exclusive prefix at its tile 0
+        int bucket = (int)(lo / n_tiles), t = (int)(lo % n_tiles);
 #pragma unroll
         for (int k = 0; k < kScanPerThread; k += 4) {
             const int64_t e = lo + k;
@@ -97,8 +104,13 @@ __global__ __launch_bounds__(256) void sort_scan_kernel(int32_t* __restrict__ co
                 x.w = x.z + v[k + 2];
                 *reinterpret_cast<int4*>(c + e) = x;
 #pragma unroll
-                for (int u = 0; u < 4; ++u)
-                    if ((e + u) % n_tiles == 0) bs[(e + u) / n_tiles] = u == 0 ? x.x : (u == 1 ? x.y : (u == 2 ? x.z : x.w));
+                for (int u = 0; u < 4; ++u) {
+                    if (t == 0) bs[bucket] = u == 0 ? x.x : (u == 1 ? x.y : (u == 2 ? x.z : x.w));
+                    if (++t == n_tiles) {
+                        t = 0;
+                        ++bucket;
+                    }
+                }
                 run = x.w + v[k + 3];
             }
         }
@@ -114,10 +126,15 @@ __global__ __launch_bounds__(256) void sort_scan_kernel(int32_t* __restrict__ co
             __syncthreads();
         }
         int run = part[threadIdx.x] - s;
+        int bucket = (int)(lo / n_tiles), t = (int)(lo % n_tiles);
         for (int64_t e = lo; e < hi; ++e) {
             const int v = c[e];
             c[e] = run;
-            if (e % n_tiles == 0) bs[e / n_tiles] = run;
+            if (t == 0) bs[bucket] = run;
+            if (++t == n_tiles) {
+                t = 0;
+                ++bucket;
+            }
             run += v;
         }
     }
@@ -148,14 +165,18 @@ __global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __rest
     for (int i = threadIdx.x; i < kSortWaves * n_b; i += blockDim.x) base[i] = 0;
     const int p0 = tile * kTile + wave * kPerWave;
     const int p1 = min(L, p0 + kPerWave);
-    // this lane's ids, all loads in flight at once (kPerWave / 64 per lane)
+    // this lane's ids, all loads in flight at once (kPerWave / 64 per lane);
+    // positions past the segment load a valid id that is never used, so the
+    // loads are unconditional and not each followed by its own wait
     constexpr int kIter = kPerWave / 64;
     int ids[kIter];
 #pragma unroll
     for (int it = 0; it < kIter; ++it) {
-        const int pos = p0 + 64 * it + lane;
-        ids[it] = pos < p1 ? clamp_bucket(buckets[(bh * L + pos) * n_r + r], n_b) : 0;
+        const int pos = min(max(p0 + 64 * it + lane, 0), max(p1 - 1, 0));
+        ids[it] = buckets[(bh * L + pos) * n_r + r];
     }
+#pragma unroll
+    for (int it = 0; it < kIter; ++it) ids[it] = clamp_bucket(ids[it], n_b);
     __syncthreads();
 #pragma unroll
     for (int it = 0; it < kIter; ++it)
@@ -235,7 +256,7 @@ hipError_t launch_sort(int64_t BH, int L, int n_rounds, int n_buckets, const int
     int n_bits = 0;
     while ((1 << n_bits) < n_buckets) ++n_bits;
 
-    sort_hist_kernel<<<dim3(n_tiles, (unsigned)BH, groups), 256, rpg * n_buckets * sizeof(int), stream>>>(
+    sort_hist_kernel<<<dim3(n_tiles, (unsigned)BH, groups), kHistThreads, rpg * n_buckets * sizeof(int), stream>>>(
         buckets, L, n_rounds, n_buckets, rpg, n_tiles, counts);
     sort_scan_kernel<<<(unsigned)(BH * n_rounds), 256, 0, stream>>>(counts, L, n_buckets, n_tiles,
                                                                     bucket_start);
