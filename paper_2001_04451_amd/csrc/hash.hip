@@ -26,13 +26,14 @@
 #include "common.h"
 #include "launch.h"
 
+#include <type_traits>
+
 namespace lsh {
 namespace {
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kRB = 2;  // 32-row blocks per wave: each staged R tile feeds 2 * 8 MFMAs
-constexpr int kMaxColsPerLane = 8;                  // exact path: n_b/2 <= 512
 
 // One R column per block of 64 lanes (lane = t): bf16 planes hi/mid,
 // [n_r][half_pad][64] (column contiguous, zero padded), and the column's
@@ -85,22 +86,30 @@ __device__ __forceinline__ float q_value(const void* q, int64_t row, int k) {
     }
 }
 
-// Exact argmax of [xR; -xR] for the listed row-rounds of one round.  The
-// round's R (fp32, at most 130 KB) is staged in LDS once per block, column
-// by column; each wave settles one row-round at a time, in two passes:
-//  1. every column's projection in fp32 (a fused multiply-add chain over t),
-//     whose distance to the fp64 value of step 2 is at most
-//     eps = (64 * 2^-24 * 1.01 + 2^-46) * |q| * max_c |R_c|; a column can
-//     hold the fp64 argmax only if its fp32 magnitude is within 2 eps of the
-//     largest one;
-//  2. for those candidates (one lane each), the projection as the oracle
-//     forms it: the left-to-right sum over t of the exact products q_t * R_tc
-//     in fp64.  Ties go to the first index of [xR; -xR].
-// A row with more than 64 candidates (for instance q = 0) takes the plain
-// fp64 pass over every column instead.
-constexpr int kRefineThreads = 512;
+// Exact argmax of [xR; -xR] for the listed row-rounds of one round.  A
+// block takes the list in groups of 64 entries, one per lane of every wave,
+// in two passes:
+//  1. each wave forms the fp32 projections of its 32 columns for all 64
+//     entries (lane = entry): R's values are the same for every lane, so they
+//     are scalar loads (R[t][c0 .. c0+31] is contiguous), fetched one t ahead,
+//     and nothing is staged.  The fp32
+//     value is within eps = (64 * 2^-24 * 1.01 + 2^-46) * |q| * max_c |R_c|
+//     of the fp64 one, so only a column whose fp32 magnitude is within 2 eps
+//     of the entry's largest can hold the fp64 argmax;
+//  2. for those candidates, the projection as the oracle forms it: the
+//     left-to-right sum over t of the exact products q_t * R_tc in fp64, one
+//     lane per (entry, candidate), sixteen candidate lanes per entry.  Ties go
+//     to the first index of [xR; -xR].
+// An entry with more than sixteen candidates (q = 0 makes every column one),
+// or none (a non-finite q), takes the plain fp64 pass over every column,
+// one wave per entry.
+constexpr int kRefineThreads = 1024;
 constexpr int kRefineWaves = kRefineThreads / 64;
-constexpr int kRsStride = kHeadDim + 1;  // floats per staged R column
+constexpr int kRefineGroup = 64;     // entries per pass
+constexpr int kRefineCand = 16;      // candidate lanes per entry
+constexpr int kRefineCols = 32;      // columns per wave in pass 1
+static_assert(kRefineWaves * kRefineCols >= 512, "pass 1 covers n_b / 2 <= 512 columns");
+static_assert(kRefineWaves * 64 == kRefineGroup * kRefineCand, "pass 2 lanes");
 
 __device__ __forceinline__ void better(double v, int i, double& bv, int& bi) {
     if (v > bv || (v == bv && i < bi)) {
@@ -108,6 +117,14 @@ __device__ __forceinline__ void better(double v, int i, double& bv, int& bi) {
         bi = i;
     }
 }
+
+struct RefineShared {
+    float qs[kRefineGroup][kHeadDim + 1];  // the group's q rows
+    float qn[kRefineGroup];                // and their norms
+    float mx[kRefineWaves][kRefineGroup];  // per wave: largest |fp32 projection| of each entry
+    int cnt[kRefineGroup];                 // candidates found per entry
+    int cand[kRefineGroup][kRefineCand];   // their columns
+};
 
 template <bool F32>
 __global__ __launch_bounds__(kRefineThreads, 1) void hash_refine_kernel(const void* __restrict__ q,
@@ -117,125 +134,162 @@ __global__ __launch_bounds__(kRefineThreads, 1) void hash_refine_kernel(const vo
                                                           const int* __restrict__ counts,
                                                           const float* __restrict__ col_norm_max,
                                                           int32_t* __restrict__ buckets) {
-    extern __shared__ float Rs[];  // [half][kRsStride] (column-major), then [waves][64] columns
+    __shared__ RefineShared S;
     const int r = blockIdx.y;
     const int n = counts[r];
-    if (n == 0 || (int)blockIdx.x * kRefineWaves >= n) return;  // uniform per block
-    // stage the round's R transposed (column c's 64 values contiguous, padded
-    // rows so that 64 lanes reading 64 columns hit distinct banks)
-    const f32x4* Rr = reinterpret_cast<const f32x4*>(R + (size_t)r * kHeadDim * half);
-    const int n4 = kHeadDim * half / 4;
-    for (int i0 = threadIdx.x; i0 < n4; i0 += 8 * blockDim.x) {
-        f32x4 tmp[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int i = i0 + u * blockDim.x;
-            if (i < n4) tmp[u] = Rr[i];
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int i = i0 + u * blockDim.x;
-            if (i < n4) {
-                const int t = (4 * i) / half, c0 = (4 * i) % half;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) Rs[(c0 + e) * kRsStride + t] = tmp[u][e];
-            }
-        }
-    }
-    __syncthreads();
+    const int groups = (n + kRefineGroup - 1) / kRefineGroup;
+    if ((int)blockIdx.x >= groups) return;  // uniform per block
     const int* list = lists + list_stride * r;
+    const float* Rr = R + (size_t)r * kHeadDim * half;  // [t][half]
     const int lane = lane_id();
-    int* cand = reinterpret_cast<int*>(Rs + half * kRsStride) + (threadIdx.x >> 6) * 64;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const float cn = col_norm_max[r];
-    const int waves = gridDim.x * kRefineWaves;
-    for (int e = blockIdx.x * kRefineWaves + (threadIdx.x >> 6); e < n; e += waves) {
-        const int64_t row = list[e];
-        const float qv = q_value<F32>(q, row, lane);
-        // pass 1: fp32 projections of this lane's columns lane + 64k
-        float p32[kMaxColsPerLane];
+    const int c0 = wave * kRefineCols;  // this wave's columns in pass 1
+    const int ncols = max(0, min(kRefineCols, half - c0));
+
+    for (int g = blockIdx.x; g < groups; g += gridDim.x) {
+        if (wave == 0) {
+            // the group's q rows, one per lane, into LDS
+            const int64_t row = list[min(g * kRefineGroup + lane, n - 1)];
+            float qr[kHeadDim];
+            if constexpr (F32) {
+                const f32x4* src = reinterpret_cast<const f32x4*>(static_cast<const float*>(q) + row * kHeadDim);
 #pragma unroll
-        for (int k = 0; k < kMaxColsPerLane; ++k) p32[k] = 0.f;
-        // columns past n_b/2 read a valid one instead; their sums are ignored
-        const float* col[kMaxColsPerLane];
+                for (int t4 = 0; t4 < kHeadDim / 4; ++t4) {
+                    const f32x4 x = src[t4];
 #pragma unroll
-        for (int k = 0; k < kMaxColsPerLane; ++k) col[k] = Rs + min(lane + 64 * k, half - 1) * kRsStride;
-#pragma unroll 8
-        for (int t = 0; t < kHeadDim; ++t) {
-            const float qt = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, qv), t));
+                    for (int e2 = 0; e2 < 4; ++e2) qr[4 * t4 + e2] = x[e2];
+                }
+            } else {
+                const u32x4* src = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(q) + row * kHeadDim);
 #pragma unroll
-            for (int k = 0; k < kMaxColsPerLane; ++k) p32[k] = fmaf(qt, col[k][t], p32[k]);
-        }
-        float ss = qv * qv, mx = 0.f;
+                for (int t8 = 0; t8 < kHeadDim / 8; ++t8) {
+                    const u32x4 x = src[t8];
 #pragma unroll
-        for (int k = 0; k < kMaxColsPerLane; ++k)
-            if (lane + 64 * k < half) mx = fmaxf(mx, fabsf(p32[k]));
-        for (int o = 32; o >= 1; o >>= 1) {
-            ss += __shfl_xor(ss, o);
-            mx = fmaxf(mx, __shfl_xor(mx, o));
-        }
-        const float eps = (float)((64.0 * 0x1p-24 * 1.01 + 0x1p-46) * 1.01) * sqrtf(ss) * cn;
-        const float cut = mx - 2.f * eps;
-        int total = 0;
-        uint64_t masks[kMaxColsPerLane];
-#pragma unroll
-        for (int k = 0; k < kMaxColsPerLane; ++k) {
-            masks[k] = __ballot(lane + 64 * k < half && fabsf(p32[k]) >= cut);
-            total += __popcll(masks[k]);
-        }
-        double bv = -__builtin_inf();
-        int bi = 0x7FFFFFFF;
-        if (total <= 64) {
-            // pass 2: one candidate column per lane, fp64 in the oracle's order
-            int base = 0;
-#pragma unroll
-            for (int k = 0; k < kMaxColsPerLane; ++k) {
-                if ((masks[k] >> lane) & 1ull)
-                    cand[base + __popcll(masks[k] & ((1ull << lane) - 1ull))] = lane + 64 * k;
-                base += __popcll(masks[k]);
-            }
-            __builtin_amdgcn_s_waitcnt(0);
-            __builtin_amdgcn_wave_barrier();
-            const int c = lane < total ? cand[lane] : 0;
-            // q_t * R_tc is exact in fp64 (at most 48 significant bits), so
-            // whether the compiler fuses the multiply into the add or not, the
-            // sum rounds exactly as the plain loop does.
-            double p = 0.0;
-#pragma unroll 8
-            for (int t = 0; t < kHeadDim; ++t) {
-                const double qt = (double)__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, qv), t));
-                p = __dadd_rn(p, __dmul_rn(qt, (double)Rs[c * kRsStride + t]));
-            }
-            if (lane < total) {
-                better(p, c, bv, bi);
-                better(-p, half + c, bv, bi);
-            }
-            __builtin_amdgcn_wave_barrier();
-        } else {
-            double p[kMaxColsPerLane];
-#pragma unroll
-            for (int k = 0; k < kMaxColsPerLane; ++k) p[k] = 0.0;
-#pragma unroll 8
-            for (int t = 0; t < kHeadDim; ++t) {
-                const double qt = (double)__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, qv), t));
-#pragma unroll
-                for (int k = 0; k < kMaxColsPerLane; ++k)
-                    p[k] = __dadd_rn(p[k], __dmul_rn(qt, (double)col[k][t]));
-            }
-#pragma unroll
-            for (int k = 0; k < kMaxColsPerLane; ++k) {
-                const int c = lane + 64 * k;
-                if (c < half) {
-                    better(p[k], c, bv, bi);
-                    better(-p[k], half + c, bv, bi);
+                    for (int e2 = 0; e2 < 4; ++e2) {
+                        qr[8 * t8 + 2 * e2] = __uint_as_float(x[e2] << 16);
+                        qr[8 * t8 + 2 * e2 + 1] = __uint_as_float(x[e2] & 0xFFFF0000u);
+                    }
                 }
             }
+            float ss = 0.f;
+#pragma unroll
+            for (int t = 0; t < kHeadDim; ++t) {
+                ss = fmaf(qr[t], qr[t], ss);
+                S.qs[lane][t] = qr[t];
+            }
+            S.qn[lane] = sqrtf(ss);
+            S.cnt[lane] = 0;
         }
-        for (int o = 32; o >= 1; o >>= 1) {
-            const double ov = __shfl_xor(bv, o);
-            const int oi = __shfl_xor(bi, o);
-            better(ov, oi, bv, bi);
+        __syncthreads();
+
+        // pass 1: fp32 projections of columns c0 .. c0+ncols-1 for the
+        // lane's entry; the next t's R values and q value are loaded before
+        // the current t's products
+        float p[kRefineCols];
+#pragma unroll
+        for (int j = 0; j < kRefineCols; ++j) p[j] = 0.f;
+        auto pass1 = [&](auto full_tag) {
+            constexpr bool FULL = decltype(full_tag)::value;  // ncols == kRefineCols
+            const int last = ncols - 1;
+            auto col = [&](int j) { return FULL ? j : min(j, last); };
+            float rc[kRefineCols], qt = S.qs[lane][0];
+#pragma unroll
+            for (int j = 0; j < kRefineCols; ++j) rc[j] = Rr[c0 + col(j)];
+            for (int t = 0; t < kHeadDim; ++t) {
+                const int tn = min(t + 1, kHeadDim - 1);
+                float rn[kRefineCols];
+                const float* rt = Rr + (size_t)tn * half + c0;
+#pragma unroll
+                for (int j = 0; j < kRefineCols; ++j) rn[j] = rt[col(j)];
+                const float qn = S.qs[lane][tn];
+#pragma unroll
+                for (int j = 0; j < kRefineCols; ++j) p[j] = fmaf(qt, rc[j], p[j]);
+#pragma unroll
+                for (int j = 0; j < kRefineCols; ++j) rc[j] = rn[j];
+                qt = qn;
+            }
+        };
+        if (ncols == kRefineCols)
+            pass1(std::true_type{});
+        else if (ncols > 0)
+            pass1(std::false_type{});
+        float mxl = 0.f;
+#pragma unroll
+        for (int j = 0; j < kRefineCols; ++j)
+            if (j < ncols) mxl = fmaxf(mxl, fabsf(p[j]));
+        S.mx[wave][lane] = mxl;
+        __syncthreads();
+        float mx = 0.f;
+#pragma unroll
+        for (int w = 0; w < kRefineWaves; ++w) mx = fmaxf(mx, S.mx[w][lane]);
+        const float eps = (float)((64.0 * 0x1p-24 * 1.01 + 0x1p-46) * 1.01) * S.qn[lane] * cn;
+        const float cut = mx - 2.f * eps;
+#pragma unroll
+        for (int j = 0; j < kRefineCols; ++j)
+            if (j < ncols && fabsf(p[j]) >= cut) {
+                const int k = atomicAdd(&S.cnt[lane], 1);
+                if (k < kRefineCand) S.cand[lane][k] = c0 + j;
+            }
+        __syncthreads();
+
+        // pass 2: lane = (entry i, candidate k), four entries per wave
+        {
+            const int i = wave * (kRefineGroup / kRefineWaves) + lane / kRefineCand;
+            const int k = lane % kRefineCand;
+            const int ci = S.cnt[i];
+            double bv = -__builtin_inf();
+            int bi = 0x7FFFFFFF;
+            if (ci >= 1 && ci <= kRefineCand && k < ci) {
+                const int c = S.cand[i][k];
+                // q_t * R_tc is exact in fp64 (at most 48 significant bits), so
+                // whether the compiler fuses the multiply into the add or not,
+                // the sum rounds exactly as the plain loop does.
+                // R's column in runs of 16 values, all of a run's loads in flight together
+                double acc = 0.0;
+                for (int t0 = 0; t0 < kHeadDim; t0 += 16) {
+                    float rcol[16];
+#pragma unroll
+                    for (int u = 0; u < 16; ++u) rcol[u] = Rr[(size_t)(t0 + u) * half + c];
+#pragma unroll
+                    for (int u = 0; u < 16; ++u)
+                        acc = __dadd_rn(acc, __dmul_rn((double)S.qs[i][t0 + u], (double)rcol[u]));
+                }
+                better(acc, c, bv, bi);
+                better(-acc, half + c, bv, bi);
+            }
+#pragma unroll
+            for (int o = 1; o < kRefineCand; o <<= 1) {
+                const double ov = __shfl_xor(bv, o);
+                const int oi = __shfl_xor(bi, o);
+                better(ov, oi, bv, bi);
+            }
+            const int ei = g * kRefineGroup + i;
+            if (k == 0 && ei < n && ci >= 1 && ci <= kRefineCand) buckets[(int64_t)list[ei] * n_r + r] = bi;
         }
-        if (lane == 0) buckets[row * n_r + r] = bi;
+
+        // entries with too many candidates: every column in fp64, one wave each
+        for (int i = wave; i < kRefineGroup; i += kRefineWaves) {
+            const int ei = g * kRefineGroup + i;
+            const int ci = S.cnt[i];
+            if (ei >= n || (ci >= 1 && ci <= kRefineCand)) continue;  // uniform per wave
+            double bv = -__builtin_inf();
+            int bi = 0x7FFFFFFF;
+            for (int c = lane; c < half; c += 64) {
+                double acc = 0.0;
+                for (int t = 0; t < kHeadDim; ++t)
+                    acc = __dadd_rn(acc, __dmul_rn((double)S.qs[i][t], (double)Rr[(size_t)t * half + c]));
+                better(acc, c, bv, bi);
+                better(-acc, half + c, bv, bi);
+            }
+            for (int o = 32; o >= 1; o >>= 1) {
+                const double ov = __shfl_xor(bv, o);
+                const int oi = __shfl_xor(bi, o);
+                better(ov, oi, bv, bi);
+            }
+            if (lane == 0) buckets[(int64_t)list[ei] * n_r + r] = bi;
+        }
+        __syncthreads();  // the group's LDS is reused by the next one
     }
 }
 
@@ -719,11 +773,11 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
     constexpr int kWaves = 8, kPairsBf16 = 1, kPairsF32 = 1;
     const int64_t rows_per_block = kWaves * 64 * (f32 ? kPairsF32 : kPairsBf16);
     const unsigned grid = (unsigned)((rows + rows_per_block - 1) / rows_per_block);
-    const size_t refine_lds = (size_t)half * kRsStride * sizeof(float) + kRefineWaves * 64 * sizeof(int);
-    // Refinement blocks per round: one 128 KB-LDS block per CU over all rounds
-    // (a typical list holds well under 1% of the rows; longer ones are strided).
+
+    // Refinement blocks per round: a typical list holds well under 1% of the
+    // rows, a few groups of 64 per round; longer lists are strided.
     const unsigned refine_blocks =
-        (unsigned)std::max<int64_t>(1, std::min<int64_t>((256 + n_rounds - 1) / n_rounds, rows / 1024));
+        (unsigned)std::max<int64_t>(1, std::min<int64_t>(256, (rows + kRefineGroup - 1) / kRefineGroup));
     if (f32) {
         const size_t lds = kStageBytes + (size_t)rows_per_block * n_rounds * 2;
         hipFuncSetAttribute(reinterpret_cast<const void*>(&hash_kernel<true, kWaves, kPairsF32>),
@@ -731,9 +785,7 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
         hash_kernel<true, kWaves, kPairsF32><<<grid, kWaves * 64, lds, stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi,
                                                      w.r_mid, w.col_norm_max, err_sum,
                                                      err_pack, buckets, w.list, w.count);
-        hipFuncSetAttribute(reinterpret_cast<const void*>(&hash_refine_kernel<true>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)refine_lds);
-        hash_refine_kernel<true><<<dim3(refine_blocks, n_rounds), kRefineThreads, refine_lds, stream>>>(
+        hash_refine_kernel<true><<<dim3(refine_blocks, n_rounds), kRefineThreads, 0, stream>>>(
             q, R, half, n_rounds, rows, w.list, w.count, w.col_norm_max, buckets);
     } else {
         const size_t lds = kStageBytes + (size_t)rows_per_block * n_rounds * 2;
@@ -742,9 +794,7 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
         hash_kernel<false, kWaves, kPairsBf16><<<grid, kWaves * 64, lds, stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi,
                                                       w.r_mid, w.col_norm_max, err_sum,
                                                       err_pack, buckets, w.list, w.count);
-        hipFuncSetAttribute(reinterpret_cast<const void*>(&hash_refine_kernel<false>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)refine_lds);
-        hash_refine_kernel<false><<<dim3(refine_blocks, n_rounds), kRefineThreads, refine_lds, stream>>>(
+        hash_refine_kernel<false><<<dim3(refine_blocks, n_rounds), kRefineThreads, 0, stream>>>(
             q, R, half, n_rounds, rows, w.list, w.count, w.col_norm_max, buckets);
     }
     return hipGetLastError();
