@@ -36,45 +36,55 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 constexpr int kRB = 2;  // 32-row blocks per wave: each staged R tile feeds 2 * 8 MFMAs
 
 // One R column per block of 64 lanes (lane = t): bf16 planes hi/mid,
-// [n_r][half_pad][64] (column contiguous, zero padded), and the column's
-// 2-norm.
+// [n_r][half_pad][64] (column contiguous, zero padded), and three 2-norms of
+// the column, [3][n_r][half_pad]: |R_c|, |R_c - hi_c|, |R_c - hi_c - mid_c|.
 __global__ __launch_bounds__(64) void prep_r_cols_kernel(const float* __restrict__ R, int half,
                                                          int half_pad, uint16_t* __restrict__ r_hi,
                                                          uint16_t* __restrict__ r_mid,
                                                          float* __restrict__ col_norm) {
     const int c = blockIdx.x, r = blockIdx.y, t = threadIdx.x;
+    const int n_r = gridDim.y;
     const float x = c < half ? R[((size_t)r * kHeadDim + t) * half + c] : 0.f;
     const uint32_t hi = f32_to_bf16_bits(x);
     const float res = x - bf16_bits_to_f32(hi);  // exact (Sterbenz)
     const uint32_t mid = f32_to_bf16_bits(res);
+    const float res2 = res - bf16_bits_to_f32(mid);  // exact
     const size_t o = ((size_t)r * half_pad + c) * kHeadDim + t;
     r_hi[o] = (uint16_t)hi;
     r_mid[o] = (uint16_t)mid;
-    float ss = x * x;
-    for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
-    if (t == 0) col_norm[(size_t)r * half_pad + c] = sqrtf(ss);
+    float s0 = x * x, s1 = res * res, s2 = res2 * res2;
+    for (int off = 32; off >= 1; off >>= 1) {
+        s0 += __shfl_xor(s0, off);
+        s1 += __shfl_xor(s1, off);
+        s2 += __shfl_xor(s2, off);
+    }
+    if (t == 0) {
+        const size_t plane = (size_t)n_r * half_pad, k = (size_t)r * half_pad + c;
+        col_norm[k] = sqrtf(s0);
+        col_norm[plane + k] = sqrtf(s1);
+        col_norm[2 * plane + k] = sqrtf(s2);
+    }
 }
 
-// Largest column norm of each round; also clears the round's refinement counter.
-__global__ __launch_bounds__(256) void prep_r_max_kernel(const float* __restrict__ col_norm,
-                                                         int half_pad,
-                                                         float* __restrict__ col_norm_max,
-                                                         int* __restrict__ refine_count) {
+// Largest of each column norm per round (block (r, which)); block (0, 0)
+// also clears the n_clear list counters.
+__global__ __launch_bounds__(256) void prep_r_max_kernel(const float* __restrict__ col_norm, int n_r,
+                                                         int half_pad, float* __restrict__ norm_max,
+                                                         int* __restrict__ counts, int n_clear) {
     __shared__ float red[256];
-    const int r = blockIdx.x;
+    const int r = blockIdx.x, which = blockIdx.y;
+    if (r == 0 && which == 0)
+        for (int i = threadIdx.x; i < n_clear; i += blockDim.x) counts[i] = 0;
+    const float* cn = col_norm + ((size_t)which * n_r + r) * half_pad;
     float mx = 0.f;
-    for (int c = threadIdx.x; c < half_pad; c += blockDim.x)
-        mx = fmaxf(mx, col_norm[(size_t)r * half_pad + c]);
+    for (int c = threadIdx.x; c < half_pad; c += blockDim.x) mx = fmaxf(mx, cn[c]);
     red[threadIdx.x] = mx;
     __syncthreads();
     for (int s = 128; s > 0; s >>= 1) {
         if ((int)threadIdx.x < s) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + s]);
         __syncthreads();
     }
-    if (threadIdx.x == 0) {
-        col_norm_max[r] = red[0];
-        refine_count[r] = 0;
-    }
+    if (threadIdx.x == 0) norm_max[which * n_r + r] = red[0];
 }
 
 template <bool F32>
@@ -294,12 +304,12 @@ __global__ __launch_bounds__(kRefineThreads, 1) void hash_refine_kernel(const vo
 }
 
 // R streams through LDS in stages of 256 columns (8 tiles of 32) of one
-// round, both bf16 planes, double-buffered: 2 x 2 x 256 x 128 B = 128 KB.  A
-// stage is copied straight from global memory into LDS (global_load_lds, no
-// registers in between) while the previous one is consumed, so there is one
-// barrier per 8 tiles.  A 16-byte piece p of column c sits at slot
-// p ^ stage_swz(c) of the column's 128 bytes: the 16 columns read together
-// by one operand load then hit distinct banks.
+// round, one or both bf16 planes, double-buffered: at most 2 x 2 x 256 x
+// 128 B = 128 KB.  A stage is copied straight from global memory into LDS
+// (global_load_lds, no registers in between) while the previous one is
+// consumed, so there is one barrier per 8 tiles.  A 16-byte piece p of
+// column c sits at slot p ^ stage_swz(c) of the column's 128 bytes: the 16
+// columns read together by one operand load then hit distinct banks.
 constexpr int kStageCols = 256;
 constexpr int kStageTiles = kStageCols / 32;
 constexpr size_t kStageBytes = 2ull * 2 * kStageCols * 128;
@@ -309,6 +319,17 @@ __device__ __forceinline__ int stage_swz(int c) { return (c ^ (c >> 3)) & 7; }
 __device__ __forceinline__ uint32_t stage_offset(int buf, int plane, int col) {
     return (uint32_t)(((buf * 2 + plane) * kStageCols + col) * 128);
 }
+
+// The screen's open row-rounds go to kSegs segments per round (workgroup b
+// appends to segment b % kSegs), so each list counter sees few atomics.
+constexpr int kSegs = 64;
+
+// Passes of the main kernel.
+enum : int {
+    kScreen = 0,  // bf16 input: R's hi plane only, every row and round
+    kExact = 1,   // both planes (three products for fp32 input), every row and round
+    kListed = 2,  // bf16 input: both planes, the rows the screen left open in one round
+};
 
 struct Tile {
     f32x16 acc[kRB];
@@ -321,7 +342,7 @@ struct Tile {
 //    |projection| in bits 5..31, j in bits 1..4): one rotate and one and-or
 //    per projection, and the key also carries the winner's sign.
 //  * bf16 input: |projection| in bits 4..30 and j in bits 0..3, one and-or;
-//    the winner's sign is recomputed once per row and round (win_sign).
+//    the winner's sign is recomputed once per row and round.
 // Keys of tiles past the round are masked to j, near zero.
 template <bool F32>
 __device__ __forceinline__ uint32_t proj_key(float x, int j, bool live) {
@@ -355,25 +376,31 @@ __device__ __forceinline__ void key_update2(uint32_t k1, uint32_t k2, uint32_t& 
     sc = max(sc, mid);
 }
 
-__device__ __forceinline__ void load_ops(u32x4 (&op)[8], const char* __restrict__ hi_base,
-                                         const char* __restrict__ mid_base, int col, int h) {
-    const int sw = stage_swz(col);
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-        const uint32_t o = (uint32_t)col * 128u + (uint32_t)(((4 * h + s) ^ sw) << 4);
-        op[2 * s] = *reinterpret_cast<const u32x4*>(hi_base + o);
-        op[2 * s + 1] = *reinterpret_cast<const u32x4*>(mid_base + o);
-    }
+// Operand piece i of a tile (NP planes): k-step i / NP of plane i % NP.
+template <int NP>
+__device__ __forceinline__ uint32_t piece_offset(int col, int h, int i) {
+    const int s = NP == 2 ? i >> 1 : i;
+    return (uint32_t)col * 128u + (uint32_t)(((4 * h + s) ^ stage_swz(col)) << 4);
 }
 
-// One step of the tile pipeline, in eight slices.  Slice i issues the two
-// (three for fp32 input) products of operand piece i of the tile held in
-// `op` into `nxt`, refills op[i] with the same piece of the following tile
-// (PREF), and runs one eighth of the epilogue of the previous tile `cur`
-// (EPI).  A wave issues in order, so this interleaving is what lets the
-// vector ALUs work while the matrix core runs; the scheduling barriers keep
-// the compiler from regrouping the slices.
-template <bool F32, bool PREF, bool EPI>
+template <int NP>
+__device__ __forceinline__ void load_ops(u32x4 (&op)[8], const char* __restrict__ hi_base,
+                                         const char* __restrict__ mid_base, int col, int h) {
+#pragma unroll
+    for (int i = 0; i < 4 * NP; ++i)
+        op[i] = *reinterpret_cast<const u32x4*>(((NP == 2 && (i & 1)) ? mid_base : hi_base) +
+                                                piece_offset<NP>(col, h, i));
+}
+
+// One step of the tile pipeline, in eight slices.  Slice i issues the
+// products of the tile held in `op` into `nxt` for operand piece i (both
+// planes; for fp32 input the hi plane also meets q's second plane) or, with
+// one plane, for piece i / 2 on even slices; refills that piece with the same
+// piece of the following tile (PREF); and runs one eighth of the epilogue of
+// the previous tile `cur` (EPI).  A wave issues in order, so this
+// interleaving is what lets the vector ALUs work while the matrix core runs;
+// the scheduling barriers keep the compiler from regrouping the slices.
+template <bool F32, int NP, bool PREF, bool EPI>
 __device__ __forceinline__ void tile_step(Tile& nxt, u32x4 (&op)[8], const char* __restrict__ hi_base,
                                           const char* __restrict__ mid_base, int col_pref, int h,
                                           const bf16x8 (&qa)[kRB][4], const bf16x8 (&qm)[kRB][4],
@@ -381,25 +408,27 @@ __device__ __forceinline__ void tile_step(Tile& nxt, u32x4 (&op)[8], const char*
                                           uint32_t (&best)[kRB], uint32_t (&second)[kRB],
                                           int (&best_tile)[kRB]) {
     static_assert(kRB == 2, "slices written for two row blocks");
-    const int sw = stage_swz(col_pref);
     uint32_t b[kRB] = {best[0], best[1]}, sc[kRB] = {second[0], second[1]};
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         __builtin_amdgcn_sched_barrier(0);
-        const int s = i >> 1;
-        const bf16x8 a = as_bf16x8(op[i]);
+        if (NP == 2 || (i & 1) == 0) {
+            const int pi = NP == 2 ? i : i >> 1;  // operand piece
+            const int s = i >> 1;  // k-step
+            const bool hi_plane = NP == 1 || (i & 1) == 0;
+            const bf16x8 a = as_bf16x8(op[pi]);
 #pragma unroll
-        for (int rb = 0; rb < kRB; ++rb)
-            nxt.acc[rb] = mfma32x32x16(a, qa[rb][s], i == 0 ? f32x16{} : nxt.acc[rb]);
-        if constexpr (F32) {
-            if ((i & 1) == 0) {
+            for (int rb = 0; rb < kRB; ++rb)
+                nxt.acc[rb] = mfma32x32x16(a, qa[rb][s], pi == 0 ? f32x16{} : nxt.acc[rb]);
+            if constexpr (F32) {
+                if (hi_plane) {
 #pragma unroll
-                for (int rb = 0; rb < kRB; ++rb) nxt.acc[rb] = mfma32x32x16(a, qm[rb][s], nxt.acc[rb]);
+                    for (int rb = 0; rb < kRB; ++rb) nxt.acc[rb] = mfma32x32x16(a, qm[rb][s], nxt.acc[rb]);
+                }
             }
-        }
-        if constexpr (PREF) {
-            const uint32_t o = (uint32_t)col_pref * 128u + (uint32_t)(((4 * h + s) ^ sw) << 4);
-            op[i] = *reinterpret_cast<const u32x4*>(((i & 1) ? mid_base : hi_base) + o);
+            if constexpr (PREF)
+                op[pi] = *reinterpret_cast<const u32x4*>((hi_plane ? hi_base : mid_base) +
+                                                         piece_offset<NP>(col_pref, h, pi));
         }
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (EPI) {
@@ -435,13 +464,14 @@ __device__ __forceinline__ void tile_epilogue(const Tile& T, int tile, bool live
     }
 }
 
-// Copy global stage g (round g / spr, columns (g % spr) * 256 ...) into
-// buffer buf.  Each wave moves whole 1 KB runs of 8 columns of one plane.
-template <int WAVES>
+// Copy global stage g (round g / spr, columns (g % spr) * 256 ...) of NP
+// planes into buffer buf.  Each wave moves whole 1 KB runs of 8 columns of
+// one plane.
+template <int WAVES, int NP>
 __device__ __forceinline__ void load_stage(char* smem, int buf, int g, int spr, int half_pad,
                                            const uint16_t* __restrict__ r_hi,
                                            const uint16_t* __restrict__ r_mid, int wave, int lane) {
-    constexpr int kRuns = 2 * kStageCols / 8;  // 1 KB runs per stage
+    constexpr int kRuns = NP * kStageCols / 8;  // 1 KB runs per stage
     static_assert(kRuns % WAVES == 0, "runs split evenly over the waves");
     const int r = g / spr, st = g % spr;
     const int cl_lane = lane >> 3, slot = lane & 7;
@@ -462,100 +492,139 @@ __device__ __forceinline__ void load_stage(char* smem, int buf, int g, int spr, 
 }
 
 // Winner of a row-round as kept in LDS until the row's ids are written:
-// the bucket id, or kUnsettled when the exact pass must decide.
+// the bucket id, or kUnsettled when a later pass must decide.
 constexpr uint16_t kUnsettled = 0xFFFFu;
 
-// A wave owns PAIRS pairs of 32-row blocks (64 * PAIRS rows); every staged
-// tile is swept once per pair, so a stage feeds PAIRS times as many products.
-template <bool F32, int WAVES, int PAIRS>
+// The main kernel, one of three passes (MODE).  A wave owns 64 rows (two
+// 32-row blocks) and sweeps every staged tile once for them.
+//  * kScreen and kExact take rows blockIdx.x * 64 * WAVES + ... and all
+//    rounds; kListed takes, for round blockIdx.z, the rows at chunk
+//    blockIdx.x of the screen's segment blockIdx.y of that round.
+//  * A row-round is settled when the gap between the best and second-best
+//    key exceeds twice the error bound
+//        eps = |q| * (res_max[r] + err_acc * max_c |R_c|) + err_pack * key
+//    (res_max: largest 2-norm of R's columns less the planes used, none
+//    for fp32 input, whose planes' residual is inside err_acc); its id goes
+//    to buckets.  Otherwise the row is appended to the round's list: the
+//    screen's lists are segmented, [round][kSegs][seg_cap] with counts
+//    [round][kSegs]; the exact passes' are [round][rows] with one count per
+//    round (few rows reach them).
+template <bool F32, int MODE, int WAVES>
 __global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
     const void* __restrict__ q, int64_t rows, int n_r, int half, int half_pad,
     const uint16_t* __restrict__ r_hi, const uint16_t* __restrict__ r_mid,
-    const float* __restrict__ col_norm_max, float err_sum, float err_pack,
-    int32_t* __restrict__ buckets, int* __restrict__ refine_lists, int* __restrict__ refine_counts) {
+    const float* __restrict__ col_norm_max, const float* __restrict__ res_max, float err_acc,
+    float err_pack, int32_t* __restrict__ buckets, const int* __restrict__ list_in,
+    const int* __restrict__ count_in, int* __restrict__ list_out, int* __restrict__ count_out,
+    int64_t seg_cap) {
+    static_assert(!F32 || MODE == kExact, "fp32 input takes the exact pass only");
+    constexpr int NP = MODE == kScreen ? 1 : 2;
+    constexpr int kWaveRows = 64;
     extern __shared__ __attribute__((aligned(16))) char smem[];
-    constexpr int kWaveRows = 64 * PAIRS;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6, h = lane >> 5, n = lane & 31;
-    const int64_t row0 = (int64_t)blockIdx.x * (WAVES * kWaveRows) + wave * kWaveRows;
     const int tpr = half_pad / 32;                         // tiles per round
     const int spr = (tpr + kStageTiles - 1) / kStageTiles;  // stages per round
-    const int n_stages = n_r * spr;
-    // this wave's winners: [row in wave][round]
-    uint16_t* win = reinterpret_cast<uint16_t*>(smem + kStageBytes) + (size_t)wave * kWaveRows * n_r;
+    const int r_lo = MODE == kListed ? (int)blockIdx.z : 0;
+    const int r_end = MODE == kListed ? r_lo + 1 : n_r;
+    const int nrb = r_end - r_lo;  // rounds of this block
+    int64_t listed = 0;            // kListed: rows in this block's segment
+    const int* seg_rows = nullptr;
+    if constexpr (MODE == kListed) {
+        const int64_t seg = (int64_t)r_lo * kSegs + blockIdx.y;
+        listed = count_in[seg];
+        seg_rows = list_in + seg * seg_cap;
+    }
+    // kListed: a few workgroups per segment take its chunks of 64 * WAVES rows
+    // in turn (an empty workgroup costs as much to launch as a busy one when
+    // one fills a CU); the other passes take one chunk each.
+    for (int64_t chunk = blockIdx.x;; chunk += gridDim.x) {
+    if (MODE == kListed && chunk * (WAVES * kWaveRows) >= listed) break;  // uniform per block
+    const int64_t slot0 = chunk * (WAVES * kWaveRows) + wave * kWaveRows;
+    // the row of lane n of row block rb (lane half h keeps row block h's
+    // results at the end)
+    auto row_of = [&](int rb, bool& valid) -> int64_t {
+        const int64_t k = slot0 + rb * 32 + n;
+        if constexpr (MODE == kListed) {
+            valid = k < listed;
+            return valid ? seg_rows[k] : 0;
+        } else {
+            valid = k < rows;
+            return valid ? k : 0;
+        }
+    };
+    // this wave's winners: [row in wave][round of the block]
+    uint16_t* win = reinterpret_cast<uint16_t*>(smem + kStageBytes) + (size_t)wave * kWaveRows * nrb;
 
-    load_stage<WAVES>(smem, 0, 0, spr, half_pad, r_hi, r_mid, wave, lane);
+    load_stage<WAVES, NP>(smem, 0, r_lo * spr, spr, half_pad, r_hi, r_mid, wave, lane);
 
     // Queries as the B operand: lane holds row (n) and k = 32h + 8s + e, s = 0..3.
-    bf16x8 qa[PAIRS][kRB][4];
-    bf16x8 qm[PAIRS][kRB][4];  // fp32 input: second bf16 plane of q
-    float qn[PAIRS][kRB];
+    bf16x8 qa[kRB][4];
+    bf16x8 qm[kRB][4];  // fp32 input: second bf16 plane of q
+    float qn[kRB];
 #pragma unroll
-    for (int pr = 0; pr < PAIRS; ++pr)
+    for (int rb = 0; rb < kRB; ++rb) {
+        bool valid;
+        const int64_t row = row_of(rb, valid);
+        float ss = 0.f;
+        if constexpr (F32) {
+            const float* src = static_cast<const float*>(q) + row * kHeadDim + 32 * h;
 #pragma unroll
-        for (int rb = 0; rb < kRB; ++rb) {
-            const int64_t row = row0 + pr * 64 + rb * 32 + n;
-            const bool valid = row < rows;
-            float ss = 0.f;
-            if constexpr (F32) {
-                const float* src = static_cast<const float*>(q) + row * kHeadDim + 32 * h;
+            for (int s4 = 0; s4 < 4; ++s4) {
+                f32x4 x0 = valid ? *reinterpret_cast<const f32x4*>(src + 8 * s4) : f32x4{0, 0, 0, 0};
+                f32x4 x1 = valid ? *reinterpret_cast<const f32x4*>(src + 8 * s4 + 4) : f32x4{0, 0, 0, 0};
+                float xs[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+                u32x4 hi, mid;
 #pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    f32x4 x0 = valid ? *reinterpret_cast<const f32x4*>(src + 8 * s) : f32x4{0, 0, 0, 0};
-                    f32x4 x1 = valid ? *reinterpret_cast<const f32x4*>(src + 8 * s + 4) : f32x4{0, 0, 0, 0};
-                    float xs[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-                    u32x4 hi, mid;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const uint32_t h0 = f32_to_bf16_bits(xs[2 * e]), h1 = f32_to_bf16_bits(xs[2 * e + 1]);
-                        const uint32_t m0 = f32_to_bf16_bits(xs[2 * e] - bf16_bits_to_f32(h0));
-                        const uint32_t m1 = f32_to_bf16_bits(xs[2 * e + 1] - bf16_bits_to_f32(h1));
-                        hi[e] = h0 | (h1 << 16);
-                        mid[e] = m0 | (m1 << 16);
-                        ss = fmaf(xs[2 * e], xs[2 * e], ss);
-                        ss = fmaf(xs[2 * e + 1], xs[2 * e + 1], ss);
-                    }
-                    qa[pr][rb][s] = as_bf16x8(hi);
-                    qm[pr][rb][s] = as_bf16x8(mid);
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t h0 = f32_to_bf16_bits(xs[2 * e]), h1 = f32_to_bf16_bits(xs[2 * e + 1]);
+                    const uint32_t m0 = f32_to_bf16_bits(xs[2 * e] - bf16_bits_to_f32(h0));
+                    const uint32_t m1 = f32_to_bf16_bits(xs[2 * e + 1] - bf16_bits_to_f32(h1));
+                    hi[e] = h0 | (h1 << 16);
+                    mid[e] = m0 | (m1 << 16);
+                    ss = fmaf(xs[2 * e], xs[2 * e], ss);
+                    ss = fmaf(xs[2 * e + 1], xs[2 * e + 1], ss);
                 }
-            } else {
-                const uint16_t* src = static_cast<const uint16_t*>(q) + row * kHeadDim + 32 * h;
-#pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    const u32x4 raw = valid ? *reinterpret_cast<const u32x4*>(src + 8 * s) : u32x4{0, 0, 0, 0};
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const float a = __uint_as_float(raw[e] << 16), b = __uint_as_float(raw[e] & 0xFFFF0000u);
-                        ss = fmaf(a, a, ss);
-                        ss = fmaf(b, b, ss);
-                    }
-                    qa[pr][rb][s] = as_bf16x8(raw);
-                    qm[pr][rb][s] = as_bf16x8(u32x4{0, 0, 0, 0});
-                }
+                qa[rb][s4] = as_bf16x8(hi);
+                qm[rb][s4] = as_bf16x8(mid);
             }
-            ss += __shfl_xor(ss, 32);
-            qn[pr][rb] = sqrtf(ss);
+        } else {
+            const uint16_t* src = static_cast<const uint16_t*>(q) + row * kHeadDim + 32 * h;
+#pragma unroll
+            for (int s4 = 0; s4 < 4; ++s4) {
+                const u32x4 raw = valid ? *reinterpret_cast<const u32x4*>(src + 8 * s4) : u32x4{0, 0, 0, 0};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float a = __uint_as_float(raw[e] << 16), b = __uint_as_float(raw[e] & 0xFFFF0000u);
+                    ss = fmaf(a, a, ss);
+                    ss = fmaf(b, b, ss);
+                }
+                qa[rb][s4] = as_bf16x8(raw);
+                qm[rb][s4] = as_bf16x8(u32x4{0, 0, 0, 0});
+            }
         }
+        ss += __shfl_xor(ss, 32);
+        qn[rb] = sqrtf(ss);
+    }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
-    uint32_t best[PAIRS][kRB], second[PAIRS][kRB];
-    int best_tile[PAIRS][kRB];
-    for (int g = 0; g < n_stages; ++g) {
-        const int r = g / spr, st = g % spr, buf = g & 1;
+    uint32_t best[kRB], second[kRB];
+    int best_tile[kRB];
+    const int g_end = r_end * spr;
+    for (int g = r_lo * spr; g < g_end; ++g) {
+        const int r = g / spr, st = g % spr, buf = (g - r_lo * spr) & 1;
         if (st == 0) {
 #pragma unroll
-            for (int pr = 0; pr < PAIRS; ++pr)
-#pragma unroll
-                for (int rb = 0; rb < kRB; ++rb) {
-                    best[pr][rb] = second[pr][rb] = 0u;
-                    best_tile[pr][rb] = 0;
-                }
+            for (int rb = 0; rb < kRB; ++rb) {
+                best[rb] = second[rb] = 0u;
+                best_tile[rb] = 0;
+            }
         }
         // the next stage lands in the other buffer while this one computes
-        if (g + 1 < n_stages)
-            load_stage<WAVES>(smem, buf ^ 1, g + 1, spr, half_pad, r_hi, r_mid, wave, lane);
+        if (g + 1 < g_end)
+            load_stage<WAVES, NP>(smem, buf ^ 1, g + 1, spr, half_pad, r_hi, r_mid, wave, lane);
         const char* hi_base = smem + stage_offset(buf, 0, 0);
         const char* mid_base = smem + stage_offset(buf, 1, 0);
         const int nt = min(kStageTiles, tpr - st * kStageTiles);
@@ -563,180 +632,184 @@ __global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
         // Every stage runs all eight tiles; tiles past the round (a last,
         // partial stage) compute on stale LDS and their keys are masked to
         // (near) zero, so they can only win when every key is tiny, and such
-        // a row is flagged and settled exactly.
+        // a row is left to the exact passes.
         static_assert(kStageTiles == 8, "pipeline written for eight tiles per stage");
-#pragma unroll 1
-        for (int pr = 0; pr < PAIRS; ++pr) {
-            // the pair's operands and running state, selected without indexing
-            bf16x8 qc[kRB][4], qmc[kRB][4];
-            uint32_t bc[kRB], sc[kRB];
-            int tc[kRB];
-#pragma unroll
-            for (int rb = 0; rb < kRB; ++rb) {
-#pragma unroll
-                for (int s4 = 0; s4 < 4; ++s4) {
-                    qc[rb][s4] = qa[0][rb][s4];
-                    qmc[rb][s4] = qm[0][rb][s4];
-#pragma unroll
-                    for (int o = 1; o < PAIRS; ++o)
-                        if (pr == o) {
-                            qc[rb][s4] = qa[o][rb][s4];
-                            qmc[rb][s4] = qm[o][rb][s4];
-                        }
-                }
-                bc[rb] = best[0][rb];
-                sc[rb] = second[0][rb];
-                tc[rb] = best_tile[0][rb];
-#pragma unroll
-                for (int o = 1; o < PAIRS; ++o)
-                    if (pr == o) {
-                        bc[rb] = best[o][rb];
-                        sc[rb] = second[o][rb];
-                        tc[rb] = best_tile[o][rb];
-                    }
-            }
+        {
             Tile ta, tb;
             u32x4 op[8];
-            load_ops(op, hi_base, mid_base, n, h);
-            tile_step<F32, true, false>(ta, op, hi_base, mid_base, 32 + n, h, qc, qmc, tb, 0, false,
-                                        bc, sc, tc);
+            load_ops<NP>(op, hi_base, mid_base, n, h);
+            tile_step<F32, NP, true, false>(ta, op, hi_base, mid_base, 32 + n, h, qa, qm, tb, 0, false,
+                                            best, second, best_tile);
 #pragma unroll 1
             for (int t = 1; t < kStageTiles - 1; t += 2) {
-                tile_step<F32, true, true>(tb, op, hi_base, mid_base, 32 * (t + 1) + n, h, qc, qmc,
-                                           ta, t0 + t - 1, t - 1 < nt, bc, sc, tc);
-                tile_step<F32, true, true>(ta, op, hi_base, mid_base, 32 * (t + 2) + n, h, qc, qmc,
-                                           tb, t0 + t, t < nt, bc, sc, tc);
+                tile_step<F32, NP, true, true>(tb, op, hi_base, mid_base, 32 * (t + 1) + n, h, qa, qm,
+                                               ta, t0 + t - 1, t - 1 < nt, best, second, best_tile);
+                tile_step<F32, NP, true, true>(ta, op, hi_base, mid_base, 32 * (t + 2) + n, h, qa, qm,
+                                               tb, t0 + t, t < nt, best, second, best_tile);
             }
-            tile_step<F32, false, true>(tb, op, hi_base, mid_base, 0, h, qc, qmc, ta, t0 + 6, 6 < nt,
-                                        bc, sc, tc);
-            tile_epilogue<F32>(tb, t0 + 7, 7 < nt, bc, sc, tc);
-#pragma unroll
-            for (int o = 0; o < PAIRS; ++o)
-                if (pr == o) {
-#pragma unroll
-                    for (int rb = 0; rb < kRB; ++rb) {
-                        best[o][rb] = bc[rb];
-                        second[o][rb] = sc[rb];
-                        best_tile[o][rb] = tc[rb];
-                    }
-                }
+            tile_step<F32, NP, false, true>(tb, op, hi_base, mid_base, 0, h, qa, qm, ta, t0 + 6, 6 < nt,
+                                            best, second, best_tile);
+            tile_epilogue<F32>(tb, t0 + 7, 7 < nt, best, second, best_tile);
         }
 
         if (st == spr - 1) {
             // Round epilogue: merge the two lane halves (different columns of
             // the same row) and decide; lane half h keeps row block h's result.
             const float cn = col_norm_max[r];
+            const float res = F32 ? 0.f : res_max[r];
 #pragma unroll
-            for (int pr = 0; pr < PAIRS; ++pr)
+            for (int rb = 0; rb < kRB; ++rb) {
+                const uint32_t bb = best[rb], ss2 = second[rb];
+                const uint32_t bp = __shfl_xor(bb, 32), sp = __shfl_xor(ss2, 32);
+                const int tp = __shfl_xor(best_tile[rb], 32);
+                const bool mine = bb > bp || (bb == bp && h == 0);
+                const uint32_t bk = mine ? bb : bp;
+                const uint32_t sk = max(min(bb, bp), max(ss2, sp));
+                const float b1 = key_magnitude<F32>(bk);
+                const float s1 = key_magnitude<F32>(sk);
+                const int hw = mine ? h : (h ^ 1);
+                const int tw = mine ? best_tile[rb] : tp;
+                const uint32_t j = key_index<F32>(bk);
+                const int col = tw * 32 + 8 * (int)(j >> 2) + 4 * hw + (int)(j & 3u);
+                // Every screened key is within eps of its exact |projection|;
+                // an exchange of winners needs a gap <= 2 eps.  When the gap is
+                // larger the winner's magnitude exceeds eps, so the sign of any
+                // value within eps of its projection is the exact one.
+                const float thr = 2.04f * (qn[rb] * (res + err_acc * cn) + err_pack * b1);
+                const bool flag = !(b1 - s1 > thr) || col >= half;
+                bool negative;
+                if constexpr (F32) {
+                    negative = (bk & 1u) != 0;
+                } else {
+                    // q_row . R_col over the planes the pass used (the same
+                    // products as the screen, fp32 sums): each lane half adds its
+                    // 32 k-values.  A flagged winner may sit past the round; any
+                    // valid column stands in, its sign unused.
+                    const int colc = min(col, half_pad - 1);
+                    const size_t o = ((size_t)r * half_pad + colc) * kHeadDim + 32 * h;
+                    const u32x4* ph = reinterpret_cast<const u32x4*>(r_hi + o);
+                    const u32x4* pm = reinterpret_cast<const u32x4*>(r_mid + o);
+                    float part = 0.f;
 #pragma unroll
-                for (int rb = 0; rb < kRB; ++rb) {
-                    const uint32_t bb = best[pr][rb], ss2 = second[pr][rb];
-                    const uint32_t bp = __shfl_xor(bb, 32), sp = __shfl_xor(ss2, 32);
-                    const int tp = __shfl_xor(best_tile[pr][rb], 32);
-                    const bool mine = bb > bp || (bb == bp && h == 0);
-                    const uint32_t bk = mine ? bb : bp;
-                    const uint32_t sk = max(min(bb, bp), max(ss2, sp));
-                    const float b1 = key_magnitude<F32>(bk);
-                    const float s1 = key_magnitude<F32>(sk);
-                    const int hw = mine ? h : (h ^ 1);
-                    const int tw = mine ? best_tile[pr][rb] : tp;
-                    const uint32_t j = key_index<F32>(bk);
-                    const int col = tw * 32 + 8 * (int)(j >> 2) + 4 * hw + (int)(j & 3u);
-                    // Every screened key is within eps = err_sum*|q|*max|R_c| + err_pack*key
-                    // of its exact |projection|; an exchange of winners needs a gap <= 2 eps.
-                    // When the gap is larger the winner's magnitude exceeds eps, so the
-                    // sign of any value within eps of its projection is the exact one.
-                    const float thr = 2.04f * (err_sum * qn[pr][rb] * cn + err_pack * b1);
-                    const bool flag = !(b1 - s1 > thr) || col >= half;
-                    bool negative;
-                    if constexpr (F32) {
-                        negative = (bk & 1u) != 0;
-                    } else {
-                        // q_row . R_col over both planes (the same products as the
-                        // screen, fp32 sums): each lane half adds its 32 k-values.
-                        // A flagged winner may sit past the round; any valid
-                        // column stands in, its sign unused.
-                        const int colc = min(col, half_pad - 1);
-                        const size_t o = ((size_t)r * half_pad + colc) * kHeadDim + 32 * h;
-                        const u32x4* ph = reinterpret_cast<const u32x4*>(r_hi + o);
-                        const u32x4* pm = reinterpret_cast<const u32x4*>(r_mid + o);
-                        float part = 0.f;
+                    for (int s4 = 0; s4 < 4; ++s4) {
+                        const u32x4 qv = __builtin_bit_cast(u32x4, qa[rb][s4]);
+                        const u32x4 hv = ph[s4];
+                        u32x4 mv = {0u, 0u, 0u, 0u};
+                        if constexpr (NP == 2) mv = pm[s4];
 #pragma unroll
-                        for (int s4 = 0; s4 < 4; ++s4) {
-                            const u32x4 qv = __builtin_bit_cast(u32x4, qa[pr][rb][s4]);
-                            const u32x4 hv = ph[s4], mv = pm[s4];
-#pragma unroll
-                            for (int e = 0; e < 4; ++e) {
-                                const uint32_t qw = qv[e], hw2 = hv[e], mw = mv[e];
-                                part = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, qw),
-                                                                       __builtin_bit_cast(bf16x2, hw2), part, false);
+                        for (int e = 0; e < 4; ++e) {
+                            const uint32_t qw = qv[e], hw2 = hv[e], mw = mv[e];
+                            part = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, qw),
+                                                                   __builtin_bit_cast(bf16x2, hw2), part, false);
+                            if constexpr (NP == 2)
                                 part = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, qw),
                                                                        __builtin_bit_cast(bf16x2, mw), part, false);
-                            }
                         }
-                        negative = part + __shfl_xor(part, 32) < 0.f;
                     }
-                    const int id = negative ? half + col : col;
-                    if (rb == h) win[(pr * 64 + rb * 32 + n) * n_r + r] = flag ? kUnsettled : (uint16_t)id;
+                    negative = part + __shfl_xor(part, 32) < 0.f;
                 }
+                const int id = negative ? half + col : col;
+                if (rb == h) win[(rb * 32 + n) * nrb + (r - r_lo)] = flag ? kUnsettled : (uint16_t)id;
+            }
         }
         // the next stage has landed and every wave is done with this buffer
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
     }
 
-    // Write each row's ids (contiguous) and queue the unsettled row-rounds.
-#pragma unroll
-    for (int pr = 0; pr < PAIRS; ++pr) {
-        const int64_t row = row0 + pr * 64 + h * 32 + n;
-        const bool valid = row < rows;
-        const uint16_t* w = win + (pr * 64 + h * 32 + n) * n_r;
-        int32_t* out = buckets + row * n_r;
-        for (int r = 0; r < n_r; ++r) {
-            const uint16_t id = w[r];
+    // Write each row's ids and queue the row-rounds left open.
+    bool valid;
+    const int64_t row = row_of(h, valid);
+    const uint16_t* w = win + (h * 32 + n) * nrb;
+    if constexpr (MODE == kScreen) {
+        // Gather the block's open rows per round in LDS (the stage buffers
+        // are free now), then reserve room in this block's segment with one
+        // atomic per round and copy them out.
+        int* lq = reinterpret_cast<int*>(smem);            // [nrb][WAVES * 64]
+        int* lcnt = lq + nrb * WAVES * kWaveRows;          // [nrb]
+        int* lbase = lcnt + nrb;                           // [nrb]
+        if (tid < nrb) lcnt[tid] = 0;
+        __syncthreads();
+        for (int rr = 0; rr < nrb; ++rr) {
+            const uint16_t id = w[rr];
             const bool queue = valid && id == kUnsettled;
-            if (valid) out[r] = id == kUnsettled ? 0 : (int32_t)id;
-            // wave-aggregated append to this round's refinement list
+            if (valid) buckets[row * n_r + r_lo + rr] = id == kUnsettled ? 0 : (int32_t)id;
             const uint64_t qmask = __ballot(queue);
             if (qmask) {
-                int* list = refine_lists + rows * r;
                 const int leader = __ffsll((unsigned long long)qmask) - 1;
-                int slot0 = 0;
-                if (lane == leader) slot0 = atomicAdd(&refine_counts[r], __popcll(qmask));
-                slot0 = __shfl(slot0, leader);
-                if (queue) list[slot0 + __popcll(qmask & ((1ull << lane) - 1ull))] = (int)row;
+                int lslot = 0;
+                if (lane == leader) lslot = atomicAdd(&lcnt[rr], __popcll(qmask));
+                lslot = __shfl(lslot, leader);
+                if (queue) lq[rr * WAVES * kWaveRows + lslot + __popcll(qmask & ((1ull << lane) - 1ull))] = (int)row;
             }
         }
+        __syncthreads();
+        const int64_t seg = blockIdx.x % kSegs;
+        if (tid < nrb) lbase[tid] = lcnt[tid] > 0 ? atomicAdd(&count_out[(int64_t)(r_lo + tid) * kSegs + seg], lcnt[tid]) : 0;
+        __syncthreads();
+        for (int rr = 0; rr < nrb; ++rr) {
+            int* dst = list_out + ((int64_t)(r_lo + rr) * kSegs + seg) * seg_cap + lbase[rr];
+            for (int i = tid; i < lcnt[rr]; i += WAVES * 64) dst[i] = lq[rr * WAVES * kWaveRows + i];
+        }
+    } else {
+        for (int rr = 0; rr < nrb; ++rr) {
+            const int r = r_lo + rr;
+            const uint16_t id = w[rr];
+            const bool queue = valid && id == kUnsettled;
+            if (valid) buckets[row * n_r + r] = id == kUnsettled ? 0 : (int32_t)id;
+            // wave-aggregated append to this round's list
+            const uint64_t qmask = __ballot(queue);
+            if (qmask) {
+                int* list = list_out + rows * r;
+                const int leader = __ffsll((unsigned long long)qmask) - 1;
+                int lslot = 0;
+                if (lane == leader) lslot = atomicAdd(&count_out[r], __popcll(qmask));
+                lslot = __shfl(lslot, leader);
+                if (queue) list[lslot + __popcll(qmask & ((1ull << lane) - 1ull))] = (int)row;
+            }
+        }
+    }
+    if (MODE != kListed) break;
+    __syncthreads();  // the next chunk restages R over the buffers just read
     }
 }
 
 struct HashWs {
     uint16_t* r_hi;
     uint16_t* r_mid;
-    float* col_norm;
-    float* col_norm_max;
-    int* count;
-    int* list;
+    float* col_norm;  // [3][n_r][half_pad]: |R_c|, |R_c - hi_c|, |R_c - hi_c - mid_c|
+    float* norm_max;  // [3][n_r]: the largest of each
+    int* count;       // [n_r][kSegs] rows left open by the screen, then [n_r] by the exact passes
+    int* list1;       // [n_r][kSegs][seg_cap]
+    int* list2;       // [n_r][rows]
+    int64_t seg_cap;
     size_t bytes;
 };
 
+constexpr int kHashWaves = 8;
+constexpr int64_t kRowsPerBlock = kHashWaves * 64;
+
 HashWs carve(void* base, int64_t rows, int n_rounds, int half_pad) {
     const size_t per = (size_t)n_rounds * half_pad * kHeadDim;
+    const int64_t blocks = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
     char* p = static_cast<char*>(base);
     HashWs w{};
+    w.seg_cap = (blocks + kSegs - 1) / kSegs * kRowsPerBlock;
     size_t off = 0;
     w.r_hi = reinterpret_cast<uint16_t*>(p + off);
     off += align256(per * 2);
     w.r_mid = reinterpret_cast<uint16_t*>(p + off);
     off += align256(per * 2);
     w.col_norm = reinterpret_cast<float*>(p + off);
-    off += align256((size_t)n_rounds * half_pad * 4);
-    w.col_norm_max = reinterpret_cast<float*>(p + off);
-    off += align256((size_t)n_rounds * 4);
+    off += align256((size_t)3 * n_rounds * half_pad * 4);
+    w.norm_max = reinterpret_cast<float*>(p + off);
+    off += align256((size_t)3 * n_rounds * 4);
     w.count = reinterpret_cast<int*>(p + off);
-    off += align256((size_t)n_rounds * 4);
-    w.list = reinterpret_cast<int*>(p + off);
-    off += align256((size_t)rows * n_rounds * 4);
+    off += align256((size_t)n_rounds * (kSegs + 1) * 4);
+    w.list1 = reinterpret_cast<int*>(p + off);
+    off += align256((size_t)n_rounds * kSegs * w.seg_cap * 4);
+    w.list2 = reinterpret_cast<int*>(p + off);
+    off += align256((size_t)n_rounds * rows * 4);
     w.bytes = off;
     return w;
 }
@@ -753,49 +826,69 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
     const int half = n_buckets / 2;
     const int half_pad = (half + 31) / 32 * 32;
     const HashWs w = carve(workspace, rows, n_rounds, half_pad);
+    const float* cn_max = w.norm_max;                       // max |R_c|
+    const float* res1_max = w.norm_max + n_rounds;          // max |R_c - hi_c|
+    const float* res2_max = w.norm_max + 2 * n_rounds;      // max |R_c - hi_c - mid_c|
+    int* count1 = w.count;                                  // [n_r][kSegs]: left open by the screen
+    int* count2 = w.count + (size_t)n_rounds * kSegs;       // [n_r]: left to the fp64 refinement
 
     prep_r_cols_kernel<<<dim3(half_pad, n_rounds), 64, 0, stream>>>(R, half, half_pad, w.r_hi,
                                                                      w.r_mid, w.col_norm);
-    prep_r_max_kernel<<<n_rounds, 256, 0, stream>>>(w.col_norm, half_pad, w.col_norm_max, w.count);
+    prep_r_max_kernel<<<dim3(n_rounds, 3), 256, 0, stream>>>(w.col_norm, n_rounds, half_pad, w.norm_max,
+                                                             w.count, n_rounds * (kSegs + 1));
     if (rows == 0) return hipGetLastError();
 
-    // Error bound of a screened key against the exact |projection| p_c:
-    //  * the dropped bf16 plane(s), <= 2^-16 sum_t |q_t R_tc| each;
+    // Error of a screened key against the exact |projection| p_c, beyond the
+    // planes' residual q . (R_c - planes) <= |q| |R_c - planes|:
     //  * fp32 accumulation of the exact bf16 products, <= one ulp of the
     //    partial sum (<= 2^-23 sum_t |q_t R_tc|) per addition;
+    //  * for fp32 input, q's own residual after two bf16 planes and R's
+    //    after two (<= 3.1 * 2^-16 sum_t |q_t R_tc| together);
     //  * the 4 index bits written over the low mantissa, < 2^-19 |key|.
     // sum_t |q_t R_tc| <= |q| |R_c| (Cauchy-Schwarz) <= |q| max_c |R_c|.
-    const double adds = f32 ? 3 * kHeadDim : 2 * kHeadDim;
-    const double resid = f32 ? 3.1 * 0x1p-16 : 0x1p-16;
-    const float err_sum = (float)((resid + adds * 0x1p-23) * 1.01);
     const float err_pack = (float)0x1p-19;
+    const float acc1 = (float)(kHeadDim * 0x1p-23 * 1.01);
+    const float acc2 = (float)(2 * kHeadDim * 0x1p-23 * 1.01);
+    const float acc_f32 = (float)((3.1 * 0x1p-16 + 3 * kHeadDim * 0x1p-23) * 1.01);
 
-    constexpr int kWaves = 8, kPairsBf16 = 1, kPairsF32 = 1;
-    const int64_t rows_per_block = kWaves * 64 * (f32 ? kPairsF32 : kPairsBf16);
-    const unsigned grid = (unsigned)((rows + rows_per_block - 1) / rows_per_block);
-
+    constexpr int kWaves = kHashWaves;
+    const unsigned grid = (unsigned)((rows + kRowsPerBlock - 1) / kRowsPerBlock);
     // Refinement blocks per round: a typical list holds well under 1% of the
     // rows, a few groups of 64 per round; longer lists are strided.
     const unsigned refine_blocks =
         (unsigned)std::max<int64_t>(1, std::min<int64_t>(256, (rows + kRefineGroup - 1) / kRefineGroup));
+    auto lds_for = [&](int rounds) { return kStageBytes + (size_t)kRowsPerBlock * rounds * 2; };
     if (f32) {
-        const size_t lds = kStageBytes + (size_t)rows_per_block * n_rounds * 2;
-        hipFuncSetAttribute(reinterpret_cast<const void*>(&hash_kernel<true, kWaves, kPairsF32>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        hash_kernel<true, kWaves, kPairsF32><<<grid, kWaves * 64, lds, stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi,
-                                                     w.r_mid, w.col_norm_max, err_sum,
-                                                     err_pack, buckets, w.list, w.count);
+        auto* k = &hash_kernel<true, kExact, kWaves>;
+        hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds_for(n_rounds));
+        k<<<grid, kWaves * 64, lds_for(n_rounds), stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi, w.r_mid,
+                                                           cn_max, nullptr, acc_f32, err_pack, buckets,
+                                                           nullptr, nullptr, w.list2, count2, 0);
         hash_refine_kernel<true><<<dim3(refine_blocks, n_rounds), kRefineThreads, 0, stream>>>(
-            q, R, half, n_rounds, rows, w.list, w.count, w.col_norm_max, buckets);
+            q, R, half, n_rounds, rows, w.list2, count2, cn_max, buckets);
     } else {
-        const size_t lds = kStageBytes + (size_t)rows_per_block * n_rounds * 2;
-        hipFuncSetAttribute(reinterpret_cast<const void*>(&hash_kernel<false, kWaves, kPairsBf16>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        hash_kernel<false, kWaves, kPairsBf16><<<grid, kWaves * 64, lds, stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi,
-                                                      w.r_mid, w.col_norm_max, err_sum,
-                                                      err_pack, buckets, w.list, w.count);
+        // screen with R's hi plane; the rows it leaves open get both planes;
+        // what those leave open gets the fp64 refinement
+        auto* ks = &hash_kernel<false, kScreen, kWaves>;
+        hipFuncSetAttribute(reinterpret_cast<const void*>(ks), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds_for(n_rounds));
+        ks<<<grid, kWaves * 64, lds_for(n_rounds), stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi,
+                                                            w.r_mid, cn_max, res1_max, acc1, err_pack,
+                                                            buckets, nullptr, nullptr, w.list1, count1,
+                                                            w.seg_cap);
+        auto* kl = &hash_kernel<false, kListed, kWaves>;
+        hipFuncSetAttribute(reinterpret_cast<const void*>(kl), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds_for(1));
+        // five workgroups per segment cover the 5 * 512 rows a segment of 32
+        // screen workgroups holds at a 15.6% open rate (Gaussian data leaves
+        // about 12% open); longer segments loop
+        const unsigned per_seg = (unsigned)std::min<int64_t>(5, w.seg_cap / kRowsPerBlock);
+        kl<<<dim3(per_seg, kSegs, n_rounds), kWaves * 64, lds_for(1), stream>>>(
+            q, rows, n_rounds, half, half_pad, w.r_hi, w.r_mid, cn_max, res2_max, acc2, err_pack, buckets,
+            w.list1, count1, w.list2, count2, w.seg_cap);
         hash_refine_kernel<false><<<dim3(refine_blocks, n_rounds), kRefineThreads, 0, stream>>>(
-            q, R, half, n_rounds, rows, w.list, w.count, w.col_norm_max, buckets);
+            q, R, half, n_rounds, rows, w.list2, count2, cn_max, buckets);
     }
     return hipGetLastError();
 }
