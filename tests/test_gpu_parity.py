@@ -257,3 +257,38 @@ def test_combine_round_counts(gpu, dtype, n_rounds):
     err = np.abs(out.float().cpu().numpy() - ref_out).max()
     assert err <= out_tolerance(dtype), f"combine max-abs error {err}"
     assert lse_close(lse.cpu().numpy(), ref_lse, dtype).all()
+
+
+def test_hash_listed_pass_many_open_rows(gpu):
+    """Round 0's queries are built as near-ties between two columns of R, so
+    the hi-plane screen leaves nearly every row of that round open: each
+    segment of the list then holds more rows than its workgroups take in one
+    pass and they loop over its chunks.  Round 1 is ordinary.  262144 rows;
+    4096 of them, drawn at random, are checked against the oracle bit for
+    bit."""
+    B, H, L, n_b, n_r, d = 1, 4, 65536, 1024, 2, 64
+    half = n_b // 2
+    rng = np.random.default_rng(4242)
+    R = rng.standard_normal((n_r, d, half)).astype(np.float32)
+    rows = B * H * L
+    a = rng.integers(0, half, rows)
+    b = (a + 1 + rng.integers(0, half - 1, rows)) % half
+    Ra, Rb = R[0][:, a].T.astype(np.float64), R[0][:, b].T.astype(np.float64)  # [rows, d]
+    gaa, gbb, gab = (Ra * Ra).sum(1), (Rb * Rb).sum(1), (Ra * Rb).sum(1)
+    # q = alpha R_a + beta R_b with q.R_a = 1 and q.R_b = 1 - 1e-4
+    det = gaa * gbb - gab * gab
+    ta, tb = np.ones(rows), np.full(rows, 1 - 1e-4)
+    alpha, beta = (gbb * ta - gab * tb) / det, (gaa * tb - gab * ta) / det
+    q32 = (alpha[:, None] * Ra + beta[:, None] * Rb).astype(np.float32)
+    q_bf = torch.from_numpy(q32).to(torch.bfloat16).reshape(B, H, L, d)
+    cfg = lsh.Config(B=B, H=H, L=L, n_buckets=n_b, n_rounds=n_r)
+    log("hash-listed-loop", rows)
+    got = lsh.lsh_hash(cfg, q_bf.cuda(), torch.from_numpy(R).cuda()).cpu().numpy().reshape(rows, n_r)
+    pick = np.sort(rng.choice(rows, 4096, replace=False))
+    q64 = q_bf.float().numpy().astype(np.float64).reshape(rows, d)[pick].reshape(1, 1, -1, d)
+    want, near = oracle.lsh_hash(q64, R.astype(np.float64))
+    want = want.reshape(-1, n_r)
+    top2 = np.isin(want[:, 0] % half, np.stack([a[pick], b[pick]], 1)).mean()
+    print(f"round 0 winner among the two built columns: {top2:.3f}; near-ties {int(near.sum())}")
+    assert top2 > 0.9  # the construction does what it is meant to
+    assert np.array_equal(got[pick], want)
