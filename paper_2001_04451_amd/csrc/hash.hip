@@ -491,6 +491,47 @@ __device__ __forceinline__ void load_stage(char* smem, int buf, int g, int spr, 
     }
 }
 
+// Copy round r's whole mid plane (up to 512 columns) into the mid-plane
+// halves of the two stage buffers, which the one-plane screen leaves free:
+// column c at buffer c / 256, slot c % 256, with the stage layout.  The
+// screen reads its winners' mid pieces from there.
+template <int WAVES>
+__device__ __forceinline__ void load_round_mid(char* smem, int r, int half_pad,
+                                               const uint16_t* __restrict__ r_mid, int wave, int lane) {
+    constexpr int kRuns = 2 * kStageCols / 8;  // 1 KB runs of 8 columns
+    static_assert(kRuns % WAVES == 0, "runs split evenly over the waves");
+    const int cl_lane = lane >> 3, slot = lane & 7;
+#pragma unroll
+    for (int i = 0; i < kRuns / WAVES; ++i) {
+        const int run = wave * (kRuns / WAVES) + i;
+        const int c0 = run * 8, c = c0 + cl_lane;  // column of the round
+        const int gcol = c < half_pad ? c : 0;     // past the round: any valid address, never read
+        const int sc = c % kStageCols;
+        const uint16_t* src = r_mid + ((size_t)r * half_pad + gcol) * kHeadDim + (slot ^ stage_swz(sc)) * 8;
+        __builtin_amdgcn_global_load_lds(
+            (const __attribute__((address_space(1))) void*)src,
+            (__attribute__((address_space(3))) void*)(smem + stage_offset(c0 / kStageCols, 1, c0 % kStageCols)),
+            16, 0, 0);
+    }
+}
+
+// This lane half's 32 k-values of q . R_col for one plane: 16 bf16 pair
+// products in four short chains (fp32 sums of exact products).
+__device__ __forceinline__ float dot_planes(const bf16x8 (&qa4)[4], const u32x4 (&rv)[4]) {
+    float part[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) {
+        const u32x4 qv = __builtin_bit_cast(u32x4, qa4[s4]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t qw = qv[e], rw = rv[s4][e];
+            part[e] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, qw), __builtin_bit_cast(bf16x2, rw),
+                                                      part[e], false);
+        }
+    }
+    return (part[0] + part[1]) + (part[2] + part[3]);
+}
+
 // Winner of a row-round as kept in LDS until the row's ids are written:
 // the bucket id, or kUnsettled when a later pass must decide.
 constexpr uint16_t kUnsettled = 0xFFFFu;
@@ -500,12 +541,16 @@ constexpr uint16_t kUnsettled = 0xFFFFu;
 //  * kScreen and kExact take rows blockIdx.x * 64 * WAVES + ... and all
 //    rounds; kListed takes, for round blockIdx.z, the rows at chunk
 //    blockIdx.x of the screen's segment blockIdx.y of that round.
-//  * A row-round is settled when the gap between the best and second-best
-//    key exceeds twice the error bound
-//        eps = |q| * (res_max[r] + err_acc * max_c |R_c|) + err_pack * key
-//    (res_max: largest 2-norm of R's columns less the planes used, none
-//    for fp32 input, whose planes' residual is inside err_acc); its id goes
-//    to buckets.  Otherwise the row is appended to the round's list: the
+//  * Every screened projection is within
+//        eps = |q| * (res_max[r] + err_acc * max_c |R_c|)
+//    of the exact one (res_max: largest 2-norm of R's columns less the
+//    planes used, none for fp32 input, whose planes' residual is inside
+//    err_acc), and a key's magnitude is low by at most err_pack of it.  For
+//    bf16 input the best key's column is then recomputed over both planes
+//    (within eps2, from res_max2 and err_acc2), and the row-round is settled
+//    when that value's magnitude less eps2 exceeds the second key plus eps;
+//    for fp32 input when the best and second keys are more than 2 eps apart.
+//    A settled id goes to buckets.  Otherwise the row is appended to the round's list: the
 //    screen's lists are segmented, [round][kSegs][seg_cap] with counts
 //    [round][kSegs]; the exact passes' are [round][rows] with one count per
 //    round (few rows reach them).
@@ -514,7 +559,8 @@ __global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
     const void* __restrict__ q, int64_t rows, int n_r, int half, int half_pad,
     const uint16_t* __restrict__ r_hi, const uint16_t* __restrict__ r_mid,
     const float* __restrict__ col_norm_max, const float* __restrict__ res_max, float err_acc,
-    float err_pack, int32_t* __restrict__ buckets, const int* __restrict__ list_in,
+    const float* __restrict__ res_max2, float err_acc2, float err_pack, int32_t* __restrict__ buckets,
+    const int* __restrict__ list_in,
     const int* __restrict__ count_in, int* __restrict__ list_out, int* __restrict__ count_out,
     int64_t seg_cap) {
     static_assert(!F32 || MODE == kExact, "fp32 input takes the exact pass only");
@@ -625,6 +671,8 @@ __global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
         // the next stage lands in the other buffer while this one computes
         if (g + 1 < g_end)
             load_stage<WAVES, NP>(smem, buf ^ 1, g + 1, spr, half_pad, r_hi, r_mid, wave, lane);
+        if constexpr (MODE == kScreen)
+            if (st == 0) load_round_mid<WAVES>(smem, r, half_pad, r_mid, wave, lane);
         const char* hi_base = smem + stage_offset(buf, 0, 0);
         const char* mid_base = smem + stage_offset(buf, 1, 0);
         const int nt = min(kStageTiles, tpr - st * kStageTiles);
@@ -653,63 +701,84 @@ __global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
         }
 
         if (st == spr - 1) {
+            if constexpr (MODE == kScreen) {
+                if (spr == 1) {  // this stage's mid-plane copies: landed and seen by every wave
+                    __builtin_amdgcn_s_waitcnt(0);
+                    __syncthreads();
+                }
+            }
             // Round epilogue: merge the two lane halves (different columns of
             // the same row) and decide; lane half h keeps row block h's result.
             const float cn = col_norm_max[r];
             const float res = F32 ? 0.f : res_max[r];
+            uint32_t bk[kRB], sk[kRB];
+            int col[kRB];
 #pragma unroll
             for (int rb = 0; rb < kRB; ++rb) {
                 const uint32_t bb = best[rb], ss2 = second[rb];
                 const uint32_t bp = __shfl_xor(bb, 32), sp = __shfl_xor(ss2, 32);
                 const int tp = __shfl_xor(best_tile[rb], 32);
                 const bool mine = bb > bp || (bb == bp && h == 0);
-                const uint32_t bk = mine ? bb : bp;
-                const uint32_t sk = max(min(bb, bp), max(ss2, sp));
-                const float b1 = key_magnitude<F32>(bk);
-                const float s1 = key_magnitude<F32>(sk);
+                bk[rb] = mine ? bb : bp;
+                sk[rb] = max(min(bb, bp), max(ss2, sp));
                 const int hw = mine ? h : (h ^ 1);
                 const int tw = mine ? best_tile[rb] : tp;
-                const uint32_t j = key_index<F32>(bk);
-                const int col = tw * 32 + 8 * (int)(j >> 2) + 4 * hw + (int)(j & 3u);
+                const uint32_t j = key_index<F32>(bk[rb]);
+                col[rb] = tw * 32 + 8 * (int)(j >> 2) + 4 * hw + (int)(j & 3u);
+            }
+            if constexpr (F32) {
                 // Every screened key is within eps of its exact |projection|;
                 // an exchange of winners needs a gap <= 2 eps.  When the gap is
-                // larger the winner's magnitude exceeds eps, so the sign of any
-                // value within eps of its projection is the exact one.
-                const float thr = 2.04f * (qn[rb] * (res + err_acc * cn) + err_pack * b1);
-                const bool flag = !(b1 - s1 > thr) || col >= half;
-                bool negative;
-                if constexpr (F32) {
-                    negative = (bk & 1u) != 0;
-                } else {
-                    // q_row . R_col over the planes the pass used (the same
-                    // products as the screen, fp32 sums): each lane half adds its
-                    // 32 k-values.  A flagged winner may sit past the round; any
-                    // valid column stands in, its sign unused.
-                    const int colc = min(col, half_pad - 1);
-                    const size_t o = ((size_t)r * half_pad + colc) * kHeadDim + 32 * h;
+                // larger the winner's magnitude exceeds eps, so the screened
+                // sign (bit 0 of the key) is the exact one.
+#pragma unroll
+                for (int rb = 0; rb < kRB; ++rb) {
+                    const float b1 = key_magnitude<F32>(bk[rb]), s1 = key_magnitude<F32>(sk[rb]);
+                    const float thr = 2.04f * (qn[rb] * (res + err_acc * cn) + err_pack * b1);
+                    const bool flag = !(b1 - s1 > thr) || col[rb] >= half;
+                    const int id = (bk[rb] & 1u) ? half + col[rb] : col[rb];
+                    if (rb == h) win[(rb * 32 + n) * nrb + (r - r_lo)] = flag ? kUnsettled : (uint16_t)id;
+                }
+            } else {
+                // x = q_row . R_col of the best key's column over both planes
+                // (fp32 sums of the exact products; each lane half adds its 32
+                // k-values), within eps2 of the exact projection.  Every other
+                // column's exact |projection| is at most the second key (raised
+                // by the truncated bits) plus the pass's eps, so the winner is
+                // certain when |x| - eps2 exceeds that, and its sign is x's.  A
+                // flagged winner may sit past the round; any valid column
+                // stands in.  The hi pieces come from global memory (the lines
+                // were staged moments ago), the screen's mid pieces from LDS.
+                u32x4 hv[kRB][4], mv[kRB][4];
+#pragma unroll
+                for (int rb = 0; rb < kRB; ++rb) {
+                    const int cc = min(col[rb], half_pad - 1);
+                    const size_t o = ((size_t)r * half_pad + cc) * kHeadDim + 32 * h;
                     const u32x4* ph = reinterpret_cast<const u32x4*>(r_hi + o);
                     const u32x4* pm = reinterpret_cast<const u32x4*>(r_mid + o);
-                    float part = 0.f;
 #pragma unroll
                     for (int s4 = 0; s4 < 4; ++s4) {
-                        const u32x4 qv = __builtin_bit_cast(u32x4, qa[rb][s4]);
-                        const u32x4 hv = ph[s4];
-                        u32x4 mv = {0u, 0u, 0u, 0u};
-                        if constexpr (NP == 2) mv = pm[s4];
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const uint32_t qw = qv[e], hw2 = hv[e], mw = mv[e];
-                            part = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, qw),
-                                                                   __builtin_bit_cast(bf16x2, hw2), part, false);
-                            if constexpr (NP == 2)
-                                part = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, qw),
-                                                                       __builtin_bit_cast(bf16x2, mw), part, false);
+                        hv[rb][s4] = ph[s4];
+                        if constexpr (MODE == kScreen) {
+                            const int sc = cc % kStageCols;
+                            mv[rb][s4] = *reinterpret_cast<const u32x4*>(
+                                smem + stage_offset(cc / kStageCols, 1, sc) + (((4 * h + s4) ^ stage_swz(sc)) << 4));
+                        } else {
+                            mv[rb][s4] = pm[s4];
                         }
                     }
-                    negative = part + __shfl_xor(part, 32) < 0.f;
                 }
-                const int id = negative ? half + col : col;
-                if (rb == h) win[(rb * 32 + n) * nrb + (r - r_lo)] = flag ? kUnsettled : (uint16_t)id;
+#pragma unroll
+                for (int rb = 0; rb < kRB; ++rb) {
+                    const float half_x = dot_planes(qa[rb], hv[rb]) + dot_planes(qa[rb], mv[rb]);
+                    const float x = half_x + __shfl_xor(half_x, 32);
+                    const float s1 = key_magnitude<F32>(sk[rb]);
+                    const float eps = 1.02f * qn[rb] * (res + err_acc * cn);
+                    const float eps2 = 1.02f * qn[rb] * (res_max2[r] + err_acc2 * cn);
+                    const bool flag = !(fabsf(x) - eps2 > s1 * (1.f + 2.f * err_pack) + eps) || col[rb] >= half;
+                    const int id = x < 0.f ? half + col[rb] : col[rb];
+                    if (rb == h) win[(rb * 32 + n) * nrb + (r - r_lo)] = flag ? kUnsettled : (uint16_t)id;
+                }
             }
         }
         // the next stage has landed and every wave is done with this buffer
@@ -863,7 +932,7 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
         hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)lds_for(n_rounds));
         k<<<grid, kWaves * 64, lds_for(n_rounds), stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi, w.r_mid,
-                                                           cn_max, nullptr, acc_f32, err_pack, buckets,
+                                                           cn_max, nullptr, acc_f32, nullptr, 0.f, err_pack, buckets,
                                                            nullptr, nullptr, w.list2, count2, 0);
         hash_refine_kernel<true><<<dim3(refine_blocks, n_rounds), kRefineThreads, 0, stream>>>(
             q, R, half, n_rounds, rows, w.list2, count2, cn_max, buckets);
@@ -874,8 +943,8 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
         hipFuncSetAttribute(reinterpret_cast<const void*>(ks), hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)lds_for(n_rounds));
         ks<<<grid, kWaves * 64, lds_for(n_rounds), stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi,
-                                                            w.r_mid, cn_max, res1_max, acc1, err_pack,
-                                                            buckets, nullptr, nullptr, w.list1, count1,
+                                                            w.r_mid, cn_max, res1_max, acc1, res2_max, acc2,
+                                                            err_pack, buckets, nullptr, nullptr, w.list1, count1,
                                                             w.seg_cap);
         auto* kl = &hash_kernel<false, kListed, kWaves>;
         hipFuncSetAttribute(reinterpret_cast<const void*>(kl), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -885,7 +954,7 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
         // about 12% open); longer segments loop
         const unsigned per_seg = (unsigned)std::min<int64_t>(5, w.seg_cap / kRowsPerBlock);
         kl<<<dim3(per_seg, kSegs, n_rounds), kWaves * 64, lds_for(1), stream>>>(
-            q, rows, n_rounds, half, half_pad, w.r_hi, w.r_mid, cn_max, res2_max, acc2, err_pack, buckets,
+            q, rows, n_rounds, half, half_pad, w.r_hi, w.r_mid, cn_max, res2_max, acc2, res2_max, acc2, err_pack, buckets,
             w.list1, count1, w.list2, count2, w.seg_cap);
         hash_refine_kernel<false><<<dim3(refine_blocks, n_rounds), kRefineThreads, 0, stream>>>(
             q, R, half, n_rounds, rows, w.list2, count2, cn_max, buckets);
