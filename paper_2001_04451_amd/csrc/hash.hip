@@ -949,10 +949,10 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
         auto* kl = &hash_kernel<false, kListed, kWaves>;
         hipFuncSetAttribute(reinterpret_cast<const void*>(kl), hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)lds_for(1));
-        // five workgroups per segment cover the 5 * 512 rows a segment of 32
-        // screen workgroups holds at a 15.6% open rate (Gaussian data leaves
-        // about 12% open); longer segments loop
-        const unsigned per_seg = (unsigned)std::min<int64_t>(5, w.seg_cap / kRowsPerBlock);
+        // three workgroups per segment cover the 3 * 512 rows a segment of 32
+        // screen workgroups holds at a 9.4% open rate (Gaussian data leaves
+        // about 6.3% open); longer segments loop
+        const unsigned per_seg = (unsigned)std::min<int64_t>(3, w.seg_cap / kRowsPerBlock);
         kl<<<dim3(per_seg, kSegs, n_rounds), kWaves * 64, lds_for(1), stream>>>(
             q, rows, n_rounds, half, half_pad, w.r_hi, w.r_mid, cn_max, res2_max, acc2, res2_max, acc2, err_pack, buckets,
             w.list1, count1, w.list2, count2, w.seg_cap);
