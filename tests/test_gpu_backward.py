@@ -29,6 +29,11 @@ CASES = {
                        backward=True),
     # eight rounds (four signature words), causal, clustered
     "eight_rounds": small("long_bf16_L65536", H=1, L=4096, n_buckets=256, backward=True),
+    # an odd round count: a half-filled signature word, non-causal
+    "three_rounds": small("mixture_bf16_L4096", B=1, H=1, L=2048, n_rounds=3, backward=True),
+    # the most rounds the library takes (eight signature words), causal
+    "sixteen_rounds": small("long_bf16_L65536", H=1, L=2048, n_buckets=256, n_rounds=16,
+                            backward=True),
 }
 
 

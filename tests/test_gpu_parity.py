@@ -292,3 +292,26 @@ def test_hash_listed_pass_many_open_rows(gpu):
     print(f"round 0 winner among the two built columns: {top2:.3f}; near-ties {int(near.sum())}")
     assert top2 > 0.9  # the construction does what it is meant to
     assert np.array_equal(got[pick], want)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("n_rounds", [3, 6, 11, 16])
+def test_forward_round_counts(gpu, n_rounds, causal):
+    """The whole forward for round counts the five workloads do not use: an
+    odd count (a half-filled signature word), and 6, 11 and 16 rounds (3, 6
+    and 8 signature words, two rounds per lane in the combine above 8).
+    Mixture inputs, so buckets are uneven and N_ij often exceeds 1."""
+    w = small("mixture_bf16_L4096", B=1, H=2, L=2048, n_rounds=n_rounds, causal=causal)
+    x, q64, v64 = _inputs(w)
+    ref = oracle.lsh_attention_fwd(q64, v64, x["R"].astype(np.float64), w.chunk, w.causal)
+    cfg = lsh.Config.of(w)
+    log("forward-rounds", n_rounds, causal, w)
+    st = lsh.lsh_attention_fwd(cfg, to_device(x["q"], w.dtype), to_device(x["v"], w.dtype),
+                               to_device(x["R"], "f32"))
+    torch.cuda.synchronize()
+    assert np.array_equal(st.buckets.cpu().numpy(), ref["buckets"])
+    assert np.array_equal(st.perm.cpu().numpy(), ref["perm"])
+    err = np.abs(st.out.float().cpu().numpy() - ref["out"]).max()
+    print(f"n_r={n_rounds} causal={causal}: max-abs err {err:.3e}")
+    assert err <= out_tolerance(w.dtype)
+    assert lse_close(st.lse.cpu().numpy(), ref["lse"], w.dtype).all()
