@@ -32,6 +32,9 @@
  *     self -> self_mask (1e5); otherwise log N_ij; N_ij counts the rounds in
  *     which j shares i's bucket, whether or not j falls in i's window;
  *   - the window has no wrap-around: chunk 0 looks back at nothing;
+ *   - when m does not divide L the last chunk holds the L mod m remaining
+ *     slots (as if the sequence were padded with tokens that are no one's
+ *     target);
  *   - a zero query gives k = 0.
  */
 #include <math.h>
@@ -210,7 +213,7 @@ int lsh_ref_chunk_attn_fwd(int64_t BH, int64_t L, int64_t d, int64_t n_rounds,
                            double *o_rounds, double *lse_rounds)
 {
     if (BH < 0 || L < 0 || d < 1 || n_rounds < 1 || chunk < 1 ||
-        (L % chunk) != 0 || !q || !v || !buckets || !perm || !o_rounds ||
+        !q || !v || !buckets || !perm || !o_rounds ||
         !lse_rounds)
         return REF_ERR_INVALID;
     double *norm = (double *)malloc((size_t)(BH * L > 0 ? BH * L : 1) * sizeof(double));
@@ -236,7 +239,7 @@ int lsh_ref_chunk_attn_fwd(int64_t BH, int64_t L, int64_t d, int64_t n_rounds,
             const int64_t i = p[s];
             const int64_t c = s / chunk;
             const int64_t t_lo = (c - 1) * chunk < 0 ? 0 : (c - 1) * chunk;
-            const int64_t t_hi = (c + 1) * chunk;
+            const int64_t t_hi = (c + 1) * chunk < L ? (c + 1) * chunk : L;
             const double *qi = q + (base + i) * d;
             int64_t n = 0;
             double amax = -INFINITY;
@@ -330,7 +333,7 @@ int lsh_ref_chunk_attn_bwd(int64_t BH, int64_t L, int64_t d, int64_t n_rounds,
                            const int32_t *perm, double *dq, double *dv)
 {
     if (BH < 0 || L < 0 || d < 1 || n_rounds < 1 || chunk < 1 ||
-        (L % chunk) != 0 || !q || !v || !out || !dout || !lse_total ||
+        !q || !v || !out || !dout || !lse_total ||
         !buckets || !perm || !dq || !dv)
         return REF_ERR_INVALID;
     int err = 0;
@@ -359,7 +362,7 @@ int lsh_ref_chunk_attn_bwd(int64_t BH, int64_t L, int64_t d, int64_t n_rounds,
                 const int64_t i = p[s];
                 const int64_t c = s / chunk;
                 const int64_t t_lo = (c - 1) * chunk < 0 ? 0 : (c - 1) * chunk;
-                const int64_t t_hi = (c + 1) * chunk;
+                const int64_t t_hi = (c + 1) * chunk < L ? (c + 1) * chunk : L;
                 const double *qi = q + (base + i) * d;
                 const double *dOi = dout + (base + i) * d;
                 const double Di = dot(dOi, out + (base + i) * d, d);

@@ -303,10 +303,13 @@ def test_duplicated_rounds(oracle_lib, causal):
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("L,m,n_b,n_r,clustered", [(128, 16, 4, 2, False), (256, 32, 8, 3, True),
-                                                  (192, 64, 2, 1, False), (256, 16, 16, 4, True)])
+                                                  (192, 64, 2, 1, False), (256, 16, 16, 4, True),
+                                                  (100, 16, 4, 2, True), (203, 32, 4, 3, False)])
 def test_dense_windowed(oracle_lib, causal, L, m, n_b, n_r, clustered):
     """Buckets overflow past m here (few buckets, clustered inputs), so keys
-    outside the window are really dropped."""
+    outside the window are really dropped.  In the last two cases m does not
+    divide L: the dense form's chunk of a slot is floor(slot / m) with no
+    padding, so its last chunk is the partial one."""
     rng = _rng(L + m + n_b + n_r + causal)
     d = 16
     if clustered:
@@ -397,10 +400,12 @@ def torch_dense_loss(q, v, dout, buckets, chunk, causal, scale, self_mask=1e5):
 
 
 @pytest.mark.parametrize("causal", [False, True])
-@pytest.mark.parametrize("n_r,n_b,m", [(1, 4, 16), (3, 8, 16), (4, 4, 32)])
-def test_backward_autograd(oracle_lib, causal, n_r, n_b, m):
-    rng = _rng(31 + n_r + n_b + causal)
-    L, d = 128, 16
+@pytest.mark.parametrize("n_r,n_b,m,L", [(1, 4, 16, 128), (3, 8, 16, 128), (4, 4, 32, 128),
+                                         (3, 8, 32, 113)])
+def test_backward_autograd(oracle_lib, causal, n_r, n_b, m, L):
+    """The last case has a partial last chunk (m does not divide L)."""
+    rng = _rng(31 + n_r + n_b + causal + L)
+    d = 16
     q = rng.standard_normal((L, d))
     v = rng.standard_normal((L, d))
     dout = rng.standard_normal((L, d))
@@ -460,4 +465,4 @@ def test_oracle_rejects_bad_arguments(oracle_lib):
         oracle.lsh_hash(q, np.zeros((1, 8, 0)))  # n_buckets = 0
     with pytest.raises(RuntimeError):
         oracle.lsh_chunk_attn_fwd(q, q, np.zeros((1, 1, 64, 1), np.int32),
-                                  np.zeros((1, 1, 1, 64), np.int32), 48, False)  # L % m != 0
+                                  np.zeros((1, 1, 1, 64), np.int32), 0, False)  # m = 0
