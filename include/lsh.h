@@ -37,7 +37,10 @@
  *   exception crosses this interface.  The library keeps no mutable global
  *   state, so calls on different streams may run concurrently.
  * Supported on the GPU: d = 64, chunk = 64, 2 <= n_buckets <= 1024 (even),
- *   1 <= n_rounds <= 16, L a multiple of the chunk, B*H*L*n_rounds < 2^31.
+ *   1 <= n_rounds <= 16, B*H*L*n_rounds < 2^31.  L need not be a multiple of
+ *   the chunk: the last chunk then holds the L mod m remaining sorted slots
+ *   (the paper is silent; read as padding with tokens that are no one's
+ *   target).
  */
 #ifndef LSH_H
 #define LSH_H
@@ -79,7 +82,7 @@ typedef struct lsh_config {
     int32_t B, H, L, d;
     int32_t n_buckets; /* b: even, >= 2 */
     int32_t n_rounds;  /* number of hash functions, >= 1 */
-    int32_t chunk;     /* m: chunk length in sorted slots; L % m == 0 */
+    int32_t chunk;     /* m: chunk length in sorted slots (the last chunk may be partial) */
     int32_t causal;    /* nonzero: a position never attends to a later one */
     float scale;       /* logit scale, 1/sqrt(d_k) in eq. attn */
     float self_mask;   /* mask value for j == i, 1e5 in App. A */

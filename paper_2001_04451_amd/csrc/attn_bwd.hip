@@ -166,7 +166,7 @@ __global__ __launch_bounds__(256, 2) void bwd_kv_kernel(
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, h = lane >> 5, n = lane & 31;
     const int cw = wave >> 1, kh = wave & 1;
-    if (c0 + cw >= L / kChunk) return;  // no barrier follows
+    if (c0 + cw >= (L + kChunk - 1) / kChunk) return;  // no barrier follows
     const int kr = cw * kChunk + kh * 32 + n;  // this lane's key row
     const int t_key = slot0 + kr;
     const float cf_k = M.cf[kr];
@@ -241,7 +241,9 @@ __global__ __launch_bounds__(256, 2) void bwd_kv_kernel(
             }
         }
     }
-    // lane holds key t_key, d = 32dt + 8i + 4h + e
+    // lane holds key t_key, d = 32dt + 8i + 4h + e; slots past L (a partial
+    // last chunk) have no row
+    if (t_key >= L) return;
     float* dvrow = dv_r + (seg * L + t_key) * kHeadDim;
     float* dkrow = dk_r + (seg * L + t_key) * kHeadDim;
 #pragma unroll
@@ -286,7 +288,7 @@ __global__ __launch_bounds__(256, 2) void bwd_q_kernel(
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, h = lane >> 5, n = lane & 31;
     const int cw = wave >> 1, qh = wave & 1;
     const int c = c0 + cw;
-    if (c >= L / kChunk) return;  // no barrier follows
+    if (c >= (L + kChunk - 1) / kChunk) return;  // no barrier follows
     const int kb = cw * kChunk;                // first key row of the window
     const int rq = kb + kChunk + qh * 32 + n;  // this lane's query row
     const int s_q = slot0 + rq;
@@ -348,6 +350,7 @@ __global__ __launch_bounds__(256, 2) void bwd_q_kernel(
                 dq_acc[dt] = mfma32x32x16(col_operand(Qs, r0, 32 * dt + n), as_bf16x8(dak[ku]), dq_acc[dt]);
         }
     }
+    if (s_q >= L) return;  // a slot past L (a partial last chunk) has no row
     float* dqrow = dq_r + (seg * L + s_q) * kHeadDim;
 #pragma unroll
     for (int dt = 0; dt < 2; ++dt)
@@ -500,7 +503,8 @@ hipError_t launch_attn_bwd(int64_t BH, int L, int n_rounds, int n_buckets, bool 
     const uint16_t* dout = static_cast<const uint16_t*>(dout_);
     const unsigned row_grid = (unsigned)((rows * 16 + 255) / 256);
     bwd_prep_kernel<<<row_grid, 256, 0, stream>>>(out, dout, rows, w.D);
-    const dim3 grid((unsigned)((L / kChunk + 1) / 2), (unsigned)(BH * n_rounds));
+    // a partial last chunk (L not a multiple of the chunk) counts as a chunk
+    const dim3 grid((unsigned)(((L + kChunk - 1) / kChunk + 1) / 2), (unsigned)(BH * n_rounds));
     const int nw = n_rounds == 1 ? 0 : (n_rounds + 1) / 2;
 #define LSH_BWD_CASE(W)                                                                          \
     case W:                                                                                      \

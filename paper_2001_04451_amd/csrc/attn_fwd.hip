@@ -178,7 +178,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
     const int64_t seg = blockIdx.y;
     const int64_t bh = seg / n_r;
     const int r = (int)(seg % n_r);
-    const int n_chunks = L / kChunk;
+    const int n_chunks = (L + kChunk - 1) / kChunk;  // the last may be partial
     const int c0 = blockIdx.x * chunks_per_strip;
     const int c1 = min(n_chunks, c0 + chunks_per_strip);
     const float scale_log2e = scale * kLog2e;
@@ -188,10 +188,12 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
     if (tid <= kMaskedIndex) S.tab[tid] = tid < n_r ? -__log2f((float)(n_r - tid)) : -__builtin_inff();
 
     // Position of row `lane` of chunk cc, as stored (clamped where it is
-    // used); outside the sequence any valid row (those slots are never a
-    // valid key, see lo below).
+    // used); for a slot outside the sequence (before chunk 0, or past L in a
+    // partial last chunk) any valid row: such slots are never a valid key
+    // (see lo and hi below) and their queries store nothing.
     auto chunk_pos = [&](int cc) -> int {
-        return cc >= 0 && cc < n_chunks ? pseg[(int64_t)cc * kChunk + lane] : 0;
+        const int slot = cc * kChunk + lane;
+        return cc >= 0 && slot < L ? pseg[slot] : 0;
     };
     // Gather chunk cc into its ring slot: wave w copies q and v rows
     // 16w .. 16w+15 (each lane the piece that belongs at its LDS slot), and
@@ -288,6 +290,9 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
             const uint64_t after = u < 63 ? bB & (~0ull << (u + 1)) : 0ull;
             hi = (c - 1) * kChunk + (after ? 62 + __ffsll((long long)after) : 127);
         }
+        // No key past the sequence (a partial last chunk).  Chunk c holds at
+        // least one slot below L, so hi stays at or above the chunk's start - 1.
+        hi = min(hi, L - 1);
         // valid keys of this lane's query as a 128-bit window mask (vm[h]:
         // window slots 64h .. 64h+63; lo_w2 <= 127 and hi_w2 >= 63 always),
         // then per lane group the complement shifted so that bit 16(kt%2) + j
@@ -402,7 +407,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
             }
             // z = scale*|q_i| - self_mask when the token is its own only target
             lse_pend = alone ? bound * kLn2 - self_mask : (mref + __log2f(lsum)) * kLn2;
-            row_pend = seg * L + s_q;
+            row_pend = s_q < L ? seg * L + s_q : -1;
         };
         if (fast)
             attend(BoolTag<true>{});
@@ -436,7 +441,7 @@ __global__ __launch_bounds__(64) void attn_fwd_f32_kernel(
     const int slot0 = (c - 1) * kChunk;
     for (int rho = 0; rho < 128; ++rho) {
         const int slot = slot0 + rho;
-        const bool ok = slot >= 0;
+        const bool ok = slot >= 0 && slot < L;
         const int pos = ok ? min(max(perm[seg * L + slot], 0), L - 1) : 0;
         Ks[rho][t] = ok ? q[(bh * L + pos) * kHeadDim + t] : 0.f;
         Vs2[rho][t] = ok ? v[(bh * L + pos) * kHeadDim + t] : 0.f;
@@ -452,6 +457,7 @@ __global__ __launch_bounds__(64) void attn_fwd_f32_kernel(
 
     const int rq = 64 + t;
     const int s_q = c * kChunk + t;
+    if (s_q >= L) return;  // a slot past L (a partial last chunk): no query, no barrier follows
     const int i_q = spos[rq];
     const int32_t* bi = buckets + (bh * L + i_q) * n_r;
     const int beta = min(max(bi[r], 0), n_b - 1);
@@ -548,7 +554,7 @@ hipError_t launch_bf16(bool causal, const uint16_t* q, const uint16_t* v, const 
     // Strips of chunks: long enough that staging the strip's first window is
     // a small overhead, short enough to give the chip several workgroups per
     // CU (three fit at once).
-    const int64_t n_chunks = L / kChunk, segs = BH * n_r;
+    const int64_t n_chunks = (L + kChunk - 1) / kChunk, segs = BH * n_r;
     const int cps = (int)std::max<int64_t>(1, std::min<int64_t>(16, n_chunks * segs / 3072));
     const dim3 grid((unsigned)((n_chunks + cps - 1) / cps), (unsigned)segs);
     if (causal)
@@ -583,7 +589,7 @@ hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, bool 
     if (BH == 0 || L == 0) return hipSuccess;
     const unsigned segs = (unsigned)(BH * n_rounds);
     if (f32) {
-        attn_fwd_f32_kernel<<<dim3(L / kChunk, segs), 64, 0, stream>>>(
+        attn_fwd_f32_kernel<<<dim3((L + kChunk - 1) / kChunk, segs), 64, 0, stream>>>(
             static_cast<const float*>(q), static_cast<const float*>(v), buckets, perm, bucket_start,
             static_cast<float*>(o_rounds), lse_rounds, L, n_rounds, n_buckets, causal ? 1 : 0, scale,
             self_mask);

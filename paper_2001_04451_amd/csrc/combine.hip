@@ -14,7 +14,8 @@ constexpr int kMaxRounds = 16;
 
 // Eight lanes share a row.  Lane p of the group first handles round p (and
 // p + 8 when n_r > 8): its slot from undo, its log-partition z_r, and after
-// a max / sum across the group (shuffles) its weight exp(z_r - z).  Then
+// a max / sum across the group (shuffles) its weight exp(z_r - z), formed as
+// exp(z_r - max_r z_r) / sum so that it is exact at any magnitude of z.  Then
 // every lane takes 8 of the row's 64 values (16 bytes of bf16, two float4
 // of fp32) from all rounds, with the slots and weights of the other rounds
 // read from their lanes.  The code is straight-line for every n_r: rounds
@@ -32,8 +33,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o
                                                       int L, int n_r) {
     const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 3;
     const int part = threadIdx.x & 7;
-    // The row count is a multiple of the 32 rows of a block for every L the
-    // library accepts (L is a multiple of the chunk, 64); whole groups leave.
+    // Rows past the end leave as whole 8-lane groups; every shuffle below
+    // stays inside a group.
     if (row >= rows) return;
     const int64_t bh = row / L;
     const int64_t i = row % L;
@@ -65,9 +66,13 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o
 #pragma unroll
     for (int o = 1; o < 8; o <<= 1) sum += __shfl_xor(sum, o);
     const float z = zmax + logf(sum);
+    // weights relative to the largest round, not to z: a token alone in its
+    // buckets has z_r near -self_mask, where one fp32 spacing of z is 2^-7,
+    // and exp(z_r - z) would carry that rounding into every weight
+    const float inv_sum = 1.f / sum;
     float wk[RPL];
 #pragma unroll
-    for (int k = 0; k < RPL; ++k) wk[k] = live[k] ? expf(zr[k] - z) : 0.f;
+    for (int k = 0; k < RPL; ++k) wk[k] = live[k] ? expf(zr[k] - zmax) * inv_sum : 0.f;
 
     // every round's slot and weight in every lane of the group (rounds
     // n_r .. NRL-1 read round n_r - 1's row with weight 0)

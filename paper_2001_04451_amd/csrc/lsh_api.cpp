@@ -20,7 +20,6 @@ int check_config(const lsh_config* cfg) {
     if (cfg->B < 1 || cfg->H < 1 || cfg->L < 1 || cfg->d < 1) return LSH_ERR_INVALID;
     if (cfg->n_buckets < 2 || (cfg->n_buckets % 2) != 0) return LSH_ERR_INVALID;
     if (cfg->n_rounds < 1 || cfg->chunk < 1) return LSH_ERR_INVALID;
-    if (cfg->L % cfg->chunk != 0) return LSH_ERR_INVALID;
     if (!finitef(cfg->scale) || !finitef(cfg->self_mask)) return LSH_ERR_INVALID;
     return LSH_OK;
 }

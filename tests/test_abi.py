@@ -51,7 +51,7 @@ FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails val
 
 @pytest.mark.parametrize("bad", [dict(B=0), dict(L=0), dict(d=0), dict(n_buckets=7),
                                  dict(n_buckets=0), dict(n_rounds=0), dict(chunk=0),
-                                 dict(L=1000), dict(scale=float("nan"))])
+                                 dict(H=0), dict(scale=float("nan"))])
 def test_invalid_config(L, bad):
     c = _cfg(**bad)
     rc = L.lsh_hash(ctypes.byref(c), lsh.LSH_BF16, FAKE, FAKE, FAKE, FAKE, 1 << 30, None)

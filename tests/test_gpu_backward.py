@@ -34,6 +34,9 @@ CASES = {
     # the most rounds the library takes (eight signature words), causal
     "sixteen_rounds": small("long_bf16_L65536", H=1, L=2048, n_buckets=256, n_rounds=16,
                             backward=True),
+    # a partial last chunk (L mod 64 = 32), causal and not
+    "partial_chunk_causal": small("fwdbwd_bf16_L32768", B=1, H=1, L=1056, n_buckets=64),
+    "partial_chunk": small("mixture_bf16_L4096", B=1, H=1, L=1000, backward=True),
 }
 
 

@@ -158,9 +158,9 @@ def test_gather_rows(gpu):
 
 
 def test_invalid_arguments_on_gpu(gpu):
-    cfg = lsh.Config(B=1, H=1, L=100, n_buckets=16, n_rounds=1)  # L % 64 != 0
+    cfg = lsh.Config(B=1, H=1, L=100, n_buckets=15, n_rounds=1)  # odd n_buckets
     q = torch.zeros((1, 1, 100, 64), device=gpu)
-    R = torch.zeros((1, 64, 8), device=gpu)
+    R = torch.zeros((1, 64, 7), device=gpu)
     with pytest.raises(lsh.LshError) as e:
         lsh.lsh_hash(cfg, q, R)
     assert e.value.status == lsh.LSH_ERR_INVALID
@@ -259,6 +259,41 @@ def test_combine_round_counts(gpu, dtype, n_rounds):
     assert lse_close(lse.cpu().numpy(), ref_lse, dtype).all()
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_combine_lone_token_weights(gpu, dtype):
+    """Tokens alone in their buckets in every round: each z_r sits near
+    -self_mask (where one fp32 spacing is 2^-7), and mixed rows put such a
+    round beside ordinary ones.  The weights must not inherit the rounding of
+    z at that magnitude: equal z_r give the mean of the rows to fp32
+    accuracy."""
+    B, H, L, d, n_rounds = 1, 1, 512, 64, 3
+    rng = np.random.default_rng(77)
+    o = rng.standard_normal((B, H, n_rounds, L, d)).astype(np.float32)
+    if dtype == "bf16":
+        o = (torch.from_numpy(o).to(torch.bfloat16).float()).numpy()
+    base = (-1e5 + 2.0 + rng.standard_normal((B, H, 1, L))).astype(np.float32)
+    lse_r = np.repeat(base, n_rounds, axis=2)
+    # every fourth token: round 1 has other targets (an ordinary z_r)
+    lse_r[:, :, 1, ::4] = rng.standard_normal(L // 4).astype(np.float32)
+    undo = np.stack([np.argsort(rng.permutation(L)) for _ in range(n_rounds)]).reshape(
+        B, H, n_rounds, L).astype(np.int32)
+    ref_out, ref_lse = oracle.lsh_combine_rounds(o.astype(np.float64), lse_r.astype(np.float64),
+                                                 undo)
+    cfg = lsh.Config(B=B, H=H, L=L, n_buckets=64, n_rounds=n_rounds)
+    tdt = torch_dtype(dtype)
+    log("combine-lone", dtype)
+    out, lse = lsh.lsh_combine_rounds(cfg, torch.from_numpy(o).to(tdt).cuda(),
+                                      torch.from_numpy(lse_r).cuda(),
+                                      torch.from_numpy(undo).cuda(), tdt)
+    torch.cuda.synchronize()
+    diff = np.abs(out.float().cpu().numpy() - ref_out)
+    # bf16 output: one rounding to nearest (half an ulp of an 8-bit
+    # significand: at most 2^-8 relative)
+    bound = 1e-5 if dtype == "f32" else 2.0 ** -8 * np.abs(ref_out) + 1e-6
+    assert (diff <= bound).all(), f"combine max-abs error {diff.max()}"
+    assert lse_close(lse.cpu().numpy(), ref_lse, dtype).all()
+
+
 def test_hash_listed_pass_many_open_rows(gpu):
     """Round 0's queries are built as near-ties between two columns of R, so
     the hi-plane screen leaves nearly every row of that round open: each
@@ -313,5 +348,29 @@ def test_forward_round_counts(gpu, n_rounds, causal):
     assert np.array_equal(st.perm.cpu().numpy(), ref["perm"])
     err = np.abs(st.out.float().cpu().numpy() - ref["out"]).max()
     print(f"n_r={n_rounds} causal={causal}: max-abs err {err:.3e}")
+    assert err <= out_tolerance(w.dtype)
+    assert lse_close(st.lse.cpu().numpy(), ref["lse"], w.dtype).all()
+
+
+
+@pytest.mark.parametrize("dtype,causal,L", [("bf16", True, 4000), ("bf16", False, 4000),
+                                            ("bf16", True, 100), ("bf16", False, 130),
+                                            ("f32", True, 1000), ("f32", False, 70)])
+def test_forward_partial_last_chunk(gpu, dtype, causal, L):
+    """L not a multiple of the chunk: the last chunk holds the L mod 64
+    remaining slots (no key or query past L).  Whole forward against the
+    oracle, which pins this reading against the dense windowed form."""
+    w = small("mixture_bf16_L4096", B=1, H=2, L=L, n_rounds=3, causal=causal, dtype=dtype)
+    x, q64, v64 = _inputs(w)
+    ref = oracle.lsh_attention_fwd(q64, v64, x["R"].astype(np.float64), w.chunk, w.causal)
+    cfg = lsh.Config.of(w)
+    log("forward-partial-chunk", dtype, causal, L)
+    st = lsh.lsh_attention_fwd(cfg, to_device(x["q"], w.dtype), to_device(x["v"], w.dtype),
+                               to_device(x["R"], "f32"))
+    torch.cuda.synchronize()
+    assert np.array_equal(st.buckets.cpu().numpy(), ref["buckets"])
+    assert np.array_equal(st.perm.cpu().numpy(), ref["perm"])
+    err = np.abs(st.out.float().cpu().numpy() - ref["out"]).max()
+    print(f"{dtype} causal={causal} L={L}: max-abs err {err:.3e}")
     assert err <= out_tolerance(w.dtype)
     assert lse_close(st.lse.cpu().numpy(), ref["lse"], w.dtype).all()
