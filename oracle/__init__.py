@@ -51,9 +51,11 @@ def _load():
         lib.lsh_ref_chunk_attn_bwd.argtypes = [_i64, _i64, _i64, _i64, _i64, ctypes.c_int,
                                                _f64, _f64, _ptr, _ptr, _ptr, _ptr, _ptr, _ptr,
                                                _ptr, _ptr, _ptr]
+        lib.lsh_ref_dense_attn_fwd.argtypes = [_i64, _i64, _i64, ctypes.c_int, _f64, _f64, _ptr,
+                                               _ptr, _ptr, _ptr]
         lib.lsh_ref_num_threads.argtypes = []
         for name in ("lsh_ref_num_threads", "lsh_ref_hash", "lsh_ref_sort_permute", "lsh_ref_chunk_attn_fwd",
-                     "lsh_ref_combine_rounds", "lsh_ref_chunk_attn_bwd"):
+                     "lsh_ref_combine_rounds", "lsh_ref_chunk_attn_bwd", "lsh_ref_dense_attn_fwd"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -119,6 +121,21 @@ def lsh_chunk_attn_fwd(q, v, buckets, perm, chunk, causal, scale=None, self_mask
                                           _p(buckets), _p(perm), _p(o_rounds), _p(lse_rounds)),
            "chunk_attn_fwd")
     return o_rounds, lse_rounds
+
+
+def dense_attn_fwd(q, v, causal, scale=None, self_mask=1e5):
+    """Full shared-QK attention (the memory-efficient baseline of Sec. 2):
+    out [B,H,L,d] and lse [B,H,L]."""
+    q, v = _f(q), _f(v)
+    B, H, L, d = q.shape
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    out = np.empty((B, H, L, d), np.float64)
+    lse = np.empty((B, H, L), np.float64)
+    _check(_load().lsh_ref_dense_attn_fwd(B * H, L, d, int(bool(causal)), float(scale),
+                                          float(self_mask), _p(q), _p(v), _p(out), _p(lse)),
+           "dense_attn_fwd")
+    return out, lse
 
 
 def lsh_combine_rounds(o_rounds, lse_rounds, undo):

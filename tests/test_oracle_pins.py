@@ -466,3 +466,68 @@ def test_oracle_rejects_bad_arguments(oracle_lib):
     with pytest.raises(RuntimeError):
         oracle.lsh_chunk_attn_fwd(q, q, np.zeros((1, 1, 64, 1), np.int32),
                                   np.zeros((1, 1, 1, 64), np.int32), 0, False)  # m = 0
+
+
+# --------------------------------------------------------------------------
+# The dense baseline (full shared-QK attention, Sec. 2 memory-efficient
+# attention): pinned to the LSH oracle's one-bucket case, to PyTorch's
+# attention routine, and to its special cases
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("L,d", [(64, 8), (100, 64), (203, 16)])
+def test_dense_is_one_bucket_one_chunk(oracle_lib, causal, L, d):
+    """With every token in one bucket, one round and a chunk holding the whole
+    sequence, the LSH window covers all keys: the two oracle functions (no
+    shared code beyond the row norms) must agree."""
+    rng = _rng(7 * L + d + causal)
+    q = rng.standard_normal((L, d))
+    v = rng.standard_normal((L, d))
+    out_l, lse_l, _ = run_oracle(q, v, np.zeros((L, 1), np.int32), chunk=L, causal=causal)
+    out_d, lse_d = oracle.dense_attn_fwd(q.reshape(1, 1, L, d), v.reshape(1, 1, L, d), causal)
+    np.testing.assert_allclose(out_d[0, 0], out_l, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(lse_d[0, 0], lse_l, atol=1e-9, rtol=0)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_dense_matches_torch_attention(oracle_lib, causal):
+    """PyTorch's scaled_dot_product_attention (CPU, float64) with K = Q/|Q|
+    and the App. A masks as an additive float mask: -1e5 on the diagonal,
+    -inf above it under causal masking."""
+    B, H, L, d = 2, 3, 96, 64
+    rng = _rng(11 + causal)
+    q = rng.standard_normal((B, H, L, d)) * rng.uniform(0.5, 3.0, (B, H, L, 1))
+    v = rng.standard_normal((B, H, L, d))
+    out, _ = oracle.dense_attn_fwd(q, v, causal)
+    qt, vt = torch.from_numpy(q), torch.from_numpy(v)
+    kt = qt / qt.norm(dim=-1, keepdim=True)
+    mask = torch.zeros((L, L), dtype=torch.float64)
+    mask.fill_diagonal_(-1e5)
+    if causal:
+        mask = mask.masked_fill(torch.ones((L, L), dtype=torch.bool).triu(1), float("-inf"))
+    ref = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, attn_mask=mask,
+                                                           scale=1.0 / np.sqrt(d))
+    np.testing.assert_allclose(out, ref.numpy(), atol=1e-12, rtol=0)
+
+
+def test_dense_special_cases(oracle_lib):
+    """Causal: the first token's only key is itself (output v_0, log-partition
+    scale*|q_0| - 1e5).  A zero query has k = 0 (logit 0 as a key) and, as a
+    query, weighs every other key equally.  Non-causal attention is
+    equivariant under a permutation of the positions."""
+    L, d = 40, 16
+    rng = _rng(5)
+    q = rng.standard_normal((L, d))
+    v = rng.standard_normal((L, d))
+    q[7] = 0.0
+    scale = 1.0 / np.sqrt(d)
+    out_c, lse_c = oracle.dense_attn_fwd(q.reshape(1, 1, L, d), v.reshape(1, 1, L, d), True)
+    assert np.array_equal(out_c[0, 0, 0], v[0])
+    assert abs(lse_c[0, 0, 0] - (scale * np.linalg.norm(q[0]) - 1e5)) < 1e-9
+    out, lse = oracle.dense_attn_fwd(q.reshape(1, 1, L, d), v.reshape(1, 1, L, d), False)
+    others = np.delete(np.arange(L), 7)
+    np.testing.assert_allclose(out[0, 0, 7], v[others].mean(0), atol=1e-12, rtol=0)
+    assert abs(lse[0, 0, 7] - np.log(L - 1)) < 1e-12
+    p = rng.permutation(L)
+    out_p, lse_p = oracle.dense_attn_fwd(q[p].reshape(1, 1, L, d), v[p].reshape(1, 1, L, d), False)
+    np.testing.assert_allclose(out_p[0, 0], out[0, 0][p], atol=1e-12, rtol=0)
+    np.testing.assert_allclose(lse_p[0, 0], lse[0, 0][p], atol=1e-12, rtol=0)
