@@ -71,7 +71,8 @@ typedef enum lsh_op {
     LSH_OP_ATTN_FWD = 2,
     LSH_OP_COMBINE = 3,
     LSH_OP_ATTN_BWD = 4,
-    LSH_OP_FORWARD = 5 /* lsh_attention_fwd: all four forward calls */
+    LSH_OP_FORWARD = 5, /* lsh_attention_fwd: all four forward calls */
+    LSH_OP_DENSE_FWD = 6 /* lsh_dense_attn_fwd */
 } lsh_op;
 
 /* Problem description (Sec. 2 of the paper: one shared Q=K tensor and V of
@@ -189,6 +190,27 @@ int lsh_chunk_attn_bwd(const lsh_config *cfg, lsh_dtype dtype, const void *q, co
                        const int32_t *buckets, const int32_t *perm, const int32_t *undo,
                        const int32_t *bucket_start, float *dq, float *dv, void *workspace,
                        size_t workspace_bytes, void *stream);
+
+/* Full shared-QK attention, the memory-efficient baseline of Sec. 2: every
+ * query's softmax over all keys computed without materialising QK^T.  Keys
+ * are k_j = q_j/|q_j| (a zero row gives k = 0), the logit of query i and
+ * key j is scale*q_i.k_j, self_mask is subtracted for j == i (App. A), and
+ * under causal masking no key later than i counts (Sec. 2, "Causal masking
+ * for shared-QK attention").  This is what the LSH forward approximates; with
+ * one bucket, one round and a chunk covering the sequence the two coincide.
+ * It is the baseline of the paper's speed-versus-length comparison (Sec. 5).
+ *   q, v      [B][H][L][d] bf16, position order
+ *   out       [B][H][L][d] bf16 (written); accumulated in fp32
+ *   lse       [B][H][L] fp32 log-partition (written; may be NULL)
+ *   workspace >= lsh_workspace_bytes(cfg, dtype, LSH_OP_DENSE_FWD): per-row
+ *             key scales
+ * Only B, H, L, d, causal, scale and self_mask of cfg are read; the hashing
+ * fields are ignored (n_buckets, n_rounds and chunk are not validated).
+ * bf16 only, d = 64, B*H < 65536 and B*H*L < 2^31 on the GPU (otherwise
+ * LSH_ERR_UNSUPPORTED). */
+int lsh_dense_attn_fwd(const lsh_config *cfg, lsh_dtype dtype, const void *q, const void *v,
+                       void *out, float *lse, void *workspace, size_t workspace_bytes,
+                       void *stream);
 
 #ifdef __cplusplus
 }

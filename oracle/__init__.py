@@ -52,7 +52,7 @@ def _load():
                                                _f64, _f64, _ptr, _ptr, _ptr, _ptr, _ptr, _ptr,
                                                _ptr, _ptr, _ptr]
         lib.lsh_ref_dense_attn_fwd.argtypes = [_i64, _i64, _i64, ctypes.c_int, _f64, _f64, _ptr,
-                                               _ptr, _ptr, _ptr]
+                                               _ptr, _i64, _ptr, _ptr, _ptr]
         lib.lsh_ref_num_threads.argtypes = []
         for name in ("lsh_ref_num_threads", "lsh_ref_hash", "lsh_ref_sort_permute", "lsh_ref_chunk_attn_fwd",
                      "lsh_ref_combine_rounds", "lsh_ref_chunk_attn_bwd", "lsh_ref_dense_attn_fwd"):
@@ -123,17 +123,26 @@ def lsh_chunk_attn_fwd(q, v, buckets, perm, chunk, causal, scale=None, self_mask
     return o_rounds, lse_rounds
 
 
-def dense_attn_fwd(q, v, causal, scale=None, self_mask=1e5):
+def dense_attn_fwd(q, v, causal, scale=None, self_mask=1e5, rows=None):
     """Full shared-QK attention (the memory-efficient baseline of Sec. 2):
-    out [B,H,L,d] and lse [B,H,L]."""
+    out [B,H,L,d] and lse [B,H,L]; or, for `rows` (flat indices b*H*L + h*L + i),
+    out [len(rows), d] and lse [len(rows)] of those rows only."""
     q, v = _f(q), _f(v)
     B, H, L, d = q.shape
     if scale is None:
         scale = 1.0 / np.sqrt(d)
-    out = np.empty((B, H, L, d), np.float64)
-    lse = np.empty((B, H, L), np.float64)
+    if rows is None:
+        sel, n_sel = None, B * H * L
+        out = np.empty((B, H, L, d), np.float64)
+        lse = np.empty((B, H, L), np.float64)
+    else:
+        sel = np.ascontiguousarray(rows, dtype=np.int64)
+        n_sel = len(sel)
+        out = np.empty((n_sel, d), np.float64)
+        lse = np.empty((n_sel,), np.float64)
     _check(_load().lsh_ref_dense_attn_fwd(B * H, L, d, int(bool(causal)), float(scale),
-                                          float(self_mask), _p(q), _p(v), _p(out), _p(lse)),
+                                          float(self_mask), _p(q), _p(v), n_sel,
+                                          None if sel is None else _p(sel), _p(out), _p(lse)),
            "dense_attn_fwd")
     return out, lse
 

@@ -276,18 +276,52 @@ int lsh_ref_chunk_attn_fwd(int64_t BH, int64_t L, int64_t d, int64_t n_rounds,
 }
 
 /* Full shared-QK attention, the memory-efficient baseline of Sec. 2 ("the
- * attention can be computed for each query separately"): for every query i
- * the softmax over all keys k_j = q_j/|q_j| of a_ij = scale * q_i.k_j, with
- * self_mask subtracted for j == i and, under causal masking, no j later than
- * i (Sec. 2, "Causal masking for shared-QK attention").  The LSH forward
- * approximates exactly this; it is the speed baseline of the paper's
- * speed-versus-length comparison (Sec. 5).  out [BH][L][d], lse [BH][L]. */
+ * attention can be computed for each query separately"): for query i of the
+ * (batch, head) slice starting at row `base`, the softmax over all keys
+ * k_j = q_j/|q_j| of a_ij = scale * q_i.k_j, with self_mask subtracted for
+ * j == i and, under causal masking, no j later than i (Sec. 2, "Causal
+ * masking for shared-QK attention").  The LSH forward approximates exactly
+ * this; it is the speed baseline of the paper's speed-versus-length
+ * comparison (Sec. 5).  a: scratch of L doubles. */
+static void dense_row(int64_t L, int64_t d, int causal, double scale, double self_mask,
+                      const double *q, const double *v, const double *norm, int64_t base,
+                      int64_t i, double *a, double *o, double *z_out)
+{
+    const int64_t n = causal ? i + 1 : L; /* keys 0 .. n-1 */
+    const double *qi = q + (base + i) * d;
+    double amax = -INFINITY;
+    for (int64_t j = 0; j < n; ++j) {
+        const double nj = norm[base + j];
+        const double qk = nj > 0.0 ? dot(qi, q + (base + j) * d, d) / nj : 0.0;
+        a[j] = scale * qk - (j == i ? self_mask : 0.0);
+        if (a[j] > amax) amax = a[j];
+    }
+    /* j = i is always a key, so n >= 1 and z is finite. */
+    double sum = 0.0;
+    for (int64_t j = 0; j < n; ++j) sum += exp(a[j] - amax);
+    const double z = amax + log(sum);
+    for (int64_t t = 0; t < d; ++t) o[t] = 0.0;
+    for (int64_t j = 0; j < n; ++j) {
+        const double w = exp(a[j] - z);
+        const double *vj = v + (base + j) * d;
+        for (int64_t t = 0; t < d; ++t) o[t] += w * vj[t];
+    }
+    *z_out = z;
+}
+
+/* Dense attention for `n_sel` selected rows (sel: flat row index bh*L + i
+ * into [BH][L]); out [n_sel][d], lse [n_sel].  All rows when sel is NULL
+ * (then n_sel must be BH*L and out is [BH][L][d]). */
 int lsh_ref_dense_attn_fwd(int64_t BH, int64_t L, int64_t d, int causal,
                            double scale, double self_mask, const double *q,
-                           const double *v, double *out, double *lse)
+                           const double *v, int64_t n_sel, const int64_t *sel,
+                           double *out, double *lse)
 {
-    if (BH < 0 || L < 0 || d < 1 || !q || !v || !out || !lse)
+    if (BH < 0 || L < 0 || d < 1 || !q || !v || !out || !lse || n_sel < 0)
         return REF_ERR_INVALID;
+    if (!sel && n_sel != BH * L) return REF_ERR_INVALID;
+    for (int64_t k = 0; sel && k < n_sel; ++k)
+        if (sel[k] < 0 || sel[k] >= BH * L) return REF_ERR_INVALID;
     double *norm = (double *)malloc((size_t)(BH * L > 0 ? BH * L : 1) * sizeof(double));
     if (!norm) return REF_ERR_NOMEM;
     row_norms(BH * L, d, q, norm);
@@ -300,30 +334,11 @@ int lsh_ref_dense_attn_fwd(int64_t BH, int64_t L, int64_t d, int causal,
             err = 1;
         }
 #pragma omp for schedule(static)
-        for (int64_t row = 0; row < BH * L; ++row) {
+        for (int64_t k = 0; k < n_sel; ++k) {
             if (!a) continue;
-            const int64_t base = (row / L) * L, i = row % L;
-            const int64_t n = causal ? i + 1 : L; /* keys 0 .. n-1 */
-            const double *qi = q + row * d;
-            double amax = -INFINITY;
-            for (int64_t j = 0; j < n; ++j) {
-                const double nj = norm[base + j];
-                const double qk = nj > 0.0 ? dot(qi, q + (base + j) * d, d) / nj : 0.0;
-                a[j] = scale * qk - (j == i ? self_mask : 0.0);
-                if (a[j] > amax) amax = a[j];
-            }
-            /* j = i is always a key, so n >= 1 and z is finite. */
-            double sum = 0.0;
-            for (int64_t j = 0; j < n; ++j) sum += exp(a[j] - amax);
-            const double z = amax + log(sum);
-            double *o = out + row * d;
-            for (int64_t t = 0; t < d; ++t) o[t] = 0.0;
-            for (int64_t j = 0; j < n; ++j) {
-                const double w = exp(a[j] - z);
-                const double *vj = v + (base + j) * d;
-                for (int64_t t = 0; t < d; ++t) o[t] += w * vj[t];
-            }
-            lse[row] = z;
+            const int64_t row = sel ? sel[k] : k;
+            dense_row(L, d, causal, scale, self_mask, q, v, norm, (row / L) * L, row % L, a,
+                      out + k * d, lse + k);
         }
         free(a);
     }

@@ -51,10 +51,6 @@ constexpr int kRing = 192;          // three chunk slots of 64 rows
 constexpr float kFastBound = 60.f;  // largest B_i handled without a running maximum
 constexpr int kMaskedIndex = 32;    // table index of a masked-out key
 
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-constexpr bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
 
 template <bool B>
 struct BoolTag {
@@ -101,48 +97,8 @@ struct FwdShared {
     float tab[kMaskedIndex + 1];              // -log2 N by mismatch count; -inf = masked
 };
 
-__device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-__device__ __forceinline__ f32x4 mfma16x16x16(bf16x4 a, bf16x4 b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
-}
 
-// Copy 16 (4) bytes per lane from global memory to LDS at lds_base + 16
-// (4) * lane; lds_base is uniform over the wave.  Written as inline assembly
-// so that the compiler does not order every later LDS read of the step
-// behind these copies (it cannot tell the slot being filled from the slots
-// being read); the kernel waits for them itself before each barrier.
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-    // the same address in every lane; readfirstlane puts it in a scalar register
-    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p);
-}
-__device__ __forceinline__ void copy16_to_lds(const void* src, const void* lds_base) {
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_addr(lds_base))
-                 : "memory", "m0");
-}
-__device__ __forceinline__ void copy4_to_lds(const void* src, const void* lds_base) {
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(src), "s"(lds_addr(lds_base))
-                 : "memory", "m0");
-}
 
-// V^T operand of a 16x16x16 product for keys r0 .. r0+15 and dims d0 .. d0+15:
-// lane l needs V[r0 + 4(l/16) + k][d0 + l%16] for k = 0..3.  The transposing
-// read gives lane i of each 16-lane group element i%4 of the 8-byte runs read
-// by lanes 4k + i/4, so lane i reads row r0 + 4(l/16) + i/4, dims
-// d0 + 4(i%4) .. +3: vt_offset is that byte offset (r0 a multiple of 16, so
-// the swizzle depends on the lane only).
-__device__ __forceinline__ uint32_t vt_offset(int r0, int d0, int lane) {
-    const int i = lane & 15;
-    const int row = r0 + 4 * (lane >> 4) + (i >> 2);
-    const int d = d0 + 4 * (i & 3);
-    return row_piece_offset(row, d >> 3) + (uint32_t)((d & 4) << 1);
-}
-__device__ __forceinline__ bf16x4 vt_read(const char* p) {
-    typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-    const i16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(__attribute__((address_space(3))) char*)p);
-    return __builtin_bit_cast(bf16x4, x);
-}
 
 template <int NW>
 __device__ __forceinline__ void read_sig(const FwdShared<NW>& S, int row, uint32_t (&out)[NW > 0 ? NW : 1]) {

@@ -53,4 +53,10 @@ hipError_t launch_attn_bwd(int64_t BH, int L, int n_rounds, int n_buckets, bool 
                            const int32_t* bucket_start, float* dq, float* dv, void* workspace,
                            hipStream_t stream);
 
+// ---- full (dense) shared-QK attention, forward ----
+size_t dense_workspace_bytes(int64_t BH, int L);
+hipError_t launch_dense_fwd(int64_t BH, int L, bool causal, float scale, float self_mask,
+                            const void* q, const void* v, void* out, float* lse, void* workspace,
+                            hipStream_t stream);
+
 }  // namespace lsh

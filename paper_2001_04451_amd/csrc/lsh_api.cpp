@@ -40,6 +40,21 @@ int check_supported(const lsh_config* cfg) {
 
 int64_t bh_of(const lsh_config* cfg) { return (int64_t)cfg->B * cfg->H; }
 
+// The dense baseline reads only the shape, the mask flag and the scales.
+int check_dense_config(const lsh_config* cfg) {
+    if (!cfg) return LSH_ERR_INVALID;
+    if (cfg->B < 1 || cfg->H < 1 || cfg->L < 1 || cfg->d < 1) return LSH_ERR_INVALID;
+    if (!finitef(cfg->scale) || !finitef(cfg->self_mask)) return LSH_ERR_INVALID;
+    return LSH_OK;
+}
+
+int check_dense_supported(const lsh_config* cfg, int dtype) {
+    if (dtype != LSH_BF16 || cfg->d != lsh::kHeadDimHost) return LSH_ERR_UNSUPPORTED;
+    const int64_t BH = (int64_t)cfg->B * cfg->H;
+    if (BH >= 65536 || BH * cfg->L >= kMaxElems) return LSH_ERR_UNSUPPORTED;
+    return LSH_OK;
+}
+
 // The kernels move rows in 16-byte pieces.
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 template <typename... P>
@@ -78,6 +93,10 @@ const char* lsh_status_string(int status) {
 }
 
 size_t lsh_workspace_bytes(const lsh_config* cfg, lsh_dtype dtype, int op) {
+    if (op == LSH_OP_DENSE_FWD) {
+        if (check_dense_config(cfg) != LSH_OK || check_dtype(dtype) != LSH_OK) return 0;
+        return lsh::dense_workspace_bytes(bh_of(cfg), cfg->L);
+    }
     if (check_config(cfg) != LSH_OK || check_dtype(dtype) != LSH_OK) return 0;
     const int64_t BH = bh_of(cfg);
     const size_t hash = lsh::hash_workspace_bytes(BH * cfg->L, cfg->n_rounds, cfg->n_buckets);
@@ -210,6 +229,20 @@ int lsh_chunk_attn_bwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, co
                                           cfg->causal != 0, cfg->scale, cfg->self_mask, q, v, out,
                                           dout, lse_total, buckets, perm, undo, bucket_start, dq,
                                           dv, workspace, static_cast<hipStream_t>(stream)));
+}
+
+int lsh_dense_attn_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, const void* v,
+                       void* out, float* lse, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+    LSH_TRY(check_dense_config(cfg));
+    LSH_TRY(check_dtype(dtype));
+    if (!q || !v || !out || !workspace) return LSH_ERR_INVALID;
+    if (!all_aligned(q, v, out, workspace)) return LSH_ERR_INVALID;
+    if (workspace_bytes < lsh::dense_workspace_bytes(bh_of(cfg), cfg->L)) return LSH_ERR_INVALID;
+    LSH_TRY(check_dense_supported(cfg, dtype));
+    return status_of(lsh::launch_dense_fwd(bh_of(cfg), cfg->L, cfg->causal != 0, cfg->scale,
+                                           cfg->self_mask, q, v, out, lse, workspace,
+                                           static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

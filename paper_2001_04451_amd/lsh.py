@@ -28,12 +28,12 @@ LIB_PATH = os.path.join(_PKG, "liblsh.so")
 LSH_OK, LSH_ERR_INVALID, LSH_ERR_UNSUPPORTED, LSH_ERR_HIP = 0, -1, -2, -3
 LSH_F32, LSH_BF16 = 0, 1
 (LSH_OP_HASH, LSH_OP_SORT, LSH_OP_ATTN_FWD, LSH_OP_COMBINE, LSH_OP_ATTN_BWD,
- LSH_OP_FORWARD) = range(6)
+ LSH_OP_FORWARD, LSH_OP_DENSE_FWD) = range(7)
 
 # Every symbol include/lsh.h declares.
 EXPORTED = ("lsh_status_string", "lsh_workspace_bytes", "lsh_hash", "lsh_sort_permute",
             "lsh_gather_rows", "lsh_chunk_attn_fwd", "lsh_combine_rounds", "lsh_attention_fwd",
-            "lsh_chunk_attn_bwd")
+            "lsh_chunk_attn_bwd", "lsh_dense_attn_fwd")
 
 
 class LshConfig(ctypes.Structure):
@@ -78,6 +78,7 @@ def lib() -> ctypes.CDLL:
             "lsh_attention_fwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
             "lsh_chunk_attn_bwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ,
                                    _P],
+            "lsh_dense_attn_fwd": [_CFG, _I, _P, _P, _P, _P, _P, _SZ, _P],
         }
         for name, args in sigs.items():
             fn = getattr(L, name)
@@ -307,3 +308,23 @@ def lsh_chunk_attn_bwd(cfg: Config, q, v, out, dout, lse_total, buckets, perm, u
                                     _ptr(perm), _ptr(undo), _ptr(bstart), _ptr(dq), _ptr(dv),
                                     _ptr(workspace), workspace.numel(), _stream(dev)))
     return dq, dv
+
+
+def lsh_dense_attn_fwd(cfg: Config, q, v, out=None, lse=None, workspace=None):
+    """Full shared-QK attention (lsh_dense_attn_fwd): out [B,H,L,d] bf16 and
+    lse [B,H,L] fp32.  Only the shape, causal flag and scales of cfg are used."""
+    _need(q, (cfg.B, cfg.H, cfg.L, cfg.d), torch.bfloat16, "q")
+    _need(v, (cfg.B, cfg.H, cfg.L, cfg.d), torch.bfloat16, "v")
+    dev = q.device
+    if out is None:
+        out = torch.empty_like(q)
+    _need(out, (cfg.B, cfg.H, cfg.L, cfg.d), torch.bfloat16, "out")
+    if lse is None:
+        lse = torch.empty((cfg.B, cfg.H, cfg.L), dtype=torch.float32, device=dev)
+    if workspace is None:
+        workspace = _workspace(cfg, q.dtype, LSH_OP_DENSE_FWD, dev)
+    _check("lsh_dense_attn_fwd",
+           lib().lsh_dense_attn_fwd(ctypes.byref(cfg.c()), _dtype_code(q), _ptr(q), _ptr(v),
+                                    _ptr(out), _ptr(lse), _ptr(workspace), workspace.numel(),
+                                    _stream(dev)))
+    return out, lse

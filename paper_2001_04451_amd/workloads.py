@@ -84,10 +84,18 @@ HEADLINE = "long_bf16_L65536"
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
-    """Round fp32 to the nearest bf16 (ties to even); returns uint16 bit patterns."""
-    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    b = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
-    return b.astype(np.uint16)
+    """Round fp32 to the nearest bf16 (ties to even); returns uint16 bit patterns.
+    Infinities stay infinite and NaNs stay (quiet) NaNs."""
+    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    r = (b >> 16) & np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += b  # no wrap-around: a finite value's bits are at most 0xFF7FFFFF
+    r >>= 16
+    special = (b & np.uint32(0x7F800000)) == np.uint32(0x7F800000)
+    if special.any():
+        hi = b[special] >> 16
+        r[special] = np.where((b[special] & np.uint32(0x7FFFFF)) != 0, hi | np.uint32(0x40), hi)
+    return r.astype(np.uint16)
 
 
 def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:

@@ -121,3 +121,25 @@ def test_product_never_touches_the_oracle():
                 text = open(os.path.join(dirpath, f)).read()
                 assert not re.search(r"^\s*(import|from)\s+oracle", text, re.M), f
                 assert "lsh_oracle" not in text and "lsh_ref_" not in text, f
+
+
+def test_dense_entry_validation(L):
+    """The dense baseline reads only the shape, causal flag and scales; its
+    errors come back before any HIP call."""
+    c = _cfg(n_buckets=0, n_rounds=0, chunk=0)  # hashing fields are not read
+    need = L.lsh_workspace_bytes(ctypes.byref(c), lsh.LSH_BF16, lsh.LSH_OP_DENSE_FWD)
+    assert need >= c.B * c.H * c.L * 4
+    args = (FAKE, FAKE, FAKE, None, FAKE)
+    assert L.lsh_dense_attn_fwd(None, lsh.LSH_BF16, *args, need, None) == lsh.LSH_ERR_INVALID
+    assert L.lsh_dense_attn_fwd(ctypes.byref(c), lsh.LSH_BF16, *args, need - 1, None) == lsh.LSH_ERR_INVALID
+    assert L.lsh_dense_attn_fwd(ctypes.byref(c), lsh.LSH_BF16, None, FAKE, FAKE, None, FAKE, need,
+                                None) == lsh.LSH_ERR_INVALID
+    assert L.lsh_dense_attn_fwd(ctypes.byref(c), lsh.LSH_BF16, FAKE, FAKE, FAKE, None, None, need,
+                                None) == lsh.LSH_ERR_INVALID
+    assert L.lsh_dense_attn_fwd(ctypes.byref(c), 5, *args, need, None) == lsh.LSH_ERR_INVALID
+    assert L.lsh_dense_attn_fwd(ctypes.byref(c), lsh.LSH_F32, *args, 1 << 30, None) == lsh.LSH_ERR_UNSUPPORTED
+    c32 = _cfg(d=32)
+    assert L.lsh_dense_attn_fwd(ctypes.byref(c32), lsh.LSH_BF16, *args, 1 << 30, None) == lsh.LSH_ERR_UNSUPPORTED
+    bad = _cfg(L=0)
+    assert L.lsh_workspace_bytes(ctypes.byref(bad), lsh.LSH_BF16, lsh.LSH_OP_DENSE_FWD) == 0
+    assert L.lsh_dense_attn_fwd(ctypes.byref(bad), lsh.LSH_BF16, *args, 1 << 30, None) == lsh.LSH_ERR_INVALID

@@ -531,3 +531,19 @@ def test_dense_special_cases(oracle_lib):
     out_p, lse_p = oracle.dense_attn_fwd(q[p].reshape(1, 1, L, d), v[p].reshape(1, 1, L, d), False)
     np.testing.assert_allclose(out_p[0, 0], out[0, 0][p], atol=1e-12, rtol=0)
     np.testing.assert_allclose(lse_p[0, 0], lse[0, 0][p], atol=1e-12, rtol=0)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_dense_selected_rows(oracle_lib, causal):
+    """The row-sampled form (used at full size) returns the same rows as the
+    whole computation, in the order asked for, across batch and head."""
+    B, H, L, d = 2, 2, 70, 8
+    rng = _rng(23 + causal)
+    q = rng.standard_normal((B, H, L, d))
+    v = rng.standard_normal((B, H, L, d))
+    out, lse = oracle.dense_attn_fwd(q, v, causal)
+    rows = np.array([0, 69, 70, 139, 215, 3 * L + 5, 4 * L - 1, 71])
+    o_s, l_s = oracle.dense_attn_fwd(q, v, causal, rows=rows)
+    assert np.array_equal(o_s, out.reshape(-1, d)[rows])
+    assert np.array_equal(l_s, lse.reshape(-1)[rows])
+
