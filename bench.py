@@ -1,7 +1,7 @@
 """Throughput of Reformer LSH attention on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                    [--cpu-budget S] [--copy-probe BYTES]
+                    [--cpu-budget S] [--copy-probe BYTES] [--sweep-length]
 
 One step is one full forward pass over one batch of the workload: hash, sort,
 chunked attention (with the gather fused into its staging) and the round
@@ -106,9 +106,10 @@ def algorithmic_work(w: W.Workload) -> dict:
     }
 
 
-def run_gpu(w: W.Workload, steps: int, warmup: int) -> dict:
+def run_gpu(w: W.Workload, steps: int, warmup: int, x: dict | None = None) -> dict:
     dev = torch.device("cuda:0")
-    x = W.make_inputs(w)
+    if x is None:
+        x = W.make_inputs(w)
     tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
 
     def up(a, bf):
@@ -195,6 +196,74 @@ def cpu_baseline(w: W.Workload, budget_s: float) -> dict:
                       f"scaled by the slice fraction"}
 
 
+SWEEP_LENGTHS = (1024, 2048, 4096, 8192, 16384, 32768, 65536)
+
+
+def dense_flop(B: int, H: int, L: int, d: int, causal: bool) -> float:
+    """Algorithmic flops of full attention: 2d for q.k and 2d for p*v per
+    (query, key) pair that takes part (j <= i under causal masking)."""
+    pairs = L * (L + 1) / 2 if causal else float(L) * L
+    return 4.0 * d * pairs * B * H
+
+
+def run_dense(B: int, H: int, L: int, q: torch.Tensor, v: torch.Tensor, causal: bool,
+              steps: int, warmup: int) -> float:
+    """Average ms of one dense attention forward (HIP events on the stream the
+    kernels run on)."""
+    cfg = lsh.Config(B=B, H=H, L=L, n_buckets=2, n_rounds=1, causal=causal)
+    out = torch.empty_like(q)
+    lse = torch.empty((B, H, L), dtype=torch.float32, device=q.device)
+    ws = torch.empty(max(256, lsh.workspace_bytes(cfg, q.dtype, lsh.LSH_OP_DENSE_FWD)),
+                     dtype=torch.uint8, device=q.device)
+    for _ in range(warmup):
+        lsh.lsh_dense_attn_fwd(cfg, q, v, out, lse, ws)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        lsh.lsh_dense_attn_fwd(cfg, q, v, out, lse, ws)
+    e1.record()
+    torch.cuda.synchronize()
+    if not torch.isfinite(out.float()).all():
+        raise RuntimeError("non-finite dense output")
+    return e0.elapsed_time(e1) / steps
+
+
+def sweep_length(steps: int, warmup: int) -> None:
+    """Speed against sequence length at a fixed number of tokens (the paper's
+    speed-versus-length comparison, Sec. 5): the tokens and values of the
+    64K x 16-head benchmark batch, cut into B = 65536/L sequences of length L.
+    LSH attention: 8 rounds, chunks of 64, L/64 buckets (64 tokens per bucket on
+    average, 1024 at 64K as in the benchmark); dense: full shared-QK attention.
+    Both causal, bf16.  One JSON line per length."""
+    base = W.WORKLOADS[W.HEADLINE]
+    x = W.make_inputs(base)
+    total, H, d = base.B * base.L, base.H, base.d
+    dev = torch.device("cuda:0")
+    for L in SWEEP_LENGTHS:
+        B = total // L
+        w = base.scaled(B=B, L=L, n_buckets=max(2, L // 64))
+        q, v = (np.ascontiguousarray(t.reshape(H, B, L, d).transpose(1, 0, 2, 3))
+                for t in (x["q"], x["v"]))
+        rng = np.random.Generator(np.random.PCG64(L))
+        R = rng.standard_normal((w.n_rounds, d, w.n_buckets // 2), dtype=np.float32)
+        g = run_gpu(w, steps, warmup, {"q": q, "v": v, "R": R})
+        qd = torch.from_numpy(q).view(torch.int16).view(torch.bfloat16).to(dev)
+        vd = torch.from_numpy(v).view(torch.int16).view(torch.bfloat16).to(dev)
+        dense_ms = run_dense(B, H, L, qd, vd, w.causal, steps, warmup)
+        del qd, vd
+        fl = dense_flop(B, H, L, d, w.causal)
+        print(json.dumps({
+            "sweep": "speed_vs_length", "L": L, "B": B, "H": H, "tokens": B * L,
+            "n_buckets": w.n_buckets, "n_rounds": w.n_rounds, "causal": w.causal,
+            "lsh_ms": g["ms_per_step"], "lsh_stage_ms": g["stage_ms"],
+            "lsh_tokens_per_s": B * L / (g["ms_per_step"] * 1e-3),
+            "dense_ms": dense_ms, "dense_tokens_per_s": B * L / (dense_ms * 1e-3),
+            "dense_tflops": fl / (dense_ms * 1e-3) / 1e12,
+            "dense_mfma_frac": fl / (dense_ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
+            "dense_over_lsh": dense_ms / g["ms_per_step"]}), flush=True)
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -206,6 +275,9 @@ def main() -> int:
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="after timing, copy this many bytes device to device (a plain copy "
                          "kernel of known size, to scale HBM traffic counters)")
+    ap.add_argument("--sweep-length", action="store_true",
+                    help="instead of the benchmark line: LSH and dense attention speed at a "
+                         "fixed number of tokens for L = 1K .. 64K (one JSON line per L)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -217,6 +289,9 @@ def main() -> int:
         return 2
     w = W.WORKLOADS[args.workload]
     lsh.lib()
+    if args.sweep_length:
+        sweep_length(args.steps, args.warmup)
+        return 0
     g = run_gpu(w, args.steps, args.warmup)
     if args.copy_probe > 0:
         n = args.copy_probe // 16 * 16
