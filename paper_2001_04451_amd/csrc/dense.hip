@@ -21,10 +21,12 @@
 // maximum is needed while the wave's logit bound B_i = scale*log2(e)*|q_i|
 // (Cauchy-Schwarz: every logit lies in [-B_i, B_i]) is at most 60, since
 // exp2 then neither overflows nor underflows; waves with a larger bound keep
-// the online maximum.  Masks are applied only in blocks that hold a query's
-// own position or the sequence end; under causal masking a wave stops after
-// the block holding its last query, and workgroups of later queries (more
-// keys) are dispatched first.
+// the online maximum.  Three workgroups share a CU (a few registers spill;
+// measured faster than two without spills, most of all for short
+// sequences, where a workgroup walks few blocks).  Masks are applied only in
+// blocks that hold a query's own position or the sequence end; under causal
+// masking a wave stops after the block holding its last query, and
+// workgroups of later queries (more keys) are dispatched first.
 #include "attn_common.h"
 #include "launch.h"
 
@@ -69,7 +71,7 @@ __global__ __launch_bounds__(256) void dense_prep_kernel(const uint16_t* __restr
 }
 
 template <bool CAUSAL>
-__global__ __launch_bounds__(256, 2) void dense_attn_fwd_kernel(
+__global__ __launch_bounds__(256, 3) void dense_attn_fwd_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ v, const float* __restrict__ cf,
     uint16_t* __restrict__ out, float* __restrict__ lse, int L, float scale_log2e, float self_mask) {
     __shared__ __attribute__((aligned(16))) DenseShared S;
