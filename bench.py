@@ -55,6 +55,9 @@ STAGES = {
     "attn": {"kernels": ["attn_prep_kernel", "attn_fwd_bf16_kernel"],
              "sources": ["attn_fwd.hip", "attn_common.h", "common.h"], "bound": "hbm",
              "work": "attn_bytes"},
+    "bwd": {"kernels": ["bwd_prep_kernel", "bwd_kv_kernel", "bwd_q_kernel", "bwd_reduce_kernel"],
+            "sources": ["attn_bwd.hip", "attn_common.h", "common.h"], "bound": "hbm",
+            "work": "bwd_bytes"},
     "combine": {"kernels": ["combine_kernel"], "sources": ["combine.hip", "common.h"],
                 "bound": "hbm", "work": "combine_bytes"},
 }
@@ -103,6 +106,13 @@ def algorithmic_work(w: W.Workload) -> dict:
         "sort_bytes": rr * 16,
         # per row: n_r o_rounds rows (dtype) + lse + undo read, one output row written
         "combine_bytes": rows * (n_r * (e * d + 8) + d * e + 4),
+        # backward, recomputing the logits: S = QK^T, dP = dO V^T, dV += P^T dO,
+        # dQ += dA K, dK += dA^T Q over the 2m-key window, 2 * (2m * d) flops each
+        "bwd_flop": rr * 20 * m * d,
+        # per row-round: q, v and dO rows gathered, the slot's position, the
+        # token's total log-partition and D_i = dO_i . o_i; per row: out and
+        # dout read once for D_i, dq and dv written in fp32
+        "bwd_bytes": rr * (3 * d * e + 4 + 8) + rows * (2 * d * e + 2 * 4 * d),
     }
 
 
@@ -118,6 +128,7 @@ def run_gpu(w: W.Workload, steps: int, warmup: int, x: dict | None = None) -> di
 
     bf = w.dtype == "bf16"
     q, v, R = up(x["q"], bf), up(x["v"], bf), up(x["R"], False)
+    dout = up(x["dout"], bf) if w.backward else None
     del x
     cfg = lsh.Config.of(w)
     B, H, L, nr, nb, d = w.B, w.H, w.L, w.n_rounds, w.n_buckets, w.d
@@ -168,7 +179,35 @@ def run_gpu(w: W.Workload, steps: int, warmup: int, x: dict | None = None) -> di
                                    for k in range(steps)])) for i, s in enumerate(stages)}
     if not torch.isfinite(out.float()).all():
         raise RuntimeError("non-finite output")
-    return {"ms_per_step": (t1 - t0) * 1e3 / steps, "stage_ms": per_stage}
+    res = {"ms_per_step": (t1 - t0) * 1e3 / steps, "stage_ms": per_stage}
+    if w.backward:
+        # the backward on the last forward's state: one lsh_chunk_attn_bwd call
+        # per step, timed the same way
+        dq = torch.empty((B, H, L, d), dtype=torch.float32, device=dev)
+        dv = torch.empty_like(dq)
+        ws_bwd = torch.empty(max(256, lsh.workspace_bytes(cfg, tdt, lsh.LSH_OP_ATTN_BWD)),
+                             dtype=torch.uint8, device=dev)
+
+        def bwd():
+            lsh.lsh_chunk_attn_bwd(cfg, q, v, out, dout, lse, buckets, perm, undo, bstart, dq, dv,
+                                   ws_bwd)
+
+        for _ in range(warmup):
+            bwd()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        tb0 = time.perf_counter()
+        e0.record()
+        for _ in range(steps):
+            bwd()
+        e1.record()
+        torch.cuda.synchronize()
+        tb1 = time.perf_counter()
+        if not (torch.isfinite(dq).all() and torch.isfinite(dv).all()):
+            raise RuntimeError("non-finite gradients")
+        res["bwd_ms"] = e0.elapsed_time(e1) / steps
+        res["bwd_wall_ms"] = (tb1 - tb0) * 1e3 / steps
+    return res
 
 
 def cpu_baseline(w: W.Workload, budget_s: float) -> dict:
@@ -338,6 +377,19 @@ def main() -> int:
         },
         "roofline": roof,
     }
+    if "bwd_ms" in g:
+        # the backward (dq, dv) of the same batch, reported the same way
+        bspec = STAGES["bwd"]
+        bach = work["bwd_bytes"] / (g["bwd_ms"] * 1e-3) / 1e9
+        line["backward"] = {
+            "tokens_per_s": tokens / (g["bwd_wall_ms"] * 1e-3), "ms_per_step": g["bwd_wall_ms"],
+            "kernel_ms": g["bwd_ms"],
+            "roofline": {"bound": "hbm", "achieved": bach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": bach / HBM_PEAK_GBS,
+                         "traffic": recorded_traffic(w.name, "bwd"), "stage": "bwd",
+                         "kernels": bspec["kernels"], "algorithmic": work["bwd_bytes"]},
+            "mfma_frac": work["bwd_flop"] / (g["bwd_ms"] * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
+        }
     if args.cpu_budget > 0:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
     print(json.dumps(line), flush=True)
