@@ -27,6 +27,7 @@ namespace lsh {
 namespace {
 
 constexpr int kWin = 192;  // staged rows: three chunks
+constexpr int kMaskedIndex = 32;  // table index of a masked-out pair
 
 template <int NW>
 struct SigStride {
@@ -42,6 +43,7 @@ struct RowMeta {
     int lo[kWin];    // slot interval of the row's valid keys (as a query)
     int hi[kWin];
     uint32_t sig[kWin][SigStride<NW>::value];
+    float tab[kMaskedIndex + 1];  // -log2 N by mismatch count; -inf = masked
 };
 
 template <int NW>
@@ -63,17 +65,17 @@ __device__ __forceinline__ void load_sig(const RowMeta<NW>& M, int row, uint32_t
     }
 }
 
+// Number of rounds in which two tokens' bucket ids differ (0 when there is
+// one round, which needs no signatures).
 template <int NW>
-__device__ __forceinline__ float neg_log2_n(const uint32_t (&a)[NW > 0 ? NW : 1],
-                                            const uint32_t (&b)[NW > 0 ? NW : 1], int n_r) {
-    if constexpr (NW == 0) {
-        return 0.f;
-    } else {
-        int nm = 0;
+__device__ __forceinline__ int n_mismatch(const uint32_t (&a)[NW > 0 ? NW : 1],
+                                          const uint32_t (&b)[NW > 0 ? NW : 1]) {
+    int nm = 0;
+    if constexpr (NW > 0) {
 #pragma unroll
         for (int w = 0; w < NW; ++w) nm += sig_mismatches(a[w], b[w]);
-        return -__log2f((float)(n_r - nm));
     }
+    return nm;
 }
 
 // Stage rows [slot0, slot0 + 192) of one segment, gathered through perm:
@@ -87,54 +89,90 @@ __device__ __forceinline__ void stage_window(
     const float* __restrict__ Dbuf, const int32_t* __restrict__ buckets,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ bstart, int64_t seg,
     int64_t bh, int r, int slot0, int L, int n_r, int n_b, float scale_log2e) {
-    const int tid = threadIdx.x;
+    // Three phases, each issuing all of its loads before any result is used:
+    // the staged slots' positions, then (through them) the rows, bucket ids,
+    // log-partitions and D, then (through the ids) the bucket bounds.  Every
+    // address is clamped to a valid one, so no load sits under a per-lane
+    // condition (which would make it a branch with its own wait); slots
+    // outside the sequence get zero rows and an empty interval afterwards.
+    constexpr int kIt = kWin * 8 / 256;
+    const int tid = threadIdx.x, part = tid & 7;
     const int32_t* bs = bstart + seg * (n_b + 1);
+    const int32_t* pseg = perm + seg * L;
+    if (tid <= kMaskedIndex) M.tab[tid] = tid < n_r ? -__log2f((float)(n_r - tid)) : -__builtin_inff();
+    const u32x4 zero = {0, 0, 0, 0};
+
+    int pos[kIt];
 #pragma unroll
-    for (int i = 0; i < kWin * 8 / 256; ++i) {
-        const int idx = tid + 256 * i;
-        const int rho = idx >> 3, part = idx & 7;
+    for (int i = 0; i < kIt; ++i) {
+        const int slot = slot0 + ((tid + 256 * i) >> 3);
+        pos[i] = pseg[min(max(slot, 0), L - 1)];
+    }
+
+    u32x4 qq[kIt], vv[kIt], dd[kIt];
+    int beta[kIt];
+    uint32_t lo_id[kIt], hi_id[kIt];
+    float zl[kIt], Dl[kIt];
+#pragma unroll
+    for (int i = 0; i < kIt; ++i) {
+        const int rho = (tid + 256 * i) >> 3;  // the same for the whole wave's 8 rows' range test
+        const int64_t grow = bh * L + min(max(pos[i], 0), L - 1);
+        const int64_t off = grow * kHeadDim + part * 8;
+        qq[i] = *reinterpret_cast<const u32x4*>(q + off);
+        vv[i] = zero;
+        if (rho >= v_lo && rho < v_hi) vv[i] = *reinterpret_cast<const u32x4*>(v + off);
+        dd[i] = zero;
+        if (rho >= d_lo && rho < d_hi) dd[i] = *reinterpret_cast<const u32x4*>(dout + off);
+        const int32_t* brow = buckets + grow * n_r;
+        beta[i] = brow[r];
+        lo_id[i] = (uint32_t)brow[min(2 * part, n_r - 1)];
+        hi_id[i] = (uint32_t)brow[min(2 * part + 1, n_r - 1)];
+        zl[i] = lse_total[grow];
+        Dl[i] = Dbuf[grow];
+    }
+
+    int b0[kIt], b1[kIt];
+#pragma unroll
+    for (int i = 0; i < kIt; ++i) {
+        const int bb = min(max(beta[i], 0), n_b - 1);
+        b0[i] = bs[bb];
+        b1[i] = bs[bb + 1];
+    }
+
+#pragma unroll
+    for (int i = 0; i < kIt; ++i) {
+        const int rho = (tid + 256 * i) >> 3;
         const int slot = slot0 + rho;
         const bool ok = slot >= 0 && slot < L;
-        const int pos = ok ? min(max(perm[seg * L + slot], 0), L - 1) : 0;
-        const int64_t grow = bh * L + pos;
-        const u32x4 zero = {0, 0, 0, 0};
-        const u32x4 qq = ok ? *reinterpret_cast<const u32x4*>(q + grow * kHeadDim + part * 8) : zero;
-        lds_store_piece(Qs, rho, part, qq);
-        if (rho >= v_lo && rho < v_hi) {
-            const u32x4 vv = ok ? *reinterpret_cast<const u32x4*>(v + grow * kHeadDim + part * 8) : zero;
-            lds_store_piece(Vs, rho - v_lo, part, vv);
-        }
-        if (rho >= d_lo && rho < d_hi) {
-            const u32x4 dd = ok ? *reinterpret_cast<const u32x4*>(dout + grow * kHeadDim + part * 8) : zero;
-            lds_store_piece(Ds, rho - d_lo, part, dd);
-        }
+        const u32x4 qv = ok ? qq[i] : zero;
+        lds_store_piece(Qs, rho, part, qv);
+        if (rho >= v_lo && rho < v_hi) lds_store_piece(Vs, rho - v_lo, part, ok ? vv[i] : zero);
+        if (rho >= d_lo && rho < d_hi) lds_store_piece(Ds, rho - d_lo, part, ok ? dd[i] : zero);
         float ss = 0.f;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const float a = __uint_as_float(qq[e] << 16), b = __uint_as_float(qq[e] & 0xFFFF0000u);
+            const float a = __uint_as_float(qv[e] << 16), b = __uint_as_float(qv[e] & 0xFFFF0000u);
             ss = fmaf(a, a, fmaf(b, b, ss));
         }
         ss += __shfl_xor(ss, 1);
         ss += __shfl_xor(ss, 2);
         ss += __shfl_xor(ss, 4);
-        const int32_t* brow = buckets + grow * n_r;
         if (part == 0) {
             const float nn = sqrtf(ss);
             M.cf[rho] = nn > 0.f ? scale_log2e / nn : 0.f;
-            M.z2[rho] = ok ? lse_total[grow] * kLog2e : 0.f;
-            M.D[rho] = ok ? Dbuf[grow] : 0.f;
-            const int beta = min(max(brow[r], 0), n_b - 1);
+            M.z2[rho] = ok ? zl[i] * kLog2e : 0.f;
+            M.D[rho] = ok ? Dl[i] : 0.f;
             const int c = (slot >= 0 ? slot : 0) / kChunk;
             const int wlo = max(0, (c - 1) * kChunk);
-            M.lo[rho] = ok ? max(bs[beta], wlo) : 1;
-            M.hi[rho] = ok ? (CAUSAL ? slot - 1 : min(bs[beta + 1], (c + 1) * kChunk) - 1) : 0;
+            M.lo[rho] = ok ? max(b0[i], wlo) : 1;
+            M.hi[rho] = ok ? (CAUSAL ? slot - 1 : min(b1[i], (c + 1) * kChunk) - 1) : 0;
         }
         if constexpr (NW > 0) {
             if (part < SigStride<NW>::value) {
                 uint32_t w = 0;
                 if (ok && part < NW) {
-                    w = (uint32_t)brow[2 * part];
-                    if (2 * part + 1 < n_r) w |= (uint32_t)brow[2 * part + 1] << 11;
+                    w = lo_id[i];
+                    if (2 * part + 1 < n_r) w |= hi_id[i] << 11;
                 }
                 M.sig[rho][part] = w;
             }
@@ -202,6 +240,16 @@ __global__ __launch_bounds__(256, 2) void bwd_kv_kernel(
 #pragma unroll
         for (int run = 0; run < 2; ++run) {
             const int qb = qr0 + 16 * run + 8 * h;  // first query row of the lane's run
+            // the run's eight queries: interval, log-partition, D
+            int lo8[8], hi8[8];
+            float z8[8], D8[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                lo8[e] = M.lo[qb + e];
+                hi8[e] = M.hi[qb + e];
+                z8[e] = M.z2[qb + e];
+                D8[e] = M.D[qb + e];
+            }
 #pragma unroll
             for (int e2 = 0; e2 < 4; ++e2) {
                 float pv[2], dav[2];
@@ -210,14 +258,15 @@ __global__ __launch_bounds__(256, 2) void bwd_kv_kernel(
                     const int e = 2 * e2 + u;
                     const int qi = qb + e;
                     const int j = 8 * run + e;
-                    bool valid = t_key >= M.lo[qi] && t_key <= M.hi[qi];
+                    bool valid = t_key >= lo8[e] && t_key <= hi8[e];
                     if constexpr (!CAUSAL) valid = valid && t_key != slot0 + qi;
                     uint32_t sig_q[NW > 0 ? NW : 1];
                     load_sig<NW>(M, qi, sig_q);
-                    const float x = fmaf(sacc[j], cf_k, neg_log2_n<NW>(sig_q, sig_k, n_r));
-                    const float p = valid ? __builtin_amdgcn_exp2f(x - M.z2[qi]) : 0.f;
+                    // -log2 N_ij, or -inf for a pair outside the query's interval
+                    const float mterm = M.tab[valid ? n_mismatch<NW>(sig_q, sig_k) : kMaskedIndex];
+                    const float p = __builtin_amdgcn_exp2f(fmaf(sacc[j], cf_k, mterm) - z8[e]);
                     pv[u] = p;
-                    dav[u] = p * (dpacc[j] - M.D[qi]);
+                    dav[u] = p * (dpacc[j] - D8[e]);
                 }
                 const uint32_t hi = pack_bf16x2(pv[0], pv[1]);
                 pk[run][e2] = hi;
@@ -320,6 +369,9 @@ __global__ __launch_bounds__(256, 2) void bwd_q_kernel(
 #pragma unroll
         for (int run = 0; run < 2; ++run) {
             const int krb = kr0 + 16 * run + 8 * h;
+            float cf8[8];  // the run's eight key scales
+#pragma unroll
+            for (int e = 0; e < 8; ++e) cf8[e] = M.cf[krb + e];
 #pragma unroll
             for (int e2 = 0; e2 < 4; ++e2) {
                 float dav[2];
@@ -333,9 +385,10 @@ __global__ __launch_bounds__(256, 2) void bwd_q_kernel(
                     if constexpr (!CAUSAL) valid = valid && t != s_q;
                     uint32_t sig_k[NW > 0 ? NW : 1];
                     load_sig<NW>(M, kj, sig_k);
-                    const float cfk = M.cf[kj];
-                    const float x = fmaf(sacc[j], cfk, neg_log2_n<NW>(sig_q, sig_k, n_r));
-                    const float p = valid ? __builtin_amdgcn_exp2f(x - z2) : 0.f;
+                    const float cfk = cf8[e];
+                    // -log2 N_ij, or -inf for a key outside the query's interval
+                    const float mterm = M.tab[valid ? n_mismatch<NW>(sig_q, sig_k) : kMaskedIndex];
+                    const float p = __builtin_amdgcn_exp2f(fmaf(sacc[j], cfk, mterm) - z2);
                     // scale/|q_j| = cf_j / log2(e); the 1/log2(e) is applied at the end
                     dav[u] = p * (dpacc[j] - Dq) * cfk;
                 }
