@@ -36,7 +36,9 @@
  *   be tested without a GPU; LSH_ERR_HIP reports a failed launch.  No C++
  *   exception crosses this interface.  The library keeps no mutable global
  *   state, so calls on different streams may run concurrently.
- * Supported on the GPU: d = 64, chunk = 64, 2 <= n_buckets <= 1024 (even),
+ * Supported on the GPU: d = 64, chunk = 64 (and chunk = 128, the length of the
+ *   paper's usual configuration, Sec. 5, on the fp32 forward; entry points that
+ *   do not use the chunk ignore it), 2 <= n_buckets <= 1024 (even),
  *   1 <= n_rounds <= 16, B*H*L*n_rounds < 2^31.  L need not be a multiple of
  *   the chunk: the last chunk then holds the L mod m remaining sorted slots
  *   (the paper is silent; read as padding with tokens that are no one's

@@ -377,49 +377,56 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
     flush();
 }
 
-// fp32 path: one wave per chunk, one lane per query, exact fp32 arithmetic
-// on the VALU with an online softmax over the query's key interval.
-__global__ __launch_bounds__(64) void attn_fwd_f32_kernel(
+// fp32 path: one workgroup per chunk of M sorted slots (M = 64, or 128, the
+// chunk length of the paper's usual configuration), one lane per query,
+// exact fp32 arithmetic on the VALU with an online softmax over the query's
+// key interval.  The window (chunks c-1 and c) is staged in LDS.
+template <int M>
+__global__ __launch_bounds__(M) void attn_fwd_f32_kernel(
     const float* __restrict__ q, const float* __restrict__ v, const int32_t* __restrict__ buckets,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ bstart,
     float* __restrict__ o_rounds, float* __restrict__ lse_rounds, int L, int n_r, int n_b,
     int causal, float scale, float self_mask) {
-    __shared__ float Ks[128][kHeadDim + 1];
-    __shared__ float Vs2[128][kHeadDim + 1];
-    __shared__ float inv[128];
-    __shared__ int spos[128];
+    __shared__ float Ks[2 * M][kHeadDim + 1];
+    __shared__ float Vs2[2 * M][kHeadDim + 1];
+    __shared__ float inv[2 * M];
+    __shared__ int spos[2 * M];
 
     const int t = threadIdx.x;
     const int64_t seg = blockIdx.y;
     const int64_t bh = seg / n_r;
     const int r = (int)(seg % n_r);
     const int c = blockIdx.x;
-    const int slot0 = (c - 1) * kChunk;
-    for (int rho = 0; rho < 128; ++rho) {
+    const int slot0 = (c - 1) * M;
+    // staging: thread t copies dim t % 64 of row t / 64 of each group of M / 64 rows
+    constexpr int kRowsPerPass = M / kHeadDim;
+    const int dcol = t % kHeadDim, rsub = t / kHeadDim;
+    for (int rho0 = 0; rho0 < 2 * M; rho0 += kRowsPerPass) {
+        const int rho = rho0 + rsub;
         const int slot = slot0 + rho;
         const bool ok = slot >= 0 && slot < L;
         const int pos = ok ? min(max(perm[seg * L + slot], 0), L - 1) : 0;
-        Ks[rho][t] = ok ? q[(bh * L + pos) * kHeadDim + t] : 0.f;
-        Vs2[rho][t] = ok ? v[(bh * L + pos) * kHeadDim + t] : 0.f;
-        if (t == 0) spos[rho] = ok ? pos : -1;
+        Ks[rho][dcol] = ok ? q[(bh * L + pos) * kHeadDim + dcol] : 0.f;
+        Vs2[rho][dcol] = ok ? v[(bh * L + pos) * kHeadDim + dcol] : 0.f;
+        if (dcol == 0) spos[rho] = ok ? pos : -1;
     }
     __syncthreads();
-    for (int rr = t; rr < 128; rr += 64) {
+    for (int rr = t; rr < 2 * M; rr += M) {
         float ss = 0.f;
         for (int u = 0; u < kHeadDim; ++u) ss = fmaf(Ks[rr][u], Ks[rr][u], ss);
         inv[rr] = ss > 0.f ? 1.f / sqrtf(ss) : 0.f;
     }
     __syncthreads();
 
-    const int rq = 64 + t;
-    const int s_q = c * kChunk + t;
+    const int rq = M + t;
+    const int s_q = c * M + t;
     if (s_q >= L) return;  // a slot past L (a partial last chunk): no query, no barrier follows
     const int i_q = spos[rq];
     const int32_t* bi = buckets + (bh * L + i_q) * n_r;
     const int beta = min(max(bi[r], 0), n_b - 1);
     const int32_t* bs = bstart + seg * (n_b + 1);
     const int lo = max(bs[beta], max(0, slot0));
-    const int hi = causal ? s_q - 1 : min(bs[beta + 1], (c + 1) * kChunk) - 1;
+    const int hi = causal ? s_q - 1 : min(bs[beta + 1], (c + 1) * M) - 1;
 
     float qi[kHeadDim];
     for (int u = 0; u < kHeadDim; ++u) qi[u] = Ks[rq][u];
@@ -537,7 +544,7 @@ size_t attn_fwd_workspace_bytes(int64_t BH, int L, int n_rounds, bool f32) {
     return align256(rows * 4 * rec_words);
 }
 
-hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, bool causal,
+hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, int chunk, bool causal,
                            float scale, float self_mask, bool f32, const void* q, const void* v,
                            const int32_t* buckets, const int32_t* perm,
                            const int32_t* bucket_start, void* o_rounds, float* lse_rounds,
@@ -545,10 +552,17 @@ hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, bool 
     if (BH == 0 || L == 0) return hipSuccess;
     const unsigned segs = (unsigned)(BH * n_rounds);
     if (f32) {
-        attn_fwd_f32_kernel<<<dim3((L + kChunk - 1) / kChunk, segs), 64, 0, stream>>>(
-            static_cast<const float*>(q), static_cast<const float*>(v), buckets, perm, bucket_start,
-            static_cast<float*>(o_rounds), lse_rounds, L, n_rounds, n_buckets, causal ? 1 : 0, scale,
-            self_mask);
+        const dim3 grid((unsigned)((L + chunk - 1) / chunk), segs);
+        if (chunk == 128)
+            attn_fwd_f32_kernel<128><<<grid, 128, 0, stream>>>(
+                static_cast<const float*>(q), static_cast<const float*>(v), buckets, perm, bucket_start,
+                static_cast<float*>(o_rounds), lse_rounds, L, n_rounds, n_buckets, causal ? 1 : 0, scale,
+                self_mask);
+        else
+            attn_fwd_f32_kernel<64><<<grid, 64, 0, stream>>>(
+                static_cast<const float*>(q), static_cast<const float*>(v), buckets, perm, bucket_start,
+                static_cast<float*>(o_rounds), lse_rounds, L, n_rounds, n_buckets, causal ? 1 : 0, scale,
+                self_mask);
         return hipGetLastError();
     }
     const uint16_t* qb = static_cast<const uint16_t*>(q);

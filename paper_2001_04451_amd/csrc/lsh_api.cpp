@@ -28,9 +28,10 @@ int check_dtype(int dtype) {
     return (dtype == LSH_F32 || dtype == LSH_BF16) ? LSH_OK : LSH_ERR_INVALID;
 }
 
-// What the kernels are specialised for.
+// What the kernels are specialised for (the chunk length is checked by the
+// entry points that use it, see check_chunk).
 int check_supported(const lsh_config* cfg) {
-    if (cfg->d != lsh::kHeadDimHost || cfg->chunk != lsh::kChunkHost) return LSH_ERR_UNSUPPORTED;
+    if (cfg->d != lsh::kHeadDimHost) return LSH_ERR_UNSUPPORTED;
     if (cfg->n_buckets > 1024 || cfg->n_rounds > 16) return LSH_ERR_UNSUPPORTED;
     const int64_t rr = (int64_t)cfg->B * cfg->H * cfg->L * cfg->n_rounds;
     if (rr >= kMaxElems || rr * cfg->d >= ((int64_t)1 << 40)) return LSH_ERR_UNSUPPORTED;
@@ -39,6 +40,14 @@ int check_supported(const lsh_config* cfg) {
 }
 
 int64_t bh_of(const lsh_config* cfg) { return (int64_t)cfg->B * cfg->H; }
+
+// Chunk lengths of the chunked-attention kernels: 64 everywhere, and 128 on
+// the fp32 forward.
+int check_chunk(const lsh_config* cfg, int dtype, bool backward) {
+    if (cfg->chunk == lsh::kChunkHost) return LSH_OK;
+    if (cfg->chunk == 128 && dtype == LSH_F32 && !backward) return LSH_OK;
+    return LSH_ERR_UNSUPPORTED;
+}
 
 // The dense baseline reads only the shape, the mask flag and the scales.
 int check_dense_config(const lsh_config* cfg) {
@@ -168,7 +177,8 @@ int lsh_chunk_attn_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, co
     if (need > 0 && (!workspace || workspace_bytes < need || !all_aligned(workspace)))
         return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
-    return status_of(lsh::launch_attn_fwd(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets,
+    LSH_TRY(check_chunk(cfg, dtype, false));
+    return status_of(lsh::launch_attn_fwd(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets, cfg->chunk,
                                           cfg->causal != 0, cfg->scale, cfg->self_mask,
                                           dtype == LSH_F32, q, v, buckets, perm, bucket_start,
                                           o_rounds, lse_rounds, workspace,
@@ -198,6 +208,7 @@ int lsh_attention_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, con
         return LSH_ERR_INVALID;
     if (workspace_bytes < lsh_workspace_bytes(cfg, dtype, LSH_OP_FORWARD)) return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
+    LSH_TRY(check_chunk(cfg, dtype, false));
     const size_t rr = (size_t)bh_of(cfg) * cfg->n_rounds * cfg->L;
     char* ws = static_cast<char*>(workspace);
     void* o_rounds = ws;
@@ -224,6 +235,7 @@ int lsh_chunk_attn_bwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, co
     if (workspace_bytes < lsh::bwd_workspace_bytes(bh_of(cfg), cfg->L, cfg->n_rounds))
         return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
+    LSH_TRY(check_chunk(cfg, dtype, true));
     if (dtype != LSH_BF16) return LSH_ERR_UNSUPPORTED;
     return status_of(lsh::launch_attn_bwd(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets,
                                           cfg->causal != 0, cfg->scale, cfg->self_mask, q, v, out,

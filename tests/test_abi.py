@@ -143,3 +143,20 @@ def test_dense_entry_validation(L):
     bad = _cfg(L=0)
     assert L.lsh_workspace_bytes(ctypes.byref(bad), lsh.LSH_BF16, lsh.LSH_OP_DENSE_FWD) == 0
     assert L.lsh_dense_attn_fwd(ctypes.byref(bad), lsh.LSH_BF16, *args, 1 << 30, None) == lsh.LSH_ERR_INVALID
+
+
+def test_chunk_lengths(L):
+    """Chunks of 64 everywhere; 128 only on the fp32 forward (its bf16 and
+    backward forms, and other lengths, are unsupported)."""
+    c128 = _cfg(chunk=128)
+    need = L.lsh_workspace_bytes(ctypes.byref(c128), lsh.LSH_BF16, lsh.LSH_OP_FORWARD)
+    rc = L.lsh_attention_fwd(ctypes.byref(c128), lsh.LSH_BF16, FAKE, FAKE, FAKE, FAKE, None, FAKE,
+                             FAKE, FAKE, FAKE, FAKE, need, None)
+    assert rc == lsh.LSH_ERR_UNSUPPORTED
+    bwd = L.lsh_workspace_bytes(ctypes.byref(c128), lsh.LSH_F32, lsh.LSH_OP_ATTN_BWD)
+    assert L.lsh_chunk_attn_bwd(ctypes.byref(c128), lsh.LSH_F32, *([FAKE] * 12), bwd,
+                                None) == lsh.LSH_ERR_UNSUPPORTED
+    c96 = _cfg(chunk=96)
+    assert L.lsh_chunk_attn_fwd(ctypes.byref(c96), lsh.LSH_F32, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                FAKE, None, 0, None) == lsh.LSH_ERR_UNSUPPORTED
+

@@ -374,3 +374,25 @@ def test_forward_partial_last_chunk(gpu, dtype, causal, L):
     print(f"{dtype} causal={causal} L={L}: max-abs err {err:.3e}")
     assert err <= out_tolerance(w.dtype)
     assert lse_close(st.lse.cpu().numpy(), ref["lse"], w.dtype).all()
+
+
+@pytest.mark.parametrize("causal,L", [(True, 1024), (False, 1024), (True, 1000), (False, 333)])
+def test_forward_chunk_128(gpu, causal, L):
+    """Chunks of 128 sorted slots (the paper's usual configuration, Sec. 5,
+    with m = 2l/n_b: 16 buckets at L = 1024) on the fp32 path: whole forward
+    against the oracle, including a partial last chunk."""
+    w = small("tiny_f32_L1024", L=L, chunk=128, n_buckets=16, n_rounds=3, causal=causal)
+    x, q64, v64 = _inputs(w)
+    ref = oracle.lsh_attention_fwd(q64, v64, x["R"].astype(np.float64), w.chunk, w.causal)
+    cfg = lsh.Config.of(w)
+    log("forward-chunk-128", causal, L)
+    st = lsh.lsh_attention_fwd(cfg, to_device(x["q"], "f32"), to_device(x["v"], "f32"),
+                               to_device(x["R"], "f32"))
+    torch.cuda.synchronize()
+    assert np.array_equal(st.buckets.cpu().numpy(), ref["buckets"])
+    assert np.array_equal(st.perm.cpu().numpy(), ref["perm"])
+    err = np.abs(st.out.float().cpu().numpy() - ref["out"]).max()
+    print(f"chunk 128 causal={causal} L={L}: max-abs err {err:.3e}")
+    assert err <= out_tolerance("f32")
+    assert lse_close(st.lse.cpu().numpy(), ref["lse"], "f32").all()
+
