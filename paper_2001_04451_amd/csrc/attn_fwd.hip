@@ -40,7 +40,8 @@
 // the wave's logit bound B_i = scale*log2(e)*|q_i| is moderate: every logit
 // lies in [-B_i - log2 n_r, B_i], so for B_i <= 60 exp2(x) itself neither
 // overflows nor underflows; waves with a larger bound fall back to the online
-// maximum.  The row sum l_i adds the bf16-rounded weights that enter P V.
+// maximum.  The row sum l_i adds the fp32 weights (P V takes them rounded to
+// bf16), so the log-partition is exact to fp32.
 #include "attn_common.h"
 #include "launch.h"
 
@@ -329,8 +330,10 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
                     const float pa = __builtin_amdgcn_exp2f(FAST ? acc[2 * h2] : acc[2 * h2] - off);
                     const float pb = __builtin_amdgcn_exp2f(FAST ? acc[2 * h2 + 1] : acc[2 * h2 + 1] - off);
                     pw[h2] = pack_bf16x2(pa, pb);
-                    // the row sum takes the bf16 weights that enter P V
-                    lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw[h2]), kOnes, lsum, false);
+                    // the row sum takes the fp32 weights, so z_r is exact to fp32 (the
+                    // backward renormalises with it); P V takes them rounded to bf16
+                    lsum += pa;
+                    lsum += pb;
                 }
                 const bf16x4 pk = __builtin_bit_cast(bf16x4, make_uint2(pw[0], pw[1]));
 #pragma unroll
