@@ -401,17 +401,26 @@ __global__ __launch_bounds__(M) void attn_fwd_f32_kernel(
     const int r = (int)(seg % n_r);
     const int c = blockIdx.x;
     const int slot0 = (c - 1) * M;
-    // staging: thread t copies dim t % 64 of row t / 64 of each group of M / 64 rows
+    // staging, in two passes so that no row load waits on its own position
+    // load: the window's positions (-1 outside the sequence), then thread t
+    // copies dim t % 64 of row t / 64 of each group of M / 64 rows, from
+    // clamped addresses
+    for (int rho = t; rho < 2 * M; rho += M) {
+        const int slot = slot0 + rho;
+        const int pos = min(max(perm[seg * L + min(max(slot, 0), L - 1)], 0), L - 1);
+        spos[rho] = slot >= 0 && slot < L ? pos : -1;
+    }
+    __syncthreads();
     constexpr int kRowsPerPass = M / kHeadDim;
     const int dcol = t % kHeadDim, rsub = t / kHeadDim;
+#pragma unroll 8
     for (int rho0 = 0; rho0 < 2 * M; rho0 += kRowsPerPass) {
         const int rho = rho0 + rsub;
-        const int slot = slot0 + rho;
-        const bool ok = slot >= 0 && slot < L;
-        const int pos = ok ? min(max(perm[seg * L + slot], 0), L - 1) : 0;
-        Ks[rho][dcol] = ok ? q[(bh * L + pos) * kHeadDim + dcol] : 0.f;
-        Vs2[rho][dcol] = ok ? v[(bh * L + pos) * kHeadDim + dcol] : 0.f;
-        if (dcol == 0) spos[rho] = ok ? pos : -1;
+        const int pos = spos[rho];
+        const int64_t src = (bh * L + max(pos, 0)) * kHeadDim + dcol;
+        const float kq = q[src], kv = v[src];
+        Ks[rho][dcol] = pos >= 0 ? kq : 0.f;
+        Vs2[rho][dcol] = pos >= 0 ? kv : 0.f;
     }
     __syncthreads();
     for (int rr = t; rr < 2 * M; rr += M) {
