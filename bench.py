@@ -98,14 +98,17 @@ def algorithmic_work(w: W.Workload) -> dict:
         "hash_flop": rr * d * w.n_buckets,
         # QK^T and PV over a 2m-key window: 2 * (2m * d) * 2 flops per row-round
         "attn_flop": rr * 8 * m * d,
-        # per row-round: q and v rows gathered, o_rounds row (dtype) and lse
-        # written, the slot's position read, the token's bucket ids (two per
-        # 32-bit word) gathered
-        "attn_bytes": rr * (2 * d * e + e * d + 4 + 4 + 4 * ((n_r + 1) // 2)),
+        # per row-round: q and v rows gathered, o_rounds row (fp16 for bf16
+        # calls, with its exponent byte; fp32 for fp32 calls) and lse written,
+        # the slot's position read, the token's bucket ids (two per 32-bit
+        # word) gathered
+        "attn_bytes": rr * (2 * d * e + e * d + (1 if e == 2 else 0) + 4 + 4
+                            + 4 * ((n_r + 1) // 2)),
         # ids read twice, perm and undo written
         "sort_bytes": rr * 16,
-        # per row: n_r o_rounds rows (dtype) + lse + undo read, one output row written
-        "combine_bytes": rows * (n_r * (e * d + 8) + d * e + 4),
+        # per row: n_r o_rounds rows (+ exponent byte for bf16 calls), lse and
+        # undo read, one output row and its log-partition written
+        "combine_bytes": rows * (n_r * (e * d + 8 + (1 if e == 2 else 0)) + d * e + 4),
         # backward, recomputing the logits: S = QK^T, dP = dO V^T, dV += P^T dO,
         # dQ += dA K, dK += dA^T Q over the 2m-key window, 2 * (2m * d) flops each
         "bwd_flop": rr * 20 * m * d,
@@ -129,14 +132,14 @@ def run_gpu(w: W.Workload, steps: int, warmup: int, x: dict | None = None) -> di
     bf = w.dtype == "bf16"
     q, v, R = up(x["q"], bf), up(x["v"], bf), up(x["R"], False)
     dout = up(x["dout"], bf) if w.backward else None
-    del x
     cfg = lsh.Config.of(w)
     B, H, L, nr, nb, d = w.B, w.H, w.L, w.n_rounds, w.n_buckets, w.d
     buckets = torch.empty((B, H, L, nr), dtype=torch.int32, device=dev)
     perm = torch.empty((B, H, nr, L), dtype=torch.int32, device=dev)
     undo = torch.empty_like(perm)
     bstart = torch.empty((B, H, nr, nb + 1), dtype=torch.int32, device=dev)
-    o_r = torch.empty((B, H, nr, L, d), dtype=tdt, device=dev)
+    o_r = torch.empty((B, H, nr, L, d), dtype=lsh.rounds_dtype(tdt), device=dev)
+    o_e = torch.empty((B, H, nr, L), dtype=torch.uint8, device=dev) if bf else None
     lse_r = torch.empty((B, H, nr, L), dtype=torch.float32, device=dev)
     out = torch.empty((B, H, L, d), dtype=tdt, device=dev)
     lse = torch.empty((B, H, L), dtype=torch.float32, device=dev)
@@ -158,10 +161,10 @@ def run_gpu(w: W.Workload, steps: int, warmup: int, x: dict | None = None) -> di
         lsh.lsh_sort_permute(cfg, buckets, ws_sort, perm, undo, bstart)
         if ev is not None:
             ev[2].record()
-        lsh.lsh_chunk_attn_fwd(cfg, q, v, buckets, perm, bstart, o_r, lse_r, ws_attn)
+        lsh.lsh_chunk_attn_fwd(cfg, q, v, buckets, perm, bstart, o_r, o_e, lse_r, ws_attn)
         if ev is not None:
             ev[3].record()
-        lsh.lsh_combine_rounds(cfg, o_r, lse_r, undo, tdt, out, lse)
+        lsh.lsh_combine_rounds(cfg, o_r, o_e, lse_r, undo, tdt, out, lse)
         if ev is not None:
             ev[4].record()
 
@@ -179,7 +182,8 @@ def run_gpu(w: W.Workload, steps: int, warmup: int, x: dict | None = None) -> di
                                    for k in range(steps)])) for i, s in enumerate(stages)}
     if not torch.isfinite(out.float()).all():
         raise RuntimeError("non-finite output")
-    res = {"ms_per_step": (t1 - t0) * 1e3 / steps, "stage_ms": per_stage}
+    res = {"ms_per_step": (t1 - t0) * 1e3 / steps, "stage_ms": per_stage,
+           "state": {"buckets": buckets, "perm": perm, "out": out}}
     if w.backward:
         # the backward on the last forward's state: one lsh_chunk_attn_bwd call
         # per step, timed the same way
@@ -210,29 +214,81 @@ def run_gpu(w: W.Workload, steps: int, warmup: int, x: dict | None = None) -> di
     return res
 
 
-def cpu_baseline(w: W.Workload, budget_s: float) -> dict:
-    """The oracle on whole (batch, head) slices of the workload until the time
-    budget is spent; rate scaled to the full workload's tokens."""
-    import oracle  # test infrastructure: used here only for the reported baseline
+def cpu_model() -> str:
+    """The host CPU's model name (as lscpu reports it)."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w: W.Workload, budget_s: float, x: dict, state: dict) -> tuple[dict, dict]:
+    """The oracle on whole (batch, head) slices of the benchmark batch, in a
+    seeded random order, until the time budget is spent; rate scaled to the
+    full workload's tokens.  The same slices of the GPU's last forward are
+    compared with the oracle's: bucket ids bit for bit (near-tie row-rounds
+    counted), the permutation, and the output's max-abs error."""
+    import oracle  # test infrastructure: used here only for the reported baseline and check
 
     oracle.build()
-    one = w.scaled(B=1, H=1)
-    x = W.make_inputs(w.scaled(B=1, H=1))
-    q64, v64 = W.as_f64(x["q"], w.dtype), W.as_f64(x["v"], w.dtype)
     R = x["R"].astype(np.float64)
-    slices, elapsed = 0, 0.0
     total_slices = w.B * w.H
+    order = np.random.default_rng(0).permutation(total_slices)
+    gpu_b = state["buckets"].cpu().numpy()
+    gpu_p = state["perm"].cpu().numpy()
+    gpu_o = state["out"].float().cpu().numpy()
+    slices, elapsed = 0, 0.0
+    n_tie = n_mism = n_mism_outside = 0
+    perm_equal, err = True, 0.0
     while slices < total_slices and (slices == 0 or elapsed < budget_s):
+        b, h = divmod(int(order[slices]), w.H)
+        q64 = W.as_f64(x["q"][b:b + 1, h:h + 1], w.dtype)
+        v64 = W.as_f64(x["v"][b:b + 1, h:h + 1], w.dtype)
         t0 = time.perf_counter()
-        oracle.lsh_attention_fwd(q64, v64, R, one.chunk, one.causal)
+        ref = oracle.lsh_attention_fwd(q64, v64, R, w.chunk, w.causal)
         elapsed += time.perf_counter() - t0
         slices += 1
+        mism = gpu_b[b:b + 1, h:h + 1] != ref["buckets"]
+        n_tie += int(ref["near_tie"].sum())
+        n_mism += int(mism.sum())
+        n_mism_outside += int((mism & ~ref["near_tie"]).sum())
+        perm_equal &= bool(np.array_equal(gpu_p[b:b + 1, h:h + 1], ref["perm"]))
+        err = max(err, float(np.abs(gpu_o[b:b + 1, h:h + 1] - ref["out"]).max()))
     tokens = w.B * w.L * slices / total_slices
-    return {"value": tokens / elapsed, "unit": "tokens/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": f"{slices} of {total_slices} (batch, head) slices of the same workload "
-                      f"(L={w.L}, n_rounds={w.n_rounds}), fp64, {elapsed:.1f} s; tokens/s "
-                      f"scaled by the slice fraction"}
+    base = {"value": tokens / elapsed, "unit": "tokens/s", "cores": oracle.num_threads(),
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "sample": f"{slices} of {total_slices} (batch, head) slices of the benchmark batch "
+                      f"(L={w.L}, n_rounds={w.n_rounds}), fp64, {elapsed:.1f} s of oracle time; "
+                      f"tokens/s scaled by the slice fraction"}
+    parity = {"slices": slices, "near_tie_row_rounds": n_tie, "bucket_mismatches": n_mism,
+              "bucket_mismatches_outside_near_ties": n_mism_outside, "perm_equal": perm_equal,
+              "out_max_abs_err": err, "tol": 2e-2 if w.dtype == "bf16" else 1e-5}
+    return base, parity
+
+
+def stage_rooflines(w: W.Workload, work: dict, st: dict) -> dict:
+    """Each forward stage against the roof that bounds it, from its algorithmic
+    work and its measured time: the hash and the chunk attention on the bf16
+    matrix peak (the attention also on HBM, its bound by arithmetic
+    intensity), the sort and the combine (the scatter back) on HBM."""
+    def mfma(flop, ms):
+        a = flop / (ms * 1e-3) / 1e12
+        return {"bound": "mfma", "achieved": a, "peak": BF16_MFMA_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": a / BF16_MFMA_PEAK_TFLOPS, "algorithmic": flop}
+
+    def hbm(nbytes, ms):
+        a = nbytes / (ms * 1e-3) / 1e9
+        return {"bound": "hbm", "achieved": a, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": a / HBM_PEAK_GBS, "algorithmic": nbytes}
+
+    attn = mfma(work["attn_flop"], st["attn"])
+    attn["hbm"] = hbm(work["attn_bytes"], st["attn"])
+    return {"hash": mfma(work["hash_flop"], st["hash"]), "sort": hbm(work["sort_bytes"], st["sort"]),
+            "attn": attn, "combine": hbm(work["combine_bytes"], st["combine"])}
 
 
 SWEEP_LENGTHS = (1024, 2048, 4096, 8192, 16384, 32768, 65536)
@@ -331,7 +387,8 @@ def main() -> int:
     if args.sweep_length:
         sweep_length(args.steps, args.warmup)
         return 0
-    g = run_gpu(w, args.steps, args.warmup)
+    x = W.make_inputs(w)
+    g = run_gpu(w, args.steps, args.warmup, x)
     if args.copy_probe > 0:
         n = args.copy_probe // 16 * 16
         src = torch.ones(n // 4, dtype=torch.int32, device="cuda:0")
@@ -368,14 +425,9 @@ def main() -> int:
                    "n_buckets": w.n_buckets, "n_rounds": w.n_rounds, "chunk": w.chunk,
                    "causal": w.causal, "inputs": w.dist},
         "stage_ms": st,
-        "stage_fracs": {
-            "hash_mfma": work["hash_flop"] / (st["hash"] * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
-            "attn_mfma": work["attn_flop"] / (st["attn"] * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
-            "attn_hbm": work["attn_bytes"] / (st["attn"] * 1e-3) / 1e9 / HBM_PEAK_GBS,
-            "sort_hbm": work["sort_bytes"] / (st["sort"] * 1e-3) / 1e9 / HBM_PEAK_GBS,
-            "combine_hbm": work["combine_bytes"] / (st["combine"] * 1e-3) / 1e9 / HBM_PEAK_GBS,
-        },
         "roofline": roof,
+        # every stage against its own roof, named (the dominant one is above)
+        "rooflines": stage_rooflines(w, work, st),
     }
     if "bwd_ms" in g:
         # the backward (dq, dv) of the same batch, reported the same way
@@ -391,7 +443,7 @@ def main() -> int:
             "mfma_frac": work["bwd_flop"] / (g["bwd_ms"] * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
         }
     if args.cpu_budget > 0:
-        line["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+        line["cpu_baseline"], line["parity"] = cpu_baseline(w, args.cpu_budget, x, g["state"])
     print(json.dumps(line), flush=True)
     return 0
 

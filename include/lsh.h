@@ -22,7 +22,12 @@
  *                                                   undo: position -> sorted slot
  *   bucket_start      [B][H][n_rounds][n_buckets+1] int32: first sorted slot of
  *                     each bucket, last entry = L
- *   o_rounds          [B][H][n_rounds][L][d] dtype of the call, sorted-slot order
+ *   o_rounds          [B][H][n_rounds][L][d] sorted-slot order: fp32 for fp32
+ *                     calls; for bf16 calls IEEE fp16, each row scaled by
+ *                     2^-o_exp[row] (11 significant bits, so that the combined
+ *                     output is rounded to bf16 only once)
+ *   o_exp             [B][H][n_rounds][L]    uint8, sorted-slot order (bf16 calls
+ *                     only): 0 unless a row's largest magnitude reaches 2^15
  *   lse_rounds        [B][H][n_rounds][L]    fp32, sorted-slot order
  *   out               [B][H][L][d]        dtype of the call
  *   lse_total         [B][H][L]           fp32
@@ -36,6 +41,13 @@
  *   be tested without a GPU; LSH_ERR_HIP reports a failed launch.  No C++
  *   exception crosses this interface.  The library keeps no mutable global
  *   state, so calls on different streams may run concurrently.
+ * self_mask.  The attention entry points (lsh_chunk_attn_fwd and _bwd,
+ *   lsh_attention_fwd, lsh_dense_attn_fwd) return LSH_ERR_UNSUPPORTED for
+ *   self_mask < 1e4.  The kernels give a token's own key weight zero whenever
+ *   the token has another target, and treat a token whose total
+ *   log-partition is below -self_mask/2 as its own only target; both are
+ *   exact in fp32 while self_mask > 2*scale*|q_i| + log(n_rounds) + 17 for
+ *   every row (App. A sets the self mask to 1e5).
  * Supported on the GPU: d = 64, chunk = 64 (and chunk = 128, the length of the
  *   paper's usual configuration, Sec. 5, on the fp32 forward; entry points that
  *   do not use the chunk ignore it), 2 <= n_buckets <= 1024 (even),
@@ -141,33 +153,36 @@ int lsh_gather_rows(const lsh_config *cfg, lsh_dtype dtype, const void *src,
  * rounds in which j shares i's bucket).
  *   q, v          [B][H][L][d] (dtype), in original position order
  *   buckets, perm, bucket_start: as written by lsh_hash / lsh_sort_permute
- *   o_rounds      [B][H][n_rounds][L][d] (dtype, written, sorted order): each
- *                 round's output is normalised and accumulated in fp32, then
- *                 stored in the call's dtype
+ *   o_rounds      [B][H][n_rounds][L][d] (written, sorted order): each round's
+ *                 output, accumulated and normalised in fp32, stored as fp32
+ *                 (fp32 calls) or as fp16 scaled by 2^-o_exp (bf16 calls)
+ *   o_exp         [B][H][n_rounds][L] uint8 (written; bf16 calls, where it must
+ *                 not be NULL; ignored and may be NULL for fp32 calls)
  *   lse_rounds    [B][H][n_rounds][L] fp32 (written, sorted order)
  *   workspace     >= lsh_workspace_bytes(cfg, dtype, LSH_OP_ATTN_FWD) bytes
  *                 (per-token key scales and packed bucket ids for bf16 calls;
  *                 0 bytes, and workspace may be NULL, for fp32 calls) */
 int lsh_chunk_attn_fwd(const lsh_config *cfg, lsh_dtype dtype, const void *q, const void *v,
                        const int32_t *buckets, const int32_t *perm,
-                       const int32_t *bucket_start, void *o_rounds, float *lse_rounds,
-                       void *workspace, size_t workspace_bytes, void *stream);
+                       const int32_t *bucket_start, void *o_rounds, uint8_t *o_exp,
+                       float *lse_rounds, void *workspace, size_t workspace_bytes,
+                       void *stream);
 
 /* Undo the sort and combine the rounds (App. A):
  *   z_i = log sum_r exp z_r(i),  out_i = sum_r exp(z_r(i) - z_i) o_r(i).
- *   o_rounds, lse_rounds: as written by lsh_chunk_attn_fwd (o_rounds in dtype);
- *                 the weighted sum is formed in fp32
+ *   o_rounds, o_exp, lse_rounds: as written by lsh_chunk_attn_fwd (o_exp
+ *                 required for bf16 calls); the weighted sum is formed in fp32
  *   undo          [B][H][n_rounds][L] int32
  *   out           [B][H][L][d] (dtype, written)
  *   lse_total     [B][H][L] fp32 (written; may be NULL) */
 int lsh_combine_rounds(const lsh_config *cfg, lsh_dtype dtype, const void *o_rounds,
-                       const float *lse_rounds, const int32_t *undo, void *out,
-                       float *lse_total, void *stream);
+                       const uint8_t *o_exp, const float *lse_rounds, const int32_t *undo,
+                       void *out, float *lse_total, void *stream);
 
 /* The whole forward: lsh_hash, lsh_sort_permute, lsh_chunk_attn_fwd and
  * lsh_combine_rounds in sequence on one stream.  buckets, perm, undo and
- * bucket_start are outputs because the backward needs them; o_rounds and
- * lse_rounds live in the workspace.
+ * bucket_start are outputs because the backward needs them; o_rounds, o_exp
+ * and lse_rounds live in the workspace.
  *   workspace >= lsh_workspace_bytes(cfg, dtype, LSH_OP_FORWARD) */
 int lsh_attention_fwd(const lsh_config *cfg, lsh_dtype dtype, const void *q, const void *v,
                       const float *R, void *out, float *lse_total, int32_t *buckets,

@@ -40,8 +40,19 @@
 // the wave's logit bound B_i = scale*log2(e)*|q_i| is moderate: every logit
 // lies in [-B_i - log2 n_r, B_i], so for B_i <= 60 exp2(x) itself neither
 // overflows nor underflows; waves with a larger bound fall back to the online
-// maximum.  The row sum l_i adds the fp32 weights (P V takes them rounded to
-// bf16), so the log-partition is exact to fp32.
+// maximum.  The row sum l_i adds the fp32 weights, so the log-partition is
+// exact to fp32.  P V takes the weights rounded to bf16, and the output is
+// normalised by the sum of those same rounded weights (one more matrix
+// product with an all-ones operand), so the weights applied to the values
+// sum to one: a query with a single target returns that value unchanged and
+// the weight rounding only moves the output by a fraction of the spread of
+// its values.
+//
+// Each round's output row is stored as fp16 (11 significant bits, the same
+// bytes as bf16) scaled by 2^-e, with e = 0 unless the row's largest
+// magnitude reaches 2^15 (then e brings it below 2^15); e goes to a byte per
+// row.  With 11 bits the only rounding of bf16 size left on the way to the
+// combined output is the output's own.
 #include "attn_common.h"
 #include "launch.h"
 
@@ -124,8 +135,8 @@ template <int NW, bool CAUSAL>
 __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ v, const uint32_t* __restrict__ rec,
     const int32_t* __restrict__ perm, uint16_t* __restrict__ o_rounds,
-    float* __restrict__ lse_rounds, int L, int n_r, float scale, float self_mask,
-    int chunks_per_strip) {
+    uint8_t* __restrict__ o_exp, float* __restrict__ lse_rounds, int L, int n_r, float scale,
+    float self_mask, int chunks_per_strip) {
     __shared__ __attribute__((aligned(16))) FwdShared<NW> S;
     constexpr int SW = FwdSig<NW>::stride, RW = FwdSig<NW>::rec_words;
 
@@ -198,13 +209,17 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
     // stores) then finds them long completed.
     uint2 out_pend[4] = {};
     float lse_pend = 0.f;
+    uint32_t exp_pend = 0;
     int64_t row_pend = -1;
     auto flush = [&]() {
         if (row_pend >= 0) {
             uint16_t* orow = o_rounds + row_pend * kHeadDim + 4 * g;
 #pragma unroll
             for (int b = 0; b < 4; ++b) *reinterpret_cast<uint2*>(orow + 16 * b) = out_pend[b];
-            if (g == 0) lse_rounds[row_pend] = lse_pend;
+            if (g == 0) {
+                lse_rounds[row_pend] = lse_pend;
+                o_exp[row_pend] = (uint8_t)exp_pend;
+            }
         }
     };
 
@@ -288,7 +303,9 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
         auto attend = [&](auto fast_tag) {
             constexpr bool FAST = decltype(fast_tag)::value;
             float m = -__builtin_inff(), lsum = 0.f;
-            f32x4 oacc[4] = {f32x4{}, f32x4{}, f32x4{}, f32x4{}};
+            // oacc[0..3]: O^T by 16-dim blocks; oacc[4]: the sum of the bf16
+            // weights (every register of a lane holds its query's sum)
+            f32x4 oacc[5] = {f32x4{}, f32x4{}, f32x4{}, f32x4{}, f32x4{}};
 #pragma unroll
             for (int kt = 0; kt < 8; ++kt) {
                 if (!act[kt]) continue;
@@ -321,7 +338,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
                     const float corr = __builtin_amdgcn_exp2f(m - off);
                     lsum *= corr;
 #pragma unroll
-                    for (int b = 0; b < 4; ++b) oacc[b] *= corr;
+                    for (int b = 0; b < 5; ++b) oacc[b] *= corr;
                     m = m_new;
                 }
                 uint32_t pw[2];
@@ -338,6 +355,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
                 const bf16x4 pk = __builtin_bit_cast(bf16x4, make_uint2(pw[0], pw[1]));
 #pragma unroll
                 for (int b = 0; b < 4; ++b) oacc[b] = mfma16x16x16(vt_read(S.Vs + vofs[ch][b] + roff * 128), pk, oacc[b]);
+                oacc[4] = mfma16x16x16(kOnes4, pk, oacc[4]);
             }
             lsum += __shfl_xor(lsum, 16);
             lsum += __shfl_xor(lsum, 32);
@@ -356,14 +374,28 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
                 for (int b = 0; b < 4; ++b) oacc[b] = mfma16x16x16(vt_read(S.Vs + vofs[1][b] + 16 * wave * 128), pk, oacc[b]);
             }
             const float mref = FAST ? 0.f : m;
-            // 1/l to within 1 ulp; the result is rounded to bf16.  A lone
-            // query divides its exact v_i by 1.
-            const float inv = alone ? 1.f : __builtin_amdgcn_rcpf(lsum);
+            // normalised by the sum of the bf16 weights P V used (1/l to
+            // within 1 ulp); a lone query divides its exact v_i by 1
+            const float inv = alone ? 1.f : __builtin_amdgcn_rcpf(oacc[4][0]);
+            float amax = 0.f;
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
-                out_pend[b].x = pack_bf16x2(oacc[b][0] * inv, oacc[b][1] * inv);
-                out_pend[b].y = pack_bf16x2(oacc[b][2] * inv, oacc[b][3] * inv);
+                oacc[b] *= inv;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) amax = fmaxf(amax, fabsf(oacc[b][e]));
             }
+            amax = fmaxf(amax, __shfl_xor(amax, 16));
+            amax = fmaxf(amax, __shfl_xor(amax, 32));
+            // 2^(E-127) <= amax < 2^(E-126): e = max(0, E - 141) puts the
+            // scaled row below 2^15, inside fp16's range
+            const int ex = max(0, (int)((__float_as_uint(amax) >> 23) & 0xFFu) - 141);
+            const float sc = __uint_as_float((uint32_t)(127 - ex) << 23);
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                out_pend[b].x = pack_f16x2(oacc[b][0] * sc, oacc[b][1] * sc);
+                out_pend[b].y = pack_f16x2(oacc[b][2] * sc, oacc[b][3] * sc);
+            }
+            exp_pend = (uint32_t)ex;
             // z = scale*|q_i| - self_mask when the token is its own only target
             lse_pend = alone ? bound * kLn2 - self_mask : (mref + __log2f(lsum)) * kLn2;
             row_pend = s_q < L ? seg * L + s_q : -1;
@@ -520,7 +552,7 @@ __global__ __launch_bounds__(256) void attn_prep_kernel(const uint16_t* __restri
 
 template <int NW>
 hipError_t launch_bf16(bool causal, const uint16_t* q, const uint16_t* v, const int32_t* buckets,
-                       const int32_t* perm, uint16_t* o, float* lse, int64_t BH, int L, int n_r,
+                       const int32_t* perm, uint16_t* o, uint8_t* o_exp, float* lse, int64_t BH, int L, int n_r,
                        float scale, float self_mask, void* workspace, hipStream_t stream) {
     const int64_t rows = BH * L;
     uint32_t* rec = static_cast<uint32_t*>(workspace);
@@ -533,11 +565,11 @@ hipError_t launch_bf16(bool causal, const uint16_t* q, const uint16_t* v, const 
     const int cps = (int)std::max<int64_t>(1, std::min<int64_t>(16, n_chunks * segs / 3072));
     const dim3 grid((unsigned)((n_chunks + cps - 1) / cps), (unsigned)segs);
     if (causal)
-        attn_fwd_bf16_kernel<NW, true><<<grid, 256, 0, stream>>>(q, v, rec, perm, o, lse, L, n_r, scale,
-                                                                 self_mask, cps);
+        attn_fwd_bf16_kernel<NW, true><<<grid, 256, 0, stream>>>(q, v, rec, perm, o, o_exp, lse, L, n_r,
+                                                                 scale, self_mask, cps);
     else
-        attn_fwd_bf16_kernel<NW, false><<<grid, 256, 0, stream>>>(q, v, rec, perm, o, lse, L, n_r, scale,
-                                                                  self_mask, cps);
+        attn_fwd_bf16_kernel<NW, false><<<grid, 256, 0, stream>>>(q, v, rec, perm, o, o_exp, lse, L, n_r,
+                                                                  scale, self_mask, cps);
     return hipGetLastError();
 }
 
@@ -559,8 +591,8 @@ size_t attn_fwd_workspace_bytes(int64_t BH, int L, int n_rounds, bool f32) {
 hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, int chunk, bool causal,
                            float scale, float self_mask, bool f32, const void* q, const void* v,
                            const int32_t* buckets, const int32_t* perm,
-                           const int32_t* bucket_start, void* o_rounds, float* lse_rounds,
-                           void* workspace, hipStream_t stream) {
+                           const int32_t* bucket_start, void* o_rounds, uint8_t* o_exp,
+                           float* lse_rounds, void* workspace, hipStream_t stream) {
     if (BH == 0 || L == 0) return hipSuccess;
     const unsigned segs = (unsigned)(BH * n_rounds);
     if (f32) {
@@ -583,7 +615,7 @@ hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, int c
     const int nw = n_rounds == 1 ? 0 : (n_rounds + 1) / 2;
 #define LSH_FWD_CASE(W)                                                                             \
     case W:                                                                                         \
-        return launch_bf16<W>(causal, qb, vb, buckets, perm, ob, lse_rounds, BH, L, n_rounds, scale, \
+        return launch_bf16<W>(causal, qb, vb, buckets, perm, ob, o_exp, lse_rounds, BH, L, n_rounds, scale, \
                               self_mask, workspace, stream);
     switch (nw) {
         LSH_FWD_CASE(0)

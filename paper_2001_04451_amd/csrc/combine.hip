@@ -1,7 +1,9 @@
 // Undo the per-round sort and combine the rounds (Reformer App. A):
 //   z_i = log sum_r exp z_r(i),   o_i = sum_r exp(z_r(i) - z_i) o_r(i).
 // The scatter back to position order is done as a gather through `undo`, so
-// every write is a contiguous output row.
+// every write is a contiguous output row.  For bf16 calls the per-round rows
+// are fp16 scaled by 2^-e (e one byte per row); 2^e is folded into the
+// round's weight.
 #include "common.h"
 #include "launch.h"
 
@@ -16,7 +18,7 @@ constexpr int kMaxRounds = 16;
 // p + 8 when n_r > 8): its slot from undo, its log-partition z_r, and after
 // a max / sum across the group (shuffles) its weight exp(z_r - z), formed as
 // exp(z_r - max_r z_r) / sum so that it is exact at any magnitude of z.  Then
-// every lane takes 8 of the row's 64 values (16 bytes of bf16, two float4
+// every lane takes 8 of the row's 64 values (16 bytes of fp16, two float4
 // of fp32) from all rounds, with the slots and weights of the other rounds
 // read from their lanes.  The code is straight-line for every n_r: rounds
 // past n_r read a valid slot and get weight 0, so each lane's loads are all
@@ -26,6 +28,7 @@ constexpr int kMaxRounds = 16;
 // formed in fp32.  NRL is n_r rounded up to a power of two.
 template <bool F32, int NRL>
 __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o_rounds,
+                                                      const uint8_t* __restrict__ o_exp,
                                                       const float* __restrict__ lse_rounds,
                                                       const int32_t* __restrict__ undo,
                                                       void* __restrict__ out,
@@ -45,6 +48,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o
     // this lane's rounds: part and part + 8
     int u[RPL];
     float zr[RPL];
+    uint32_t ex[RPL];
     bool live[RPL];
 #pragma unroll
     for (int k = 0; k < RPL; ++k) {
@@ -53,6 +57,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o
         const int rc = min(r, n_r - 1);
         u[k] = min(max(undo[(seg0 + rc) * L + i], 0), L - 1);
         zr[k] = lse_rounds[(seg0 + rc) * L + u[k]];
+        ex[k] = F32 ? 0u : min((uint32_t)o_exp[(seg0 + rc) * L + u[k]], 126u);
     }
     float zmax = -__builtin_inff();
 #pragma unroll
@@ -72,7 +77,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o
     const float inv_sum = 1.f / sum;
     float wk[RPL];
 #pragma unroll
-    for (int k = 0; k < RPL; ++k) wk[k] = live[k] ? expf(zr[k] - zmax) * inv_sum : 0.f;
+    for (int k = 0; k < RPL; ++k)  // times 2^e, the scale of the stored row
+        wk[k] = live[k] ? expf(zr[k] - zmax) * inv_sum * __uint_as_float((127u + ex[k]) << 23) : 0.f;
 
     // every round's slot and weight in every lane of the group (rounds
     // n_r .. NRL-1 read round n_r - 1's row with weight 0)
@@ -113,8 +119,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o
         for (int r = 0; r < NR; ++r)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                acc[2 * e] = fmaf(w[r], bf16_bits_to_f32(o[r][e] & 0xFFFFu), acc[2 * e]);
-                acc[2 * e + 1] = fmaf(w[r], __uint_as_float(o[r][e] & 0xFFFF0000u), acc[2 * e + 1]);
+                acc[2 * e] = fmaf(w[r], f16_bits_to_f32(o[r][e] & 0xFFFFu), acc[2 * e]);
+                acc[2 * e + 1] = fmaf(w[r], f16_bits_to_f32(o[r][e] >> 16), acc[2 * e + 1]);
             }
         u32x4 packed;
 #pragma unroll
@@ -127,7 +133,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o
 }  // namespace
 
 hipError_t launch_combine(int64_t BH, int L, int n_rounds, bool f32, const void* o_rounds,
-                          const float* lse_rounds, const int32_t* undo, void* out,
+                          const uint8_t* o_exp, const float* lse_rounds, const int32_t* undo, void* out,
                           float* lse_total, hipStream_t stream) {
     const int64_t rows = BH * L;
     if (rows == 0) return hipSuccess;
@@ -135,7 +141,7 @@ hipError_t launch_combine(int64_t BH, int L, int n_rounds, bool f32, const void*
     if (n_rounds > kMaxRounds) return hipErrorInvalidValue;
     auto go = [&](auto f32_tag, auto nrl_tag) {
         combine_kernel<decltype(f32_tag)::value, decltype(nrl_tag)::value><<<grid, 256, 0, stream>>>(
-            o_rounds, lse_rounds, undo, out, lse_total, rows, L, n_rounds);
+            o_rounds, o_exp, lse_rounds, undo, out, lse_total, rows, L, n_rounds);
     };
     auto by_rounds = [&](auto f32_tag) {
         if (n_rounds <= 1) go(f32_tag, std::integral_constant<int, 1>{});

@@ -12,6 +12,13 @@ namespace {
 
 constexpr int64_t kMaxElems = (int64_t)1 << 31;
 
+// Smallest self_mask the kernels accept.  They give a token's own key weight
+// zero whenever it has another target, and treat a row whose total
+// log-partition is below -self_mask/2 as its own only target; both are exact
+// in fp32 while self_mask > 2*scale*|q_i| + log(n_rounds) + 17 for every row,
+// which at this minimum holds for scale*|q_i| up to about 4,990.
+constexpr float kMinSelfMask = 1e4f;
+
 bool finitef(float x) { return std::isfinite(x); }
 
 // Shape checks shared by every entry point.
@@ -41,6 +48,11 @@ int check_supported(const lsh_config* cfg) {
 
 int64_t bh_of(const lsh_config* cfg) { return (int64_t)cfg->B * cfg->H; }
 
+// The attention entry points need self_mask >= kMinSelfMask.
+int check_self_mask(const lsh_config* cfg) {
+    return cfg->self_mask >= kMinSelfMask ? LSH_OK : LSH_ERR_UNSUPPORTED;
+}
+
 // Chunk lengths of the chunked-attention kernels: 64 everywhere, and 128 on
 // the fp32 forward.
 int check_chunk(const lsh_config* cfg, int dtype, bool backward) {
@@ -59,6 +71,7 @@ int check_dense_config(const lsh_config* cfg) {
 
 int check_dense_supported(const lsh_config* cfg, int dtype) {
     if (dtype != LSH_BF16 || cfg->d != lsh::kHeadDimHost) return LSH_ERR_UNSUPPORTED;
+    if (check_self_mask(cfg) != LSH_OK) return LSH_ERR_UNSUPPORTED;
     const int64_t BH = (int64_t)cfg->B * cfg->H;
     if (BH >= 65536 || BH * cfg->L >= kMaxElems) return LSH_ERR_UNSUPPORTED;
     return LSH_OK;
@@ -73,12 +86,21 @@ bool all_aligned(P... p) {
 
 int status_of(hipError_t e) { return e == hipSuccess ? LSH_OK : LSH_ERR_HIP; }
 
+// bytes of one o_rounds value: fp32 for fp32 calls, fp16 for bf16 calls
 size_t elem_bytes(lsh_dtype dtype) { return dtype == LSH_F32 ? 4 : 2; }
 
-// o_rounds (dtype) then lse_rounds (fp32), each 256-byte aligned
+// o_rounds, then o_exp (bf16 calls only), then lse_rounds (fp32), each
+// 256-byte aligned
+size_t rounds_bytes(const lsh_config* cfg, lsh_dtype dtype) {
+    const size_t rr = (size_t)bh_of(cfg) * cfg->n_rounds * cfg->L;
+    return lsh::align256(rr * cfg->d * elem_bytes(dtype));
+}
+size_t exp_bytes(const lsh_config* cfg, lsh_dtype dtype) {
+    return dtype == LSH_F32 ? 0 : lsh::align256((size_t)bh_of(cfg) * cfg->n_rounds * cfg->L);
+}
 size_t fwd_rounds_bytes(const lsh_config* cfg, lsh_dtype dtype) {
     const size_t rr = (size_t)bh_of(cfg) * cfg->n_rounds * cfg->L;
-    return lsh::align256(rr * cfg->d * elem_bytes(dtype)) + lsh::align256(rr * sizeof(float));
+    return rounds_bytes(cfg, dtype) + exp_bytes(cfg, dtype) + lsh::align256(rr * sizeof(float));
 }
 
 #define LSH_TRY(expr)              \
@@ -166,35 +188,38 @@ int lsh_gather_rows(const lsh_config* cfg, lsh_dtype dtype, const void* src, con
 
 int lsh_chunk_attn_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, const void* v,
                        const int32_t* buckets, const int32_t* perm, const int32_t* bucket_start,
-                       void* o_rounds, float* lse_rounds, void* workspace,
+                       void* o_rounds, uint8_t* o_exp, float* lse_rounds, void* workspace,
                        size_t workspace_bytes, void* stream) {
     LSH_TRY(check_config(cfg));
     LSH_TRY(check_dtype(dtype));
     if (!q || !v || !buckets || !perm || !bucket_start || !o_rounds || !lse_rounds)
         return LSH_ERR_INVALID;
+    if (dtype == LSH_BF16 && !o_exp) return LSH_ERR_INVALID;
     if (!all_aligned(q, v, o_rounds)) return LSH_ERR_INVALID;
     const size_t need = lsh_workspace_bytes(cfg, dtype, LSH_OP_ATTN_FWD);
     if (need > 0 && (!workspace || workspace_bytes < need || !all_aligned(workspace)))
         return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
     LSH_TRY(check_chunk(cfg, dtype, false));
+    LSH_TRY(check_self_mask(cfg));
     return status_of(lsh::launch_attn_fwd(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets, cfg->chunk,
                                           cfg->causal != 0, cfg->scale, cfg->self_mask,
                                           dtype == LSH_F32, q, v, buckets, perm, bucket_start,
-                                          o_rounds, lse_rounds, workspace,
+                                          o_rounds, o_exp, lse_rounds, workspace,
                                           static_cast<hipStream_t>(stream)));
 }
 
 int lsh_combine_rounds(const lsh_config* cfg, lsh_dtype dtype, const void* o_rounds,
-                       const float* lse_rounds, const int32_t* undo, void* out, float* lse_total,
-                       void* stream) {
+                       const uint8_t* o_exp, const float* lse_rounds, const int32_t* undo,
+                       void* out, float* lse_total, void* stream) {
     LSH_TRY(check_config(cfg));
     LSH_TRY(check_dtype(dtype));
     if (!o_rounds || !lse_rounds || !undo || !out) return LSH_ERR_INVALID;
+    if (dtype == LSH_BF16 && !o_exp) return LSH_ERR_INVALID;
     if (!all_aligned(o_rounds, out)) return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
     return status_of(lsh::launch_combine(bh_of(cfg), cfg->L, cfg->n_rounds, dtype == LSH_F32,
-                                         o_rounds, lse_rounds, undo, out, lse_total,
+                                         o_rounds, o_exp, lse_rounds, undo, out, lse_total,
                                          static_cast<hipStream_t>(stream)));
 }
 
@@ -209,17 +234,19 @@ int lsh_attention_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, con
     if (workspace_bytes < lsh_workspace_bytes(cfg, dtype, LSH_OP_FORWARD)) return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
     LSH_TRY(check_chunk(cfg, dtype, false));
-    const size_t rr = (size_t)bh_of(cfg) * cfg->n_rounds * cfg->L;
+    LSH_TRY(check_self_mask(cfg));
     char* ws = static_cast<char*>(workspace);
     void* o_rounds = ws;
-    float* lse_rounds = reinterpret_cast<float*>(ws + lsh::align256(rr * cfg->d * elem_bytes(dtype)));
+    uint8_t* o_exp = dtype == LSH_F32 ? nullptr : reinterpret_cast<uint8_t*>(ws + rounds_bytes(cfg, dtype));
+    float* lse_rounds =
+        reinterpret_cast<float*>(ws + rounds_bytes(cfg, dtype) + exp_bytes(cfg, dtype));
     void* scratch = ws + fwd_rounds_bytes(cfg, dtype);
     const size_t scratch_bytes = workspace_bytes - fwd_rounds_bytes(cfg, dtype);
     LSH_TRY(lsh_hash(cfg, dtype, q, R, buckets, scratch, scratch_bytes, stream));
     LSH_TRY(lsh_sort_permute(cfg, buckets, perm, undo, bucket_start, scratch, scratch_bytes, stream));
-    LSH_TRY(lsh_chunk_attn_fwd(cfg, dtype, q, v, buckets, perm, bucket_start, o_rounds, lse_rounds,
-                               scratch, scratch_bytes, stream));
-    return lsh_combine_rounds(cfg, dtype, o_rounds, lse_rounds, undo, out, lse_total, stream);
+    LSH_TRY(lsh_chunk_attn_fwd(cfg, dtype, q, v, buckets, perm, bucket_start, o_rounds, o_exp,
+                               lse_rounds, scratch, scratch_bytes, stream));
+    return lsh_combine_rounds(cfg, dtype, o_rounds, o_exp, lse_rounds, undo, out, lse_total, stream);
 }
 
 int lsh_chunk_attn_bwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, const void* v,
@@ -232,10 +259,12 @@ int lsh_chunk_attn_bwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, co
     if (!q || !v || !out || !dout || !lse_total || !buckets || !perm || !undo || !bucket_start ||
         !dq || !dv || !workspace)
         return LSH_ERR_INVALID;
+    if (!all_aligned(q, v, out, dout, dq, dv, workspace)) return LSH_ERR_INVALID;
     if (workspace_bytes < lsh::bwd_workspace_bytes(bh_of(cfg), cfg->L, cfg->n_rounds))
         return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
     LSH_TRY(check_chunk(cfg, dtype, true));
+    LSH_TRY(check_self_mask(cfg));
     if (dtype != LSH_BF16) return LSH_ERR_UNSUPPORTED;
     return status_of(lsh::launch_attn_bwd(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets,
                                           cfg->causal != 0, cfg->scale, cfg->self_mask, q, v, out,

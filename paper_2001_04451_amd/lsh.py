@@ -73,8 +73,8 @@ def lib() -> ctypes.CDLL:
             "lsh_hash": [_CFG, _I, _P, _P, _P, _P, _SZ, _P],
             "lsh_sort_permute": [_CFG, _P, _P, _P, _P, _P, _SZ, _P],
             "lsh_gather_rows": [_CFG, _I, _P, _P, _P, _P],
-            "lsh_chunk_attn_fwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
-            "lsh_combine_rounds": [_CFG, _I, _P, _P, _P, _P, _P, _P],
+            "lsh_chunk_attn_fwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
+            "lsh_combine_rounds": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P],
             "lsh_attention_fwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
             "lsh_chunk_attn_bwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ,
                                    _P],
@@ -210,49 +210,72 @@ def lsh_gather_rows(cfg: Config, src: torch.Tensor, perm: torch.Tensor) -> torch
     return dst
 
 
-def lsh_chunk_attn_fwd(cfg: Config, q, v, buckets, perm, bstart, o_rounds=None, lse_rounds=None,
-                       workspace=None):
-    """Per-round outputs o_rounds [B,H,n_r,L,d] (q's dtype) and lse_rounds [B,H,n_r,L]
-    (fp32), sorted order."""
+def rounds_dtype(dtype: torch.dtype) -> torch.dtype:
+    """Element type of o_rounds for a call in `dtype`: fp32 for fp32 calls, fp16
+    (each row scaled by 2^-o_exp) for bf16 calls."""
+    return torch.float32 if dtype == torch.float32 else torch.float16
+
+
+def lsh_chunk_attn_fwd(cfg: Config, q, v, buckets, perm, bstart, o_rounds=None, o_exp=None,
+                       lse_rounds=None, workspace=None):
+    """Per-round outputs in sorted order (lsh_chunk_attn_fwd): o_rounds [B,H,n_r,L,d]
+    (fp32 for fp32 q; fp16 scaled by 2^-o_exp for bf16 q), o_exp [B,H,n_r,L] uint8
+    (None for fp32 q) and lse_rounds [B,H,n_r,L] fp32."""
     _need(q, (cfg.B, cfg.H, cfg.L, cfg.d), name="q")
     _need(v, (cfg.B, cfg.H, cfg.L, cfg.d), q.dtype, "v")
     _need(perm, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.int32, "perm")
     _need(bstart, (cfg.B, cfg.H, cfg.n_rounds, cfg.n_buckets + 1), torch.int32, "bucket_start")
     _need(buckets, (cfg.B, cfg.H, cfg.L, cfg.n_rounds), torch.int32, "buckets")
     dev = q.device
+    rdt = rounds_dtype(q.dtype)
     if o_rounds is None:
-        o_rounds = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.L, cfg.d), dtype=q.dtype,
+        o_rounds = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.L, cfg.d), dtype=rdt,
                                device=dev)
-    _need(o_rounds, (cfg.B, cfg.H, cfg.n_rounds, cfg.L, cfg.d), q.dtype, "o_rounds")
+    _need(o_rounds, (cfg.B, cfg.H, cfg.n_rounds, cfg.L, cfg.d), rdt, "o_rounds")
+    if q.dtype != torch.float32:
+        if o_exp is None:
+            o_exp = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.L), dtype=torch.uint8,
+                                device=dev)
+        _need(o_exp, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.uint8, "o_exp")
+    else:
+        o_exp = None
     if lse_rounds is None:
         lse_rounds = torch.empty((cfg.B, cfg.H, cfg.n_rounds, cfg.L), dtype=torch.float32,
                                  device=dev)
+    _need(lse_rounds, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.float32, "lse_rounds")
     if workspace is None:
         workspace = _workspace(cfg, q.dtype, LSH_OP_ATTN_FWD, dev)
     _check("lsh_chunk_attn_fwd",
            lib().lsh_chunk_attn_fwd(ctypes.byref(cfg.c()), _dtype_code(q), _ptr(q), _ptr(v),
                                     _ptr(buckets), _ptr(perm), _ptr(bstart), _ptr(o_rounds),
-                                    _ptr(lse_rounds), _ptr(workspace), workspace.numel(),
-                                    _stream(dev)))
-    return o_rounds, lse_rounds
+                                    _ptr(o_exp), _ptr(lse_rounds), _ptr(workspace),
+                                    workspace.numel(), _stream(dev)))
+    return o_rounds, o_exp, lse_rounds
 
 
-def lsh_combine_rounds(cfg: Config, o_rounds, lse_rounds, undo, out_dtype: torch.dtype,
-                   out=None, lse_total=None):
-    """Output [B,H,L,d] and lse_total [B,H,L] fp32 (lsh_combine_rounds).  o_rounds and the
-    output share the call's dtype (out_dtype)."""
-    _need(o_rounds, (cfg.B, cfg.H, cfg.n_rounds, cfg.L, cfg.d), out_dtype, "o_rounds")
+def lsh_combine_rounds(cfg: Config, o_rounds, o_exp, lse_rounds, undo, out_dtype: torch.dtype,
+                       out=None, lse_total=None):
+    """Output [B,H,L,d] in out_dtype and lse_total [B,H,L] fp32 (lsh_combine_rounds).
+    o_rounds, o_exp and lse_rounds as lsh_chunk_attn_fwd writes them for a call in
+    out_dtype."""
+    _need(o_rounds, (cfg.B, cfg.H, cfg.n_rounds, cfg.L, cfg.d), rounds_dtype(out_dtype),
+          "o_rounds")
+    if out_dtype != torch.float32:
+        if o_exp is None:
+            raise ValueError("o_exp is required for bf16 calls")
+        _need(o_exp, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.uint8, "o_exp")
     _need(lse_rounds, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.float32, "lse_rounds")
     _need(undo, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.int32, "undo")
     dev = o_rounds.device
     if out is None:
         out = torch.empty((cfg.B, cfg.H, cfg.L, cfg.d), dtype=out_dtype, device=dev)
+    _need(out, (cfg.B, cfg.H, cfg.L, cfg.d), out_dtype, "out")
     if lse_total is None:
         lse_total = torch.empty((cfg.B, cfg.H, cfg.L), dtype=torch.float32, device=dev)
     _check("lsh_combine_rounds",
            lib().lsh_combine_rounds(ctypes.byref(cfg.c()), _dtype_code(out), _ptr(o_rounds),
-                                    _ptr(lse_rounds), _ptr(undo), _ptr(out), _ptr(lse_total),
-                                    _stream(dev)))
+                                    _ptr(o_exp), _ptr(lse_rounds), _ptr(undo), _ptr(out),
+                                    _ptr(lse_total), _stream(dev)))
     return out, lse_total
 
 
@@ -295,11 +318,17 @@ def lsh_chunk_attn_bwd(cfg: Config, q, v, out, dout, lse_total, buckets, perm, u
     for name, t in (("v", v), ("out", out), ("dout", dout)):
         _need(t, shp, q.dtype, name)
     _need(lse_total, (cfg.B, cfg.H, cfg.L), torch.float32, "lse_total")
+    _need(buckets, (cfg.B, cfg.H, cfg.L, cfg.n_rounds), torch.int32, "buckets")
+    _need(perm, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.int32, "perm")
+    _need(undo, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.int32, "undo")
+    _need(bstart, (cfg.B, cfg.H, cfg.n_rounds, cfg.n_buckets + 1), torch.int32, "bucket_start")
     dev = q.device
     if dq is None:
         dq = torch.empty(shp, dtype=torch.float32, device=dev)
     if dv is None:
         dv = torch.empty(shp, dtype=torch.float32, device=dev)
+    _need(dq, shp, torch.float32, "dq")
+    _need(dv, shp, torch.float32, "dv")
     if workspace is None:
         workspace = _workspace(cfg, q.dtype, LSH_OP_ATTN_BWD, dev)
     _check("lsh_chunk_attn_bwd",

@@ -33,6 +33,15 @@ def out_tolerance(dtype: str) -> float:
     return 1e-5 if dtype == "f32" else 2e-2
 
 
+def rounds_f64(o_rounds: torch.Tensor, o_exp: torch.Tensor | None) -> np.ndarray:
+    """Per-round outputs as float64: fp32 rows as they are; fp16 rows times
+    2^o_exp (the scale lsh_chunk_attn_fwd applies to bf16 calls)."""
+    o = o_rounds.float().cpu().numpy().astype(np.float64)
+    if o_exp is None:
+        return o
+    return np.ldexp(o, o_exp.cpu().numpy().astype(np.int32)[..., None])
+
+
 def lse_close(gpu: np.ndarray, ref: np.ndarray, dtype: str) -> np.ndarray:
     """Log-partition comparison.  Rows whose only target is themselves sit at
     z ~ -1e5, where one fp32 spacing is 2^-7, so the bound is relative there."""

@@ -57,7 +57,7 @@ def test_invalid_config(L, bad):
     rc = L.lsh_hash(ctypes.byref(c), lsh.LSH_BF16, FAKE, FAKE, FAKE, FAKE, 1 << 30, None)
     assert rc == lsh.LSH_ERR_INVALID
     rc = L.lsh_chunk_attn_fwd(ctypes.byref(c), lsh.LSH_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                              FAKE, FAKE, 1 << 30, None)
+                              FAKE, FAKE, FAKE, 1 << 30, None)
     assert rc == lsh.LSH_ERR_INVALID
     assert L.lsh_workspace_bytes(ctypes.byref(c), lsh.LSH_BF16, lsh.LSH_OP_FORWARD) == 0
 
@@ -71,7 +71,11 @@ def test_null_pointers_and_small_workspace(L):
     assert L.lsh_hash(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, need - 1, None) == lsh.LSH_ERR_INVALID
     assert L.lsh_hash(ctypes.byref(c), 7, FAKE, FAKE, FAKE, FAKE, need, None) == lsh.LSH_ERR_INVALID
     assert L.lsh_sort_permute(ctypes.byref(c), FAKE, None, FAKE, FAKE, FAKE, 1 << 30, None) == lsh.LSH_ERR_INVALID
-    assert L.lsh_combine_rounds(ctypes.byref(c), 1, FAKE, FAKE, None, FAKE, None, None) == lsh.LSH_ERR_INVALID
+    assert L.lsh_combine_rounds(ctypes.byref(c), 1, FAKE, FAKE, FAKE, None, FAKE, None,
+                                None) == lsh.LSH_ERR_INVALID
+    # bf16 calls need the per-row exponents of the fp16 rows; fp32 calls do not
+    assert L.lsh_combine_rounds(ctypes.byref(c), 1, FAKE, None, FAKE, FAKE, FAKE, None,
+                                None) == lsh.LSH_ERR_INVALID
     fwd = L.lsh_workspace_bytes(ctypes.byref(c), 1, lsh.LSH_OP_FORWARD)
     assert L.lsh_attention_fwd(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE,
                                FAKE, FAKE, fwd - 1, None) == lsh.LSH_ERR_INVALID
@@ -79,9 +83,11 @@ def test_null_pointers_and_small_workspace(L):
     attn = L.lsh_workspace_bytes(ctypes.byref(c), 1, lsh.LSH_OP_ATTN_FWD)
     assert attn > 0 and L.lsh_workspace_bytes(ctypes.byref(c), 0, lsh.LSH_OP_ATTN_FWD) == 0
     assert L.lsh_chunk_attn_fwd(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                                FAKE, attn - 1, None) == lsh.LSH_ERR_INVALID
+                                FAKE, FAKE, attn - 1, None) == lsh.LSH_ERR_INVALID
     assert L.lsh_chunk_attn_fwd(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                                None, attn, None) == lsh.LSH_ERR_INVALID
+                                FAKE, None, attn, None) == lsh.LSH_ERR_INVALID
+    assert L.lsh_chunk_attn_fwd(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                FAKE, FAKE, attn, None) == lsh.LSH_ERR_INVALID
 
 
 @pytest.mark.parametrize("unsup", [dict(d=32), dict(chunk=128, L=1024), dict(n_buckets=2048),
@@ -104,9 +110,10 @@ def test_backward_is_bf16_only(L):
 def test_workspace_sizes(L):
     c = _cfg(B=1, H=16, L=65536, n_buckets=1024, n_rounds=8)
     rr = 16 * 65536 * 8
-    # per-round outputs in the call's dtype (bf16 here) plus fp32 log-partitions
+    # per-round outputs (fp16 rows and their exponent bytes for bf16 calls, fp32
+    # rows for fp32 calls) plus fp32 log-partitions
     fwd = L.lsh_workspace_bytes(ctypes.byref(c), 1, lsh.LSH_OP_FORWARD)
-    assert fwd >= rr * 64 * 2 + rr * 4
+    assert fwd >= rr * 64 * 2 + rr + rr * 4
     fwd32 = L.lsh_workspace_bytes(ctypes.byref(c), 0, lsh.LSH_OP_FORWARD)
     assert fwd32 >= rr * 64 * 4 + rr * 4
     assert L.lsh_workspace_bytes(ctypes.byref(c), 0, lsh.LSH_OP_ATTN_FWD) == 0
@@ -158,5 +165,45 @@ def test_chunk_lengths(L):
                                 None) == lsh.LSH_ERR_UNSUPPORTED
     c96 = _cfg(chunk=96)
     assert L.lsh_chunk_attn_fwd(ctypes.byref(c96), lsh.LSH_F32, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                                FAKE, None, 0, None) == lsh.LSH_ERR_UNSUPPORTED
+                                None, FAKE, None, 0, None) == lsh.LSH_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("self_mask", [0.0, 10.0, -1e5, 9999.0])
+def test_self_mask_below_bound(L, self_mask):
+    """The attention calls drop a token's own key whenever it has another target,
+    which is exact only for a large self mask (App. A uses 1e5): below 1e4 they
+    refuse the configuration before any HIP call.  Hash and sort do not read
+    self_mask and accept it."""
+    c = _cfg(self_mask=self_mask)
+    bf = lsh.LSH_BF16
+    fwd = L.lsh_workspace_bytes(ctypes.byref(c), bf, lsh.LSH_OP_FORWARD)
+    assert L.lsh_attention_fwd(ctypes.byref(c), bf, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE,
+                               FAKE, FAKE, fwd, None) == lsh.LSH_ERR_UNSUPPORTED
+    attn = L.lsh_workspace_bytes(ctypes.byref(c), bf, lsh.LSH_OP_ATTN_FWD)
+    assert L.lsh_chunk_attn_fwd(ctypes.byref(c), bf, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                FAKE, attn, None) == lsh.LSH_ERR_UNSUPPORTED
+    bwd = L.lsh_workspace_bytes(ctypes.byref(c), bf, lsh.LSH_OP_ATTN_BWD)
+    assert L.lsh_chunk_attn_bwd(ctypes.byref(c), bf, *([FAKE] * 12), bwd, None) == lsh.LSH_ERR_UNSUPPORTED
+    dense = L.lsh_workspace_bytes(ctypes.byref(c), bf, lsh.LSH_OP_DENSE_FWD)
+    assert L.lsh_dense_attn_fwd(ctypes.byref(c), bf, FAKE, FAKE, FAKE, None, FAKE, dense,
+                                None) == lsh.LSH_ERR_UNSUPPORTED
+    # hash with an undersized workspace: INVALID (validation reached), not UNSUPPORTED
+    assert L.lsh_hash(ctypes.byref(c), bf, FAKE, FAKE, FAKE, FAKE, 0, None) == lsh.LSH_ERR_INVALID
+
+
+def test_backward_alignment(L):
+    """The backward moves rows in 16-byte pieces: a misaligned q, v, out, dout,
+    dq, dv or workspace is refused before any HIP call."""
+    c = _cfg()
+    bf = lsh.LSH_BF16
+    need = L.lsh_workspace_bytes(ctypes.byref(c), bf, lsh.LSH_OP_ATTN_BWD)
+    odd = ctypes.c_void_p(0x1008)
+    # pointer arguments: q, v, out, dout, lse_total, buckets, perm, undo,
+    # bucket_start, dq, dv, workspace
+    for k in (0, 1, 2, 3, 9, 10, 11):
+        args = [FAKE] * 12
+        args[k] = odd
+        rc = L.lsh_chunk_attn_bwd(ctypes.byref(c), bf, *args, need, None)
+        assert rc == lsh.LSH_ERR_INVALID, k
+    assert L.lsh_chunk_attn_bwd(ctypes.byref(c), bf, *([FAKE] * 12), 0, None) == lsh.LSH_ERR_INVALID
 

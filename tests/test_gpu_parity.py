@@ -13,7 +13,7 @@ import oracle
 from paper_2001_04451_amd import lsh
 from paper_2001_04451_amd import workloads as W
 
-from gpu_common import log, lse_close, out_tolerance, small, to_device, torch_dtype
+from gpu_common import log, lse_close, out_tolerance, rounds_f64, small, to_device, torch_dtype
 
 pytestmark = pytest.mark.gpu
 
@@ -96,11 +96,11 @@ def test_chunk_attention_and_combine(gpu, name):
     buckets = torch.from_numpy(ref["buckets"]).cuda()
     log("attn", name, w)
     perm, undo, bstart = lsh.lsh_sort_permute(cfg, buckets)
-    o_r, lse_r = lsh.lsh_chunk_attn_fwd(cfg, q, v, buckets, perm, bstart)
-    out, lse = lsh.lsh_combine_rounds(cfg, o_r, lse_r, undo, torch_dtype(w.dtype))
+    o_r, o_e, lse_r = lsh.lsh_chunk_attn_fwd(cfg, q, v, buckets, perm, bstart)
+    out, lse = lsh.lsh_combine_rounds(cfg, o_r, o_e, lse_r, undo, torch_dtype(w.dtype))
     torch.cuda.synchronize()
     tol = out_tolerance(w.dtype)
-    err_or = np.abs(o_r.float().cpu().numpy() - ref["o_rounds"]).max()
+    err_or = np.abs(rounds_f64(o_r, o_e) - ref["o_rounds"]).max()
     assert err_or <= tol, f"per-round output max-abs error {err_or}"
     assert lse_close(lse_r.cpu().numpy(), ref["lse_rounds"], w.dtype).all()
     got = out.float().cpu().numpy()
@@ -167,7 +167,7 @@ def test_invalid_arguments_on_gpu(gpu):
 
 
 @pytest.mark.parametrize("causal", [True, False])
-@pytest.mark.parametrize("variant", ["large_norm", "duplicates_and_zeros"])
+@pytest.mark.parametrize("variant", ["large_norm", "duplicates_and_zeros", "large_values"])
 def test_attention_edge_inputs(gpu, variant, causal):
     """Attention on edited inputs, with the oracle's bucket ids.
 
@@ -175,15 +175,23 @@ def test_attention_edge_inputs(gpu, variant, causal):
     scale*log2(e)*|q| is far above the range the kernel covers without a
     running maximum; the waves holding such rows take the online-maximum path.
     duplicates_and_zeros: pairs of identical tokens (N_ij = n_r, the largest
-    repeat count) and all-zero rows (zero norm, every logit zero)."""
+    repeat count) and all-zero rows (zero norm, every logit zero).
+    large_values: every value row times 2^17, so the per-round rows pass
+    fp16's range and are stored with a nonzero exponent; the softmax weights
+    do not change, so outputs and their errors scale by 2^17 and so does the
+    tolerance."""
     w = small("mixture_bf16_L4096", B=1, H=2, L=2048, causal=causal)
     x = W.make_inputs(w)
     qf = W.bf16_bits_to_f32(x["q"])
+    scale = 1.0
     if variant == "large_norm":
         qf[:, :, ::5, :] *= 64.0
-    else:
+    elif variant == "duplicates_and_zeros":
         qf[:, :, 1::4, :] = qf[:, :, 0::4, :]
         qf[:, :, 2::16, :] = 0.0
+    else:
+        scale = 2.0 ** 17
+        x["v"] = W.f32_to_bf16_bits(W.bf16_bits_to_f32(x["v"]) * np.float32(scale))
     x["q"] = W.f32_to_bf16_bits(qf)
     q64, v64 = W.as_f64(x["q"], w.dtype), W.as_f64(x["v"], w.dtype)
     ref = oracle.lsh_attention_fwd(q64, v64, x["R"].astype(np.float64), w.chunk, w.causal)
@@ -192,16 +200,20 @@ def test_attention_edge_inputs(gpu, variant, causal):
     buckets = torch.from_numpy(ref["buckets"]).cuda()
     log("attn-edge", variant, w)
     perm, undo, bstart = lsh.lsh_sort_permute(cfg, buckets)
-    o_r, lse_r = lsh.lsh_chunk_attn_fwd(cfg, q, v, buckets, perm, bstart)
-    out, lse = lsh.lsh_combine_rounds(cfg, o_r, lse_r, undo, torch.bfloat16)
+    o_r, o_e, lse_r = lsh.lsh_chunk_attn_fwd(cfg, q, v, buckets, perm, bstart)
+    out, lse = lsh.lsh_combine_rounds(cfg, o_r, o_e, lse_r, undo, torch.bfloat16)
     torch.cuda.synchronize()
-    tol = out_tolerance(w.dtype)
-    err_or = np.abs(o_r.float().cpu().numpy() - ref["o_rounds"]).max()
-    print(f"{variant} causal={causal}: per-round err {err_or:.3e}")
+    tol = out_tolerance(w.dtype) * scale
+    if scale > 1.0:
+        assert (o_e.cpu().numpy() > 0).any()  # the scaled form is exercised
+    err_or = np.abs(rounds_f64(o_r, o_e) - ref["o_rounds"]).max()
+    print(f"{variant} causal={causal}: per-round err {err_or:.3e} (tol {tol:.3g})")
     assert err_or <= tol
     assert lse_close(lse_r.cpu().numpy(), ref["lse_rounds"], w.dtype).all()
     got = out.float().cpu().numpy()
-    assert (np.abs(got - ref["out"]) <= tol + np.abs(ref["out"]) * 2.0 ** -8).all()
+    err = np.abs(got - ref["out"]).max()
+    print(f"{variant} causal={causal}: out max-abs err {err:.3e}")
+    assert err <= tol
     assert lse_close(lse.cpu().numpy(), ref["lse"], w.dtype).all()
 
 
@@ -230,6 +242,21 @@ def test_hash_exact_ties(gpu, dtype):
     assert np.array_equal(got, want)
 
 
+def _rounds_input(o: np.ndarray, dtype: str, rng):
+    """Per-round rows in the format lsh_combine_rounds takes for `dtype`, and
+    their exact float64 values.  For bf16 calls: fp16 rows with a per-row
+    exponent; with `rng`, every 97th row is scaled up by 2^20 and stored with
+    exponent 20 (the form the attention writes for rows past fp16's range)."""
+    if dtype == "f32":
+        return torch.from_numpy(o).cuda(), None, o.astype(np.float64)
+    e = np.zeros(o.shape[:-1], np.uint8)
+    if rng is not None:
+        e.reshape(-1)[::97] = 20
+    h = o.astype(np.float16)
+    o64 = np.ldexp(h.astype(np.float64), e.astype(np.int32)[..., None])
+    return torch.from_numpy(h).cuda(), torch.from_numpy(e).cuda(), o64
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("n_rounds", [3, 6, 9, 16])
 def test_combine_round_counts(gpu, dtype, n_rounds):
@@ -240,22 +267,30 @@ def test_combine_round_counts(gpu, dtype, n_rounds):
     B, H, L, d = 1, 2, 1024, 64
     rng = np.random.default_rng(1000 + n_rounds)
     o = rng.standard_normal((B, H, n_rounds, L, d)).astype(np.float32)
-    if dtype == "bf16":  # round to bf16 first so both sides see the same values
-        o = (torch.from_numpy(o).to(torch.bfloat16).float()).numpy()
     lse_r = (5.0 * rng.standard_normal((B, H, n_rounds, L))).astype(np.float32)
     undo = np.stack([np.stack([np.argsort(rng.permutation(L)) for _ in range(n_rounds)])
                      for _ in range(B * H)]).reshape(B, H, n_rounds, L).astype(np.int32)
-    ref_out, ref_lse = oracle.lsh_combine_rounds(o.astype(np.float64), lse_r.astype(np.float64),
-                                                 undo)
+    o_r, o_e, o64 = _rounds_input(o, dtype, rng)
+    ref_out, ref_lse = oracle.lsh_combine_rounds(o64, lse_r.astype(np.float64), undo)
     cfg = lsh.Config(B=B, H=H, L=L, n_buckets=64, n_rounds=n_rounds)
     tdt = torch_dtype(dtype)
     log("combine", dtype, n_rounds)
-    out, lse = lsh.lsh_combine_rounds(cfg, torch.from_numpy(o).to(tdt).cuda(),
-                                      torch.from_numpy(lse_r).cuda(),
+    out, lse = lsh.lsh_combine_rounds(cfg, o_r, o_e, torch.from_numpy(lse_r).cuda(),
                                       torch.from_numpy(undo).cuda(), tdt)
     torch.cuda.synchronize()
-    err = np.abs(out.float().cpu().numpy() - ref_out).max()
+    got = out.float().cpu().numpy()
+    if o_e is None:
+        big = np.zeros(ref_lse.shape, bool)
+    else:  # tokens with a scaled row in some round: outputs near 2^20
+        e_tok = np.take_along_axis(o_e.cpu().numpy(), undo.astype(np.int64), axis=3)
+        big = (e_tok > 0).any(axis=2)
+    err = np.abs(got - ref_out)[~big].max()
     assert err <= out_tolerance(dtype), f"combine max-abs error {err}"
+    if big.any():
+        # outputs of magnitude ~2^20: one bf16 rounding (2^-8 relative) plus
+        # fp32 accumulation, relative to the row's scale
+        rel = np.abs(got - ref_out)[big] / (2.0 ** -8 * np.abs(ref_out)[big] + 2.0 ** -20 * 2.0 ** 20)
+        assert rel.max() <= 1.0, f"scaled rows: error {rel.max()} of the bound"
     assert lse_close(lse.cpu().numpy(), ref_lse, dtype).all()
 
 
@@ -269,27 +304,24 @@ def test_combine_lone_token_weights(gpu, dtype):
     B, H, L, d, n_rounds = 1, 1, 512, 64, 3
     rng = np.random.default_rng(77)
     o = rng.standard_normal((B, H, n_rounds, L, d)).astype(np.float32)
-    if dtype == "bf16":
-        o = (torch.from_numpy(o).to(torch.bfloat16).float()).numpy()
+    o_r, o_e, o64 = _rounds_input(o, dtype, None)
     base = (-1e5 + 2.0 + rng.standard_normal((B, H, 1, L))).astype(np.float32)
     lse_r = np.repeat(base, n_rounds, axis=2)
     # every fourth token: round 1 has other targets (an ordinary z_r)
     lse_r[:, :, 1, ::4] = rng.standard_normal(L // 4).astype(np.float32)
     undo = np.stack([np.argsort(rng.permutation(L)) for _ in range(n_rounds)]).reshape(
         B, H, n_rounds, L).astype(np.int32)
-    ref_out, ref_lse = oracle.lsh_combine_rounds(o.astype(np.float64), lse_r.astype(np.float64),
-                                                 undo)
+    ref_out, ref_lse = oracle.lsh_combine_rounds(o64, lse_r.astype(np.float64), undo)
     cfg = lsh.Config(B=B, H=H, L=L, n_buckets=64, n_rounds=n_rounds)
     tdt = torch_dtype(dtype)
     log("combine-lone", dtype)
-    out, lse = lsh.lsh_combine_rounds(cfg, torch.from_numpy(o).to(tdt).cuda(),
-                                      torch.from_numpy(lse_r).cuda(),
+    out, lse = lsh.lsh_combine_rounds(cfg, o_r, o_e, torch.from_numpy(lse_r).cuda(),
                                       torch.from_numpy(undo).cuda(), tdt)
     torch.cuda.synchronize()
     diff = np.abs(out.float().cpu().numpy() - ref_out)
-    # bf16 output: one rounding to nearest (half an ulp of an 8-bit
-    # significand: at most 2^-8 relative)
-    bound = 1e-5 if dtype == "f32" else 2.0 ** -8 * np.abs(ref_out) + 1e-6
+    # bf16 output: the weighted mean to fp32 accuracy, then one rounding to
+    # nearest (half an ulp of an 8-bit significand: at most 2^-8 relative)
+    bound = 1e-5 if dtype == "f32" else np.minimum(2.0 ** -8 * np.abs(ref_out) + 1e-6, 2e-2)
     assert (diff <= bound).all(), f"combine max-abs error {diff.max()}"
     assert lse_close(lse.cpu().numpy(), ref_lse, dtype).all()
 
