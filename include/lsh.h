@@ -40,7 +40,8 @@
  *   LSH_ERR_UNSUPPORTED are returned before any HIP call is made, so they can
  *   be tested without a GPU; LSH_ERR_HIP reports a failed launch.  No C++
  *   exception crosses this interface.  The library keeps no mutable global
- *   state, so calls on different streams may run concurrently.
+ *   state (apart from lsh_sort_permute_static's fixed scratch array), so
+ *   calls on different streams may run concurrently.
  * self_mask.  The attention entry points (lsh_chunk_attn_fwd and _bwd,
  *   lsh_attention_fwd, lsh_dense_attn_fwd) return LSH_ERR_UNSUPPORTED for
  *   self_mask < 1e4.  The kernels give a token's own key weight zero whenever
@@ -134,6 +135,20 @@ int lsh_hash(const lsh_config *cfg, lsh_dtype dtype, const void *q, const float 
 int lsh_sort_permute(const lsh_config *cfg, const int32_t *buckets, int32_t *perm,
                      int32_t *undo, int32_t *bucket_start, void *workspace,
                      size_t workspace_bytes, void *stream);
+
+/* lsh_sort_permute without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops).
+ * Its scratch (per-tile bucket counts, 4 * B*H*n_rounds*n_buckets*ceil(L/4096)
+ * bytes) is a fixed 16 MiB device array inside the library, one per GPU,
+ * held until the process ends; its address is looked up on the first call
+ * on each device (the current device).  The call allocates nothing.
+ * Configurations whose counts exceed 16 MiB return LSH_ERR_UNSUPPORTED.
+ * Every call on a GPU shares that GPU's array: calls that may overlap on one
+ * GPU (other streams, other host threads) race and must be serialised by the
+ * caller.  Each call writes every count it reads, so no state carries over
+ * from the previous call.  Arguments and results as lsh_sort_permute. */
+int lsh_sort_permute_static(const lsh_config *cfg, const int32_t *buckets, int32_t *perm,
+                            int32_t *undo, int32_t *bucket_start, void *stream);
 
 /* Gather rows into sorted order (the "chunks of m consecutive queries after
  * sorting" of Sec. 2): dst[b][h][r][s] = src[b][h][perm[b][h][r][s]].

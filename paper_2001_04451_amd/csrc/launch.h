@@ -28,6 +28,12 @@ size_t sort_workspace_bytes(int64_t BH, int L, int n_rounds, int n_buckets);
 hipError_t launch_sort(int64_t BH, int L, int n_rounds, int n_buckets, const int32_t* buckets,
                        int32_t* perm, int32_t* undo, int32_t* bucket_start, void* workspace,
                        hipStream_t stream);
+// The fixed scratch array of lsh_sort_permute_static (sort.hip): its size,
+// and its device address on the current device (looked up on the first call
+// on each device).
+constexpr size_t kSortScratchBytes = (size_t)16 << 20;
+constexpr int kMaxDevices = 64;
+hipError_t sort_static_scratch(void** ptr);
 hipError_t launch_gather(int64_t BH, int L, int n_rounds, bool f32, const void* src,
                          const int32_t* perm, void* dst, hipStream_t stream);
 

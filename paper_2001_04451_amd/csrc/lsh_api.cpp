@@ -175,6 +175,22 @@ int lsh_sort_permute(const lsh_config* cfg, const int32_t* buckets, int32_t* per
                                       static_cast<hipStream_t>(stream)));
 }
 
+int lsh_sort_permute_static(const lsh_config* cfg, const int32_t* buckets, int32_t* perm,
+                            int32_t* undo, int32_t* bucket_start, void* stream) {
+    LSH_TRY(check_config(cfg));
+    if (!buckets || !perm || !undo || !bucket_start) return LSH_ERR_INVALID;
+    LSH_TRY(check_supported(cfg));
+    if (lsh::sort_workspace_bytes(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets) >
+        lsh::kSortScratchBytes)
+        return LSH_ERR_UNSUPPORTED;
+    void* scratch = nullptr;
+    LSH_TRY(status_of(lsh::sort_static_scratch(&scratch)));
+    // the counts are written in full by every call: nothing needs clearing
+    return status_of(lsh::launch_sort(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets, buckets,
+                                      perm, undo, bucket_start, scratch,
+                                      static_cast<hipStream_t>(stream)));
+}
+
 int lsh_gather_rows(const lsh_config* cfg, lsh_dtype dtype, const void* src, const int32_t* perm,
                     void* dst, void* stream) {
     LSH_TRY(check_config(cfg));

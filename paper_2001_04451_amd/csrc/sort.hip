@@ -15,6 +15,8 @@
 #include "common.h"
 #include "launch.h"
 
+#include <mutex>
+
 namespace lsh {
 namespace {
 
@@ -239,6 +241,34 @@ __global__ __launch_bounds__(256) void gather_kernel(const char* __restrict__ sr
 }  // namespace
 
 int sort_tile_positions(int L) { return kTile; }
+
+// Scratch of lsh_sort_permute_static: a fixed device array in this code
+// object, so that call allocates nothing.  Host code never passes `scratch`
+// itself to a kernel (on the host it names a stand-in, not device memory):
+// its device address is looked up once per device with that device current,
+// and that address is what the kernels receive.
+static __device__ __align__(256) char scratch[kSortScratchBytes];
+
+namespace {
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t sort_static_scratch(void** ptr) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return hipSuccess;
+}
 
 size_t sort_workspace_bytes(int64_t BH, int L, int n_rounds, int n_buckets) {
     const int64_t n_tiles = (L + kTile - 1) / kTile;

@@ -32,6 +32,7 @@ LSH_F32, LSH_BF16 = 0, 1
 
 # Every symbol include/lsh.h declares.
 EXPORTED = ("lsh_status_string", "lsh_workspace_bytes", "lsh_hash", "lsh_sort_permute",
+            "lsh_sort_permute_static",
             "lsh_gather_rows", "lsh_chunk_attn_fwd", "lsh_combine_rounds", "lsh_attention_fwd",
             "lsh_chunk_attn_bwd", "lsh_dense_attn_fwd")
 
@@ -72,6 +73,7 @@ def lib() -> ctypes.CDLL:
         sigs = {
             "lsh_hash": [_CFG, _I, _P, _P, _P, _P, _SZ, _P],
             "lsh_sort_permute": [_CFG, _P, _P, _P, _P, _P, _SZ, _P],
+            "lsh_sort_permute_static": [_CFG, _P, _P, _P, _P, _P],
             "lsh_gather_rows": [_CFG, _I, _P, _P, _P, _P],
             "lsh_chunk_attn_fwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
             "lsh_combine_rounds": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P],
