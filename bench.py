@@ -55,7 +55,7 @@ STAGES = {
     "attn": {"kernels": ["attn_prep_kernel", "attn_fwd_bf16_kernel"],
              "sources": ["attn_fwd.hip", "attn_common.h", "common.h"], "bound": "hbm",
              "work": "attn_bytes"},
-    "bwd": {"kernels": ["bwd_prep_kernel", "bwd_fused_kernel", "bwd_reduce_kernel"],
+    "bwd": {"kernels": ["bwd_prep_kernel", "bwd_strip_kernel", "bwd_reduce_kernel"],
             "sources": ["attn_bwd.hip", "attn_common.h", "common.h"], "bound": "hbm",
             "work": "bwd_bytes"},
     "combine": {"kernels": ["combine_kernel"], "sources": ["combine.hip", "common.h"],

@@ -5,492 +5,467 @@
 // perm and the forward's total log-partition z_i, with
 //   P = exp(a - z_i),  dA = P (dO_i . v_j - D_i),  D_i = dO_i . o_i,
 //   dv_j += P dO_i,  dq_i += scale dA k_j,  dk_j += scale dA q_i,
-// and dk flows back through k_j = q_j/|q_j| in the final reduction.
+// and dk flows back through k_j = q_j/|q_j|:
+//   dq_j += (dk_j - (dk_j . k_j) k_j) / |q_j|.
 //
 // Kernels (gfx950):
-//  * bwd_prep:   D_i per position.
-//  * bwd_fused:  per chunk c of a round, one staged window (chunks c-1, c,
-//                c+1).  Two waves take the key role for chunk c's keys
-//                (lanes on keys): S = Q K^T and dP = dO V^T on the matrix
-//                cores against the queries of chunks c and c+1 (the only ones
-//                whose window holds chunk c), then dV^T += dO^T P and
-//                dK^T += Q^T dA.  Two waves take the query role for chunk c's
-//                queries (lanes on queries, as in the forward): S^T = K Q^T,
-//                dP^T = V dO^T over chunks c-1 and c, then dQ^T += K^T dA^T.
-//                The key role hands dK to the query role through LDS, which
-//                adds it through the normalisation Jacobian and writes one
-//                per-round dq partial; the key role writes the dv partial.
-//  * bwd_reduce: per position, sum the rounds through `undo`, write dq, dv.
-// Every (query, key) pair of a round is owned by exactly one lane of each
-// role, so no atomics are used and results are deterministic.
+//  * bwd_prep:   one record per token: its packed bucket ids, its key scale
+//                scale*log2(e)/|q|, its log-partition in log2 units and
+//                D = dO . o.
+//  * bwd_strip:  eight waves walk a strip of chunks of one (batch, head,
+//                round) segment.  Step c takes the queries of chunk c
+//                against the 128 keys of chunks c-1 and c (their whole
+//                window), so every (query, key) pair of the round is met in
+//                exactly one step, and the keys of chunk c meet their last
+//                queries in step c+1.  The rows of chunks c-1 and c sit in
+//                LDS rings (q and v: three slots, dO: two), and chunk c+1 is
+//                gathered into the free slots (through perm, straight from
+//                global memory into LDS) while step c computes.
+//                Pass 1, lanes on keys: each wave owns one 16-key block of
+//                one chunk for the two steps in which that chunk is in the
+//                window.  Per 16x16 tile S = Q K^T and dP = dO V^T on the
+//                matrix cores, then P, dA and dA' = dA * scale/|q_j| per
+//                element; P (as bf16 hi + lo, so dv keeps fp32 accuracy) and
+//                dA are already the B operands of dV^T += dO^T P and
+//                dK^T += Q^T dA, and dA' goes to LDS transposed.
+//                Pass 2, lanes on queries: dQ^T += K^T dA'^T over the window,
+//                with dA'^T read back through the LDS transpose read; dQ goes
+//                to LDS for the step that finishes those tokens as keys.
+//                When a key block's chunk leaves the window its owner adds
+//                dk through the normalisation Jacobian to dQ (the same 16
+//                tokens) and writes the round's partials of dq and dv, in
+//                position order, as fp16 rows scaled by 2^-e (e = 0 unless a
+//                row's largest magnitude reaches 2^15; one byte per row).
+//  * bwd_reduce: per position, the sum over rounds; plus dO for a token that
+//                was its own only target in every round (its weights are
+//                then 1/n_rounds on each round's self entry).
+// Every (query, key) pair of a round is computed once, by one lane, and every
+// sum has a fixed order: no atomics, and the results are deterministic.
 #include "attn_common.h"
 #include "launch.h"
+
+#include <type_traits>
 
 namespace lsh {
 namespace {
 
-constexpr int kWin = 192;  // staged rows: three chunks
 constexpr int kMaskedIndex = 32;  // table index of a masked-out pair
+constexpr int kBwdThreads = 512;  // eight waves
+constexpr int kXStride = kHeadDim + 4;  // X row stride: rows of 16-lane accesses in different banks
 
+// Per-token record: signature words [0, SW), then the key scale, the total
+// log-partition in log2 units and D, in the last three words.
 template <int NW>
-struct SigStride {
-    static constexpr int value = NW <= 1 ? 1 : (NW <= 2 ? 2 : (NW <= 4 ? 4 : 8));
+struct BwdRec {
+    static constexpr int SW = sig_stride(NW);
+    static constexpr int RW = SW + 3 <= 4 ? 4 : (SW + 3 <= 8 ? 8 : 16);
 };
 
-// Row metadata of the staged window (one entry per staged row).
-template <int NW>
-struct RowMeta {
-    float cf[kWin];  // scale*log2(e)/|q_row|
-    float z2[kWin];  // the row's total log-partition, log2 units
-    float D[kWin];   // dO_row . o_row
-    int lo[kWin];    // slot interval of the row's valid keys (as a query)
-    int hi[kWin];
-    uint32_t sig[kWin][SigStride<NW>::value];
-    float tab[kMaskedIndex + 1];  // -log2 N by mismatch count; -inf = masked
+// LDS of one workgroup.  DEPTH: how many chunks ahead the gather runs (the
+// q, v and record rings hold chunks c-1 .. c+DEPTH, the dO ring c .. c+DEPTH);
+// the step loop waits for all of a step's copies, so it is written for 1.
+template <int NW, int DEPTH>
+struct BwdShared {
+    static_assert(DEPTH == 1, "the step loop waits for the copies of one chunk ahead");
+    static constexpr int kSlots = DEPTH + 2, kDSlots = DEPTH + 1;
+    char Qs[kSlots * kChunk * 128];  // q rows (swizzled)
+    char Vs[kSlots * kChunk * 128];  // v rows, same ring
+    char Ds[kDSlots * kChunk * 128]; // dO rows
+    char Ts[2 * kChunk * 128];       // dA'^T: 128 window keys x 64 queries (bf16)
+    float X[kChunk * kXStride];      // dQ of the step's queries, [token][dim] (padded rows)
+    uint32_t rec[kSlots * kChunk][BwdRec<NW>::RW];
+    int pos[kSlots * kChunk];        // position of each ring row
+    // per wave, per query of the step (lane order): its key interval in window
+    // rows, its log-partition (log2 units) and D, and its signature words
+    int lo[8][kChunk], hi[8][kChunk];
+    float2 zd[8][kChunk];
+    uint32_t qsig[8][NW > 0 ? NW : 1][kChunk];
+    float tab[kMaskedIndex + 1];     // -log2 N by mismatch count; -inf = masked
 };
 
-template <int NW>
-__device__ __forceinline__ void load_sig(const RowMeta<NW>& M, int row, uint32_t (&out)[NW > 0 ? NW : 1]) {
-    if constexpr (NW == 1) {
-        out[0] = M.sig[row][0];
-    } else if constexpr (NW == 2) {
-        const uint2 v = *reinterpret_cast<const uint2*>(&M.sig[row][0]);
-        out[0] = v.x;
-        out[1] = v.y;
-    } else if constexpr (NW > 2) {
-#pragma unroll
-        for (int w4 = 0; w4 < (NW + 3) / 4; ++w4) {
-            const u32x4 v = *reinterpret_cast<const u32x4*>(&M.sig[row][4 * w4]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                if (4 * w4 + e < NW) out[4 * w4 + e] = v[e];
-        }
-    }
+// Row i of chunk `chunk` in a ring of SLOTS chunk slots.
+template <int SLOTS>
+__device__ __forceinline__ int slot_row(int chunk, int i) {
+    return ((chunk % SLOTS + SLOTS) % SLOTS) * kChunk + i;
 }
 
-// Number of rounds in which two tokens' bucket ids differ (0 when there is
-// one round, which needs no signatures).
-template <int NW>
-__device__ __forceinline__ int n_mismatch(const uint32_t (&a)[NW > 0 ? NW : 1],
-                                          const uint32_t (&b)[NW > 0 ? NW : 1]) {
-    int nm = 0;
-    if constexpr (NW > 0) {
-#pragma unroll
-        for (int w = 0; w < NW; ++w) nm += sig_mismatches(a[w], b[w]);
-    }
-    return nm;
-}
-
-// Stage rows [slot0, slot0 + 192) of one segment, gathered through perm:
-// q rows into Qs (all rows), v rows into Vs for rows [v_lo, v_hi), dO rows
-// into Ds for rows [d_lo, d_hi) (stored at row - d_lo), and per-row metadata.
-template <int NW, bool CAUSAL>
-__device__ __forceinline__ void stage_window(
-    char* Qs, char* Vs, int v_lo, int v_hi, char* Ds, int d_lo, int d_hi, RowMeta<NW>& M,
+template <int NW, bool CAUSAL, int DEPTH>
+__global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ v,
-    const uint16_t* __restrict__ dout, const float* __restrict__ lse_total,
-    const float* __restrict__ Dbuf, const int32_t* __restrict__ buckets,
-    const int32_t* __restrict__ perm, const int32_t* __restrict__ bstart, int64_t seg,
-    int64_t bh, int r, int slot0, int L, int n_r, int n_b, float scale_log2e) {
-    // Three phases, each issuing all of its loads before any result is used:
-    // the staged slots' positions, then (through them) the rows, bucket ids,
-    // log-partitions and D, then (through the ids) the bucket bounds.  Every
-    // address is clamped to a valid one, so no load sits under a per-lane
-    // condition (which would make it a branch with its own wait); slots
-    // outside the sequence get zero rows and an empty interval afterwards.
-    constexpr int kIt = kWin * 8 / 256;
-    const int tid = threadIdx.x, part = tid & 7;
-    const int32_t* bs = bstart + seg * (n_b + 1);
-    const int32_t* pseg = perm + seg * L;
-    if (tid <= kMaskedIndex) M.tab[tid] = tid < n_r ? -__log2f((float)(n_r - tid)) : -__builtin_inff();
-    const u32x4 zero = {0, 0, 0, 0};
+    const uint16_t* __restrict__ dout, const uint32_t* __restrict__ rec,
+    const int32_t* __restrict__ perm, uint16_t* __restrict__ part_q, uint16_t* __restrict__ part_v,
+    uint8_t* __restrict__ part_e, int L, int n_r, float scale, int chunks_per_strip) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    using Shared = BwdShared<NW, DEPTH>;
+    Shared& S = *reinterpret_cast<Shared*>(smem);
+    constexpr int SW = BwdRec<NW>::SW, RW = BwdRec<NW>::RW;
+    auto ring_row = [](int chunk, int i) { return slot_row<Shared::kSlots>(chunk, i); };
+    auto ring2_row = [](int chunk, int i) { return slot_row<Shared::kDSlots>(chunk, i); };
 
-    int pos[kIt];
-#pragma unroll
-    for (int i = 0; i < kIt; ++i) {
-        const int slot = slot0 + ((tid + 256 * i) >> 3);
-        pos[i] = pseg[min(max(slot, 0), L - 1)];
-    }
-
-    u32x4 qq[kIt], vv[kIt], dd[kIt];
-    int beta[kIt];
-    uint32_t lo_id[kIt], hi_id[kIt];
-    float zl[kIt], Dl[kIt];
-#pragma unroll
-    for (int i = 0; i < kIt; ++i) {
-        const int rho = (tid + 256 * i) >> 3;  // the same for the whole wave's 8 rows' range test
-        const int64_t grow = bh * L + min(max(pos[i], 0), L - 1);
-        const int64_t off = grow * kHeadDim + part * 8;
-        qq[i] = *reinterpret_cast<const u32x4*>(q + off);
-        vv[i] = zero;
-        if (rho >= v_lo && rho < v_hi) vv[i] = *reinterpret_cast<const u32x4*>(v + off);
-        dd[i] = zero;
-        if (rho >= d_lo && rho < d_hi) dd[i] = *reinterpret_cast<const u32x4*>(dout + off);
-        const int32_t* brow = buckets + grow * n_r;
-        beta[i] = brow[r];
-        lo_id[i] = (uint32_t)brow[min(2 * part, n_r - 1)];
-        hi_id[i] = (uint32_t)brow[min(2 * part + 1, n_r - 1)];
-        zl[i] = lse_total[grow];
-        Dl[i] = Dbuf[grow];
-    }
-
-    int b0[kIt], b1[kIt];
-#pragma unroll
-    for (int i = 0; i < kIt; ++i) {
-        const int bb = min(max(beta[i], 0), n_b - 1);
-        b0[i] = bs[bb];
-        b1[i] = bs[bb + 1];
-    }
-
-#pragma unroll
-    for (int i = 0; i < kIt; ++i) {
-        const int rho = (tid + 256 * i) >> 3;
-        const int slot = slot0 + rho;
-        const bool ok = slot >= 0 && slot < L;
-        const u32x4 qv = ok ? qq[i] : zero;
-        lds_store_piece(Qs, rho, part, qv);
-        if (rho >= v_lo && rho < v_hi) lds_store_piece(Vs, rho - v_lo, part, ok ? vv[i] : zero);
-        if (rho >= d_lo && rho < d_hi) lds_store_piece(Ds, rho - d_lo, part, ok ? dd[i] : zero);
-        float ss = 0.f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float a = __uint_as_float(qv[e] << 16), b = __uint_as_float(qv[e] & 0xFFFF0000u);
-            ss = fmaf(a, a, fmaf(b, b, ss));
-        }
-        ss += __shfl_xor(ss, 1);
-        ss += __shfl_xor(ss, 2);
-        ss += __shfl_xor(ss, 4);
-        if (part == 0) {
-            const float nn = sqrtf(ss);
-            M.cf[rho] = nn > 0.f ? scale_log2e / nn : 0.f;
-            M.z2[rho] = ok ? zl[i] * kLog2e : 0.f;
-            M.D[rho] = ok ? Dl[i] : 0.f;
-            const int c = (slot >= 0 ? slot : 0) / kChunk;
-            const int wlo = max(0, (c - 1) * kChunk);
-            M.lo[rho] = ok ? max(b0[i], wlo) : 1;
-            M.hi[rho] = ok ? (CAUSAL ? slot - 1 : min(b1[i], (c + 1) * kChunk) - 1) : 0;
-        }
-        if constexpr (NW > 0) {
-            if (part < SigStride<NW>::value) {
-                uint32_t w = 0;
-                if (ok && part < NW) {
-                    w = lo_id[i];
-                    if (2 * part + 1 < n_r) w |= hi_id[i] << 11;
-                }
-                M.sig[rho][part] = w;
-            }
-        }
-    }
-}
-
-// ---- fused: per chunk c, the key role (dK, dV of chunk c's keys, lanes on
-// keys) and the query role (dQ of chunk c's queries, lanes on queries) over
-// one staged window, chunks c-1, c and c+1 ----
-// Waves 0 and 1 take the key role: S = Q K^T and dP = dO V^T against the
-// queries of chunks c and c+1 (the only ones whose window holds chunk c),
-// then dV^T += dO^T P and dK^T += Q^T dA.  Waves 2 and 3 take the query role:
-// S^T = K Q^T, dP^T = V dO^T over chunks c-1 and c, then dQ^T += K^T dA^T.
-// Both roles cover the same 64 tokens, so the key role hands dK_i to the
-// query role through LDS, which adds it through the normalisation Jacobian
-// (dq_i += (dk_i - (dk_i.k_i) k_i)/|q_i|, linear, so per round is exact) and
-// writes one per-round partial for dq and one for dv.
-template <int NW, bool CAUSAL>
-__global__ __launch_bounds__(256, 2) void bwd_fused_kernel(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ v,
-    const uint16_t* __restrict__ dout, const float* __restrict__ lse_total,
-    const float* __restrict__ Dbuf, const int32_t* __restrict__ buckets,
-    const int32_t* __restrict__ perm, const int32_t* __restrict__ bstart,
-    float* __restrict__ dq_r, float* __restrict__ dv_r, int L, int n_r, int n_b, float scale) {
-    __shared__ __attribute__((aligned(16))) char Qs[kWin * 128];
-    __shared__ __attribute__((aligned(16))) char Vs[128 * 128];    // chunks c-1, c
-    __shared__ __attribute__((aligned(16))) char Ds[128 * 128];    // chunks c, c+1; then dK of chunk c
-    __shared__ __attribute__((aligned(16))) RowMeta<NW> M;
-
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n = lane & 15, g = lane >> 4;
     const int64_t seg = blockIdx.y;
     const int64_t bh = seg / n_r;
     const int r = (int)(seg % n_r);
-    const int c = blockIdx.x;
-    const int slot0 = (c - 1) * kChunk;  // row 0 = first slot of chunk c - 1
-    stage_window<NW, CAUSAL>(Qs, Vs, 0, 2 * kChunk, Ds, kChunk, kWin, M, q, v, dout, lse_total,
-                             Dbuf, buckets, perm, bstart, seg, bh, r, slot0, L, n_r, n_b,
-                             scale * kLog2e);
+    const int n_chunks = (L + kChunk - 1) / kChunk;
+    const int c0 = blockIdx.x * chunks_per_strip;
+    const int c1 = min(n_chunks, c0 + chunks_per_strip);
+    const int32_t* pseg = perm + seg * L;
+    const int64_t rowbase = bh * L;
+    const float scale_log2e = scale * kLog2e;
+    if (tid <= kMaskedIndex) S.tab[tid] = tid < n_r ? -__log2f((float)(n_r - tid)) : -__builtin_inff();
+
+    // Position of slot `lane` of chunk cc (any valid row for slots outside the
+    // sequence: they are never a valid key or query, and write nothing).
+    auto chunk_pos = [&](int cc) -> int {
+        const int slot = cc * kChunk + lane;
+        return cc >= 0 && slot < L ? pseg[slot] : 0;
+    };
+    // Gather chunk cc into its ring slots: wave w copies q, v and dO rows
+    // 8w .. 8w+7 (each lane the 16-byte piece that belongs at its LDS slot);
+    // the records go through the first RW/4 waves, the positions through the
+    // last.
+    auto stage = [&](int cc, int pos_raw) {
+        const int pos_lane = min(max(pos_raw, 0), L - 1);
+        const int row = 8 * wave + (lane >> 3);
+        const int p = __shfl(pos_lane, row);
+        const int64_t off = (rowbase + p) * kHeadDim + swz(row, lane & 7) * 8;
+        copy16_to_lds(q + off, S.Qs + ring_row(cc, 8 * wave) * 128);
+        copy16_to_lds(v + off, S.Vs + ring_row(cc, 8 * wave) * 128);
+        copy16_to_lds(dout + off, S.Ds + ring2_row(cc, 8 * wave) * 128);
+        constexpr int U = RW / 4;  // 16-byte units per record
+        if (wave < U) {
+            const int u = 64 * wave + lane, rr = u / U;
+            const int pr = __shfl(pos_lane, rr);
+            copy16_to_lds(rec + (rowbase + pr) * RW + 4 * (u % U), &S.rec[ring_row(cc, 0)][0] + 256 * wave);
+        }
+        if (wave == 7) S.pos[ring_row(cc, lane)] = pos_lane;
+    };
+
+    stage(c0 - 1, chunk_pos(c0 - 1));
+    stage(c0, chunk_pos(c0));
+    int pf_pos = chunk_pos(c0 + DEPTH);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, h = lane >> 5, n = lane & 31;
-    f32x16 accA[2] = {f32x16{}, f32x16{}};  // key role: dK; query role: dQ
-    f32x16 accB[2] = {f32x16{}, f32x16{}};  // key role: dV
-    if (wave < 2) {
-        const int kh = wave & 1;
-        const int kr = kChunk + kh * 32 + n;  // this lane's key row (chunk c)
-        const int t_key = slot0 + kr;
-        const float cf_k = M.cf[kr];
-        uint32_t sig_k[NW > 0 ? NW : 1];
-        load_sig<NW>(M, kr, sig_k);
-        bf16x8 bk[4], bv[4];
-    #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            bk[s] = row_operand(Qs, kr, h, s);
-            bv[s] = row_operand(Vs, kr, h, s);
-        }
-        const int key_lo = slot0 + kChunk + kh * 32;  // slot range of the wave's keys
-        const int key_hi = key_lo + 31;
+    // This wave's key block: block b of every chunk of parity cp, held for
+    // the two steps in which the chunk is in the window.
+    const int b = wave & 3, cp = wave >> 2;
+    f32x4 accK[4] = {f32x4{}, f32x4{}, f32x4{}, f32x4{}};  // dK^T by 16-dim blocks
+    f32x4 accV[4] = {f32x4{}, f32x4{}, f32x4{}, f32x4{}};  // dV^T
 
-        const int qrow0 = kChunk;  // queries: chunks c and c+1
-    #pragma unroll 1
-        for (int qt = 0; qt < 4; ++qt) {
-            const int qr0 = qrow0 + qt * 32;
-            // skip query tiles none of whose intervals reaches the wave's keys
-            const int lo_n = M.lo[qr0 + n], hi_n = M.hi[qr0 + n];
-            if (__ballot(lo_n <= hi_n && lo_n <= key_hi && hi_n >= key_lo) == 0) continue;
+    for (int c = c0; c <= c1; ++c) {
+        if (c + DEPTH <= c1) stage(c + DEPTH, pf_pos);
+        const int pf_next = chunk_pos(c + DEPTH + 1);
 
-            f32x16 sacc = {}, dpacc = {};
-            const int arow = qr0 + kappa(n);
-    #pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                sacc = mfma32x32x16(row_operand(Qs, arow, h, s), bk[s], sacc);
-                dpacc = mfma32x32x16(row_operand(Ds, arow - kChunk, h, s), bv[s], dpacc);
+        // ---- each query's key interval [lo, hi] in window rows (0..63:
+        // chunk c-1, 64..127: chunk c), from the bucket boundaries of the
+        // window: lane = query of chunk c ----
+        int lo_q, hi_q;
+        {
+            const uint32_t kA = sig_round_id(&S.rec[ring_row(c - 1, lane)][0], r);
+            const uint32_t kB = sig_round_id(&S.rec[ring_row(c, lane)][0], r);
+            const uint32_t prevA = __shfl_up(kA, 1);
+            const uint32_t lastA = __shfl(kA, 63);
+            const uint32_t prevB0 = __shfl_up(kB, 1);
+            const uint32_t prevB = lane == 0 ? lastA : prevB0;
+            const uint64_t bA = __ballot(lane == 0 || kA != prevA);
+            const uint64_t bB = __ballot(kB != prevB);
+            const uint64_t upto = bB & (~0ull >> (63 - lane));
+            const int lo_w = upto ? 127 - __clzll(upto) : 63 - __clzll(bA);
+            lo_q = max(lo_w, (1 - c) * kChunk);  // no slot before 0
+            if constexpr (CAUSAL) {
+                hi_q = kChunk + lane - 1;
+            } else {
+                const uint64_t after = lane < 63 ? bB & (~0ull << (lane + 1)) : 0ull;
+                hi_q = after ? 62 + __ffsll((long long)after) : 127;
             }
-            u32x4 pk[2], pl[2], dak[2];  // P as bf16 hi + lo planes (dV), dA as bf16 (dK)
-    #pragma unroll
-            for (int run = 0; run < 2; ++run) {
-                const int qb = qr0 + 16 * run + 8 * h;  // first query row of the lane's run
-                // the run's eight queries: interval, log-partition, D
-                int lo8[8], hi8[8];
-                float z8[8], D8[8];
-    #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    lo8[e] = M.lo[qb + e];
-                    hi8[e] = M.hi[qb + e];
-                    z8[e] = M.z2[qb + e];
-                    D8[e] = M.D[qb + e];
+            hi_q = min(hi_q, L - 1 - (c - 1) * kChunk);  // no slot past the sequence
+            if (c * kChunk + lane >= L) {                // no query here
+                lo_q = 1;
+                hi_q = 0;
+            }
+            S.lo[wave][lane] = lo_q;
+            S.hi[wave][lane] = hi_q;
+            const uint32_t* qrec = &S.rec[ring_row(c, lane)][0];
+            S.zd[wave][lane] = make_float2(__uint_as_float(qrec[RW - 2]), __uint_as_float(qrec[RW - 1]));
+            if constexpr (NW > 0) {
+#pragma unroll
+                for (int w = 0; w < NW; ++w) S.qsig[wave][w][lane] = qrec[w];
+            }
+        }
+        // queries with a key in window block kw (one bit per query)
+        auto block_queries = [&](int kw) -> uint64_t {
+            return __ballot(lo_q <= hi_q && lo_q <= 16 * kw + 15 && hi_q >= 16 * kw);
+        };
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+        // ---- pass 1: this wave's key block against the 64 queries ----
+        const int k_chunk = (c & 1) == cp ? c : c - 1;  // the chunk of this wave's parity
+        const int kw = (k_chunk == c ? 4 : 0) + b;      // its window block
+        if (!(k_chunk == c && c == c1)) {               // chunk c1 belongs to the next strip
+            const uint64_t qmask = block_queries(kw);    // queries that reach this key block
+            const int krow = ring_row(k_chunk, 16 * b + n);
+            const int key_w = 16 * kw + n;
+            const uint32_t* krec = &S.rec[krow][0];
+            const float cf_k = __uint_as_float(krec[RW - 3]);
+            uint32_t ks[NW > 0 ? NW : 1];
+#pragma unroll
+            for (int w = 0; w < (NW > 0 ? NW : 1); ++w) ks[w] = krec[w];
+            const bf16x8 bk0 = as_bf16x8(lds_piece(S.Qs, krow, g));
+            const bf16x8 bk1 = as_bf16x8(lds_piece(S.Qs, krow, 4 + g));
+            const bf16x8 bv0 = as_bf16x8(lds_piece(S.Vs, krow, g));
+            const bf16x8 bv1 = as_bf16x8(lds_piece(S.Vs, krow, 4 + g));
+#pragma unroll
+            for (int qb = 0; qb < 4; ++qb) {
+                if (((qmask >> (16 * qb)) & 0xFFFFull) == 0) continue;
+                const int qrow = ring_row(c, 16 * qb + n);
+                const int drow = ring2_row(c, 16 * qb + n);
+                f32x4 sacc = mfma16x16x32(as_bf16x8(lds_piece(S.Qs, qrow, g)), bk0, f32x4{});
+                sacc = mfma16x16x32(as_bf16x8(lds_piece(S.Qs, qrow, 4 + g)), bk1, sacc);
+                f32x4 dpacc = mfma16x16x32(as_bf16x8(lds_piece(S.Ds, drow, g)), bv0, f32x4{});
+                dpacc = mfma16x16x32(as_bf16x8(lds_piece(S.Ds, drow, 4 + g)), bv1, dpacc);
+                // lane holds queries 16qb + 4g + j (j = 0..3) against key n
+                // the lane's four queries: intervals, log-partitions, D and
+                // signature words, one 16-byte read per field (lane groups
+                // read consecutive runs, so these reads do not conflict)
+                const int q0 = 16 * qb + 4 * g;
+                const int4 lo4 = *reinterpret_cast<const int4*>(&S.lo[wave][q0]);
+                const int4 hi4 = *reinterpret_cast<const int4*>(&S.hi[wave][q0]);
+                const f32x4 zd01 = *reinterpret_cast<const f32x4*>(&S.zd[wave][q0]);
+                const f32x4 zd23 = *reinterpret_cast<const f32x4*>(&S.zd[wave][q0 + 2]);
+                u32x4 qs4[NW > 0 ? NW : 1];
+                if constexpr (NW > 0) {
+#pragma unroll
+                    for (int w = 0; w < NW; ++w) qs4[w] = *reinterpret_cast<const u32x4*>(&S.qsig[wave][w][q0]);
                 }
-    #pragma unroll
-                for (int e2 = 0; e2 < 4; ++e2) {
-                    float pv[2], dav[2];
-    #pragma unroll
-                    for (int u = 0; u < 2; ++u) {
-                        const int e = 2 * e2 + u;
-                        const int qi = qb + e;
-                        const int j = 8 * run + e;
-                        bool valid = t_key >= lo8[e] && t_key <= hi8[e];
-                        if constexpr (!CAUSAL) valid = valid && t_key != slot0 + qi;
-                        uint32_t sig_q[NW > 0 ? NW : 1];
-                        load_sig<NW>(M, qi, sig_q);
-                        // -log2 N_ij, or -inf for a pair outside the query's interval
-                        const float mterm = M.tab[valid ? n_mismatch<NW>(sig_q, sig_k) : kMaskedIndex];
-                        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[j], cf_k, mterm) - z8[e]);
-                        pv[u] = p;
-                        dav[u] = p * (dpacc[j] - D8[e]);
+                const int lo_a[4] = {lo4.x, lo4.y, lo4.z, lo4.w};
+                const int hi_a[4] = {hi4.x, hi4.y, hi4.z, hi4.w};
+                const float z2_a[4] = {zd01[0], zd01[2], zd23[0], zd23[2]};
+                const float D_a[4] = {zd01[1], zd01[3], zd23[1], zd23[3]};
+                float p[4], da[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    bool valid = lo_a[j] <= key_w && key_w <= hi_a[j];
+                    if constexpr (!CAUSAL) valid = valid && key_w != kChunk + q0 + j;
+                    uint32_t t = valid ? 0u : ~0u;
+                    if constexpr (NW > 0) {
+#pragma unroll
+                        for (int w = 0; w < NW; ++w) t = and_or((qs4[w][j] ^ ks[w]) + sig_add(w), sig_guard(w), t);
                     }
-                    const uint32_t hi = pack_bf16x2(pv[0], pv[1]);
-                    pk[run][e2] = hi;
-                    pl[run][e2] = pack_bf16x2(pv[0] - __uint_as_float(hi << 16),
-                                              pv[1] - __uint_as_float(hi & 0xFFFF0000u));
-                    dak[run][e2] = pack_bf16x2(dav[0], dav[1]);
+                    p[j] = __builtin_amdgcn_exp2f(fmaf(sacc[j], cf_k, S.tab[__popc(t)] - z2_a[j]));
+                    da[j] = p[j] * (dpacc[j] - D_a[j]);
+                }
+                // P as bf16 hi + lo planes, dA and dA' = dA * scale*log2(e)/|q_j|
+                uint32_t ph[2], pl[2], dab[2], dpb[2];
+#pragma unroll
+                for (int h2 = 0; h2 < 2; ++h2) {
+                    ph[h2] = pack_bf16x2(p[2 * h2], p[2 * h2 + 1]);
+                    pl[h2] = pack_bf16x2(p[2 * h2] - __uint_as_float(ph[h2] << 16),
+                                         p[2 * h2 + 1] - __uint_as_float(ph[h2] & 0xFFFF0000u));
+                    dab[h2] = pack_bf16x2(da[2 * h2], da[2 * h2 + 1]);
+                    dpb[h2] = pack_bf16x2(da[2 * h2] * cf_k, da[2 * h2 + 1] * cf_k);
+                }
+                const bf16x4 Bph = __builtin_bit_cast(bf16x4, make_uint2(ph[0], ph[1]));
+                const bf16x4 Bpl = __builtin_bit_cast(bf16x4, make_uint2(pl[0], pl[1]));
+                const bf16x4 Bda = __builtin_bit_cast(bf16x4, make_uint2(dab[0], dab[1]));
+                // dA'^T row key_w, queries q0 .. q0+3
+                *reinterpret_cast<uint2*>(S.Ts + row_piece_offset(key_w, 2 * qb + (g >> 1)) + 8 * (g & 1)) =
+                    make_uint2(dpb[0], dpb[1]);
+                const int dbase = ring2_row(c, 16 * qb), qbase = ring_row(c, 16 * qb);
+#pragma unroll
+                for (int bd = 0; bd < 4; ++bd) {
+                    const bf16x4 dOt = vt_read(S.Ds + vt_offset(dbase, 16 * bd, lane));
+                    accV[bd] = mfma16x16x16(dOt, Bph, accV[bd]);
+                    accV[bd] = mfma16x16x16(dOt, Bpl, accV[bd]);
+                    accK[bd] = mfma16x16x16(vt_read(S.Qs + vt_offset(qbase, 16 * bd, lane)), Bda, accK[bd]);
                 }
             }
-            // dV^T += dO^T (P_hi + P_lo),  dK^T += Q^T dA  (k = queries of the tile).
-            // dO is exact in bf16 and P_hi + P_lo carries P to ~2^-16, so dV keeps
-            // fp32-level accuracy; dA (then scaled and summed) stays one plane.
-    #pragma unroll
-            for (int ku = 0; ku < 2; ++ku) {
-                const int r0 = qr0 + 16 * ku + 8 * h;
-    #pragma unroll
-                for (int dt = 0; dt < 2; ++dt) {
-                    const bf16x8 dOt = col_operand(Ds, r0 - kChunk, 32 * dt + n);
-                    accB[dt] = mfma32x32x16(dOt, as_bf16x8(pk[ku]), accB[dt]);
-                    accB[dt] = mfma32x32x16(dOt, as_bf16x8(pl[ku]), accB[dt]);
-                    accA[dt] = mfma32x32x16(col_operand(Qs, r0, 32 * dt + n), as_bf16x8(dak[ku]), accA[dt]);
-                }
-            }
-        }
-    } else {
-        const int qh = wave & 1;
-        const int kb = 0;                          // first key row of the window
-        const int rq = kb + kChunk + qh * 32 + n;  // this lane's query row
-        const int s_q = slot0 + rq;
-        const int lo = M.lo[rq], hi = M.hi[rq];
-        const float z2 = M.z2[rq], Dq = M.D[rq];
-        uint32_t sig_q[NW > 0 ? NW : 1];
-        load_sig<NW>(M, rq, sig_q);
-        bf16x8 bq[4], bdo[4];
-    #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            bq[s] = row_operand(Qs, rq, h, s);
-            bdo[s] = row_operand(Ds, rq - kChunk, h, s);
         }
 
-    #pragma unroll 1
-        for (int kt = 0; kt < 4; ++kt) {
-            const int tb = slot0 + kb + kt * 32;
-            if (__ballot(lo <= hi && lo <= tb + 31 && hi >= tb) == 0) continue;
-            const int kr0 = kb + kt * 32;
-            f32x16 sacc = {}, dpacc = {};
-            const int arow = kr0 + kappa(n);
-    #pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                sacc = mfma32x32x16(row_operand(Qs, arow, h, s), bq[s], sacc);
-                dpacc = mfma32x32x16(row_operand(Vs, arow, h, s), bdo[s], dpacc);
-            }
-            u32x4 dak[2];
-    #pragma unroll
-            for (int run = 0; run < 2; ++run) {
-                const int krb = kr0 + 16 * run + 8 * h;
-                float cf8[8];  // the run's eight key scales
-    #pragma unroll
-                for (int e = 0; e < 8; ++e) cf8[e] = M.cf[krb + e];
-    #pragma unroll
-                for (int e2 = 0; e2 < 4; ++e2) {
-                    float dav[2];
-    #pragma unroll
-                    for (int u = 0; u < 2; ++u) {
-                        const int e = 2 * e2 + u;
-                        const int kj = krb + e;
-                        const int j = 8 * run + e;
-                        const int t = slot0 + kj;
-                        bool valid = t >= lo && t <= hi;
-                        if constexpr (!CAUSAL) valid = valid && t != s_q;
-                        uint32_t sig_k[NW > 0 ? NW : 1];
-                        load_sig<NW>(M, kj, sig_k);
-                        const float cfk = cf8[e];
-                        // -log2 N_ij, or -inf for a key outside the query's interval
-                        const float mterm = M.tab[valid ? n_mismatch<NW>(sig_q, sig_k) : kMaskedIndex];
-                        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[j], cfk, mterm) - z2);
-                        // scale/|q_j| = cf_j / log2(e); the 1/log2(e) is applied at the end
-                        dav[u] = p * (dpacc[j] - Dq) * cfk;
+        // ---- a key block whose chunk leaves the window: its tokens are
+        // done as keys (and, in the previous step, as queries) ----
+        if (k_chunk == c - 1) {
+            const int t_i = 16 * b + n;
+            const int slot = k_chunk * kChunk + t_i;
+            if (k_chunk >= c0 && slot < L) {  // chunk c0-1 belongs to the previous strip
+                const int tr = ring_row(k_chunk, t_i);
+                const float cf = __uint_as_float(S.rec[tr][RW - 3]);
+                const float inv = cf * (1.f / scale_log2e);  // 1/|q|, 0 for a zero row
+                const int pos = S.pos[tr];
+                f32x4 qv[4], xq[4];
+                float kd = 0.f;
+#pragma unroll
+                for (int bd = 0; bd < 4; ++bd) {
+                    const uint2 w2 = *reinterpret_cast<const uint2*>(
+                        S.Qs + row_piece_offset(tr, 2 * bd + (g >> 1)) + 8 * (g & 1));
+                    qv[bd] = f32x4{__uint_as_float(w2.x << 16), __uint_as_float(w2.x & 0xFFFF0000u),
+                                   __uint_as_float(w2.y << 16), __uint_as_float(w2.y & 0xFFFF0000u)};
+                    xq[bd] = *reinterpret_cast<const f32x4*>(&S.X[t_i * kXStride + 16 * bd + 4 * g]);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) kd = fmaf(accK[bd][j], qv[bd][j], kd);
+                }
+                kd += __shfl_xor(kd, 16);
+                kd += __shfl_xor(kd, 32);
+                const float proj = scale * kd * inv;  // dk . k
+                f32x4 a[4];
+                float mq = 0.f, mv = 0.f;
+#pragma unroll
+                for (int bd = 0; bd < 4; ++bd)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        a[bd][j] = kLn2 * xq[bd][j] + (scale * accK[bd][j] - proj * qv[bd][j] * inv) * inv;
+                        mq = fmaxf(mq, fabsf(a[bd][j]));
+                        mv = fmaxf(mv, fabsf(accV[bd][j]));
                     }
-                    dak[run][e2] = pack_bf16x2(dav[0], dav[1]);
+                mq = fmaxf(mq, __shfl_xor(mq, 16));
+                mq = fmaxf(mq, __shfl_xor(mq, 32));
+                mv = fmaxf(mv, __shfl_xor(mv, 16));
+                mv = fmaxf(mv, __shfl_xor(mv, 32));
+                // 2^(E-127) <= max < 2^(E-126): e = max(0, E - 141) puts the
+                // scaled row below 2^15, inside fp16's range
+                const int eq = max(0, (int)((__float_as_uint(mq) >> 23) & 0xFFu) - 141);
+                const int ev = max(0, (int)((__float_as_uint(mv) >> 23) & 0xFFu) - 141);
+                const float sq = __uint_as_float((uint32_t)(127 - eq) << 23);
+                const float sv = __uint_as_float((uint32_t)(127 - ev) << 23);
+                const int64_t prow = seg * L + pos;
+                uint16_t* dqrow = part_q + prow * kHeadDim;
+                uint16_t* dvrow = part_v + prow * kHeadDim;
+#pragma unroll
+                for (int bd = 0; bd < 4; ++bd) {
+                    *reinterpret_cast<uint2*>(dqrow + 16 * bd + 4 * g) =
+                        make_uint2(pack_f16x2(a[bd][0] * sq, a[bd][1] * sq), pack_f16x2(a[bd][2] * sq, a[bd][3] * sq));
+                    *reinterpret_cast<uint2*>(dvrow + 16 * bd + 4 * g) =
+                        make_uint2(pack_f16x2(accV[bd][0] * sv, accV[bd][1] * sv),
+                                   pack_f16x2(accV[bd][2] * sv, accV[bd][3] * sv));
                 }
+                if (g == 0) part_e[prow] = (uint8_t)eq;
+                if (g == 1) part_e[(int64_t)gridDim.y * L + prow] = (uint8_t)ev;
             }
-    #pragma unroll
-            for (int ku = 0; ku < 2; ++ku) {
-                const int r0 = kr0 + 16 * ku + 8 * h;
-    #pragma unroll
-                for (int dt = 0; dt < 2; ++dt)
-                    accA[dt] = mfma32x32x16(col_operand(Qs, r0, 32 * dt + n), as_bf16x8(dak[ku]), accA[dt]);
+#pragma unroll
+            for (int bd = 0; bd < 4; ++bd) {
+                accK[bd] = f32x4{};
+                accV[bd] = f32x4{};
             }
         }
-    }
-    __syncthreads();  // every wave is done with Ds: it now carries dK
-    float* X = reinterpret_cast<float*>(Ds);  // [64 tokens of chunk c][64] fp32
-    const int xr = (wave & 1) * 32 + n;      // this lane's token in chunk c
-    const int tok = slot0 + kChunk + xr;     // its slot
-    if (wave < 2) {
-        // lane holds key xr, d = 32dt + 8i + 4h + e
+        __syncthreads();  // dA'^T complete; every finishing read of X done
+
+        // ---- pass 2: dQ of query block qb, dims of half dh, over the window ----
+        if (c < c1) {
+            const int qb = wave & 3, dh = wave >> 2;
+            f32x4 dq2[2] = {f32x4{}, f32x4{}};
 #pragma unroll
-        for (int dt = 0; dt < 2; ++dt)
+            for (int kw2 = 0; kw2 < 8; ++kw2) {
+                if (((block_queries(kw2) >> (16 * qb)) & 0xFFFFull) == 0) continue;
+                const bf16x4 bT = vt_read(S.Ts + vt_offset(16 * kw2, 16 * qb, lane));
+                const int kbase = ring_row(c - 1 + (kw2 >> 2), 16 * (kw2 & 3));
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int d0 = 32 * dt + 8 * i + 4 * h;
-                f32x4 b;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) b[e] = scale * accA[dt][4 * i + e];
-                *reinterpret_cast<f32x4*>(X + xr * kHeadDim + d0) = b;
+                for (int i = 0; i < 2; ++i)
+                    dq2[i] = mfma16x16x16(vt_read(S.Qs + vt_offset(kbase, 16 * (2 * dh + i), lane)), bT, dq2[i]);
             }
-        if (tok < L) {  // a slot past L (a partial last chunk) has no row
-            float* dvrow = dv_r + (seg * L + tok) * kHeadDim;
 #pragma unroll
-            for (int dt = 0; dt < 2; ++dt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    f32x4 a;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) a[e] = accB[dt][4 * i + e];
-                    *reinterpret_cast<f32x4*>(dvrow + 32 * dt + 8 * i + 4 * h) = a;
-                }
+            for (int i = 0; i < 2; ++i)
+                *reinterpret_cast<f32x4*>(&S.X[(16 * qb + n) * kXStride + 16 * (2 * dh + i) + 4 * g]) = dq2[i];
         }
-    }
-    __syncthreads();
-    if (wave >= 2) {
-        // lane holds query xr, d = 32dt + 8i + 4h + e: its q values (bf16, the
-        // row's pieces in Qs) and its dK from the key role
-        const int rq = kChunk + xr;
-        f32x4 dk[2][4], qv[2][4];
-        float ss = 0.f, kd = 0.f;
-#pragma unroll
-        for (int dt = 0; dt < 2; ++dt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                dk[dt][i] = *reinterpret_cast<const f32x4*>(X + xr * kHeadDim + 32 * dt + 8 * i + 4 * h);
-                const u32x4 pc = lds_piece(Qs, rq, 4 * dt + i);
-                const uint32_t w0 = pc[2 * h], w1 = pc[2 * h + 1];
-                qv[dt][i] = f32x4{__uint_as_float(w0 << 16), __uint_as_float(w0 & 0xFFFF0000u),
-                                  __uint_as_float(w1 << 16), __uint_as_float(w1 & 0xFFFF0000u)};
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    ss = fmaf(qv[dt][i][e], qv[dt][i][e], ss);
-                    kd = fmaf(dk[dt][i][e], qv[dt][i][e], kd);
-                }
-            }
-        ss += __shfl_xor(ss, 32);
-        kd += __shfl_xor(kd, 32);
-        const float nn = sqrtf(ss);
-        const float inv = nn > 0.f ? 1.f / nn : 0.f;  // a zero query has k = 0 and no key gradient
-        const float proj = kd * inv;                  // dk . k
-        if (tok < L) {
-            float* dqrow = dq_r + (seg * L + tok) * kHeadDim;
-#pragma unroll
-            for (int dt = 0; dt < 2; ++dt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    f32x4 a;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        a[e] = kLn2 * accA[dt][4 * i + e] + (dk[dt][i][e] - proj * qv[dt][i][e] * inv) * inv;
-                    *reinterpret_cast<f32x4*>(dqrow + 32 * dt + 8 * i + 4 * h) = a;
-                }
-        }
+        pf_pos = pf_next;
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of chunk c+1 have landed
+        __syncthreads();                // ... and every wave is done with step c
     }
 }
 
-// D_i = dO_i . o_i, 16 lanes per row.
-__global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t* __restrict__ out,
+// Per-token record (see BwdRec): eight lanes per token, one 16-byte piece of
+// the q, out and dout rows each; lane p writes record words p (and p + 8).
+template <int NW>
+__global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t* __restrict__ q,
+                                                       const uint16_t* __restrict__ out,
                                                        const uint16_t* __restrict__ dout,
-                                                       int64_t rows, float* __restrict__ Dbuf) {
-    const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
-    const int part = threadIdx.x & 15;
-    if (row >= rows) return;  // whole 16-lane groups leave together
-    const uint2 o = *reinterpret_cast<const uint2*>(out + row * kHeadDim + part * 4);
-    const uint2 g = *reinterpret_cast<const uint2*>(dout + row * kHeadDim + part * 4);
-    float s = bf16_bits_to_f32(o.x & 0xFFFF) * bf16_bits_to_f32(g.x & 0xFFFF);
-    s = fmaf(bf16_bits_to_f32(o.x >> 16), bf16_bits_to_f32(g.x >> 16), s);
-    s = fmaf(bf16_bits_to_f32(o.y & 0xFFFF), bf16_bits_to_f32(g.y & 0xFFFF), s);
-    s = fmaf(bf16_bits_to_f32(o.y >> 16), bf16_bits_to_f32(g.y >> 16), s);
-    for (int off = 8; off >= 1; off >>= 1) s += __shfl_xor(s, off);
-    if (part == 0) Dbuf[row] = s;
+                                                       const float* __restrict__ lse_total,
+                                                       const int32_t* __restrict__ buckets,
+                                                       int64_t rows, int n_r, float scale_log2e,
+                                                       uint32_t* __restrict__ rec) {
+    constexpr int SW = BwdRec<NW>::SW, RW = BwdRec<NW>::RW;
+    const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 3;
+    const int part = threadIdx.x & 7;
+    if (row >= rows) return;  // whole groups of eight lanes leave together
+    const u32x4 x = *reinterpret_cast<const u32x4*>(q + row * kHeadDim + part * 8);
+    const u32x4 o = *reinterpret_cast<const u32x4*>(out + row * kHeadDim + part * 8);
+    const u32x4 gd = *reinterpret_cast<const u32x4*>(dout + row * kHeadDim + part * 8);
+    float ss = 0.f, D = 0.f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float lo = __uint_as_float(x[e] << 16), hi = __uint_as_float(x[e] & 0xFFFF0000u);
+        ss = fmaf(lo, lo, fmaf(hi, hi, ss));
+        D = fmaf(__uint_as_float(o[e] << 16), __uint_as_float(gd[e] << 16), D);
+        D = fmaf(__uint_as_float(o[e] & 0xFFFF0000u), __uint_as_float(gd[e] & 0xFFFF0000u), D);
+    }
+#pragma unroll
+    for (int off = 1; off < 8; off <<= 1) {
+        ss += __shfl_xor(ss, off);
+        D += __shfl_xor(D, off);
+    }
+    const int32_t* brow = buckets + row * n_r;
+#pragma unroll
+    for (int w = part; w < RW; w += 8) {
+        uint32_t word = 0;
+        if (w < SW) {
+            const uint32_t id0 = 2 * w < n_r ? (uint32_t)brow[2 * w] & 0x3FFu : 0u;
+            const uint32_t id1 = 2 * w + 1 < n_r ? (uint32_t)brow[2 * w + 1] & 0x3FFu : 0u;
+            word = (id0 << w) | (id1 << (w + 11));
+        } else if (w == RW - 3) {
+            const float nn = sqrtf(ss);
+            word = __float_as_uint(nn > 0.f ? scale_log2e / nn : 0.f);
+        } else if (w == RW - 2) {
+            word = __float_as_uint(lse_total[row] * kLog2e);
+        } else if (w == RW - 1) {
+            word = __float_as_uint(D);
+        }
+        rec[row * RW + w] = word;
+    }
 }
 
-constexpr int kMaxRounds = 16;
 
-// Sum the rounds per position and add the key role:
-//   dq_j = sum_r dq_r + (dk_j - (dk_j . k_j) k_j) / |q_j|,  dv_j = sum_r dv_r,
-// plus dO_j for a token whose only target in every round was itself (its
-// weights are then 1/n_rounds on each round's self entry).
+// dq, dv of a position: the sum of its per-round partials (position order,
+// fixed round order, each fp16 row times 2^e), plus dO for a token whose only
+// target in every round was itself.  NRL: n_r rounded up to a power of two;
+// rounds past n_r read round 0 with weight 0, so the loads are unconditional.
+template <int NRL>
 __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     const uint16_t* __restrict__ dout, const float* __restrict__ lse_total,
-    const int32_t* __restrict__ undo, const float* __restrict__ dq_r,
-    const float* __restrict__ dv_r, int64_t rows, int L, int n_r, float self_mask,
+    const uint16_t* __restrict__ part_q, const uint16_t* __restrict__ part_v,
+    const uint8_t* __restrict__ part_e, int64_t rows, int L, int n_r, float self_mask,
     float* __restrict__ dq, float* __restrict__ dv) {
     const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
     const int part = threadIdx.x & 15;
     if (row >= rows) return;  // whole 16-lane groups leave together
     const int64_t bh = row / L, i = row % L;
-    int64_t base[kMaxRounds];
+    const int64_t rr_total = rows * n_r;  // offset of the dv exponents
+    uint2 xq[NRL], xv[NRL];
+    uint32_t eq[NRL], ev[NRL];
 #pragma unroll
-    for (int r = 0; r < kMaxRounds; ++r)
-        if (r < n_r) base[r] = ((bh * n_r + r) * L + min(max(undo[(bh * n_r + r) * L + i], 0), L - 1)) * kHeadDim + part * 4;
+    for (int rr = 0; rr < NRL; ++rr) {
+        const int64_t prow = (bh * n_r + (rr < n_r ? rr : 0)) * L + i;
+        xq[rr] = *reinterpret_cast<const uint2*>(part_q + prow * kHeadDim + part * 4);
+        xv[rr] = *reinterpret_cast<const uint2*>(part_v + prow * kHeadDim + part * 4);
+        eq[rr] = part_e[prow];
+        ev[rr] = part_e[rr_total + prow];
+    }
     f32x4 aq = {0, 0, 0, 0}, av = {0, 0, 0, 0};
 #pragma unroll
-    for (int r = 0; r < kMaxRounds; ++r)
-        if (r < n_r) {
-            const f32x4 x = *reinterpret_cast<const f32x4*>(dq_r + base[r]);
-            const f32x4 z = *reinterpret_cast<const f32x4*>(dv_r + base[r]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                aq[e] += x[e];
-                av[e] += z[e];
-            }
-        }
+    for (int rr = 0; rr < NRL; ++rr) {
+        const float wq = rr < n_r ? __uint_as_float((127u + min(eq[rr], 126u)) << 23) : 0.f;
+        const float wv = rr < n_r ? __uint_as_float((127u + min(ev[rr], 126u)) << 23) : 0.f;
+        aq[0] = fmaf(wq, f16_bits_to_f32(xq[rr].x & 0xFFFFu), aq[0]);
+        aq[1] = fmaf(wq, f16_bits_to_f32(xq[rr].x >> 16), aq[1]);
+        aq[2] = fmaf(wq, f16_bits_to_f32(xq[rr].y & 0xFFFFu), aq[2]);
+        aq[3] = fmaf(wq, f16_bits_to_f32(xq[rr].y >> 16), aq[3]);
+        av[0] = fmaf(wv, f16_bits_to_f32(xv[rr].x & 0xFFFFu), av[0]);
+        av[1] = fmaf(wv, f16_bits_to_f32(xv[rr].x >> 16), av[1]);
+        av[2] = fmaf(wv, f16_bits_to_f32(xv[rr].y & 0xFFFFu), av[2]);
+        av[3] = fmaf(wv, f16_bits_to_f32(xv[rr].y >> 16), av[3]);
+    }
     if (lse_total[row] < -0.5f * self_mask) {
         const uint2 g = *reinterpret_cast<const uint2*>(dout + row * kHeadDim + part * 4);
         av[0] += bf16_bits_to_f32(g.x & 0xFFFF);
@@ -502,10 +477,17 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     *reinterpret_cast<f32x4*>(dv + row * kHeadDim + part * 4) = av;
 }
 
+int rec_words(int n_rounds) {
+    const int nw = n_rounds == 1 ? 0 : (n_rounds + 1) / 2;
+    const int sw = sig_stride(nw);
+    return sw + 3 <= 4 ? 4 : (sw + 3 <= 8 ? 8 : 16);
+}
+
 struct BwdWs {
-    float* dq_r;  // per round: dq through the query role plus the key role's dk through k = q/|q|
-    float* dv_r;
-    float* D;
+    uint16_t* part_q;  // per round: dq through the query role plus the key role's dk through k = q/|q|
+    uint16_t* part_v;
+    uint8_t* part_e;   // exponents: [round-rows] of dq, then [round-rows] of dv
+    uint32_t* rec;
     size_t bytes;
 };
 
@@ -514,23 +496,49 @@ BwdWs carve(void* base, int64_t BH, int L, int n_rounds) {
     char* p = static_cast<char*>(base);
     BwdWs w{};
     size_t off = 0;
-    w.dq_r = reinterpret_cast<float*>(p + off);
-    off += align256(rr * kHeadDim * 4);
-    w.dv_r = reinterpret_cast<float*>(p + off);
-    off += align256(rr * kHeadDim * 4);
-    w.D = reinterpret_cast<float*>(p + off);
-    off += align256((size_t)BH * L * 4);
+    w.part_q = reinterpret_cast<uint16_t*>(p + off);
+    off += align256(rr * kHeadDim * 2);
+    w.part_v = reinterpret_cast<uint16_t*>(p + off);
+    off += align256(rr * kHeadDim * 2);
+    w.part_e = reinterpret_cast<uint8_t*>(p + off);
+    off += align256(rr * 2);
+    w.rec = reinterpret_cast<uint32_t*>(p + off);
+    off += align256((size_t)BH * L * 4 * rec_words(n_rounds));
     w.bytes = off;
     return w;
 }
 
-template <int NW, bool CAUSAL>
-void launch_chunks(dim3 grid, hipStream_t stream, const uint16_t* q, const uint16_t* v,
-                   const uint16_t* dout, const float* lse, const float* D, const int32_t* buckets,
-                   const int32_t* perm, const int32_t* bs, float* dq_r, float* dv_r, int L, int n_r,
-                   int n_b, float scale) {
-    bwd_fused_kernel<NW, CAUSAL><<<grid, 256, 0, stream>>>(q, v, dout, lse, D, buckets, perm, bs,
-                                                           dq_r, dv_r, L, n_r, n_b, scale);
+template <int NW>
+hipError_t launch_nw(bool causal, int64_t BH, int L, int n_rounds, float scale, const uint16_t* q,
+                     const uint16_t* v, const uint16_t* out, const uint16_t* dout,
+                     const float* lse_total, const int32_t* buckets, const int32_t* perm,
+                     const BwdWs& w, hipStream_t stream) {
+    const int64_t rows = BH * L;
+    bwd_prep_kernel<NW><<<(unsigned)((rows * 8 + 255) / 256), 256, 0, stream>>>(
+        q, out, dout, lse_total, buckets, rows, n_rounds, scale * kLog2e, w.rec);
+    // Strips of chunks: long enough that the first window and the pair that
+    // the previous strip also computes are a small overhead, short enough to
+    // give every CU several workgroups in turn (one fits at a time).
+    const int64_t n_chunks = (L + kChunk - 1) / kChunk, segs = BH * n_rounds;
+    const int cps = (int)std::max<int64_t>(1, std::min<int64_t>(32, n_chunks * segs / 2048));
+    const dim3 grid((unsigned)((n_chunks + cps - 1) / cps), (unsigned)segs);
+    // one chunk in flight: gathering two ahead (deeper rings, which still fit
+    // in LDS below eight signature words) measured slower
+    auto go = [&](auto causal_tag, auto depth_tag) {
+        constexpr bool C = decltype(causal_tag)::value;
+        constexpr int D = decltype(depth_tag)::value;
+        const size_t lds = sizeof(BwdShared<NW, D>);
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&bwd_strip_kernel<NW, C, D>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        bwd_strip_kernel<NW, C, D><<<grid, kBwdThreads, lds, stream>>>(
+            q, v, dout, w.rec, perm, w.part_q, w.part_v, w.part_e, L, n_rounds, scale, cps);
+    };
+    using Depth = std::integral_constant<int, 1>;
+    if (causal)
+        go(std::true_type{}, Depth{});
+    else
+        go(std::false_type{}, Depth{});
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -552,22 +560,12 @@ hipError_t launch_attn_bwd(int64_t BH, int L, int n_rounds, int n_buckets, bool 
     const uint16_t* v = static_cast<const uint16_t*>(v_);
     const uint16_t* out = static_cast<const uint16_t*>(out_);
     const uint16_t* dout = static_cast<const uint16_t*>(dout_);
-    const unsigned row_grid = (unsigned)((rows * 16 + 255) / 256);
-    bwd_prep_kernel<<<row_grid, 256, 0, stream>>>(out, dout, rows, w.D);
-    // one workgroup per chunk; a partial last chunk (L not a multiple of the
-    // chunk) counts as a chunk
-    const dim3 grid((unsigned)((L + kChunk - 1) / kChunk), (unsigned)(BH * n_rounds));
     const int nw = n_rounds == 1 ? 0 : (n_rounds + 1) / 2;
-#define LSH_BWD_CASE(W)                                                                          \
-    case W:                                                                                      \
-        if (causal)                                                                              \
-            launch_chunks<W, true>(grid, stream, q, v, dout, lse_total, w.D, buckets, perm,      \
-                                   bucket_start, w.dq_r, w.dv_r, L, n_rounds, n_buckets,        \
-                                   scale);                                                       \
-        else                                                                                     \
-            launch_chunks<W, false>(grid, stream, q, v, dout, lse_total, w.D, buckets, perm,     \
-                                    bucket_start, w.dq_r, w.dv_r, L, n_rounds,                   \
-                                    n_buckets, scale);                                           \
+    hipError_t e;
+#define LSH_BWD_CASE(W)                                                                             \
+    case W:                                                                                         \
+        e = launch_nw<W>(causal, BH, L, n_rounds, scale, q, v, out, dout, lse_total, buckets, perm, \
+                         w, stream);                                                                \
         break;
     switch (nw) {
         LSH_BWD_CASE(0)
@@ -583,8 +581,17 @@ hipError_t launch_attn_bwd(int64_t BH, int L, int n_rounds, int n_buckets, bool 
             return hipErrorInvalidValue;
     }
 #undef LSH_BWD_CASE
-    bwd_reduce_kernel<<<row_grid, 256, 0, stream>>>(dout, lse_total, undo, w.dq_r, w.dv_r, rows, L,
-                                                    n_rounds, self_mask, dq, dv);
+    if (e != hipSuccess) return e;
+    const unsigned row_grid = (unsigned)((rows * 16 + 255) / 256);
+    auto reduce = [&](auto nrl) {
+        bwd_reduce_kernel<decltype(nrl)::value><<<row_grid, 256, 0, stream>>>(
+            dout, lse_total, w.part_q, w.part_v, w.part_e, rows, L, n_rounds, self_mask, dq, dv);
+    };
+    if (n_rounds <= 1) reduce(std::integral_constant<int, 1>{});
+    else if (n_rounds <= 2) reduce(std::integral_constant<int, 2>{});
+    else if (n_rounds <= 4) reduce(std::integral_constant<int, 4>{});
+    else if (n_rounds <= 8) reduce(std::integral_constant<int, 8>{});
+    else reduce(std::integral_constant<int, 16>{});
     return hipGetLastError();
 }
 

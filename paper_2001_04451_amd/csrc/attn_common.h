@@ -104,14 +104,32 @@ __device__ __forceinline__ bf16x4 vt_read(const char* p) {
     return __builtin_bit_cast(bf16x4, x);
 }
 
-// Bucket signatures: two rounds' ids (10 bits each) per word at bits 0 and 11,
-// guard bits 10 and 21.  For a = sig_i, b = sig_j the number of rounds in which
-// the ids differ is popcount(((a ^ b) + kSigAdd) & kSigGuard) summed over words.
-constexpr uint32_t kSigAdd = 0x3FFu | (0x3FFu << 11);
-constexpr uint32_t kSigGuard = (1u << 10) | (1u << 21);
+// Bucket signature word w of a token: its ids in rounds 2w and 2w+1 (10 bits
+// each) at bit offsets w and w+11.  Adding sig_add(w) to (a ^ b) carries into
+// guard bit w+10 (w+21) exactly when the first (second) ids differ; the guard
+// bits of different words are distinct, so the number of rounds in which two
+// tokens differ is the popcount of the OR over w of
+// ((a_w ^ b_w) + sig_add(w)) & sig_guard(w).
+__device__ __forceinline__ constexpr uint32_t sig_add(int w) {
+    return (0x3FFu << w) | (0x3FFu << (w + 11));
+}
+__device__ __forceinline__ constexpr uint32_t sig_guard(int w) {
+    return (1u << (w + 10)) | (1u << (w + 21));
+}
 
-__device__ __forceinline__ int sig_mismatches(uint32_t a, uint32_t b) {
-    return __popc(((a ^ b) + kSigAdd) & kSigGuard);
+// Words per token for NW signature words (NW = 0 for one round, whose id still
+// sits in word 0), and the round-r id of a token from its words.
+__host__ __device__ constexpr int sig_stride(int nw) { return nw <= 1 ? 1 : (nw <= 2 ? 2 : (nw <= 4 ? 4 : 8)); }
+__device__ __forceinline__ uint32_t sig_round_id(const uint32_t* words, int r) {
+    return (words[r >> 1] >> ((r >> 1) + 11 * (r & 1))) & 0x3FFu;
+}
+
+// (a & b) | c as one v_and_or_b32: left to itself the compiler regroups the
+// OR chain over the signature words into separate ANDs and three-way ORs.
+__device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t b, uint32_t c) {
+    uint32_t d;
+    asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(d) : "v"(a), "s"(b), "v"(c));
+    return d;
 }
 
 }  // namespace lsh

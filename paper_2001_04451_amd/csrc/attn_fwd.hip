@@ -71,27 +71,6 @@ struct BoolTag {
 
 __device__ __forceinline__ int ring_row(int chunk, int i) { return ((chunk + 3) % 3) * kChunk + i; }
 
-// Bucket signature word w of a token: its ids in rounds 2w and 2w+1 (10 bits
-// each) at bit offsets w and w+11.  Adding sig_add(w) to (a ^ b) carries into
-// guard bit w+10 (w+21) exactly when the first (second) ids differ; the guard
-// bits of different words are distinct, so the number of rounds in which two
-// tokens differ is the popcount of the OR over w of
-// ((a_w ^ b_w) + sig_add(w)) & sig_guard(w).
-__device__ __forceinline__ constexpr uint32_t sig_add(int w) {
-    return (0x3FFu << w) | (0x3FFu << (w + 11));
-}
-__device__ __forceinline__ constexpr uint32_t sig_guard(int w) {
-    return (1u << (w + 10)) | (1u << (w + 21));
-}
-
-// (a & b) | c as one v_and_or_b32: left to itself the compiler regroups the
-// OR chain over the signature words into separate ANDs and three-way ORs.
-__device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t b, uint32_t c) {
-    uint32_t d;
-    asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(d) : "v"(a), "s"(b), "v"(c));
-    return d;
-}
-
 template <int NW>
 struct FwdSig {
     static constexpr int stride = NW <= 1 ? 1 : (NW <= 2 ? 2 : (NW <= 4 ? 4 : 8));  // words per token

@@ -86,3 +86,21 @@ def test_backward_full_size(gpu):
     entry at spread heads."""
     w = W.WORKLOADS["fwdbwd_bf16_L32768"]
     assert _run(w, slices=[(b, (3 * b + 1) % w.H) for b in range(w.B)]) <= TOL
+
+
+def test_backward_deterministic(gpu):
+    """Two backward calls on the same forward state give bit-identical dq and
+    dv: every sum has a fixed order (no atomics)."""
+    w = CASES["fwdbwd_small"]
+    x = W.make_inputs(w, with_dout=True)
+    cfg = lsh.Config.of(w)
+    q, v, dout = (to_device(x[k], "bf16") for k in ("q", "v", "dout"))
+    log("backward-determinism", w)
+    st = lsh.lsh_attention_fwd(cfg, q, v, to_device(x["R"], "f32"))
+    dq1, dv1 = lsh.lsh_chunk_attn_bwd(cfg, q, v, st.out, dout, st.lse, st.buckets, st.perm,
+                                      st.undo, st.bstart)
+    dq2, dv2 = lsh.lsh_chunk_attn_bwd(cfg, q, v, st.out, dout, st.lse, st.buckets, st.perm,
+                                      st.undo, st.bstart)
+    torch.cuda.synchronize()
+    assert torch.equal(dq1.view(torch.int32), dq2.view(torch.int32))
+    assert torch.equal(dv1.view(torch.int32), dv2.view(torch.int32))
