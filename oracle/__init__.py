@@ -43,14 +43,15 @@ def _load():
     if _lib is None:
         build()
         lib = ctypes.CDLL(_LIB)
-        lib.lsh_ref_hash.argtypes = [_i64, _i64, _i64, _i64, _i64, _ptr, _ptr, _ptr, _ptr]
+        lib.lsh_ref_hash.argtypes = [_i64, _i64, _i64, _i64, _i64, _i64, _ptr, _ptr, _ptr, _ptr]
         lib.lsh_ref_sort_permute.argtypes = [_i64, _i64, _i64, _ptr, _ptr, _ptr]
-        lib.lsh_ref_chunk_attn_fwd.argtypes = [_i64, _i64, _i64, _i64, _i64, ctypes.c_int,
-                                               _f64, _f64, _ptr, _ptr, _ptr, _ptr, _ptr, _ptr]
+        lib.lsh_ref_chunk_attn_fwd.argtypes = [_i64, _i64, _i64, _i64, _i64, _i64, ctypes.c_int,
+                                               ctypes.c_int, _f64, _f64, _ptr, _ptr, _ptr, _ptr,
+                                               _ptr, _ptr]
         lib.lsh_ref_combine_rounds.argtypes = [_i64, _i64, _i64, _i64, _ptr, _ptr, _ptr, _ptr, _ptr]
-        lib.lsh_ref_chunk_attn_bwd.argtypes = [_i64, _i64, _i64, _i64, _i64, ctypes.c_int,
-                                               _f64, _f64, _ptr, _ptr, _ptr, _ptr, _ptr, _ptr,
-                                               _ptr, _ptr, _ptr]
+        lib.lsh_ref_chunk_attn_bwd.argtypes = [_i64, _i64, _i64, _i64, _i64, _i64, ctypes.c_int,
+                                               ctypes.c_int, _f64, _f64, _ptr, _ptr, _ptr, _ptr,
+                                               _ptr, _ptr, _ptr, _ptr, _ptr]
         lib.lsh_ref_dense_attn_fwd.argtypes = [_i64, _i64, _i64, ctypes.c_int, _f64, _f64, _ptr,
                                                _ptr, _i64, _ptr, _ptr, _ptr]
         lib.lsh_ref_num_threads.argtypes = []
@@ -84,14 +85,20 @@ def _check(rc: int, what: str) -> None:
 
 
 def lsh_hash(q, R):
-    """Bucket ids [B,H,L,n_rounds] and near-tie flags for q [B,H,L,d], R [n_r,d,n_b/2]."""
+    """Bucket ids [B,H,L,n_rounds] and near-tie flags for q [B,H,L,d] and
+    R [n_r,d,n_b/2] (shared by every head) or [H,n_r,d,n_b/2] (one per head)."""
     q, R = _f(q), _f(R)
     B, H, L, d = q.shape
-    n_rounds, dR, half = R.shape
+    if R.ndim == 4:
+        assert R.shape[0] == H, "one R per head"
+        H_R = H
+    else:
+        H_R = 1
+    n_rounds, dR, half = R.shape[-3:]
     assert dR == d
     buckets = np.empty((B, H, L, n_rounds), np.int32)
     near_tie = np.empty((B, H, L, n_rounds), np.uint8)
-    _check(_load().lsh_ref_hash(B * H, L, d, 2 * half, n_rounds, _p(q), _p(R),
+    _check(_load().lsh_ref_hash(B * H, L, d, 2 * half, n_rounds, H_R, _p(q), _p(R),
                                 _p(buckets), _p(near_tie)), "hash")
     return buckets, near_tie.astype(bool)
 
@@ -107,8 +114,10 @@ def lsh_sort_permute(buckets):
     return perm, undo
 
 
-def lsh_chunk_attn_fwd(q, v, buckets, perm, chunk, causal, scale=None, self_mask=1e5):
-    """Per-round outputs o_rounds [B,H,n_r,L,d] and lse_rounds [B,H,n_r,L], sorted order."""
+def lsh_chunk_attn_fwd(q, v, buckets, perm, chunk, causal, scale=None, self_mask=1e5,
+                       after=0, across=False):
+    """Per-round outputs o_rounds [B,H,n_r,L,d] and lse_rounds [B,H,n_r,L], sorted order.
+    after: look-ahead chunks in the window; across: attend across buckets."""
     q, v, buckets, perm = _f(q), _f(v), _i(buckets), _i(perm)
     B, H, L, d = q.shape
     n_rounds = buckets.shape[-1]
@@ -116,7 +125,8 @@ def lsh_chunk_attn_fwd(q, v, buckets, perm, chunk, causal, scale=None, self_mask
         scale = 1.0 / np.sqrt(d)
     o_rounds = np.empty((B, H, n_rounds, L, d), np.float64)
     lse_rounds = np.empty((B, H, n_rounds, L), np.float64)
-    _check(_load().lsh_ref_chunk_attn_fwd(B * H, L, d, n_rounds, chunk, int(bool(causal)),
+    _check(_load().lsh_ref_chunk_attn_fwd(B * H, L, d, n_rounds, chunk, int(after),
+                                          int(bool(across)), int(bool(causal)),
                                           float(scale), float(self_mask), _p(q), _p(v),
                                           _p(buckets), _p(perm), _p(o_rounds), _p(lse_rounds)),
            "chunk_attn_fwd")
@@ -159,7 +169,7 @@ def lsh_combine_rounds(o_rounds, lse_rounds, undo):
 
 
 def lsh_chunk_attn_bwd(q, v, out, dout, lse_total, buckets, perm, chunk, causal,
-                       scale=None, self_mask=1e5):
+                       scale=None, self_mask=1e5, after=0, across=False):
     """dq, dv [B,H,L,d] for upstream gradient dout, buckets held fixed."""
     q, v, out, dout, lse_total = _f(q), _f(v), _f(out), _f(dout), _f(lse_total)
     buckets, perm = _i(buckets), _i(perm)
@@ -169,21 +179,25 @@ def lsh_chunk_attn_bwd(q, v, out, dout, lse_total, buckets, perm, chunk, causal,
         scale = 1.0 / np.sqrt(d)
     dq = np.empty((B, H, L, d), np.float64)
     dv = np.empty((B, H, L, d), np.float64)
-    _check(_load().lsh_ref_chunk_attn_bwd(B * H, L, d, n_rounds, chunk, int(bool(causal)),
+    _check(_load().lsh_ref_chunk_attn_bwd(B * H, L, d, n_rounds, chunk, int(after),
+                                          int(bool(across)), int(bool(causal)),
                                           float(scale), float(self_mask), _p(q), _p(v), _p(out),
                                           _p(dout), _p(lse_total), _p(buckets), _p(perm),
                                           _p(dq), _p(dv)), "chunk_attn_bwd")
     return dq, dv
 
 
-def lsh_attention_fwd(q, v, R, chunk, causal, scale=None, self_mask=1e5):
+def lsh_attention_fwd(q, v, R, chunk, causal, scale=None, self_mask=1e5, after=0,
+                      across=False):
     """The whole forward: hash, sort, chunked attention per round, combine.
+    R: [n_r,d,n_b/2] shared, or [H,n_r,d,n_b/2] one per head.
 
     Returns a dict with every intermediate so tests can compare stage by stage.
     """
     buckets, near_tie = lsh_hash(q, R)
     perm, undo = lsh_sort_permute(buckets)
-    o_rounds, lse_rounds = lsh_chunk_attn_fwd(q, v, buckets, perm, chunk, causal, scale, self_mask)
+    o_rounds, lse_rounds = lsh_chunk_attn_fwd(q, v, buckets, perm, chunk, causal, scale, self_mask,
+                                              after, across)
     out, lse = lsh_combine_rounds(o_rounds, lse_rounds, undo)
     return dict(buckets=buckets, near_tie=near_tie, perm=perm, undo=undo, o_rounds=o_rounds,
                 lse_rounds=lse_rounds, out=out, lse=lse)

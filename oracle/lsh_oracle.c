@@ -35,7 +35,15 @@
  *   - when m does not divide L the last chunk holds the L mod m remaining
  *     slots (as if the sequence were padded with tokens that are no one's
  *     target);
- *   - a zero query gives k = 0.
+ *   - a zero query gives k = 0;
+ *   - variants the paper does not spell out, each off by default: a
+ *     look-ahead of `after` chunks (the window of chunk c is chunks
+ *     c-1 .. c+after; the paper's P~ is after = 0), attending across buckets
+ *     (the target set of round r is the window itself instead of the bucket
+ *     within it, so App. A applies with P^(r)_i read as P~^(r)_i and N_ij
+ *     counts the rounds in which j falls in i's window), and one R per head
+ *     (R holds H_R sets [n_rounds][d][n_buckets/2]; a row of head h uses set
+ *     h mod H_R).
  */
 #include <math.h>
 #include <stdint.h>
@@ -77,15 +85,17 @@ static void row_norms(int64_t rows, int64_t d, const double *q, double *norm)
 
 /* Angular LSH (Sec. 2, "Locality sensitive hashing"): with a random R of
  * shape [d_k, b/2], h(x) = argmax([xR; -xR]).  One R per round (Sec. 2,
- * "Multi-round LSH attention", eq. union-pairs), shared by every batch entry
- * and head.  near_tie marks row-rounds whose two largest entries of
- * [xR; -xR] differ by less than 1e-6 of the largest (or are equal). */
+ * "Multi-round LSH attention", eq. union-pairs).  H_R = 1: one R shared by
+ * every batch entry and head; H_R = H: one R per head, a row of slice bh
+ * (bh = b*H + h) using set bh mod H_R.  near_tie marks row-rounds whose two
+ * largest entries of [xR; -xR] differ by less than 1e-6 of the largest (or
+ * are equal). */
 int lsh_ref_hash(int64_t BH, int64_t L, int64_t d, int64_t n_buckets,
-                 int64_t n_rounds, const double *q, const double *R,
+                 int64_t n_rounds, int64_t H_R, const double *q, const double *R,
                  int32_t *buckets, uint8_t *near_tie)
 {
     if (BH < 0 || L < 0 || d < 1 || n_buckets < 2 || n_buckets % 2 ||
-        n_rounds < 1 || !q || !R || !buckets)
+        n_rounds < 1 || H_R < 1 || !q || !R || !buckets)
         return REF_ERR_INVALID;
     const int64_t half = n_buckets / 2;
     const int64_t rows = BH * L;
@@ -101,8 +111,9 @@ int lsh_ref_hash(int64_t BH, int64_t L, int64_t d, int64_t n_buckets,
         for (int64_t row = 0; row < rows; ++row) {
             if (!vals) continue;
             const double *x = q + row * d;
+            const double *Rh = R + ((row / (L > 0 ? L : 1)) % H_R) * n_rounds * d * half;
             for (int64_t r = 0; r < n_rounds; ++r) {
-                const double *Rr = R + r * d * half;
+                const double *Rr = Rh + r * d * half;
                 /* [xR; -xR] */
                 for (int64_t c = 0; c < half; ++c) {
                     double p = 0.0;
@@ -184,46 +195,84 @@ static int64_t n_shared(const int32_t *buckets, int64_t base, int64_t i,
     return n;
 }
 
+/* Attending across buckets: the number of rounds in which key j lies in
+ * query i's window, chunks floor(s_i/m) - 1 .. floor(s_i/m) + after of that
+ * round's sorted order (undo: position -> slot, [n_rounds][L] of the
+ * slice). */
+static int64_t n_window(const int32_t *undo, int64_t L, int64_t i, int64_t j,
+                        int64_t n_rounds, int64_t chunk, int64_t after)
+{
+    int64_t n = 0;
+    for (int64_t r = 0; r < n_rounds; ++r) {
+        const int64_t ci = undo[r * L + i] / chunk, cj = undo[r * L + j] / chunk;
+        n += cj >= ci - 1 && cj <= ci + after;
+    }
+    return n;
+}
+
 /* Mask term m^(r)_ij of App. A for query i and key j in round r.  Returns 0
  * when j is not a target at all (other bucket, or the future under causal
  * masking, Sec. 2 "Causal masking for shared-QK attention"); otherwise sets
- * *M to 1e5 for j == i and to log N_ij for every other target. */
-static int mask_term(const int32_t *buckets, int64_t base, int64_t i, int64_t j,
-                     int64_t r, int64_t n_rounds, int causal, double self_mask,
-                     double *M)
+ * *M to 1e5 for j == i and to log N_ij for every other target.  Across
+ * buckets (undo non-NULL) no key of the window is dropped for its bucket
+ * and N_ij counts window memberships. */
+static int mask_term(const int32_t *buckets, const int32_t *undo, int64_t L,
+                     int64_t chunk, int64_t after, int64_t base, int64_t i,
+                     int64_t j, int64_t r, int64_t n_rounds, int causal,
+                     double self_mask, double *M)
 {
-    if (buckets[(base + j) * n_rounds + r] != buckets[(base + i) * n_rounds + r])
+    if (!undo && buckets[(base + j) * n_rounds + r] != buckets[(base + i) * n_rounds + r])
         return 0;
     if (causal && j > i) return 0;
     if (j == i)
         *M = self_mask;
+    else if (undo)
+        *M = log((double)n_window(undo, L, i, j, n_rounds, chunk, after));
     else
         *M = log((double)n_shared(buckets, base, i, j, n_rounds));
     return 1;
 }
 
+/* undo[slice][r][perm[slice][r][s]] = s, for the across-buckets counts. */
+static int32_t *undo_of(int64_t BH, int64_t n_rounds, int64_t L, const int32_t *perm)
+{
+    int32_t *u = (int32_t *)malloc((size_t)(BH * n_rounds * L > 0 ? BH * n_rounds * L : 1) *
+                                   sizeof(int32_t));
+    if (!u) return NULL;
+    for (int64_t seg = 0; seg < BH * n_rounds; ++seg)
+        for (int64_t s = 0; s < L; ++s) u[seg * L + perm[seg * L + s]] = (int32_t)s;
+    return u;
+}
+
 /* One round of chunked LSH attention for every query (App. A, o^(r)_i and
  * z(i, P^(r)_i)).  The query at sorted slot s, in chunk c = floor(s/m),
- * looks at the keys whose slots lie in chunks c-1 and c (the set P~ of
- * Sec. 2), with logits a_ij = scale * q_i.k_j - m^(r)_ij. */
+ * looks at the keys whose slots lie in chunks c-1 .. c+after (the set P~ of
+ * Sec. 2 for after = 0), with logits a_ij = scale * q_i.k_j - m^(r)_ij. */
 int lsh_ref_chunk_attn_fwd(int64_t BH, int64_t L, int64_t d, int64_t n_rounds,
-                           int64_t chunk, int causal, double scale,
-                           double self_mask, const double *q, const double *v,
-                           const int32_t *buckets, const int32_t *perm,
-                           double *o_rounds, double *lse_rounds)
+                           int64_t chunk, int64_t after, int across, int causal,
+                           double scale, double self_mask, const double *q,
+                           const double *v, const int32_t *buckets,
+                           const int32_t *perm, double *o_rounds,
+                           double *lse_rounds)
 {
-    if (BH < 0 || L < 0 || d < 1 || n_rounds < 1 || chunk < 1 ||
+    if (BH < 0 || L < 0 || d < 1 || n_rounds < 1 || chunk < 1 || after < 0 ||
         !q || !v || !buckets || !perm || !o_rounds ||
         !lse_rounds)
         return REF_ERR_INVALID;
     double *norm = (double *)malloc((size_t)(BH * L > 0 ? BH * L : 1) * sizeof(double));
     if (!norm) return REF_ERR_NOMEM;
+    int32_t *undo = across ? undo_of(BH, n_rounds, L, perm) : NULL;
+    if (across && !undo) {
+        free(norm);
+        return REF_ERR_NOMEM;
+    }
     row_norms(BH * L, d, q, norm);
+    const int64_t span = (2 + after) * chunk; /* keys in a window */
     int err = 0;
 #pragma omp parallel
     {
-        double *a = (double *)malloc((size_t)(2 * chunk) * sizeof(double));
-        int64_t *tgt = (int64_t *)malloc((size_t)(2 * chunk) * sizeof(int64_t));
+        double *a = (double *)malloc((size_t)span * sizeof(double));
+        int64_t *tgt = (int64_t *)malloc((size_t)span * sizeof(int64_t));
         if (!a || !tgt) {
 #pragma omp atomic write
             err = 1;
@@ -239,14 +288,16 @@ int lsh_ref_chunk_attn_fwd(int64_t BH, int64_t L, int64_t d, int64_t n_rounds,
             const int64_t i = p[s];
             const int64_t c = s / chunk;
             const int64_t t_lo = (c - 1) * chunk < 0 ? 0 : (c - 1) * chunk;
-            const int64_t t_hi = (c + 1) * chunk < L ? (c + 1) * chunk : L;
+            const int64_t t_hi = (c + 1 + after) * chunk < L ? (c + 1 + after) * chunk : L;
             const double *qi = q + (base + i) * d;
+            const int32_t *u = undo ? undo + bh * n_rounds * L : NULL;
             int64_t n = 0;
             double amax = -INFINITY;
             for (int64_t t = t_lo; t < t_hi; ++t) {
                 const int64_t j = p[t];
                 double M;
-                if (!mask_term(buckets, base, i, j, r, n_rounds, causal, self_mask, &M))
+                if (!mask_term(buckets, u, L, chunk, after, base, i, j, r, n_rounds, causal,
+                               self_mask, &M))
                     continue;
                 const double nj = norm[base + j];
                 const double qk = nj > 0.0 ? dot(qi, q + (base + j) * d, d) / nj : 0.0;
@@ -272,6 +323,7 @@ int lsh_ref_chunk_attn_fwd(int64_t BH, int64_t L, int64_t d, int64_t n_rounds,
         free(tgt);
     }
     free(norm);
+    free(undo);
     return err ? REF_ERR_NOMEM : REF_OK;
 }
 
@@ -397,16 +449,19 @@ int lsh_ref_combine_rounds(int64_t BH, int64_t L, int64_t d, int64_t n_rounds,
  * The logits are recomputed from q, as the paper does for memory-efficient
  * attention (Sec. 2, "Memory-efficient attention"). */
 int lsh_ref_chunk_attn_bwd(int64_t BH, int64_t L, int64_t d, int64_t n_rounds,
-                           int64_t chunk, int causal, double scale,
-                           double self_mask, const double *q, const double *v,
-                           const double *out, const double *dout,
-                           const double *lse_total, const int32_t *buckets,
-                           const int32_t *perm, double *dq, double *dv)
+                           int64_t chunk, int64_t after, int across, int causal,
+                           double scale, double self_mask, const double *q,
+                           const double *v, const double *out,
+                           const double *dout, const double *lse_total,
+                           const int32_t *buckets, const int32_t *perm,
+                           double *dq, double *dv)
 {
-    if (BH < 0 || L < 0 || d < 1 || n_rounds < 1 || chunk < 1 ||
+    if (BH < 0 || L < 0 || d < 1 || n_rounds < 1 || chunk < 1 || after < 0 ||
         !q || !v || !out || !dout || !lse_total ||
         !buckets || !perm || !dq || !dv)
         return REF_ERR_INVALID;
+    int32_t *undo = across ? undo_of(BH, n_rounds, L, perm) : NULL;
+    if (across && !undo) return REF_ERR_NOMEM;
     int err = 0;
 #pragma omp parallel for schedule(dynamic, 1)
     for (int64_t bh = 0; bh < BH; ++bh) {
@@ -433,15 +488,17 @@ int lsh_ref_chunk_attn_bwd(int64_t BH, int64_t L, int64_t d, int64_t n_rounds,
                 const int64_t i = p[s];
                 const int64_t c = s / chunk;
                 const int64_t t_lo = (c - 1) * chunk < 0 ? 0 : (c - 1) * chunk;
-                const int64_t t_hi = (c + 1) * chunk < L ? (c + 1) * chunk : L;
+                const int64_t t_hi = (c + 1 + after) * chunk < L ? (c + 1 + after) * chunk : L;
                 const double *qi = q + (base + i) * d;
                 const double *dOi = dout + (base + i) * d;
                 const double Di = dot(dOi, out + (base + i) * d, d);
                 const double zi = lse_total[base + i];
+                const int32_t *u = undo ? undo + bh * n_rounds * L : NULL;
                 for (int64_t t = t_lo; t < t_hi; ++t) {
                     const int64_t j = p[t];
                     double M;
-                    if (!mask_term(buckets, base, i, j, r, n_rounds, causal, self_mask, &M))
+                    if (!mask_term(buckets, u, L, chunk, after, base, i, j, r, n_rounds, causal,
+                                   self_mask, &M))
                         continue;
                     const double nj = norm[j];
                     for (int64_t u = 0; u < d; ++u)
@@ -470,5 +527,6 @@ int lsh_ref_chunk_attn_bwd(int64_t BH, int64_t L, int64_t d, int64_t n_rounds,
         free(dk);
         free(kj);
     }
+    free(undo);
     return err ? REF_ERR_NOMEM : REF_OK;
 }

@@ -29,36 +29,53 @@ def _keys(q):
     return np.where(n > 0, q / np.where(n > 0, n, 1.0), 0.0)
 
 
-def dense_logits(q, buckets, chunk, causal, scale, self_mask=1e5):
-    """Logits a^(r)_ij of every (round, key) entry of every query, as dense
-    [n_r, L, L] arrays with -inf where j is no target (App. A, m^(r)_ij),
-    built from lexsort slots without any chunk loop."""
-    L, _ = q.shape
-    n_r = buckets.shape[1]
-    k = _keys(q)
+def window_masks(buckets, chunk, after=0):
+    """Per round, the [L, L] window membership of App. A's P~^(r) read from
+    lexsort slots without any chunk loop: key j is in query i's window when
+    floor(s_j/m) lies in floor(s_i/m) - 1 .. floor(s_i/m) + after."""
+    L, n_r = buckets.shape
     pos = np.arange(L)
-    N = (buckets[:, None, :] == buckets[None, :, :]).sum(-1)
-    with np.errstate(divide="ignore"):
-        logN = np.log(N.astype(np.float64))
-    M = np.where(np.eye(L, dtype=bool), self_mask, logN)
-    out = np.empty((n_r, L, L))
+    masks = []
     for r in range(n_r):
         order = np.lexsort((pos, buckets[:, r]))
         slot = np.empty(L, np.int64)
         slot[order] = pos
         ci = slot // chunk
-        window = (ci[None, :] >= ci[:, None] - 1) & (ci[None, :] <= ci[:, None])
-        same = buckets[:, r][:, None] == buckets[:, r][None, :]
-        ok = window & same
+        masks.append((ci[None, :] >= ci[:, None] - 1) & (ci[None, :] <= ci[:, None] + after))
+    return masks
+
+
+def dense_logits(q, buckets, chunk, causal, scale, self_mask=1e5, after=0, across=False):
+    """Logits a^(r)_ij of every (round, key) entry of every query, as dense
+    [n_r, L, L] arrays with -inf where j is no target (App. A, m^(r)_ij).
+    Across buckets the target set of a round is its window, and N_ij counts
+    window memberships instead of shared buckets."""
+    L, _ = q.shape
+    n_r = buckets.shape[1]
+    k = _keys(q)
+    pos = np.arange(L)
+    win = window_masks(buckets, chunk, after)
+    if across:
+        N = sum(w.astype(np.int64) for w in win)
+    else:
+        N = (buckets[:, None, :] == buckets[None, :, :]).sum(-1)
+    with np.errstate(divide="ignore"):
+        logN = np.log(N.astype(np.float64))
+    M = np.where(np.eye(L, dtype=bool), self_mask, logN)
+    out = np.empty((n_r, L, L))
+    for r in range(n_r):
+        ok = win[r].copy()
+        if not across:
+            ok &= buckets[:, r][:, None] == buckets[:, r][None, :]
         if causal:
             ok &= pos[None, :] <= pos[:, None]
         out[r] = np.where(ok, scale * (q @ k.T) - M, -np.inf)
     return out
 
 
-def dense_output(q, v, buckets, chunk, causal, scale, self_mask=1e5):
+def dense_output(q, v, buckets, chunk, causal, scale, self_mask=1e5, after=0, across=False):
     """The combined output as one softmax over every (round, key) entry."""
-    a = dense_logits(q, buckets, chunk, causal, scale, self_mask)
+    a = dense_logits(q, buckets, chunk, causal, scale, self_mask, after, across)
     L = q.shape[0]
     flat = np.transpose(a, (1, 0, 2)).reshape(L, -1)  # [L, n_r * L]
     amax = flat.max(1, keepdims=True)
@@ -69,13 +86,13 @@ def dense_output(q, v, buckets, chunk, causal, scale, self_mask=1e5):
     return w @ vv, z
 
 
-def run_oracle(q, v, buckets, chunk, causal, scale=None, self_mask=1e5):
+def run_oracle(q, v, buckets, chunk, causal, scale=None, self_mask=1e5, after=0, across=False):
     """Oracle forward on one (b, h) slice with given bucket ids."""
     L, d = q.shape
     b4 = buckets.reshape(1, 1, L, -1)
     perm, undo = oracle.lsh_sort_permute(b4)
     o_r, lse_r = oracle.lsh_chunk_attn_fwd(q.reshape(1, 1, L, d), v.reshape(1, 1, L, d), b4,
-                                           perm, chunk, causal, scale, self_mask)
+                                           perm, chunk, causal, scale, self_mask, after, across)
     out, lse = oracle.lsh_combine_rounds(o_r, lse_r, undo)
     return out[0, 0], lse[0, 0], dict(perm=perm, undo=undo, o_r=o_r, lse_r=lse_r)
 
@@ -371,24 +388,26 @@ def test_single_round_combine_identity(oracle_lib):
 # --------------------------------------------------------------------------
 # P8: backward against fp64 autograd and finite differences
 # --------------------------------------------------------------------------
-def torch_dense_loss(q, v, dout, buckets, chunk, causal, scale, self_mask=1e5):
+def torch_dense_loss(q, v, dout, buckets, chunk, causal, scale, self_mask=1e5, after=0,
+                     across=False):
     """sum(dO * O) with O the dense App. A output, differentiable in q and v."""
     L, d = q.shape
     n_r = buckets.shape[1]
     k = q / q.norm(dim=1, keepdim=True)
     pos = np.arange(L)
-    N = (buckets[:, None, :] == buckets[None, :, :]).sum(-1)
+    win = window_masks(buckets, chunk, after)
+    if across:
+        N = sum(w.astype(np.int64) for w in win)
+    else:
+        N = (buckets[:, None, :] == buckets[None, :, :]).sum(-1)
     with np.errstate(divide="ignore"):
         M = np.where(np.eye(L, dtype=bool), self_mask, np.log(N.astype(np.float64)))
     M = torch.from_numpy(M)
     logits = []
     for r in range(n_r):
-        order = np.lexsort((pos, buckets[:, r]))
-        slot = np.empty(L, np.int64)
-        slot[order] = pos
-        ci = slot // chunk
-        ok = (ci[None, :] >= ci[:, None] - 1) & (ci[None, :] <= ci[:, None])
-        ok &= buckets[:, r][:, None] == buckets[:, r][None, :]
+        ok = win[r].copy()
+        if not across:
+            ok &= buckets[:, r][:, None] == buckets[:, r][None, :]
         if causal:
             ok &= pos[None, :] <= pos[:, None]
         a = scale * (q @ k.T) - M
@@ -547,3 +566,127 @@ def test_dense_selected_rows(oracle_lib, causal):
     assert np.array_equal(o_s, out.reshape(-1, d)[rows])
     assert np.array_equal(l_s, lse.reshape(-1)[rows])
 
+
+
+# --------------------------------------------------------------------------
+# Variants (off by default; the paper does not spell them out): a look-ahead
+# chunk, attending across buckets, one R per head.  Each is pinned to a dense
+# or brute-force form that shares nothing with the oracle's loops.
+# --------------------------------------------------------------------------
+def _clustered(rng, L, d, k=4):
+    centres = rng.standard_normal((k, d))
+    return centres[rng.integers(0, k, L)] + 0.3 * rng.standard_normal((L, d))
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("after,across", [(1, False), (0, True), (1, True)])
+@pytest.mark.parametrize("L,m,n_b,n_r", [(128, 16, 4, 2), (203, 32, 8, 3), (256, 16, 16, 4)])
+def test_variants_dense_windowed(oracle_lib, causal, after, across, L, m, n_b, n_r):
+    """The chunk loops with a look-ahead and/or attention across buckets equal
+    the dense evaluation of App. A with those windows and target sets (the
+    P6 form), with buckets overflowing m and a partial last chunk."""
+    rng = _rng(L + m + n_b + n_r + causal + 10 * after + 20 * across)
+    d = 16
+    q = _clustered(rng, L, d)
+    v = rng.standard_normal((L, d))
+    R = rng.standard_normal((n_r, d, n_b // 2))
+    b = oracle.lsh_hash(q.reshape(1, 1, L, d), R)[0][0, 0]
+    out, lse, _ = run_oracle(q, v, b, chunk=m, causal=causal, after=after, across=across)
+    want, zwant = dense_output(q, v, b, m, causal, 1.0 / np.sqrt(d), after=after, across=across)
+    np.testing.assert_allclose(out, want, atol=1e-10, rtol=0)
+    np.testing.assert_allclose(lse, zwant, atol=1e-9, rtol=1e-13)
+
+
+def test_lookahead_covers_small_buckets_non_causal(oracle_lib):
+    """Without causal masking P~ misses the part of a bucket that spills into
+    the next chunk, so the rounds do not add up to attention over the union of
+    buckets even when every bucket holds at most m tokens; one look-ahead
+    chunk closes that gap (Sec. 2, 'If max |P_i| < m then P_i is a subset of
+    P~_i')."""
+    rng = _rng(6)
+    L, d, m, n_rounds = 256, 16, 16, 3
+    q = rng.standard_normal((L, d))
+    v = rng.standard_normal((L, d))
+    b = np.stack([rng.permutation(np.arange(L) % (L // 12)) for _ in range(n_rounds)], 1)
+    b = b.astype(np.int32)
+    assert max(np.bincount(b[:, r]).max() for r in range(n_rounds)) <= m
+    want = union_attention(q, v, b, False, 1.0 / np.sqrt(d))
+    plain, _, _ = run_oracle(q, v, b, chunk=m, causal=False)
+    ahead, _, _ = run_oracle(q, v, b, chunk=m, causal=False, after=1)
+    assert np.abs(plain - want).max() > 1e-3  # the gap is real
+    np.testing.assert_allclose(ahead, want, atol=1e-10, rtol=0)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_across_one_chunk_is_dense(oracle_lib, causal):
+    """Across buckets with one chunk spanning the sequence every round's
+    target set is every key, N_ij = n_rounds for every pair and the output is
+    dense self-masked shared-QK attention (eq. attn with k = q/|q|) whatever
+    the bucket ids."""
+    rng = _rng(61 + causal)
+    L, d, n_r = 96, 16, 3
+    q = rng.standard_normal((L, d))
+    v = rng.standard_normal((L, d))
+    b = rng.integers(0, 8, size=(L, n_r)).astype(np.int32)
+    out, _, _ = run_oracle(q, v, b, chunk=L, causal=causal, across=True)
+    k = _keys(q)
+    a = q @ k.T / np.sqrt(d)
+    ok = ~np.eye(L, dtype=bool)
+    if causal:
+        ok &= np.tri(L, dtype=bool)
+    a = np.where(ok, a, -np.inf)
+    want = np.empty_like(v)
+    for i in range(L):
+        if not ok[i].any():
+            want[i] = v[i]
+            continue
+        w = np.exp(a[i] - a[i].max())
+        want[i] = (w / w.sum()) @ v
+    np.testing.assert_allclose(out, want, atol=1e-10, rtol=0)
+
+
+@pytest.mark.parametrize("after,across", [(1, False), (0, True), (1, True)])
+def test_variants_backward_autograd(oracle_lib, after, across):
+    """The backward of the variants against fp64 autograd of the dense form."""
+    rng = _rng(71 + after + 2 * across)
+    L, d, n_r, n_b, m = 113, 16, 3, 8, 16
+    for causal in (False, True):
+        q = _clustered(rng, L, d)
+        v = rng.standard_normal((L, d))
+        dout = rng.standard_normal((L, d))
+        R = rng.standard_normal((n_r, d, n_b // 2))
+        buckets, _ = oracle.lsh_hash(q.reshape(1, 1, L, d), R)
+        b = buckets[0, 0]
+        scale = 1.0 / np.sqrt(d)
+        qt = torch.tensor(q, requires_grad=True)
+        vt = torch.tensor(v, requires_grad=True)
+        loss, out_t = torch_dense_loss(qt, vt, torch.tensor(dout), b, m, causal, scale,
+                                       after=after, across=across)
+        loss.backward()
+        out, lse, _ = run_oracle(q, v, b, chunk=m, causal=causal, after=after, across=across)
+        np.testing.assert_allclose(out, out_t.detach().numpy(), atol=1e-10, rtol=0)
+        dq, dv = oracle.lsh_chunk_attn_bwd(q[None, None], v[None, None], out[None, None],
+                                           dout[None, None], lse[None, None], buckets,
+                                           oracle.lsh_sort_permute(buckets)[0], m, causal,
+                                           after=after, across=across)
+        np.testing.assert_allclose(dq[0, 0], qt.grad.numpy(), atol=1e-10, rtol=0)
+        np.testing.assert_allclose(dv[0, 0], vt.grad.numpy(), atol=1e-10, rtol=0)
+
+
+def test_hash_per_head(oracle_lib):
+    """One R per head: head h's ids are the brute-force argmax of
+    [x R_h; -x R_h] (Sec. 2), and R repeated over the heads gives the ids of
+    the shared R."""
+    rng = _rng(81)
+    B, H, L, d, n_r, n_b = 2, 3, 40, 16, 2, 16
+    q = rng.standard_normal((B, H, L, d))
+    Rh = rng.standard_normal((H, n_r, d, n_b // 2))
+    got, _ = oracle.lsh_hash(q, Rh)
+    for h in range(H):
+        for r in range(n_r):
+            p = q[:, h] @ Rh[h, r]
+            want = np.argmax(np.concatenate([p, -p], axis=-1), axis=-1)
+            assert np.array_equal(got[:, h, :, r], want)
+    shared, _ = oracle.lsh_hash(q, Rh[0])
+    same, _ = oracle.lsh_hash(q, np.repeat(Rh[:1], H, axis=0))
+    assert np.array_equal(same, shared)
