@@ -51,7 +51,9 @@
  *   every row (App. A sets the self mask to 1e5).
  * Supported on the GPU: d = 64, chunk = 64 (and chunk = 128, the length of the
  *   paper's usual configuration, Sec. 5, on the fp32 forward; entry points that
- *   do not use the chunk ignore it), 2 <= n_buckets <= 1024 (even),
+ *   do not use the chunk ignore it), chunks_after <= 1 and attend_across on the
+ *   fp32 forward (the bf16 forward and the backward return LSH_ERR_UNSUPPORTED
+ *   for them), r_per_head everywhere, 2 <= n_buckets <= 1024 (even),
  *   1 <= n_rounds <= 16, B*H*L*n_rounds < 2^31.  L need not be a multiple of
  *   the chunk: the last chunk then holds the L mod m remaining sorted slots
  *   (the paper is silent; read as padding with tokens that are no one's
@@ -102,6 +104,15 @@ typedef struct lsh_config {
     int32_t causal;    /* nonzero: a position never attends to a later one */
     float scale;       /* logit scale, 1/sqrt(d_k) in eq. attn */
     float self_mask;   /* mask value for j == i, 1e5 in App. A */
+    /* Variants the paper does not spell out (0 = the paper's method): */
+    int32_t chunks_after;  /* look-ahead: the window of chunk c is chunks c-1 .. c+after
+                              (one chunk closes the non-causal gap in Sec. 2's claim that
+                              buckets smaller than m lie inside the window) */
+    int32_t attend_across; /* nonzero: every key of the window is a target, not only the
+                              query's bucket; N_ij counts the rounds in which j falls in
+                              i's window (App. A with P^(r)_i read as the window) */
+    int32_t r_per_head;    /* nonzero: R holds one [n_rounds][d][n_buckets/2] set per head,
+                              [H][n_rounds][d][n_buckets/2] */
 } lsh_config;
 
 /* Human-readable name of a status code (static storage). */
@@ -112,7 +123,9 @@ size_t lsh_workspace_bytes(const lsh_config *cfg, lsh_dtype dtype, int op);
 
 /* Angular LSH of every query in every round (Sec. 2, "Locality sensitive
  * hashing": h(x) = argmax([xR; -xR]), one R per round as in eq.
- * union-pairs).  R is shared by every batch entry and head.  The hash is of
+ * union-pairs).  R is shared by every batch entry and head, or with
+ * r_per_head one set per head, [H][n_rounds][d][n_buckets/2] (each (batch,
+ * head) slice is then hashed in its own pass).  The hash is of
  * the stored q (the normalised key has the same hash).  Ties in the argmax
  * resolve to the first index of [xR; -xR].  The ids equal those of the exact
  * argmax: projections are screened with bf16 matrix cores under a
@@ -168,6 +181,8 @@ int lsh_gather_rows(const lsh_config *cfg, lsh_dtype dtype, const void *src,
  * rounds in which j shares i's bucket).
  *   q, v          [B][H][L][d] (dtype), in original position order
  *   buckets, perm, bucket_start: as written by lsh_hash / lsh_sort_permute
+ *   undo          as written by lsh_sort_permute; read only with attend_across
+ *                 (where it must not be NULL; it may be NULL otherwise)
  *   o_rounds      [B][H][n_rounds][L][d] (written, sorted order): each round's
  *                 output, accumulated and normalised in fp32, stored as fp32
  *                 (fp32 calls) or as fp16 scaled by 2^-o_exp (bf16 calls)
@@ -178,7 +193,7 @@ int lsh_gather_rows(const lsh_config *cfg, lsh_dtype dtype, const void *src,
  *                 (per-token key scales and packed bucket ids for bf16 calls;
  *                 0 bytes, and workspace may be NULL, for fp32 calls) */
 int lsh_chunk_attn_fwd(const lsh_config *cfg, lsh_dtype dtype, const void *q, const void *v,
-                       const int32_t *buckets, const int32_t *perm,
+                       const int32_t *buckets, const int32_t *perm, const int32_t *undo,
                        const int32_t *bucket_start, void *o_rounds, uint8_t *o_exp,
                        float *lse_rounds, void *workspace, size_t workspace_bytes,
                        void *stream);

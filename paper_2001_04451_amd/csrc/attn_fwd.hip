@@ -394,96 +394,128 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
 // fp32 path: one workgroup per chunk of M sorted slots (M = 64, or 128, the
 // chunk length of the paper's usual configuration), one lane per query,
 // exact fp32 arithmetic on the VALU with an online softmax over the query's
-// key interval.  The window (chunks c-1 and c) is staged in LDS.
+// keys.  The window is chunks c-1 .. c+after; it is walked one chunk at a
+// time (the query's own chunk first), each staged in LDS.  Two variants the
+// paper does not spell out: a look-ahead of `after` chunks, and attending
+// across buckets (every key of the window is a target, and N_ij counts the
+// rounds in which j falls in i's window, from undo).
 template <int M>
 __global__ __launch_bounds__(M) void attn_fwd_f32_kernel(
     const float* __restrict__ q, const float* __restrict__ v, const int32_t* __restrict__ buckets,
-    const int32_t* __restrict__ perm, const int32_t* __restrict__ bstart,
-    float* __restrict__ o_rounds, float* __restrict__ lse_rounds, int L, int n_r, int n_b,
-    int causal, float scale, float self_mask) {
-    __shared__ float Ks[2 * M][kHeadDim + 1];
-    __shared__ float Vs2[2 * M][kHeadDim + 1];
-    __shared__ float inv[2 * M];
-    __shared__ int spos[2 * M];
+    const int32_t* __restrict__ perm, const int32_t* __restrict__ undo,
+    const int32_t* __restrict__ bstart, float* __restrict__ o_rounds,
+    float* __restrict__ lse_rounds, int L, int n_r, int n_b, int causal, int after, int across,
+    float scale, float self_mask) {
+    __shared__ float Ks[M][kHeadDim + 1];
+    __shared__ float Vs2[M][kHeadDim + 1];
+    __shared__ float inv[M];
+    __shared__ int spos[M];
 
     const int t = threadIdx.x;
     const int64_t seg = blockIdx.y;
     const int64_t bh = seg / n_r;
     const int r = (int)(seg % n_r);
     const int c = blockIdx.x;
-    const int slot0 = (c - 1) * M;
-    // staging, in two passes so that no row load waits on its own position
-    // load: the window's positions (-1 outside the sequence), then thread t
-    // copies dim t % 64 of row t / 64 of each group of M / 64 rows, from
-    // clamped addresses
-    for (int rho = t; rho < 2 * M; rho += M) {
-        const int slot = slot0 + rho;
-        const int pos = min(max(perm[seg * L + min(max(slot, 0), L - 1)], 0), L - 1);
-        spos[rho] = slot >= 0 && slot < L ? pos : -1;
-    }
-    __syncthreads();
-    constexpr int kRowsPerPass = M / kHeadDim;
-    const int dcol = t % kHeadDim, rsub = t / kHeadDim;
-#pragma unroll 8
-    for (int rho0 = 0; rho0 < 2 * M; rho0 += kRowsPerPass) {
-        const int rho = rho0 + rsub;
-        const int pos = spos[rho];
-        const int64_t src = (bh * L + max(pos, 0)) * kHeadDim + dcol;
-        const float kq = q[src], kv = v[src];
-        Ks[rho][dcol] = pos >= 0 ? kq : 0.f;
-        Vs2[rho][dcol] = pos >= 0 ? kv : 0.f;
-    }
-    __syncthreads();
-    for (int rr = t; rr < 2 * M; rr += M) {
-        float ss = 0.f;
-        for (int u = 0; u < kHeadDim; ++u) ss = fmaf(Ks[rr][u], Ks[rr][u], ss);
-        inv[rr] = ss > 0.f ? 1.f / sqrtf(ss) : 0.f;
-    }
-    __syncthreads();
-
-    const int rq = M + t;
     const int s_q = c * M + t;
-    if (s_q >= L) return;  // a slot past L (a partial last chunk): no query, no barrier follows
-    const int i_q = spos[rq];
+    const bool has_q = s_q < L;  // a slot past L (a partial last chunk) has no query
+    const int32_t* pseg = perm + seg * L;
+    const int i_q = pseg[min(s_q, L - 1)];
     const int32_t* bi = buckets + (bh * L + i_q) * n_r;
     const int beta = min(max(bi[r], 0), n_b - 1);
     const int32_t* bs = bstart + seg * (n_b + 1);
-    const int lo = max(bs[beta], max(0, slot0));
-    const int hi = causal ? s_q - 1 : min(bs[beta + 1], (c + 1) * M) - 1;
+    const int w_lo = max(0, (c - 1) * M), w_hi = min(L, (c + 1 + after) * M) - 1;  // window slots
+    // the query's keys: its bucket's slots inside the window, or the whole
+    // window across buckets.  No key later than the query under causal
+    // masking: inside one bucket slot order is position order, so that is
+    // the slot bound s_q - 1; across buckets it is a test of positions.
+    const int lo = across ? w_lo : max(bs[beta], w_lo);
+    const int hi = across ? w_hi : (causal ? s_q - 1 : min(bs[beta + 1] - 1, w_hi));
+    const bool pos_causal = across && causal;
+    // across buckets: the query's chunk in every round
+    int ci[16];
+    if (across)
+        for (int rr = 0; rr < n_r; ++rr) ci[rr] = undo[(bh * n_r + rr) * L + i_q] / M;
 
     float qi[kHeadDim];
-    for (int u = 0; u < kHeadDim; ++u) qi[u] = Ks[rq][u];
     float m = -__builtin_inff(), l = 0.f;
     float o[kHeadDim];
     for (int u = 0; u < kHeadDim; ++u) o[u] = 0.f;
-    for (int tk = lo; tk <= hi; ++tk) {
-        if (tk == s_q) continue;
-        const int rho = tk - slot0;
-        float dot = 0.f;
-        for (int u = 0; u < kHeadDim; ++u) dot = fmaf(qi[u], Ks[rho][u], dot);
-        float a = scale * (dot * inv[rho]);
-        if (n_r > 1) {
-            const int32_t* bj = buckets + (bh * L + spos[rho]) * n_r;
-            int nn = 0;
-            for (int rr = 0; rr < n_r; ++rr) nn += bi[rr] == bj[rr];
-            a -= logf((float)nn);
+    const int n_win = 2 + after;
+    for (int piece = 0; piece < n_win; ++piece) {
+        // chunk c first (it holds the queries), then c-1, c+1, ...
+        const int k = piece == 0 ? c : (piece == 1 ? c - 1 : c + piece - 1);
+        const int slot0 = k * M;
+        __syncthreads();  // the previous piece is no longer read
+        // positions first, then thread t copies dim t % 64 of row t / 64 of
+        // each group of M / 64 rows, from clamped addresses
+        {
+            const int slot = slot0 + t;
+            const int pos = min(max(pseg[min(max(slot, 0), L - 1)], 0), L - 1);
+            spos[t] = slot >= 0 && slot < L ? pos : -1;
         }
-        const float mn = fmaxf(m, a);
-        const float corr = expf(m - mn);
-        const float p = expf(a - mn);
-        l = l * corr + p;
-        for (int u = 0; u < kHeadDim; ++u) o[u] = fmaf(o[u], corr, p * Vs2[rho][u]);
-        m = mn;
+        __syncthreads();
+        constexpr int kRowsPerPass = M / kHeadDim;
+        const int dcol = t % kHeadDim, rsub = t / kHeadDim;
+#pragma unroll 8
+        for (int rho0 = 0; rho0 < M; rho0 += kRowsPerPass) {
+            const int rho = rho0 + rsub;
+            const int pos = spos[rho];
+            const int64_t src = (bh * L + max(pos, 0)) * kHeadDim + dcol;
+            const float kq = q[src], kv = v[src];
+            Ks[rho][dcol] = pos >= 0 ? kq : 0.f;
+            Vs2[rho][dcol] = pos >= 0 ? kv : 0.f;
+        }
+        __syncthreads();
+        {
+            float ss = 0.f;
+            for (int u = 0; u < kHeadDim; ++u) ss = fmaf(Ks[t][u], Ks[t][u], ss);
+            inv[t] = ss > 0.f ? 1.f / sqrtf(ss) : 0.f;
+        }
+        if (piece == 0)
+            for (int u = 0; u < kHeadDim; ++u) qi[u] = Ks[t][u];
+        __syncthreads();
+        if (!has_q) continue;
+        const int t_lo = max(lo, slot0), t_hi = min(hi, slot0 + M - 1);
+        for (int tk = t_lo; tk <= t_hi; ++tk) {
+            if (tk == s_q) continue;
+            const int rho = tk - slot0;
+            if (pos_causal && spos[rho] > i_q) continue;
+            float dot = 0.f;
+            for (int u = 0; u < kHeadDim; ++u) dot = fmaf(qi[u], Ks[rho][u], dot);
+            float a = scale * (dot * inv[rho]);
+            if (n_r > 1) {
+                int nn = 0;
+                if (across) {
+                    for (int rr = 0; rr < n_r; ++rr) {
+                        const int cj = undo[(bh * n_r + rr) * L + spos[rho]] / M;
+                        nn += cj >= ci[rr] - 1 && cj <= ci[rr] + after;
+                    }
+                } else {
+                    const int32_t* bj = buckets + (bh * L + spos[rho]) * n_r;
+                    for (int rr = 0; rr < n_r; ++rr) nn += bi[rr] == bj[rr];
+                }
+                a -= logf((float)nn);
+            }
+            const float mn = fmaxf(m, a);
+            const float corr = expf(m - mn);
+            const float p = expf(a - mn);
+            l = l * corr + p;
+            for (int u = 0; u < kHeadDim; ++u) o[u] = fmaf(o[u], corr, p * Vs2[rho][u]);
+            m = mn;
+        }
     }
+    if (!has_q) return;
     float* orow = o_rounds + (seg * L + s_q) * kHeadDim;
     if (l > 0.f) {
         const float il = 1.f / l;
         for (int u = 0; u < kHeadDim; ++u) orow[u] = o[u] * il;
         lse_rounds[seg * L + s_q] = m + logf(l);
     } else {
+        // only itself left as a target: v_i, log-partition scale*|q_i| - self_mask
         float ss = 0.f;
         for (int u = 0; u < kHeadDim; ++u) ss = fmaf(qi[u], qi[u], ss);
-        for (int u = 0; u < kHeadDim; ++u) orow[u] = Vs2[rq][u];
+        const int64_t src = (bh * L + i_q) * kHeadDim;
+        for (int u = 0; u < kHeadDim; ++u) orow[u] = v[src + u];
         lse_rounds[seg * L + s_q] = scale * sqrtf(ss) - self_mask;
     }
 }
@@ -567,9 +599,10 @@ size_t attn_fwd_workspace_bytes(int64_t BH, int L, int n_rounds, bool f32) {
     return align256(rows * 4 * rec_words);
 }
 
-hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, int chunk, bool causal,
-                           float scale, float self_mask, bool f32, const void* q, const void* v,
-                           const int32_t* buckets, const int32_t* perm,
+hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, int chunk, int after,
+                           bool across, bool causal, float scale, float self_mask, bool f32,
+                           const void* q, const void* v, const int32_t* buckets,
+                           const int32_t* perm, const int32_t* undo,
                            const int32_t* bucket_start, void* o_rounds, uint8_t* o_exp,
                            float* lse_rounds, void* workspace, hipStream_t stream) {
     if (BH == 0 || L == 0) return hipSuccess;
@@ -578,14 +611,14 @@ hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, int c
         const dim3 grid((unsigned)((L + chunk - 1) / chunk), segs);
         if (chunk == 128)
             attn_fwd_f32_kernel<128><<<grid, 128, 0, stream>>>(
-                static_cast<const float*>(q), static_cast<const float*>(v), buckets, perm, bucket_start,
-                static_cast<float*>(o_rounds), lse_rounds, L, n_rounds, n_buckets, causal ? 1 : 0, scale,
-                self_mask);
+                static_cast<const float*>(q), static_cast<const float*>(v), buckets, perm, undo,
+                bucket_start, static_cast<float*>(o_rounds), lse_rounds, L, n_rounds, n_buckets,
+                causal ? 1 : 0, after, across ? 1 : 0, scale, self_mask);
         else
             attn_fwd_f32_kernel<64><<<grid, 64, 0, stream>>>(
-                static_cast<const float*>(q), static_cast<const float*>(v), buckets, perm, bucket_start,
-                static_cast<float*>(o_rounds), lse_rounds, L, n_rounds, n_buckets, causal ? 1 : 0, scale,
-                self_mask);
+                static_cast<const float*>(q), static_cast<const float*>(v), buckets, perm, undo,
+                bucket_start, static_cast<float*>(o_rounds), lse_rounds, L, n_rounds, n_buckets,
+                causal ? 1 : 0, after, across ? 1 : 0, scale, self_mask);
         return hipGetLastError();
     }
     const uint16_t* qb = static_cast<const uint16_t*>(q);

@@ -39,9 +39,10 @@ hipError_t launch_gather(int64_t BH, int L, int n_rounds, bool f32, const void* 
 
 // ---- chunked attention, forward ----
 size_t attn_fwd_workspace_bytes(int64_t BH, int L, int n_rounds, bool f32);
-hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, int chunk, bool causal,
-                           float scale, float self_mask, bool f32, const void* q, const void* v,
-                           const int32_t* buckets, const int32_t* perm,
+hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, int chunk, int after,
+                           bool across, bool causal, float scale, float self_mask, bool f32,
+                           const void* q, const void* v, const int32_t* buckets,
+                           const int32_t* perm, const int32_t* undo,
                            const int32_t* bucket_start, void* o_rounds, uint8_t* o_exp,
                            float* lse_rounds, void* workspace, hipStream_t stream);
 

@@ -28,6 +28,7 @@ int check_config(const lsh_config* cfg) {
     if (cfg->n_buckets < 2 || (cfg->n_buckets % 2) != 0) return LSH_ERR_INVALID;
     if (cfg->n_rounds < 1 || cfg->chunk < 1) return LSH_ERR_INVALID;
     if (!finitef(cfg->scale) || !finitef(cfg->self_mask)) return LSH_ERR_INVALID;
+    if (cfg->chunks_after < 0) return LSH_ERR_INVALID;
     return LSH_OK;
 }
 
@@ -53,12 +54,20 @@ int check_self_mask(const lsh_config* cfg) {
     return cfg->self_mask >= kMinSelfMask ? LSH_OK : LSH_ERR_UNSUPPORTED;
 }
 
-// Chunk lengths of the chunked-attention kernels: 64 everywhere, and 128 on
-// the fp32 forward.
+// What the chunked-attention kernels take: chunks of 64 everywhere and of 128
+// on the fp32 forward; a look-ahead of at most one chunk and attention across
+// buckets on the fp32 forward; the backward only the paper's own window
+// (chunks of 64, no look-ahead, bucket-restricted targets).
 int check_chunk(const lsh_config* cfg, int dtype, bool backward) {
-    if (cfg->chunk == lsh::kChunkHost) return LSH_OK;
-    if (cfg->chunk == 128 && dtype == LSH_F32 && !backward) return LSH_OK;
-    return LSH_ERR_UNSUPPORTED;
+    if (cfg->chunks_after > 1) return LSH_ERR_UNSUPPORTED;
+    if (backward)
+        return cfg->chunk == lsh::kChunkHost && cfg->chunks_after == 0 && !cfg->attend_across
+                   ? LSH_OK
+                   : LSH_ERR_UNSUPPORTED;
+    if (dtype == LSH_F32) return cfg->chunk == 64 || cfg->chunk == 128 ? LSH_OK : LSH_ERR_UNSUPPORTED;
+    if (cfg->chunk != lsh::kChunkHost || cfg->chunks_after != 0 || cfg->attend_across)
+        return LSH_ERR_UNSUPPORTED;
+    return LSH_OK;
 }
 
 // The dense baseline reads only the shape, the mask flag and the scales.
@@ -156,9 +165,24 @@ int lsh_hash(const lsh_config* cfg, lsh_dtype dtype, const void* q, const float*
     if (workspace_bytes < lsh::hash_workspace_bytes(bh_of(cfg) * cfg->L, cfg->n_rounds, cfg->n_buckets))
         return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
-    const int64_t rows = bh_of(cfg) * cfg->L;
-    return status_of(lsh::launch_hash(q, dtype == LSH_F32, rows, cfg->n_rounds, cfg->n_buckets, R,
-                                      buckets, workspace, static_cast<hipStream_t>(stream)));
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    const bool f32 = dtype == LSH_F32;
+    if (!cfg->r_per_head) {
+        const int64_t rows = bh_of(cfg) * cfg->L;
+        return status_of(lsh::launch_hash(q, f32, rows, cfg->n_rounds, cfg->n_buckets, R, buckets,
+                                          workspace, st));
+    }
+    // one R per head: every (batch, head) slice is hashed with its head's R,
+    // slice by slice (the slices share nothing, and each pass needs one R)
+    const size_t r_set = (size_t)cfg->n_rounds * cfg->d * (cfg->n_buckets / 2);
+    const size_t row_bytes = (size_t)cfg->d * elem_bytes(dtype);
+    for (int64_t bh = 0; bh < bh_of(cfg); ++bh) {
+        const int64_t row0 = bh * cfg->L;
+        LSH_TRY(status_of(lsh::launch_hash(static_cast<const char*>(q) + row0 * row_bytes, f32, cfg->L,
+                                           cfg->n_rounds, cfg->n_buckets, R + (bh % cfg->H) * r_set,
+                                           buckets + row0 * cfg->n_rounds, workspace, st)));
+    }
+    return LSH_OK;
 }
 
 int lsh_sort_permute(const lsh_config* cfg, const int32_t* buckets, int32_t* perm, int32_t* undo,
@@ -203,13 +227,14 @@ int lsh_gather_rows(const lsh_config* cfg, lsh_dtype dtype, const void* src, con
 }
 
 int lsh_chunk_attn_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, const void* v,
-                       const int32_t* buckets, const int32_t* perm, const int32_t* bucket_start,
-                       void* o_rounds, uint8_t* o_exp, float* lse_rounds, void* workspace,
-                       size_t workspace_bytes, void* stream) {
+                       const int32_t* buckets, const int32_t* perm, const int32_t* undo,
+                       const int32_t* bucket_start, void* o_rounds, uint8_t* o_exp,
+                       float* lse_rounds, void* workspace, size_t workspace_bytes, void* stream) {
     LSH_TRY(check_config(cfg));
     LSH_TRY(check_dtype(dtype));
     if (!q || !v || !buckets || !perm || !bucket_start || !o_rounds || !lse_rounds)
         return LSH_ERR_INVALID;
+    if (cfg->attend_across && !undo) return LSH_ERR_INVALID;
     if (dtype == LSH_BF16 && !o_exp) return LSH_ERR_INVALID;
     if (!all_aligned(q, v, o_rounds)) return LSH_ERR_INVALID;
     const size_t need = lsh_workspace_bytes(cfg, dtype, LSH_OP_ATTN_FWD);
@@ -219,8 +244,9 @@ int lsh_chunk_attn_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, co
     LSH_TRY(check_chunk(cfg, dtype, false));
     LSH_TRY(check_self_mask(cfg));
     return status_of(lsh::launch_attn_fwd(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets, cfg->chunk,
+                                          cfg->chunks_after, cfg->attend_across != 0,
                                           cfg->causal != 0, cfg->scale, cfg->self_mask,
-                                          dtype == LSH_F32, q, v, buckets, perm, bucket_start,
+                                          dtype == LSH_F32, q, v, buckets, perm, undo, bucket_start,
                                           o_rounds, o_exp, lse_rounds, workspace,
                                           static_cast<hipStream_t>(stream)));
 }
@@ -260,8 +286,8 @@ int lsh_attention_fwd(const lsh_config* cfg, lsh_dtype dtype, const void* q, con
     const size_t scratch_bytes = workspace_bytes - fwd_rounds_bytes(cfg, dtype);
     LSH_TRY(lsh_hash(cfg, dtype, q, R, buckets, scratch, scratch_bytes, stream));
     LSH_TRY(lsh_sort_permute(cfg, buckets, perm, undo, bucket_start, scratch, scratch_bytes, stream));
-    LSH_TRY(lsh_chunk_attn_fwd(cfg, dtype, q, v, buckets, perm, bucket_start, o_rounds, o_exp,
-                               lse_rounds, scratch, scratch_bytes, stream));
+    LSH_TRY(lsh_chunk_attn_fwd(cfg, dtype, q, v, buckets, perm, undo, bucket_start, o_rounds,
+                               o_exp, lse_rounds, scratch, scratch_bytes, stream));
     return lsh_combine_rounds(cfg, dtype, o_rounds, o_exp, lse_rounds, undo, out, lse_total, stream);
 }
 

@@ -42,7 +42,8 @@ class LshConfig(ctypes.Structure):
                 ("d", ctypes.c_int32), ("n_buckets", ctypes.c_int32),
                 ("n_rounds", ctypes.c_int32), ("chunk", ctypes.c_int32),
                 ("causal", ctypes.c_int32), ("scale", ctypes.c_float),
-                ("self_mask", ctypes.c_float)]
+                ("self_mask", ctypes.c_float), ("chunks_after", ctypes.c_int32),
+                ("attend_across", ctypes.c_int32), ("r_per_head", ctypes.c_int32)]
 
 
 class LshError(RuntimeError):
@@ -75,7 +76,7 @@ def lib() -> ctypes.CDLL:
             "lsh_sort_permute": [_CFG, _P, _P, _P, _P, _P, _SZ, _P],
             "lsh_sort_permute_static": [_CFG, _P, _P, _P, _P, _P],
             "lsh_gather_rows": [_CFG, _I, _P, _P, _P, _P],
-            "lsh_chunk_attn_fwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
+            "lsh_chunk_attn_fwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
             "lsh_combine_rounds": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P],
             "lsh_attention_fwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
             "lsh_chunk_attn_bwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ,
@@ -105,17 +106,28 @@ class Config:
     d: int = 64
     scale: float | None = None
     self_mask: float = 1e5
+    chunks_after: int = 0
+    attend_across: bool = False
+    r_per_head: bool = False
 
     def c(self) -> LshConfig:
         scale = 1.0 / math.sqrt(self.d) if self.scale is None else self.scale
         return LshConfig(self.B, self.H, self.L, self.d, self.n_buckets, self.n_rounds, self.chunk,
-                         int(bool(self.causal)), scale, self.self_mask)
+                         int(bool(self.causal)), scale, self.self_mask, int(self.chunks_after),
+                         int(bool(self.attend_across)), int(bool(self.r_per_head)))
+
+    def r_shape(self) -> tuple:
+        """Shape of R: one set per round, or per head and round with r_per_head."""
+        base = (self.n_rounds, self.d, self.n_buckets // 2)
+        return (self.H,) + base if self.r_per_head else base
 
     @staticmethod
-    def of(w) -> "Config":
-        """From a workloads.Workload."""
-        return Config(B=w.B, H=w.H, L=w.L, n_buckets=w.n_buckets, n_rounds=w.n_rounds,
-                      chunk=w.chunk, causal=w.causal, d=w.d)
+    def of(w, **kw) -> "Config":
+        """From a workloads.Workload (keyword arguments override fields)."""
+        c = dict(B=w.B, H=w.H, L=w.L, n_buckets=w.n_buckets, n_rounds=w.n_rounds, chunk=w.chunk,
+                 causal=w.causal, d=w.d)
+        c.update(kw)
+        return Config(**c)
 
 
 def _dtype_code(t: torch.Tensor) -> int:
@@ -167,7 +179,7 @@ def lsh_hash(cfg: Config, q: torch.Tensor, R: torch.Tensor, buckets: torch.Tenso
          workspace: torch.Tensor | None = None) -> torch.Tensor:
     """Bucket ids [B,H,L,n_rounds] int32 (lsh_hash)."""
     _need(q, (cfg.B, cfg.H, cfg.L, cfg.d), name="q")
-    _need(R, (cfg.n_rounds, cfg.d, cfg.n_buckets // 2), torch.float32, "R")
+    _need(R, cfg.r_shape(), torch.float32, "R")
     if buckets is None:
         buckets = torch.empty((cfg.B, cfg.H, cfg.L, cfg.n_rounds), dtype=torch.int32, device=q.device)
     if workspace is None:
@@ -219,7 +231,7 @@ def rounds_dtype(dtype: torch.dtype) -> torch.dtype:
 
 
 def lsh_chunk_attn_fwd(cfg: Config, q, v, buckets, perm, bstart, o_rounds=None, o_exp=None,
-                       lse_rounds=None, workspace=None):
+                       lse_rounds=None, workspace=None, undo=None):
     """Per-round outputs in sorted order (lsh_chunk_attn_fwd): o_rounds [B,H,n_r,L,d]
     (fp32 for fp32 q; fp16 scaled by 2^-o_exp for bf16 q), o_exp [B,H,n_r,L] uint8
     (None for fp32 q) and lse_rounds [B,H,n_r,L] fp32."""
@@ -228,6 +240,10 @@ def lsh_chunk_attn_fwd(cfg: Config, q, v, buckets, perm, bstart, o_rounds=None, 
     _need(perm, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.int32, "perm")
     _need(bstart, (cfg.B, cfg.H, cfg.n_rounds, cfg.n_buckets + 1), torch.int32, "bucket_start")
     _need(buckets, (cfg.B, cfg.H, cfg.L, cfg.n_rounds), torch.int32, "buckets")
+    if undo is not None:
+        _need(undo, (cfg.B, cfg.H, cfg.n_rounds, cfg.L), torch.int32, "undo")
+    elif cfg.attend_across:
+        raise ValueError("undo is required with attend_across")
     dev = q.device
     rdt = rounds_dtype(q.dtype)
     if o_rounds is None:
@@ -249,7 +265,7 @@ def lsh_chunk_attn_fwd(cfg: Config, q, v, buckets, perm, bstart, o_rounds=None, 
         workspace = _workspace(cfg, q.dtype, LSH_OP_ATTN_FWD, dev)
     _check("lsh_chunk_attn_fwd",
            lib().lsh_chunk_attn_fwd(ctypes.byref(cfg.c()), _dtype_code(q), _ptr(q), _ptr(v),
-                                    _ptr(buckets), _ptr(perm), _ptr(bstart), _ptr(o_rounds),
+                                    _ptr(buckets), _ptr(perm), _ptr(undo), _ptr(bstart), _ptr(o_rounds),
                                     _ptr(o_exp), _ptr(lse_rounds), _ptr(workspace),
                                     workspace.numel(), _stream(dev)))
     return o_rounds, o_exp, lse_rounds
@@ -300,7 +316,7 @@ def lsh_attention_fwd(cfg: Config, q, v, R, state: ForwardState | None = None) -
     """The whole forward (lsh_attention_fwd): hash, sort, chunked attention, combine."""
     _need(q, (cfg.B, cfg.H, cfg.L, cfg.d), name="q")
     _need(v, (cfg.B, cfg.H, cfg.L, cfg.d), q.dtype, "v")
-    _need(R, (cfg.n_rounds, cfg.d, cfg.n_buckets // 2), torch.float32, "R")
+    _need(R, cfg.r_shape(), torch.float32, "R")
     if state is None:
         state = ForwardState(cfg, q.dtype, q.device)
     s = state

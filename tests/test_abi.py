@@ -57,7 +57,7 @@ def test_invalid_config(L, bad):
     rc = L.lsh_hash(ctypes.byref(c), lsh.LSH_BF16, FAKE, FAKE, FAKE, FAKE, 1 << 30, None)
     assert rc == lsh.LSH_ERR_INVALID
     rc = L.lsh_chunk_attn_fwd(ctypes.byref(c), lsh.LSH_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                              FAKE, FAKE, FAKE, 1 << 30, None)
+                              FAKE, FAKE, FAKE, FAKE, 1 << 30, None)
     assert rc == lsh.LSH_ERR_INVALID
     assert L.lsh_workspace_bytes(ctypes.byref(c), lsh.LSH_BF16, lsh.LSH_OP_FORWARD) == 0
 
@@ -82,12 +82,12 @@ def test_null_pointers_and_small_workspace(L):
     # bf16 attention needs its per-token workspace; fp32 needs none
     attn = L.lsh_workspace_bytes(ctypes.byref(c), 1, lsh.LSH_OP_ATTN_FWD)
     assert attn > 0 and L.lsh_workspace_bytes(ctypes.byref(c), 0, lsh.LSH_OP_ATTN_FWD) == 0
-    assert L.lsh_chunk_attn_fwd(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                                FAKE, FAKE, attn - 1, None) == lsh.LSH_ERR_INVALID
-    assert L.lsh_chunk_attn_fwd(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                                FAKE, None, attn, None) == lsh.LSH_ERR_INVALID
-    assert L.lsh_chunk_attn_fwd(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
-                                FAKE, FAKE, attn, None) == lsh.LSH_ERR_INVALID
+    assert L.lsh_chunk_attn_fwd(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE,
+                                FAKE, FAKE, FAKE, attn - 1, None) == lsh.LSH_ERR_INVALID
+    assert L.lsh_chunk_attn_fwd(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE,
+                                FAKE, FAKE, None, attn, None) == lsh.LSH_ERR_INVALID
+    assert L.lsh_chunk_attn_fwd(ctypes.byref(c), 1, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE,
+                                None, FAKE, FAKE, attn, None) == lsh.LSH_ERR_INVALID
 
 
 @pytest.mark.parametrize("unsup", [dict(d=32), dict(chunk=128, L=1024), dict(n_buckets=2048),
@@ -164,8 +164,8 @@ def test_chunk_lengths(L):
     assert L.lsh_chunk_attn_bwd(ctypes.byref(c128), lsh.LSH_F32, *([FAKE] * 12), bwd,
                                 None) == lsh.LSH_ERR_UNSUPPORTED
     c96 = _cfg(chunk=96)
-    assert L.lsh_chunk_attn_fwd(ctypes.byref(c96), lsh.LSH_F32, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                                None, FAKE, None, 0, None) == lsh.LSH_ERR_UNSUPPORTED
+    assert L.lsh_chunk_attn_fwd(ctypes.byref(c96), lsh.LSH_F32, FAKE, FAKE, FAKE, FAKE, None, FAKE,
+                                FAKE, None, FAKE, None, 0, None) == lsh.LSH_ERR_UNSUPPORTED
 
 
 @pytest.mark.parametrize("self_mask", [0.0, 10.0, -1e5, 9999.0])
@@ -181,7 +181,7 @@ def test_self_mask_below_bound(L, self_mask):
                                FAKE, FAKE, fwd, None) == lsh.LSH_ERR_UNSUPPORTED
     attn = L.lsh_workspace_bytes(ctypes.byref(c), bf, lsh.LSH_OP_ATTN_FWD)
     assert L.lsh_chunk_attn_fwd(ctypes.byref(c), bf, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                                FAKE, attn, None) == lsh.LSH_ERR_UNSUPPORTED
+                                FAKE, FAKE, attn, None) == lsh.LSH_ERR_UNSUPPORTED
     bwd = L.lsh_workspace_bytes(ctypes.byref(c), bf, lsh.LSH_OP_ATTN_BWD)
     assert L.lsh_chunk_attn_bwd(ctypes.byref(c), bf, *([FAKE] * 12), bwd, None) == lsh.LSH_ERR_UNSUPPORTED
     dense = L.lsh_workspace_bytes(ctypes.byref(c), bf, lsh.LSH_OP_DENSE_FWD)
@@ -207,3 +207,30 @@ def test_backward_alignment(L):
         assert rc == lsh.LSH_ERR_INVALID, k
     assert L.lsh_chunk_attn_bwd(ctypes.byref(c), bf, *([FAKE] * 12), 0, None) == lsh.LSH_ERR_INVALID
 
+
+
+@pytest.mark.parametrize("variant", [dict(chunks_after=1), dict(attend_across=1),
+                                     dict(chunks_after=2)])
+def test_variant_support(L, variant):
+    """Look-ahead and attention across buckets: the fp32 forward takes them
+    (one look-ahead chunk at most); the bf16 forward and the backward refuse
+    them before any HIP call; a negative look-ahead is invalid."""
+    c = _cfg(**variant)
+    for dtype in (lsh.LSH_BF16, lsh.LSH_F32):
+        fwd = L.lsh_workspace_bytes(ctypes.byref(c), dtype, lsh.LSH_OP_FORWARD)
+        rc = L.lsh_attention_fwd(ctypes.byref(c), dtype, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE,
+                                 FAKE, FAKE, FAKE, fwd, None)
+        if dtype == lsh.LSH_F32 and variant.get("chunks_after", 0) <= 1:
+            continue  # would launch: not called without a GPU
+        assert rc == lsh.LSH_ERR_UNSUPPORTED
+    bwd = L.lsh_workspace_bytes(ctypes.byref(c), lsh.LSH_BF16, lsh.LSH_OP_ATTN_BWD)
+    assert L.lsh_chunk_attn_bwd(ctypes.byref(c), lsh.LSH_BF16, *([FAKE] * 12), bwd,
+                                None) == lsh.LSH_ERR_UNSUPPORTED
+    neg = _cfg(chunks_after=-1)
+    assert L.lsh_workspace_bytes(ctypes.byref(neg), lsh.LSH_F32, lsh.LSH_OP_FORWARD) == 0
+
+
+def test_across_needs_undo(L):
+    c = _cfg(attend_across=1)
+    assert L.lsh_chunk_attn_fwd(ctypes.byref(c), lsh.LSH_F32, FAKE, FAKE, FAKE, FAKE, None, FAKE,
+                                FAKE, None, FAKE, None, 0, None) == lsh.LSH_ERR_INVALID
