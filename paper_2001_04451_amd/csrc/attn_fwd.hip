@@ -59,7 +59,6 @@
 namespace lsh {
 namespace {
 
-constexpr int kRing = 192;          // three chunk slots of 64 rows
 constexpr float kFastBound = 60.f;  // largest B_i handled without a running maximum
 constexpr int kMaskedIndex = 32;    // table index of a masked-out key
 
@@ -69,7 +68,24 @@ struct BoolTag {
     static constexpr bool value = B;
 };
 
-__device__ __forceinline__ int ring_row(int chunk, int i) { return ((chunk + 3) % 3) * kChunk + i; }
+// Shape of the bf16 kernel for chunks of M sorted slots and a look-ahead of
+// AFTER chunks: 16 queries per wave; the window is chunks c-1 .. c+AFTER;
+// the ring holds the window and the chunk being gathered.
+template <int M, int AFTER>
+struct FwdGeom {
+    static constexpr int kWaves = M / 16;
+    static constexpr int kThreads = 64 * kWaves;
+    static constexpr int kWinChunks = 2 + AFTER;
+    static constexpr int kWinKeys = kWinChunks * M;
+    static constexpr int kGroups = kWinKeys / 64;  // 64-slot groups of the window
+    static constexpr int kTiles = kWinKeys / 16;
+    static constexpr int kTilesPerChunk = M / 16;
+    static constexpr int kSlots = kWinChunks + 1;
+    static constexpr int kRows = kSlots * M;
+    static constexpr int kPosRegs = M / 64;        // slot positions a lane holds per chunk
+    // workgroups per CU the LDS allows (and that the kernel is built for)
+    static constexpr int kOcc = M == 64 ? (AFTER == 0 ? 3 : 2) : 1;
+};
 
 template <int NW>
 struct FwdSig {
@@ -79,20 +95,18 @@ struct FwdSig {
     static constexpr int rec_words = stride + 1 <= 4 ? 4 : (stride + 1 <= 8 ? 8 : 16);
 };
 
-template <int NW>
+template <int NW, int M, int AFTER>
 struct FwdShared {
-    char Qs[kRing * 128];  // q rows, 16-byte pieces at swizzled slots (see swz)
-    char Vs[kRing * 128];  // v rows, same layout
-    uint32_t sig[kRing][FwdSig<NW>::stride];  // bucket signature words
-    float cf[kRing];                          // scale*log2(e)/|q_row| (0 for a zero row)
+    static constexpr int kRows = FwdGeom<M, AFTER>::kRows;
+    char Qs[kRows * 128];  // q rows, 16-byte pieces at swizzled slots (see swz)
+    char Vs[kRows * 128];  // v rows, same layout
+    uint32_t sig[kRows][FwdSig<NW>::stride];  // bucket signature words
+    float cf[kRows];                          // scale*log2(e)/|q_row| (0 for a zero row)
     float tab[kMaskedIndex + 1];              // -log2 N by mismatch count; -inf = masked
 };
 
-
-
-
-template <int NW>
-__device__ __forceinline__ void read_sig(const FwdShared<NW>& S, int row, uint32_t (&out)[NW > 0 ? NW : 1]) {
+template <int NW, class SH>
+__device__ __forceinline__ void read_sig(const SH& S, int row, uint32_t (&out)[NW > 0 ? NW : 1]) {
     if constexpr (NW <= 1) {
         out[0] = S.sig[row][0];
     } else if constexpr (NW == 2) {
@@ -110,14 +124,18 @@ __device__ __forceinline__ void read_sig(const FwdShared<NW>& S, int row, uint32
     }
 }
 
-template <int NW, bool CAUSAL>
-__global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
+template <int NW, bool CAUSAL, int M, int AFTER>
+__global__ __launch_bounds__((FwdGeom<M, AFTER>::kThreads), (FwdGeom<M, AFTER>::kOcc)) void attn_fwd_bf16_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ v, const uint32_t* __restrict__ rec,
     const int32_t* __restrict__ perm, uint16_t* __restrict__ o_rounds,
     uint8_t* __restrict__ o_exp, float* __restrict__ lse_rounds, int L, int n_r, float scale,
     float self_mask, int chunks_per_strip) {
-    __shared__ __attribute__((aligned(16))) FwdShared<NW> S;
+    using G = FwdGeom<M, AFTER>;
+    using Shared = FwdShared<NW, M, AFTER>;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    Shared& S = *reinterpret_cast<Shared*>(smem);
     constexpr int SW = FwdSig<NW>::stride, RW = FwdSig<NW>::rec_words;
+    auto ring_row = [](int chunk, int i) { return ((chunk % G::kSlots + G::kSlots) % G::kSlots) * M + i; };
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -125,7 +143,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
     const int64_t seg = blockIdx.y;
     const int64_t bh = seg / n_r;
     const int r = (int)(seg % n_r);
-    const int n_chunks = (L + kChunk - 1) / kChunk;  // the last may be partial
+    const int n_chunks = (L + M - 1) / M;  // the last may be partial
     const int c0 = blockIdx.x * chunks_per_strip;
     const int c1 = min(n_chunks, c0 + chunks_per_strip);
     const float scale_log2e = scale * kLog2e;
@@ -134,24 +152,42 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
     const int rw = r >> 1, rsh = (r >> 1) + 11 * (r & 1);  // field r of a signature
     if (tid <= kMaskedIndex) S.tab[tid] = tid < n_r ? -__log2f((float)(n_r - tid)) : -__builtin_inff();
 
-    // Position of row `lane` of chunk cc, as stored (clamped where it is
-    // used); for a slot outside the sequence (before chunk 0, or past L in a
-    // partial last chunk) any valid row: such slots are never a valid key
-    // (see lo and hi below) and their queries store nothing.
-    auto chunk_pos = [&](int cc) -> int {
-        const int slot = cc * kChunk + lane;
-        return cc >= 0 && slot < L ? pseg[slot] : 0;
+    // Positions of slots 64p + lane of chunk cc, as stored (clamped where
+    // they are used); for a slot outside the sequence (before chunk 0, or
+    // past L) any valid row: such slots are never a valid key (see lo and hi
+    // below) and their queries store nothing.
+    struct Pos {
+        int p[G::kPosRegs];
+    };
+    auto chunk_pos = [&](int cc) -> Pos {
+        Pos x;
+#pragma unroll
+        for (int k = 0; k < G::kPosRegs; ++k) {
+            const int slot = cc * M + 64 * k + lane;
+            x.p[k] = cc >= 0 && slot < L ? pseg[slot] : 0;
+        }
+        return x;
     };
     // Gather chunk cc into its ring slot: wave w copies q and v rows
     // 16w .. 16w+15 (each lane the piece that belongs at its LDS slot), and
     // the signature words and key scales are split over the waves.
-    auto stage = [&](int cc, int pos_raw) {
-        const int pos_lane = min(max(pos_raw, 0), L - 1);
+    auto stage = [&](int cc, Pos pos_raw) {
+        int pos_lane[G::kPosRegs];
+#pragma unroll
+        for (int k = 0; k < G::kPosRegs; ++k) pos_lane[k] = min(max(pos_raw.p[k], 0), L - 1);
+        // position of chunk row `row` (uniform choice of register per wave)
+        auto pos_of = [&](int row) {
+            int p = __shfl(pos_lane[0], row & 63);
+#pragma unroll
+            for (int k = 1; k < G::kPosRegs; ++k)
+                if ((row >> 6) == k) p = __shfl(pos_lane[k], row & 63);
+            return p;
+        };
         const int slot0 = ring_row(cc, 0);
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
             const int row = 16 * wave + 8 * k + (lane >> 3);
-            const int p = __shfl(pos_lane, row);
+            const int p = pos_of(row);
             const int64_t off = (rowbase + p) * kHeadDim + swz(row, lane & 7) * 8;
             copy16_to_lds(q + off, S.Qs + (slot0 + 16 * wave + 8 * k) * 128);
             copy16_to_lds(v + off, S.Vs + (slot0 + 16 * wave + 8 * k) * 128);
@@ -159,27 +195,30 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
         if constexpr (SW >= 4) {
             constexpr int U = SW / 4;  // 16-byte units per row
 #pragma unroll
-            for (int k = 0; k < U; ++k)
+            for (int k = 0; k < M * U / 64; ++k)
                 if (wave == k) {
                     const int u = 64 * k + lane, row = u / U;
-                    const int p = __shfl(pos_lane, row);
+                    const int p = pos_of(row);
                     copy16_to_lds(rec + (rowbase + p) * RW + 4 * (u % U), &S.sig[slot0][0] + 256 * k);
                 }
         } else {
 #pragma unroll
-            for (int k = 0; k < SW; ++k)
+            for (int k = 0; k < M * SW / 64; ++k)
                 if (wave == k) {
                     const int u = 64 * k + lane, row = u / SW;
-                    const int p = __shfl(pos_lane, row);
+                    const int p = pos_of(row);
                     copy4_to_lds(rec + (rowbase + p) * RW + (u % SW), &S.sig[slot0][0] + 64 * k);
                 }
         }
-        if (wave == 3) copy4_to_lds(rec + (rowbase + pos_lane) * RW + (RW - 1), &S.cf[slot0]);
+#pragma unroll
+        for (int k = 0; k < G::kPosRegs; ++k)
+            if (wave == G::kWaves - 1 - k)
+                copy4_to_lds(rec + (rowbase + pos_lane[k]) * RW + (RW - 1), &S.cf[slot0 + 64 * k]);
     };
 
-    stage(c0 - 1, chunk_pos(c0 - 1));
-    stage(c0, chunk_pos(c0));
-    int pf_pos = chunk_pos(c0 + 1);
+#pragma unroll
+    for (int k = -1; k <= AFTER; ++k) stage(c0 + k, chunk_pos(c0 + k));
+    Pos pf_pos = chunk_pos(c0 + AFTER + 1);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
@@ -203,13 +242,13 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
     };
 
     for (int c = c0; c < c1; ++c) {
-        if (c + 1 < c1) stage(c + 1, pf_pos);
-        const int pf_next = chunk_pos(c + 2);
+        if (c + 1 < c1) stage(c + AFTER + 1, pf_pos);
+        const Pos pf_next = chunk_pos(c + AFTER + 2);
         flush();
 
         // ---- this wave's 16 queries of chunk c ----
         const int u = 16 * wave + n;  // query row inside the chunk
-        const int s_q = c * kChunk + u;
+        const int s_q = c * M + u;
         const int rq = ring_row(c, u);
         uint32_t qsig[NW > 0 ? NW : 1];
         read_sig<NW>(S, rq, qsig);
@@ -221,56 +260,82 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
         const float bound = cfq > 0.f ? scale_log2e * scale_log2e * __builtin_amdgcn_rcpf(cfq) : 0.f;
         const bool fast = __ballot(!(bound <= kFastBound)) == 0;
 
-        // bucket boundaries of the window (chunks c-1, c): bit k of bA (bB)
-        // is set when slot k of chunk c-1 (c) starts a new round-r bucket
-        const uint32_t kA = (S.sig[ring_row(c - 1, lane)][rw] >> rsh) & 0x3FFu;
-        const uint32_t kB = (S.sig[ring_row(c, lane)][rw] >> rsh) & 0x3FFu;
-        const uint32_t prevA = __shfl_up(kA, 1);
-        const uint32_t lastA = __shfl(kA, 63);
-        const uint32_t prevB0 = __shfl_up(kB, 1);
-        const uint32_t prevB = lane == 0 ? lastA : prevB0;
-        const uint64_t bA = __ballot(lane == 0 || kA != prevA);
-        const uint64_t bB = __ballot(kB != prevB);
-        const uint64_t upto = bB & (~0ull >> (63 - u));
-        const int lo_w = upto ? 127 - __clzll(upto) : 63 - __clzll(bA);
-        const int lo = max((c - 1) * kChunk + lo_w, 0);
-        int hi;
-        if constexpr (CAUSAL) {
-            hi = s_q - 1;
-        } else {
-            const uint64_t after = u < 63 ? bB & (~0ull << (u + 1)) : 0ull;
-            hi = (c - 1) * kChunk + (after ? 62 + __ffsll((long long)after) : 127);
+        // Bucket boundaries of the window (window slot w = slot (c-1)M + w):
+        // bit l of bnd[gi] is set when window slot 64 gi + l starts a new
+        // round-r bucket (window slot 0 always does).
+        uint64_t bnd[G::kGroups];
+        {
+            uint32_t last = 0;
+#pragma unroll
+            for (int gi = 0; gi < G::kGroups; ++gi) {
+                const int wc = (64 * gi) / M, wrow = (64 * gi) % M + lane;
+                const uint32_t id = (S.sig[ring_row(c - 1 + wc, wrow)][rw] >> rsh) & 0x3FFu;
+                const uint32_t up = __shfl_up(id, 1);
+                const uint32_t prev = lane == 0 ? last : up;
+                bnd[gi] = __ballot((gi == 0 && lane == 0) || id != prev);
+                last = __shfl(id, 63);
+            }
         }
-        // No key past the sequence (a partial last chunk).  Chunk c holds at
-        // least one slot below L, so hi stays at or above the chunk's start - 1.
-        hi = min(hi, L - 1);
-        // valid keys of this lane's query as a 128-bit window mask (vm[h]:
-        // window slots 64h .. 64h+63; lo_w2 <= 127 and hi_w2 >= 63 always),
-        // then per lane group the complement shifted so that bit 16(kt%2) + j
-        // of nv[kt/2] is set when tile key 4g + j of tile kt is masked out
-        const int lo_w2 = lo - (c - 1) * kChunk, hi_w2 = hi - (c - 1) * kChunk;
-        uint64_t vm[2];
-        vm[0] = lo_w2 < 64 ? (~0ull << lo_w2) & (hi_w2 < 64 ? ~0ull >> (63 - hi_w2) : ~0ull) : 0ull;
-        vm[1] = hi_w2 >= 64 ? (~0ull >> (127 - hi_w2)) & (lo_w2 >= 64 ? ~0ull << (lo_w2 - 64) : ~0ull) : 0ull;
-        if constexpr (!CAUSAL) vm[1] &= ~(1ull << u);  // the query itself
-        uint32_t nv[4];
-        bool act[8];
+        // the query's key interval [lo_w, hi_w] in window slots: the last
+        // boundary at or before its own slot M + u, and (without causal
+        // masking) the slot before the next boundary; its group gq is
+        // uniform over the wave
+        const int qs = M + u, gq = qs >> 6, bq = qs & 63;
+        int lo_w = 0;
 #pragma unroll
-        for (int h2 = 0; h2 < 2; ++h2) {
-            const uint64_t sh = ~vm[h2] >> (4 * g);
-            nv[2 * h2] = (uint32_t)sh;
-            nv[2 * h2 + 1] = (uint32_t)(sh >> 32);
+        for (int gi = 0; gi < G::kGroups; ++gi) {
+            const uint64_t mm = gi < gq ? bnd[gi] : (gi == gq ? bnd[gi] & (~0ull >> (63 - bq)) : 0ull);
+            if (mm) lo_w = 64 * gi + 63 - __clzll(mm);
+        }
+        int hi_w;
+        if constexpr (CAUSAL) {
+            hi_w = qs - 1;
+        } else {
+            hi_w = G::kWinKeys - 1;
 #pragma unroll
-            for (int k = 0; k < 4; ++k) act[4 * h2 + k] = __ballot(((vm[h2] >> (16 * k)) & 0xFFFFu) != 0) != 0;
+            for (int gi = G::kGroups - 1; gi >= 0; --gi) {
+                const uint64_t mm = gi > gq ? bnd[gi]
+                                            : (gi == gq && bq < 63 ? bnd[gi] & (~0ull << (bq + 1)) : 0ull);
+                if (mm) hi_w = 64 * gi + __ffsll((long long)mm) - 2;
+            }
+        }
+        // no slot before 0 and no key past the sequence
+        lo_w = max(lo_w, (1 - c) * M);
+        hi_w = min(hi_w, L - 1 - (c - 1) * M);
+        // valid keys of this lane's query as a window mask (vm[gi]: window
+        // slots 64 gi .. 64 gi + 63), then per lane group the complement
+        // shifted so that bit 16(kt%2) + j of nv[kt/2] is set when tile key
+        // 4g + j of tile kt is masked out
+        uint64_t vm[G::kGroups];
+#pragma unroll
+        for (int gi = 0; gi < G::kGroups; ++gi) {
+            const int lg = lo_w - 64 * gi, hg = hi_w - 64 * gi;
+            vm[gi] = (hg < 0 || lg > 63) ? 0ull
+                                         : ((lg <= 0 ? ~0ull : ~0ull << lg) & (hg >= 63 ? ~0ull : ~0ull >> (63 - hg)));
+        }
+        if constexpr (!CAUSAL) {  // the query itself
+#pragma unroll
+            for (int gi = 0; gi < G::kGroups; ++gi)
+                if (gi == gq) vm[gi] &= ~(1ull << bq);
+        }
+        uint32_t nv[2 * G::kGroups];
+        bool act[G::kTiles];
+#pragma unroll
+        for (int gi = 0; gi < G::kGroups; ++gi) {
+            const uint64_t sh = ~vm[gi] >> (4 * g);
+            nv[2 * gi] = (uint32_t)sh;
+            nv[2 * gi + 1] = (uint32_t)(sh >> 32);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) act[4 * gi + k] = __ballot(((vm[gi] >> (16 * k)) & 0xFFFFu) != 0) != 0;
         }
 
-        // Per-lane LDS offsets of the two window chunks' first rows (tile kt
-        // adds 16 (kt % 4) rows, a constant): K operand pieces g and 4+g,
-        // the V^T operands of the four 16-dim blocks, the signature row.
-        uint32_t kofs[2][2], vofs[2][4];
-        int srow[2];
+        // Per-lane LDS offsets of the window chunks' first rows (tile kt adds
+        // a constant number of rows): K operand pieces g and 4+g, the V^T
+        // operands of the four 16-dim blocks, the signature row.
+        uint32_t kofs[G::kWinChunks][2], vofs[G::kWinChunks][4];
+        int srow[G::kWinChunks];
 #pragma unroll
-        for (int ch = 0; ch < 2; ++ch) {
+        for (int ch = 0; ch < G::kWinChunks; ++ch) {
             const int base = ring_row(c - 1 + ch, 0);
             kofs[ch][0] = row_piece_offset(base + n, g);
             kofs[ch][1] = row_piece_offset(base + n, 4 + g);
@@ -286,9 +351,10 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
             // weights (every register of a lane holds its query's sum)
             f32x4 oacc[5] = {f32x4{}, f32x4{}, f32x4{}, f32x4{}, f32x4{}};
 #pragma unroll
-            for (int kt = 0; kt < 8; ++kt) {
+            for (int kt = 0; kt < G::kTiles; ++kt) {
                 if (!act[kt]) continue;
-                const int ch = kt >> 2, roff = 16 * (kt & 3);  // chunk of the tile, its first row
+                // window chunk of the tile and its first row in that chunk
+                const int ch = kt / G::kTilesPerChunk, roff = 16 * (kt % G::kTilesPerChunk);
                 f32x4 acc = mfma16x16x32(as_bf16x8(*reinterpret_cast<const u32x4*>(S.Qs + kofs[ch][0] + roff * 128)),
                                          qb0, f32x4{});
                 acc = mfma16x16x32(as_bf16x8(*reinterpret_cast<const u32x4*>(S.Qs + kofs[ch][1] + roff * 128)), qb1,
@@ -343,8 +409,8 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
                 // The output of a lone query is v_i: one more P V step on the
                 // diagonal tile with P = 1 at (i, i) for those queries and 0
                 // elsewhere adds exactly v_i to their (zero) accumulators.
-                // Query n's own key is key n of that tile, held by lane group
-                // n / 4 as its element n % 4.
+                // Query n's own key is key n of that tile (rows 16w .. 16w+15
+                // of chunk c), held by lane group n / 4 as its element n % 4.
                 const bool mine = alone && g == (n >> 2);
                 const uint32_t one = (n & 1) ? 0x3F800000u : 0x3F80u;  // bf16 1.0 in its half
                 const uint2 w2 = make_uint2(mine && (n & 2) == 0 ? one : 0u, mine && (n & 2) != 0 ? one : 0u);
@@ -385,7 +451,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_bf16_kernel(
             attend(BoolTag<false>{});
 
         pf_pos = pf_next;
-        __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of chunk c+1 have landed
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of the next chunk have landed
         __syncthreads();                // ... and every wave is done with chunk c-1
     }
     flush();
@@ -561,26 +627,47 @@ __global__ __launch_bounds__(256) void attn_prep_kernel(const uint16_t* __restri
 }
 
 
+template <int NW, int M, int AFTER>
+void launch_kernel(bool causal, dim3 grid, const uint16_t* q, const uint16_t* v, const uint32_t* rec,
+                   const int32_t* perm, uint16_t* o, uint8_t* o_exp, float* lse, int L, int n_r,
+                   float scale, float self_mask, int cps, hipStream_t stream) {
+    constexpr int kThreads = FwdGeom<M, AFTER>::kThreads;
+    const size_t lds = sizeof(FwdShared<NW, M, AFTER>);
+    auto go = [&](auto kernel) {
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds);
+        kernel<<<grid, kThreads, lds, stream>>>(q, v, rec, perm, o, o_exp, lse, L, n_r, scale, self_mask, cps);
+    };
+    if (causal)
+        go(&attn_fwd_bf16_kernel<NW, true, M, AFTER>);
+    else
+        go(&attn_fwd_bf16_kernel<NW, false, M, AFTER>);
+}
+
 template <int NW>
-hipError_t launch_bf16(bool causal, const uint16_t* q, const uint16_t* v, const int32_t* buckets,
-                       const int32_t* perm, uint16_t* o, uint8_t* o_exp, float* lse, int64_t BH, int L, int n_r,
-                       float scale, float self_mask, void* workspace, hipStream_t stream) {
+hipError_t launch_bf16(bool causal, int M, int after, const uint16_t* q, const uint16_t* v,
+                       const int32_t* buckets, const int32_t* perm, uint16_t* o, uint8_t* o_exp,
+                       float* lse, int64_t BH, int L, int n_r, float scale, float self_mask,
+                       void* workspace, hipStream_t stream) {
     const int64_t rows = BH * L;
     uint32_t* rec = static_cast<uint32_t*>(workspace);
     attn_prep_kernel<NW><<<(unsigned)((rows * 8 + 255) / 256), 256, 0, stream>>>(
         q, buckets, rows, n_r, scale * kLog2e, rec);
     // Strips of chunks: long enough that staging the strip's first window is
-    // a small overhead, short enough to give the chip several workgroups per
-    // CU (three fit at once).
-    const int64_t n_chunks = (L + kChunk - 1) / kChunk, segs = BH * n_r;
-    const int cps = (int)std::max<int64_t>(1, std::min<int64_t>(16, n_chunks * segs / 3072));
+    // a small overhead, short enough to give the chip several rounds of
+    // workgroups (kOcc fit on a CU at once).
+    const int64_t n_chunks = (L + M - 1) / M, segs = BH * n_r;
+    const int occ = M == 64 ? (after == 0 ? 3 : 2) : 1;
+    const int cps = (int)std::max<int64_t>(1, std::min<int64_t>(16, n_chunks * segs / (1024 * occ)));
     const dim3 grid((unsigned)((n_chunks + cps - 1) / cps), (unsigned)segs);
-    if (causal)
-        attn_fwd_bf16_kernel<NW, true><<<grid, 256, 0, stream>>>(q, v, rec, perm, o, o_exp, lse, L, n_r,
-                                                                 scale, self_mask, cps);
+    if (M == 64 && after == 0)
+        launch_kernel<NW, 64, 0>(causal, grid, q, v, rec, perm, o, o_exp, lse, L, n_r, scale, self_mask, cps, stream);
+    else if (M == 64)
+        launch_kernel<NW, 64, 1>(causal, grid, q, v, rec, perm, o, o_exp, lse, L, n_r, scale, self_mask, cps, stream);
+    else if (after == 0)
+        launch_kernel<NW, 128, 0>(causal, grid, q, v, rec, perm, o, o_exp, lse, L, n_r, scale, self_mask, cps, stream);
     else
-        attn_fwd_bf16_kernel<NW, false><<<grid, 256, 0, stream>>>(q, v, rec, perm, o, o_exp, lse, L, n_r,
-                                                                  scale, self_mask, cps);
+        launch_kernel<NW, 128, 1>(causal, grid, q, v, rec, perm, o, o_exp, lse, L, n_r, scale, self_mask, cps, stream);
     return hipGetLastError();
 }
 
@@ -625,10 +712,10 @@ hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, int c
     const uint16_t* vb = static_cast<const uint16_t*>(v);
     uint16_t* ob = static_cast<uint16_t*>(o_rounds);
     const int nw = n_rounds == 1 ? 0 : (n_rounds + 1) / 2;
-#define LSH_FWD_CASE(W)                                                                             \
-    case W:                                                                                         \
-        return launch_bf16<W>(causal, qb, vb, buckets, perm, ob, o_exp, lse_rounds, BH, L, n_rounds, scale, \
-                              self_mask, workspace, stream);
+#define LSH_FWD_CASE(W)                                                                              \
+    case W:                                                                                          \
+        return launch_bf16<W>(causal, chunk, after, qb, vb, buckets, perm, ob, o_exp, lse_rounds, BH, L, \
+                              n_rounds, scale, self_mask, workspace, stream);
     switch (nw) {
         LSH_FWD_CASE(0)
         LSH_FWD_CASE(1)

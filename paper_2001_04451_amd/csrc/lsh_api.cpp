@@ -54,19 +54,18 @@ int check_self_mask(const lsh_config* cfg) {
     return cfg->self_mask >= kMinSelfMask ? LSH_OK : LSH_ERR_UNSUPPORTED;
 }
 
-// What the chunked-attention kernels take: chunks of 64 everywhere and of 128
-// on the fp32 forward; a look-ahead of at most one chunk and attention across
-// buckets on the fp32 forward; the backward only the paper's own window
-// (chunks of 64, no look-ahead, bucket-restricted targets).
+// What the chunked-attention kernels take: the forward chunks of 64 or 128
+// and a look-ahead of at most one chunk, attention across buckets on the fp32
+// forward; the backward only the paper's own window (chunks of 64, no
+// look-ahead, bucket-restricted targets).
 int check_chunk(const lsh_config* cfg, int dtype, bool backward) {
     if (cfg->chunks_after > 1) return LSH_ERR_UNSUPPORTED;
     if (backward)
         return cfg->chunk == lsh::kChunkHost && cfg->chunks_after == 0 && !cfg->attend_across
                    ? LSH_OK
                    : LSH_ERR_UNSUPPORTED;
-    if (dtype == LSH_F32) return cfg->chunk == 64 || cfg->chunk == 128 ? LSH_OK : LSH_ERR_UNSUPPORTED;
-    if (cfg->chunk != lsh::kChunkHost || cfg->chunks_after != 0 || cfg->attend_across)
-        return LSH_ERR_UNSUPPORTED;
+    if (cfg->chunk != 64 && cfg->chunk != 128) return LSH_ERR_UNSUPPORTED;
+    if (dtype == LSH_BF16 && cfg->attend_across) return LSH_ERR_UNSUPPORTED;
     return LSH_OK;
 }
 

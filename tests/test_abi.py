@@ -90,7 +90,7 @@ def test_null_pointers_and_small_workspace(L):
                                 None, FAKE, FAKE, attn, None) == lsh.LSH_ERR_INVALID
 
 
-@pytest.mark.parametrize("unsup", [dict(d=32), dict(chunk=128, L=1024), dict(n_buckets=2048),
+@pytest.mark.parametrize("unsup", [dict(d=32), dict(chunk=96, L=1056), dict(n_buckets=2048),
                                    dict(n_rounds=17)])
 def test_unsupported_shapes(L, unsup):
     c = _cfg(**unsup)
@@ -153,19 +153,17 @@ def test_dense_entry_validation(L):
 
 
 def test_chunk_lengths(L):
-    """Chunks of 64 everywhere; 128 only on the fp32 forward (its bf16 and
-    backward forms, and other lengths, are unsupported)."""
+    """Chunks of 64 or 128 on the forward (other lengths unsupported); the
+    backward takes chunks of 64 only."""
     c128 = _cfg(chunk=128)
-    need = L.lsh_workspace_bytes(ctypes.byref(c128), lsh.LSH_BF16, lsh.LSH_OP_FORWARD)
-    rc = L.lsh_attention_fwd(ctypes.byref(c128), lsh.LSH_BF16, FAKE, FAKE, FAKE, FAKE, None, FAKE,
-                             FAKE, FAKE, FAKE, FAKE, need, None)
-    assert rc == lsh.LSH_ERR_UNSUPPORTED
-    bwd = L.lsh_workspace_bytes(ctypes.byref(c128), lsh.LSH_F32, lsh.LSH_OP_ATTN_BWD)
-    assert L.lsh_chunk_attn_bwd(ctypes.byref(c128), lsh.LSH_F32, *([FAKE] * 12), bwd,
-                                None) == lsh.LSH_ERR_UNSUPPORTED
+    for dtype in (lsh.LSH_BF16, lsh.LSH_F32):
+        bwd = L.lsh_workspace_bytes(ctypes.byref(c128), dtype, lsh.LSH_OP_ATTN_BWD)
+        assert L.lsh_chunk_attn_bwd(ctypes.byref(c128), dtype, *([FAKE] * 12), bwd,
+                                    None) == lsh.LSH_ERR_UNSUPPORTED
     c96 = _cfg(chunk=96)
-    assert L.lsh_chunk_attn_fwd(ctypes.byref(c96), lsh.LSH_F32, FAKE, FAKE, FAKE, FAKE, None, FAKE,
-                                FAKE, None, FAKE, None, 0, None) == lsh.LSH_ERR_UNSUPPORTED
+    for dtype in (lsh.LSH_BF16, lsh.LSH_F32):
+        assert L.lsh_chunk_attn_fwd(ctypes.byref(c96), dtype, FAKE, FAKE, FAKE, FAKE, None, FAKE,
+                                    FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == lsh.LSH_ERR_UNSUPPORTED
 
 
 @pytest.mark.parametrize("self_mask", [0.0, 10.0, -1e5, 9999.0])
@@ -212,16 +210,19 @@ def test_backward_alignment(L):
 @pytest.mark.parametrize("variant", [dict(chunks_after=1), dict(attend_across=1),
                                      dict(chunks_after=2)])
 def test_variant_support(L, variant):
-    """Look-ahead and attention across buckets: the fp32 forward takes them
-    (one look-ahead chunk at most); the bf16 forward and the backward refuse
-    them before any HIP call; a negative look-ahead is invalid."""
+    """Look-ahead and attention across buckets: the fp32 forward takes both
+    (one look-ahead chunk at most), the bf16 forward the look-ahead; the rest
+    and the backward refuse them before any HIP call; a negative look-ahead is
+    invalid."""
     c = _cfg(**variant)
     for dtype in (lsh.LSH_BF16, lsh.LSH_F32):
+        supported = variant.get("chunks_after", 0) <= 1 and (
+            dtype == lsh.LSH_F32 or not variant.get("attend_across", 0))
+        if supported:
+            continue  # would launch: not called without a GPU
         fwd = L.lsh_workspace_bytes(ctypes.byref(c), dtype, lsh.LSH_OP_FORWARD)
         rc = L.lsh_attention_fwd(ctypes.byref(c), dtype, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE,
                                  FAKE, FAKE, FAKE, fwd, None)
-        if dtype == lsh.LSH_F32 and variant.get("chunks_after", 0) <= 1:
-            continue  # would launch: not called without a GPU
         assert rc == lsh.LSH_ERR_UNSUPPORTED
     bwd = L.lsh_workspace_bytes(ctypes.byref(c), lsh.LSH_BF16, lsh.LSH_OP_ATTN_BWD)
     assert L.lsh_chunk_attn_bwd(ctypes.byref(c), lsh.LSH_BF16, *([FAKE] * 12), bwd,

@@ -56,6 +56,25 @@ def test_f32_lookahead_and_across(gpu, causal, chunk, L, after, across):
     print(f"f32 chunk={chunk} L={L} after={after} across={across} causal={causal}: err {err:.3e}")
 
 
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("chunk,after,L", [(128, 0, 4096), (128, 0, 1000), (64, 1, 4096),
+                                           (64, 1, 1000), (128, 1, 4096), (128, 1, 1000)])
+def test_bf16_chunk128_and_lookahead(gpu, causal, chunk, after, L):
+    """The bf16 matrix-core forward with chunks of 128 sorted slots (the
+    paper's usual configuration, m = 2l/n_b, Sec. 5) and/or one look-ahead
+    chunk, including a partial last chunk; 8 rounds of a 64-Gaussian mixture,
+    so buckets are uneven and the window's masks span several 64-slot
+    groups."""
+    n_b = max(2, (2 * L // chunk) // 2 * 2)  # m = 2l/n_b, rounded to an even count
+    w = small("long_bf16_L65536", H=2, L=L, n_components=64, n_buckets=n_b, chunk=chunk,
+              causal=causal)
+    x = W.make_inputs(w)
+    cfg = lsh.Config.of(w, chunks_after=after)
+    log("variant bf16", causal, chunk, after, L)
+    err = _forward(w, x["R"], cfg, after)
+    print(f"bf16 chunk={chunk} after={after} L={L} causal={causal}: err {err:.3e}")
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_r_per_head(gpu, dtype):
     """One R per head: each (batch, head) slice hashed with its head's R, bit
