@@ -20,7 +20,10 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "lsh_oracle.c")
-_LIB = os.path.join(_HERE, "liblsh_oracle.so")
+# LSH_ORACLE_LIB points at another build of the same source (the sanitizer
+# test loads an instrumented one); it is never built here
+_LIB = os.environ.get("LSH_ORACLE_LIB") or os.path.join(_HERE, "liblsh_oracle.so")
+_FIXED = "LSH_ORACLE_LIB" in os.environ
 _lib = None
 
 _i64 = ctypes.c_int64
@@ -30,6 +33,8 @@ _ptr = ctypes.c_void_p
 
 def build(force: bool = False) -> str:
     """Compile lsh_oracle.c into liblsh_oracle.so with gcc and OpenMP."""
+    if _FIXED:
+        return _LIB
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + f".tmp{os.getpid()}"
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared",
