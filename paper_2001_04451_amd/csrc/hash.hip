@@ -4,25 +4,29 @@
 //
 // Design (gfx950):
 //  * The projections xR are a dense [rows x 64] * [64 x n_b/2] contraction per
-//    round, run on the bf16 matrix cores.  R (fp32) is split exactly into
-//    bf16 planes R = R_hi + R_mid + res with |res| <= 2^-16 |R|; bf16 x bf16
-//    products are exact in fp32, so the screened projection differs from the
-//    exact one by a bounded amount (residual, fp32 accumulation, and the
-//    index bits packed into the low mantissa).
+//    round, run on the matrix cores with 16-bit operands and fp32
+//    accumulation.  For bf16 input, q and each round of R are scaled by
+//    powers of two (which leaves every argmax unchanged) and R is split into
+//    binary16 planes R = R_hi + R_mid + res, |R_hi - R| <= 2^-12 |R|;
+//    the scaled bf16 q is exact in binary16.  For fp32 input, q and R are
+//    split into bf16 planes instead.  16-bit products are exact in fp32, so
+//    a screened projection differs from the exact one by a bounded amount
+//    (residual, fp32 accumulation, and the index bits packed into the low
+//    mantissa).
 //  * R streams through LDS by direct global-to-LDS copies, 256 columns per
 //    stage, while each wave's products for the next tile are interleaved
 //    with the vector epilogue of the current one (one in-order instruction
 //    stream keeps both the matrix core and the vector ALUs busy).
 //  * Each lane keeps the two largest |projection| keys it has seen; the
-//    sign and the index inside a 32-column tile ride in the low bits of the
-//    key, so a rotate, an and-or, a max and a median-of-three per projection
-//    suffice, and the tile of the best key is noted once per tile.  A row's
-//    ids for all rounds are written together at the end.
+//    index inside a 32-column tile rides in the low bits of the key, so an
+//    and-or per projection and a max3, a med3 and a max per two suffice, and
+//    the tile of the best key is noted once per tile.  A row's ids for all
+//    rounds are written together at the end.
 //  * If the gap between the best and second-best key cannot rule out an
 //    exchange under the error bound, the row-round is appended to a list and
-//    recomputed afterwards in fp64 by a second kernel (same products and
-//    summation order as a plain loop), so the ids always equal the exact
-//    argmax.
+//    recomputed afterwards over both planes, and what that leaves open in
+//    fp64 by a last kernel (same products and summation order as a plain
+//    loop), so the ids always equal the exact argmax.
 #include "common.h"
 #include "launch.h"
 
@@ -35,34 +39,112 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kRB = 2;  // 32-row blocks per wave: each staged R tile feeds 2 * 8 MFMAs
 
-// One R column per block of 64 lanes (lane = t): bf16 planes hi/mid,
+// Largest |R| of each 1/kScaleParts of each round (block (part, r)): the
+// fp16 planes' scale is taken from these partial maxima.
+constexpr int kScaleParts = 32;
+
+__global__ __launch_bounds__(256) void prep_r_part_kernel(const float* __restrict__ R, int half,
+                                                          float* __restrict__ r_part) {
+    __shared__ float red[4];
+    const int part = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
+    const int n = kHeadDim * half;
+    const int per = (n + kScaleParts - 1) / kScaleParts;
+    const int lo = part * per, hi = min(n, lo + per);
+    const float* Rr = R + (size_t)r * n;
+    float m = 0.f;
+    for (int i = lo + tid; i < hi; i += 256) m = fmaxf(m, fabsf(Rr[i]));
+    m = wave_max(m);
+    if ((tid & 63) == 0) red[tid >> 6] = m;
+    __syncthreads();
+    if (tid == 0) r_part[r * kScaleParts + part] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+// The exponent sr with max |R| * 2^sr in [2^14, 2^15) (0 when the round is
+// zero or not finite): a positive scale of a whole round leaves every
+// argmax unchanged.
+__device__ __forceinline__ int round_scale_exp(const float* __restrict__ part) {
+    float m = 0.f;
+    for (int i = 0; i < kScaleParts; ++i) m = fmaxf(m, part[i]);
+    // m in [2^e, 2^(e+1)) (frexp: m = f 2^k with f in [0.5, 1), e = k - 1)
+    int k = 0;
+    (void)frexpf(m, &k);
+    return (m > 0.f && m <= 3.4e38f) ? 14 - (k - 1) : 0;
+}
+
+// x * 2^e for |e| up to 254, in two exact steps.
+__device__ __forceinline__ double ldexp2(double x, int e) {
+    const int a = e / 2;
+    return x * __builtin_bit_cast(double, (uint64_t)(1023 + a) << 52) *
+           __builtin_bit_cast(double, (uint64_t)(1023 + e - a) << 52);
+}
+
+// Nearest binary16 of x (|x| < 2^15 here), or 0 below fp16's normal range:
+// the planes hold no subnormal, whatever the matrix cores do with them.
+__device__ __forceinline__ uint32_t f16_normal_bits(double x) {
+    const _Float16 h = fabs(x) < 0x1p-14 ? (_Float16)0.f : (_Float16)(float)x;
+    return (uint32_t)__builtin_bit_cast(uint16_t, h);
+}
+
+// One R column per block of 64 lanes (lane = t): two 16-bit planes hi/mid,
 // [n_r][half_pad][64] (column contiguous, zero padded), and three 2-norms of
 // the column, [3][n_r][half_pad]: |R_c|, |R_c - hi_c|, |R_c - hi_c - mid_c|.
+//  * F16 (bf16 input): binary16 planes of R_c * 2^sr[r] (sr from the
+//    round's partial maxima, also written to r_exp); the norms are of the
+//    scaled column, formed in fp64 from exact residuals.
+//  * bf16 planes (fp32 input): R = hi + mid + res with each step exact.
+template <bool F16>
 __global__ __launch_bounds__(64) void prep_r_cols_kernel(const float* __restrict__ R, int half,
-                                                         int half_pad, uint16_t* __restrict__ r_hi,
+                                                         int half_pad, const float* __restrict__ r_part,
+                                                         int* __restrict__ r_exp,
+                                                         uint16_t* __restrict__ r_hi,
                                                          uint16_t* __restrict__ r_mid,
                                                          float* __restrict__ col_norm) {
     const int c = blockIdx.x, r = blockIdx.y, t = threadIdx.x;
     const int n_r = gridDim.y;
     const float x = c < half ? R[((size_t)r * kHeadDim + t) * half + c] : 0.f;
-    const uint32_t hi = f32_to_bf16_bits(x);
-    const float res = x - bf16_bits_to_f32(hi);  // exact (Sterbenz)
-    const uint32_t mid = f32_to_bf16_bits(res);
-    const float res2 = res - bf16_bits_to_f32(mid);  // exact
+    uint32_t hi, mid;
+    float n0, n1, n2;
+    if constexpr (F16) {
+        const int sr = round_scale_exp(r_part + r * kScaleParts);
+        if (c == 0 && t == 0) r_exp[r] = sr;
+        const double xs = ldexp2((double)x, sr);
+        hi = f16_normal_bits(xs);
+        const double res = xs - (double)f16_bits_to_f32(hi);  // exact in fp64
+        mid = f16_normal_bits(res);
+        const double res2 = res - (double)f16_bits_to_f32(mid);  // exact
+        double s0 = xs * xs, s1 = res * res, s2 = res2 * res2;
+        for (int off = 32; off >= 1; off >>= 1) {
+            s0 += __shfl_xor(s0, off);
+            s1 += __shfl_xor(s1, off);
+            s2 += __shfl_xor(s2, off);
+        }
+        // rounded up to fp32 (the bounds that use them are upper bounds)
+        n0 = (float)sqrt(s0) * (1.f + 0x1p-22f);
+        n1 = (float)sqrt(s1) * (1.f + 0x1p-22f);
+        n2 = (float)sqrt(s2) * (1.f + 0x1p-22f);
+    } else {
+        hi = f32_to_bf16_bits(x);
+        const float res = x - bf16_bits_to_f32(hi);  // exact (Sterbenz)
+        mid = f32_to_bf16_bits(res);
+        const float res2 = res - bf16_bits_to_f32(mid);  // exact
+        float s0 = x * x, s1 = res * res, s2 = res2 * res2;
+        for (int off = 32; off >= 1; off >>= 1) {
+            s0 += __shfl_xor(s0, off);
+            s1 += __shfl_xor(s1, off);
+            s2 += __shfl_xor(s2, off);
+        }
+        n0 = sqrtf(s0);
+        n1 = sqrtf(s1);
+        n2 = sqrtf(s2);
+    }
     const size_t o = ((size_t)r * half_pad + c) * kHeadDim + t;
     r_hi[o] = (uint16_t)hi;
     r_mid[o] = (uint16_t)mid;
-    float s0 = x * x, s1 = res * res, s2 = res2 * res2;
-    for (int off = 32; off >= 1; off >>= 1) {
-        s0 += __shfl_xor(s0, off);
-        s1 += __shfl_xor(s1, off);
-        s2 += __shfl_xor(s2, off);
-    }
     if (t == 0) {
         const size_t plane = (size_t)n_r * half_pad, k = (size_t)r * half_pad + c;
-        col_norm[k] = sqrtf(s0);
-        col_norm[plane + k] = sqrtf(s1);
-        col_norm[2 * plane + k] = sqrtf(s2);
+        col_norm[k] = n0;
+        col_norm[plane + k] = n1;
+        col_norm[2 * plane + k] = n2;
     }
 }
 
@@ -143,6 +225,7 @@ __global__ __launch_bounds__(kRefineThreads, 1) void hash_refine_kernel(const vo
                                                           const int* __restrict__ lists,
                                                           const int* __restrict__ counts,
                                                           const float* __restrict__ col_norm_max,
+                                                          const int* __restrict__ r_exp,
                                                           int32_t* __restrict__ buckets) {
     __shared__ RefineShared S;
     const int r = blockIdx.y;
@@ -153,7 +236,8 @@ __global__ __launch_bounds__(kRefineThreads, 1) void hash_refine_kernel(const vo
     const float* Rr = R + (size_t)r * kHeadDim * half;  // [t][half]
     const int lane = lane_id();
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const float cn = col_norm_max[r];
+    // max_c |R_c| of the round as given (the planes' norms are of R * 2^r_exp)
+    const float cn = r_exp ? ldexpf(col_norm_max[r], -r_exp[r]) : col_norm_max[r];
     const int c0 = wave * kRefineCols;  // this wave's columns in pass 1
     const int ncols = max(0, min(kRefineCols, half - c0));
 
@@ -303,26 +387,43 @@ __global__ __launch_bounds__(kRefineThreads, 1) void hash_refine_kernel(const vo
     }
 }
 
-// R streams through LDS in stages of 256 columns (8 tiles of 32) of one
-// round, one or both bf16 planes, double-buffered: at most 2 x 2 x 256 x
-// 128 B = 128 KB.  A stage is copied straight from global memory into LDS
-// (global_load_lds, no registers in between) while the previous one is
-// consumed, so there is one barrier per 8 tiles.  A 16-byte piece p of
-// column c sits at slot p ^ stage_swz(c) of the column's 128 bytes: the 16
-// columns read together by one operand load then hit distinct banks.
-constexpr int kStageCols = 256;
-constexpr int kStageTiles = kStageCols / 32;
-constexpr size_t kStageBytes = 2ull * 2 * kStageCols * 128;
+// R streams through LDS in stages of ST tiles (32 ST columns) of one round,
+// NP planes, double-buffered: 2 x NP x 32 ST x 128 B, at most 128 KB (one
+// plane with ST = 16, two with ST = 8).  ST is the round's tile count
+// rounded up to a power of two, capped there, so small rounds compute no
+// idle tiles and large ones few barriers.  A stage is copied straight from
+// global memory into LDS (buffer loads to LDS, no registers in between)
+// while the previous one is consumed, so there is one barrier per stage.  A
+// 16-byte piece p of column c sits at slot p ^ stage_swz(c) of the column's
+// 128 bytes: the 16 columns read together by one operand load then hit
+// distinct banks.
+template <int NP, int ST>
+struct Stage {
+    static constexpr int kCols = 32 * ST;
+    static constexpr size_t kBytes = 2ull * NP * kCols * 128;  // both buffers
+    static __device__ __forceinline__ uint32_t offset(int buf, int plane, int col) {
+        return (uint32_t)(((buf * NP + plane) * kCols + col) * 128);
+    }
+};
 
 __device__ __forceinline__ int stage_swz(int c) { return (c ^ (c >> 3)) & 7; }
 
-__device__ __forceinline__ uint32_t stage_offset(int buf, int plane, int col) {
-    return (uint32_t)(((buf * 2 + plane) * kStageCols + col) * 128);
+// LDS past the stage buffers: each wave's winners [64 rows][rounds] as
+// 16-bit ids.  The stage area is at least as large as the screen's final
+// list gathering needs, [rounds][64 WAVES] rows and two counters per round.
+__host__ __device__ constexpr size_t hash_win_offset(size_t stage_bytes, int waves, int rounds) {
+    const size_t lists = (size_t)rounds * (64 * waves + 2) * 4;
+    return ((stage_bytes > lists ? stage_bytes : lists) + 15) / 16 * 16;
 }
 
 // The screen's open row-rounds go to kSegs segments per round (workgroup b
 // appends to segment b % kSegs), so each list counter sees few atomics.
 constexpr int kSegs = 64;
+
+// The screen: waves per SIMD it is built for (three workgroups of four waves
+// on a CU, registers and LDS permitting), and its largest stage.
+constexpr int kScreenOcc = 3;
+constexpr int kScreenMaxTiles = 4;
 
 // Passes of the main kernel.
 enum : int {
@@ -335,31 +436,37 @@ struct Tile {
     f32x16 acc[kRB];
 };
 
-// Keys order projections by |projection| truncated to 19 mantissa bits
-// (non-negative floats order like their bit patterns), with the register
-// index j inside the tile in bits the truncation frees.
+// Keys order projections by |projection| truncated to a few bits less than
+// fp32's 24 (non-negative floats order like their bit patterns), with an
+// index in the bits the truncation frees:
 //  * fp32 input: the bit pattern rotated left by one (sign in bit 0,
-//    |projection| in bits 5..31, j in bits 1..4): one rotate and one and-or
-//    per projection, and the key also carries the winner's sign.
-//  * bf16 input: |projection| in bits 4..30 and j in bits 0..3, one and-or;
-//    the winner's sign is recomputed once per row and round.
-// Keys of tiles past the round are masked to j, near zero.
+//    |projection| in bits 5..31, the register j of the tile in bits 1..4):
+//    one rotate and one and-or per projection, and the key also carries the
+//    winner's sign.  The winner's tile is noted after every tile.
+//  * bf16 input: |projection| in bits 6..30 and 16 (t % 4) + j in bits
+//    0..5 (tile t of the round), one and-or; the winner's group of four
+//    tiles is noted after every fourth tile, and its sign is recomputed once
+//    per row and round.
+// Keys of tiles past the round are masked to their index, near zero.
+template <bool F32, int ST>
+constexpr int kKeyTiles = F32 ? 1 : (ST < 4 ? ST : 4);  // tiles sharing one index field
+
 template <bool F32>
-__device__ __forceinline__ uint32_t proj_key(float x, int j, bool live) {
+__device__ __forceinline__ uint32_t proj_key(float x, int idx, bool live) {
     const uint32_t u = __float_as_uint(x);
     if constexpr (F32) {
-        return (__builtin_amdgcn_alignbit(u, u, 31) & (live ? 0xFFFFFFE1u : 0u)) | ((uint32_t)j << 1);
+        return (__builtin_amdgcn_alignbit(u, u, 31) & (live ? 0xFFFFFFE1u : 0u)) | ((uint32_t)idx << 1);
     } else {
-        return (u & (live ? 0x7FFFFFF0u : 0u)) | (uint32_t)j;
+        return (u & (live ? 0x7FFFFFC0u : 0u)) | (uint32_t)idx;
     }
 }
 template <bool F32>
 __device__ __forceinline__ uint32_t key_index(uint32_t key) {
-    return F32 ? (key >> 1) & 15u : key & 15u;
+    return F32 ? (key >> 1) & 15u : key & 63u;
 }
 template <bool F32>
 __device__ __forceinline__ float key_magnitude(uint32_t key) {
-    return __uint_as_float(F32 ? (key >> 1) & 0x7FFFFFF0u : key & 0x7FFFFFF0u);
+    return __uint_as_float(F32 ? (key >> 1) & 0x7FFFFFF0u : key & 0x7FFFFFC0u);
 }
 
 // Running best b and second best sc (b >= sc) after two more keys: the
@@ -376,160 +483,182 @@ __device__ __forceinline__ void key_update2(uint32_t k1, uint32_t k2, uint32_t& 
     sc = max(sc, mid);
 }
 
-// Operand piece i of a tile (NP planes): k-step i / NP of plane i % NP.
-template <int NP>
-__device__ __forceinline__ uint32_t piece_offset(int col, int h, int i) {
-    const int s = NP == 2 ? i >> 1 : i;
-    return (uint32_t)col * 128u + (uint32_t)(((4 * h + s) ^ stage_swz(col)) << 4);
-}
-
-template <int NP>
-__device__ __forceinline__ void load_ops(u32x4 (&op)[8], const char* __restrict__ hi_base,
-                                         const char* __restrict__ mid_base, int col, int h) {
+// Lane offsets of the NP-plane operand pieces of tiles 0 and 1 inside a
+// stage buffer: piece i is k-step i / NP of plane i % NP.  Column 32 t + n
+// of tile t sits at 4096 t + 128 n with its pieces in swizzled slots, and
+// stage_swz(32 t + n) = stage_swz(n) ^ 4 (t % 2): even tiles share tile 0's
+// slot pattern, odd ones tile 1's.
+template <int NP, int ST>
+__device__ __forceinline__ void piece_offsets(uint32_t (&off)[2][8], int n, int h) {
 #pragma unroll
-    for (int i = 0; i < 4 * NP; ++i)
-        op[i] = *reinterpret_cast<const u32x4*>(((NP == 2 && (i & 1)) ? mid_base : hi_base) +
-                                                piece_offset<NP>(col, h, i));
+    for (int par = 0; par < 2; ++par)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int s = NP == 2 ? i >> 1 : i;
+            const int plane = NP == 2 ? (i & 1) : 0;
+            off[par][i] = (uint32_t)(plane * Stage<NP, ST>::kCols * 128 + (32 * par + n) * 128 +
+                                     (((4 * h + s) ^ stage_swz(32 * par + n)) << 4));
+        }
 }
 
-// One step of the tile pipeline, in eight slices.  Slice i issues the
+// Products of 16-bit operand words: bf16 planes for fp32 input, binary16
+// planes (of scaled q and R) for bf16 input.
+template <bool F32>
+__device__ __forceinline__ f32x16 mfma_op(u32x4 a, u32x4 b, f32x16 c) {
+    if constexpr (F32)
+        return mfma32x32x16(as_bf16x8(a), as_bf16x8(b), c);
+    else
+        return mfma32x32x16(as_f16x8(a), as_f16x8(b), c);
+}
+
+// One step of the tile pipeline, in eight slices.  Slice i issues (MF) the
 // products of the tile held in `op` into `nxt` for operand piece i (both
 // planes; for fp32 input the hi plane also meets q's second plane) or, with
 // one plane, for piece i / 2 on even slices; refills that piece with the same
-// piece of the following tile (PREF); and runs one eighth of the epilogue of
-// the previous tile `cur` (EPI).  A wave issues in order, so this
-// interleaving is what lets the vector ALUs work while the matrix core runs;
-// the scheduling barriers keep the compiler from regrouping the slices.
-template <bool F32, int NP, bool PREF, bool EPI>
-__device__ __forceinline__ void tile_step(Tile& nxt, u32x4 (&op)[8], const char* __restrict__ hi_base,
-                                          const char* __restrict__ mid_base, int col_pref, int h,
-                                          const bf16x8 (&qa)[kRB][4], const bf16x8 (&qm)[kRB][4],
-                                          const Tile& cur, int tile_cur, bool live,
-                                          uint32_t (&best)[kRB], uint32_t (&second)[kRB],
-                                          int (&best_tile)[kRB]) {
+// piece of tile TP (PREF) of the stage at `sb`; and runs one eighth of the
+// epilogue of the previous tile `cur`, tile TC of the stage (EPI).  A wave
+// issues in order, so this interleaving is what lets the vector ALUs work
+// while the matrix core runs; the scheduling barriers keep the compiler from
+// regrouping the slices.  Tile numbers are compile-time constants, so the
+// operand addresses are a lane offset plus an immediate and the key indices
+// are inline constants.
+template <bool F32, int NP, int G, bool MF, int TP, int TC>
+__device__ __forceinline__ void tile_step(Tile& nxt, u32x4 (&op)[8], const char* __restrict__ sb,
+                                          const uint32_t (&poff)[2][8], const u32x4 (&qa)[kRB][4],
+                                          const u32x4 (&qm)[kRB][4], const Tile& cur, bool live,
+                                          uint32_t (&best)[kRB], uint32_t (&second)[kRB]) {
     static_assert(kRB == 2, "slices written for two row blocks");
+    constexpr bool PREF = TP >= 0, EPI = TC >= 0;
+    constexpr int idx0 = EPI ? 16 * (TC % G) : 0;
     uint32_t b[kRB] = {best[0], best[1]}, sc[kRB] = {second[0], second[1]};
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         __builtin_amdgcn_sched_barrier(0);
-        if (NP == 2 || (i & 1) == 0) {
+        if (MF && (NP == 2 || (i & 1) == 0)) {
             const int pi = NP == 2 ? i : i >> 1;  // operand piece
             const int s = i >> 1;  // k-step
             const bool hi_plane = NP == 1 || (i & 1) == 0;
-            const bf16x8 a = as_bf16x8(op[pi]);
 #pragma unroll
             for (int rb = 0; rb < kRB; ++rb)
-                nxt.acc[rb] = mfma32x32x16(a, qa[rb][s], pi == 0 ? f32x16{} : nxt.acc[rb]);
+                nxt.acc[rb] = mfma_op<F32>(op[pi], qa[rb][s], pi == 0 ? f32x16{} : nxt.acc[rb]);
             if constexpr (F32) {
                 if (hi_plane) {
 #pragma unroll
-                    for (int rb = 0; rb < kRB; ++rb) nxt.acc[rb] = mfma32x32x16(a, qm[rb][s], nxt.acc[rb]);
+                    for (int rb = 0; rb < kRB; ++rb) nxt.acc[rb] = mfma_op<F32>(op[pi], qm[rb][s], nxt.acc[rb]);
                 }
             }
             if constexpr (PREF)
-                op[pi] = *reinterpret_cast<const u32x4*>((hi_plane ? hi_base : mid_base) +
-                                                         piece_offset<NP>(col_pref, h, pi));
+                op[pi] = *reinterpret_cast<const u32x4*>(sb + poff[TP & 1][pi] + (TP & ~1) * 4096);
         }
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (EPI) {
 #pragma unroll
             for (int rb = 0; rb < kRB; ++rb)
-                key_update2(proj_key<F32>(cur.acc[rb][2 * i], 2 * i, live),
-                            proj_key<F32>(cur.acc[rb][2 * i + 1], 2 * i + 1, live), b[rb], sc[rb]);
+                key_update2(proj_key<F32>(cur.acc[rb][2 * i], idx0 + 2 * i, live),
+                            proj_key<F32>(cur.acc[rb][2 * i + 1], idx0 + 2 * i + 1, live), b[rb], sc[rb]);
         }
     }
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (EPI) {
 #pragma unroll
         for (int rb = 0; rb < kRB; ++rb) {
-            best_tile[rb] = b[rb] != best[rb] ? tile_cur : best_tile[rb];
             best[rb] = b[rb];
             second[rb] = sc[rb];
         }
     }
 }
 
-template <bool F32>
-__device__ __forceinline__ void tile_epilogue(const Tile& T, int tile, bool live, uint32_t (&best)[kRB],
-                                              uint32_t (&second)[kRB], int (&best_tile)[kRB]) {
-#pragma unroll
-    for (int rb = 0; rb < kRB; ++rb) {
-        uint32_t b = best[rb], sc = second[rb];
-#pragma unroll
-        for (int j = 0; j < 16; j += 2)
-            key_update2(proj_key<F32>(T.acc[rb][j], j, live), proj_key<F32>(T.acc[rb][j + 1], j + 1, live), b, sc);
-        best_tile[rb] = b != best[rb] ? tile : best_tile[rb];
-        best[rb] = b;
-        second[rb] = sc;
-    }
+// Source offsets of 1 KB runs of 8 columns (c0 .. c0+7, c0 a multiple of
+// 8, stage-local): lane = 8 cl + slot fetches the piece that belongs at LDS
+// slot `slot` of column c0 + cl, piece slot ^ stage_swz(c0 + cl).  As
+// stage_swz(c0 + cl) = cl ^ (c0 / 8 % 8), the lane's byte offset in the run
+// is run_lane_offset(lane) ^ (16 * (c0 / 8 % 8)): one xor per run.
+__device__ __forceinline__ uint32_t run_lane_offset(int lane) {
+    const int cl = lane >> 3, slot = lane & 7;
+    return (uint32_t)(cl * 128 + ((slot ^ cl) << 4));
 }
 
-// Copy global stage g (round g / spr, columns (g % spr) * 256 ...) of NP
+// Raw buffer over one R plane (word 3 of the descriptor: raw, untyped
+// 32-bit data as on other CDNA parts); loads past num_records return 0.
+constexpr int kRawBufferWord3 = 0x00020000;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_buffer(const uint16_t* plane, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(plane), 0, (int)bytes, kRawBufferWord3);
+}
+
+// One run straight into LDS: a buffer load with the run's column in the
+// scalar offset and the lane's piece in the vector offset (no 64-bit vector
+// addresses to keep).
+__device__ __forceinline__ void copy_run(__amdgpu_buffer_rsrc_t plane, int64_t col0, uint32_t lane_off, int c0,
+                                         char* lds_dst) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(plane, (__attribute__((address_space(3))) void*)lds_dst, 16,
+                                             lane_off ^ (uint32_t)(((c0 >> 3) & 7) << 4), (uint32_t)(col0 * 128),
+                                             0, 0);
+}
+
+// Copy global stage g (round g / spr, columns (g % spr) * 32 ST ...) of NP
 // planes into buffer buf.  Each wave moves whole 1 KB runs of 8 columns of
-// one plane.
-template <int WAVES, int NP>
+// one plane; a run past the round copies the round's first columns instead
+// (any valid address: never read).
+template <int WAVES, int NP, int ST>
 __device__ __forceinline__ void load_stage(char* smem, int buf, int g, int spr, int half_pad,
-                                           const uint16_t* __restrict__ r_hi,
-                                           const uint16_t* __restrict__ r_mid, int wave, int lane) {
-    constexpr int kRuns = NP * kStageCols / 8;  // 1 KB runs per stage
-    static_assert(kRuns % WAVES == 0, "runs split evenly over the waves");
+                                           __amdgpu_buffer_rsrc_t r_hi, __amdgpu_buffer_rsrc_t r_mid, int wave,
+                                           uint32_t lane_off) {
+    constexpr int kCols = Stage<NP, ST>::kCols;
+    constexpr int kRuns = NP * kCols / 8;  // 1 KB runs per stage
     const int r = g / spr, st = g % spr;
-    const int cl_lane = lane >> 3, slot = lane & 7;
 #pragma unroll
-    for (int i = 0; i < kRuns / WAVES; ++i) {
-        const int run = wave * (kRuns / WAVES) + i;
-        const int plane = run / (kStageCols / 8);
-        const int c0 = (run % (kStageCols / 8)) * 8;
-        const int c = c0 + cl_lane;
-        int gcol = st * kStageCols + c;
-        gcol = gcol < half_pad ? gcol : 0;  // past the round: any valid address, never read
-        const uint16_t* src = (plane ? r_mid : r_hi) +
-                              ((size_t)r * half_pad + gcol) * kHeadDim + (slot ^ stage_swz(c)) * 8;
-        __builtin_amdgcn_global_load_lds(
-            (const __attribute__((address_space(1))) void*)src,
-            (__attribute__((address_space(3))) void*)(smem + stage_offset(buf, plane, c0)), 16, 0, 0);
+    for (int i = 0; i < (kRuns + WAVES - 1) / WAVES; ++i) {
+        const int run = wave + i * WAVES;  // uniform per wave
+        if (kRuns % WAVES == 0 || run < kRuns) {
+            const int plane = run / (kCols / 8);
+            const int c0 = (run % (kCols / 8)) * 8;
+            const int gc0 = st * kCols + c0;
+            copy_run(plane ? r_mid : r_hi, (int64_t)r * half_pad + (gc0 < half_pad ? gc0 : 0), lane_off, c0,
+                     smem + Stage<NP, ST>::offset(buf, plane, c0));
+        }
     }
 }
 
-// Copy round r's whole mid plane (up to 512 columns) into the mid-plane
-// halves of the two stage buffers, which the one-plane screen leaves free:
-// column c at buffer c / 256, slot c % 256, with the stage layout.  The
-// screen reads its winners' mid pieces from there.
-template <int WAVES>
-__device__ __forceinline__ void load_round_mid(char* smem, int r, int half_pad,
-                                               const uint16_t* __restrict__ r_mid, int wave, int lane) {
-    constexpr int kRuns = 2 * kStageCols / 8;  // 1 KB runs of 8 columns
-    static_assert(kRuns % WAVES == 0, "runs split evenly over the waves");
-    const int cl_lane = lane >> 3, slot = lane & 7;
-#pragma unroll
-    for (int i = 0; i < kRuns / WAVES; ++i) {
-        const int run = wave * (kRuns / WAVES) + i;
-        const int c0 = run * 8, c = c0 + cl_lane;  // column of the round
-        const int gcol = c < half_pad ? c : 0;     // past the round: any valid address, never read
-        const int sc = c % kStageCols;
-        const uint16_t* src = r_mid + ((size_t)r * half_pad + gcol) * kHeadDim + (slot ^ stage_swz(sc)) * 8;
-        __builtin_amdgcn_global_load_lds(
-            (const __attribute__((address_space(1))) void*)src,
-            (__attribute__((address_space(3))) void*)(smem + stage_offset(c0 / kStageCols, 1, c0 % kStageCols)),
-            16, 0, 0);
-    }
-}
-
-// This lane half's 32 k-values of q . R_col for one plane: 16 bf16 pair
+// This lane half's 32 k-values of q . R_col for one binary16 plane: 16 pair
 // products in four short chains (fp32 sums of exact products).
-__device__ __forceinline__ float dot_planes(const bf16x8 (&qa4)[4], const u32x4 (&rv)[4]) {
+__device__ __forceinline__ float dot_planes(const u32x4 (&qa4)[4], const u32x4 (&rv)[4]) {
+    typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
     float part[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s4 = 0; s4 < 4; ++s4) {
-        const u32x4 qv = __builtin_bit_cast(u32x4, qa4[s4]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const uint32_t qw = qv[e], rw = rv[s4][e];
-            part[e] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, qw), __builtin_bit_cast(bf16x2, rw),
-                                                      part[e], false);
+            const uint32_t qw = qa4[s4][e], rw = rv[s4][e];
+            part[e] = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, qw), __builtin_bit_cast(f16x2, rw), part[e],
+                                             false);
         }
     }
     return (part[0] + part[1]) + (part[2] + part[3]);
+}
+
+// The tile pipeline of one stage of ST tiles: step T issues tile T's
+// products (into ta for even T, tb for odd), prefetches tile T + 1's
+// operands and runs the epilogue of tile T - 1; a last step runs tile
+// ST - 1's epilogue alone.  ge(t) is called after tile t's epilogue.
+template <bool F32, int NP, int ST, int T, class GE>
+__device__ __forceinline__ void stage_pipe(Tile& ta, Tile& tb, u32x4 (&op)[8], const char* __restrict__ sb,
+                                           const uint32_t (&poff)[2][8], const u32x4 (&qa)[kRB][4],
+                                           const u32x4 (&qm)[kRB][4], int nt, uint32_t (&best)[kRB],
+                                           uint32_t (&second)[kRB], GE& ge) {
+    if constexpr (T < ST) {
+        Tile& nxt = T % 2 == 0 ? ta : tb;
+        Tile& cur = T % 2 == 0 ? tb : ta;
+        tile_step<F32, NP, kKeyTiles<F32, ST>, true, (T + 1 < ST ? T + 1 : -1), T - 1>(
+            nxt, op, sb, poff, qa, qm, cur, T - 1 < nt, best, second);
+        if constexpr (T >= 1) ge(T - 1);
+        stage_pipe<F32, NP, ST, T + 1>(ta, tb, op, sb, poff, qa, qm, nt, best, second, ge);
+    } else {
+        Tile& cur = (ST - 1) % 2 == 0 ? ta : tb;
+        tile_step<F32, NP, kKeyTiles<F32, ST>, false, -1, ST - 1>(cur, op, sb, poff, qa, qm, cur, ST - 1 < nt, best,
+                                                                  second);
+        ge(ST - 1);
+    }
 }
 
 // Winner of a row-round as kept in LDS until the row's ids are written:
@@ -539,8 +668,9 @@ constexpr uint16_t kUnsettled = 0xFFFFu;
 // The main kernel, one of three passes (MODE).  A wave owns 64 rows (two
 // 32-row blocks) and sweeps every staged tile once for them.
 //  * kScreen and kExact take rows blockIdx.x * 64 * WAVES + ... and all
-//    rounds; kListed takes, for round blockIdx.z, the rows at chunk
-//    blockIdx.x of the screen's segment blockIdx.y of that round.
+//    rounds; kListed takes, for round blockIdx.z, the rows the screen left
+//    open in that round (its segments one after another), in chunks of
+//    64 * WAVES, workgroup blockIdx.x taking every gridDim.x-th chunk.
 //  * Every screened projection is within
 //        eps = |q| * (res_max[r] + err_acc * max_c |R_c|)
 //    of the exact one (res_max: largest 2-norm of R's columns less the
@@ -554,8 +684,8 @@ constexpr uint16_t kUnsettled = 0xFFFFu;
 //    screen's lists are segmented, [round][kSegs][seg_cap] with counts
 //    [round][kSegs]; the exact passes' are [round][rows] with one count per
 //    round (few rows reach them).
-template <bool F32, int MODE, int WAVES>
-__global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
+template <bool F32, int MODE, int WAVES, int ST>
+__global__ __launch_bounds__(WAVES * 64, (MODE == kScreen ? kScreenOcc : 1)) void hash_kernel(
     const void* __restrict__ q, int64_t rows, int n_r, int half, int half_pad,
     const uint16_t* __restrict__ r_hi, const uint16_t* __restrict__ r_mid,
     const float* __restrict__ col_norm_max, const float* __restrict__ res_max, float err_acc,
@@ -569,22 +699,33 @@ __global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
     extern __shared__ __attribute__((aligned(16))) char smem[];
 
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6, h = lane >> 5, n = lane & 31;
-    const int tpr = half_pad / 32;                         // tiles per round
-    const int spr = (tpr + kStageTiles - 1) / kStageTiles;  // stages per round
+    const int lane = tid & 63, h = lane >> 5, n = lane & 31;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint32_t run_off = run_lane_offset(lane);
+    const uint32_t plane_bytes = (uint32_t)((size_t)n_r * half_pad * kHeadDim * 2);
+    const __amdgpu_buffer_rsrc_t rs_hi = plane_buffer(r_hi, plane_bytes), rs_mid = plane_buffer(r_mid, plane_bytes);
+    using SG = Stage<NP, ST>;
+    const int tpr = half_pad / 32;            // tiles per round
+    const int spr = (tpr + ST - 1) / ST;      // stages per round
     const int r_lo = MODE == kListed ? (int)blockIdx.z : 0;
     const int r_end = MODE == kListed ? r_lo + 1 : n_r;
     const int nrb = r_end - r_lo;  // rounds of this block
-    int64_t listed = 0;            // kListed: rows in this block's segment
-    const int* seg_rows = nullptr;
+    // kListed: the round's open rows, segment after segment; lane s holds
+    // the end of segment s in that sequence (kSegs is the wave width)
+    int64_t listed = 0;
+    int seg_end = 0;
     if constexpr (MODE == kListed) {
-        const int64_t seg = (int64_t)r_lo * kSegs + blockIdx.y;
-        listed = count_in[seg];
-        seg_rows = list_in + seg * seg_cap;
+        static_assert(kSegs == 64, "one segment per lane");
+        int incl = count_in[(int64_t)r_lo * kSegs + lane];
+        for (int o = 1; o < 64; o <<= 1) {
+            const int y = __shfl_up(incl, o);
+            if (lane >= o) incl += y;
+        }
+        seg_end = incl;
+        listed = __shfl(incl, 63);
     }
-    // kListed: a few workgroups per segment take its chunks of 64 * WAVES rows
-    // in turn (an empty workgroup costs as much to launch as a busy one when
-    // one fills a CU); the other passes take one chunk each.
+    // kListed: the workgroups take the round's chunks of 64 * WAVES rows in
+    // turn; the other passes take one chunk each.
     for (int64_t chunk = blockIdx.x;; chunk += gridDim.x) {
     if (MODE == kListed && chunk * (WAVES * kWaveRows) >= listed) break;  // uniform per block
     const int64_t slot0 = chunk * (WAVES * kWaveRows) + wave * kWaveRows;
@@ -594,20 +735,31 @@ __global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
         const int64_t k = slot0 + rb * 32 + n;
         if constexpr (MODE == kListed) {
             valid = k < listed;
-            return valid ? seg_rows[k] : 0;
+            // segment of entry k: the first s with seg_end[s] > k (binary
+            // search over the lanes; every lane takes part in the shuffles)
+            const int kk = (int)min(k, max(listed - 1, (int64_t)0));
+            int sg = 0;
+#pragma unroll
+            for (int step = 32; step >= 1; step >>= 1)
+                if (__shfl(seg_end, sg + step - 1) <= kk) sg += step;
+            sg = min(sg, 63);
+            const int before = __shfl(seg_end, max(sg - 1, 0));
+            const int64_t at = ((int64_t)r_lo * kSegs + sg) * seg_cap + (kk - (sg > 0 ? before : 0));
+            return valid ? list_in[at] : 0;
         } else {
             valid = k < rows;
             return valid ? k : 0;
         }
     };
     // this wave's winners: [row in wave][round of the block]
-    uint16_t* win = reinterpret_cast<uint16_t*>(smem + kStageBytes) + (size_t)wave * kWaveRows * nrb;
+    uint16_t* win = reinterpret_cast<uint16_t*>(smem + hash_win_offset(SG::kBytes, WAVES, nrb)) +
+                    (size_t)wave * kWaveRows * nrb;
 
-    load_stage<WAVES, NP>(smem, 0, r_lo * spr, spr, half_pad, r_hi, r_mid, wave, lane);
+    load_stage<WAVES, NP, ST>(smem, 0, r_lo * spr, spr, half_pad, rs_hi, rs_mid, wave, run_off);
 
     // Queries as the B operand: lane holds row (n) and k = 32h + 8s + e, s = 0..3.
-    bf16x8 qa[kRB][4];
-    bf16x8 qm[kRB][4];  // fp32 input: second bf16 plane of q
+    u32x4 qa[kRB][4];
+    u32x4 qm[kRB][4];  // fp32 input: second bf16 plane of q
     float qn[kRB];
 #pragma unroll
     for (int rb = 0; rb < kRB; ++rb) {
@@ -632,22 +784,45 @@ __global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
                     ss = fmaf(xs[2 * e], xs[2 * e], ss);
                     ss = fmaf(xs[2 * e + 1], xs[2 * e + 1], ss);
                 }
-                qa[rb][s4] = as_bf16x8(hi);
-                qm[rb][s4] = as_bf16x8(mid);
+                qa[rb][s4] = hi;
+                qm[rb][s4] = mid;
             }
         } else {
+            // The row times 2^sq, with its largest |q_t| brought into
+            // [2^14, 2^15): exact in fp32, and in binary16 for every value
+            // from fp16's smallest normal 2^-14 up (bf16 has 8 significant
+            // bits); smaller values are dropped, |delta q| <= 8 * 2^-14.
             const uint16_t* src = static_cast<const uint16_t*>(q) + row * kHeadDim + 32 * h;
+            u32x4 raw[4];
+            float mx = 0.f;
 #pragma unroll
             for (int s4 = 0; s4 < 4; ++s4) {
-                const u32x4 raw = valid ? *reinterpret_cast<const u32x4*>(src + 8 * s4) : u32x4{0, 0, 0, 0};
+                raw[s4] = valid ? *reinterpret_cast<const u32x4*>(src + 8 * s4) : u32x4{0, 0, 0, 0};
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float a = __uint_as_float(raw[e] << 16), b = __uint_as_float(raw[e] & 0xFFFF0000u);
-                    ss = fmaf(a, a, ss);
-                    ss = fmaf(b, b, ss);
-                }
-                qa[rb][s4] = as_bf16x8(raw);
-                qm[rb][s4] = as_bf16x8(u32x4{0, 0, 0, 0});
+                for (int e = 0; e < 4; ++e)
+                    mx = fmaxf(mx, fmaxf(fabsf(__uint_as_float(raw[s4][e] << 16)),
+                                         fabsf(__uint_as_float(raw[s4][e] & 0xFFFF0000u))));
+            }
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            int k = 0;
+            (void)frexpf(mx, &k);
+            const int sq = (mx > 0.f && mx <= 3.4e38f) ? 14 - (k - 1) : 0;
+            const float f1 = __uint_as_float((uint32_t)(127 + sq / 2) << 23);
+            const float f2 = __uint_as_float((uint32_t)(127 + sq - sq / 2) << 23);
+            auto to_f16 = [&](float x) {
+                const float xs = x * f1 * f2;
+                ss = fmaf(xs, xs, ss);
+                return fabsf(xs) < 0x1p-14f ? 0.f : xs;
+            };
+#pragma unroll
+            for (int s4 = 0; s4 < 4; ++s4) {
+                u32x4 w;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    w[e] = pack_f16x2(to_f16(__uint_as_float(raw[s4][e] << 16)),
+                                      to_f16(__uint_as_float(raw[s4][e] & 0xFFFF0000u)));
+                qa[rb][s4] = w;
+                qm[rb][s4] = u32x4{0, 0, 0, 0};
             }
         }
         ss += __shfl_xor(ss, 32);
@@ -656,57 +831,53 @@ __global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
-    uint32_t best[kRB], second[kRB];
-    int best_tile[kRB];
+    uint32_t poff[2][8];
+    piece_offsets<NP, ST>(poff, n, h);
+    constexpr int G = kKeyTiles<F32, ST>;
+    // best and second key, the best key before the current group of G
+    // tiles, and the group the best key came from
+    uint32_t best[kRB], second[kRB], grp_start[kRB];
+    int best_grp[kRB];
     const int g_end = r_end * spr;
     for (int g = r_lo * spr; g < g_end; ++g) {
         const int r = g / spr, st = g % spr, buf = (g - r_lo * spr) & 1;
         if (st == 0) {
 #pragma unroll
             for (int rb = 0; rb < kRB; ++rb) {
-                best[rb] = second[rb] = 0u;
-                best_tile[rb] = 0;
+                best[rb] = second[rb] = grp_start[rb] = 0u;
+                best_grp[rb] = 0;
             }
         }
         // the next stage lands in the other buffer while this one computes
         if (g + 1 < g_end)
-            load_stage<WAVES, NP>(smem, buf ^ 1, g + 1, spr, half_pad, r_hi, r_mid, wave, lane);
-        if constexpr (MODE == kScreen)
-            if (st == 0) load_round_mid<WAVES>(smem, r, half_pad, r_mid, wave, lane);
-        const char* hi_base = smem + stage_offset(buf, 0, 0);
-        const char* mid_base = smem + stage_offset(buf, 1, 0);
-        const int nt = min(kStageTiles, tpr - st * kStageTiles);
-        const int t0 = st * kStageTiles;
-        // Every stage runs all eight tiles; tiles past the round (a last,
+            load_stage<WAVES, NP, ST>(smem, buf ^ 1, g + 1, spr, half_pad, rs_hi, rs_mid, wave, run_off);
+        const char* sb = smem + SG::offset(buf, 0, 0);
+        const int nt = min(ST, tpr - st * ST);
+        const int t0 = st * ST;
+        // after the epilogue of stage tile tc: note the group if it ends there
+        // (stages start on group boundaries: G divides ST)
+        auto group_end = [&](int tc) {
+            if ((tc + 1) % G == 0) {
+#pragma unroll
+                for (int rb = 0; rb < kRB; ++rb) {
+                    best_grp[rb] = best[rb] != grp_start[rb] ? (t0 + tc) / G : best_grp[rb];
+                    grp_start[rb] = best[rb];
+                }
+            }
+        };
+        // Every stage runs all ST tiles; tiles past the round (a last,
         // partial stage) compute on stale LDS and their keys are masked to
         // (near) zero, so they can only win when every key is tiny, and such
         // a row is left to the exact passes.
-        static_assert(kStageTiles == 8, "pipeline written for eight tiles per stage");
         {
             Tile ta, tb;
             u32x4 op[8];
-            load_ops<NP>(op, hi_base, mid_base, n, h);
-            tile_step<F32, NP, true, false>(ta, op, hi_base, mid_base, 32 + n, h, qa, qm, tb, 0, false,
-                                            best, second, best_tile);
-#pragma unroll 1
-            for (int t = 1; t < kStageTiles - 1; t += 2) {
-                tile_step<F32, NP, true, true>(tb, op, hi_base, mid_base, 32 * (t + 1) + n, h, qa, qm,
-                                               ta, t0 + t - 1, t - 1 < nt, best, second, best_tile);
-                tile_step<F32, NP, true, true>(ta, op, hi_base, mid_base, 32 * (t + 2) + n, h, qa, qm,
-                                               tb, t0 + t, t < nt, best, second, best_tile);
-            }
-            tile_step<F32, NP, false, true>(tb, op, hi_base, mid_base, 0, h, qa, qm, ta, t0 + 6, 6 < nt,
-                                            best, second, best_tile);
-            tile_epilogue<F32>(tb, t0 + 7, 7 < nt, best, second, best_tile);
+#pragma unroll
+            for (int i = 0; i < 4 * NP; ++i) op[i] = *reinterpret_cast<const u32x4*>(sb + poff[0][i]);
+            stage_pipe<F32, NP, ST, 0>(ta, tb, op, sb, poff, qa, qm, nt, best, second, group_end);
         }
 
         if (st == spr - 1) {
-            if constexpr (MODE == kScreen) {
-                if (spr == 1) {  // this stage's mid-plane copies: landed and seen by every wave
-                    __builtin_amdgcn_s_waitcnt(0);
-                    __syncthreads();
-                }
-            }
             // Round epilogue: merge the two lane halves (different columns of
             // the same row) and decide; lane half h keeps row block h's result.
             const float cn = col_norm_max[r];
@@ -717,13 +888,14 @@ __global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
             for (int rb = 0; rb < kRB; ++rb) {
                 const uint32_t bb = best[rb], ss2 = second[rb];
                 const uint32_t bp = __shfl_xor(bb, 32), sp = __shfl_xor(ss2, 32);
-                const int tp = __shfl_xor(best_tile[rb], 32);
+                const int tp = __shfl_xor(best_grp[rb], 32);
                 const bool mine = bb > bp || (bb == bp && h == 0);
                 bk[rb] = mine ? bb : bp;
                 sk[rb] = max(min(bb, bp), max(ss2, sp));
                 const int hw = mine ? h : (h ^ 1);
-                const int tw = mine ? best_tile[rb] : tp;
-                const uint32_t j = key_index<F32>(bk[rb]);
+                const int gw = mine ? best_grp[rb] : tp;
+                const uint32_t idx = key_index<F32>(bk[rb]), j = idx & 15u;
+                const int tw = gw * G + (int)(idx >> 4);  // tile of the round
                 col[rb] = tw * 32 + 8 * (int)(j >> 2) + 4 * hw + (int)(j & 3u);
             }
             if constexpr (F32) {
@@ -747,8 +919,8 @@ __global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
                 // by the truncated bits) plus the pass's eps, so the winner is
                 // certain when |x| - eps2 exceeds that, and its sign is x's.  A
                 // flagged winner may sit past the round; any valid column
-                // stands in.  The hi pieces come from global memory (the lines
-                // were staged moments ago), the screen's mid pieces from LDS.
+                // stands in.  Both planes' pieces come from global memory (the
+                // planes are small and stay in the caches).
                 u32x4 hv[kRB][4], mv[kRB][4];
 #pragma unroll
                 for (int rb = 0; rb < kRB; ++rb) {
@@ -759,13 +931,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void hash_kernel(
 #pragma unroll
                     for (int s4 = 0; s4 < 4; ++s4) {
                         hv[rb][s4] = ph[s4];
-                        if constexpr (MODE == kScreen) {
-                            const int sc = cc % kStageCols;
-                            mv[rb][s4] = *reinterpret_cast<const u32x4*>(
-                                smem + stage_offset(cc / kStageCols, 1, sc) + (((4 * h + s4) ^ stage_swz(sc)) << 4));
-                        } else {
-                            mv[rb][s4] = pm[s4];
-                        }
+                        mv[rb][s4] = pm[s4];
                     }
                 }
 #pragma unroll
@@ -848,6 +1014,8 @@ struct HashWs {
     uint16_t* r_mid;
     float* col_norm;  // [3][n_r][half_pad]: |R_c|, |R_c - hi_c|, |R_c - hi_c - mid_c|
     float* norm_max;  // [3][n_r]: the largest of each
+    int* r_exp;       // [n_r]: binary16 planes hold R * 2^r_exp (bf16 input)
+    float* r_part;    // [n_r][kScaleParts]: partial maxima of |R|
     int* count;       // [n_r][kSegs] rows left open by the screen, then [n_r] by the exact passes
     int* list1;       // [n_r][kSegs][seg_cap]
     int* list2;       // [n_r][rows]
@@ -855,7 +1023,7 @@ struct HashWs {
     size_t bytes;
 };
 
-constexpr int kHashWaves = 8;
+constexpr int kHashWaves = 4;
 constexpr int64_t kRowsPerBlock = kHashWaves * 64;
 
 HashWs carve(void* base, int64_t rows, int n_rounds, int half_pad) {
@@ -873,6 +1041,10 @@ HashWs carve(void* base, int64_t rows, int n_rounds, int half_pad) {
     off += align256((size_t)3 * n_rounds * half_pad * 4);
     w.norm_max = reinterpret_cast<float*>(p + off);
     off += align256((size_t)3 * n_rounds * 4);
+    w.r_exp = reinterpret_cast<int*>(p + off);
+    off += align256((size_t)n_rounds * 4);
+    w.r_part = reinterpret_cast<float*>(p + off);
+    off += align256((size_t)n_rounds * kScaleParts * 4);
     w.count = reinterpret_cast<int*>(p + off);
     off += align256((size_t)n_rounds * (kSegs + 1) * 4);
     w.list1 = reinterpret_cast<int*>(p + off);
@@ -881,6 +1053,54 @@ HashWs carve(void* base, int64_t rows, int n_rounds, int half_pad) {
     off += align256((size_t)n_rounds * rows * 4);
     w.bytes = off;
     return w;
+}
+
+// Arguments of one pass of hash_kernel.
+struct PassArgs {
+    const void* q;
+    int64_t rows;
+    int n_r, half, half_pad;
+    const uint16_t *r_hi, *r_mid;
+    const float *cn_max, *res;
+    float err_acc;
+    const float* res2;
+    float err_acc2, err_pack;
+    int32_t* buckets;
+    const int *list_in, *count_in;
+    int *list_out, *count_out;
+    int64_t seg_cap;
+};
+
+template <bool F32, int MODE, int WAVES, int ST>
+void launch_pass_st(const PassArgs& a, dim3 grid, int rounds, hipStream_t stream) {
+    constexpr int NP = MODE == kScreen ? 1 : 2;
+    const size_t lds = hash_win_offset(Stage<NP, ST>::kBytes, WAVES, rounds) + (size_t)WAVES * 64 * rounds * 2;
+    auto* k = &hash_kernel<F32, MODE, WAVES, ST>;
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    k<<<grid, WAVES * 64, lds, stream>>>(a.q, a.rows, a.n_r, a.half, a.half_pad, a.r_hi, a.r_mid, a.cn_max, a.res,
+                                         a.err_acc, a.res2, a.err_acc2, a.err_pack, a.buckets, a.list_in,
+                                         a.count_in, a.list_out, a.count_out, a.seg_cap);
+}
+
+// Tiles per stage: the round's tile count rounded up to a power of two, at
+// most 16 for the screen (one plane, 64 KB a buffer), 8 for the fp32 pass
+// (two planes) and 4 for the listed pass (two planes; past that its
+// registers would spill).
+template <bool F32, int MODE, int WAVES>
+void launch_pass(const PassArgs& a, dim3 grid, int rounds, hipStream_t stream) {
+    constexpr int kMax = MODE == kScreen ? kScreenMaxTiles : (MODE == kListed ? 4 : 8);
+    const int tpr = a.half_pad / 32;
+    if (tpr <= 1)
+        launch_pass_st<F32, MODE, WAVES, 1>(a, grid, rounds, stream);
+    else if (tpr <= 2)
+        launch_pass_st<F32, MODE, WAVES, 2>(a, grid, rounds, stream);
+    else if (tpr <= 4 || kMax == 4)
+        launch_pass_st<F32, MODE, WAVES, 4>(a, grid, rounds, stream);
+    else if (tpr <= 8 || kMax == 8) {
+        if constexpr (kMax >= 8) launch_pass_st<F32, MODE, WAVES, 8>(a, grid, rounds, stream);
+    } else {
+        if constexpr (kMax >= 16) launch_pass_st<F32, MODE, WAVES, 16>(a, grid, rounds, stream);
+    }
 }
 
 }  // namespace
@@ -901,23 +1121,32 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
     int* count1 = w.count;                                  // [n_r][kSegs]: left open by the screen
     int* count2 = w.count + (size_t)n_rounds * kSegs;       // [n_r]: left to the fp64 refinement
 
-    prep_r_cols_kernel<<<dim3(half_pad, n_rounds), 64, 0, stream>>>(R, half, half_pad, w.r_hi,
-                                                                     w.r_mid, w.col_norm);
+    if (f32) {
+        prep_r_cols_kernel<false><<<dim3(half_pad, n_rounds), 64, 0, stream>>>(
+            R, half, half_pad, nullptr, nullptr, w.r_hi, w.r_mid, w.col_norm);
+    } else {
+        prep_r_part_kernel<<<dim3(kScaleParts, n_rounds), 256, 0, stream>>>(R, half, w.r_part);
+        prep_r_cols_kernel<true><<<dim3(half_pad, n_rounds), 64, 0, stream>>>(
+            R, half, half_pad, w.r_part, w.r_exp, w.r_hi, w.r_mid, w.col_norm);
+    }
     prep_r_max_kernel<<<dim3(n_rounds, 3), 256, 0, stream>>>(w.col_norm, n_rounds, half_pad, w.norm_max,
                                                              w.count, n_rounds * (kSegs + 1));
     if (rows == 0) return hipGetLastError();
 
     // Error of a screened key against the exact |projection| p_c, beyond the
     // planes' residual q . (R_c - planes) <= |q| |R_c - planes|:
-    //  * fp32 accumulation of the exact bf16 products, <= one ulp of the
+    //  * fp32 accumulation of the exact 16-bit products, <= one ulp of the
     //    partial sum (<= 2^-23 sum_t |q_t R_tc|) per addition;
+    //  * for bf16 input, the scaled q's values below 2^-14 that binary16
+    //    drops: |delta q| <= 8 * 2^-14 <= 2^-25 |q| (|q| >= 2^14 scaled);
     //  * for fp32 input, q's own residual after two bf16 planes and R's
     //    after two (<= 3.1 * 2^-16 sum_t |q_t R_tc| together);
-    //  * the 4 index bits written over the low mantissa, < 2^-19 |key|.
+    //  * the index bits written over the low mantissa, < 2^-19 |key| for
+    //    fp32 input (4 bits), < 2^-17 |key| for bf16 input (6 bits).
     // sum_t |q_t R_tc| <= |q| |R_c| (Cauchy-Schwarz) <= |q| max_c |R_c|.
-    const float err_pack = (float)0x1p-19;
-    const float acc1 = (float)(kHeadDim * 0x1p-23 * 1.01);
-    const float acc2 = (float)(2 * kHeadDim * 0x1p-23 * 1.01);
+    const float err_pack = f32 ? (float)0x1p-19 : (float)0x1p-17;
+    const float acc1 = (float)((kHeadDim * 0x1p-23 + 0x1p-25) * 1.01);
+    const float acc2 = (float)((2 * kHeadDim * 0x1p-23 + 0x1p-25) * 1.01);
     const float acc_f32 = (float)((3.1 * 0x1p-16 + 3 * kHeadDim * 0x1p-23) * 1.01);
 
     constexpr int kWaves = kHashWaves;
@@ -926,38 +1155,34 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
     // rows, a few groups of 64 per round; longer lists are strided.
     const unsigned refine_blocks =
         (unsigned)std::max<int64_t>(1, std::min<int64_t>(256, (rows + kRefineGroup - 1) / kRefineGroup));
-    auto lds_for = [&](int rounds) { return kStageBytes + (size_t)kRowsPerBlock * rounds * 2; };
     if (f32) {
-        auto* k = &hash_kernel<true, kExact, kWaves>;
-        hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)lds_for(n_rounds));
-        k<<<grid, kWaves * 64, lds_for(n_rounds), stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi, w.r_mid,
-                                                           cn_max, nullptr, acc_f32, nullptr, 0.f, err_pack, buckets,
-                                                           nullptr, nullptr, w.list2, count2, 0);
+        launch_pass<true, kExact, kWaves>(
+            PassArgs{q, rows, n_rounds, half, half_pad, w.r_hi, w.r_mid, cn_max, nullptr, acc_f32, nullptr, 0.f,
+                     err_pack, buckets, nullptr, nullptr, w.list2, count2, 0},
+            dim3(grid), n_rounds, stream);
         hash_refine_kernel<true><<<dim3(refine_blocks, n_rounds), kRefineThreads, 0, stream>>>(
-            q, R, half, n_rounds, rows, w.list2, count2, cn_max, buckets);
+            q, R, half, n_rounds, rows, w.list2, count2, cn_max, nullptr, buckets);
     } else {
         // screen with R's hi plane; the rows it leaves open get both planes;
         // what those leave open gets the fp64 refinement
-        auto* ks = &hash_kernel<false, kScreen, kWaves>;
-        hipFuncSetAttribute(reinterpret_cast<const void*>(ks), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)lds_for(n_rounds));
-        ks<<<grid, kWaves * 64, lds_for(n_rounds), stream>>>(q, rows, n_rounds, half, half_pad, w.r_hi,
-                                                            w.r_mid, cn_max, res1_max, acc1, res2_max, acc2,
-                                                            err_pack, buckets, nullptr, nullptr, w.list1, count1,
-                                                            w.seg_cap);
-        auto* kl = &hash_kernel<false, kListed, kWaves>;
-        hipFuncSetAttribute(reinterpret_cast<const void*>(kl), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)lds_for(1));
-        // three workgroups per segment cover the 3 * 512 rows a segment of 32
-        // screen workgroups holds at a 9.4% open rate (Gaussian data leaves
-        // about 6.3% open); longer segments loop
-        const unsigned per_seg = (unsigned)std::min<int64_t>(3, w.seg_cap / kRowsPerBlock);
-        kl<<<dim3(per_seg, kSegs, n_rounds), kWaves * 64, lds_for(1), stream>>>(
-            q, rows, n_rounds, half, half_pad, w.r_hi, w.r_mid, cn_max, res2_max, acc2, res2_max, acc2, err_pack, buckets,
-            w.list1, count1, w.list2, count2, w.seg_cap);
+        launch_pass<false, kScreen, kWaves>(
+            PassArgs{q, rows, n_rounds, half, half_pad, w.r_hi, w.r_mid, cn_max, res1_max, acc1, res2_max, acc2,
+                     err_pack, buckets, nullptr, nullptr, w.list1, count1, w.seg_cap},
+            dim3(grid), n_rounds, stream);
+        // Four waves a workgroup: with one wave per SIMD the two-plane
+        // pipeline keeps its values in registers.  The screen leaves about
+        // 0.9% of row-rounds open on Gaussian data (binary16 planes): 64
+        // workgroups per round cover 64 * 256 open rows, 1.6% of 1M rows;
+        // longer lists loop.
+        constexpr int kListedWaves = 4;
+        const int64_t listed_rows = kListedWaves * 64;
+        const unsigned per_round = (unsigned)std::min<int64_t>(64, (rows + listed_rows - 1) / listed_rows);
+        launch_pass<false, kListed, kListedWaves>(
+            PassArgs{q, rows, n_rounds, half, half_pad, w.r_hi, w.r_mid, cn_max, res2_max, acc2, res2_max, acc2,
+                     err_pack, buckets, w.list1, count1, w.list2, count2, w.seg_cap},
+            dim3(per_round, 1, n_rounds), 1, stream);
         hash_refine_kernel<false><<<dim3(refine_blocks, n_rounds), kRefineThreads, 0, stream>>>(
-            q, R, half, n_rounds, rows, w.list2, count2, cn_max, buckets);
+            q, R, half, n_rounds, rows, w.list2, count2, cn_max, w.r_exp, buckets);
     }
     return hipGetLastError();
 }

@@ -242,6 +242,64 @@ def test_hash_exact_ties(gpu, dtype):
     assert np.array_equal(got, want)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("n_buckets", [2, 6, 66, 128, 200, 640, 1022])
+def test_hash_bucket_counts(gpu, dtype, n_buckets):
+    """Bucket counts the five workloads do not use: rounds of 1 to 511
+    columns, so R's stages hold 1, 2, 4, 8 or 16 tiles and the last tile or
+    stage of a round is partial.  Bit for bit against the oracle."""
+    w = small("causal_bf16_L16384", B=1, H=2, L=1536, n_buckets=n_buckets, n_rounds=2, dtype=dtype)
+    x, q64, _ = _inputs(w)
+    want, near = oracle.lsh_hash(q64, x["R"].astype(np.float64))
+    cfg = lsh.Config.of(w)
+    log("hash-buckets", dtype, n_buckets)
+    got = lsh.lsh_hash(cfg, to_device(x["q"], dtype), to_device(x["R"], "f32")).cpu().numpy()
+    print(f"{dtype} n_b={n_buckets}: near-tie row-rounds {int(near.sum())}, mismatches {int((got != want).sum())}")
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_hash_extreme_scales(gpu, dtype):
+    """Rows and rounds far from unit scale.  Each round's R is scaled by a
+    power of two (2^-60, 1, 2^50 for bf16 input; 2^-30, 1, 2^30 for fp32);
+    query rows are scaled by 2^k with k spread over [-100, 100] (bf16) or
+    [-40, 40] (fp32), and for bf16 input some rows also hold a few values
+    2^30 times larger than the rest (after the row's scaling the small ones
+    fall below binary16's normal range) or lie in bf16's subnormal range.
+    The argmax is scale invariant and the GPU's ids must equal the fp64
+    oracle's everywhere."""
+    w = small("causal_bf16_L16384", B=1, H=2, L=2048, n_buckets=256, n_rounds=3, dtype=dtype)
+    x = W.make_inputs(w)
+    R = x["R"].astype(np.float32).copy()
+    q = W.as_f64(x["q"], dtype).astype(np.float32).reshape(-1, w.d)
+    rng = np.random.default_rng(5150)
+    kmax = 100 if dtype == "bf16" else 40
+    rows = q.shape[0]
+    k = rng.integers(-kmax, kmax + 1, rows)
+    q = q * np.ldexp(1.0, k)[:, None].astype(np.float32)
+    if dtype == "bf16":
+        R[0] *= np.float32(2.0 ** -60)
+        R[1] *= np.float32(2.0 ** 50)
+        wide = np.arange(rows) % 4 == 1  # a few large values beside small ones
+        q[wide] *= np.float32(2.0 ** -40)  # stays inside fp32's range
+        q[wide, :4] *= np.float32(2.0 ** 30)
+        sub = np.arange(rows) % 4 == 2   # bf16 subnormals (below 2^-126)
+        q[sub] = (W.as_f64(x["q"], dtype).reshape(-1, w.d)[sub] * 2.0 ** -130).astype(np.float32)
+        qin = W.f32_to_bf16_bits(q).reshape(x["q"].shape)
+    else:
+        R[0] *= np.float32(2.0 ** -30)
+        R[1] *= np.float32(2.0 ** 30)
+        qin = q.reshape(x["q"].shape)
+    q64 = W.as_f64(qin, dtype)
+    assert np.isfinite(q64).all() and (np.abs(q64).max(axis=-1) > 0).all()
+    want, near = oracle.lsh_hash(q64, R.astype(np.float64))
+    cfg = lsh.Config.of(w)
+    log("hash-scales", dtype)
+    got = lsh.lsh_hash(cfg, to_device(qin, dtype), to_device(R, "f32")).cpu().numpy()
+    print(f"{dtype}: near-tie row-rounds {int(near.sum())}, mismatches {int((got != want).sum())}")
+    assert np.array_equal(got, want)
+
+
 def _rounds_input(o: np.ndarray, dtype: str, rng):
     """Per-round rows in the format lsh_combine_rounds takes for `dtype`, and
     their exact float64 values.  For bf16 calls: fp16 rows with a per-row
