@@ -16,6 +16,16 @@ Draw order, from one ``numpy.random.Generator(PCG64(seed))``:
   4. dO [B, H, L, d], iid N(0, 1) (only for workloads with a backward).
 bf16 tensors are fp32 draws rounded to nearest even and are carried as their
 uint16 bit patterns.
+
+The reversible-block workloads (BLOCKS, make_block_inputs) draw, in order:
+R; x1 [B, L, d_model] ~ N(0, 1); x2 the same, or for "exact" inputs rows of
++-1 with d_model/2 of each sign in random order; LayerNorm 1 gain 1 + 0.1 N
+and bias 0.1 N (exact inputs: 1 and 0); W_qk and W_v [H*64, d_model] ~
+N(0, 1/d_model) in bf16 (exact inputs: k 2^-10 with k uniform in -127..127);
+W_o [d_model, H*64] ~ N(0, 1/(H*64)); LayerNorm 2 like LayerNorm 1 (always
+random); W1 [d_ff, d_model] ~ N(0, 1/d_model), b1 [d_ff] ~ 0.1 N;
+W2 [d_model, d_ff] ~ N(0, 1/d_ff), b2 [d_model] ~ 0.1 N.  Weight matrices
+are bf16 bit patterns, the rest fp32.
 """
 from __future__ import annotations
 
@@ -144,6 +154,83 @@ def make_inputs(w: Workload, seed: int | None = None, with_dout: bool | None = N
             out["dout"] = dout
     else:
         raise ValueError(f"unknown dtype {w.dtype!r}")
+    return out
+
+
+@dataclass(frozen=True)
+class BlockWorkload:
+    """A reversible block (attention half + chunked feed-forward half) around
+    LSH attention with H heads of 64 (d_model = 64 H)."""
+    name: str
+    B: int
+    L: int
+    H: int
+    d_ff: int
+    n_buckets: int
+    n_rounds: int
+    chunk: int
+    causal: bool
+    ff_chunk: int           # rows per feed-forward chunk (0: all rows)
+    ln_eps: float = 1e-5
+    seed: int = 0
+    exact: bool = False     # inputs whose LayerNorm and projections are exact
+    notes: str = field(default="", compare=False)
+
+    @property
+    def d_model(self) -> int:
+        return 64 * self.H
+
+    @property
+    def rows(self) -> int:
+        return self.B * self.L
+
+    def scaled(self, **kw) -> "BlockWorkload":
+        return replace(self, **kw)
+
+
+BLOCKS = {
+    "revblock_bf16_L65536": BlockWorkload(
+        "revblock_bf16_L65536", B=1, L=65536, H=16, d_ff=4096, n_buckets=1024, n_rounds=8, chunk=64,
+        causal=True, ff_chunk=16384, seed=5,
+        notes="d_model 1024, d_ff 4096 (the paper's sizes), the long workload's attention"),
+}
+
+
+def make_block_inputs(w: BlockWorkload, seed: int | None = None) -> dict:
+    """Draw R, x1, x2 and the block's weights (see the module notes)."""
+    rng = np.random.Generator(np.random.PCG64(w.seed if seed is None else seed))
+    D, F, HD = w.d_model, w.d_ff, 64 * w.H
+    out = {"R": rng.standard_normal((w.n_rounds, 64, w.n_buckets // 2), dtype=np.float32)}
+    out["x1"] = rng.standard_normal((w.B, w.L, D), dtype=np.float32)
+    if w.exact:
+        signs = np.tile(np.repeat(np.array([1.0, -1.0], np.float32), D // 2), (w.B * w.L, 1))
+        out["x2"] = rng.permuted(signs, axis=1).reshape(w.B, w.L, D)
+    else:
+        out["x2"] = rng.standard_normal((w.B, w.L, D), dtype=np.float32)
+
+    def ln_params(unit):
+        if unit:
+            return np.ones(D, np.float32), np.zeros(D, np.float32)
+        g = (1.0 + 0.1 * rng.standard_normal(D)).astype(np.float32)
+        return g, (0.1 * rng.standard_normal(D)).astype(np.float32)
+
+    def dense(rows, cols, fan_in):
+        return f32_to_bf16_bits((rng.standard_normal((rows, cols)) / np.sqrt(fan_in)).astype(np.float32))
+
+    out["ln1_g"], out["ln1_b"] = ln_params(w.exact)
+    if w.exact:
+        k = rng.integers(-127, 128, size=(2, HD, D))
+        out["w_qk"] = f32_to_bf16_bits((k[0] * 2.0 ** -10).astype(np.float32))
+        out["w_v"] = f32_to_bf16_bits((k[1] * 2.0 ** -10).astype(np.float32))
+    else:
+        out["w_qk"] = dense(HD, D, D)
+        out["w_v"] = dense(HD, D, D)
+    out["w_o"] = dense(D, HD, HD)
+    out["ln2_g"], out["ln2_b"] = ln_params(False)
+    out["w1"] = dense(F, D, D)
+    out["b1"] = (0.1 * rng.standard_normal(F)).astype(np.float32)
+    out["w2"] = dense(D, F, F)
+    out["b2"] = (0.1 * rng.standard_normal(D)).astype(np.float32)
     return out
 
 
