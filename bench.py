@@ -291,6 +291,132 @@ def stage_rooflines(w: W.Workload, work: dict, st: dict) -> dict:
             "attn": attn, "combine": hbm(work["combine_bytes"], st["combine"])}
 
 
+def block_flop(wb: W.BlockWorkload) -> dict:
+    """Algorithmic flops of one block direction (forward or inverse): the
+    products of F (q and v projections, output projection: 3 x 2 M D D) and
+    of G (2 x 2 M D d_ff), and the LSH attention's hash and chunk products."""
+    M, D, F = wb.rows, wb.d_model, wb.d_ff
+    att = W.Workload("block-attn", B=wb.B, H=wb.H, L=wb.L, d=64, dtype="bf16", n_buckets=wb.n_buckets,
+                     n_rounds=wb.n_rounds, chunk=wb.chunk, causal=wb.causal)
+    a = algorithmic_work(att)
+    return {"proj": 3 * 2.0 * M * D * D, "ff": 2 * 2.0 * M * D * F, "hash": a["hash_flop"], "attn": a["attn_flop"]}
+
+
+def run_block(wb: W.BlockWorkload, steps: int, warmup: int, cpu_budget: float) -> dict:
+    """One step: the block forward (y1, y2 from x1, x2) and its inverse (x1, x2
+    back from y1, y2), each one library call.  Also times F and G alone and
+    the feed-forward's first product at one chunk's shape (M = ff_chunk,
+    N = d_ff, K = d_model), the block's dominant kernel."""
+    dev = torch.device("cuda:0")
+    x = W.make_block_inputs(wb)
+
+    def up(a):
+        t = torch.from_numpy(np.ascontiguousarray(a))
+        return (t.view(torch.int16).view(torch.bfloat16) if a.dtype == np.uint16 else t).to(dev)
+
+    wts = lsh.BlockWeights(**{k: up(v) for k, v in x.items() if k not in ("x1", "x2")})
+    cfg = lsh.BlockConfig.of(wb)
+    x1, x2 = up(x["x1"]), up(x["x2"])
+    y1, y2, r1, r2 = (torch.empty_like(x1) for _ in range(4))
+    ws = torch.empty(lsh.block_workspace_bytes(cfg, lsh.LSH_BLOCK_OP_BLOCK), dtype=torch.uint8, device=dev)
+    rows = wb.ff_chunk if 0 < wb.ff_chunk < wb.rows else wb.rows
+    a = torch.randn((rows, wb.d_model), device=dev).to(torch.bfloat16)
+
+    def timed(fn, n):
+        for _ in range(warmup):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    fwd = lambda: lsh.rev_block_fwd(cfg, wts, x1, x2, y1, y2, ws)
+    inv = lambda: lsh.rev_block_inv(cfg, wts, y1, y2, r1, r2, ws)
+    for _ in range(warmup):
+        fwd()
+        inv()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fwd()
+        inv()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    res = {"ms_per_step": ms, "fwd_ms": timed(fwd, steps), "inv_ms": timed(inv, steps),
+           "F_ms": timed(lambda: lsh.rev_attention(cfg, wts, x2, x1, 1.0, y1, ws), steps),
+           "G_ms": timed(lambda: lsh.rev_feed_forward(cfg, wts, y1, x2, 1.0, y2, ws), steps),
+           "ff1_ms": timed(lambda: lsh.linear_bf16(a, wts.w1, wts.b1, relu_bf16=True), steps)}
+    fwd()
+    inv()
+    torch.cuda.synchronize()
+    res["inverse_max_err"] = {"x1": float((r1 - x1).abs().max()), "x2": float((r2 - x2).abs().max())}
+    if cpu_budget > 0:
+        res["cpu_baseline"] = block_cpu_baseline(wb, cpu_budget)
+    return res
+
+
+def block_cpu_baseline(wb: W.BlockWorkload, budget_s: float) -> dict:
+    """The oracle's block forward and inverse on a shortened sequence of the
+    same block (same widths, heads and hashing), L halved until one pass
+    should fit the budget; tokens/s of forward + inverse."""
+    from oracle import block as OB  # test infrastructure: only for the reported baseline
+
+    # flops of a forward + inverse per token: 2 x (3 projections 2 D^2 + 2
+    # feed-forward products 2 D d_ff); fp64 NumPy products run at roughly
+    # 20 GFLOP/s on the host
+    per_token = 2 * (6 * wb.d_model ** 2 + 4 * wb.d_model * wb.d_ff)
+    L = wb.L
+    while L > 256 and L * per_token > budget_s * 20e9:
+        L //= 2
+    w = wb.scaled(L=L)
+    x = W.make_block_inputs(w)
+    f = lambda v: W.as_f64(v, "bf16") if v.dtype == np.uint16 else v.astype(np.float64)
+    wh = OB.BlockWeights(**{k: f(v) for k, v in x.items() if k not in ("x1", "x2")})
+    args = (wh, w.H, w.chunk, w.causal, w.ln_eps, w.ff_chunk)
+    import oracle
+    t0 = time.perf_counter()
+    y1, y2 = OB.rev_block_fwd(x["x1"], x["x2"], *args)
+    OB.rev_block_inv(y1, y2, *args)
+    el = time.perf_counter() - t0
+    return {"value": w.rows / el, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "cpu_model": cpu_model(),
+            "sample": f"one block forward and inverse at L={L} (B={w.B}, d_model={w.d_model}, d_ff={w.d_ff}, "
+                      f"{w.H} heads, {w.n_rounds} rounds), fp64 NumPy and the C oracle, {el:.1f} s"}
+
+
+def block_line(wb: W.BlockWorkload, steps: int, warmup: int, cpu_budget: float) -> dict:
+    g = run_block(wb, steps, warmup, cpu_budget)
+    fl = block_flop(wb)
+    rows = wb.ff_chunk if 0 < wb.ff_chunk < wb.rows else wb.rows
+    ff1 = 2.0 * rows * wb.d_model * wb.d_ff
+    ach = ff1 / (g["ff1_ms"] * 1e-3) / 1e12
+    total = sum(fl.values())
+    line = {
+        "metric": "reversible block (LSH attention + chunked feed-forward) forward + inverse tokens/sec",
+        "value": wb.rows / (g["ms_per_step"] * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": steps,
+        "warmup": warmup, "ms_per_step": g["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wb.name, "B": wb.B, "L": wb.L, "H": wb.H, "d_model": wb.d_model, "d_ff": wb.d_ff,
+                   "n_buckets": wb.n_buckets, "n_rounds": wb.n_rounds, "chunk": wb.chunk, "causal": wb.causal,
+                   "ff_chunk": wb.ff_chunk},
+        "stage_ms": {"forward": g["fwd_ms"], "inverse": g["inv_ms"], "F": g["F_ms"], "G": g["G_ms"]},
+        "roofline": {"bound": "mfma", "achieved": ach, "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": ach / BF16_MFMA_PEAK_TFLOPS, "traffic": None, "stage": "ff1",
+                     "kernels": ["gemm_bf16_kernel"], "algorithmic": ff1,
+                     "shape": {"M": rows, "N": wb.d_ff, "K": wb.d_model}},
+        "block_mfma_frac": total / (g["fwd_ms"] * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
+        "algorithmic_flop_per_direction": fl,
+        "inverse_max_err": g["inverse_max_err"],
+    }
+    if "cpu_baseline" in g:
+        line["cpu_baseline"] = g["cpu_baseline"]
+    return line
+
+
 SWEEP_LENGTHS = (1024, 2048, 4096, 8192, 16384, 32768, 65536)
 
 
@@ -364,7 +490,7 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--workload", default=W.HEADLINE, choices=sorted(W.WORKLOADS))
+    ap.add_argument("--workload", default=W.HEADLINE, choices=sorted(W.WORKLOADS) + sorted(W.BLOCKS))
     ap.add_argument("--cpu-budget", type=float, default=8.0,
                     help="seconds of oracle time for the CPU baseline (0 to skip)")
     ap.add_argument("--copy-probe", type=int, default=0,
@@ -382,8 +508,11 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         return 2
-    w = W.WORKLOADS[args.workload]
     lsh.lib()
+    if args.workload in W.BLOCKS:
+        print(json.dumps(block_line(W.BLOCKS[args.workload], args.steps, args.warmup, args.cpu_budget)), flush=True)
+        return 0
+    w = W.WORKLOADS[args.workload]
     if args.sweep_length:
         sweep_length(args.steps, args.warmup)
         return 0

@@ -21,7 +21,8 @@ BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "liblsh.so")
 ARCH = os.environ.get("LSH_OFFLOAD_ARCH", "gfx950")
 
-SOURCES = ["hash.hip", "sort.hip", "attn_fwd.hip", "attn_bwd.hip", "combine.hip", "dense.hip", "lsh_api.cpp"]
+SOURCES = ["hash.hip", "sort.hip", "attn_fwd.hip", "attn_bwd.hip", "combine.hip", "dense.hip", "block.hip",
+           "lsh_api.cpp", "block_api.cpp"]
 
 COMMON_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

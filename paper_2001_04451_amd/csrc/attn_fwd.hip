@@ -420,25 +420,26 @@ __global__ __launch_bounds__((FwdGeom<M, AFTER>::kThreads), (FwdGeom<M, AFTER>::
             }
             const float mref = FAST ? 0.f : m;
             // normalised by the sum of the bf16 weights P V used (1/l to
-            // within 1 ulp); a lone query divides its exact v_i by 1
+            // within 1 ulp); a lone query divides its exact v_i by 1.  The
+            // largest magnitude is taken before normalising (one multiply
+            // less per element): scaling by inv > 0 keeps the maximum's place.
             const float inv = alone ? 1.f : __builtin_amdgcn_rcpf(oacc[4][0]);
             float amax = 0.f;
 #pragma unroll
-            for (int b = 0; b < 4; ++b) {
-                oacc[b] *= inv;
+            for (int b = 0; b < 4; ++b)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) amax = fmaxf(amax, fabsf(oacc[b][e]));
-            }
             amax = fmaxf(amax, __shfl_xor(amax, 16));
             amax = fmaxf(amax, __shfl_xor(amax, 32));
+            amax *= inv;
             // 2^(E-127) <= amax < 2^(E-126): e = max(0, E - 141) puts the
             // scaled row below 2^15, inside fp16's range
             const int ex = max(0, (int)((__float_as_uint(amax) >> 23) & 0xFFu) - 141);
-            const float sc = __uint_as_float((uint32_t)(127 - ex) << 23);
+            const float fac = inv * __uint_as_float((uint32_t)(127 - ex) << 23);
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
-                out_pend[b].x = pack_f16x2(oacc[b][0] * sc, oacc[b][1] * sc);
-                out_pend[b].y = pack_f16x2(oacc[b][2] * sc, oacc[b][3] * sc);
+                out_pend[b].x = pack_f16x2(oacc[b][0] * fac, oacc[b][1] * fac);
+                out_pend[b].y = pack_f16x2(oacc[b][2] * fac, oacc[b][3] * fac);
             }
             exp_pend = (uint32_t)ex;
             // z = scale*|q_i| - self_mask when the token is its own only target

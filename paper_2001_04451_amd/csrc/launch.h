@@ -10,6 +10,8 @@
 #include <algorithm>
 #include <cmath>
 
+struct lsh_config;  // include/lsh.h
+
 namespace lsh {
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -65,5 +67,23 @@ size_t dense_workspace_bytes(int64_t BH, int L);
 hipError_t launch_dense_fwd(int64_t BH, int L, bool causal, float scale, float self_mask,
                             const void* q, const void* v, void* out, float* lse, void* workspace,
                             hipStream_t stream);
+
+// ---- reversible block: LayerNorm and the dense products ----
+// LSH_OK when lsh_attention_fwd takes this configuration and dtype (its
+// checks, without any HIP call); otherwise the status it would return.
+int attention_fwd_supported(const ::lsh_config* cfg, int dtype);
+// fp32 rows [rows][D] -> bf16 rows, D a multiple of 128 up to 4096.
+hipError_t launch_layer_norm(const float* x, const float* g, const float* b, uint16_t* out, int64_t rows, int D,
+                             float eps, hipStream_t stream);
+// C = A W^T (A: [M][K] bf16 rows, or with a_heads the [B][H][L][64] layout
+// with K = 64 H, M = B L; W [N][K] bf16; N a multiple of 128, K of 64), then:
+enum : int {
+    kLinearResid = 0,     // out_f32 = resid + sign (C + bias)   (resid may be null)
+    kLinearReluBf16 = 1,  // out_bf16 = bf16(relu(C + bias))      [M][N]
+    kLinearHeads = 2      // out_bf16 = bf16(C + bias) in the [B][H][L][64] layout (N = 64 H)
+};
+hipError_t launch_linear(const uint16_t* a, bool a_heads, int L, int H, const uint16_t* w, int64_t M, int N, int K,
+                         const float* bias, int out_kind, const float* resid, float sign, float* out_f32,
+                         uint16_t* out_bf16, hipStream_t stream);
 
 }  // namespace lsh

@@ -119,6 +119,16 @@ size_t fwd_rounds_bytes(const lsh_config* cfg, lsh_dtype dtype) {
 
 }  // namespace
 
+namespace lsh {
+int attention_fwd_supported(const lsh_config* cfg, int dtype) {
+    LSH_TRY(check_config(cfg));
+    LSH_TRY(check_dtype(dtype));
+    LSH_TRY(check_supported(cfg));
+    LSH_TRY(check_chunk(cfg, dtype, false));
+    return check_self_mask(cfg);
+}
+}  // namespace lsh
+
 extern "C" {
 
 const char* lsh_status_string(int status) {

@@ -34,7 +34,11 @@ LSH_F32, LSH_BF16 = 0, 1
 EXPORTED = ("lsh_status_string", "lsh_workspace_bytes", "lsh_hash", "lsh_sort_permute",
             "lsh_sort_permute_static",
             "lsh_gather_rows", "lsh_chunk_attn_fwd", "lsh_combine_rounds", "lsh_attention_fwd",
-            "lsh_chunk_attn_bwd", "lsh_dense_attn_fwd")
+            "lsh_chunk_attn_bwd", "lsh_dense_attn_fwd",
+            # include/lsh_block.h
+            "lsh_block_workspace_bytes", "lsh_rev_attention", "lsh_rev_feed_forward",
+            "lsh_rev_block_fwd", "lsh_rev_block_inv", "lsh_linear_bf16")
+LSH_BLOCK_OP_ATTN, LSH_BLOCK_OP_FF, LSH_BLOCK_OP_BLOCK = 0, 1, 2
 
 
 class LshConfig(ctypes.Structure):
@@ -44,6 +48,16 @@ class LshConfig(ctypes.Structure):
                 ("causal", ctypes.c_int32), ("scale", ctypes.c_float),
                 ("self_mask", ctypes.c_float), ("chunks_after", ctypes.c_int32),
                 ("attend_across", ctypes.c_int32), ("r_per_head", ctypes.c_int32)]
+
+
+class BlockConfigC(ctypes.Structure):
+    _fields_ = [("attn", LshConfig), ("d_ff", ctypes.c_int32), ("ff_chunk", ctypes.c_int32),
+                ("ln_eps", ctypes.c_float)]
+
+
+class BlockWeightsC(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("ln1_g", "ln1_b", "w_qk", "w_v", "w_o", "R", "ln2_g",
+                                               "ln2_b", "w1", "b1", "w2", "b2")]
 
 
 class LshError(RuntimeError):
@@ -56,6 +70,8 @@ class LshError(RuntimeError):
 _lib = None
 _P = ctypes.c_void_p
 _CFG = ctypes.POINTER(LshConfig)
+_BCFG = ctypes.POINTER(BlockConfigC)
+_BW = ctypes.POINTER(BlockWeightsC)
 _SZ = ctypes.c_size_t
 _I = ctypes.c_int
 
@@ -82,7 +98,15 @@ def lib() -> ctypes.CDLL:
             "lsh_chunk_attn_bwd": [_CFG, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ,
                                    _P],
             "lsh_dense_attn_fwd": [_CFG, _I, _P, _P, _P, _P, _P, _SZ, _P],
+            "lsh_rev_attention": [_BCFG, _BW, _P, _P, _P, ctypes.c_float, _P, _SZ, _P],
+            "lsh_rev_feed_forward": [_BCFG, _BW, _P, _P, _P, ctypes.c_float, _P, _SZ, _P],
+            "lsh_rev_block_fwd": [_BCFG, _BW, _P, _P, _P, _P, _P, _SZ, _P],
+            "lsh_rev_block_inv": [_BCFG, _BW, _P, _P, _P, _P, _P, _SZ, _P],
+            "lsh_linear_bf16": [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P,
+                                ctypes.c_float, _P, _P, _P],
         }
+        L.lsh_block_workspace_bytes.argtypes = [_BCFG, _I]
+        L.lsh_block_workspace_bytes.restype = _SZ
         for name, args in sigs.items():
             fn = getattr(L, name)
             fn.argtypes = args
@@ -375,3 +399,136 @@ def lsh_dense_attn_fwd(cfg: Config, q, v, out=None, lse=None, workspace=None):
                                     _ptr(out), _ptr(lse), _ptr(workspace), workspace.numel(),
                                     _stream(dev)))
     return out, lse
+
+
+# --------------------------------------------------------------------------
+# the reversible block (include/lsh_block.h)
+# --------------------------------------------------------------------------
+@dataclass(frozen=True)
+class BlockConfig:
+    attn: Config
+    d_ff: int
+    ff_chunk: int = 0
+    ln_eps: float = 1e-5
+
+    @property
+    def d_model(self) -> int:
+        return 64 * self.attn.H
+
+    @property
+    def rows(self) -> int:
+        return self.attn.B * self.attn.L
+
+    def c(self) -> BlockConfigC:
+        return BlockConfigC(self.attn.c(), self.d_ff, self.ff_chunk, self.ln_eps)
+
+    @staticmethod
+    def of(w, **kw) -> "BlockConfig":
+        """From a workloads.BlockWorkload (keyword arguments override fields)."""
+        attn = Config(B=w.B, H=w.H, L=w.L, n_buckets=w.n_buckets, n_rounds=w.n_rounds, chunk=w.chunk,
+                      causal=w.causal)
+        c = dict(attn=attn, d_ff=w.d_ff, ff_chunk=w.ff_chunk, ln_eps=w.ln_eps)
+        c.update(kw)
+        return BlockConfig(**c)
+
+
+_WEIGHT_NAMES = ("ln1_g", "ln1_b", "w_qk", "w_v", "w_o", "R", "ln2_g", "ln2_b", "w1", "b1", "w2", "b2")
+
+
+class BlockWeights:
+    """Device tensors of the block's weights (bf16 matrices, fp32 vectors and R)."""
+
+    def __init__(self, **tensors):
+        for n in _WEIGHT_NAMES:
+            setattr(self, n, tensors[n])
+
+    def c(self) -> BlockWeightsC:
+        return BlockWeightsC(*[_ptr(getattr(self, n)) for n in _WEIGHT_NAMES])
+
+
+def block_workspace_bytes(cfg: BlockConfig, op: int) -> int:
+    return int(lib().lsh_block_workspace_bytes(ctypes.byref(cfg.c()), op))
+
+
+def _block_ws(cfg: BlockConfig, op: int, device) -> torch.Tensor:
+    return torch.empty(max(block_workspace_bytes(cfg, op), 256), dtype=torch.uint8, device=device)
+
+
+def _rows(cfg: BlockConfig, t: torch.Tensor, name: str) -> None:
+    _need(t, (cfg.attn.B, cfg.attn.L, cfg.d_model), torch.float32, name)
+
+
+def rev_attention(cfg: BlockConfig, w: BlockWeights, x, resid=None, sign: float = 1.0, out=None,
+                  workspace=None):
+    """out = resid + sign * F(x) (lsh_rev_attention)."""
+    _rows(cfg, x, "x")
+    if resid is not None:
+        _rows(cfg, resid, "resid")
+    out = torch.empty_like(x) if out is None else out
+    _rows(cfg, out, "out")
+    ws = _block_ws(cfg, LSH_BLOCK_OP_ATTN, x.device) if workspace is None else workspace
+    _check("lsh_rev_attention",
+           lib().lsh_rev_attention(ctypes.byref(cfg.c()), ctypes.byref(w.c()), _ptr(x), _ptr(resid), _ptr(out),
+                                   sign, _ptr(ws), ws.numel(), _stream(x.device)))
+    return out
+
+
+def rev_feed_forward(cfg: BlockConfig, w: BlockWeights, x, resid=None, sign: float = 1.0, out=None,
+                     workspace=None):
+    """out = resid + sign * G(x), chunked (lsh_rev_feed_forward)."""
+    _rows(cfg, x, "x")
+    if resid is not None:
+        _rows(cfg, resid, "resid")
+    out = torch.empty_like(x) if out is None else out
+    _rows(cfg, out, "out")
+    ws = _block_ws(cfg, LSH_BLOCK_OP_FF, x.device) if workspace is None else workspace
+    _check("lsh_rev_feed_forward",
+           lib().lsh_rev_feed_forward(ctypes.byref(cfg.c()), ctypes.byref(w.c()), _ptr(x), _ptr(resid),
+                                      _ptr(out), sign, _ptr(ws), ws.numel(), _stream(x.device)))
+    return out
+
+
+def rev_block_fwd(cfg: BlockConfig, w: BlockWeights, x1, x2, y1=None, y2=None, workspace=None):
+    """(y1, y2) = (x1 + F(x2), x2 + G(y1)) (lsh_rev_block_fwd)."""
+    for t, n in ((x1, "x1"), (x2, "x2")):
+        _rows(cfg, t, n)
+    y1 = torch.empty_like(x1) if y1 is None else y1
+    y2 = torch.empty_like(x2) if y2 is None else y2
+    ws = _block_ws(cfg, LSH_BLOCK_OP_BLOCK, x1.device) if workspace is None else workspace
+    _check("lsh_rev_block_fwd",
+           lib().lsh_rev_block_fwd(ctypes.byref(cfg.c()), ctypes.byref(w.c()), _ptr(x1), _ptr(x2), _ptr(y1),
+                                   _ptr(y2), _ptr(ws), ws.numel(), _stream(x1.device)))
+    return y1, y2
+
+
+def rev_block_inv(cfg: BlockConfig, w: BlockWeights, y1, y2, x1=None, x2=None, workspace=None):
+    """(x1, x2) = (y1 - F(x2), y2 - G(y1)) (lsh_rev_block_inv)."""
+    for t, n in ((y1, "y1"), (y2, "y2")):
+        _rows(cfg, t, n)
+    x1 = torch.empty_like(y1) if x1 is None else x1
+    x2 = torch.empty_like(y2) if x2 is None else x2
+    ws = _block_ws(cfg, LSH_BLOCK_OP_BLOCK, y1.device) if workspace is None else workspace
+    _check("lsh_rev_block_inv",
+           lib().lsh_rev_block_inv(ctypes.byref(cfg.c()), ctypes.byref(w.c()), _ptr(y1), _ptr(y2), _ptr(x1),
+                                   _ptr(x2), _ptr(ws), ws.numel(), _stream(y1.device)))
+    return x1, x2
+
+
+def linear_bf16(a: torch.Tensor, w: torch.Tensor, bias=None, resid=None, sign: float = 1.0,
+                relu_bf16: bool = False) -> torch.Tensor:
+    """The block's product (lsh_linear_bf16): resid + sign (a w^T + bias) in
+    fp32, or bf16(relu(a w^T + bias)) with relu_bf16."""
+    M, K = a.shape
+    N = w.shape[0]
+    _need(a, (M, K), torch.bfloat16, "a")
+    _need(w, (N, K), torch.bfloat16, "w")
+    if relu_bf16:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=a.device)
+        args = (None, _ptr(out))
+    else:
+        out = torch.empty((M, N), dtype=torch.float32, device=a.device)
+        args = (_ptr(out), None)
+    _check("lsh_linear_bf16",
+           lib().lsh_linear_bf16(M, N, K, _ptr(a), _ptr(w), _ptr(bias), _ptr(resid), sign, *args,
+                                 _stream(a.device)))
+    return out

@@ -9,7 +9,7 @@ import pytest
 from paper_2001_04451_amd import lsh
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "lsh.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("lsh.h", "lsh_block.h")]
 
 
 @pytest.fixture(scope="module")
@@ -20,9 +20,9 @@ def L():
 
 
 def declared_symbols():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(lsh_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(lsh_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_header_symbols_exported(L):
@@ -235,3 +235,63 @@ def test_across_needs_undo(L):
     c = _cfg(attend_across=1)
     assert L.lsh_chunk_attn_fwd(ctypes.byref(c), lsh.LSH_F32, FAKE, FAKE, FAKE, FAKE, None, FAKE,
                                 FAKE, None, FAKE, None, 0, None) == lsh.LSH_ERR_INVALID
+
+
+def _bcfg(attn=None, d_ff=256, ff_chunk=0, ln_eps=1e-5):
+    attn = attn or _cfg(B=1, H=2, L=256, n_buckets=16, n_rounds=2, causal=1)
+    return lsh.BlockConfigC(attn, d_ff, ff_chunk, ln_eps)
+
+
+def _bweights(**kw):
+    names = [n for n, _ in lsh.BlockWeightsC._fields_]
+    vals = {n: FAKE.value for n in names}
+    vals.update(kw)
+    return lsh.BlockWeightsC(**vals)
+
+
+def test_block_workspace_and_validation(L):
+    """The reversible block's entry points validate before any HIP call."""
+    c = _bcfg()
+    for op in (lsh.LSH_BLOCK_OP_ATTN, lsh.LSH_BLOCK_OP_FF, lsh.LSH_BLOCK_OP_BLOCK):
+        assert L.lsh_block_workspace_bytes(ctypes.byref(c), op) > 0
+    assert L.lsh_block_workspace_bytes(None, 0) == 0
+    # the feed-forward's scratch follows its chunk
+    big = L.lsh_block_workspace_bytes(ctypes.byref(_bcfg(ff_chunk=0)), lsh.LSH_BLOCK_OP_FF)
+    small = L.lsh_block_workspace_bytes(ctypes.byref(_bcfg(ff_chunk=64)), lsh.LSH_BLOCK_OP_FF)
+    assert small < big
+    w = _bweights()
+    huge = 1 << 40
+
+    def att(cfg, wts, ws_bytes=huge, x=FAKE):
+        return L.lsh_rev_attention(ctypes.byref(cfg), ctypes.byref(wts) if wts else None, x, None, FAKE,
+                                   1.0, FAKE, ws_bytes, None)
+
+    def ff(cfg, wts, ws_bytes=huge):
+        return L.lsh_rev_feed_forward(ctypes.byref(cfg), ctypes.byref(wts) if wts else None, FAKE, None, FAKE,
+                                      1.0, FAKE, ws_bytes, None)
+
+    assert att(_bcfg(d_ff=0), w) == lsh.LSH_ERR_INVALID
+    assert att(_bcfg(d_ff=100), w) == lsh.LSH_ERR_UNSUPPORTED
+    assert att(_bcfg(attn=_cfg(B=1, H=3, L=256, n_buckets=16, n_rounds=2)), w) == lsh.LSH_ERR_UNSUPPORTED
+    assert att(_bcfg(attn=_cfg(B=1, H=2, L=256, n_buckets=16, n_rounds=2, d=32)), w) == lsh.LSH_ERR_UNSUPPORTED
+    assert att(_bcfg(ln_eps=float("nan")), w) == lsh.LSH_ERR_INVALID
+    assert att(c, None) == lsh.LSH_ERR_INVALID
+    assert att(c, _bweights(w_qk=None)) == lsh.LSH_ERR_INVALID
+    assert att(c, _bweights(w_o=FAKE.value + 4)) == lsh.LSH_ERR_INVALID  # misaligned
+    assert att(c, w, ws_bytes=16) == lsh.LSH_ERR_INVALID
+    assert att(c, w, x=None) == lsh.LSH_ERR_INVALID
+    assert ff(c, _bweights(b2=None)) == lsh.LSH_ERR_INVALID
+    assert ff(c, w, ws_bytes=16) == lsh.LSH_ERR_INVALID
+    for fn in (L.lsh_rev_block_fwd, L.lsh_rev_block_inv):
+        assert fn(ctypes.byref(c), ctypes.byref(w), FAKE, FAKE, FAKE, None, FAKE, huge, None) == lsh.LSH_ERR_INVALID
+        assert fn(ctypes.byref(c), ctypes.byref(w), FAKE, FAKE, FAKE, FAKE, FAKE, 16, None) == lsh.LSH_ERR_INVALID
+
+
+def test_linear_validation(L):
+    f = L.lsh_linear_bf16
+    assert f(128, 100, 64, FAKE, FAKE, None, None, 1.0, FAKE, None, None) == lsh.LSH_ERR_UNSUPPORTED
+    assert f(128, 128, 32, FAKE, FAKE, None, None, 1.0, FAKE, None, None) == lsh.LSH_ERR_UNSUPPORTED
+    assert f(128, 128, 64, None, FAKE, None, None, 1.0, FAKE, None, None) == lsh.LSH_ERR_INVALID
+    assert f(128, 128, 64, FAKE, FAKE, None, None, 1.0, None, None, None) == lsh.LSH_ERR_INVALID
+    assert f(-1, 128, 64, FAKE, FAKE, None, None, 1.0, FAKE, None, None) == lsh.LSH_ERR_INVALID
+    assert f(1 << 30, 4096, 64, FAKE, FAKE, None, None, 1.0, FAKE, None, None) == lsh.LSH_ERR_UNSUPPORTED
