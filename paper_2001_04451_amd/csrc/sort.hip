@@ -4,13 +4,14 @@
 // order.
 //
 // A segment of L positions is cut into tiles of kTile positions.
-//   1. hist:    per (tile, round) bucket counts, LDS atomics.
+//   1. hist:    per (tile, round) bucket counts, LDS atomics; stored
+//               [segment][tile][bucket].
 //   2. scan:    exclusive scan of the counts in (bucket, tile) order gives
 //               every (bucket, tile) pair its first output slot, and the
 //               bucket start offsets.
 //   3. scatter: each wave ranks its quarter of a tile in position order; the
 //               rank of a position among equal buckets of its 64-lane group
-//               comes from ballots over the bucket bits (peer mask + popcount),
+//               comes from a per-bucket lane mask in LDS (peers + popcount),
 //               so equal keys keep their position order (stable).
 #include "common.h"
 #include "launch.h"
@@ -31,6 +32,9 @@ __device__ __forceinline__ int clamp_bucket(int b, int n_b) { return min(max(b, 
 // waves to keep enough loads in flight.
 constexpr int kHistThreads = 1024;
 
+constexpr int kHistRows = kTile / kHistThreads;  // positions per thread
+constexpr int kHistMaxRounds = 16;
+
 __global__ __launch_bounds__(kHistThreads) void sort_hist_kernel(const int32_t* __restrict__ buckets, int L,
                                                         int n_r, int n_b, int rounds_per_group,
                                                         int n_tiles, int32_t* __restrict__ counts) {
@@ -40,49 +44,64 @@ __global__ __launch_bounds__(kHistThreads) void sort_hist_kernel(const int32_t* 
     const int r0 = blockIdx.z * rounds_per_group;
     const int nr = min(rounds_per_group, n_r - r0);
     for (int i = threadIdx.x; i < nr * n_b; i += blockDim.x) hist[i] = 0;
-    __syncthreads();
     const int p0 = tile * kTile, p1 = min(L, p0 + kTile);
-    for (int p = p0 + threadIdx.x; p < p1; p += blockDim.x) {
+    // every id of the thread's positions loaded before the first atomic
+    // (16-byte loads when a position's ids of this group are aligned)
+    int ids[kHistRows][kHistMaxRounds];
+    const bool vec = (n_r % 4) == 0 && (r0 % 4) == 0;
+#pragma unroll
+    for (int k = 0; k < kHistRows; ++k) {
+        const int p = min(p0 + (int)threadIdx.x + kHistThreads * k, p1 - 1);  // past the tile: reloads a valid row
         const int32_t* row = buckets + (bh * L + p) * n_r + r0;
-        for (int r = 0; r < nr; ++r) atomicAdd(&hist[r * n_b + clamp_bucket(row[r], n_b)], 1);
+        if (vec) {
+#pragma unroll
+            for (int c4 = 0; c4 < kHistMaxRounds / 4; ++c4)
+                if (4 * c4 < nr) {
+                    const int4 x = *reinterpret_cast<const int4*>(row + 4 * c4);
+                    ids[k][4 * c4] = x.x;
+                    ids[k][4 * c4 + 1] = x.y;
+                    ids[k][4 * c4 + 2] = x.z;
+                    ids[k][4 * c4 + 3] = x.w;
+                }
+        } else {
+#pragma unroll
+            for (int r = 0; r < kHistMaxRounds; ++r)
+                if (r < nr) ids[k][r] = row[r];
+        }
     }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kHistRows; ++k)
+        if (p0 + (int)threadIdx.x + kHistThreads * k < p1) {
+#pragma unroll
+            for (int r = 0; r < kHistMaxRounds; ++r)
+                if (r < nr) atomicAdd(&hist[r * n_b + clamp_bucket(ids[k][r], n_b)], 1);
+        }
     __syncthreads();
     for (int i = threadIdx.x; i < nr * n_b; i += blockDim.x) {
         const int r = r0 + i / n_b, b = i % n_b;
-        counts[((bh * n_r + r) * n_b + b) * n_tiles + tile] = hist[i];
+        counts[((bh * n_r + r) * n_tiles + tile) * n_b + b] = hist[i];
     }
 }
 
-// Each thread owns a contiguous run of the segment's (bucket, tile) counts
-// and holds it in registers (16-byte loads, all in flight together), so the
-// scan costs one round trip to memory instead of one per count.
-constexpr int kScanPerThread = 64;  // counts per thread held in registers
+// Counts of a segment are [tile][bucket].  Each thread owns up to four
+// consecutive buckets and holds their counts for up to kScanTiles tiles in
+// registers (all loads in flight together), so the scan costs one round trip
+// to memory; the threads' sums are scanned in LDS, and every (bucket, tile)
+// count is replaced by its first output slot in (bucket, tile) order.
+constexpr int kScanTiles = 16;
+constexpr int kScanBuckets = 4;  // n_buckets <= 1024 over 256 threads
 
 __global__ __launch_bounds__(256) void sort_scan_kernel(int32_t* __restrict__ counts, int L,
                                                         int n_b, int n_tiles,
                                                         int32_t* __restrict__ bucket_start) {
     __shared__ int part[256];
     const int64_t seg = blockIdx.x;
-    const int64_t E = (int64_t)n_b * n_tiles;
-    int32_t* c = counts + seg * E;
+    int32_t* c = counts + seg * (int64_t)n_b * n_tiles;
     int32_t* bs = bucket_start + seg * (n_b + 1);
-    const int64_t per = (E + 255) / 256;
-    const int64_t lo = min(E, threadIdx.x * per), hi = min(E, lo + per);
-    int s = 0;
-    if (per <= kScanPerThread && (E & 3) == 0 && (per & 3) == 0) {
-        int v[kScanPerThread];
-#pragma unroll
-        for (int k = 0; k < kScanPerThread; k += 4) {
-            const int64_t e = lo + k;
-            int4 x = make_int4(0, 0, 0, 0);
-            if (k < per && e < hi) x = *reinterpret_cast<const int4*>(c + e);
-            v[k] = x.x;
-            v[k + 1] = x.y;
-            v[k + 2] = x.z;
-            v[k + 3] = x.w;
-        }
-#pragma unroll
-        for (int k = 0; k < kScanPerThread; ++k) s += v[k];
+    const int per = (n_b + 255) / 256;
+    const int b0 = min(n_b, (int)threadIdx.x * per), b1 = min(n_b, b0 + per);
+    auto scan_threads = [&](int s) {  // exclusive prefix of the threads' sums
         part[threadIdx.x] = s;
         __syncthreads();
         for (int o = 1; o < 256; o <<= 1) {
@@ -91,64 +110,59 @@ __global__ __launch_bounds__(256) void sort_scan_kernel(int32_t* __restrict__ co
             part[threadIdx.x] += x;
             __syncthreads();
         }
-        int run = part[threadIdx.x] - s;
-        // (bucket, tile) of element lo, stepped along the run: a bucket's
-        // start is the exclusive prefix at its tile 0
-        int bucket = (int)(lo / n_tiles), t = (int)(lo % n_tiles);
+        return part[threadIdx.x] - s;
+    };
+    if (n_tiles <= kScanTiles && per <= kScanBuckets) {
+        int v[kScanBuckets][kScanTiles];
+        int s = 0;
 #pragma unroll
-        for (int k = 0; k < kScanPerThread; k += 4) {
-            const int64_t e = lo + k;
-            if (k < per && e < hi) {
-                int4 x;
-                x.x = run;
-                x.y = run + v[k];
-                x.z = x.y + v[k + 1];
-                x.w = x.z + v[k + 2];
-                *reinterpret_cast<int4*>(c + e) = x;
+        for (int t = 0; t < kScanTiles; ++t)
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    if (t == 0) bs[bucket] = u == 0 ? x.x : (u == 1 ? x.y : (u == 2 ? x.z : x.w));
-                    if (++t == n_tiles) {
-                        t = 0;
-                        ++bucket;
+            for (int bi = 0; bi < kScanBuckets; ++bi) {
+                v[bi][t] = (t < n_tiles && b0 + bi < b1) ? c[(int64_t)t * n_b + b0 + bi] : 0;
+                s += v[bi][t];
+            }
+        int run = scan_threads(s);
+#pragma unroll
+        for (int bi = 0; bi < kScanBuckets; ++bi)
+            if (b0 + bi < b1) {
+                bs[b0 + bi] = run;
+#pragma unroll
+                for (int t = 0; t < kScanTiles; ++t)
+                    if (t < n_tiles) {
+                        c[(int64_t)t * n_b + b0 + bi] = run;
+                        run += v[bi][t];
                     }
-                }
-                run = x.w + v[k + 3];
             }
-        }
     } else {
-        for (int64_t e = lo; e < hi; ++e) s += c[e];
-        part[threadIdx.x] = s;
-        __syncthreads();
-        // Hillis-Steele inclusive scan over 256 partial sums.
-        for (int o = 1; o < 256; o <<= 1) {
-            const int x = (int)threadIdx.x >= o ? part[threadIdx.x - o] : 0;
-            __syncthreads();
-            part[threadIdx.x] += x;
-            __syncthreads();
-        }
-        int run = part[threadIdx.x] - s;
-        int bucket = (int)(lo / n_tiles), t = (int)(lo % n_tiles);
-        for (int64_t e = lo; e < hi; ++e) {
-            const int v = c[e];
-            c[e] = run;
-            if (t == 0) bs[bucket] = run;
-            if (++t == n_tiles) {
-                t = 0;
-                ++bucket;
+        int s = 0;
+        for (int b = b0; b < b1; ++b)
+            for (int t = 0; t < n_tiles; ++t) s += c[(int64_t)t * n_b + b];
+        int run = scan_threads(s);
+        for (int b = b0; b < b1; ++b) {
+            bs[b] = run;
+            for (int t = 0; t < n_tiles; ++t) {
+                const int x = c[(int64_t)t * n_b + b];
+                c[(int64_t)t * n_b + b] = run;
+                run += x;
             }
-            run += v;
         }
     }
     if (threadIdx.x == 0) bs[n_b] = L;
 }
 
+// LDS of the scatter: per-wave next slot of every bucket [kSortWaves][n_b],
+// and per wave a 64-bit mask of the lanes holding each bucket [kSortWaves][n_b][2].
+size_t scatter_lds_bytes(int n_b) { return (size_t)3 * kSortWaves * n_b * sizeof(int); }
+
 __global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __restrict__ buckets,
                                                            const int32_t* __restrict__ offsets,
-                                                           int L, int n_r, int n_b, int n_bits,
+                                                           int L, int n_r, int n_b,
                                                            int n_tiles, int32_t* __restrict__ perm,
                                                            int32_t* __restrict__ undo) {
-    extern __shared__ int base[];  // [kSortWaves][n_b]
+    extern __shared__ int smem[];
+    int* base = smem;                                                // [kSortWaves][n_b]
+    uint32_t* lanes = reinterpret_cast<uint32_t*>(smem + kSortWaves * n_b);  // [kSortWaves][n_b][2]
     // Workgroup b of the launch runs on XCD b % 8 (round-robin dispatch).
     // Each XCD is given a contiguous run of (segment, tile) items, so the
     // tiles of a segment write their scattered 4-byte slots into the same
@@ -163,8 +177,9 @@ __global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __rest
     const int r = (int)(seg % n_r);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int* wbase = base + wave * n_b;
+    uint32_t* wlanes = lanes + 2 * wave * n_b;
 
-    for (int i = threadIdx.x; i < kSortWaves * n_b; i += blockDim.x) base[i] = 0;
+    for (int i = threadIdx.x; i < 3 * kSortWaves * n_b; i += blockDim.x) smem[i] = 0;
     const int p0 = tile * kTile + wave * kPerWave;
     const int p1 = min(L, p0 + kPerWave);
     // this lane's ids, all loads in flight at once (kPerWave / 64 per lane);
@@ -187,7 +202,7 @@ __global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __rest
     // Per-wave starting slot of every bucket: the tile's offset plus the counts
     // of the earlier waves of this tile.
     for (int b = threadIdx.x; b < n_b; b += blockDim.x) {
-        int off = offsets[(seg * n_b + b) * n_tiles + tile];
+        int off = offsets[(seg * n_tiles + tile) * n_b + b];
         for (int w = 0; w < kSortWaves; ++w) {
             const int cnt = base[w * n_b + b];
             base[w * n_b + b] = off;
@@ -196,6 +211,11 @@ __global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __rest
     }
     __syncthreads();
 
+    // Rank of a position among the equal buckets of its 64-lane group: every
+    // lane sets its bit in its bucket's lane mask, reads the mask back (the
+    // wave's LDS operations run in order) and counts the lanes below it, so
+    // equal keys keep their position order; the mask is cleared for the next
+    // group by its lanes.
     int32_t* pseg = perm + seg * L;
     int32_t* useg = undo + seg * L;
     const uint64_t lt_mask = (1ull << lane) - 1ull;
@@ -204,20 +224,22 @@ __global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __rest
         const int pos = p0 + 64 * it + lane;
         const bool active = pos < p1;
         const int b = ids[it];
-        uint64_t peers = __ballot(active);
-        for (int bit = 0; bit < n_bits; ++bit) {
-            const bool set = (b >> bit) & 1;
-            const uint64_t m = __ballot(set && active);
-            peers &= set ? m : ~m;
-        }
+        uint32_t* m = wlanes + 2 * b;
+        if (active) atomicOr(m + (lane >> 5), 1u << (lane & 31));
+        __builtin_amdgcn_wave_barrier();
+        const uint2 pm = active ? *reinterpret_cast<const uint2*>(m) : make_uint2(0u, 0u);
+        const uint64_t peers = (uint64_t)pm.x | ((uint64_t)pm.y << 32);
         const int before = __popcll(peers & lt_mask);
-        const int start = wbase[b];
+        const int start = active ? wbase[b] : 0;
+        __builtin_amdgcn_wave_barrier();
         if (active) {
             const int slot = start + before;
             pseg[slot] = pos;
             useg[pos] = slot;
+            *reinterpret_cast<uint2*>(m) = make_uint2(0u, 0u);
             if ((peers >> lane) == 1ull) wbase[b] = start + __popcll(peers);
         }
+        __builtin_amdgcn_wave_barrier();
     }
 }
 
@@ -283,16 +305,14 @@ hipError_t launch_sort(int64_t BH, int L, int n_rounds, int n_buckets, const int
     int32_t* counts = static_cast<int32_t*>(workspace);
     const int rpg = std::max(1, std::min(n_rounds, kHistLdsInts / n_buckets));
     const int groups = (n_rounds + rpg - 1) / rpg;
-    int n_bits = 0;
-    while ((1 << n_bits) < n_buckets) ++n_bits;
 
     sort_hist_kernel<<<dim3(n_tiles, (unsigned)BH, groups), kHistThreads, rpg * n_buckets * sizeof(int), stream>>>(
         buckets, L, n_rounds, n_buckets, rpg, n_tiles, counts);
     sort_scan_kernel<<<(unsigned)(BH * n_rounds), 256, 0, stream>>>(counts, L, n_buckets, n_tiles,
                                                                     bucket_start);
-    sort_scatter_kernel<<<dim3(n_tiles, (unsigned)(BH * n_rounds)), 256,
-                          kSortWaves * n_buckets * sizeof(int), stream>>>(
-        buckets, counts, L, n_rounds, n_buckets, n_bits, n_tiles, perm, undo);
+    sort_scatter_kernel<<<dim3(n_tiles, (unsigned)(BH * n_rounds)), 256, scatter_lds_bytes(n_buckets),
+                          stream>>>(
+        buckets, counts, L, n_rounds, n_buckets, n_tiles, perm, undo);
     return hipGetLastError();
 }
 
