@@ -49,12 +49,13 @@
  *   log-partition is below -self_mask/2 as its own only target; both are
  *   exact in fp32 while self_mask > 2*scale*|q_i| + log(n_rounds) + 17 for
  *   every row (App. A sets the self mask to 1e5).
- * Supported on the GPU: d = 64, chunk = 64 (and chunk = 128, the length of the
- *   paper's usual configuration, Sec. 5, on the fp32 forward; entry points that
- *   do not use the chunk ignore it), chunks_after <= 1 and attend_across on the
- *   fp32 forward (the bf16 forward and the backward return LSH_ERR_UNSUPPORTED
- *   for them), r_per_head everywhere, 2 <= n_buckets <= 1024 (even),
- *   1 <= n_rounds <= 16, B*H*L*n_rounds < 2^31.  L need not be a multiple of
+ * Supported on the GPU: d = 64; on the forward (both dtypes) chunk = 64 or
+ *   128 (the length of the paper's usual configuration, Sec. 5) and
+ *   chunks_after <= 1; attend_across on the fp32 forward only; the backward
+ *   takes chunk = 64 without look-ahead or attend_across (LSH_ERR_UNSUPPORTED
+ *   otherwise; entry points that do not use the chunk ignore it);
+ *   r_per_head everywhere; 2 <= n_buckets <= 1024 (even), 1 <= n_rounds <= 16,
+ *   B*H*L*n_rounds < 2^31.  L need not be a multiple of
  *   the chunk: the last chunk then holds the L mod m remaining sorted slots
  *   (the paper is silent; read as padding with tokens that are no one's
  *   target).
