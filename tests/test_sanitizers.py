@@ -60,7 +60,7 @@ def test_oracle_under_sanitizers(tmp_path):
 
 def test_abi_validation_under_sanitizers(tmp_path):
     objs = [os.path.join(PKG, "_build", f + ".o")
-            for f in ("hash", "sort", "attn_fwd", "attn_bwd", "combine", "dense")]
+            for f in ("hash", "sort", "attn_fwd", "attn_bwd", "combine", "dense", "block")]
     if not all(os.path.exists(o) for o in objs):
         pytest.skip("kernel objects not built (run __graft_entry__.build())")
     hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
@@ -69,13 +69,16 @@ def test_abi_validation_under_sanitizers(tmp_path):
         pytest.skip("hipcc or the clang sanitizer runtime is missing")
     san = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
            "-Xarch_host", "-fno-sanitize-recover=undefined"]
-    api_o = str(tmp_path / "lsh_api_san.o")
-    subprocess.check_call([hipcc, "-O1", "-g", "-std=c++17", "-fPIC", "--offload-arch=gfx950", *san,
-                           "-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc"),
-                           "-c", os.path.join(PKG, "csrc", "lsh_api.cpp"), "-o", api_o])
+    api_objs = []
+    for src in ("lsh_api.cpp", "block_api.cpp"):
+        o = str(tmp_path / (src + ".san.o"))
+        subprocess.check_call([hipcc, "-O1", "-g", "-std=c++17", "-fPIC", "--offload-arch=gfx950", *san,
+                               "-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc"),
+                               "-c", os.path.join(PKG, "csrc", src), "-o", o])
+        api_objs.append(o)
     lib = str(tmp_path / "liblsh_san.so")
     subprocess.check_call([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *san, "-shared-libasan",
-                           api_o, *objs, "-o", lib])
+                           *api_objs, *objs, "-o", lib])
     res = _run(f"""
         import ctypes, os
         from paper_2001_04451_amd import lsh
@@ -107,6 +110,16 @@ def test_abi_validation_under_sanitizers(tmp_path):
         assert L.lsh_chunk_attn_bwd(ctypes.byref(c), 1, *args, n, None) == -1
         big = cfg(B=8, H=16, L=65536, n_buckets=1024, n_rounds=8)
         assert L.lsh_sort_permute_static(ctypes.byref(big), FAKE, FAKE, FAKE, FAKE, None) == -2
+        # the reversible block's validation
+        bc = lsh.BlockConfigC(cfg(), 256, 64, 1e-5)
+        for op in range(3):
+            assert L.lsh_block_workspace_bytes(ctypes.byref(bc), op) > 0
+        w = lsh.BlockWeightsC(*([FAKE.value] * 12))
+        assert L.lsh_rev_attention(ctypes.byref(bc), ctypes.byref(w), FAKE, None, FAKE, 1.0, FAKE, 16,
+                                   None) == -1
+        assert L.lsh_rev_feed_forward(ctypes.byref(lsh.BlockConfigC(cfg(), 100, 0, 1e-5)), ctypes.byref(w),
+                                      FAKE, None, FAKE, 1.0, FAKE, 1 << 40, None) == -2
+        assert L.lsh_linear_bf16(128, 100, 64, FAKE, FAKE, None, None, 1.0, FAKE, None, None) == -2
         for s in (0, -1, -2, -3, 5):
             L.lsh_status_string(s)
         print("ok")
