@@ -34,11 +34,14 @@
 //                When a key block's chunk leaves the window its owner adds
 //                dk through the normalisation Jacobian to dQ (the same 16
 //                tokens) and writes the round's partials of dq and dv, in
-//                position order, as fp16 rows scaled by 2^-e (e = 0 unless a
-//                row's largest magnitude reaches 2^15; one byte per row).
-//  * bwd_reduce: per position, the sum over rounds; plus dO for a token that
-//                was its own only target in every round (its weights are
-//                then 1/n_rounds on each round's self entry).
+//                sorted-slot order (whole contiguous rows; scattering them to
+//                position order here costs more than gathering them below),
+//                as fp16 rows scaled by 2^-e (e = 0 unless a row's largest
+//                magnitude reaches 2^15; one byte per row).
+//  * bwd_reduce: per position, the sum over rounds, each round's partial
+//                gathered through undo; plus dO for a token that was its own
+//                only target in every round (its weights are then 1/n_rounds
+//                on each round's self entry).
 // Every (query, key) pair of a round is computed once, by one lane, and every
 // sum has a fixed order: no atomics, and the results are deterministic.
 #include "attn_common.h"
@@ -74,7 +77,6 @@ struct BwdShared {
     char Ts[2 * kChunk * 128];       // dA'^T: 128 window keys x 64 queries (bf16)
     float X[kChunk * kXStride];      // dQ of the step's queries, [token][dim] (padded rows)
     uint32_t rec[kSlots * kChunk][BwdRec<NW>::RW];
-    int pos[kSlots * kChunk];        // position of each ring row
     // per wave, per query of the step (lane order): its key interval in window
     // rows, its log-partition (log2 units) and D, and its signature words
     int lo[8][kChunk], hi[8][kChunk];
@@ -140,7 +142,6 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
             const int pr = __shfl(pos_lane, rr);
             copy16_to_lds(rec + (rowbase + pr) * RW + 4 * (u % U), &S.rec[ring_row(cc, 0)][0] + 256 * wave);
         }
-        if (wave == 7) S.pos[ring_row(cc, lane)] = pos_lane;
     };
 
     stage(c0 - 1, chunk_pos(c0 - 1));
@@ -295,7 +296,6 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
                 const int tr = ring_row(k_chunk, t_i);
                 const float cf = __uint_as_float(S.rec[tr][RW - 3]);
                 const float inv = cf * (1.f / scale_log2e);  // 1/|q|, 0 for a zero row
-                const int pos = S.pos[tr];
                 f32x4 qv[4], xq[4];
                 float kd = 0.f;
 #pragma unroll
@@ -331,7 +331,7 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
                 const int ev = max(0, (int)((__float_as_uint(mv) >> 23) & 0xFFu) - 141);
                 const float sq = __uint_as_float((uint32_t)(127 - eq) << 23);
                 const float sv = __uint_as_float((uint32_t)(127 - ev) << 23);
-                const int64_t prow = seg * L + pos;
+                const int64_t prow = seg * L + slot;  // sorted order
                 uint16_t* dqrow = part_q + prow * kHeadDim;
                 uint16_t* dvrow = part_v + prow * kHeadDim;
 #pragma unroll
@@ -427,26 +427,34 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t* __restric
 }
 
 
-// dq, dv of a position: the sum of its per-round partials (position order,
-// fixed round order, each fp16 row times 2^e), plus dO for a token whose only
-// target in every round was itself.  NRL: n_r rounded up to a power of two;
-// rounds past n_r read round 0 with weight 0, so the loads are unconditional.
+// dq, dv of a position: the sum of its per-round partials (each at the
+// token's slot undo[i] of its round, fixed round order, each fp16 row times
+// 2^e), plus dO for a token whose only target in every round was itself.
+// NRL: n_r rounded up to a power of two; rounds past n_r read round 0 with
+// weight 0, so the loads are unconditional.
 template <int NRL>
 __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     const uint16_t* __restrict__ dout, const float* __restrict__ lse_total,
     const uint16_t* __restrict__ part_q, const uint16_t* __restrict__ part_v,
-    const uint8_t* __restrict__ part_e, int64_t rows, int L, int n_r, float self_mask,
-    float* __restrict__ dq, float* __restrict__ dv) {
+    const uint8_t* __restrict__ part_e, const int32_t* __restrict__ undo, int64_t rows, int L,
+    int n_r, float self_mask, float* __restrict__ dq, float* __restrict__ dv) {
     const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
     const int part = threadIdx.x & 15;
     if (row >= rows) return;  // whole 16-lane groups leave together
     const int64_t bh = row / L, i = row % L;
     const int64_t rr_total = rows * n_r;  // offset of the dv exponents
+    int64_t sbase[NRL];
+    int slot[NRL];
+#pragma unroll
+    for (int rr = 0; rr < NRL; ++rr) {
+        sbase[rr] = (bh * n_r + (rr < n_r ? rr : 0)) * L;
+        slot[rr] = min(max(undo[sbase[rr] + i], 0), L - 1);
+    }
     uint2 xq[NRL], xv[NRL];
     uint32_t eq[NRL], ev[NRL];
 #pragma unroll
     for (int rr = 0; rr < NRL; ++rr) {
-        const int64_t prow = (bh * n_r + (rr < n_r ? rr : 0)) * L + i;
+        const int64_t prow = sbase[rr] + slot[rr];
         xq[rr] = *reinterpret_cast<const uint2*>(part_q + prow * kHeadDim + part * 4);
         xv[rr] = *reinterpret_cast<const uint2*>(part_v + prow * kHeadDim + part * 4);
         eq[rr] = part_e[prow];
@@ -585,7 +593,7 @@ hipError_t launch_attn_bwd(int64_t BH, int L, int n_rounds, int n_buckets, bool 
     const unsigned row_grid = (unsigned)((rows * 16 + 255) / 256);
     auto reduce = [&](auto nrl) {
         bwd_reduce_kernel<decltype(nrl)::value><<<row_grid, 256, 0, stream>>>(
-            dout, lse_total, w.part_q, w.part_v, w.part_e, rows, L, n_rounds, self_mask, dq, dv);
+            dout, lse_total, w.part_q, w.part_v, w.part_e, undo, rows, L, n_rounds, self_mask, dq, dv);
     };
     if (n_rounds <= 1) reduce(std::integral_constant<int, 1>{});
     else if (n_rounds <= 2) reduce(std::integral_constant<int, 2>{});
