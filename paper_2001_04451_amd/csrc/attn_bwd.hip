@@ -308,8 +308,7 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
 #pragma unroll
                     for (int j = 0; j < 4; ++j) kd = fmaf(accK[bd][j], qv[bd][j], kd);
                 }
-                kd += __shfl_xor(kd, 16);
-                kd += __shfl_xor(kd, 32);
+                kd = sum_xor32(sum_xor16(kd));
                 const float proj = scale * kd * inv;  // dk . k
                 f32x4 a[4];
                 float mq = 0.f, mv = 0.f;
@@ -321,10 +320,8 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
                         mq = fmaxf(mq, fabsf(a[bd][j]));
                         mv = fmaxf(mv, fabsf(accV[bd][j]));
                     }
-                mq = fmaxf(mq, __shfl_xor(mq, 16));
-                mq = fmaxf(mq, __shfl_xor(mq, 32));
-                mv = fmaxf(mv, __shfl_xor(mv, 16));
-                mv = fmaxf(mv, __shfl_xor(mv, 32));
+                mq = max_xor32(max_xor16(mq));
+                mv = max_xor32(max_xor16(mv));
                 // 2^(E-127) <= max < 2^(E-126): e = max(0, E - 141) puts the
                 // scaled row below 2^15, inside fp16's range
                 const int eq = max(0, (int)((__float_as_uint(mq) >> 23) & 0xFFu) - 141);

@@ -376,8 +376,7 @@ __global__ __launch_bounds__((FwdGeom<M, AFTER>::kThreads), (FwdGeom<M, AFTER>::
                 float off = 0.f;
                 if constexpr (!FAST) {  // online maximum over the four lane groups of a query
                     float mt = fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3]));
-                    mt = fmaxf(mt, __shfl_xor(mt, 16));
-                    mt = fmaxf(mt, __shfl_xor(mt, 32));
+                    mt = max_xor32(max_xor16(mt));
                     const float m_new = fmaxf(m, mt);
                     off = m_new > -__builtin_inff() ? m_new : 0.f;
                     const float corr = __builtin_amdgcn_exp2f(m - off);
@@ -402,8 +401,7 @@ __global__ __launch_bounds__((FwdGeom<M, AFTER>::kThreads), (FwdGeom<M, AFTER>::
                 for (int b = 0; b < 4; ++b) oacc[b] = mfma16x16x16(vt_read(S.Vs + vofs[ch][b] + roff * 128), pk, oacc[b]);
                 oacc[4] = mfma16x16x16(kOnes4, pk, oacc[4]);
             }
-            lsum += __shfl_xor(lsum, 16);
-            lsum += __shfl_xor(lsum, 32);
+            lsum = sum_xor32(sum_xor16(lsum));
             const bool alone = !(lsum > 0.f);  // only itself left as a target
             if (__ballot(alone) != 0) {
                 // The output of a lone query is v_i: one more P V step on the
@@ -429,8 +427,7 @@ __global__ __launch_bounds__((FwdGeom<M, AFTER>::kThreads), (FwdGeom<M, AFTER>::
             for (int b = 0; b < 4; ++b)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) amax = fmaxf(amax, fabsf(oacc[b][e]));
-            amax = fmaxf(amax, __shfl_xor(amax, 16));
-            amax = fmaxf(amax, __shfl_xor(amax, 32));
+            amax = max_xor32(max_xor16(amax));
             amax *= inv;
             // 2^(E-127) <= amax < 2^(E-126): e = max(0, E - 141) puts the
             // scaled row below 2^15, inside fp16's range

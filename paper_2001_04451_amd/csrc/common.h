@@ -64,6 +64,52 @@ __device__ __forceinline__ f32x16 mfma32x32x16(f16x8 a, f16x8 b, f32x16 c) {
 
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63); }
 
+// Exchanges between the 16-lane rows of a wave with gfx950's row swaps:
+// VALU operations, without the LDS round trip of __shfl_xor.  pair16(x)
+// gives, in some order, x of lane l and of lane l ^ 16; pair32 likewise for
+// l ^ 32.  (permlane16_swap(a, b) trades the odd rows of a with the even
+// rows of b, permlane32_swap(a, b) the upper half of a with the lower half
+// of b; with a = b = x each lane ends up holding both values.)
+struct LanePair {
+    uint32_t a, b;
+};
+__device__ __forceinline__ LanePair pair16(uint32_t x) {
+    const auto p = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    return {p[0], p[1]};
+}
+__device__ __forceinline__ LanePair pair32(uint32_t x) {
+    const auto p = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    return {p[0], p[1]};
+}
+// x of lane l ^ 16 and of lane l ^ 32 (the partner's value is the first of
+// the pair in the upper row or half, the second in the lower).
+__device__ __forceinline__ uint32_t xor16(uint32_t x) {
+    const LanePair p = pair16(x);
+    return (threadIdx.x & 16) ? p.a : p.b;
+}
+__device__ __forceinline__ uint32_t xor32(uint32_t x) {
+    const LanePair p = pair32(x);
+    return (threadIdx.x & 32) ? p.a : p.b;
+}
+// x[l] + x[l ^ 16] and x[l] + x[l ^ 32] (the same value in both lanes of a
+// pair, as the additions commute); likewise the maxima.
+__device__ __forceinline__ float sum_xor16(float x) {
+    const LanePair p = pair16(__float_as_uint(x));
+    return __uint_as_float(p.a) + __uint_as_float(p.b);
+}
+__device__ __forceinline__ float sum_xor32(float x) {
+    const LanePair p = pair32(__float_as_uint(x));
+    return __uint_as_float(p.a) + __uint_as_float(p.b);
+}
+__device__ __forceinline__ float max_xor16(float x) {
+    const LanePair p = pair16(__float_as_uint(x));
+    return fmaxf(__uint_as_float(p.a), __uint_as_float(p.b));
+}
+__device__ __forceinline__ float max_xor32(float x) {
+    const LanePair p = pair32(__float_as_uint(x));
+    return fmaxf(__uint_as_float(p.a), __uint_as_float(p.b));
+}
+
 __device__ __forceinline__ float wave_max(float x) {
     for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
     return x;

@@ -803,7 +803,7 @@ __global__ __launch_bounds__(WAVES * 64, (MODE == kScreen ? kScreenOcc : 1)) voi
                     mx = fmaxf(mx, fmaxf(fabsf(__uint_as_float(raw[s4][e] << 16)),
                                          fabsf(__uint_as_float(raw[s4][e] & 0xFFFF0000u))));
             }
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            mx = max_xor32(mx);
             int k = 0;
             (void)frexpf(mx, &k);
             const int sq = (mx > 0.f && mx <= 3.4e38f) ? 14 - (k - 1) : 0;
@@ -825,7 +825,7 @@ __global__ __launch_bounds__(WAVES * 64, (MODE == kScreen ? kScreenOcc : 1)) voi
                 qm[rb][s4] = u32x4{0, 0, 0, 0};
             }
         }
-        ss += __shfl_xor(ss, 32);
+        ss = sum_xor32(ss);
         qn[rb] = sqrtf(ss);
     }
     __builtin_amdgcn_s_waitcnt(0);
@@ -887,8 +887,8 @@ __global__ __launch_bounds__(WAVES * 64, (MODE == kScreen ? kScreenOcc : 1)) voi
 #pragma unroll
             for (int rb = 0; rb < kRB; ++rb) {
                 const uint32_t bb = best[rb], ss2 = second[rb];
-                const uint32_t bp = __shfl_xor(bb, 32), sp = __shfl_xor(ss2, 32);
-                const int tp = __shfl_xor(best_grp[rb], 32);
+                const uint32_t bp = xor32(bb), sp = xor32(ss2);
+                const int tp = (int)xor32((uint32_t)best_grp[rb]);
                 const bool mine = bb > bp || (bb == bp && h == 0);
                 bk[rb] = mine ? bb : bp;
                 sk[rb] = max(min(bb, bp), max(ss2, sp));
@@ -937,7 +937,7 @@ __global__ __launch_bounds__(WAVES * 64, (MODE == kScreen ? kScreenOcc : 1)) voi
 #pragma unroll
                 for (int rb = 0; rb < kRB; ++rb) {
                     const float half_x = dot_planes(qa[rb], hv[rb]) + dot_planes(qa[rb], mv[rb]);
-                    const float x = half_x + __shfl_xor(half_x, 32);
+                    const float x = sum_xor32(half_x);
                     const float s1 = key_magnitude<F32>(sk[rb]);
                     const float eps = 1.02f * qn[rb] * (res + err_acc * cn);
                     const float eps2 = 1.02f * qn[rb] * (res_max2[r] + err_acc2 * cn);
