@@ -47,29 +47,45 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o
 
     // this lane's rounds: part and part + 8
     int u[RPL];
-    float zr[RPL];
-    uint32_t ex[RPL];
     bool live[RPL];
 #pragma unroll
     for (int k = 0; k < RPL; ++k) {
         const int r = part + 8 * k;
         live[k] = r < n_r;
-        const int rc = min(r, n_r - 1);
-        u[k] = min(max(undo[(seg0 + rc) * L + i], 0), L - 1);
-        zr[k] = lse_rounds[(seg0 + rc) * L + u[k]];
-        ex[k] = F32 ? 0u : min((uint32_t)o_exp[(seg0 + rc) * L + u[k]], 126u);
+        u[k] = min(max(undo[(seg0 + min(r, n_r - 1)) * L + i], 0), L - 1);
+    }
+    // every round's slot in every lane of the group (rounds n_r .. NRL-1
+    // read round n_r - 1's row, with weight 0 below); the rows' loads are
+    // issued here, alongside the log-partitions', not after the weights
+    constexpr int NR = NRL;
+    int64_t sl[NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) sl[r] = (seg0 + min(r, n_r - 1)) * L + __shfl(u[r >> 3], group0 + (r & 7));
+    constexpr int kPieces = F32 ? 2 : 1;  // 16-byte pieces of a lane's 8 values
+    u32x4 o[NR][kPieces];
+#pragma unroll
+    for (int r = 0; r < NR; ++r)
+#pragma unroll
+        for (int pc = 0; pc < kPieces; ++pc)
+            o[r][pc] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(
+                static_cast<const char*>(o_rounds) + (sl[r] * kHeadDim + part * 8) * (F32 ? 4 : 2) + 16 * pc));
+    float zr[RPL];
+    uint32_t ex[RPL];
+#pragma unroll
+    for (int k = 0; k < RPL; ++k) {
+        const int64_t at = (seg0 + min(part + 8 * k, n_r - 1)) * L + u[k];
+        zr[k] = lse_rounds[at];
+        ex[k] = F32 ? 0u : min((uint32_t)o_exp[at], 126u);
     }
     float zmax = -__builtin_inff();
 #pragma unroll
     for (int k = 0; k < RPL; ++k)
         if (live[k]) zmax = fmaxf(zmax, zr[k]);
-#pragma unroll
-    for (int o = 1; o < 8; o <<= 1) zmax = fmaxf(zmax, __shfl_xor(zmax, o));
+    zmax = group8_max(zmax);
     float sum = 0.f;
 #pragma unroll
     for (int k = 0; k < RPL; ++k) sum += live[k] ? expf(zr[k] - zmax) : 0.f;
-#pragma unroll
-    for (int o = 1; o < 8; o <<= 1) sum += __shfl_xor(sum, o);
+    sum = group8_sum(sum);
     const float z = zmax + logf(sum);
     // weights relative to the largest round, not to z: a token alone in its
     // buckets has z_r near -self_mask, where one fp32 spacing of z is 2^-7,
@@ -79,48 +95,26 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o
 #pragma unroll
     for (int k = 0; k < RPL; ++k)  // times 2^e, the scale of the stored row
         wk[k] = live[k] ? expf(zr[k] - zmax) * inv_sum * __uint_as_float((127u + ex[k]) << 23) : 0.f;
-
-    // every round's slot and weight in every lane of the group (rounds
-    // n_r .. NRL-1 read round n_r - 1's row with weight 0)
-    constexpr int NR = NRL;
-    int64_t sl[NR];
     float w[NR];
 #pragma unroll
-    for (int r = 0; r < NR; ++r) {
-        const int src_lane = group0 + (r & 7);
-        const int k = r >> 3;
-        sl[r] = (seg0 + min(r, n_r - 1)) * L + __shfl(u[k], src_lane);
-        w[r] = __shfl(wk[k], src_lane);
-    }
+    for (int r = 0; r < NR; ++r) w[r] = __shfl(wk[r >> 3], group0 + (r & 7));
 
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if constexpr (F32) {
-        const float* src = static_cast<const float*>(o_rounds);
-        f32x4 o[NR][2];
-#pragma unroll
-        for (int r = 0; r < NR; ++r) {
-            o[r][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src + sl[r] * kHeadDim + part * 8));
-            o[r][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src + sl[r] * kHeadDim + part * 8 + 4));
-        }
 #pragma unroll
         for (int r = 0; r < NR; ++r)
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[e] = fmaf(w[r], o[r][e >> 2][e & 3], acc[e]);
+            for (int e = 0; e < 8; ++e) acc[e] = fmaf(w[r], __uint_as_float(o[r][e >> 2][e & 3]), acc[e]);
         float* dst = static_cast<float*>(out) + row * kHeadDim + part * 8;
         *reinterpret_cast<f32x4*>(dst) = f32x4{acc[0], acc[1], acc[2], acc[3]};
         *reinterpret_cast<f32x4*>(dst + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
     } else {
-        const uint16_t* src = static_cast<const uint16_t*>(o_rounds);
-        u32x4 o[NR];
-#pragma unroll
-        for (int r = 0; r < NR; ++r)
-            o[r] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + sl[r] * kHeadDim + part * 8));
 #pragma unroll
         for (int r = 0; r < NR; ++r)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                acc[2 * e] = fmaf(w[r], f16_bits_to_f32(o[r][e] & 0xFFFFu), acc[2 * e]);
-                acc[2 * e + 1] = fmaf(w[r], f16_bits_to_f32(o[r][e] >> 16), acc[2 * e + 1]);
+                acc[2 * e] = fmaf(w[r], f16_bits_to_f32(o[r][0][e] & 0xFFFFu), acc[2 * e]);
+                acc[2 * e + 1] = fmaf(w[r], f16_bits_to_f32(o[r][0][e] >> 16), acc[2 * e + 1]);
             }
         u32x4 packed;
 #pragma unroll

@@ -110,6 +110,29 @@ __device__ __forceinline__ float max_xor32(float x) {
     return fmaxf(__uint_as_float(p.a), __uint_as_float(p.b));
 }
 
+// Sum / max over each aligned group of eight lanes with DPP moves (no LDS
+// round trip): lanes i ^ 1, then i ^ 2 (quad permutes), then the mirrored
+// lane 7 - i of the group, which after the first two steps holds the same
+// value as lane i ^ 4.  Every lane of a group ends with the same value, the
+// one the xor butterfly gives.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141; // lane 7 - i within each group of eight
+__device__ __forceinline__ float group8_sum(float x) {
+    x += dpp_f32<kDppXor1>(x);
+    x += dpp_f32<kDppXor2>(x);
+    return x + dpp_f32<kDppHalfMirror>(x);
+}
+__device__ __forceinline__ float group8_max(float x) {
+    x = fmaxf(x, dpp_f32<kDppXor1>(x));
+    x = fmaxf(x, dpp_f32<kDppXor2>(x));
+    return fmaxf(x, dpp_f32<kDppHalfMirror>(x));
+}
+
 __device__ __forceinline__ float wave_max(float x) {
     for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
     return x;
