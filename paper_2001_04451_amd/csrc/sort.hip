@@ -11,8 +11,9 @@
 //               bucket start offsets.
 //   3. scatter: each wave ranks its quarter of a tile in position order; the
 //               rank of a position among equal buckets of its 64-lane group
-//               comes from a per-bucket lane mask in LDS (peers + popcount),
-//               so equal keys keep their position order (stable).
+//               is the count of lower lanes with the same bucket, whose lane
+//               mask comes from one ballot per bucket-id bit, so equal keys
+//               keep their position order (stable).
 #include "common.h"
 #include "launch.h"
 
@@ -151,9 +152,8 @@ __global__ __launch_bounds__(256) void sort_scan_kernel(int32_t* __restrict__ co
     if (threadIdx.x == 0) bs[n_b] = L;
 }
 
-// LDS of the scatter: per-wave next slot of every bucket [kSortWaves][n_b],
-// and per wave a 64-bit mask of the lanes holding each bucket [kSortWaves][n_b][2].
-size_t scatter_lds_bytes(int n_b) { return (size_t)3 * kSortWaves * n_b * sizeof(int); }
+// LDS of the scatter: per-wave next slot of every bucket [kSortWaves][n_b].
+size_t scatter_lds_bytes(int n_b) { return (size_t)kSortWaves * n_b * sizeof(int); }
 
 __global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __restrict__ buckets,
                                                            const int32_t* __restrict__ offsets,
@@ -161,8 +161,7 @@ __global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __rest
                                                            int n_tiles, int32_t* __restrict__ perm,
                                                            int32_t* __restrict__ undo) {
     extern __shared__ int smem[];
-    int* base = smem;                                                // [kSortWaves][n_b]
-    uint32_t* lanes = reinterpret_cast<uint32_t*>(smem + kSortWaves * n_b);  // [kSortWaves][n_b][2]
+    int* base = smem;  // [kSortWaves][n_b]
     // Workgroup b of the launch runs on XCD b % 8 (round-robin dispatch).
     // Each XCD is given a contiguous run of (segment, tile) items, so the
     // tiles of a segment write their scattered 4-byte slots into the same
@@ -177,9 +176,8 @@ __global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __rest
     const int r = (int)(seg % n_r);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int* wbase = base + wave * n_b;
-    uint32_t* wlanes = lanes + 2 * wave * n_b;
 
-    for (int i = threadIdx.x; i < 3 * kSortWaves * n_b; i += blockDim.x) smem[i] = 0;
+    for (int i = threadIdx.x; i < kSortWaves * n_b; i += blockDim.x) smem[i] = 0;
     const int p0 = tile * kTile + wave * kPerWave;
     const int p1 = min(L, p0 + kPerWave);
     // this lane's ids, all loads in flight at once (kPerWave / 64 per lane);
@@ -211,35 +209,35 @@ __global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __rest
     }
     __syncthreads();
 
-    // Rank of a position among the equal buckets of its 64-lane group: every
-    // lane sets its bit in its bucket's lane mask, reads the mask back (the
-    // wave's LDS operations run in order) and counts the lanes below it, so
-    // equal keys keep their position order; the mask is cleared for the next
-    // group by its lanes.
+    // Rank of a position among the equal buckets of its 64-lane group: the
+    // lanes holding the same bucket are the AND over the id's bits of the
+    // ballot of lanes agreeing on that bit (ids are below n_b <= 1024), and
+    // the rank counts those below the lane, so equal keys keep their
+    // position order.  The highest lane of each bucket moves the bucket's
+    // next slot on (the wave's LDS operations run in order).
     int32_t* pseg = perm + seg * L;
     int32_t* useg = undo + seg * L;
-    const uint64_t lt_mask = (1ull << lane) - 1ull;
+    const int id_bits = 32 - __clz(max(n_b - 1, 1));
 #pragma unroll
     for (int it = 0; it < kIter; ++it) {
         const int pos = p0 + 64 * it + lane;
         const bool active = pos < p1;
         const int b = ids[it];
-        uint32_t* m = wlanes + 2 * b;
-        if (active) atomicOr(m + (lane >> 5), 1u << (lane & 31));
-        __builtin_amdgcn_wave_barrier();
-        const uint2 pm = active ? *reinterpret_cast<const uint2*>(m) : make_uint2(0u, 0u);
-        const uint64_t peers = (uint64_t)pm.x | ((uint64_t)pm.y << 32);
-        const int before = __popcll(peers & lt_mask);
-        const int start = active ? wbase[b] : 0;
-        __builtin_amdgcn_wave_barrier();
+        const int start = wbase[b];
+        uint64_t peers = __ballot(active);
+        for (int bit = 0; bit < id_bits; ++bit) {
+            const bool one = (b >> bit) & 1;
+            const uint64_t ones = __ballot(one);
+            peers &= one ? ones : ~ones;
+        }
+        const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(peers >> 32),
+                                                     __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u));
         if (active) {
             const int slot = start + before;
             pseg[slot] = pos;
             useg[pos] = slot;
-            *reinterpret_cast<uint2*>(m) = make_uint2(0u, 0u);
             if ((peers >> lane) == 1ull) wbase[b] = start + __popcll(peers);
         }
-        __builtin_amdgcn_wave_barrier();
     }
 }
 
