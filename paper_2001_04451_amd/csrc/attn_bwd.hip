@@ -17,10 +17,13 @@
 //                against the 128 keys of chunks c-1 and c (their whole
 //                window), so every (query, key) pair of the round is met in
 //                exactly one step, and the keys of chunk c meet their last
-//                queries in step c+1.  The rows of chunks c-1 and c sit in
-//                LDS rings (q and v: three slots, dO: two), and chunk c+1 is
+//                queries in step c+1.  The rows sit in LDS rings (q rows and
+//                records: four slots, v: three, dO: two), and chunk c+1 is
 //                gathered into the free slots (through perm, straight from
-//                global memory into LDS) while step c computes.
+//                global memory into LDS) while step c computes.  A step runs
+//                the finishing of chunk c-2's key blocks, pass 2 of step c-1
+//                and pass 1 of step c, with dA'^T and dQ double-buffered, so
+//                it needs a single barrier.
 //                Pass 1, lanes on keys: each wave owns one 16-key block of
 //                one chunk for the two steps in which that chunk is in the
 //                window.  Per 16x16 tile S = Q K^T and dP = dO V^T on the
@@ -31,9 +34,9 @@
 //                Pass 2, lanes on queries: dQ^T += K^T dA'^T over the window,
 //                with dA'^T read back through the LDS transpose read; dQ goes
 //                to LDS for the step that finishes those tokens as keys.
-//                When a key block's chunk leaves the window its owner adds
-//                dk through the normalisation Jacobian to dQ (the same 16
-//                tokens) and writes the round's partials of dq and dv, in
+//                The step after a key block's chunk leaves the window, its
+//                owner adds dk through the normalisation Jacobian to dQ (the
+//                same 16 tokens) and writes the round's partials of dq and dv, in
 //                sorted-slot order (whole contiguous rows; scattering them to
 //                position order here costs more than gathering them below),
 //                as fp16 rows scaled by 2^-e (e = 0 unless a row's largest
@@ -54,36 +57,41 @@ namespace {
 
 constexpr int kMaskedIndex = 32;  // table index of a masked-out pair
 constexpr int kBwdThreads = 512;  // eight waves
-constexpr int kXStride = kHeadDim + 4;  // X row stride: rows of 16-lane accesses in different banks
 
 // Per-token record: signature words [0, SW), then the key scale, the total
 // log-partition in log2 units and D, in the last three words.
 template <int NW>
 struct BwdRec {
     static constexpr int SW = sig_stride(NW);
-    static constexpr int RW = SW + 3 <= 4 ? 4 : (SW + 3 <= 8 ? 8 : 16);
+    static constexpr int RW = SW + 3 <= 4 ? 4 : (SW + 3 <= 8 ? 8 : 12);
 };
 
-// LDS of one workgroup.  DEPTH: how many chunks ahead the gather runs (the
-// q, v and record rings hold chunks c-1 .. c+DEPTH, the dO ring c .. c+DEPTH);
-// the step loop waits for all of a step's copies, so it is written for 1.
-template <int NW, int DEPTH>
+// LDS of one workgroup.  Step c reads the q rows and records of chunks
+// c-2 .. c (the finishing of chunk c-2, the dQ of chunk c-1, the pairs of
+// step c) and gathers chunk c+1: a four-slot ring; v rows are read for
+// chunks c-1 and c (three slots), dO rows for chunk c (two slots).  dA'^T
+// and dQ are double-buffered by the parity of their chunk, so that a step
+// needs one barrier.  The per-wave copies of each query's interval,
+// log-partition, D and signature words let every wave read its four queries'
+// fields as 16-byte runs without a second barrier; beyond four signature
+// words (more than eight rounds) they are read from the records instead, to
+// stay within 160 KB.
+template <int NW>
 struct BwdShared {
-    static_assert(DEPTH == 1, "the step loop waits for the copies of one chunk ahead");
-    static constexpr int kSlots = DEPTH + 2, kDSlots = DEPTH + 1;
-    char Qs[kSlots * kChunk * 128];  // q rows (swizzled)
-    char Vs[kSlots * kChunk * 128];  // v rows, same ring
-    char Ds[kDSlots * kChunk * 128]; // dO rows
-    char Ts[2 * kChunk * 128];       // dA'^T: 128 window keys x 64 queries (bf16)
-    float X[kChunk * kXStride];      // dQ of the step's queries, [token][dim] (padded rows)
-    uint32_t rec[kSlots * kChunk][BwdRec<NW>::RW];
-    // per wave, per query of the step (lane order): its key interval in window
-    // rows, its log-partition (log2 units) and D, and its signature words
-    int lo[8][kChunk], hi[8][kChunk];
+    static constexpr int kQSlots = 4, kVSlots = 3, kDSlots = 2;
+    static constexpr int kQsigWords = NW >= 1 && NW <= 4 ? NW : 1;
+    char Qs[kQSlots * kChunk * 128];  // q rows (swizzled)
+    char Vs[kVSlots * kChunk * 128];  // v rows
+    char Ds[kDSlots * kChunk * 128];  // dO rows
+    char Ts[2][2 * kChunk * 128];     // dA'^T: 128 window keys x 64 queries (bf16), by step parity
+    float X[2][kChunk * kHeadDim];    // dQ of a chunk's tokens, [token][dim] (see xoff), by chunk parity
+    uint32_t rec[kQSlots * kChunk][BwdRec<NW>::RW];
+    uint32_t lohi[8][kChunk];         // lo | hi << 16 (both in 0 .. 127)
     float2 zd[8][kChunk];
-    uint32_t qsig[8][NW > 0 ? NW : 1][kChunk];
-    float tab[kMaskedIndex + 1];     // -log2 N by mismatch count; -inf = masked
+    uint32_t qsig[8][kQsigWords][kChunk];
+    float tab[kMaskedIndex + 1];      // -log2 N by mismatch count; -inf = masked
 };
+static_assert(sizeof(BwdShared<4>) <= 160 * 1024 && sizeof(BwdShared<8>) <= 160 * 1024, "LDS");
 
 // Row i of chunk `chunk` in a ring of SLOTS chunk slots.
 template <int SLOTS>
@@ -91,17 +99,24 @@ __device__ __forceinline__ int slot_row(int chunk, int i) {
     return ((chunk % SLOTS + SLOTS) % SLOTS) * kChunk + i;
 }
 
-template <int NW, bool CAUSAL, int DEPTH>
+// Float offset of dims 4cb .. 4cb+3 of token t in a dQ buffer: rows of 64
+// floats, their 16-byte groups xor-swizzled by the row so that the 16 tokens
+// a lane group touches fall in different banks.
+__device__ __forceinline__ int xoff(int t, int cb) { return t * kHeadDim + ((cb ^ (t & 7)) << 2); }
+
+template <int NW, bool CAUSAL>
 __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const uint32_t* __restrict__ rec,
     const int32_t* __restrict__ perm, uint16_t* __restrict__ part_q, uint16_t* __restrict__ part_v,
     uint8_t* __restrict__ part_e, int L, int n_r, float scale, int chunks_per_strip) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
-    using Shared = BwdShared<NW, DEPTH>;
+    using Shared = BwdShared<NW>;
     Shared& S = *reinterpret_cast<Shared*>(smem);
     constexpr int SW = BwdRec<NW>::SW, RW = BwdRec<NW>::RW;
-    auto ring_row = [](int chunk, int i) { return slot_row<Shared::kSlots>(chunk, i); };
+    constexpr bool kWaveSig = NW >= 1 && NW <= 4;  // per-wave signature copies
+    auto ring_row = [](int chunk, int i) { return slot_row<Shared::kQSlots>(chunk, i); };
+    auto ringv_row = [](int chunk, int i) { return slot_row<Shared::kVSlots>(chunk, i); };
     auto ring2_row = [](int chunk, int i) { return slot_row<Shared::kDSlots>(chunk, i); };
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -126,15 +141,14 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
     };
     // Gather chunk cc into its ring slots: wave w copies q, v and dO rows
     // 8w .. 8w+7 (each lane the 16-byte piece that belongs at its LDS slot);
-    // the records go through the first RW/4 waves, the positions through the
-    // last.
+    // the records go through the first RW/4 waves.
     auto stage = [&](int cc, int pos_raw) {
         const int pos_lane = min(max(pos_raw, 0), L - 1);
         const int row = 8 * wave + (lane >> 3);
         const int p = __shfl(pos_lane, row);
         const int64_t off = (rowbase + p) * kHeadDim + swz(row, lane & 7) * 8;
         copy16_to_lds(q + off, S.Qs + ring_row(cc, 8 * wave) * 128);
-        copy16_to_lds(v + off, S.Vs + ring_row(cc, 8 * wave) * 128);
+        copy16_to_lds(v + off, S.Vs + ringv_row(cc, 8 * wave) * 128);
         copy16_to_lds(dout + off, S.Ds + ring2_row(cc, 8 * wave) * 128);
         constexpr int U = RW / 4;  // 16-byte units per record
         if (wave < U) {
@@ -146,156 +160,37 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
 
     stage(c0 - 1, chunk_pos(c0 - 1));
     stage(c0, chunk_pos(c0));
-    int pf_pos = chunk_pos(c0 + DEPTH);
+    int pf_pos = chunk_pos(c0 + 1);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
     // This wave's key block: block b of every chunk of parity cp, held for
-    // the two steps in which the chunk is in the window.
+    // the two steps in which the chunk is in the window and finished at the
+    // start of the step after (when its tokens' dQ is complete).
     const int b = wave & 3, cp = wave >> 2;
     f32x4 accK[4] = {f32x4{}, f32x4{}, f32x4{}, f32x4{}};  // dK^T by 16-dim blocks
     f32x4 accV[4] = {f32x4{}, f32x4{}, f32x4{}, f32x4{}};  // dV^T
+    // the key intervals of this lane's query in the previous step (for its dQ)
+    int prev_lo = 1, prev_hi = 0;
 
-    for (int c = c0; c <= c1; ++c) {
-        if (c + DEPTH <= c1) stage(c + DEPTH, pf_pos);
-        const int pf_next = chunk_pos(c + DEPTH + 1);
+    // Step c: (A) the waves of chunk c's parity finish their key block of
+    // chunk c-2; (B) dQ of chunk c-1's queries from the dA'^T of step c-1;
+    // (C) the pairs of chunk c's queries with the keys of chunks c-1 and c.
+    for (int c = c0; c <= c1 + 1; ++c) {
+        if (c + 1 <= c1) stage(c + 1, pf_pos);
+        const int pf_next = chunk_pos(c + 2);
 
-        // ---- each query's key interval [lo, hi] in window rows (0..63:
-        // chunk c-1, 64..127: chunk c), from the bucket boundaries of the
-        // window: lane = query of chunk c ----
-        int lo_q, hi_q;
-        {
-            const uint32_t kA = sig_round_id(&S.rec[ring_row(c - 1, lane)][0], r);
-            const uint32_t kB = sig_round_id(&S.rec[ring_row(c, lane)][0], r);
-            const uint32_t prevA = __shfl_up(kA, 1);
-            const uint32_t lastA = __shfl(kA, 63);
-            const uint32_t prevB0 = __shfl_up(kB, 1);
-            const uint32_t prevB = lane == 0 ? lastA : prevB0;
-            const uint64_t bA = __ballot(lane == 0 || kA != prevA);
-            const uint64_t bB = __ballot(kB != prevB);
-            const uint64_t upto = bB & (~0ull >> (63 - lane));
-            const int lo_w = upto ? 127 - __clzll(upto) : 63 - __clzll(bA);
-            lo_q = max(lo_w, (1 - c) * kChunk);  // no slot before 0
-            if constexpr (CAUSAL) {
-                hi_q = kChunk + lane - 1;
-            } else {
-                const uint64_t after = lane < 63 ? bB & (~0ull << (lane + 1)) : 0ull;
-                hi_q = after ? 62 + __ffsll((long long)after) : 127;
-            }
-            hi_q = min(hi_q, L - 1 - (c - 1) * kChunk);  // no slot past the sequence
-            if (c * kChunk + lane >= L) {                // no query here
-                lo_q = 1;
-                hi_q = 0;
-            }
-            S.lo[wave][lane] = lo_q;
-            S.hi[wave][lane] = hi_q;
-            const uint32_t* qrec = &S.rec[ring_row(c, lane)][0];
-            S.zd[wave][lane] = make_float2(__uint_as_float(qrec[RW - 2]), __uint_as_float(qrec[RW - 1]));
-            if constexpr (NW > 0) {
-#pragma unroll
-                for (int w = 0; w < NW; ++w) S.qsig[wave][w][lane] = qrec[w];
-            }
-        }
-        // queries with a key in window block kw (one bit per query)
-        auto block_queries = [&](int kw) -> uint64_t {
-            return __ballot(lo_q <= hi_q && lo_q <= 16 * kw + 15 && hi_q >= 16 * kw);
-        };
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-        // ---- pass 1: this wave's key block against the 64 queries ----
-        const int k_chunk = (c & 1) == cp ? c : c - 1;  // the chunk of this wave's parity
-        const int kw = (k_chunk == c ? 4 : 0) + b;      // its window block
-        if (!(k_chunk == c && c == c1)) {               // chunk c1 belongs to the next strip
-            const uint64_t qmask = block_queries(kw);    // queries that reach this key block
-            const int krow = ring_row(k_chunk, 16 * b + n);
-            const int key_w = 16 * kw + n;
-            const uint32_t* krec = &S.rec[krow][0];
-            const float cf_k = __uint_as_float(krec[RW - 3]);
-            uint32_t ks[NW > 0 ? NW : 1];
-#pragma unroll
-            for (int w = 0; w < (NW > 0 ? NW : 1); ++w) ks[w] = krec[w];
-            const bf16x8 bk0 = as_bf16x8(lds_piece(S.Qs, krow, g));
-            const bf16x8 bk1 = as_bf16x8(lds_piece(S.Qs, krow, 4 + g));
-            const bf16x8 bv0 = as_bf16x8(lds_piece(S.Vs, krow, g));
-            const bf16x8 bv1 = as_bf16x8(lds_piece(S.Vs, krow, 4 + g));
-#pragma unroll
-            for (int qb = 0; qb < 4; ++qb) {
-                if (((qmask >> (16 * qb)) & 0xFFFFull) == 0) continue;
-                const int qrow = ring_row(c, 16 * qb + n);
-                const int drow = ring2_row(c, 16 * qb + n);
-                f32x4 sacc = mfma16x16x32(as_bf16x8(lds_piece(S.Qs, qrow, g)), bk0, f32x4{});
-                sacc = mfma16x16x32(as_bf16x8(lds_piece(S.Qs, qrow, 4 + g)), bk1, sacc);
-                f32x4 dpacc = mfma16x16x32(as_bf16x8(lds_piece(S.Ds, drow, g)), bv0, f32x4{});
-                dpacc = mfma16x16x32(as_bf16x8(lds_piece(S.Ds, drow, 4 + g)), bv1, dpacc);
-                // lane holds queries 16qb + 4g + j (j = 0..3) against key n
-                // the lane's four queries: intervals, log-partitions, D and
-                // signature words, one 16-byte read per field (lane groups
-                // read consecutive runs, so these reads do not conflict)
-                const int q0 = 16 * qb + 4 * g;
-                const int4 lo4 = *reinterpret_cast<const int4*>(&S.lo[wave][q0]);
-                const int4 hi4 = *reinterpret_cast<const int4*>(&S.hi[wave][q0]);
-                const f32x4 zd01 = *reinterpret_cast<const f32x4*>(&S.zd[wave][q0]);
-                const f32x4 zd23 = *reinterpret_cast<const f32x4*>(&S.zd[wave][q0 + 2]);
-                u32x4 qs4[NW > 0 ? NW : 1];
-                if constexpr (NW > 0) {
-#pragma unroll
-                    for (int w = 0; w < NW; ++w) qs4[w] = *reinterpret_cast<const u32x4*>(&S.qsig[wave][w][q0]);
-                }
-                const int lo_a[4] = {lo4.x, lo4.y, lo4.z, lo4.w};
-                const int hi_a[4] = {hi4.x, hi4.y, hi4.z, hi4.w};
-                const float z2_a[4] = {zd01[0], zd01[2], zd23[0], zd23[2]};
-                const float D_a[4] = {zd01[1], zd01[3], zd23[1], zd23[3]};
-                float p[4], da[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    bool valid = lo_a[j] <= key_w && key_w <= hi_a[j];
-                    if constexpr (!CAUSAL) valid = valid && key_w != kChunk + q0 + j;
-                    uint32_t t = valid ? 0u : ~0u;
-                    if constexpr (NW > 0) {
-#pragma unroll
-                        for (int w = 0; w < NW; ++w) t = and_or((qs4[w][j] ^ ks[w]) + sig_add(w), sig_guard(w), t);
-                    }
-                    p[j] = __builtin_amdgcn_exp2f(fmaf(sacc[j], cf_k, S.tab[__popc(t)] - z2_a[j]));
-                    da[j] = p[j] * (dpacc[j] - D_a[j]);
-                }
-                // P as bf16 hi + lo planes, dA and dA' = dA * scale*log2(e)/|q_j|
-                uint32_t ph[2], pl[2], dab[2], dpb[2];
-#pragma unroll
-                for (int h2 = 0; h2 < 2; ++h2) {
-                    ph[h2] = pack_bf16x2(p[2 * h2], p[2 * h2 + 1]);
-                    pl[h2] = pack_bf16x2(p[2 * h2] - __uint_as_float(ph[h2] << 16),
-                                         p[2 * h2 + 1] - __uint_as_float(ph[h2] & 0xFFFF0000u));
-                    dab[h2] = pack_bf16x2(da[2 * h2], da[2 * h2 + 1]);
-                    dpb[h2] = pack_bf16x2(da[2 * h2] * cf_k, da[2 * h2 + 1] * cf_k);
-                }
-                const bf16x4 Bph = __builtin_bit_cast(bf16x4, make_uint2(ph[0], ph[1]));
-                const bf16x4 Bpl = __builtin_bit_cast(bf16x4, make_uint2(pl[0], pl[1]));
-                const bf16x4 Bda = __builtin_bit_cast(bf16x4, make_uint2(dab[0], dab[1]));
-                // dA'^T row key_w, queries q0 .. q0+3
-                *reinterpret_cast<uint2*>(S.Ts + row_piece_offset(key_w, 2 * qb + (g >> 1)) + 8 * (g & 1)) =
-                    make_uint2(dpb[0], dpb[1]);
-                const int dbase = ring2_row(c, 16 * qb), qbase = ring_row(c, 16 * qb);
-#pragma unroll
-                for (int bd = 0; bd < 4; ++bd) {
-                    const bf16x4 dOt = vt_read(S.Ds + vt_offset(dbase, 16 * bd, lane));
-                    accV[bd] = mfma16x16x16(dOt, Bph, accV[bd]);
-                    accV[bd] = mfma16x16x16(dOt, Bpl, accV[bd]);
-                    accK[bd] = mfma16x16x16(vt_read(S.Qs + vt_offset(qbase, 16 * bd, lane)), Bda, accK[bd]);
-                }
-            }
-        }
-
-        // ---- a key block whose chunk leaves the window: its tokens are
-        // done as keys (and, in the previous step, as queries) ----
-        if (k_chunk == c - 1) {
+        // ---- (A) key block of chunk c-2: its tokens are done as keys (steps
+        // c-2, c-1) and as queries (dQ from step c-1) ----
+        if ((c & 1) == cp) {
+            const int kc = c - 2;
             const int t_i = 16 * b + n;
-            const int slot = k_chunk * kChunk + t_i;
-            if (k_chunk >= c0 && slot < L) {  // chunk c0-1 belongs to the previous strip
-                const int tr = ring_row(k_chunk, t_i);
+            const int slot = kc * kChunk + t_i;
+            if (kc >= c0 && slot < L) {  // chunk c0-1 belongs to the previous strip
+                const int tr = ring_row(kc, t_i);
                 const float cf = __uint_as_float(S.rec[tr][RW - 3]);
                 const float inv = cf * (1.f / scale_log2e);  // 1/|q|, 0 for a zero row
+                const float* Xk = S.X[kc & 1];
                 f32x4 qv[4], xq[4];
                 float kd = 0.f;
 #pragma unroll
@@ -304,7 +199,7 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
                         S.Qs + row_piece_offset(tr, 2 * bd + (g >> 1)) + 8 * (g & 1));
                     qv[bd] = f32x4{__uint_as_float(w2.x << 16), __uint_as_float(w2.x & 0xFFFF0000u),
                                    __uint_as_float(w2.y << 16), __uint_as_float(w2.y & 0xFFFF0000u)};
-                    xq[bd] = *reinterpret_cast<const f32x4*>(&S.X[t_i * kXStride + 16 * bd + 4 * g]);
+                    xq[bd] = *reinterpret_cast<const f32x4*>(&Xk[xoff(t_i, 4 * bd + g)]);
 #pragma unroll
                     for (int j = 0; j < 4; ++j) kd = fmaf(accK[bd][j], qv[bd][j], kd);
                 }
@@ -348,24 +243,166 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
                 accV[bd] = f32x4{};
             }
         }
-        __syncthreads();  // dA'^T complete; every finishing read of X done
 
-        // ---- pass 2: dQ of query block qb, dims of half dh, over the window ----
-        if (c < c1) {
+        // ---- (B) dQ of query block qb of chunk c-1, dims of half dh, over
+        // the window of step c-1 (keys of chunks c-2 and c-1) ----
+        if (c - 1 >= c0 && c - 1 < c1) {
             const int qb = wave & 3, dh = wave >> 2;
+            const char* Tp = S.Ts[(c - 1) & 1];
             f32x4 dq2[2] = {f32x4{}, f32x4{}};
 #pragma unroll
             for (int kw2 = 0; kw2 < 8; ++kw2) {
-                if (((block_queries(kw2) >> (16 * qb)) & 0xFFFFull) == 0) continue;
-                const bf16x4 bT = vt_read(S.Ts + vt_offset(16 * kw2, 16 * qb, lane));
-                const int kbase = ring_row(c - 1 + (kw2 >> 2), 16 * (kw2 & 3));
+                const uint64_t reach = __ballot(prev_lo <= prev_hi && prev_lo <= 16 * kw2 + 15 && prev_hi >= 16 * kw2);
+                if (((reach >> (16 * qb)) & 0xFFFFull) == 0) continue;
+                const bf16x4 bT = vt_read(Tp + vt_offset(16 * kw2, 16 * qb, lane));
+                const int kbase = ring_row(c - 2 + (kw2 >> 2), 16 * (kw2 & 3));
 #pragma unroll
                 for (int i = 0; i < 2; ++i)
                     dq2[i] = mfma16x16x16(vt_read(S.Qs + vt_offset(kbase, 16 * (2 * dh + i), lane)), bT, dq2[i]);
             }
+            float* Xq = S.X[(c - 1) & 1];
 #pragma unroll
             for (int i = 0; i < 2; ++i)
-                *reinterpret_cast<f32x4*>(&S.X[(16 * qb + n) * kXStride + 16 * (2 * dh + i) + 4 * g]) = dq2[i];
+                *reinterpret_cast<f32x4*>(&Xq[xoff(16 * qb + n, 4 * (2 * dh + i) + g)]) = dq2[i];
+        }
+
+        // ---- (C) step c ----
+        if (c <= c1) {
+            // each query's key interval [lo, hi] in window rows (0..63: chunk
+            // c-1, 64..127: chunk c), from the bucket boundaries of the window:
+            // lane = query of chunk c
+            int lo_q, hi_q;
+            {
+                const uint32_t kA = sig_round_id(&S.rec[ring_row(c - 1, lane)][0], r);
+                const uint32_t kB = sig_round_id(&S.rec[ring_row(c, lane)][0], r);
+                const uint32_t prevA = __shfl_up(kA, 1);
+                const uint32_t lastA = __shfl(kA, 63);
+                const uint32_t prevB0 = __shfl_up(kB, 1);
+                const uint32_t prevB = lane == 0 ? lastA : prevB0;
+                const uint64_t bA = __ballot(lane == 0 || kA != prevA);
+                const uint64_t bB = __ballot(kB != prevB);
+                const uint64_t upto = bB & (~0ull >> (63 - lane));
+                const int lo_w = upto ? 127 - __clzll(upto) : 63 - __clzll(bA);
+                lo_q = max(lo_w, (1 - c) * kChunk);  // no slot before 0
+                if constexpr (CAUSAL) {
+                    hi_q = kChunk + lane - 1;
+                } else {
+                    const uint64_t after = lane < 63 ? bB & (~0ull << (lane + 1)) : 0ull;
+                    hi_q = after ? 62 + __ffsll((long long)after) : 127;
+                }
+                hi_q = min(hi_q, L - 1 - (c - 1) * kChunk);  // no slot past the sequence
+                if (c * kChunk + lane >= L) {                // no query here
+                    lo_q = 1;
+                    hi_q = 0;
+                }
+                S.lohi[wave][lane] = (uint32_t)lo_q | ((uint32_t)hi_q << 16);
+                const uint32_t* qrec = &S.rec[ring_row(c, lane)][0];
+                S.zd[wave][lane] = make_float2(__uint_as_float(qrec[RW - 2]), __uint_as_float(qrec[RW - 1]));
+                if constexpr (kWaveSig) {
+#pragma unroll
+                    for (int w = 0; w < NW; ++w) S.qsig[wave][w][lane] = qrec[w];
+                }
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+            // pass 1: this wave's key block against the 64 queries
+            const int k_chunk = (c & 1) == cp ? c : c - 1;  // the chunk of this wave's parity
+            const int kw = (k_chunk == c ? 4 : 0) + b;      // its window block
+            if (!(k_chunk == c && c == c1)) {               // chunk c1 belongs to the next strip
+                // queries that reach this key block (one bit per query)
+                const uint64_t qmask = __ballot(lo_q <= hi_q && lo_q <= 16 * kw + 15 && hi_q >= 16 * kw);
+                const int krow = ring_row(k_chunk, 16 * b + n);
+                const int krow_v = ringv_row(k_chunk, 16 * b + n);
+                const int key_w = 16 * kw + n;
+                const uint32_t* krec = &S.rec[krow][0];
+                const float cf_k = __uint_as_float(krec[RW - 3]);
+                uint32_t ks[NW > 0 ? NW : 1];
+#pragma unroll
+                for (int w = 0; w < (NW > 0 ? NW : 1); ++w) ks[w] = krec[w];
+                const bf16x8 bk0 = as_bf16x8(lds_piece(S.Qs, krow, g));
+                const bf16x8 bk1 = as_bf16x8(lds_piece(S.Qs, krow, 4 + g));
+                const bf16x8 bv0 = as_bf16x8(lds_piece(S.Vs, krow_v, g));
+                const bf16x8 bv1 = as_bf16x8(lds_piece(S.Vs, krow_v, 4 + g));
+                char* Tc = S.Ts[c & 1];
+#pragma unroll
+                for (int qb = 0; qb < 4; ++qb) {
+                    if (((qmask >> (16 * qb)) & 0xFFFFull) == 0) continue;
+                    const int qrow = ring_row(c, 16 * qb + n);
+                    const int drow = ring2_row(c, 16 * qb + n);
+                    f32x4 sacc = mfma16x16x32(as_bf16x8(lds_piece(S.Qs, qrow, g)), bk0, f32x4{});
+                    sacc = mfma16x16x32(as_bf16x8(lds_piece(S.Qs, qrow, 4 + g)), bk1, sacc);
+                    f32x4 dpacc = mfma16x16x32(as_bf16x8(lds_piece(S.Ds, drow, g)), bv0, f32x4{});
+                    dpacc = mfma16x16x32(as_bf16x8(lds_piece(S.Ds, drow, 4 + g)), bv1, dpacc);
+                    // lane holds queries 16qb + 4g + j (j = 0..3) against key n
+                    // the lane's four queries: intervals, log-partitions, D and
+                    // signature words, one 16-byte read per field (lane groups
+                    // read consecutive runs, so these reads do not conflict)
+                    const int q0 = 16 * qb + 4 * g;
+                    const u32x4 lh4 = *reinterpret_cast<const u32x4*>(&S.lohi[wave][q0]);
+                    const f32x4 zd01 = *reinterpret_cast<const f32x4*>(&S.zd[wave][q0]);
+                    const f32x4 zd23 = *reinterpret_cast<const f32x4*>(&S.zd[wave][q0 + 2]);
+                    u32x4 qs4[NW > 0 ? NW : 1];
+                    if constexpr (NW > 0) {
+#pragma unroll
+                        for (int w = 0; w < NW; ++w) {
+                            if constexpr (kWaveSig) {
+                                qs4[w] = *reinterpret_cast<const u32x4*>(&S.qsig[wave][w][q0]);
+                            } else {
+#pragma unroll
+                                for (int j = 0; j < 4; ++j) qs4[w][j] = S.rec[ring_row(c, q0 + j)][w];
+                            }
+                        }
+                    }
+                    const int lo_a[4] = {(int)(lh4[0] & 0xFFFFu), (int)(lh4[1] & 0xFFFFu), (int)(lh4[2] & 0xFFFFu),
+                                         (int)(lh4[3] & 0xFFFFu)};
+                    const int hi_a[4] = {(int)(lh4[0] >> 16), (int)(lh4[1] >> 16), (int)(lh4[2] >> 16),
+                                         (int)(lh4[3] >> 16)};
+                    const float z2_a[4] = {zd01[0], zd01[2], zd23[0], zd23[2]};
+                    const float D_a[4] = {zd01[1], zd01[3], zd23[1], zd23[3]};
+                    float p[4], da[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        bool valid = lo_a[j] <= key_w && key_w <= hi_a[j];
+                        if constexpr (!CAUSAL) valid = valid && key_w != kChunk + q0 + j;
+                        uint32_t t = valid ? 0u : ~0u;
+                        if constexpr (NW > 0) {
+#pragma unroll
+                            for (int w = 0; w < NW; ++w)
+                                t = and_or((qs4[w][j] ^ ks[w]) + sig_add(w), sig_guard(w), t);
+                        }
+                        p[j] = __builtin_amdgcn_exp2f(fmaf(sacc[j], cf_k, S.tab[__popc(t)] - z2_a[j]));
+                        da[j] = p[j] * (dpacc[j] - D_a[j]);
+                    }
+                    // P as bf16 hi + lo planes, dA and dA' = dA * scale*log2(e)/|q_j|
+                    uint32_t ph[2], pl[2], dab[2], dpb[2];
+#pragma unroll
+                    for (int h2 = 0; h2 < 2; ++h2) {
+                        ph[h2] = pack_bf16x2(p[2 * h2], p[2 * h2 + 1]);
+                        pl[h2] = pack_bf16x2(p[2 * h2] - __uint_as_float(ph[h2] << 16),
+                                             p[2 * h2 + 1] - __uint_as_float(ph[h2] & 0xFFFF0000u));
+                        dab[h2] = pack_bf16x2(da[2 * h2], da[2 * h2 + 1]);
+                        dpb[h2] = pack_bf16x2(da[2 * h2] * cf_k, da[2 * h2 + 1] * cf_k);
+                    }
+                    const bf16x4 Bph = __builtin_bit_cast(bf16x4, make_uint2(ph[0], ph[1]));
+                    const bf16x4 Bpl = __builtin_bit_cast(bf16x4, make_uint2(pl[0], pl[1]));
+                    const bf16x4 Bda = __builtin_bit_cast(bf16x4, make_uint2(dab[0], dab[1]));
+                    // dA'^T row key_w, queries q0 .. q0+3
+                    *reinterpret_cast<uint2*>(Tc + row_piece_offset(key_w, 2 * qb + (g >> 1)) + 8 * (g & 1)) =
+                        make_uint2(dpb[0], dpb[1]);
+                    const int dbase = ring2_row(c, 16 * qb), qbase = ring_row(c, 16 * qb);
+#pragma unroll
+                    for (int bd = 0; bd < 4; ++bd) {
+                        const bf16x4 dOt = vt_read(S.Ds + vt_offset(dbase, 16 * bd, lane));
+                        accV[bd] = mfma16x16x16(dOt, Bph, accV[bd]);
+                        accV[bd] = mfma16x16x16(dOt, Bpl, accV[bd]);
+                        accK[bd] = mfma16x16x16(vt_read(S.Qs + vt_offset(qbase, 16 * bd, lane)), Bda, accK[bd]);
+                    }
+                }
+            }
+            prev_lo = lo_q;
+            prev_hi = hi_q;
         }
         pf_pos = pf_next;
         __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of chunk c+1 have landed
@@ -485,7 +522,7 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
 int rec_words(int n_rounds) {
     const int nw = n_rounds == 1 ? 0 : (n_rounds + 1) / 2;
     const int sw = sig_stride(nw);
-    return sw + 3 <= 4 ? 4 : (sw + 3 <= 8 ? 8 : 16);
+    return sw + 3 <= 4 ? 4 : (sw + 3 <= 8 ? 8 : 12);
 }
 
 struct BwdWs {
@@ -527,22 +564,18 @@ hipError_t launch_nw(bool causal, int64_t BH, int L, int n_rounds, float scale, 
     const int64_t n_chunks = (L + kChunk - 1) / kChunk, segs = BH * n_rounds;
     const int cps = (int)std::max<int64_t>(1, std::min<int64_t>(32, n_chunks * segs / 2048));
     const dim3 grid((unsigned)((n_chunks + cps - 1) / cps), (unsigned)segs);
-    // one chunk in flight: gathering two ahead (deeper rings, which still fit
-    // in LDS below eight signature words) measured slower
-    auto go = [&](auto causal_tag, auto depth_tag) {
+    auto go = [&](auto causal_tag) {
         constexpr bool C = decltype(causal_tag)::value;
-        constexpr int D = decltype(depth_tag)::value;
-        const size_t lds = sizeof(BwdShared<NW, D>);
-        hipFuncSetAttribute(reinterpret_cast<const void*>(&bwd_strip_kernel<NW, C, D>),
+        const size_t lds = sizeof(BwdShared<NW>);
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&bwd_strip_kernel<NW, C>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        bwd_strip_kernel<NW, C, D><<<grid, kBwdThreads, lds, stream>>>(
+        bwd_strip_kernel<NW, C><<<grid, kBwdThreads, lds, stream>>>(
             q, v, dout, w.rec, perm, w.part_q, w.part_v, w.part_e, L, n_rounds, scale, cps);
     };
-    using Depth = std::integral_constant<int, 1>;
     if (causal)
-        go(std::true_type{}, Depth{});
+        go(std::true_type{});
     else
-        go(std::false_type{}, Depth{});
+        go(std::false_type{});
     return hipGetLastError();
 }
 
