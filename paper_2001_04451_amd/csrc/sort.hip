@@ -23,8 +23,9 @@ namespace lsh {
 namespace {
 
 constexpr int kTile = 4096;
-constexpr int kSortWaves = 4;
+constexpr int kSortWaves = 8;
 constexpr int kPerWave = kTile / kSortWaves;
+constexpr int kOffPerThread = (1024 + kSortWaves * 64 - 1) / (kSortWaves * 64);  // n_b <= 1024
 constexpr int kHistLdsInts = 8192;
 
 __device__ __forceinline__ int clamp_bucket(int b, int n_b) { return min(max(b, 0), n_b - 1); }
@@ -155,7 +156,7 @@ __global__ __launch_bounds__(256) void sort_scan_kernel(int32_t* __restrict__ co
 // LDS of the scatter: per-wave next slot of every bucket [kSortWaves][n_b].
 size_t scatter_lds_bytes(int n_b) { return (size_t)kSortWaves * n_b * sizeof(int); }
 
-__global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __restrict__ buckets,
+__global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int32_t* __restrict__ buckets,
                                                            const int32_t* __restrict__ offsets,
                                                            int L, int n_r, int n_b,
                                                            int n_tiles, int32_t* __restrict__ perm,
@@ -190,6 +191,11 @@ __global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __rest
         const int pos = min(max(p0 + 64 * it + lane, 0), max(p1 - 1, 0));
         ids[it] = buckets[(bh * L + pos) * n_r + r];
     }
+    // the tile's first slot of every bucket this thread sets up below
+    int off_pre[kOffPerThread];
+#pragma unroll
+    for (int k = 0; k < kOffPerThread; ++k)
+        off_pre[k] = offsets[(seg * n_tiles + tile) * n_b + min((int)threadIdx.x + k * kSortWaves * 64, n_b - 1)];
 #pragma unroll
     for (int it = 0; it < kIter; ++it) ids[it] = clamp_bucket(ids[it], n_b);
     __syncthreads();
@@ -197,10 +203,13 @@ __global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t* __rest
     for (int it = 0; it < kIter; ++it)
         if (p0 + 64 * it + lane < p1) atomicAdd(&wbase[ids[it]], 1);
     __syncthreads();
-    // Per-wave starting slot of every bucket: the tile's offset plus the counts
-    // of the earlier waves of this tile.
-    for (int b = threadIdx.x; b < n_b; b += blockDim.x) {
-        int off = offsets[(seg * n_tiles + tile) * n_b + b];
+    // Per-wave starting slot of every bucket: the tile's offset (loaded with
+    // the ids) plus the counts of the earlier waves of this tile.
+#pragma unroll
+    for (int k = 0; k < kOffPerThread; ++k) {
+        const int b = threadIdx.x + k * kSortWaves * 64;
+        if (b >= n_b) break;
+        int off = off_pre[k];
         for (int w = 0; w < kSortWaves; ++w) {
             const int cnt = base[w * n_b + b];
             base[w * n_b + b] = off;
@@ -308,7 +317,7 @@ hipError_t launch_sort(int64_t BH, int L, int n_rounds, int n_buckets, const int
         buckets, L, n_rounds, n_buckets, rpg, n_tiles, counts);
     sort_scan_kernel<<<(unsigned)(BH * n_rounds), 256, 0, stream>>>(counts, L, n_buckets, n_tiles,
                                                                     bucket_start);
-    sort_scatter_kernel<<<dim3(n_tiles, (unsigned)(BH * n_rounds)), 256, scatter_lds_bytes(n_buckets),
+    sort_scatter_kernel<<<dim3(n_tiles, (unsigned)(BH * n_rounds)), kSortWaves * 64, scatter_lds_bytes(n_buckets),
                           stream>>>(
         buckets, counts, L, n_rounds, n_buckets, n_tiles, perm, undo);
     return hipGetLastError();
