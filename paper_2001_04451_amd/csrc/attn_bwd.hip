@@ -12,8 +12,9 @@
 //  * bwd_prep:   one record per token: its packed bucket ids, its key scale
 //                scale*log2(e)/|q|, its log-partition in log2 units and
 //                D = dO . o.
-//  * bwd_strip:  eight waves walk a strip of chunks of one (batch, head,
-//                round) segment.  Step c takes the queries of chunk c
+//  * bwd_strip:  twelve waves walk a strip of chunks of one (batch, head,
+//                round) segment: eight own key blocks (pass 1 and the
+//                finishing below), four form dQ (pass 2).  Step c takes the queries of chunk c
 //                against the 128 keys of chunks c-1 and c (their whole
 //                window), so every (query, key) pair of the round is met in
 //                exactly one step, and the keys of chunk c meet their last
@@ -21,9 +22,10 @@
 //                records: four slots, v: three, dO: two), and chunk c+1 is
 //                gathered into the free slots (through perm, straight from
 //                global memory into LDS) while step c computes.  A step runs
-//                the finishing of chunk c-2's key blocks, pass 2 of step c-1
-//                and pass 1 of step c, with dA'^T and dQ double-buffered, so
-//                it needs a single barrier.
+//                the finishing of chunk c-2's key blocks and pass 1 of step c
+//                on the key waves while the dQ waves run pass 2 of step c-1,
+//                with dA'^T and dQ double-buffered, so it needs a single
+//                barrier.
 //                Pass 1, lanes on keys: each wave owns one 16-key block of
 //                one chunk for the two steps in which that chunk is in the
 //                window.  Per 16x16 tile S = Q K^T and dP = dO V^T on the
@@ -56,7 +58,8 @@ namespace lsh {
 namespace {
 
 constexpr int kMaskedIndex = 32;  // table index of a masked-out pair
-constexpr int kBwdThreads = 512;  // eight waves
+constexpr int kKeyWaves = 8;                      // waves owning key blocks (passes 1 and the finishing)
+constexpr int kBwdThreads = (kKeyWaves + 4) * 64;  // plus four dQ waves (pass 2)
 
 // Per-token record: signature words [0, SW), then the key scale, the total
 // log-partition in log2 units and D, in the last three words.
@@ -70,12 +73,10 @@ struct BwdRec {
 // c-2 .. c (the finishing of chunk c-2, the dQ of chunk c-1, the pairs of
 // step c) and gathers chunk c+1: a four-slot ring; v rows are read for
 // chunks c-1 and c (three slots), dO rows for chunk c (two slots).  dA'^T
-// and dQ are double-buffered by the parity of their chunk, so that a step
-// needs one barrier.  The per-wave copies of each query's interval,
-// log-partition, D and signature words let every wave read its four queries'
-// fields as 16-byte runs without a second barrier; beyond four signature
-// words (more than eight rounds) they are read from the records instead, to
-// stay within 160 KB.
+// and dQ are double-buffered by the parity of their chunk, and the query
+// fields (interval, log-partition, D, signature words) kept for three
+// chunks, so that a step needs one barrier.  Beyond four signature words
+// (more than eight rounds) the signature words are read from the records.
 template <int NW>
 struct BwdShared {
     static constexpr int kQSlots = 4, kVSlots = 3, kDSlots = 2;
@@ -86,9 +87,14 @@ struct BwdShared {
     char Ts[2][2 * kChunk * 128];     // dA'^T: 128 window keys x 64 queries (bf16), by step parity
     float X[2][kChunk * kHeadDim];    // dQ of a chunk's tokens, [token][dim] (see xoff), by chunk parity
     uint32_t rec[kQSlots * kChunk][BwdRec<NW>::RW];
-    uint32_t lohi[8][kChunk];         // lo | hi << 16 (both in 0 .. 127)
-    float2 zd[8][kChunk];
-    uint32_t qsig[8][kQsigWords][kChunk];
+    // per chunk (three chunks: c-1, c and the one set up for c+1), per
+    // query: its key interval in window rows (lo | hi << 16, both in
+    // 0 .. 127), its log-partition (log2 units) and D, and its signature
+    // words, laid out so that a lane reads its four queries' fields as
+    // 16-byte runs
+    uint32_t lohi[3][kChunk];
+    float2 zd[3][kChunk];
+    uint32_t qsig[3][kQsigWords][kChunk];
     float tab[kMaskedIndex + 1];      // -log2 N by mismatch count; -inf = masked
 };
 static_assert(sizeof(BwdShared<4>) <= 160 * 1024 && sizeof(BwdShared<8>) <= 160 * 1024, "LDS");
@@ -139,9 +145,10 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
         const int slot = cc * kChunk + lane;
         return cc >= 0 && slot < L ? pseg[slot] : 0;
     };
-    // Gather chunk cc into its ring slots: wave w copies q, v and dO rows
-    // 8w .. 8w+7 (each lane the 16-byte piece that belongs at its LDS slot);
-    // the records go through the first RW/4 waves.
+    // Gather chunk cc into its ring slots (key waves only): wave w copies q,
+    // v and dO rows 8w .. 8w+7 (each lane the 16-byte piece that belongs at
+    // its LDS slot), and wave 0 also the whole chunk's records, which it then
+    // reads to set up the chunk's query fields (set_queries).
     auto stage = [&](int cc, int pos_raw) {
         const int pos_lane = min(max(pos_raw, 0), L - 1);
         const int row = 8 * wave + (lane >> 3);
@@ -151,17 +158,69 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
         copy16_to_lds(v + off, S.Vs + ringv_row(cc, 8 * wave) * 128);
         copy16_to_lds(dout + off, S.Ds + ring2_row(cc, 8 * wave) * 128);
         constexpr int U = RW / 4;  // 16-byte units per record
-        if (wave < U) {
-            const int u = 64 * wave + lane, rr = u / U;
-            const int pr = __shfl(pos_lane, rr);
-            copy16_to_lds(rec + (rowbase + pr) * RW + 4 * (u % U), &S.rec[ring_row(cc, 0)][0] + 256 * wave);
+        if (wave == 0) {
+#pragma unroll
+            for (int k = 0; k < U; ++k) {
+                const int u = 64 * k + lane, rr = u / U;
+                const int pr = __shfl(pos_lane, rr);
+                copy16_to_lds(rec + (rowbase + pr) * RW + 4 * (u % U), &S.rec[ring_row(cc, 0)][0] + 256 * k);
+            }
         }
     };
+    // The query fields of chunk cc (wave 0, lane = query, once the records of
+    // chunks cc-1 and cc are in LDS): each query's key interval [lo, hi] in
+    // window rows (0..63: chunk cc-1, 64..127: chunk cc) from the bucket
+    // boundaries of the window, its log-partition and D, its signature words.
+    auto set_queries = [&](int cc) {
+        const uint32_t kA = sig_round_id(&S.rec[ring_row(cc - 1, lane)][0], r);
+        const uint32_t kB = sig_round_id(&S.rec[ring_row(cc, lane)][0], r);
+        const uint32_t prevA = __shfl_up(kA, 1);
+        const uint32_t lastA = __shfl(kA, 63);
+        const uint32_t prevB0 = __shfl_up(kB, 1);
+        const uint32_t prevB = lane == 0 ? lastA : prevB0;
+        const uint64_t bA = __ballot(lane == 0 || kA != prevA);
+        const uint64_t bB = __ballot(kB != prevB);
+        const uint64_t upto = bB & (~0ull >> (63 - lane));
+        const int lo_w = upto ? 127 - __clzll(upto) : 63 - __clzll(bA);
+        int lo_q = max(lo_w, (1 - cc) * kChunk);  // no slot before 0
+        int hi_q;
+        if constexpr (CAUSAL) {
+            hi_q = kChunk + lane - 1;
+        } else {
+            const uint64_t after = lane < 63 ? bB & (~0ull << (lane + 1)) : 0ull;
+            hi_q = after ? 62 + __ffsll((long long)after) : 127;
+        }
+        hi_q = min(hi_q, L - 1 - (cc - 1) * kChunk);  // no slot past the sequence
+        if (cc * kChunk + lane >= L) {                // no query here
+            lo_q = 1;
+            hi_q = 0;
+        }
+        const int buf = cc % 3;
+        S.lohi[buf][lane] = (uint32_t)lo_q | ((uint32_t)hi_q << 16);
+        const uint32_t* qrec = &S.rec[ring_row(cc, lane)][0];
+        S.zd[buf][lane] = make_float2(__uint_as_float(qrec[RW - 2]), __uint_as_float(qrec[RW - 1]));
+        if constexpr (kWaveSig) {
+#pragma unroll
+            for (int w = 0; w < NW; ++w) S.qsig[buf][w][lane] = qrec[w];
+        }
+    };
+    // whether the query of this lane, in the step of chunk cc, reaches window
+    // block kw
+    auto reaches = [&](int cc, int kw) {
+        const uint32_t lh = S.lohi[cc % 3][lane];
+        const int lo = (int)(lh & 0xFFFFu), hi = (int)(lh >> 16);
+        return lo <= hi && lo <= 16 * kw + 15 && hi >= 16 * kw;
+    };
 
-    stage(c0 - 1, chunk_pos(c0 - 1));
-    stage(c0, chunk_pos(c0));
-    int pf_pos = chunk_pos(c0 + 1);
+    const bool key_wave = wave < kKeyWaves;
+    int pf_pos = 0;
+    if (key_wave) {
+        stage(c0 - 1, chunk_pos(c0 - 1));
+        stage(c0, chunk_pos(c0));
+        pf_pos = chunk_pos(c0 + 1);
+    }
     __builtin_amdgcn_s_waitcnt(0);
+    if (wave == 0) set_queries(c0);
     __syncthreads();
 
     // This wave's key block: block b of every chunk of parity cp, held for
@@ -170,19 +229,21 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
     const int b = wave & 3, cp = wave >> 2;
     f32x4 accK[4] = {f32x4{}, f32x4{}, f32x4{}, f32x4{}};  // dK^T by 16-dim blocks
     f32x4 accV[4] = {f32x4{}, f32x4{}, f32x4{}, f32x4{}};  // dV^T
-    // the key intervals of this lane's query in the previous step (for its dQ)
-    int prev_lo = 1, prev_hi = 0;
 
-    // Step c: (A) the waves of chunk c's parity finish their key block of
-    // chunk c-2; (B) dQ of chunk c-1's queries from the dA'^T of step c-1;
-    // (C) the pairs of chunk c's queries with the keys of chunks c-1 and c.
+    // Step c: (A) the key waves of chunk c's parity finish their key block of
+    // chunk c-2; (B) the dQ waves form dQ of chunk c-1's queries from the
+    // dA'^T of step c-1; (C) the key waves take the pairs of chunk c's
+    // queries with the keys of chunks c-1 and c.
     for (int c = c0; c <= c1 + 1; ++c) {
-        if (c + 1 <= c1) stage(c + 1, pf_pos);
-        const int pf_next = chunk_pos(c + 2);
+        int pf_next = 0;
+        if (key_wave) {
+            if (c + 1 <= c1) stage(c + 1, pf_pos);
+            pf_next = chunk_pos(c + 2);
+        }
 
         // ---- (A) key block of chunk c-2: its tokens are done as keys (steps
         // c-2, c-1) and as queries (dQ from step c-1) ----
-        if ((c & 1) == cp) {
+        if (key_wave && (c & 1) == cp) {
             const int kc = c - 2;
             const int t_i = 16 * b + n;
             const int slot = kc * kChunk + t_i;
@@ -244,75 +305,35 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
             }
         }
 
-        // ---- (B) dQ of query block qb of chunk c-1, dims of half dh, over
-        // the window of step c-1 (keys of chunks c-2 and c-1) ----
-        if (c - 1 >= c0 && c - 1 < c1) {
-            const int qb = wave & 3, dh = wave >> 2;
+        // ---- (B) dQ of query block qb of chunk c-1 over the window of
+        // step c-1 (keys of chunks c-2 and c-1) ----
+        if (!key_wave && c - 1 >= c0 && c - 1 < c1) {
+            const int qb = wave - kKeyWaves;
             const char* Tp = S.Ts[(c - 1) & 1];
-            f32x4 dq2[2] = {f32x4{}, f32x4{}};
+            f32x4 dq4[4] = {f32x4{}, f32x4{}, f32x4{}, f32x4{}};
 #pragma unroll
             for (int kw2 = 0; kw2 < 8; ++kw2) {
-                const uint64_t reach = __ballot(prev_lo <= prev_hi && prev_lo <= 16 * kw2 + 15 && prev_hi >= 16 * kw2);
+                const uint64_t reach = __ballot(reaches(c - 1, kw2));
                 if (((reach >> (16 * qb)) & 0xFFFFull) == 0) continue;
                 const bf16x4 bT = vt_read(Tp + vt_offset(16 * kw2, 16 * qb, lane));
                 const int kbase = ring_row(c - 2 + (kw2 >> 2), 16 * (kw2 & 3));
 #pragma unroll
-                for (int i = 0; i < 2; ++i)
-                    dq2[i] = mfma16x16x16(vt_read(S.Qs + vt_offset(kbase, 16 * (2 * dh + i), lane)), bT, dq2[i]);
+                for (int i = 0; i < 4; ++i)
+                    dq4[i] = mfma16x16x16(vt_read(S.Qs + vt_offset(kbase, 16 * i, lane)), bT, dq4[i]);
             }
             float* Xq = S.X[(c - 1) & 1];
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
-                *reinterpret_cast<f32x4*>(&Xq[xoff(16 * qb + n, 4 * (2 * dh + i) + g)]) = dq2[i];
+            for (int i = 0; i < 4; ++i) *reinterpret_cast<f32x4*>(&Xq[xoff(16 * qb + n, 4 * i + g)]) = dq4[i];
         }
 
         // ---- (C) step c ----
-        if (c <= c1) {
-            // each query's key interval [lo, hi] in window rows (0..63: chunk
-            // c-1, 64..127: chunk c), from the bucket boundaries of the window:
-            // lane = query of chunk c
-            int lo_q, hi_q;
-            {
-                const uint32_t kA = sig_round_id(&S.rec[ring_row(c - 1, lane)][0], r);
-                const uint32_t kB = sig_round_id(&S.rec[ring_row(c, lane)][0], r);
-                const uint32_t prevA = __shfl_up(kA, 1);
-                const uint32_t lastA = __shfl(kA, 63);
-                const uint32_t prevB0 = __shfl_up(kB, 1);
-                const uint32_t prevB = lane == 0 ? lastA : prevB0;
-                const uint64_t bA = __ballot(lane == 0 || kA != prevA);
-                const uint64_t bB = __ballot(kB != prevB);
-                const uint64_t upto = bB & (~0ull >> (63 - lane));
-                const int lo_w = upto ? 127 - __clzll(upto) : 63 - __clzll(bA);
-                lo_q = max(lo_w, (1 - c) * kChunk);  // no slot before 0
-                if constexpr (CAUSAL) {
-                    hi_q = kChunk + lane - 1;
-                } else {
-                    const uint64_t after = lane < 63 ? bB & (~0ull << (lane + 1)) : 0ull;
-                    hi_q = after ? 62 + __ffsll((long long)after) : 127;
-                }
-                hi_q = min(hi_q, L - 1 - (c - 1) * kChunk);  // no slot past the sequence
-                if (c * kChunk + lane >= L) {                // no query here
-                    lo_q = 1;
-                    hi_q = 0;
-                }
-                S.lohi[wave][lane] = (uint32_t)lo_q | ((uint32_t)hi_q << 16);
-                const uint32_t* qrec = &S.rec[ring_row(c, lane)][0];
-                S.zd[wave][lane] = make_float2(__uint_as_float(qrec[RW - 2]), __uint_as_float(qrec[RW - 1]));
-                if constexpr (kWaveSig) {
-#pragma unroll
-                    for (int w = 0; w < NW; ++w) S.qsig[wave][w][lane] = qrec[w];
-                }
-            }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
+        if (key_wave && c <= c1) {
             // pass 1: this wave's key block against the 64 queries
             const int k_chunk = (c & 1) == cp ? c : c - 1;  // the chunk of this wave's parity
             const int kw = (k_chunk == c ? 4 : 0) + b;      // its window block
             if (!(k_chunk == c && c == c1)) {               // chunk c1 belongs to the next strip
                 // queries that reach this key block (one bit per query)
-                const uint64_t qmask = __ballot(lo_q <= hi_q && lo_q <= 16 * kw + 15 && hi_q >= 16 * kw);
+                const uint64_t qmask = __ballot(reaches(c, kw));
                 const int krow = ring_row(k_chunk, 16 * b + n);
                 const int krow_v = ringv_row(k_chunk, 16 * b + n);
                 const int key_w = 16 * kw + n;
@@ -340,15 +361,16 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
                     // signature words, one 16-byte read per field (lane groups
                     // read consecutive runs, so these reads do not conflict)
                     const int q0 = 16 * qb + 4 * g;
-                    const u32x4 lh4 = *reinterpret_cast<const u32x4*>(&S.lohi[wave][q0]);
-                    const f32x4 zd01 = *reinterpret_cast<const f32x4*>(&S.zd[wave][q0]);
-                    const f32x4 zd23 = *reinterpret_cast<const f32x4*>(&S.zd[wave][q0 + 2]);
+                    const int qbuf = c % 3;
+                    const u32x4 lh4 = *reinterpret_cast<const u32x4*>(&S.lohi[qbuf][q0]);
+                    const f32x4 zd01 = *reinterpret_cast<const f32x4*>(&S.zd[qbuf][q0]);
+                    const f32x4 zd23 = *reinterpret_cast<const f32x4*>(&S.zd[qbuf][q0 + 2]);
                     u32x4 qs4[NW > 0 ? NW : 1];
                     if constexpr (NW > 0) {
 #pragma unroll
                         for (int w = 0; w < NW; ++w) {
                             if constexpr (kWaveSig) {
-                                qs4[w] = *reinterpret_cast<const u32x4*>(&S.qsig[wave][w][q0]);
+                                qs4[w] = *reinterpret_cast<const u32x4*>(&S.qsig[qbuf][w][q0]);
                             } else {
 #pragma unroll
                                 for (int j = 0; j < 4; ++j) qs4[w][j] = S.rec[ring_row(c, q0 + j)][w];
@@ -401,11 +423,10 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
                     }
                 }
             }
-            prev_lo = lo_q;
-            prev_hi = hi_q;
         }
         pf_pos = pf_next;
         __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of chunk c+1 have landed
+        if (wave == 0 && c + 1 <= c1) set_queries(c + 1);
         __syncthreads();                // ... and every wave is done with step c
     }
 }
