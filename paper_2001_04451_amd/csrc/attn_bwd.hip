@@ -145,20 +145,26 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
         const int slot = cc * kChunk + lane;
         return cc >= 0 && slot < L ? pseg[slot] : 0;
     };
-    // Gather chunk cc into its ring slots (key waves only): wave w copies q,
-    // v and dO rows 8w .. 8w+7 (each lane the 16-byte piece that belongs at
-    // its LDS slot), and wave 0 also the whole chunk's records, which it then
+    // Gather chunk cc into its ring slots (dQ waves only, so that the key
+    // waves issue no global loads): dQ wave w copies q, v and dO rows
+    // 16w .. 16w+15 (each lane the 16-byte piece that belongs at its LDS
+    // slot), and dQ wave 0 also the whole chunk's records, which it then
     // reads to set up the chunk's query fields (set_queries).
+    const int dw = wave - kKeyWaves;  // dQ wave index (0..3 on the dQ waves)
     auto stage = [&](int cc, int pos_raw) {
         const int pos_lane = min(max(pos_raw, 0), L - 1);
-        const int row = 8 * wave + (lane >> 3);
-        const int p = __shfl(pos_lane, row);
-        const int64_t off = (rowbase + p) * kHeadDim + swz(row, lane & 7) * 8;
-        copy16_to_lds(q + off, S.Qs + ring_row(cc, 8 * wave) * 128);
-        copy16_to_lds(v + off, S.Vs + ringv_row(cc, 8 * wave) * 128);
-        copy16_to_lds(dout + off, S.Ds + ring2_row(cc, 8 * wave) * 128);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int r0 = 16 * dw + 8 * h;
+            const int row = r0 + (lane >> 3);
+            const int p = __shfl(pos_lane, row);
+            const int64_t off = (rowbase + p) * kHeadDim + swz(row, lane & 7) * 8;
+            copy16_to_lds(q + off, S.Qs + ring_row(cc, r0) * 128);
+            copy16_to_lds(v + off, S.Vs + ringv_row(cc, r0) * 128);
+            copy16_to_lds(dout + off, S.Ds + ring2_row(cc, r0) * 128);
+        }
         constexpr int U = RW / 4;  // 16-byte units per record
-        if (wave == 0) {
+        if (dw == 0) {
 #pragma unroll
             for (int k = 0; k < U; ++k) {
                 const int u = 64 * k + lane, rr = u / U;
@@ -167,7 +173,7 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
             }
         }
     };
-    // The query fields of chunk cc (wave 0, lane = query, once the records of
+    // The query fields of chunk cc (dQ wave 0, lane = query, once the records of
     // chunks cc-1 and cc are in LDS): each query's key interval [lo, hi] in
     // window rows (0..63: chunk cc-1, 64..127: chunk cc) from the bucket
     // boundaries of the window, its log-partition and D, its signature words.
@@ -214,13 +220,13 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
 
     const bool key_wave = wave < kKeyWaves;
     int pf_pos = 0;
-    if (key_wave) {
+    if (!key_wave) {
         stage(c0 - 1, chunk_pos(c0 - 1));
         stage(c0, chunk_pos(c0));
         pf_pos = chunk_pos(c0 + 1);
     }
     __builtin_amdgcn_s_waitcnt(0);
-    if (wave == 0) set_queries(c0);
+    if (dw == 0) set_queries(c0);
     __syncthreads();
 
     // This wave's key block: block b of every chunk of parity cp, held for
@@ -236,7 +242,7 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
     // queries with the keys of chunks c-1 and c.
     for (int c = c0; c <= c1 + 1; ++c) {
         int pf_next = 0;
-        if (key_wave) {
+        if (!key_wave) {
             if (c + 1 <= c1) stage(c + 1, pf_pos);
             pf_next = chunk_pos(c + 2);
         }
@@ -426,7 +432,7 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
         }
         pf_pos = pf_next;
         __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of chunk c+1 have landed
-        if (wave == 0 && c + 1 <= c1) set_queries(c + 1);
+        if (dw == 0 && c + 1 <= c1) set_queries(c + 1);
         __syncthreads();                // ... and every wave is done with step c
     }
 }
