@@ -9,7 +9,7 @@
 //   2. scan:    exclusive scan of the counts in (bucket, tile) order gives
 //               every (bucket, tile) pair its first output slot, and the
 //               bucket start offsets.
-//   3. scatter: each wave ranks its quarter of a tile in position order; the
+//   3. scatter: each of eight waves ranks its eighth of a tile in position order; the
 //               rank of a position among equal buckets of its 64-lane group
 //               is the count of lower lanes with the same bucket, whose lane
 //               mask comes from one ballot per bucket-id bit, so equal keys
