@@ -13,7 +13,9 @@
 //               rank of a position among equal buckets of its 64-lane group
 //               is the count of lower lanes with the same bucket, whose lane
 //               mask comes from one ballot per bucket-id bit, so equal keys
-//               keep their position order (stable).
+//               keep their position order (stable).  undo is written in
+//               position order; perm is first put in the tile's sorted
+//               order in LDS and written from there, run by run.
 #include "common.h"
 #include "launch.h"
 
@@ -25,7 +27,6 @@ namespace {
 constexpr int kTile = 4096;
 constexpr int kSortWaves = 8;
 constexpr int kPerWave = kTile / kSortWaves;
-constexpr int kOffPerThread = (1024 + kSortWaves * 64 - 1) / (kSortWaves * 64);  // n_b <= 1024
 constexpr int kHistLdsInts = 8192;
 
 __device__ __forceinline__ int clamp_bucket(int b, int n_b) { return min(max(b, 0), n_b - 1); }
@@ -153,8 +154,13 @@ __global__ __launch_bounds__(256) void sort_scan_kernel(int32_t* __restrict__ co
     if (threadIdx.x == 0) bs[n_b] = L;
 }
 
-// LDS of the scatter: per-wave next slot of every bucket [kSortWaves][n_b].
-size_t scatter_lds_bytes(int n_b) { return (size_t)kSortWaves * n_b * sizeof(int); }
+// LDS of the scatter: per-wave next slot of every bucket [kSortWaves][n_b],
+// the tile's (first global slot - first local slot) of every bucket [n_b],
+// the tile in sorted order [kTile], and the waves' sums of the bucket scan.
+constexpr int kScatterBucketsPerThread = (1024 + kSortWaves * 64 - 1) / (kSortWaves * 64);
+size_t scatter_lds_bytes(int n_b) {
+    return (size_t)(kSortWaves + 1) * n_b * sizeof(int) + kTile * sizeof(uint32_t) + kSortWaves * sizeof(int);
+}
 
 __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int32_t* __restrict__ buckets,
                                                            const int32_t* __restrict__ offsets,
@@ -162,12 +168,15 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
                                                            int n_tiles, int32_t* __restrict__ perm,
                                                            int32_t* __restrict__ undo) {
     extern __shared__ int smem[];
-    int* base = smem;  // [kSortWaves][n_b]
+    int* base = smem;                      // [kSortWaves][n_b]
+    int* delta = base + kSortWaves * n_b;  // [n_b]
+    uint32_t* staged = reinterpret_cast<uint32_t*>(delta + n_b);  // [kTile]: bucket << 16 | position in tile
+    int* wsum = reinterpret_cast<int*>(staged + kTile);           // [kSortWaves]
     // Workgroup b of the launch runs on XCD b % 8 (round-robin dispatch).
     // Each XCD is given a contiguous run of (segment, tile) items, so the
-    // tiles of a segment write their scattered 4-byte slots into the same
-    // XCD's L2, which merges them into whole lines before they reach HBM,
-    // and the rounds of one (batch, head) read its bucket ids through one L2.
+    // tiles of a segment write their perm runs into the same XCD's L2, which
+    // merges them into whole lines before they reach HBM, and the rounds of
+    // one (batch, head) read its bucket ids through one L2.
     const int64_t nblk = (int64_t)gridDim.x * gridDim.y;
     const int64_t bid = blockIdx.x + (int64_t)blockIdx.y * gridDim.x;
     const int64_t item = nblk % 8 == 0 ? (bid % 8) * (nblk / 8) + bid / 8 : bid;
@@ -179,7 +188,9 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
     int* wbase = base + wave * n_b;
 
     for (int i = threadIdx.x; i < kSortWaves * n_b; i += blockDim.x) smem[i] = 0;
-    const int p0 = tile * kTile + wave * kPerWave;
+    const int t0 = tile * kTile;
+    const int n_tile = min(kTile, L - t0);
+    const int p0 = t0 + wave * kPerWave;
     const int p1 = min(L, p0 + kPerWave);
     // this lane's ids, all loads in flight at once (kPerWave / 64 per lane);
     // positions past the segment load a valid id that is never used, so the
@@ -191,11 +202,13 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
         const int pos = min(max(p0 + 64 * it + lane, 0), max(p1 - 1, 0));
         ids[it] = buckets[(bh * L + pos) * n_r + r];
     }
-    // the tile's first slot of every bucket this thread sets up below
-    int off_pre[kOffPerThread];
+    // the tile's first global slot of each of this thread's (consecutive)
+    // buckets, loaded with the ids
+    const int b0 = (int)threadIdx.x * kScatterBucketsPerThread;
+    int goff[kScatterBucketsPerThread];
 #pragma unroll
-    for (int k = 0; k < kOffPerThread; ++k)
-        off_pre[k] = offsets[(seg * n_tiles + tile) * n_b + min((int)threadIdx.x + k * kSortWaves * 64, n_b - 1)];
+    for (int k = 0; k < kScatterBucketsPerThread; ++k)
+        goff[k] = offsets[(seg * n_tiles + tile) * n_b + min(b0 + k, n_b - 1)];
 #pragma unroll
     for (int it = 0; it < kIter; ++it) ids[it] = clamp_bucket(ids[it], n_b);
     __syncthreads();
@@ -203,19 +216,44 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
     for (int it = 0; it < kIter; ++it)
         if (p0 + 64 * it + lane < p1) atomicAdd(&wbase[ids[it]], 1);
     __syncthreads();
-    // Per-wave starting slot of every bucket: the tile's offset (loaded with
-    // the ids) plus the counts of the earlier waves of this tile.
+    // Per-wave starting slot of every bucket: the tile's first slot plus the
+    // counts of the earlier waves of this tile; and the tile's count of the
+    // thread's buckets, whose exclusive scan over the workgroup (thread order
+    // is bucket order) is each bucket's first slot in the tile's own sorted
+    // order.
+    int cnt[kScatterBucketsPerThread];
+    int tot = 0;
 #pragma unroll
-    for (int k = 0; k < kOffPerThread; ++k) {
-        const int b = threadIdx.x + k * kSortWaves * 64;
-        if (b >= n_b) break;
-        int off = off_pre[k];
-        for (int w = 0; w < kSortWaves; ++w) {
-            const int cnt = base[w * n_b + b];
-            base[w * n_b + b] = off;
-            off += cnt;
+    for (int k = 0; k < kScatterBucketsPerThread; ++k) {
+        const int b = b0 + k;
+        cnt[k] = 0;
+        if (b < n_b) {
+            int off = goff[k];
+            for (int w = 0; w < kSortWaves; ++w) {
+                const int c = base[w * n_b + b];
+                base[w * n_b + b] = off;
+                off += c;
+            }
+            cnt[k] = off - goff[k];
         }
+        tot += cnt[k];
     }
+    int incl = tot;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    int local = incl - tot;
+    for (int w = 0; w < wave; ++w) local += wsum[w];
+#pragma unroll
+    for (int k = 0; k < kScatterBucketsPerThread; ++k)
+        if (b0 + k < n_b) {
+            delta[b0 + k] = goff[k] - local;
+            local += cnt[k];
+        }
     __syncthreads();
 
     // Rank of a position among the equal buckets of its 64-lane group: the
@@ -223,7 +261,9 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
     // ballot of lanes agreeing on that bit (ids are below n_b <= 1024), and
     // the rank counts those below the lane, so equal keys keep their
     // position order.  The highest lane of each bucket moves the bucket's
-    // next slot on (the wave's LDS operations run in order).
+    // next slot on (the wave's LDS operations run in order).  undo is
+    // written here, in position order; perm goes to the tile's sorted copy
+    // in LDS first.
     int32_t* pseg = perm + seg * L;
     int32_t* useg = undo + seg * L;
     const int id_bits = 32 - __clz(max(n_b - 1, 1));
@@ -233,6 +273,7 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
         const bool active = pos < p1;
         const int b = ids[it];
         const int start = wbase[b];
+        const int d = delta[b];
         uint64_t peers = __ballot(active);
         for (int bit = 0; bit < id_bits; ++bit) {
             const bool one = (b >> bit) & 1;
@@ -243,10 +284,23 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u));
         if (active) {
             const int slot = start + before;
-            pseg[slot] = pos;
+            staged[min(max(slot - d, 0), kTile - 1)] = ((uint32_t)b << 16) | (uint32_t)(pos - t0);
             useg[pos] = slot;
             if ((peers >> lane) == 1ull) wbase[b] = start + __popcll(peers);
         }
+    }
+    __syncthreads();
+    // The tile in sorted order: consecutive entries of one bucket go to
+    // consecutive slots, so each wave's stores cover a few runs of whole
+    // words instead of one scattered word per lane.
+    constexpr int kOut = kTile / (kSortWaves * 64);
+    uint32_t e[kOut];
+#pragma unroll
+    for (int k = 0; k < kOut; ++k) e[k] = staged[threadIdx.x + k * kSortWaves * 64];
+#pragma unroll
+    for (int k = 0; k < kOut; ++k) {
+        const int j = threadIdx.x + k * kSortWaves * 64;
+        if (j < n_tile) pseg[min(max(delta[e[k] >> 16] + j, 0), L - 1)] = t0 + (int)(e[k] & 0xFFFFu);
     }
 }
 
@@ -317,8 +371,11 @@ hipError_t launch_sort(int64_t BH, int L, int n_rounds, int n_buckets, const int
         buckets, L, n_rounds, n_buckets, rpg, n_tiles, counts);
     sort_scan_kernel<<<(unsigned)(BH * n_rounds), 256, 0, stream>>>(counts, L, n_buckets, n_tiles,
                                                                     bucket_start);
-    sort_scatter_kernel<<<dim3(n_tiles, (unsigned)(BH * n_rounds)), kSortWaves * 64, scatter_lds_bytes(n_buckets),
-                          stream>>>(
+    const size_t lds = scatter_lds_bytes(n_buckets);
+    if (lds > 65536)
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&sort_scatter_kernel),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    sort_scatter_kernel<<<dim3(n_tiles, (unsigned)(BH * n_rounds)), kSortWaves * 64, lds, stream>>>(
         buckets, counts, L, n_rounds, n_buckets, n_tiles, perm, undo);
     return hipGetLastError();
 }
