@@ -154,12 +154,16 @@ __global__ __launch_bounds__(256) void sort_scan_kernel(int32_t* __restrict__ co
     if (threadIdx.x == 0) bs[n_b] = L;
 }
 
-// LDS of the scatter: per-wave next slot of every bucket [kSortWaves][n_b],
-// the tile's (first global slot - first local slot) of every bucket [n_b],
+// LDS of the scatter: per-wave next local slot of every bucket as 16-bit
+// fields [kSortWaves][n_b rounded up to even] (slots in a tile stay below
+// 2^16), the tile's (first global slot - first local slot) of every bucket,
 // the tile in sorted order [kTile], and the waves' sums of the bucket scan.
-constexpr int kScatterBucketsPerThread = (1024 + kSortWaves * 64 - 1) / (kSortWaves * 64);
+// At 1024 buckets this is 36 KB, four workgroups per CU.
+constexpr int kScatterBucketsPerThread = 2;  // one 32-bit word of 16-bit fields; n_b <= 2 * kSortWaves * 64
+__host__ __device__ inline int even_buckets(int n_b) { return (n_b + 1) & ~1; }
 size_t scatter_lds_bytes(int n_b) {
-    return (size_t)(kSortWaves + 1) * n_b * sizeof(int) + kTile * sizeof(uint32_t) + kSortWaves * sizeof(int);
+    return (size_t)kSortWaves * even_buckets(n_b) * sizeof(uint16_t) + even_buckets(n_b) * sizeof(int) +
+           kTile * sizeof(uint32_t) + kSortWaves * sizeof(int);
 }
 
 __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int32_t* __restrict__ buckets,
@@ -168,10 +172,11 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
                                                            int n_tiles, int32_t* __restrict__ perm,
                                                            int32_t* __restrict__ undo) {
     extern __shared__ int smem[];
-    int* base = smem;                      // [kSortWaves][n_b]
-    int* delta = base + kSortWaves * n_b;  // [n_b]
-    uint32_t* staged = reinterpret_cast<uint32_t*>(delta + n_b);  // [kTile]: bucket << 16 | position in tile
-    int* wsum = reinterpret_cast<int*>(staged + kTile);           // [kSortWaves]
+    const int half = even_buckets(n_b) / 2;  // 32-bit words per wave's row
+    uint32_t* base = reinterpret_cast<uint32_t*>(smem);  // [kSortWaves][half], two 16-bit fields each
+    int* delta = smem + kSortWaves * half;                // [2 * half]
+    uint32_t* staged = reinterpret_cast<uint32_t*>(delta + 2 * half);  // [kTile]: bucket << 16 | position in tile
+    int* wsum = reinterpret_cast<int*>(staged + kTile);                 // [kSortWaves]
     // Workgroup b of the launch runs on XCD b % 8 (round-robin dispatch).
     // Each XCD is given a contiguous run of (segment, tile) items, so the
     // tiles of a segment write their perm runs into the same XCD's L2, which
@@ -185,9 +190,10 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
     const int64_t bh = seg / n_r;
     const int r = (int)(seg % n_r);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int* wbase = base + wave * n_b;
+    uint32_t* wrow = base + wave * half;
+    uint16_t* wslot = reinterpret_cast<uint16_t*>(wrow);
 
-    for (int i = threadIdx.x; i < kSortWaves * n_b; i += blockDim.x) smem[i] = 0;
+    for (int i = threadIdx.x; i < kSortWaves * half; i += blockDim.x) base[i] = 0;
     const int t0 = tile * kTile;
     const int n_tile = min(kTile, L - t0);
     const int p0 = t0 + wave * kPerWave;
@@ -202,8 +208,8 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
         const int pos = min(max(p0 + 64 * it + lane, 0), max(p1 - 1, 0));
         ids[it] = buckets[(bh * L + pos) * n_r + r];
     }
-    // the tile's first global slot of each of this thread's (consecutive)
-    // buckets, loaded with the ids
+    // the tile's first global slot of this thread's two buckets, loaded
+    // with the ids
     const int b0 = (int)threadIdx.x * kScatterBucketsPerThread;
     int goff[kScatterBucketsPerThread];
 #pragma unroll
@@ -212,32 +218,26 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
 #pragma unroll
     for (int it = 0; it < kIter; ++it) ids[it] = clamp_bucket(ids[it], n_b);
     __syncthreads();
+    // per-wave counts (a wave holds at most kPerWave < 2^16 of a bucket)
 #pragma unroll
     for (int it = 0; it < kIter; ++it)
-        if (p0 + 64 * it + lane < p1) atomicAdd(&wbase[ids[it]], 1);
+        if (p0 + 64 * it + lane < p1) atomicAdd(&wrow[ids[it] >> 1], 1u << ((ids[it] & 1) << 4));
     __syncthreads();
-    // Per-wave starting slot of every bucket: the tile's first slot plus the
-    // counts of the earlier waves of this tile; and the tile's count of the
-    // thread's buckets, whose exclusive scan over the workgroup (thread order
-    // is bucket order) is each bucket's first slot in the tile's own sorted
-    // order.
-    int cnt[kScatterBucketsPerThread];
-    int tot = 0;
+    // The tile's count of the thread's two buckets (one word of every
+    // wave's row), whose exclusive scan over the workgroup (thread order is
+    // bucket order) is each bucket's first slot in the tile's own sorted
+    // order; then every wave's first local slot of the two buckets: that
+    // plus the counts of the earlier waves of this tile.
+    const bool owner = b0 < n_b;
+    uint32_t word[kSortWaves];
+    uint32_t c_lo = 0, c_hi = 0;
 #pragma unroll
-    for (int k = 0; k < kScatterBucketsPerThread; ++k) {
-        const int b = b0 + k;
-        cnt[k] = 0;
-        if (b < n_b) {
-            int off = goff[k];
-            for (int w = 0; w < kSortWaves; ++w) {
-                const int c = base[w * n_b + b];
-                base[w * n_b + b] = off;
-                off += c;
-            }
-            cnt[k] = off - goff[k];
-        }
-        tot += cnt[k];
+    for (int w = 0; w < kSortWaves; ++w) {
+        word[w] = owner ? base[w * half + threadIdx.x] : 0u;
+        c_lo += word[w] & 0xFFFFu;
+        c_hi += word[w] >> 16;
     }
+    const int tot = (int)(c_lo + c_hi);
     int incl = tot;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
@@ -248,17 +248,22 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
     __syncthreads();
     int local = incl - tot;
     for (int w = 0; w < wave; ++w) local += wsum[w];
+    if (owner) {
+        uint32_t run_lo = (uint32_t)local, run_hi = (uint32_t)local + c_lo;
+        delta[b0] = goff[0] - (int)run_lo;
+        delta[b0 + 1] = goff[1] - (int)run_hi;
 #pragma unroll
-    for (int k = 0; k < kScatterBucketsPerThread; ++k)
-        if (b0 + k < n_b) {
-            delta[b0 + k] = goff[k] - local;
-            local += cnt[k];
+        for (int w = 0; w < kSortWaves; ++w) {
+            base[w * half + threadIdx.x] = run_lo | (run_hi << 16);
+            run_lo += word[w] & 0xFFFFu;
+            run_hi += word[w] >> 16;
         }
+    }
     __syncthreads();
 
     // Rank of a position among the equal buckets of its 64-lane group: the
-    // lanes holding the same bucket are the AND over the id's bits of the
-    // ballot of lanes agreeing on that bit (ids are below n_b <= 1024), and
+    // lanes holding the same bucket are those agreeing with it on every bit
+    // of the id (one ballot per bit; ids are below n_b <= 1024), and
     // the rank counts those below the lane, so equal keys keep their
     // position order.  The highest lane of each bucket moves the bucket's
     // next slot on (the wave's LDS operations run in order).  undo is
@@ -266,27 +271,32 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
     // in LDS first.
     int32_t* pseg = perm + seg * L;
     int32_t* useg = undo + seg * L;
-    const int id_bits = 32 - __clz(max(n_b - 1, 1));
+    constexpr int kIdBits = 10;  // ids below n_b <= 1024
 #pragma unroll
     for (int it = 0; it < kIter; ++it) {
         const int pos = p0 + 64 * it + lane;
         const bool active = pos < p1;
         const int b = ids[it];
-        const int start = wbase[b];
+        const int start = wslot[b];
         const int d = delta[b];
-        uint64_t peers = __ballot(active);
-        for (int bit = 0; bit < id_bits; ++bit) {
-            const bool one = (b >> bit) & 1;
-            const uint64_t ones = __ballot(one);
-            peers &= one ? ones : ~ones;
+        // lanes differing from this one in some bit: for every bit, the
+        // ballot of the bit xor this lane's bit spread over the word
+        uint32_t diff_lo = 0, diff_hi = 0;
+#pragma unroll
+        for (int bit = 0; bit < kIdBits; ++bit) {
+            const uint32_t spread = (uint32_t)__builtin_amdgcn_sbfe(b, bit, 1);  // 0 or all ones
+            const uint64_t ones = __ballot(spread != 0u);
+            diff_lo |= (uint32_t)ones ^ spread;
+            diff_hi |= (uint32_t)(ones >> 32) ^ spread;
         }
+        const uint64_t peers = __ballot(active) & ~(((uint64_t)diff_hi << 32) | diff_lo);
         const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(peers >> 32),
                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u));
         if (active) {
-            const int slot = start + before;
-            staged[min(max(slot - d, 0), kTile - 1)] = ((uint32_t)b << 16) | (uint32_t)(pos - t0);
-            useg[pos] = slot;
-            if ((peers >> lane) == 1ull) wbase[b] = start + __popcll(peers);
+            const int slot = start + before;  // in the tile's sorted order
+            staged[min(slot, kTile - 1)] = ((uint32_t)b << 16) | (uint32_t)(pos - t0);
+            useg[pos] = slot + d;
+            if ((peers >> lane) == 1ull) wslot[b] = (uint16_t)(start + __popcll(peers));
         }
     }
     __syncthreads();
