@@ -87,68 +87,84 @@ __global__ __launch_bounds__(kHistThreads) void sort_hist_kernel(const int32_t* 
     }
 }
 
-// Counts of a segment are [tile][bucket].  Each thread owns up to four
-// consecutive buckets and holds their counts for up to kScanTiles tiles in
-// registers (all loads in flight together), so the scan costs one round trip
-// to memory; the threads' sums are scanned in LDS, and every (bucket, tile)
-// count is replaced by its first output slot in (bucket, tile) order.
+// Counts of a segment are [tile][bucket]; the scan replaces every count by
+// its first output slot in (bucket, tile) order and writes the bucket start
+// offsets.  Up to 16 tiles (L <= 65536) and 1024 buckets: one thread per
+// bucket holds its counts for every tile in registers (all loads in flight
+// together), the threads' sums are scanned across each wave with shuffles
+// and across the waves in LDS, so the scan costs one round trip to memory.
 constexpr int kScanTiles = 16;
-constexpr int kScanBuckets = 4;  // n_buckets <= 1024 over 256 threads
+constexpr int kScanThreads = 1024;
 
-__global__ __launch_bounds__(256) void sort_scan_kernel(int32_t* __restrict__ counts, int L,
-                                                        int n_b, int n_tiles,
-                                                        int32_t* __restrict__ bucket_start) {
+__global__ __launch_bounds__(kScanThreads) void sort_scan_kernel(int32_t* __restrict__ counts, int L, int n_b,
+                                                                 int n_tiles, int32_t* __restrict__ bucket_start) {
+    __shared__ int wsum[kScanThreads / 64];
+    const int64_t seg = blockIdx.x;
+    int32_t* c = counts + seg * (int64_t)n_b * n_tiles;
+    int32_t* bs = bucket_start + seg * (n_b + 1);
+    const int b = threadIdx.x, lane = b & 63, wave = b >> 6;
+    const bool owner = b < n_b;
+    const int bl = min(b, n_b - 1);
+    int v[kScanTiles];
+#pragma unroll
+    for (int t = 0; t < kScanTiles; ++t) v[t] = c[(int64_t)min(t, n_tiles - 1) * n_b + bl];
+    int sum = 0;
+#pragma unroll
+    for (int t = 0; t < kScanTiles; ++t) {
+        if (t >= n_tiles || !owner) v[t] = 0;
+        sum += v[t];
+    }
+    int incl = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    int run = incl - sum;
+    for (int w = 0; w < wave; ++w) run += wsum[w];
+    if (owner) {
+        bs[b] = run;
+#pragma unroll
+        for (int t = 0; t < kScanTiles; ++t)
+            if (t < n_tiles) {
+                c[(int64_t)t * n_b + b] = run;
+                run += v[t];
+            }
+    }
+    if (b == 0) bs[n_b] = L;
+}
+
+// The same for any number of tiles and buckets: each of 256 threads owns a
+// run of consecutive buckets and walks their tiles twice.
+__global__ __launch_bounds__(256) void sort_scan_any_kernel(int32_t* __restrict__ counts, int L, int n_b,
+                                                            int n_tiles, int32_t* __restrict__ bucket_start) {
     __shared__ int part[256];
     const int64_t seg = blockIdx.x;
     int32_t* c = counts + seg * (int64_t)n_b * n_tiles;
     int32_t* bs = bucket_start + seg * (n_b + 1);
     const int per = (n_b + 255) / 256;
     const int b0 = min(n_b, (int)threadIdx.x * per), b1 = min(n_b, b0 + per);
-    auto scan_threads = [&](int s) {  // exclusive prefix of the threads' sums
-        part[threadIdx.x] = s;
+    int s = 0;
+    for (int b = b0; b < b1; ++b)
+        for (int t = 0; t < n_tiles; ++t) s += c[(int64_t)t * n_b + b];
+    // exclusive prefix of the threads' sums
+    part[threadIdx.x] = s;
+    __syncthreads();
+    for (int o = 1; o < 256; o <<= 1) {
+        const int x = (int)threadIdx.x >= o ? part[threadIdx.x - o] : 0;
         __syncthreads();
-        for (int o = 1; o < 256; o <<= 1) {
-            const int x = (int)threadIdx.x >= o ? part[threadIdx.x - o] : 0;
-            __syncthreads();
-            part[threadIdx.x] += x;
-            __syncthreads();
-        }
-        return part[threadIdx.x] - s;
-    };
-    if (n_tiles <= kScanTiles && per <= kScanBuckets) {
-        int v[kScanBuckets][kScanTiles];
-        int s = 0;
-#pragma unroll
-        for (int t = 0; t < kScanTiles; ++t)
-#pragma unroll
-            for (int bi = 0; bi < kScanBuckets; ++bi) {
-                v[bi][t] = (t < n_tiles && b0 + bi < b1) ? c[(int64_t)t * n_b + b0 + bi] : 0;
-                s += v[bi][t];
-            }
-        int run = scan_threads(s);
-#pragma unroll
-        for (int bi = 0; bi < kScanBuckets; ++bi)
-            if (b0 + bi < b1) {
-                bs[b0 + bi] = run;
-#pragma unroll
-                for (int t = 0; t < kScanTiles; ++t)
-                    if (t < n_tiles) {
-                        c[(int64_t)t * n_b + b0 + bi] = run;
-                        run += v[bi][t];
-                    }
-            }
-    } else {
-        int s = 0;
-        for (int b = b0; b < b1; ++b)
-            for (int t = 0; t < n_tiles; ++t) s += c[(int64_t)t * n_b + b];
-        int run = scan_threads(s);
-        for (int b = b0; b < b1; ++b) {
-            bs[b] = run;
-            for (int t = 0; t < n_tiles; ++t) {
-                const int x = c[(int64_t)t * n_b + b];
-                c[(int64_t)t * n_b + b] = run;
-                run += x;
-            }
+        part[threadIdx.x] += x;
+        __syncthreads();
+    }
+    int run = part[threadIdx.x] - s;
+    for (int b = b0; b < b1; ++b) {
+        bs[b] = run;
+        for (int t = 0; t < n_tiles; ++t) {
+            const int x = c[(int64_t)t * n_b + b];
+            c[(int64_t)t * n_b + b] = run;
+            run += x;
         }
     }
     if (threadIdx.x == 0) bs[n_b] = L;
@@ -379,8 +395,12 @@ hipError_t launch_sort(int64_t BH, int L, int n_rounds, int n_buckets, const int
 
     sort_hist_kernel<<<dim3(n_tiles, (unsigned)BH, groups), kHistThreads, rpg * n_buckets * sizeof(int), stream>>>(
         buckets, L, n_rounds, n_buckets, rpg, n_tiles, counts);
-    sort_scan_kernel<<<(unsigned)(BH * n_rounds), 256, 0, stream>>>(counts, L, n_buckets, n_tiles,
-                                                                    bucket_start);
+    if (n_tiles <= kScanTiles && n_buckets <= kScanThreads)
+        sort_scan_kernel<<<(unsigned)(BH * n_rounds), kScanThreads, 0, stream>>>(counts, L, n_buckets, n_tiles,
+                                                                                 bucket_start);
+    else
+        sort_scan_any_kernel<<<(unsigned)(BH * n_rounds), 256, 0, stream>>>(counts, L, n_buckets, n_tiles,
+                                                                            bucket_start);
     const size_t lds = scatter_lds_bytes(n_buckets);
     if (lds > 65536)
         (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&sort_scatter_kernel),
