@@ -26,10 +26,14 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
 
 // ---- counting sort and row gather ----
 int sort_tile_positions(int L);
+// Workspace of launch_sort: the per-tile bucket counts, plus, when
+// round_major_ids is set, a 16-bit copy of the ids in [segment][position]
+// order (sort_workspace_bytes covers both, sort_counts_bytes the counts).
+size_t sort_counts_bytes(int64_t BH, int L, int n_rounds, int n_buckets);
 size_t sort_workspace_bytes(int64_t BH, int L, int n_rounds, int n_buckets);
 hipError_t launch_sort(int64_t BH, int L, int n_rounds, int n_buckets, const int32_t* buckets,
                        int32_t* perm, int32_t* undo, int32_t* bucket_start, void* workspace,
-                       hipStream_t stream);
+                       bool round_major_ids, hipStream_t stream);
 // The fixed scratch array of lsh_sort_permute_static (sort.hip): its size,
 // and its device address on the current device (looked up on the first call
 // on each device).

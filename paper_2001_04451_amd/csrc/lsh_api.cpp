@@ -204,7 +204,7 @@ int lsh_sort_permute(const lsh_config* cfg, const int32_t* buckets, int32_t* per
         return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
     return status_of(lsh::launch_sort(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets, buckets,
-                                      perm, undo, bucket_start, workspace,
+                                      perm, undo, bucket_start, workspace, true,
                                       static_cast<hipStream_t>(stream)));
 }
 
@@ -213,14 +213,14 @@ int lsh_sort_permute_static(const lsh_config* cfg, const int32_t* buckets, int32
     LSH_TRY(check_config(cfg));
     if (!buckets || !perm || !undo || !bucket_start) return LSH_ERR_INVALID;
     LSH_TRY(check_supported(cfg));
-    if (lsh::sort_workspace_bytes(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets) >
-        lsh::kSortScratchBytes)
+    if (lsh::sort_counts_bytes(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets) > lsh::kSortScratchBytes)
         return LSH_ERR_UNSUPPORTED;
     void* scratch = nullptr;
     LSH_TRY(status_of(lsh::sort_static_scratch(&scratch)));
-    // the counts are written in full by every call: nothing needs clearing
+    // the counts are written in full by every call: nothing needs clearing;
+    // the scatter reads the ids where they are (no 16-bit copy in scratch)
     return status_of(lsh::launch_sort(bh_of(cfg), cfg->L, cfg->n_rounds, cfg->n_buckets, buckets,
-                                      perm, undo, bucket_start, scratch,
+                                      perm, undo, bucket_start, scratch, false,
                                       static_cast<hipStream_t>(stream)));
 }
 

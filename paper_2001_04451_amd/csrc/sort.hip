@@ -5,7 +5,10 @@
 //
 // A segment of L positions is cut into tiles of kTile positions.
 //   1. hist:    per (tile, round) bucket counts, LDS atomics; stored
-//               [segment][tile][bucket].
+//               [segment][tile][bucket].  With a workspace it also writes
+//               the ids once more, one round after another as 16-bit values
+//               ([segment][position]), so that the scatter reads them
+//               coalesced instead of one 4-byte word in every n_r.
 //   2. scan:    exclusive scan of the counts in (bucket, tile) order gives
 //               every (bucket, tile) pair its first output slot, and the
 //               bucket start offsets.
@@ -40,7 +43,8 @@ constexpr int kHistMaxRounds = 16;
 
 __global__ __launch_bounds__(kHistThreads) void sort_hist_kernel(const int32_t* __restrict__ buckets, int L,
                                                         int n_r, int n_b, int rounds_per_group,
-                                                        int n_tiles, int32_t* __restrict__ counts) {
+                                                        int n_tiles, int32_t* __restrict__ counts,
+                                                        uint16_t* __restrict__ ids16) {
     extern __shared__ int hist[];
     const int tile = blockIdx.x;
     const int64_t bh = blockIdx.y;
@@ -80,6 +84,18 @@ __global__ __launch_bounds__(kHistThreads) void sort_hist_kernel(const int32_t* 
             for (int r = 0; r < kHistMaxRounds; ++r)
                 if (r < nr) atomicAdd(&hist[r * n_b + clamp_bucket(ids[k][r], n_b)], 1);
         }
+    // the ids again, one round after another as 16-bit values, for the scatter's coalesced reads
+    if (ids16) {
+#pragma unroll
+        for (int k = 0; k < kHistRows; ++k) {
+            const int p = p0 + (int)threadIdx.x + kHistThreads * k;
+            if (p < p1) {
+#pragma unroll
+                for (int r = 0; r < kHistMaxRounds; ++r)
+                    if (r < nr) ids16[(bh * n_r + r0 + r) * L + p] = (uint16_t)clamp_bucket(ids[k][r], n_b);
+            }
+        }
+    }
     __syncthreads();
     for (int i = threadIdx.x; i < nr * n_b; i += blockDim.x) {
         const int r = r0 + i / n_b, b = i % n_b;
@@ -182,7 +198,9 @@ size_t scatter_lds_bytes(int n_b) {
            kTile * sizeof(uint32_t) + kSortWaves * sizeof(int);
 }
 
+template <bool IDS16>
 __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int32_t* __restrict__ buckets,
+                                                           const uint16_t* __restrict__ ids16,
                                                            const int32_t* __restrict__ offsets,
                                                            int L, int n_r, int n_b,
                                                            int n_tiles, int32_t* __restrict__ perm,
@@ -222,7 +240,7 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
 #pragma unroll
     for (int it = 0; it < kIter; ++it) {
         const int pos = min(max(p0 + 64 * it + lane, 0), max(p1 - 1, 0));
-        ids[it] = buckets[(bh * L + pos) * n_r + r];
+        ids[it] = IDS16 ? (int)ids16[seg * L + pos] : buckets[(bh * L + pos) * n_r + r];
     }
     // the tile's first global slot of this thread's two buckets, loaded
     // with the ids
@@ -379,34 +397,41 @@ hipError_t sort_static_scratch(void** ptr) {
     return hipSuccess;
 }
 
-size_t sort_workspace_bytes(int64_t BH, int L, int n_rounds, int n_buckets) {
+size_t sort_counts_bytes(int64_t BH, int L, int n_rounds, int n_buckets) {
     const int64_t n_tiles = (L + kTile - 1) / kTile;
     return align256((size_t)(BH * n_rounds * n_buckets * n_tiles) * sizeof(int32_t));
+}
+size_t sort_workspace_bytes(int64_t BH, int L, int n_rounds, int n_buckets) {
+    return sort_counts_bytes(BH, L, n_rounds, n_buckets) + align256((size_t)BH * n_rounds * L * sizeof(uint16_t));
 }
 
 hipError_t launch_sort(int64_t BH, int L, int n_rounds, int n_buckets, const int32_t* buckets,
                        int32_t* perm, int32_t* undo, int32_t* bucket_start, void* workspace,
-                       hipStream_t stream) {
+                       bool round_major_ids, hipStream_t stream) {
     if (BH == 0 || L == 0) return hipSuccess;
     const int n_tiles = (L + kTile - 1) / kTile;
     int32_t* counts = static_cast<int32_t*>(workspace);
+    uint16_t* ids16 = round_major_ids ? reinterpret_cast<uint16_t*>(static_cast<char*>(workspace) +
+                                                                     sort_counts_bytes(BH, L, n_rounds, n_buckets))
+                                      : nullptr;
     const int rpg = std::max(1, std::min(n_rounds, kHistLdsInts / n_buckets));
     const int groups = (n_rounds + rpg - 1) / rpg;
 
     sort_hist_kernel<<<dim3(n_tiles, (unsigned)BH, groups), kHistThreads, rpg * n_buckets * sizeof(int), stream>>>(
-        buckets, L, n_rounds, n_buckets, rpg, n_tiles, counts);
+        buckets, L, n_rounds, n_buckets, rpg, n_tiles, counts, ids16);
     if (n_tiles <= kScanTiles && n_buckets <= kScanThreads)
         sort_scan_kernel<<<(unsigned)(BH * n_rounds), kScanThreads, 0, stream>>>(counts, L, n_buckets, n_tiles,
                                                                                  bucket_start);
     else
         sort_scan_any_kernel<<<(unsigned)(BH * n_rounds), 256, 0, stream>>>(counts, L, n_buckets, n_tiles,
                                                                             bucket_start);
-    const size_t lds = scatter_lds_bytes(n_buckets);
-    if (lds > 65536)
-        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&sort_scatter_kernel),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    sort_scatter_kernel<<<dim3(n_tiles, (unsigned)(BH * n_rounds)), kSortWaves * 64, lds, stream>>>(
-        buckets, counts, L, n_rounds, n_buckets, n_tiles, perm, undo);
+    const dim3 grid(n_tiles, (unsigned)(BH * n_rounds));
+    if (ids16)
+        sort_scatter_kernel<true><<<grid, kSortWaves * 64, scatter_lds_bytes(n_buckets), stream>>>(
+            buckets, ids16, counts, L, n_rounds, n_buckets, n_tiles, perm, undo);
+    else
+        sort_scatter_kernel<false><<<grid, kSortWaves * 64, scatter_lds_bytes(n_buckets), stream>>>(
+            buckets, ids16, counts, L, n_rounds, n_buckets, n_tiles, perm, undo);
     return hipGetLastError();
 }
 
