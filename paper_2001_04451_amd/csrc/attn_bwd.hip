@@ -491,59 +491,80 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t* __restric
 // dq, dv of a position: the sum of its per-round partials (each at the
 // token's slot undo[i] of its round, fixed round order, each fp16 row times
 // 2^e), plus dO for a token whose only target in every round was itself.
+// Sixteen lanes take kReduceRows adjacent positions (two up to four rounds,
+// where the registers allow it at full occupancy; else one), four values of
+// each row per lane, with every load of those rows in flight together.
 // NRL: n_r rounded up to a power of two; rounds past n_r read round 0 with
 // weight 0, so the loads are unconditional.
+template <int NRL>
+constexpr int reduce_rows() { return NRL <= 4 ? 2 : 1; }
+
 template <int NRL>
 __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     const uint16_t* __restrict__ dout, const float* __restrict__ lse_total,
     const uint16_t* __restrict__ part_q, const uint16_t* __restrict__ part_v,
     const uint8_t* __restrict__ part_e, const int32_t* __restrict__ undo, int64_t rows, int L,
     int n_r, float self_mask, float* __restrict__ dq, float* __restrict__ dv) {
-    const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
+    constexpr int kReduceRows = reduce_rows<NRL>();
+    const int64_t row0 = (((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4) * kReduceRows;
     const int part = threadIdx.x & 15;
-    if (row >= rows) return;  // whole 16-lane groups leave together
-    const int64_t bh = row / L, i = row % L;
+    if (row0 >= rows) return;  // whole 16-lane groups leave together
     const int64_t rr_total = rows * n_r;  // offset of the dv exponents
-    int64_t sbase[NRL];
-    int slot[NRL];
+    int64_t sbase[kReduceRows][NRL];
+    int slot[kReduceRows][NRL];
+    float z[kReduceRows];
 #pragma unroll
-    for (int rr = 0; rr < NRL; ++rr) {
-        sbase[rr] = (bh * n_r + (rr < n_r ? rr : 0)) * L;
-        slot[rr] = min(max(undo[sbase[rr] + i], 0), L - 1);
-    }
-    uint2 xq[NRL], xv[NRL];
-    uint32_t eq[NRL], ev[NRL];
+    for (int k = 0; k < kReduceRows; ++k) {
+        const int64_t row = min(row0 + k, rows - 1);  // past the end: a valid row, never stored
+        const int64_t bh = row / L, i = row % L;
+        z[k] = lse_total[row];
 #pragma unroll
-    for (int rr = 0; rr < NRL; ++rr) {
-        const int64_t prow = sbase[rr] + slot[rr];
-        xq[rr] = *reinterpret_cast<const uint2*>(part_q + prow * kHeadDim + part * 4);
-        xv[rr] = *reinterpret_cast<const uint2*>(part_v + prow * kHeadDim + part * 4);
-        eq[rr] = part_e[prow];
-        ev[rr] = part_e[rr_total + prow];
+        for (int rr = 0; rr < NRL; ++rr) {
+            sbase[k][rr] = (bh * n_r + (rr < n_r ? rr : 0)) * L;
+            slot[k][rr] = undo[sbase[k][rr] + i];
+        }
     }
-    f32x4 aq = {0, 0, 0, 0}, av = {0, 0, 0, 0};
+    uint2 xq[kReduceRows][NRL], xv[kReduceRows][NRL];
+    uint32_t eq[kReduceRows][NRL], ev[kReduceRows][NRL];
 #pragma unroll
-    for (int rr = 0; rr < NRL; ++rr) {
-        const float wq = rr < n_r ? __uint_as_float((127u + min(eq[rr], 126u)) << 23) : 0.f;
-        const float wv = rr < n_r ? __uint_as_float((127u + min(ev[rr], 126u)) << 23) : 0.f;
-        aq[0] = fmaf(wq, f16_bits_to_f32(xq[rr].x & 0xFFFFu), aq[0]);
-        aq[1] = fmaf(wq, f16_bits_to_f32(xq[rr].x >> 16), aq[1]);
-        aq[2] = fmaf(wq, f16_bits_to_f32(xq[rr].y & 0xFFFFu), aq[2]);
-        aq[3] = fmaf(wq, f16_bits_to_f32(xq[rr].y >> 16), aq[3]);
-        av[0] = fmaf(wv, f16_bits_to_f32(xv[rr].x & 0xFFFFu), av[0]);
-        av[1] = fmaf(wv, f16_bits_to_f32(xv[rr].x >> 16), av[1]);
-        av[2] = fmaf(wv, f16_bits_to_f32(xv[rr].y & 0xFFFFu), av[2]);
-        av[3] = fmaf(wv, f16_bits_to_f32(xv[rr].y >> 16), av[3]);
+    for (int k = 0; k < kReduceRows; ++k)
+#pragma unroll
+        for (int rr = 0; rr < NRL; ++rr) {
+            const int64_t prow = sbase[k][rr] + min(max(slot[k][rr], 0), L - 1);
+            xq[k][rr] = *reinterpret_cast<const uint2*>(part_q + prow * kHeadDim + part * 4);
+            xv[k][rr] = *reinterpret_cast<const uint2*>(part_v + prow * kHeadDim + part * 4);
+            eq[k][rr] = part_e[prow];
+            ev[k][rr] = part_e[rr_total + prow];
+        }
+#pragma unroll
+    for (int k = 0; k < kReduceRows; ++k) {
+        const int64_t row = row0 + k;
+        f32x4 aq = {0, 0, 0, 0}, av = {0, 0, 0, 0};
+#pragma unroll
+        for (int rr = 0; rr < NRL; ++rr) {
+            const float wq = rr < n_r ? __uint_as_float((127u + min(eq[k][rr], 126u)) << 23) : 0.f;
+            const float wv = rr < n_r ? __uint_as_float((127u + min(ev[k][rr], 126u)) << 23) : 0.f;
+            aq[0] = fmaf(wq, f16_bits_to_f32(xq[k][rr].x & 0xFFFFu), aq[0]);
+            aq[1] = fmaf(wq, f16_bits_to_f32(xq[k][rr].x >> 16), aq[1]);
+            aq[2] = fmaf(wq, f16_bits_to_f32(xq[k][rr].y & 0xFFFFu), aq[2]);
+            aq[3] = fmaf(wq, f16_bits_to_f32(xq[k][rr].y >> 16), aq[3]);
+            av[0] = fmaf(wv, f16_bits_to_f32(xv[k][rr].x & 0xFFFFu), av[0]);
+            av[1] = fmaf(wv, f16_bits_to_f32(xv[k][rr].x >> 16), av[1]);
+            av[2] = fmaf(wv, f16_bits_to_f32(xv[k][rr].y & 0xFFFFu), av[2]);
+            av[3] = fmaf(wv, f16_bits_to_f32(xv[k][rr].y >> 16), av[3]);
+        }
+        if (row < rows) {
+            if (z[k] < -0.5f * self_mask) {
+                const uint2 g = *reinterpret_cast<const uint2*>(dout + row * kHeadDim + part * 4);
+                av[0] += bf16_bits_to_f32(g.x & 0xFFFF);
+                av[1] += bf16_bits_to_f32(g.x >> 16);
+                av[2] += bf16_bits_to_f32(g.y & 0xFFFF);
+                av[3] += bf16_bits_to_f32(g.y >> 16);
+            }
+            *reinterpret_cast<f32x4*>(dq + row * kHeadDim + part * 4) = aq;
+            *reinterpret_cast<f32x4*>(dv + row * kHeadDim + part * 4) = av;
+        }
     }
-    if (lse_total[row] < -0.5f * self_mask) {
-        const uint2 g = *reinterpret_cast<const uint2*>(dout + row * kHeadDim + part * 4);
-        av[0] += bf16_bits_to_f32(g.x & 0xFFFF);
-        av[1] += bf16_bits_to_f32(g.x >> 16);
-        av[2] += bf16_bits_to_f32(g.y & 0xFFFF);
-        av[3] += bf16_bits_to_f32(g.y >> 16);
-    }
-    *reinterpret_cast<f32x4*>(dq + row * kHeadDim + part * 4) = aq;
-    *reinterpret_cast<f32x4*>(dv + row * kHeadDim + part * 4) = av;
 }
 
 int rec_words(int n_rounds) {
@@ -647,8 +668,9 @@ hipError_t launch_attn_bwd(int64_t BH, int L, int n_rounds, int n_buckets, bool 
     }
 #undef LSH_BWD_CASE
     if (e != hipSuccess) return e;
-    const unsigned row_grid = (unsigned)((rows * 16 + 255) / 256);
     auto reduce = [&](auto nrl) {
+        constexpr int kRows = reduce_rows<decltype(nrl)::value>();
+        const unsigned row_grid = (unsigned)(((rows + kRows - 1) / kRows * 16 + 255) / 256);
         bwd_reduce_kernel<decltype(nrl)::value><<<row_grid, 256, 0, stream>>>(
             dout, lse_total, w.part_q, w.part_v, w.part_e, undo, rows, L, n_rounds, self_mask, dq, dv);
     };
