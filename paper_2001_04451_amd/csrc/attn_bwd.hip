@@ -301,8 +301,7 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_strip_kernel(
                         make_uint2(pack_f16x2(accV[bd][0] * sv, accV[bd][1] * sv),
                                    pack_f16x2(accV[bd][2] * sv, accV[bd][3] * sv));
                 }
-                if (g == 0) part_e[prow] = (uint8_t)eq;
-                if (g == 1) part_e[(int64_t)gridDim.y * L + prow] = (uint8_t)ev;
+                if (g == 0) reinterpret_cast<uint16_t*>(part_e)[prow] = (uint16_t)(eq | (ev << 8));
             }
 #pragma unroll
             for (int bd = 0; bd < 4; ++bd) {
@@ -509,7 +508,6 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     const int64_t row0 = (((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4) * kReduceRows;
     const int part = threadIdx.x & 15;
     if (row0 >= rows) return;  // whole 16-lane groups leave together
-    const int64_t rr_total = rows * n_r;  // offset of the dv exponents
     int64_t sbase[kReduceRows][NRL];
     int slot[kReduceRows][NRL];
     float z[kReduceRows];
@@ -533,8 +531,9 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
             const int64_t prow = sbase[k][rr] + min(max(slot[k][rr], 0), L - 1);
             xq[k][rr] = *reinterpret_cast<const uint2*>(part_q + prow * kHeadDim + part * 4);
             xv[k][rr] = *reinterpret_cast<const uint2*>(part_v + prow * kHeadDim + part * 4);
-            eq[k][rr] = part_e[prow];
-            ev[k][rr] = part_e[rr_total + prow];
+            const uint32_t e2 = reinterpret_cast<const uint16_t*>(part_e)[prow];
+            eq[k][rr] = e2 & 0xFFu;
+            ev[k][rr] = e2 >> 8;
         }
 #pragma unroll
     for (int k = 0; k < kReduceRows; ++k) {
@@ -576,7 +575,7 @@ int rec_words(int n_rounds) {
 struct BwdWs {
     uint16_t* part_q;  // per round: dq through the query role plus the key role's dk through k = q/|q|
     uint16_t* part_v;
-    uint8_t* part_e;   // exponents: [round-rows] of dq, then [round-rows] of dv
+    uint8_t* part_e;   // exponents: [round-rows] pairs, dq's byte then dv's
     uint32_t* rec;
     size_t bytes;
 };
