@@ -461,11 +461,8 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t* __restric
         D = fmaf(__uint_as_float(o[e] << 16), __uint_as_float(gd[e] << 16), D);
         D = fmaf(__uint_as_float(o[e] & 0xFFFF0000u), __uint_as_float(gd[e] & 0xFFFF0000u), D);
     }
-#pragma unroll
-    for (int off = 1; off < 8; off <<= 1) {
-        ss += __shfl_xor(ss, off);
-        D += __shfl_xor(D, off);
-    }
+    ss = group8_sum(ss);
+    D = group8_sum(D);
     const int32_t* brow = buckets + row * n_r;
 #pragma unroll
     for (int w = part; w < RW; w += 8) {
