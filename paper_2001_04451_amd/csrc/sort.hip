@@ -189,13 +189,15 @@ __global__ __launch_bounds__(256) void sort_scan_any_kernel(int32_t* __restrict_
 // LDS of the scatter: per-wave next local slot of every bucket as 16-bit
 // fields [kSortWaves][n_b rounded up to even] (slots in a tile stay below
 // 2^16), the tile's (first global slot - first local slot) of every bucket,
-// the tile in sorted order [kTile], and the waves' sums of the bucket scan.
-// At 1024 buckets this is 36 KB, four workgroups per CU.
+// the tile in sorted order [kTile], the waves' sums of the bucket scan, and
+// per wave a table of lane masks by the low bits of the id.  At 1024
+// buckets this is 38 KB, four workgroups per CU.
 constexpr int kScatterBucketsPerThread = 2;  // one 32-bit word of 16-bit fields; n_b <= 2 * kSortWaves * 64
 __host__ __device__ inline int even_buckets(int n_b) { return (n_b + 1) & ~1; }
+constexpr int kLowBits = 5;  // id bits resolved through the mask table; the rest by ballots
 size_t scatter_lds_bytes(int n_b) {
     return (size_t)kSortWaves * even_buckets(n_b) * sizeof(uint16_t) + even_buckets(n_b) * sizeof(int) +
-           kTile * sizeof(uint32_t) + kSortWaves * sizeof(int);
+           kTile * sizeof(uint32_t) + kSortWaves * sizeof(int) + kSortWaves * (1 << kLowBits) * sizeof(uint64_t);
 }
 
 template <bool IDS16>
@@ -211,6 +213,8 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
     int* delta = smem + kSortWaves * half;                // [2 * half]
     uint32_t* staged = reinterpret_cast<uint32_t*>(delta + 2 * half);  // [kTile]: bucket << 16 | position in tile
     int* wsum = reinterpret_cast<int*>(staged + kTile);                 // [kSortWaves]
+    // [kSortWaves][2^kLowBits] lane masks (8-byte aligned: every part above is a multiple of 8 bytes)
+    uint64_t* masks = reinterpret_cast<uint64_t*>(wsum + kSortWaves);
     // Workgroup b of the launch runs on XCD b % 8 (round-robin dispatch).
     // Each XCD is given a contiguous run of (segment, tile) items, so the
     // tiles of a segment write their perm runs into the same XCD's L2, which
@@ -226,6 +230,8 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     uint32_t* wrow = base + wave * half;
     uint16_t* wslot = reinterpret_cast<uint16_t*>(wrow);
+    uint64_t* wmask = masks + wave * (1 << kLowBits);
+    if (lane < (1 << kLowBits)) wmask[lane] = 0;
 
     for (int i = threadIdx.x; i < kSortWaves * half; i += blockDim.x) base[i] = 0;
     const int t0 = tile * kTile;
@@ -297,9 +303,12 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
 
     // Rank of a position among the equal buckets of its 64-lane group: the
     // lanes holding the same bucket are those agreeing with it on every bit
-    // of the id (one ballot per bit; ids are below n_b <= 1024), and
-    // the rank counts those below the lane, so equal keys keep their
-    // position order.  The highest lane of each bucket moves the bucket's
+    // of the id (ids are below n_b <= 1024): on the low kLowBits bits, the
+    // lanes that set their bit in the wave's mask entry of those bits (an
+    // LDS atomic or, read back and cleared by the same wave, whose LDS
+    // operations run in order), on each higher bit, the lanes whose ballot
+    // of that bit agrees; the rank counts those below the lane, so equal
+    // keys keep their position order.  The highest lane of each bucket moves the bucket's
     // next slot on (the wave's LDS operations run in order).  undo is
     // written here, in position order; perm goes to the tile's sorted copy
     // in LDS first.
@@ -313,17 +322,21 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
         const int b = ids[it];
         const int start = wslot[b];
         const int d = delta[b];
-        // lanes differing from this one in some bit: for every bit, the
+        uint64_t* entry = wmask + (b & ((1 << kLowBits) - 1));
+        if (active) atomicOr(reinterpret_cast<unsigned long long*>(entry), 1ull << lane);
+        const uint64_t same_low = *entry;  // after every lane's or
+        *entry = 0;                        // after every lane's read
+        // lanes differing from this one in a higher bit: for every bit, the
         // ballot of the bit xor this lane's bit spread over the word
         uint32_t diff_lo = 0, diff_hi = 0;
 #pragma unroll
-        for (int bit = 0; bit < kIdBits; ++bit) {
+        for (int bit = kLowBits; bit < kIdBits; ++bit) {
             const uint32_t spread = (uint32_t)__builtin_amdgcn_sbfe(b, bit, 1);  // 0 or all ones
             const uint64_t ones = __ballot(spread != 0u);
             diff_lo |= (uint32_t)ones ^ spread;
             diff_hi |= (uint32_t)(ones >> 32) ^ spread;
         }
-        const uint64_t peers = __ballot(active) & ~(((uint64_t)diff_hi << 32) | diff_lo);
+        const uint64_t peers = same_low & ~(((uint64_t)diff_hi << 32) | diff_lo);
         const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(peers >> 32),
                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u));
         if (active) {
