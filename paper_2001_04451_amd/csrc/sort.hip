@@ -39,6 +39,13 @@ __device__ __forceinline__ int clamp_bucket(int b, int n_b) { return min(max(b, 
 constexpr int kHistThreads = 1024;
 
 constexpr int kHistRows = kTile / kHistThreads;  // positions per thread
+
+// LDS of the histogram: the counts of its rounds (rounded up to 16 bytes),
+// then, when it writes the 16-bit id copy, the tile's ids of those rounds.
+__host__ __device__ inline int hist_words(int rounds, int n_b) { return (rounds * n_b + 3) & ~3; }
+size_t hist_lds_bytes(int rounds, int n_b, bool ids16) {
+    return (size_t)hist_words(rounds, n_b) * sizeof(int) + (ids16 ? (size_t)rounds * kTile * sizeof(uint16_t) : 0);
+}
 constexpr int kHistMaxRounds = 16;
 
 __global__ __launch_bounds__(kHistThreads) void sort_hist_kernel(const int32_t* __restrict__ buckets, int L,
@@ -84,22 +91,36 @@ __global__ __launch_bounds__(kHistThreads) void sort_hist_kernel(const int32_t* 
             for (int r = 0; r < kHistMaxRounds; ++r)
                 if (r < nr) atomicAdd(&hist[r * n_b + clamp_bucket(ids[k][r], n_b)], 1);
         }
-    // the ids again, one round after another as 16-bit values, for the scatter's coalesced reads
+    // The ids again, one round after another as 16-bit values, for the
+    // scatter's coalesced reads: transposed in LDS, then written 16 bytes
+    // per lane.
+    uint16_t* t16 = reinterpret_cast<uint16_t*>(hist + hist_words(rounds_per_group, n_b));
     if (ids16) {
 #pragma unroll
         for (int k = 0; k < kHistRows; ++k) {
-            const int p = p0 + (int)threadIdx.x + kHistThreads * k;
-            if (p < p1) {
+            const int u = (int)threadIdx.x + kHistThreads * k;
 #pragma unroll
-                for (int r = 0; r < kHistMaxRounds; ++r)
-                    if (r < nr) ids16[(bh * n_r + r0 + r) * L + p] = (uint16_t)clamp_bucket(ids[k][r], n_b);
-            }
+            for (int r = 0; r < kHistMaxRounds; ++r)
+                if (r < nr) t16[r * kTile + u] = (uint16_t)clamp_bucket(ids[k][r], n_b);
         }
     }
     __syncthreads();
     for (int i = threadIdx.x; i < nr * n_b; i += blockDim.x) {
         const int r = r0 + i / n_b, b = i % n_b;
         counts[((bh * n_r + r) * n_tiles + tile) * n_b + b] = hist[i];
+    }
+    if (ids16) {
+        constexpr int kPieces = kTile / 8;  // 16-byte pieces of a round's row
+        const bool aligned = (L % 8) == 0;
+        for (int i = threadIdx.x; i < nr * kPieces; i += blockDim.x) {
+            const int r = i / kPieces, u = 8 * (i % kPieces);
+            uint16_t* dst = ids16 + (bh * n_r + r0 + r) * L + p0 + u;
+            if (aligned && p0 + u + 8 <= p1) {
+                *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>(t16 + r * kTile + u);
+            } else {
+                for (int e = 0; e < 8 && p0 + u + e < p1; ++e) dst[e] = t16[r * kTile + u + e];
+            }
+        }
     }
 }
 
@@ -430,7 +451,11 @@ hipError_t launch_sort(int64_t BH, int L, int n_rounds, int n_buckets, const int
     const int rpg = std::max(1, std::min(n_rounds, kHistLdsInts / n_buckets));
     const int groups = (n_rounds + rpg - 1) / rpg;
 
-    sort_hist_kernel<<<dim3(n_tiles, (unsigned)BH, groups), kHistThreads, rpg * n_buckets * sizeof(int), stream>>>(
+    const size_t hist_lds = hist_lds_bytes(rpg, n_buckets, ids16 != nullptr);
+    if (hist_lds > 65536)
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&sort_hist_kernel),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)hist_lds);
+    sort_hist_kernel<<<dim3(n_tiles, (unsigned)BH, groups), kHistThreads, hist_lds, stream>>>(
         buckets, L, n_rounds, n_buckets, rpg, n_tiles, counts, ids16);
     if (n_tiles <= kScanTiles && n_buckets <= kScanThreads)
         sort_scan_kernel<<<(unsigned)(BH * n_rounds), kScanThreads, 0, stream>>>(counts, L, n_buckets, n_tiles,
