@@ -60,12 +60,15 @@ def test_hash_bit_exact(gpu, name):
 @pytest.mark.parametrize("n_buckets,L,n_rounds,B,H", [
     (2, 64, 1, 1, 1), (16, 1024, 1, 1, 1), (64, 4096, 2, 2, 3), (1024, 8192, 3, 1, 2),
     (1024, 4160, 2, 1, 1), (512, 12352, 4, 1, 1), (256, 64, 16, 2, 1),
-    (1024, 65536, 2, 1, 1), (1024, 69632, 2, 1, 1)])
+    (1024, 65536, 2, 1, 1), (1024, 69632, 2, 1, 1),
+    (14, 1001, 3, 1, 2), (1024, 4100, 2, 1, 1), (256, 37, 2, 2, 1)])
 def test_sort_bit_exact(gpu, n_buckets, L, n_rounds, B, H):
     """Counting sort vs the oracle on test-drawn ids, including ragged tiles
     (L not a multiple of 4096), empty buckets and one-bucket segments.  The
-    last two shapes have 16 tiles of 4096 positions, the most the scan holds
-    in registers, and 17, which takes its general loop."""
+    shapes with L = 65536 and 69632 have 16 tiles of 4096 positions, the
+    most the scan holds in registers, and 17, which takes its general loop;
+    L = 1001, 4100 and 37 are not multiples of 8 (the 16-bit id copy's
+    element-wise path), and 14 buckets are not a multiple of four."""
     rng = np.random.Generator(np.random.PCG64(L + n_buckets))
     b = rng.integers(0, n_buckets, size=(B, H, L, n_rounds)).astype(np.int32)
     b[0, 0, :, 0] = n_buckets - 1  # one segment entirely in the last bucket
