@@ -12,13 +12,14 @@
 //   2. scan:    exclusive scan of the counts in (bucket, tile) order gives
 //               every (bucket, tile) pair its first output slot, and the
 //               bucket start offsets.
-//   3. scatter: each of eight waves ranks its eighth of a tile in position order; the
-//               rank of a position among equal buckets of its 64-lane group
-//               is the count of lower lanes with the same bucket, whose lane
-//               mask comes from one ballot per bucket-id bit, so equal keys
-//               keep their position order (stable).  undo is written in
-//               position order; perm is first put in the tile's sorted
-//               order in LDS and written from there, run by run.
+//   3. scatter: each of eight waves ranks its eighth of a tile in position
+//               order; the rank of a position among equal buckets of its
+//               64-lane group is the count of lower lanes with the same
+//               bucket (their lane mask from an LDS table on the id's low
+//               bits and one ballot per high bit), so equal keys keep their
+//               position order (stable).  undo is written in position
+//               order; perm is first put in the tile's sorted order in LDS
+//               and written from there, run by run.
 #include "common.h"
 #include "launch.h"
 
