@@ -211,15 +211,16 @@ __global__ __launch_bounds__(256) void sort_scan_any_kernel(int32_t* __restrict_
 // LDS of the scatter: per-wave next local slot of every bucket as 16-bit
 // fields [kSortWaves][n_b rounded up to even] (slots in a tile stay below
 // 2^16), the tile's (first global slot - first local slot) of every bucket,
-// the tile in sorted order [kTile], the waves' sums of the bucket scan, and
-// per wave a table of lane masks by the low bits of the id.  At 1024
-// buckets this is 38 KB, four workgroups per CU.
+// the tile in sorted order [kTile], and per wave a table of lane masks by the
+// low bits of the id, whose first words hold the waves' sums of the bucket
+// scan before the ranking starts.  At 1024 buckets this is 40 KB, four
+// workgroups per CU.
 constexpr int kScatterBucketsPerThread = 2;  // one 32-bit word of 16-bit fields; n_b <= 2 * kSortWaves * 64
 __host__ __device__ inline int even_buckets(int n_b) { return (n_b + 1) & ~1; }
-constexpr int kLowBits = 5;  // id bits resolved through the mask table; the rest by ballots
+constexpr int kLowBits = 6;  // id bits resolved through the mask table; the rest by ballots
 size_t scatter_lds_bytes(int n_b) {
     return (size_t)kSortWaves * even_buckets(n_b) * sizeof(uint16_t) + even_buckets(n_b) * sizeof(int) +
-           kTile * sizeof(uint32_t) + kSortWaves * sizeof(int) + kSortWaves * (1 << kLowBits) * sizeof(uint64_t);
+           kTile * sizeof(uint32_t) + kSortWaves * (1 << kLowBits) * sizeof(uint64_t);
 }
 
 template <bool IDS16>
@@ -234,9 +235,11 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
     uint32_t* base = reinterpret_cast<uint32_t*>(smem);  // [kSortWaves][half], two 16-bit fields each
     int* delta = smem + kSortWaves * half;                // [2 * half]
     uint32_t* staged = reinterpret_cast<uint32_t*>(delta + 2 * half);  // [kTile]: bucket << 16 | position in tile
-    int* wsum = reinterpret_cast<int*>(staged + kTile);                 // [kSortWaves]
-    // [kSortWaves][2^kLowBits] lane masks (8-byte aligned: every part above is a multiple of 8 bytes)
-    uint64_t* masks = reinterpret_cast<uint64_t*>(wsum + kSortWaves);
+    // [kSortWaves][2^kLowBits] lane masks (8-byte aligned: every part above
+    // is a multiple of 8 bytes); until the ranking, its first words are the
+    // waves' sums of the bucket scan [kSortWaves]
+    uint64_t* masks = reinterpret_cast<uint64_t*>(staged + kTile);
+    int* wsum = reinterpret_cast<int*>(masks);
     // Workgroup b of the launch runs on XCD b % 8 (round-robin dispatch).
     // Each XCD is given a contiguous run of (segment, tile) items, so the
     // tiles of a segment write their perm runs into the same XCD's L2, which
@@ -253,7 +256,6 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
     uint32_t* wrow = base + wave * half;
     uint16_t* wslot = reinterpret_cast<uint16_t*>(wrow);
     uint64_t* wmask = masks + wave * (1 << kLowBits);
-    if (lane < (1 << kLowBits)) wmask[lane] = 0;
 
     for (int i = threadIdx.x; i < kSortWaves * half; i += blockDim.x) base[i] = 0;
     const int t0 = tile * kTile;
@@ -322,6 +324,9 @@ __global__ __launch_bounds__(kSortWaves * 64) void sort_scatter_kernel(const int
         }
     }
     __syncthreads();
+    // the wave's mask table, cleared now that no wave reads the scan sums
+    // (the wave's own LDS operations run in order, so no barrier follows)
+    if (lane < (1 << kLowBits)) wmask[lane] = 0;
 
     // Rank of a position among the equal buckets of its 64-lane group: the
     // lanes holding the same bucket are those agreeing with it on every bit
