@@ -9,19 +9,28 @@
 namespace lsh {
 
 // Rows of 64 bf16 values (128 B) are staged in LDS as 8 pieces of 16 B with
-// piece p of row r stored at slot p ^ (r & 7) ^ (((r >> 3) & 1) << 2).  Rows
-// read together by the operand loads (rows kappa(0..7), rows r..r+7, and the
-// two lane halves 8 rows apart) then fall into different banks.
+// piece p of row r stored at slot p ^ (r & 7) ^ (((r >> 3) & 1) << k), where
+// layout K picks k: K = 0, k = 2, for reads of rows kappa(0..7), rows
+// r..r+7 and the two lane halves 8 rows apart (32-row operands); K = 1,
+// k = 1, for the same piece of sixteen consecutive rows read by the sixteen
+// lanes of a 16-row operand.  Measured with SQ_LDS_BANK_CONFLICT on the
+// forward kernel (the hardware's grouping of a 16-byte read's lanes is not
+// documented): 6.4 M conflict cycles per call under K = 1, 31 M under K = 0
+// and under p ^ ((r ^ (r >> 3)) & 7), 28 M under p ^ ((r >> 1) & 7), 145 M
+// under p ^ ((r >> 2) & 7) and with no swizzle.
+template <int K = 0>
 __device__ __forceinline__ int swz(int row, int piece) {
-    return piece ^ (row & 7) ^ (((row >> 3) & 1) << 2);
+    return piece ^ (row & 7) ^ (((row >> 3) & 1) << (K == 0 ? 2 : 1));
 }
 
+template <int K = 0>
 __device__ __forceinline__ uint32_t row_piece_offset(int row, int piece) {
-    return (uint32_t)row * 128u + (uint32_t)swz(row, piece) * 16u;
+    return (uint32_t)row * 128u + (uint32_t)swz<K>(row, piece) * 16u;
 }
 
+template <int K = 0>
 __device__ __forceinline__ u32x4 lds_piece(const char* base, int row, int piece) {
-    return *reinterpret_cast<const u32x4*>(base + row_piece_offset(row, piece));
+    return *reinterpret_cast<const u32x4*>(base + row_piece_offset<K>(row, piece));
 }
 
 __device__ __forceinline__ void lds_store_piece(char* base, int row, int piece, u32x4 v) {
@@ -92,11 +101,12 @@ __device__ __forceinline__ void copy4_to_lds(const void* src, const void* lds_ba
 // by lanes 4k + i/4, so lane i reads row r0 + 4(l/16) + i/4, dims
 // d0 + 4(i%4) .. +3: vt_offset is that byte offset (r0 a multiple of 16, so
 // the swizzle depends on the lane only).
+template <int K = 0>
 __device__ __forceinline__ uint32_t vt_offset(int r0, int d0, int lane) {
     const int i = lane & 15;
     const int row = r0 + 4 * (lane >> 4) + (i >> 2);
     const int d = d0 + 4 * (i & 3);
-    return row_piece_offset(row, d >> 3) + (uint32_t)((d & 4) << 1);
+    return row_piece_offset<K>(row, d >> 3) + (uint32_t)((d & 4) << 1);
 }
 __device__ __forceinline__ bf16x4 vt_read(const char* p) {
     typedef __attribute__((address_space(3))) i16x4 lds_i16x4;

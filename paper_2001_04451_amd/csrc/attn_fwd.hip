@@ -60,6 +60,7 @@ namespace lsh {
 namespace {
 
 constexpr float kFastBound = 60.f;  // largest B_i handled without a running maximum
+constexpr int kSwz = 1;             // LDS row layout (attn_common.h): 16-row operand reads
 constexpr int kMaskedIndex = 32;    // table index of a masked-out key
 
 
@@ -188,7 +189,7 @@ __global__ __launch_bounds__((FwdGeom<M, AFTER>::kThreads), (FwdGeom<M, AFTER>::
         for (int k = 0; k < 2; ++k) {
             const int row = 16 * wave + 8 * k + (lane >> 3);
             const int p = pos_of(row);
-            const int64_t off = (rowbase + p) * kHeadDim + swz(row, lane & 7) * 8;
+            const int64_t off = (rowbase + p) * kHeadDim + swz<kSwz>(row, lane & 7) * 8;
             copy16_to_lds(q + off, S.Qs + (slot0 + 16 * wave + 8 * k) * 128);
             copy16_to_lds(v + off, S.Vs + (slot0 + 16 * wave + 8 * k) * 128);
         }
@@ -252,8 +253,8 @@ __global__ __launch_bounds__((FwdGeom<M, AFTER>::kThreads), (FwdGeom<M, AFTER>::
         const int rq = ring_row(c, u);
         uint32_t qsig[NW > 0 ? NW : 1];
         read_sig<NW>(S, rq, qsig);
-        const bf16x8 qb0 = as_bf16x8(lds_piece(S.Qs, rq, g));
-        const bf16x8 qb1 = as_bf16x8(lds_piece(S.Qs, rq, 4 + g));
+        const bf16x8 qb0 = as_bf16x8(lds_piece<kSwz>(S.Qs, rq, g));
+        const bf16x8 qb1 = as_bf16x8(lds_piece<kSwz>(S.Qs, rq, 4 + g));
         const float cfq = S.cf[rq];
         // B_i (to within an ulp: it picks the fast path, with a wide margin,
         // and gives a lone query's log-partition)
@@ -337,10 +338,10 @@ __global__ __launch_bounds__((FwdGeom<M, AFTER>::kThreads), (FwdGeom<M, AFTER>::
 #pragma unroll
         for (int ch = 0; ch < G::kWinChunks; ++ch) {
             const int base = ring_row(c - 1 + ch, 0);
-            kofs[ch][0] = row_piece_offset(base + n, g);
-            kofs[ch][1] = row_piece_offset(base + n, 4 + g);
+            kofs[ch][0] = row_piece_offset<kSwz>(base + n, g);
+            kofs[ch][1] = row_piece_offset<kSwz>(base + n, 4 + g);
 #pragma unroll
-            for (int b = 0; b < 4; ++b) vofs[ch][b] = vt_offset(base, 16 * b, lane);
+            for (int b = 0; b < 4; ++b) vofs[ch][b] = vt_offset<kSwz>(base, 16 * b, lane);
             srow[ch] = base + 4 * g;
         }
 
