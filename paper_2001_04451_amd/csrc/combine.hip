@@ -34,7 +34,12 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ o
                                                       void* __restrict__ out,
                                                       float* __restrict__ lse_total, int64_t rows,
                                                       int L, int n_r) {
-    const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 3;
+    // Rows from the last to the first: the attention kernel writes the
+    // per-round rows segment after segment, so the last (batch, head) slices'
+    // rows are the ones most likely still in the Infinity Cache when the
+    // combine starts (at L = 64K, 16 heads, 8 rounds: 0.290 -> 0.276 ms;
+    // unchanged at L = 32K, 64 slices, 4 rounds).
+    const int64_t row = ((int64_t)(gridDim.x - 1 - blockIdx.x) * blockDim.x + threadIdx.x) >> 3;
     const int part = threadIdx.x & 7;
     // Rows past the end leave as whole 8-lane groups; every shuffle below
     // stays inside a group.
