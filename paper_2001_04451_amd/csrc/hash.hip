@@ -676,10 +676,12 @@ constexpr uint16_t kUnsettled = 0xFFFFu;
 //    of the exact one (res_max: largest 2-norm of R's columns less the
 //    planes used, none for fp32 input, whose planes' residual is inside
 //    err_acc), and a key's magnitude is low by at most err_pack of it.  For
-//    bf16 input the best key's column is then recomputed over both planes
-//    (within eps2, from res_max2 and err_acc2), and the row-round is settled
-//    when that value's magnitude less eps2 exceeds the second key plus eps;
-//    for fp32 input when the best and second keys are more than 2 eps apart.
+//    bf16 input the best key's column w is then recomputed, by the screen
+//    over the hi plane (within |q| (|R_w - hi_w| + err_acc max_c |R_c|)),
+//    by the listed pass over both planes (within eps2, from res_max2 and
+//    err_acc2), and the row-round is settled when that value's magnitude
+//    less its bound exceeds the second key plus eps; for fp32 input when the
+//    best and second keys are more than 2 eps apart.
 //    A settled id goes to buckets.  Otherwise the row is appended to the round's list: the
 //    screen's lists are segmented, [round][kSegs][seg_cap] with counts
 //    [round][kSegs]; the exact passes' are [round][rows] with one count per
@@ -689,8 +691,8 @@ __global__ __launch_bounds__(WAVES * 64, (MODE == kScreen ? kScreenOcc : 1)) voi
     const void* __restrict__ q, int64_t rows, int n_r, int half, int half_pad,
     const uint16_t* __restrict__ r_hi, const uint16_t* __restrict__ r_mid,
     const float* __restrict__ col_norm_max, const float* __restrict__ res_max, float err_acc,
-    const float* __restrict__ res_max2, float err_acc2, float err_pack, int32_t* __restrict__ buckets,
-    const int* __restrict__ list_in,
+    const float* __restrict__ res_max2, float err_acc2, float err_pack, const float* __restrict__ col_res,
+    int32_t* __restrict__ buckets, const int* __restrict__ list_in,
     const int* __restrict__ count_in, int* __restrict__ list_out, int* __restrict__ count_out,
     int64_t seg_cap) {
     static_assert(!F32 || MODE == kExact, "fp32 input takes the exact pass only");
@@ -912,16 +914,23 @@ __global__ __launch_bounds__(WAVES * 64, (MODE == kScreen ? kScreenOcc : 1)) voi
                     if (rb == h) win[(rb * 32 + n) * nrb + (r - r_lo)] = flag ? kUnsettled : (uint16_t)id;
                 }
             } else {
-                // x = q_row . R_col of the best key's column over both planes
-                // (fp32 sums of the exact products; each lane half adds its 32
-                // k-values), within eps2 of the exact projection.  Every other
-                // column's exact |projection| is at most the second key (raised
-                // by the truncated bits) plus the pass's eps, so the winner is
-                // certain when |x| - eps2 exceeds that, and its sign is x's.  A
-                // flagged winner may sit past the round; any valid column
-                // stands in.  Both planes' pieces come from global memory (the
-                // planes are small and stay in the caches).
+                // x = q_row . R_col of the best key's column (fp32 sums of
+                // the exact products; each lane half adds its 32 k-values).
+                // Every other column's exact |projection| is at most the
+                // second key (raised by the truncated bits) plus the pass's
+                // eps, so the winner is certain when |x| less x's own error
+                // bound exceeds that, and its sign is x's.  A flagged winner
+                // may sit past the round; any valid column stands in.
+                //  * The screen takes x over the hi plane alone: within
+                //    eps_w = |q| (|R_w - hi_w| + err_acc max_c |R_c|) for the
+                //    winner's column w.  Rows it leaves open go to the listed
+                //    pass, which costs less than the mid plane's loads here.
+                //  * The listed pass takes x over both planes, within eps2.
+                // The pieces come from global memory (the planes are small
+                // and stay in the caches).
+                constexpr bool kHiOnly = MODE == kScreen;
                 u32x4 hv[kRB][4], mv[kRB][4];
+                float res_w[kRB];
 #pragma unroll
                 for (int rb = 0; rb < kRB; ++rb) {
                     const int cc = min(col[rb], half_pad - 1);
@@ -931,17 +940,20 @@ __global__ __launch_bounds__(WAVES * 64, (MODE == kScreen ? kScreenOcc : 1)) voi
 #pragma unroll
                     for (int s4 = 0; s4 < 4; ++s4) {
                         hv[rb][s4] = ph[s4];
-                        mv[rb][s4] = pm[s4];
+                        if constexpr (!kHiOnly) mv[rb][s4] = pm[s4];
                     }
+                    if constexpr (kHiOnly) res_w[rb] = col_res[(size_t)r * half_pad + cc];
                 }
 #pragma unroll
                 for (int rb = 0; rb < kRB; ++rb) {
-                    const float half_x = dot_planes(qa[rb], hv[rb]) + dot_planes(qa[rb], mv[rb]);
+                    float half_x = dot_planes(qa[rb], hv[rb]);
+                    if constexpr (!kHiOnly) half_x += dot_planes(qa[rb], mv[rb]);
                     const float x = sum_xor32(half_x);
                     const float s1 = key_magnitude<F32>(sk[rb]);
                     const float eps = 1.02f * qn[rb] * (res + err_acc * cn);
-                    const float eps2 = 1.02f * qn[rb] * (res_max2[r] + err_acc2 * cn);
-                    const bool flag = !(fabsf(x) - eps2 > s1 * (1.f + 2.f * err_pack) + eps) || col[rb] >= half;
+                    const float eps_x = kHiOnly ? 1.02f * qn[rb] * (res_w[rb] + err_acc * cn)
+                                                : 1.02f * qn[rb] * (res_max2[r] + err_acc2 * cn);
+                    const bool flag = !(fabsf(x) - eps_x > s1 * (1.f + 2.f * err_pack) + eps) || col[rb] >= half;
                     const int id = x < 0.f ? half + col[rb] : col[rb];
                     if (rb == h) win[(rb * 32 + n) * nrb + (r - r_lo)] = flag ? kUnsettled : (uint16_t)id;
                 }
@@ -1065,6 +1077,7 @@ struct PassArgs {
     float err_acc;
     const float* res2;
     float err_acc2, err_pack;
+    const float* col_res;
     int32_t* buckets;
     const int *list_in, *count_in;
     int *list_out, *count_out;
@@ -1078,24 +1091,25 @@ void launch_pass_st(const PassArgs& a, dim3 grid, int rounds, hipStream_t stream
     auto* k = &hash_kernel<F32, MODE, WAVES, ST>;
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     k<<<grid, WAVES * 64, lds, stream>>>(a.q, a.rows, a.n_r, a.half, a.half_pad, a.r_hi, a.r_mid, a.cn_max, a.res,
-                                         a.err_acc, a.res2, a.err_acc2, a.err_pack, a.buckets, a.list_in,
+                                         a.err_acc, a.res2, a.err_acc2, a.err_pack, a.col_res, a.buckets, a.list_in,
                                          a.count_in, a.list_out, a.count_out, a.seg_cap);
 }
 
 // Tiles per stage: the round's tile count rounded up to a power of two, at
-// most 16 for the screen (one plane, 64 KB a buffer), 8 for the fp32 pass
-// (two planes) and 4 for the listed pass (two planes; past that its
-// registers would spill).
+// most kScreenMaxTiles for the screen (one plane), 8 for the fp32 pass (two
+// planes) and 2 for the listed pass (two planes: 240 registers, two waves a
+// SIMD; four tiles take 337, one wave a SIMD, and were slower).
 template <bool F32, int MODE, int WAVES>
 void launch_pass(const PassArgs& a, dim3 grid, int rounds, hipStream_t stream) {
-    constexpr int kMax = MODE == kScreen ? kScreenMaxTiles : (MODE == kListed ? 4 : 8);
+    constexpr int kMax = MODE == kScreen ? kScreenMaxTiles : (MODE == kListed ? 2 : 8);
     const int tpr = a.half_pad / 32;
     if (tpr <= 1)
         launch_pass_st<F32, MODE, WAVES, 1>(a, grid, rounds, stream);
-    else if (tpr <= 2)
+    else if (tpr <= 2 || kMax == 2)
         launch_pass_st<F32, MODE, WAVES, 2>(a, grid, rounds, stream);
-    else if (tpr <= 4 || kMax == 4)
-        launch_pass_st<F32, MODE, WAVES, 4>(a, grid, rounds, stream);
+    else if (tpr <= 4 || kMax == 4) {
+        if constexpr (kMax >= 4) launch_pass_st<F32, MODE, WAVES, 4>(a, grid, rounds, stream);
+    }
     else if (tpr <= 8 || kMax == 8) {
         if constexpr (kMax >= 8) launch_pass_st<F32, MODE, WAVES, 8>(a, grid, rounds, stream);
     } else {
@@ -1158,7 +1172,7 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
     if (f32) {
         launch_pass<true, kExact, kWaves>(
             PassArgs{q, rows, n_rounds, half, half_pad, w.r_hi, w.r_mid, cn_max, nullptr, acc_f32, nullptr, 0.f,
-                     err_pack, buckets, nullptr, nullptr, w.list2, count2, 0},
+                     err_pack, nullptr, buckets, nullptr, nullptr, w.list2, count2, 0},
             dim3(grid), n_rounds, stream);
         hash_refine_kernel<true><<<dim3(refine_blocks, n_rounds), kRefineThreads, 0, stream>>>(
             q, R, half, n_rounds, rows, w.list2, count2, cn_max, nullptr, buckets);
@@ -1167,19 +1181,19 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
         // what those leave open gets the fp64 refinement
         launch_pass<false, kScreen, kWaves>(
             PassArgs{q, rows, n_rounds, half, half_pad, w.r_hi, w.r_mid, cn_max, res1_max, acc1, res2_max, acc2,
-                     err_pack, buckets, nullptr, nullptr, w.list1, count1, w.seg_cap},
+                     err_pack, w.col_norm + (size_t)n_rounds * half_pad, buckets, nullptr, nullptr, w.list1, count1,
+                     w.seg_cap},
             dim3(grid), n_rounds, stream);
-        // Four waves a workgroup: with one wave per SIMD the two-plane
-        // pipeline keeps its values in registers.  The screen leaves about
-        // 0.9% of row-rounds open on Gaussian data (binary16 planes): 64
-        // workgroups per round cover 64 * 256 open rows, 1.6% of 1M rows;
-        // longer lists loop.
+        // Four waves a workgroup.  Deciding from the hi plane alone, the
+        // screen leaves about 1.5-2% of row-rounds open on Gaussian data:
+        // 128 workgroups per round cover 128 * 256 open rows, 3.1% of 1M
+        // rows; longer lists loop.
         constexpr int kListedWaves = 4;
         const int64_t listed_rows = kListedWaves * 64;
-        const unsigned per_round = (unsigned)std::min<int64_t>(64, (rows + listed_rows - 1) / listed_rows);
+        const unsigned per_round = (unsigned)std::min<int64_t>(128, (rows + listed_rows - 1) / listed_rows);
         launch_pass<false, kListed, kListedWaves>(
             PassArgs{q, rows, n_rounds, half, half_pad, w.r_hi, w.r_mid, cn_max, res2_max, acc2, res2_max, acc2,
-                     err_pack, buckets, w.list1, count1, w.list2, count2, w.seg_cap},
+                     err_pack, nullptr, buckets, w.list1, count1, w.list2, count2, w.seg_cap},
             dim3(per_round, 1, n_rounds), 1, stream);
         hash_refine_kernel<false><<<dim3(refine_blocks, n_rounds), kRefineThreads, 0, stream>>>(
             q, R, half, n_rounds, rows, w.list2, count2, cn_max, w.r_exp, buckets);
