@@ -471,8 +471,11 @@ __global__ __launch_bounds__(M) void attn_fwd_f32_kernel(
     const int32_t* __restrict__ bstart, float* __restrict__ o_rounds,
     float* __restrict__ lse_rounds, int L, int n_r, int n_b, int causal, int after, int across,
     float scale, float self_mask) {
-    __shared__ float Ks[M][kHeadDim + 1];
-    __shared__ float Vs2[M][kHeadDim + 1];
+    // rows padded to 68 floats: 16-byte aligned for the broadcast reads of
+    // the key loop
+    constexpr int kRow = kHeadDim + 4;
+    __shared__ __attribute__((aligned(16))) float Ks[M][kRow];
+    __shared__ __attribute__((aligned(16))) float Vs2[M][kRow];
     __shared__ float inv[M];
     __shared__ int spos[M];
 
@@ -545,8 +548,17 @@ __global__ __launch_bounds__(M) void attn_fwd_f32_kernel(
             if (tk == s_q) continue;
             const int rho = tk - slot0;
             if (pos_causal && spos[rho] > i_q) continue;
-            float dot = 0.f;
-            for (int u = 0; u < kHeadDim; ++u) dot = fmaf(qi[u], Ks[rho][u], dot);
+            // four independent chains: one wave per chunk leaves nothing
+            // else to hide a 64-long chain of dependent FMAs
+            const f32x4* kr = reinterpret_cast<const f32x4*>(&Ks[rho][0]);
+            float d[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int u4 = 0; u4 < kHeadDim / 4; ++u4) {
+                const f32x4 kk = kr[u4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) d[e] = fmaf(qi[4 * u4 + e], kk[e], d[e]);
+            }
+            const float dot = (d[0] + d[1]) + (d[2] + d[3]);
             float a = scale * (dot * inv[rho]);
             if (n_r > 1) {
                 int nn = 0;
@@ -565,7 +577,13 @@ __global__ __launch_bounds__(M) void attn_fwd_f32_kernel(
             const float corr = expf(m - mn);
             const float p = expf(a - mn);
             l = l * corr + p;
-            for (int u = 0; u < kHeadDim; ++u) o[u] = fmaf(o[u], corr, p * Vs2[rho][u]);
+            const f32x4* vr = reinterpret_cast<const f32x4*>(&Vs2[rho][0]);
+#pragma unroll
+            for (int u4 = 0; u4 < kHeadDim / 4; ++u4) {
+                const f32x4 vv = vr[u4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[4 * u4 + e] = fmaf(o[4 * u4 + e], corr, p * vv[e]);
+            }
             m = mn;
         }
     }
@@ -573,7 +591,10 @@ __global__ __launch_bounds__(M) void attn_fwd_f32_kernel(
     float* orow = o_rounds + (seg * L + s_q) * kHeadDim;
     if (l > 0.f) {
         const float il = 1.f / l;
-        for (int u = 0; u < kHeadDim; ++u) orow[u] = o[u] * il;
+#pragma unroll
+        for (int u4 = 0; u4 < kHeadDim / 4; ++u4)
+            reinterpret_cast<f32x4*>(orow)[u4] =
+                f32x4{o[4 * u4] * il, o[4 * u4 + 1] * il, o[4 * u4 + 2] * il, o[4 * u4 + 3] * il};
         lse_rounds[seg * L + s_q] = m + logf(l);
     } else {
         // only itself left as a target: v_i, log-partition scale*|q_i| - self_mask
