@@ -930,7 +930,14 @@ __global__ __launch_bounds__(WAVES * 64, (MODE == kScreen ? kScreenOcc : 1)) voi
                 // and stay in the caches).
                 constexpr bool kHiOnly = MODE == kScreen;
                 u32x4 hv[kRB][4], mv[kRB][4];
-                float res_w[kRB];
+                // Lane half h keeps only row block h's decision, so it needs
+                // only that winner's residual: one gather (a 4-byte gather
+                // costs the address unit as much as a 16-byte one), issued
+                // first, with the planes' (left to itself the compiler issues
+                // it after the first block's products and waits on it).
+                float res_own = 0.f;
+                if constexpr (kHiOnly)
+                    res_own = col_res[(size_t)r * half_pad + min(h ? col[1] : col[0], half_pad - 1)];
 #pragma unroll
                 for (int rb = 0; rb < kRB; ++rb) {
                     const int cc = min(col[rb], half_pad - 1);
@@ -942,8 +949,8 @@ __global__ __launch_bounds__(WAVES * 64, (MODE == kScreen ? kScreenOcc : 1)) voi
                         hv[rb][s4] = ph[s4];
                         if constexpr (!kHiOnly) mv[rb][s4] = pm[s4];
                     }
-                    if constexpr (kHiOnly) res_w[rb] = col_res[(size_t)r * half_pad + cc];
                 }
+                if constexpr (kHiOnly) asm volatile("" : "+v"(res_own));
 #pragma unroll
                 for (int rb = 0; rb < kRB; ++rb) {
                     float half_x = dot_planes(qa[rb], hv[rb]);
@@ -951,7 +958,7 @@ __global__ __launch_bounds__(WAVES * 64, (MODE == kScreen ? kScreenOcc : 1)) voi
                     const float x = sum_xor32(half_x);
                     const float s1 = key_magnitude<F32>(sk[rb]);
                     const float eps = 1.02f * qn[rb] * (res + err_acc * cn);
-                    const float eps_x = kHiOnly ? 1.02f * qn[rb] * (res_w[rb] + err_acc * cn)
+                    const float eps_x = kHiOnly ? 1.02f * qn[rb] * (res_own + err_acc * cn)  // kept for rb == h
                                                 : 1.02f * qn[rb] * (res_max2[r] + err_acc2 * cn);
                     const bool flag = !(fabsf(x) - eps_x > s1 * (1.f + 2.f * err_pack) + eps) || col[rb] >= half;
                     const int id = x < 0.f ? half + col[rb] : col[rb];
