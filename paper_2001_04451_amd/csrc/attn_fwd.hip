@@ -457,15 +457,16 @@ __global__ __launch_bounds__((FwdGeom<M, AFTER>::kThreads), (FwdGeom<M, AFTER>::
 }
 
 // fp32 path: one workgroup per chunk of M sorted slots (M = 64, or 128, the
-// chunk length of the paper's usual configuration), one lane per query,
-// exact fp32 arithmetic on the VALU with an online softmax over the query's
-// keys.  The window is chunks c-1 .. c+after; it is walked one chunk at a
+// chunk length of the paper's usual configuration), one lane per query in
+// each of KS waves, exact fp32 arithmetic on the VALU with an online softmax
+// over the query's keys.  Wave s takes every KS-th key of the query's range;
+// the KS partial softmaxes (max, sum, weighted row) are merged at the end.  The window is chunks c-1 .. c+after; it is walked one chunk at a
 // time (the query's own chunk first), each staged in LDS.  Two variants the
 // paper does not spell out: a look-ahead of `after` chunks, and attending
 // across buckets (every key of the window is a target, and N_ij counts the
 // rounds in which j falls in i's window, from undo).
-template <int M>
-__global__ __launch_bounds__(M) void attn_fwd_f32_kernel(
+template <int M, int KS>
+__global__ __launch_bounds__(M * KS) void attn_fwd_f32_kernel(
     const float* __restrict__ q, const float* __restrict__ v, const int32_t* __restrict__ buckets,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ undo,
     const int32_t* __restrict__ bstart, float* __restrict__ o_rounds,
@@ -478,8 +479,14 @@ __global__ __launch_bounds__(M) void attn_fwd_f32_kernel(
     __shared__ __attribute__((aligned(16))) float Vs2[M][kRow];
     __shared__ float inv[M];
     __shared__ int spos[M];
+    // waves 1 .. KS-1: their partial (max, sum, row) per query
+    __shared__ float part[KS > 1 ? KS - 1 : 1][KS > 1 ? M : 1][kHeadDim + 2];
+    static_assert(M == 64 || KS == 1, "one wave of queries per key split");
 
-    const int t = threadIdx.x;
+    constexpr int NT = M * KS;
+    const int tid = threadIdx.x;
+    const int t = tid % M;       // the query's slot in the chunk
+    const int ks = tid / M;      // the key split
     const int64_t seg = blockIdx.y;
     const int64_t bh = seg / n_r;
     const int r = (int)(seg % n_r);
@@ -514,16 +521,16 @@ __global__ __launch_bounds__(M) void attn_fwd_f32_kernel(
         const int k = piece == 0 ? c : (piece == 1 ? c - 1 : c + piece - 1);
         const int slot0 = k * M;
         __syncthreads();  // the previous piece is no longer read
-        // positions first, then thread t copies dim t % 64 of row t / 64 of
-        // each group of M / 64 rows, from clamped addresses
-        {
+        // positions first, then thread tid copies dim tid % 64 of row
+        // tid / 64 of each group of NT / 64 rows, from clamped addresses
+        if (ks == 0) {
             const int slot = slot0 + t;
             const int pos = min(max(pseg[min(max(slot, 0), L - 1)], 0), L - 1);
             spos[t] = slot >= 0 && slot < L ? pos : -1;
         }
         __syncthreads();
-        constexpr int kRowsPerPass = M / kHeadDim;
-        const int dcol = t % kHeadDim, rsub = t / kHeadDim;
+        constexpr int kRowsPerPass = NT / kHeadDim;
+        const int dcol = tid % kHeadDim, rsub = tid / kHeadDim;
 #pragma unroll 8
         for (int rho0 = 0; rho0 < M; rho0 += kRowsPerPass) {
             const int rho = rho0 + rsub;
@@ -534,7 +541,7 @@ __global__ __launch_bounds__(M) void attn_fwd_f32_kernel(
             Vs2[rho][dcol] = pos >= 0 ? kv : 0.f;
         }
         __syncthreads();
-        {
+        if (ks == 0) {
             float ss = 0.f;
             for (int u = 0; u < kHeadDim; ++u) ss = fmaf(Ks[t][u], Ks[t][u], ss);
             inv[t] = ss > 0.f ? 1.f / sqrtf(ss) : 0.f;
@@ -544,7 +551,7 @@ __global__ __launch_bounds__(M) void attn_fwd_f32_kernel(
         __syncthreads();
         if (!has_q) continue;
         const int t_lo = max(lo, slot0), t_hi = min(hi, slot0 + M - 1);
-        for (int tk = t_lo; tk <= t_hi; ++tk) {
+        for (int tk = t_lo + ks; tk <= t_hi; tk += KS) {
             if (tk == s_q) continue;
             const int rho = tk - slot0;
             if (pos_causal && spos[rho] > i_q) continue;
@@ -585,6 +592,32 @@ __global__ __launch_bounds__(M) void attn_fwd_f32_kernel(
                 for (int e = 0; e < 4; ++e) o[4 * u4 + e] = fmaf(o[4 * u4 + e], corr, p * vv[e]);
             }
             m = mn;
+        }
+    }
+    if constexpr (KS > 1) {
+        // merge the splits' partial softmaxes into wave 0 (a split that saw
+        // no key has m = -inf and l = 0, and weighs nothing)
+        if (ks > 0) {
+            float* pp = part[ks - 1][t];
+            pp[0] = m;
+            pp[1] = l;
+            for (int u = 0; u < kHeadDim; ++u) pp[2 + u] = o[u];
+        }
+        __syncthreads();
+        if (ks > 0) return;
+        float mm = m;
+        for (int k = 0; k < KS - 1; ++k) mm = fmaxf(mm, part[k][t][0]);
+        if (mm > -__builtin_inff()) {
+            const float c0 = expf(m - mm);
+            l *= c0;
+            for (int u = 0; u < kHeadDim; ++u) o[u] *= c0;
+            for (int k = 0; k < KS - 1; ++k) {
+                const float* pp = part[k][t];
+                const float ck = expf(pp[0] - mm);
+                l = fmaf(pp[1], ck, l);
+                for (int u = 0; u < kHeadDim; ++u) o[u] = fmaf(pp[2 + u], ck, o[u]);
+            }
+            m = mm;
         }
     }
     if (!has_q) return;
@@ -717,12 +750,12 @@ hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, int c
     if (f32) {
         const dim3 grid((unsigned)((L + chunk - 1) / chunk), segs);
         if (chunk == 128)
-            attn_fwd_f32_kernel<128><<<grid, 128, 0, stream>>>(
+            attn_fwd_f32_kernel<128, 1><<<grid, 128, 0, stream>>>(
                 static_cast<const float*>(q), static_cast<const float*>(v), buckets, perm, undo,
                 bucket_start, static_cast<float*>(o_rounds), lse_rounds, L, n_rounds, n_buckets,
                 causal ? 1 : 0, after, across ? 1 : 0, scale, self_mask);
         else
-            attn_fwd_f32_kernel<64><<<grid, 64, 0, stream>>>(
+            attn_fwd_f32_kernel<64, 4><<<grid, 256, 0, stream>>>(
                 static_cast<const float*>(q), static_cast<const float*>(v), buckets, perm, undo,
                 bucket_start, static_cast<float*>(o_rounds), lse_rounds, L, n_rounds, n_buckets,
                 causal ? 1 : 0, after, across ? 1 : 0, scale, self_mask);
