@@ -1192,7 +1192,7 @@ hipError_t launch_hash(const void* q, bool f32, int64_t rows, int n_rounds, int 
                      w.seg_cap},
             dim3(grid), n_rounds, stream);
         // Four waves a workgroup.  Deciding from the hi plane alone, the
-        // screen leaves about 1.5-2% of row-rounds open on Gaussian data:
+        // screen leaves about 1.5% of row-rounds open on Gaussian data:
         // 128 workgroups per round cover 128 * 256 open rows, 3.1% of 1M
         // rows; longer lists loop.
         constexpr int kListedWaves = 4;
