@@ -481,7 +481,7 @@ __global__ __launch_bounds__(M * KS) void attn_fwd_f32_kernel(
     __shared__ int spos[M];
     // waves 1 .. KS-1: their partial (max, sum, row) per query
     __shared__ float part[KS > 1 ? KS - 1 : 1][KS > 1 ? M : 1][kHeadDim + 2];
-    static_assert(M == 64 || KS == 1, "one wave of queries per key split");
+    static_assert(M % kHeadDim == 0 && M * KS <= 256, "whole waves of queries per key split");
 
     constexpr int NT = M * KS;
     const int tid = threadIdx.x;
@@ -750,7 +750,7 @@ hipError_t launch_attn_fwd(int64_t BH, int L, int n_rounds, int n_buckets, int c
     if (f32) {
         const dim3 grid((unsigned)((L + chunk - 1) / chunk), segs);
         if (chunk == 128)
-            attn_fwd_f32_kernel<128, 1><<<grid, 128, 0, stream>>>(
+            attn_fwd_f32_kernel<128, 2><<<grid, 256, 0, stream>>>(
                 static_cast<const float*>(q), static_cast<const float*>(v), buckets, perm, undo,
                 bucket_start, static_cast<float*>(o_rounds), lse_rounds, L, n_rounds, n_buckets,
                 causal ? 1 : 0, after, across ? 1 : 0, scale, self_mask);
